@@ -1,0 +1,316 @@
+"""CPU oracle for (post-)local SGD -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this module. The product path never calls it.
+
+Plain, slow and fp64. It follows "Don't Use Large Mini-Batches, Use Local SGD"
+(Lin, Stich, Patel, Jaggi, ICLR 2020); every function names the passage it
+implements. It shares no code with the HIP path: the only common module is
+``workloads`` (seeded inputs, no arithmetic of the method).
+
+Readings of the paper taken here (it is silent or garbled on these points):
+
+* sampling -- each worker draws its B_loc indices i.i.d. with replacement
+  from its own contiguous shard [floor(kN/K), floor((k+1)N/K)), using
+  Philox4x32-10 (Salmon et al., SC'11) keyed by the seed, with counter
+  (slot // 4, step low word, worker, step high word); slot j takes output word
+  j mod 4 and maps u in [0, 2^32) to the shard by the multiply-shift
+  lo + floor(u * n / 2^32);
+* averaging -- the plain mean of eq. (2); the Delta form of Algorithms 1 and 2
+  is the same thing once the stray step size is dropped (all replicas start a
+  round equal);
+* optimiser -- coupled L2 decay g = grad + wd * w, buffer u = m u + g, step
+  d = u (heavy ball) or d = g + m u (Nesterov), w = w - lr * d; buffers start
+  at zero, belong to one replica and are never averaged; decay applies to
+  weights and biases;
+* post-local switch -- rounds 1..t' use one local step, later rounds H, with
+  the decayed step size from round t'+1 on; momentum buffers carry over;
+* loss -- per-sample cross-entropy in the numerically stable form, mean over
+  the local batch, taken in the forward pass before the update;
+* bf16 workloads -- GEMM operands (gathered inputs, hidden activations after
+  ReLU, weight copies, and the back-propagated dZ including the one used for
+  the bias gradient) are rounded to bfloat16 with round-to-nearest-even;
+  everything else stays at full precision.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+MASK32 = np.uint64(0xFFFFFFFF)
+
+# Philox4x32 constants (Salmon, Moraes, Dror, Shaw, "Parallel random numbers:
+# as easy as 1, 2, 3", SC'11): the two round multipliers and the Weyl key
+# increments (golden ratio and sqrt(3) - 1 in 0.32 fixed point).
+PHILOX_M0 = np.uint64(0xD2511F53)
+PHILOX_M1 = np.uint64(0xCD9E8D57)
+PHILOX_W0 = np.uint64(0x9E3779B9)
+PHILOX_W1 = np.uint64(0xBB67AE85)
+
+
+# --------------------------------------------------------------------------
+# Sampling (eq. 1: index sets drawn from the worker's local data; setup
+# section: data partitioned among workers, local mini-batches sampled among
+# the local data)
+# --------------------------------------------------------------------------
+def philox4x32_10(ctr, key):
+    """Philox4x32 with 10 rounds.
+
+    ``ctr``: four arrays of 32-bit words (any integer dtype, same shape);
+    ``key``: two 32-bit words. Returns four uint64 arrays holding 32-bit words.
+    Each round multiplies words 0 and 2 by the two constants, and the new
+    state is (hi(M1*c2) ^ c1 ^ k0, lo(M1*c2), hi(M0*c0) ^ c3 ^ k1, lo(M0*c0));
+    the key is bumped by the Weyl increments between rounds.
+    """
+    c0, c1, c2, c3 = (np.asarray(c).astype(np.uint64) & MASK32 for c in ctr)
+    k0 = np.uint64(int(key[0]) & 0xFFFFFFFF)
+    k1 = np.uint64(int(key[1]) & 0xFFFFFFFF)
+    for r in range(10):
+        if r:
+            k0 = (k0 + PHILOX_W0) & MASK32
+            k1 = (k1 + PHILOX_W1) & MASK32
+        p0 = PHILOX_M0 * c0          # < 2^64, exact in uint64
+        p1 = PHILOX_M1 * c2
+        c0, c1, c2, c3 = ((p1 >> np.uint64(32)) ^ c1 ^ k0, p1 & MASK32,
+                          (p0 >> np.uint64(32)) ^ c3 ^ k1, p0 & MASK32)
+    return c0, c1, c2, c3
+
+
+def shard(k: int, K: int, N: int):
+    """Worker k's disjoint slice [lo, hi) of the N training rows."""
+    return (k * N) // K, ((k + 1) * N) // K
+
+
+def sample_indices(seed: int, step: int, k: int, K: int, N: int, B: int):
+    """I^k for local step ``step`` (counted from init over all rounds).
+
+    Returns int64 [B], i.i.d. uniform (with replacement) over worker k's
+    shard.
+    """
+    lo, hi = shard(k, K, N)
+    n = hi - lo
+    j = np.arange(B, dtype=np.uint64)
+    ctr = (j >> np.uint64(2),
+           np.full(B, step & 0xFFFFFFFF, np.uint64),
+           np.full(B, k, np.uint64),
+           np.full(B, (step >> 32) & 0xFFFFFFFF, np.uint64))
+    words = np.stack(philox4x32_10(ctr, (seed & 0xFFFFFFFF, seed >> 32)))
+    u = words[(j & np.uint64(3)).astype(np.int64), np.arange(B)]
+    return lo + ((u * np.uint64(n)) >> np.uint64(32)).astype(np.int64)
+
+
+# --------------------------------------------------------------------------
+# bfloat16 rounding (operand precision of the bf16 workload)
+# --------------------------------------------------------------------------
+def rne_bf16(x):
+    """Round to the nearest bfloat16 value, ties to even; returns float64.
+
+    bfloat16 keeps 8 significant bits and fp32's exponent range: normal
+    values below 2^-126 fall onto the fixed subnormal grid of 2^-133.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                       # x = m * 2^e, |m| in [0.5, 1)
+    q = np.ldexp(1.0, np.maximum(e, -125) - 8)   # spacing of bf16 near x
+    r = np.round(x / q) * q                  # np.round is half-to-even
+    big = np.abs(r) > 3.3895313892515355e38  # beyond the largest bf16
+    if np.any(big):
+        r = np.where(big, np.sign(r) * np.inf, r)
+    return r
+
+
+# --------------------------------------------------------------------------
+# The model: fully-connected ReLU network with a softmax cross-entropy loss
+# (f_i of the sum-structured objective in the introduction); with no hidden
+# layer it is softmax regression.
+# --------------------------------------------------------------------------
+def unpack(w, widths):
+    """Views (W_l [d_in][d_out], b_l [d_out]) into a flat parameter vector."""
+    out, o = [], 0
+    for din, dout in zip(widths[:-1], widths[1:]):
+        W = w[o:o + din * dout].reshape(din, dout)
+        o += din * dout
+        b = w[o:o + dout]
+        o += dout
+        out.append((W, b))
+    assert o == w.size, (o, w.size)
+    return out
+
+
+def cross_entropy(z, y):
+    """Per-row loss -log softmax(z)_y and the softmax probabilities.
+
+    Stable form: with m = max_j z_j, the loss is log1p(sum_{j != y} e^{z_j-m})
+    when z_y is the maximum, else (m - z_y) + log(sum_j e^{z_j - m}).
+    """
+    z = np.asarray(z, np.float64)
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    s = e.sum(axis=1)
+    rows = np.arange(z.shape[0])
+    zy = z[rows, y]
+    is_max = zy >= m[:, 0]
+    others = e.copy()
+    others[rows, y] = 0.0
+    rest = others.sum(axis=1)         # summed directly: no cancellation
+    loss = np.where(is_max, np.log1p(rest), (m[:, 0] - zy) + np.log(s))
+    p = e / s[:, None]
+    return loss, p
+
+
+def loss_and_grad(w, widths, A0, y, bf16=False):
+    """Mean mini-batch loss and its gradient (the bracket of eq. 2).
+
+    ``A0`` [B][d_in] are the gathered rows, ``y`` their labels. Returns
+    (loss_mean, flat gradient in the layout of ``w``).
+    """
+    rnd = rne_bf16 if bf16 else (lambda v: v)
+    B = A0.shape[0]
+    layers = unpack(np.asarray(w, np.float64), widths)
+    L = len(layers)
+    Wq = [rnd(W) for W, _ in layers]
+    acts = [rnd(np.asarray(A0, np.float64))]
+    pre = []
+    for l, (W, b) in enumerate(layers):
+        z = acts[-1] @ Wq[l] + b
+        pre.append(z)
+        if l < L - 1:
+            acts.append(rnd(np.maximum(z, 0.0)))
+    loss, p = cross_entropy(pre[-1], y)
+    dz = p.copy()
+    dz[np.arange(B), y] -= 1.0
+    dz /= B
+    grads = [None] * L
+    for l in range(L - 1, -1, -1):
+        dzq = rnd(dz)
+        gW = acts[l].T @ dzq
+        gb = dzq.sum(axis=0)
+        grads[l] = (gW, gb)
+        if l > 0:
+            dz = (dzq @ Wq[l].T) * (pre[l - 1] > 0.0)
+    flat = np.concatenate([np.concatenate([gW.ravel(), gb]) for gW, gb in grads])
+    return float(loss.mean()), flat
+
+
+def decay_mask(widths):
+    """1 where weight decay applies: every weight and bias of the network."""
+    return np.ones(sum(a * b + b for a, b in zip(widths[:-1], widths[1:])))
+
+
+# --------------------------------------------------------------------------
+# Optimiser step (local update of eq. 2 with the local momentum of the
+# appendix on local SGD with momentum; Nesterov, no dampening, weight decay
+# from the CIFAR hyper-parameter paragraph)
+# --------------------------------------------------------------------------
+def sgd_update(w, u, grad, lr, momentum, weight_decay, nesterov, wd_mask=1.0):
+    """One local step on one replica: returns (w_new, u_new)."""
+    g = grad + (weight_decay * wd_mask) * w
+    u = momentum * u + g
+    d = g + momentum * u if nesterov else u
+    return w - lr * d, u
+
+
+# --------------------------------------------------------------------------
+# Synchronisation (eq. 2, right part; Algorithms 1 and 2)
+# --------------------------------------------------------------------------
+def average(W):
+    """Replace every replica by the mean of the K replicas. W: [K][P]."""
+    W = np.asarray(W, np.float64)
+    wbar = W.sum(axis=0) / W.shape[0]
+    return np.broadcast_to(wbar, W.shape).copy()
+
+
+def average_delta_form(W_start, W_end):
+    """Algorithm 1's form: w_(t) - (1/K) sum_k Delta^k with Delta^k =
+    w^k_(t) - w^k_(t)+H, read without the stray step size; all rows of
+    ``W_start`` are the synchronised w_(t)."""
+    D = np.asarray(W_start, np.float64) - np.asarray(W_end, np.float64)
+    wbar = np.asarray(W_start, np.float64)[0] - D.sum(axis=0) / D.shape[0]
+    return np.broadcast_to(wbar, D.shape).copy()
+
+
+# --------------------------------------------------------------------------
+# Drivers
+# --------------------------------------------------------------------------
+class State:
+    """K replicas w^k, their momentum buffers u^k, and the step counter."""
+
+    def __init__(self, w0, K):
+        self.W = np.repeat(np.asarray(w0, np.float64)[None, :], K, axis=0)
+        self.U = np.zeros_like(self.W)
+        self.step = 0
+
+
+def local_step(state, wl, X, y, lr, replicas=None):
+    """One local step (inner loop body of Algorithm 1) on each replica.
+
+    ``wl`` is a ``workloads.Workload``. Returns the per-replica mini-batch
+    losses (NaN for replicas not in ``replicas``).
+    """
+    K = state.W.shape[0]
+    ks = range(K) if replicas is None else replicas
+    losses = np.full(K, np.nan)
+    mask = decay_mask(wl.widths)
+    for k in ks:
+        idx = sample_indices(wl.sample_seed, state.step, k, K, wl.N, wl.B_loc)
+        A0 = np.asarray(X[idx], np.float64)
+        loss, grad = loss_and_grad(state.W[k], wl.widths, A0, y[idx],
+                                   bf16=(wl.dtype == "bf16"))
+        state.W[k], state.U[k] = sgd_update(
+            state.W[k], state.U[k], grad, lr, wl.momentum, wl.weight_decay,
+            wl.nesterov, mask)
+        losses[k] = loss
+    state.step += 1
+    return losses
+
+
+def run_round(state, wl, X, y, H, lr):
+    """H local steps on every replica, then the average; returns [H][K]
+    losses."""
+    losses = np.stack([local_step(state, wl, X, y, lr) for _ in range(H)])
+    state.W = average(state.W)
+    return losses
+
+
+def schedule(wl):
+    """(H_t, lr_t) per round: the post-local rule H_(t) = 1 for t <= t',
+    else H (section 3), with the decayed step size after the switch."""
+    out = []
+    for t in range(1, wl.warm_rounds + wl.rounds + 1):
+        if t <= wl.warm_rounds:
+            out.append((1, wl.lr))
+        else:
+            out.append((wl.H, wl.lr_after_switch if wl.warm_rounds else wl.lr))
+    return out
+
+
+def run(wl, X, y, w0, rounds=None):
+    """Whole (post-)local SGD run (Algorithm 2; Algorithm 1 when t' = 0).
+
+    Returns (state, per-round list of [H_t][K] loss arrays).
+    """
+    st = State(w0, wl.K)
+    sched = schedule(wl)
+    if rounds is not None:
+        sched = sched[:rounds]
+    traj = [run_round(st, wl, X, y, H, lr) for H, lr in sched]
+    return st, traj
+
+
+def minibatch_sgd(wl, X, y, w0, steps, lr):
+    """Plain mini-batch SGD of eq. (1) with one global momentum buffer (the
+    distributed mini-batch momentum recursion of the momentum appendix): the
+    gradient is taken over the union of the K workers' index sets at once.
+    Used only as the comparator of the H = 1 special case."""
+    w = np.asarray(w0, np.float64).copy()
+    u = np.zeros_like(w)
+    mask = decay_mask(wl.widths)
+    for s in range(steps):
+        idx = np.concatenate([
+            sample_indices(wl.sample_seed, s, k, wl.K, wl.N, wl.B_loc)
+            for k in range(wl.K)])
+        _, grad = loss_and_grad(w, wl.widths, np.asarray(X[idx], np.float64),
+                                y[idx], bf16=(wl.dtype == "bf16"))
+        g = grad + wl.weight_decay * mask * w
+        u = wl.momentum * u + g
+        d = g + wl.momentum * u if wl.nesterov else u
+        w = w - lr * d
+    return w

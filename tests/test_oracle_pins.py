@@ -1,0 +1,369 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these compares the oracle with itself: each checks it against a
+published vector, an independent library, a closed form, brute force in high
+precision, or a special case of the method that reduces to a simpler,
+separately written algorithm. No GPU is needed.
+"""
+import decimal
+import math
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+import workloads as wk
+from oracle import lsgd_oracle as O
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+# ------------------------------------------------------------------ sampler
+def _kat_rows():
+    rows = []
+    with open(os.path.join(HERE, "golden", "philox4x32_10_kat.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                rows.append([int(v, 16) for v in line.split()])
+    return rows
+
+
+def test_philox_known_answer_vectors():
+    for r in _kat_rows():
+        out = O.philox4x32_10([np.array([v]) for v in r[:4]], r[4:6])
+        assert [int(o[0]) for o in out] == r[6:10]
+
+
+def test_philox_matches_rocrand_engine(tmp_path):
+    """rocRAND's Philox4x32-10 (host-callable ROCm header) on random blocks."""
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    exe = tmp_path / "ref"
+    subprocess.run([hipcc, "-x", "hip", "--offload-arch=gfx950", "-O1",
+                    os.path.join(HERE, "rocrand_philox_ref.cpp"), "-o",
+                    str(exe)], check=True, capture_output=True)
+    rng = np.random.default_rng(7)
+    blocks = rng.integers(0, 2**32, size=(500, 6), dtype=np.uint64)
+    text = "\n".join(" ".join(f"{int(v):08x}" for v in b) for b in blocks)
+    res = subprocess.run([str(exe)], input=text + "\n", check=True,
+                         capture_output=True, text=True).stdout.split()
+    got = np.array([int(v, 16) for v in res], dtype=np.uint64).reshape(-1, 4)
+    mine = np.stack([
+        np.stack(O.philox4x32_10([blocks[i:i + 1, c] for c in range(4)],
+                                 (int(blocks[i, 4]), int(blocks[i, 5]))))[:, 0]
+        for i in range(len(blocks))])
+    np.testing.assert_array_equal(mine, got)
+
+
+@pytest.mark.parametrize("K,N,sizes", [(4, 4096, {1024}), (16, 50000, {3125}),
+                                       (64, 50000, {781, 782})])
+def test_shards_partition_the_data(K, N, sizes):
+    bounds = [O.shard(k, K, N) for k in range(K)]
+    assert bounds[0][0] == 0 and bounds[-1][1] == N
+    assert all(bounds[k][1] == bounds[k + 1][0] for k in range(K - 1))
+    assert {hi - lo for lo, hi in bounds} == sizes
+
+
+def test_sampler_stays_in_shard_and_is_deterministic():
+    K, N, B = 64, 50000, 64
+    for s in (0, 1, 17, 2**32 + 5):
+        for k in (0, 1, 31, 63):
+            lo, hi = O.shard(k, K, N)
+            a = O.sample_indices(99, s, k, K, N, B)
+            assert a.dtype == np.int64 and a.shape == (B,)
+            assert a.min() >= lo and a.max() < hi
+            np.testing.assert_array_equal(a, O.sample_indices(99, s, k, K, N, B))
+
+
+def test_sampler_uniform_over_shard():
+    """Chi-square test of the shard occupancy over many steps (n = 37)."""
+    K, N, B = 4, 148, 32
+    counts = np.zeros(N // K)
+    for s in range(400):
+        counts += np.bincount(O.sample_indices(5, s, 2, K, N, B) - 74,
+                              minlength=N // K)
+    exp = counts.sum() / counts.size
+    chi2 = ((counts - exp) ** 2 / exp).sum()
+    # 36 degrees of freedom: the 99.9% quantile is about 67.98
+    assert chi2 < 68.0, chi2
+
+
+def test_sampler_streams_differ_across_workers_and_steps():
+    K, N, B = 2, 2**20, 256
+    a = O.sample_indices(1, 3, 0, K, N, B).astype(float)
+    b = O.sample_indices(1, 3, 1, K, N, B).astype(float) - N // 2
+    c = O.sample_indices(1, 4, 0, K, N, B).astype(float)
+    d = O.sample_indices(2, 3, 0, K, N, B).astype(float)
+    for other in (b, c, d):
+        assert abs(np.corrcoef(a, other)[0, 1]) < 0.25
+        assert not np.array_equal(a, other)
+
+
+# ------------------------------------------------------------------ bf16
+@pytest.mark.parametrize("x,want", [
+    (1.0, 1.0),
+    (1.0 + 2.0**-8, 1.0),                         # tie -> even (mantissa 0)
+    (1.0 + 3 * 2.0**-8, 1.0 + 2.0**-6),           # tie -> even (mantissa 2)
+    (1.0 + 2.0**-8 + 2.0**-30, 1.0 + 2.0**-7),    # just above the tie
+    (-(1.0 + 2.0**-8 + 2.0**-30), -(1.0 + 2.0**-7)),
+    (3.0 * 2.0**-133 / 2, 2.0**-132),             # subnormal tie -> even
+    (2.0**-134, 0.0),                             # half the smallest -> 0
+    (0.0, 0.0),
+    (255.5, 256.0),                               # 8 significant bits
+])
+def test_bf16_rounding_hand_values(x, want):
+    assert O.rne_bf16(x) == want
+
+
+def test_bf16_rounding_matches_torch_on_fp32_values():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal(200000) *
+         np.exp2(rng.integers(-140, 120, 200000))).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.rne_bf16(x.astype(np.float64)), ref)
+
+
+# ------------------------------------------------------------------ loss
+def _exact_ce(z, y):
+    with decimal.localcontext() as ctx:
+        ctx.prec = 60
+        zs = [decimal.Decimal(float(v)) for v in z]
+        m = max(zs)
+        s = sum((v - m).exp() for v in zs)
+        return float(m + s.ln() - zs[y])
+
+
+def test_cross_entropy_against_high_precision():
+    rng = np.random.default_rng(11)
+    z = rng.standard_normal((40, 10)) * np.linspace(0.1, 40, 40)[:, None]
+    y = rng.integers(0, 10, 40)
+    # rows where the true class wins by a wide margin: loss near 1e-15
+    z[:5, :] = 0.0
+    z[np.arange(5), y[:5]] = np.linspace(20, 35, 5)
+    loss, p = O.cross_entropy(z, y)
+    for i in range(40):
+        ref = _exact_ce(z[i], y[i])
+        assert abs(loss[i] - ref) <= 1e-14 * max(ref, 1e-300) + 1e-300, (i, loss[i], ref)
+    np.testing.assert_allclose(p.sum(1), 1.0, rtol=1e-15)
+
+
+def test_initial_loss_is_log_of_classes():
+    """Classifier weights ~ N(0, 0.01^2) give near-uniform softmax: loss ~ ln 10."""
+    wl = wk.get("softmax_d64")
+    X, y = wk.dataset(wl)
+    loss, _ = O.loss_and_grad(wk.initial_weights(wl).astype(np.float64),
+                              wl.widths, X[:512].astype(np.float64), y[:512])
+    assert abs(loss - math.log(10.0)) < 0.1
+
+
+# ------------------------------------------------------------------ gradient
+@pytest.mark.parametrize("widths", [(5, 3), (6, 5, 4, 3), (7, 9, 3)])
+def test_gradient_matches_central_differences(widths):
+    rng = np.random.default_rng(sum(widths))
+    P = wk.param_count(widths)
+    w = rng.standard_normal(P) * 0.7
+    A0 = rng.standard_normal((8, widths[0]))
+    y = rng.integers(0, widths[-1], 8)
+    _, g = O.loss_and_grad(w, widths, A0, y)
+    eps = 1e-6
+    fd = np.empty(P)
+    for i in range(P):
+        wp, wm = w.copy(), w.copy()
+        wp[i] += eps
+        wm[i] -= eps
+        fd[i] = (O.loss_and_grad(wp, widths, A0, y)[0] -
+                 O.loss_and_grad(wm, widths, A0, y)[0]) / (2 * eps)
+    assert np.max(np.abs(fd - g)) <= 1e-7 * max(1.0, np.max(np.abs(g)))
+
+
+def test_softmax_regression_gradient_closed_form():
+    """For one layer the gradient is X^T (P - Y) / B and 1^T (P - Y) / B."""
+    rng = np.random.default_rng(4)
+    d, C, B = 6, 4, 10
+    W = rng.standard_normal((d, C))
+    b = rng.standard_normal(C)
+    X = rng.standard_normal((B, d))
+    y = rng.integers(0, C, B)
+    Z = X @ W + b
+    P = np.exp(Z - Z.max(1, keepdims=True))
+    P /= P.sum(1, keepdims=True)
+    Y = np.eye(C)[y]
+    _, g = O.loss_and_grad(np.concatenate([W.ravel(), b]), (d, C), X, y)
+    np.testing.assert_allclose(g[:d * C].reshape(d, C), X.T @ (P - Y) / B,
+                               rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(g[d * C:], (P - Y).sum(0) / B, rtol=1e-12,
+                               atol=1e-15)
+
+
+# ------------------------------------------------------------------ update
+@pytest.mark.parametrize("nesterov", [False, True])
+def test_local_momentum_closed_form_constant_gradient(nesterov):
+    """H local momentum steps with a constant gradient g.
+
+    Heavy ball follows the expansion of the local-momentum appendix:
+    w_H = w_0 - lr (sum_{tau=1..H} m^tau u_0 + sum_{h=0..H-1} sum_{tau=0..H-1-h}
+    m^tau g). Nesterov (d = g + m u) with u_0 = 0 sums to
+    w_H = w_0 - lr g (H - m^2 (1 - m^H) / (1 - m)) / (1 - m).
+    """
+    rng = np.random.default_rng(5)
+    w0 = rng.standard_normal(50)
+    g = rng.standard_normal(50)
+    u0 = rng.standard_normal(50) if not nesterov else np.zeros(50)
+    lr, m, H = 0.07, 0.9, 13
+    w, u = w0.copy(), u0.copy()
+    for _ in range(H):
+        w, u = O.sgd_update(w, u, g, lr, m, 0.0, nesterov)
+    if nesterov:
+        want = w0 - lr * g * (H - m * m * (1 - m**H) / (1 - m)) / (1 - m)
+    else:
+        acc = sum(m**tau for tau in range(1, H + 1)) * u0
+        acc = acc + sum(sum(m**tau for tau in range(H - h)) for h in range(H)) * g
+        want = w0 - lr * acc
+    np.testing.assert_allclose(w, want, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("nesterov", [False, True])
+def test_weight_decay_is_a_linear_recurrence(nesterov):
+    """Zero loss gradient, decay lam: (w, u) evolves by a fixed 2x2 matrix."""
+    lr, m, lam, H = 0.3, 0.8, 0.05, 25
+    if nesterov:
+        M = np.array([[1 - lr * lam * (1 + m), -lr * m * m], [lam, m]])
+    else:
+        M = np.array([[1 - lr * lam, -lr * m], [lam, m]])
+    w, u = np.array([1.5, -2.0]), np.array([0.25, 0.5])
+    want = np.linalg.matrix_power(M, H) @ np.stack([w, u])
+    for _ in range(H):
+        w, u = O.sgd_update(w, u, np.zeros(2), lr, m, lam, nesterov)
+    np.testing.assert_allclose(np.stack([w, u]), want, rtol=1e-12, atol=1e-14)
+
+
+# ------------------------------------------------------------------ average
+def test_average_identity_invariance_and_delta_form():
+    rng = np.random.default_rng(6)
+    w = rng.standard_normal(33)
+    same = np.repeat(w[None], 8, axis=0)
+    np.testing.assert_allclose(O.average(same), same, rtol=4e-16, atol=0)
+    W = rng.standard_normal((8, 33))
+    A = O.average(W)
+    np.testing.assert_allclose(A.mean(0), W.mean(0), rtol=1e-14, atol=1e-15)
+    assert np.all(A == A[0])
+    np.testing.assert_allclose(O.average_delta_form(same, W), A,
+                               rtol=1e-13, atol=1e-14)
+    np.testing.assert_array_equal(O.average(W[:1]), W[:1])   # K = 1
+
+
+# ------------------------------------------------------------------ method
+def _small(nesterov, momentum=0.9, wd=1e-3, K=4, H=1, B=8, rounds=3):
+    base = wk.get("softmax_d64")
+    return base.scaled(widths=(64, 12, 10), K=K, B_loc=B, H=H, rounds=rounds,
+                       lr=0.05, momentum=momentum, nesterov=nesterov,
+                       weight_decay=wd)
+
+
+@pytest.mark.parametrize("nesterov,momentum", [(False, 0.0), (False, 0.9),
+                                               (True, 0.9)])
+def test_h1_local_sgd_is_minibatch_sgd(nesterov, momentum):
+    """H = 1 with averaging after each step equals mini-batch SGD with batch
+    K*B_loc (introduction, below eq. 2), including coupled decay and, by
+    linearity of the buffers, heavy-ball and Nesterov momentum."""
+    wl = _small(nesterov, momentum, H=1, rounds=6)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(1).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st, _ = O.run(wl, X, y, w0)
+    ref = O.minibatch_sgd(wl, X, y, w0, steps=6, lr=wl.lr)
+    np.testing.assert_allclose(st.W[0], ref, rtol=1e-12, atol=1e-13)
+
+
+def test_single_worker_is_sequential_sgd():
+    wl = _small(False, 0.9, K=1, H=4, rounds=3)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(2).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st, _ = O.run(wl, X, y, w0)
+    ref = O.minibatch_sgd(wl, X, y, w0, steps=12, lr=wl.lr)
+    np.testing.assert_allclose(st.W[0], ref, rtol=1e-12, atol=1e-13)
+
+
+def test_post_local_limits():
+    """t' >= T is mini-batch SGD; t' = 0 is local SGD (section 3)."""
+    X, y = wk.dataset(wk.get("softmax_d64"))
+    w0 = np.random.default_rng(3).standard_normal(wk.param_count((64, 12, 10))) * 0.1
+    warm_only = _small(True, 0.9, H=4, rounds=0).scaled(warm_rounds=5,
+                                                        lr_after_switch=0.005)
+    st, traj = O.run(warm_only, X, y, w0)
+    assert [t.shape[0] for t in traj] == [1] * 5
+    np.testing.assert_allclose(
+        st.W[0], O.minibatch_sgd(warm_only, X, y, w0, 5, warm_only.lr),
+        rtol=1e-12, atol=1e-13)
+    # a switch after 2 warm rounds = 2 H=1 rounds, then H=4 rounds at lr/10
+    post = _small(True, 0.9, H=4, rounds=2).scaled(warm_rounds=2,
+                                                   lr_after_switch=0.005)
+    assert O.schedule(post) == [(1, 0.05), (1, 0.05), (4, 0.005), (4, 0.005)]
+    assert O.schedule(post.scaled(warm_rounds=0)) == [(4, 0.05), (4, 0.05)]
+
+
+def test_momentum_buffers_stay_local():
+    """Averaging touches the models only; each worker keeps its own u^k."""
+    wl = _small(False, 0.9, H=3, rounds=1)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(4).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st, manual = O.State(w0, wl.K), O.State(w0, wl.K)
+    O.run_round(st, wl, X, y, 3, wl.lr)
+    for _ in range(3):
+        O.local_step(manual, wl, X, y, wl.lr)
+    np.testing.assert_array_equal(st.U, manual.U)
+    assert not np.allclose(st.U[0], st.U[1])
+    np.testing.assert_allclose(st.W[1], manual.W.mean(0), rtol=1e-15, atol=1e-16)
+
+
+def test_round_matches_local_momentum_expansion():
+    """After one round, each replica obeys the local-momentum expansion of
+    the appendix: w^k_H = w^k_0 - lr (sum_tau m^tau u^k_0 + sum_h
+    (sum_{tau<H-h} m^tau) grad^k_h); checked with decay off, using the
+    replica's own per-step gradients."""
+    wl = _small(False, 0.9, wd=0.0, H=5, rounds=1)
+    X, y = wk.dataset(wl)
+    rng = np.random.default_rng(8)
+    w0 = rng.standard_normal(wk.param_count(wl.widths)) * 0.1
+    st = O.State(w0, wl.K)
+    st.U = rng.standard_normal(st.U.shape) * 0.01
+    st.step = 40
+    U0 = st.U.copy()
+    W0 = st.W.copy()
+    grads = [[None] * wl.K for _ in range(wl.H)]
+    for h in range(wl.H):
+        for k in range(wl.K):
+            idx = O.sample_indices(wl.sample_seed, st.step, k, wl.K, wl.N, wl.B_loc)
+            grads[h][k] = O.loss_and_grad(st.W[k], wl.widths, X[idx].astype(float),
+                                          y[idx])[1]
+        O.local_step(st, wl, X, y, wl.lr)
+    m, H = wl.momentum, wl.H
+    for k in range(wl.K):
+        acc = sum(m**t for t in range(1, H + 1)) * U0[k]
+        for h in range(H):
+            acc = acc + sum(m**t for t in range(H - h)) * grads[h][k]
+        np.testing.assert_allclose(st.W[k], W0[k] - wl.lr * acc, rtol=1e-11,
+                                   atol=1e-13)
+
+
+def test_replicas_are_independent_between_averages():
+    wl = _small(True, 0.9, H=2, rounds=1)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(9).standard_normal(wk.param_count(wl.widths)) * 0.1
+    a, b = O.State(w0, wl.K), O.State(w0, wl.K)
+    for _ in range(2):
+        O.local_step(a, wl, X, y, wl.lr)
+        O.local_step(b, wl, X, y, wl.lr, replicas=[2])
+    np.testing.assert_array_equal(a.W[2], b.W[2])
+    np.testing.assert_array_equal(b.W[0], np.asarray(w0, float))
+
+
+def test_loss_decreases_on_every_workload_first_rounds():
+    wl = wk.get("softmax_d64")
+    X, y = wk.dataset(wl)
+    _, traj = O.run(wl, X, y, wk.initial_weights(wl), rounds=10)
+    means = [t.mean() for t in traj]
+    assert means[-1] < 0.2 * means[0]
