@@ -1,0 +1,189 @@
+/*
+ * lsgd.h -- C ABI of the MI355X (gfx950) local-SGD hot path.
+ *
+ * Method: local SGD and post-local SGD of Lin, Stich, Patel, Jaggi, "Don't Use
+ * Large Mini-Batches, Use Local SGD" (ICLR 2020). K workers each run H
+ * sequential mini-batch SGD steps of batch B_loc on their own model copy, then
+ * the K models are replaced by their mean (eq. 2; Algorithm 1). Post-local SGD
+ * runs rounds with H = 1 first (eq. "post-local SGD", Algorithm 2); that
+ * schedule is a sequence of run_round calls.
+ *
+ * On one GPU the K workers are K model replicas resident in device memory.
+ *
+ * Conventions for every call:
+ *  - Pointers prefixed d_ are device pointers, h_ host pointers. The caller owns
+ *    all memory; the library never allocates device memory. Device buffers
+ *    handed to lsgd_init_replicas (dataset, labels, workspace) must stay alive
+ *    and unmodified by the caller until lsgd_destroy.
+ *  - Work is enqueued asynchronously on the stream given at init (a
+ *    hipStream_t passed as void*, NULL = the null stream). Results are valid
+ *    once that stream has been synchronised (lsgd_sync does it).
+ *  - Every call returns a status. Argument errors return LSGD_E_INVALID and
+ *    change nothing. A failed HIP call returns LSGD_E_HIP and latches: from
+ *    then on every call on that context returns LSGD_E_STATE until destroy.
+ *  - One context must not be used from two host threads at once. Distinct
+ *    contexts are independent.
+ *
+ * Flat parameter layout of one replica ([P] fp32): for each layer l = 1..L in
+ * order, W_l row-major [d_{l-1}][d_l] (element (i, j) maps input i to output
+ * j), then the bias b_l [d_l].
+ */
+#ifndef LSGD_H
+#define LSGD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lsgd_ctx lsgd_ctx; /* opaque, host-side */
+
+typedef enum lsgd_status {
+  LSGD_OK = 0,
+  LSGD_E_INVALID = 1,     /* bad argument; no state was changed */
+  LSGD_E_WORKSPACE = 2,   /* workspace smaller than lsgd_workspace_bytes */
+  LSGD_E_HIP = 3,         /* a HIP runtime call or launch failed (latched) */
+  LSGD_E_STATE = 4,       /* context unusable after an earlier HIP error */
+  LSGD_E_UNSUPPORTED = 5  /* valid request this build does not implement */
+} lsgd_status;
+
+enum { LSGD_MODEL_MLP = 0 };      /* ReLU MLP; L = 1 is softmax regression */
+enum { LSGD_FP32 = 0, LSGD_BF16 = 1 };
+#define LSGD_MAX_LAYERS 8
+
+/*
+ * Problem statement, after the REQUIRE list of Algorithms 1 and 2: model,
+ * mini-batch size per worker, number of workers, momentum, plus the sampler
+ * key. The step size and H are per call (run_round), so schedules such as
+ * post-local SGD stay on the host.
+ */
+typedef struct lsgd_config {
+  int32_t model;                          /* LSGD_MODEL_MLP */
+  int32_t n_layers;                       /* L, 1..LSGD_MAX_LAYERS */
+  int32_t widths[LSGD_MAX_LAYERS + 1];    /* d_0 (features) .. d_L (classes) */
+  int32_t K;                              /* workers = replicas, >= 1 */
+  int32_t B_loc;                          /* local mini-batch, >= 1 */
+  int32_t gemm_dtype;                     /* LSGD_FP32 or LSGD_BF16 */
+  int32_t nesterov;                       /* 0 heavy ball, 1 Nesterov */
+  float momentum;                         /* m in [0, 1) */
+  float weight_decay;                     /* coupled L2 on weights and biases */
+  uint64_t seed;                          /* Philox4x32-10 key for sampling */
+  int64_t N;                              /* dataset rows, >= K */
+} lsgd_config;
+
+/* Number of parameters P of one replica. */
+lsgd_status lsgd_param_count(const lsgd_config* cfg, int64_t* P);
+
+/* Bytes of device workspace lsgd_init_replicas needs (replicas, momentum
+ * buffers, activations, indices, and for bf16 the operand copies). */
+lsgd_status lsgd_workspace_bytes(const lsgd_config* cfg, size_t* bytes);
+
+/*
+ * Create a context and synchronise all replicas to w0 (first line of
+ * Algorithm 1: w^k_(0) := w_(0)); momentum buffers are zeroed and the local
+ * step counter s is set to 0.
+ *  d_X   fp32 [N][d_0] row-major dataset, d_y int32 [N] labels in [0, d_L).
+ *  d_w0  fp32 [P], copied (stream-ordered); may be freed after the stream
+ *        has passed this call.
+ *  d_ws  workspace of ws_bytes >= lsgd_workspace_bytes, 256-byte aligned.
+ * For LSGD_BF16 the dataset is converted once to a bf16 copy in the
+ * workspace (round to nearest even).
+ */
+lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
+                               const int32_t* d_y, const float* d_w0,
+                               void* d_ws, size_t ws_bytes, void* stream,
+                               lsgd_ctx** out);
+
+/*
+ * One local step on every replica (inner loop of Algorithm 1, local update
+ * of eq. 2 with per-replica momentum): sample B_loc indices per worker from
+ * its shard, forward, softmax cross-entropy, backward, and
+ *   g = grad + wd * w;  u = m u + g;  d = nesterov ? g + m u : u;
+ *   w = w - lr * d.
+ * d_loss: fp32 [K] receives each replica's mean mini-batch loss at the
+ * pre-update weights, or NULL. Increments s.
+ */
+lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss);
+
+/* Synchronisation of eq. 2: every replica becomes (1/K) sum_k w^k, summed in
+ * a fixed pairwise tree over k. Momentum buffers are left as they are. */
+lsgd_status lsgd_average(lsgd_ctx* ctx);
+
+/* H local steps with step sizes h_lr[0..H-1] (host array), then
+ * lsgd_average. d_loss: fp32 [H][K] or NULL. */
+lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
+                           float* d_loss);
+
+/* Copy replica `replica`'s parameters (or, for replica == -1, their mean by
+ * the same tree as lsgd_average, without changing state) to d_dst fp32 [P]. */
+lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst);
+
+/* Copy replica `replica`'s momentum buffer to d_dst fp32 [P]. */
+lsgd_status lsgd_read_momentum(lsgd_ctx* ctx, int32_t replica, float* d_dst);
+
+/* Overwrite replica `replica` (or all replicas for -1) with d_src fp32 [P]
+ * (and the bf16 operand copy). For checkpoint restore and tests. */
+lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
+                              const float* d_src);
+
+/* Local step counter s (the sampler counter of the next local step). */
+lsgd_status lsgd_get_step(lsgd_ctx* ctx, int64_t* step);
+lsgd_status lsgd_set_step(lsgd_ctx* ctx, int64_t step);
+
+/* The indices the sampler draws at local step `step`: int32 [K][B_loc],
+ * i.i.d. uniform over worker k's shard [floor(kN/K), floor((k+1)N/K)),
+ * Philox4x32-10 with key (seed low, seed high) and counter
+ * (j / 4, step low, k, step high), word j mod 4, mapped by
+ * lo + floor(u * n / 2^32). */
+lsgd_status lsgd_sample_indices(lsgd_ctx* ctx, int64_t step, int32_t* d_idx);
+
+/* Synchronise the context's stream; returns the latched status. */
+lsgd_status lsgd_sync(lsgd_ctx* ctx);
+
+/* Release the host context (device memory stays with the caller). */
+lsgd_status lsgd_destroy(lsgd_ctx* ctx);
+
+/* Static description of a status; never NULL. */
+const char* lsgd_status_string(lsgd_status s);
+
+/* Text of the last error recorded on ctx ("" if none); never NULL. */
+const char* lsgd_last_error(const lsgd_ctx* ctx);
+
+/*
+ * Building blocks, exposed for kernel-level tests and bandwidth sweeps.
+ */
+
+/* Grouped GEMM over G independent problems (the per-replica layer
+ * contractions of the gradient in eq. 2):
+ *   C_g[M][N] = opA(A_g)[M][Kd] * opB(B_g)[Kd][N]   (fp32 accumulation)
+ * trans_a = 0: A_g is [M][Kd] row-major with leading dimension lda;
+ *         = 1: A_g is [Kd][M] row-major (lda >= M).
+ * trans_b = 0: B_g is [Kd][N] (ldb >= N); = 1: B_g is [N][Kd] (ldb >= Kd).
+ * dtype LSGD_FP32: A, B are float; LSGD_BF16: A, B are bfloat16 bit patterns
+ * (uint16). C is fp32 [G][M][N] with leading dimension N, group stride M*N.
+ * Group strides sA, sB are in elements. */
+lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
+                              int32_t G, int32_t M, int32_t N, int32_t Kd,
+                              const void* d_A, int64_t lda, int64_t sA,
+                              const void* d_B, int64_t ldb, int64_t sB,
+                              float* d_C, void* stream);
+
+/* In-place K-way replica average of d_W fp32 [K][P] (the kernel behind
+ * lsgd_average). */
+lsgd_status lsgd_replica_average(float* d_W, int32_t K, int64_t P,
+                                 void* stream);
+
+/* Fused update over n elements (the kernel behind the parameter update of
+ * lsgd_local_step): g = d_G + wd * w; u = m u + g; d = nesterov ? g + m u
+ * : u; w -= lr * d. d_W, d_U updated in place. */
+lsgd_status lsgd_sgd_update(float* d_W, float* d_U, const float* d_G,
+                            int64_t n, float lr, float momentum,
+                            float weight_decay, int32_t nesterov,
+                            void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LSGD_H */

@@ -1,0 +1,455 @@
+// C ABI and host runtime of liblsgd: workspace layout, the launch sequence
+// of one local step, the round driver and error latching.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/lsgd.h"
+#include "kernels.h"
+
+using lsgd::bf16_t;
+using lsgd::GemmArgs;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kReplicaPad = 64;  // replica stride in elements: 256 B
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Layout {
+  int L = 0;
+  int64_t P = 0, Ps = 0;
+  int64_t offW[LSGD_MAX_LAYERS] = {}, offB[LSGD_MAX_LAYERS] = {};
+  size_t esz = 4;  // activation / operand element size
+  // byte offsets into the workspace
+  size_t W = 0, U = 0, Wb = 0, Xb = 0, idx = 0, Z = 0;
+  size_t act[LSGD_MAX_LAYERS] = {}, dZ[LSGD_MAX_LAYERS + 1] = {};
+  size_t total = 0;
+};
+
+bool valid_config(const lsgd_config* c) {
+  if (!c) return false;
+  if (c->model != LSGD_MODEL_MLP) return false;
+  if (c->n_layers < 1 || c->n_layers > LSGD_MAX_LAYERS) return false;
+  for (int i = 0; i <= c->n_layers; ++i)
+    if (c->widths[i] < 1 || c->widths[i] > (1 << 20)) return false;
+  if (c->widths[c->n_layers] < 2) return false;  // classes
+  if (c->K < 1 || c->K > 65535) return false;
+  if (c->B_loc < 1 || c->B_loc > (1 << 20)) return false;
+  if (c->gemm_dtype != LSGD_FP32 && c->gemm_dtype != LSGD_BF16) return false;
+  if (c->nesterov != 0 && c->nesterov != 1) return false;
+  if (!std::isfinite(c->momentum) || c->momentum < 0.f || c->momentum >= 1.f)
+    return false;
+  if (!std::isfinite(c->weight_decay) || c->weight_decay < 0.f) return false;
+  if (c->N < c->K || c->N > (int64_t)INT32_MAX) return false;
+  return true;
+}
+
+Layout make_layout(const lsgd_config* c) {
+  Layout l;
+  l.L = c->n_layers;
+  int64_t o = 0;
+  for (int i = 0; i < l.L; ++i) {
+    l.offW[i] = o;
+    o += (int64_t)c->widths[i] * c->widths[i + 1];
+    l.offB[i] = o;
+    o += c->widths[i + 1];
+  }
+  l.P = o;
+  l.Ps = (o + kReplicaPad - 1) / kReplicaPad * kReplicaPad;
+  const bool bf = c->gemm_dtype == LSGD_BF16;
+  l.esz = bf ? 2 : 4;
+  const size_t K = c->K, B = c->B_loc;
+  size_t t = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = t;
+    t = align_up(t + bytes, kAlign);
+    return at;
+  };
+  l.W = take(K * l.Ps * 4);
+  l.U = take(K * l.Ps * 4);
+  if (bf) {
+    l.Wb = take(K * l.Ps * 2);
+    l.Xb = take((size_t)c->N * c->widths[0] * 2);
+  }
+  l.idx = take(K * B * 4);
+  for (int i = 1; i < l.L; ++i) l.act[i] = take(K * B * c->widths[i] * l.esz);
+  l.Z = take(K * B * c->widths[l.L] * 4);
+  for (int i = 1; i <= l.L; ++i) l.dZ[i] = take(K * B * c->widths[i] * l.esz);
+  l.total = t;
+  return l;
+}
+
+}  // namespace
+
+struct lsgd_ctx {
+  lsgd_config cfg;
+  Layout lay;
+  const float* X = nullptr;
+  const int32_t* y = nullptr;
+  char* ws = nullptr;
+  hipStream_t stream = nullptr;
+  int64_t step = 0;
+  lsgd_status latched = LSGD_OK;
+  std::string err;
+
+  float* W() const { return (float*)(ws + lay.W); }
+  float* U() const { return (float*)(ws + lay.U); }
+  bf16_t* Wb() const { return bf16() ? (bf16_t*)(ws + lay.Wb) : nullptr; }
+  bf16_t* Xb() const { return (bf16_t*)(ws + lay.Xb); }
+  int32_t* idx() const { return (int32_t*)(ws + lay.idx); }
+  void* act(int l) const { return ws + lay.act[l]; }
+  float* Z() const { return (float*)(ws + lay.Z); }
+  void* dZ(int l) const { return ws + lay.dZ[l]; }
+  bool bf16() const { return cfg.gemm_dtype == LSGD_BF16; }
+
+  lsgd_status fail(hipError_t e, const char* what) {
+    latched = LSGD_E_HIP;
+    char buf[256];
+    std::snprintf(buf, sizeof buf, "%s: %s", what, hipGetErrorString(e));
+    err = buf;
+    return LSGD_E_HIP;
+  }
+};
+
+#define LSGD_CK(ctx, expr)                                  \
+  do {                                                      \
+    hipError_t e_ = (expr);                                 \
+    if (e_ != hipSuccess) return (ctx)->fail(e_, #expr);    \
+  } while (0)
+
+namespace {
+
+lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
+  const lsgd_config& cf = c->cfg;
+  const Layout& ly = c->lay;
+  const int K = cf.K, B = cf.B_loc, L = ly.L;
+  const int* w = cf.widths;
+  const int dt = c->bf16() ? 1 : 0;
+  const hipStream_t s = c->stream;
+  float* W = c->W();
+  float* U = c->U();
+  bf16_t* Wb = c->Wb();
+  const void* X0 = dt ? (const void*)c->Xb() : (const void*)c->X;
+
+  LSGD_CK(c, lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
+
+  // forward: Z_l = A_{l-1} W_l + b_l, A_l = relu(Z_l) below the top layer
+  for (int l = 1; l <= L; ++l) {
+    const int din = w[l - 1], dout = w[l];
+    GemmArgs a{};
+    a.G = K;
+    a.M = B;
+    a.N = dout;
+    a.Kd = din;
+    if (l == 1) {
+      a.A = X0;
+      a.sA = 0;
+      a.rowmap = c->idx();
+      a.sRow = B;
+    } else {
+      a.A = c->act(l - 1);
+      a.sA = (long long)B * din;
+    }
+    a.lda = din;
+    a.B = dt ? (const void*)(Wb + ly.offW[l - 1]) : (const void*)(W + ly.offW[l - 1]);
+    a.ldb = dout;
+    a.sB = ly.Ps;
+    a.bias = W + ly.offB[l - 1];
+    a.sBias = ly.Ps;
+    a.ldc = dout;
+    a.sC = (long long)B * dout;
+    if (l < L) {
+      a.C = c->act(l);
+      LSGD_CK(c, lsgd::launch_gemm(dt, 0, 0, lsgd::EPI_BIAS_RELU, dt, a, s));
+    } else {
+      a.C = c->Z();
+      LSGD_CK(c, lsgd::launch_gemm(dt, 0, 0, lsgd::EPI_BIAS, 0, a, s));
+    }
+  }
+
+  LSGD_CK(c, lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L], c->dZ(L), dt,
+                               d_loss, s));
+
+  // backward, top layer first. The input gradient of layer l reads the
+  // pre-update W_l, so it is enqueued before W_l's fused update.
+  for (int l = L; l >= 1; --l) {
+    const int din = w[l - 1], dout = w[l];
+    if (l > 1) {
+      GemmArgs a{};
+      a.G = K;
+      a.M = B;
+      a.N = din;
+      a.Kd = dout;
+      a.A = c->dZ(l);
+      a.lda = dout;
+      a.sA = (long long)B * dout;
+      a.B = dt ? (const void*)(Wb + ly.offW[l - 1]) : (const void*)(W + ly.offW[l - 1]);
+      a.ldb = dout;
+      a.sB = ly.Ps;
+      a.C = c->dZ(l - 1);
+      a.ldc = din;
+      a.sC = (long long)B * din;
+      a.mask = c->act(l - 1);
+      LSGD_CK(c, lsgd::launch_gemm(dt, 0, 1, lsgd::EPI_RELU_MASK, dt, a, s));
+    }
+    GemmArgs a{};
+    a.G = K;
+    a.M = din;
+    a.N = dout;
+    a.Kd = B;
+    if (l == 1) {
+      a.A = X0;
+      a.sA = 0;
+      a.rowmap = c->idx();
+      a.sRow = B;
+    } else {
+      a.A = c->act(l - 1);
+      a.sA = (long long)B * din;
+    }
+    a.lda = din;
+    a.B = c->dZ(l);
+    a.ldb = dout;
+    a.sB = (long long)B * dout;
+    a.ldc = dout;
+    a.sC = ly.Ps;
+    a.W = W + ly.offW[l - 1];
+    a.U = U + ly.offW[l - 1];
+    a.Wb = dt ? Wb + ly.offW[l - 1] : nullptr;
+    a.lr = lr;
+    a.mom = cf.momentum;
+    a.wd = cf.weight_decay;
+    a.nesterov = cf.nesterov;
+    LSGD_CK(c, lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
+    LSGD_CK(c, lsgd::launch_bias_update(c->dZ(l), dt, K, B, dout,
+                                        W + ly.offB[l - 1], U + ly.offB[l - 1],
+                                        ly.Ps, lr, cf.momentum, cf.weight_decay,
+                                        cf.nesterov, s));
+  }
+  c->step += 1;
+  return LSGD_OK;
+}
+
+lsgd_status do_average(lsgd_ctx* c) {
+  LSGD_CK(c, lsgd::launch_average(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
+                                  c->lay.Ps, nullptr, c->stream));
+  return LSGD_OK;
+}
+
+#define LSGD_USABLE(ctx)                                   \
+  do {                                                     \
+    if (!(ctx)) return LSGD_E_INVALID;                     \
+    if ((ctx)->latched != LSGD_OK) return LSGD_E_STATE;    \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+lsgd_status lsgd_param_count(const lsgd_config* cfg, int64_t* P) {
+  if (!valid_config(cfg) || !P) return LSGD_E_INVALID;
+  *P = make_layout(cfg).P;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_workspace_bytes(const lsgd_config* cfg, size_t* bytes) {
+  if (!valid_config(cfg) || !bytes) return LSGD_E_INVALID;
+  *bytes = make_layout(cfg).total;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
+                               const int32_t* d_y, const float* d_w0,
+                               void* d_ws, size_t ws_bytes, void* stream,
+                               lsgd_ctx** out) {
+  if (!out) return LSGD_E_INVALID;
+  *out = nullptr;
+  if (!valid_config(cfg) || !d_X || !d_y || !d_w0 || !d_ws) return LSGD_E_INVALID;
+  if (((uintptr_t)d_ws) % kAlign) return LSGD_E_INVALID;
+  Layout ly = make_layout(cfg);
+  if (ws_bytes < ly.total) return LSGD_E_WORKSPACE;
+  lsgd_ctx* c = new (std::nothrow) lsgd_ctx();
+  if (!c) return LSGD_E_INVALID;
+  c->cfg = *cfg;
+  c->lay = ly;
+  c->X = d_X;
+  c->y = d_y;
+  c->ws = (char*)d_ws;
+  c->stream = (hipStream_t)stream;
+  const int K = cfg->K;
+  lsgd_status st = LSGD_OK;
+  auto check = [&](hipError_t e, const char* what) {
+    if (st == LSGD_OK && e != hipSuccess) st = c->fail(e, what);
+  };
+  check(lsgd::launch_fill(c->W(), 0.f, (long long)K * ly.Ps, c->stream), "fill W");
+  check(lsgd::launch_fill(c->U(), 0.f, (long long)K * ly.Ps, c->stream), "fill U");
+  check(lsgd::launch_broadcast(d_w0, c->W(), c->Wb(), K, ly.P, ly.Ps, -1,
+                               c->stream), "broadcast w0");
+  if (c->bf16())
+    check(lsgd::launch_to_bf16(d_X, c->Xb(), (long long)cfg->N * cfg->widths[0],
+                               c->stream), "dataset to bf16");
+  if (st != LSGD_OK) {
+    delete c;
+    return st;
+  }
+  *out = c;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss) {
+  LSGD_USABLE(ctx);
+  if (!std::isfinite(lr)) return LSGD_E_INVALID;
+  return do_local_step(ctx, lr, d_loss);
+}
+
+lsgd_status lsgd_average(lsgd_ctx* ctx) {
+  LSGD_USABLE(ctx);
+  return do_average(ctx);
+}
+
+lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
+                           float* d_loss) {
+  LSGD_USABLE(ctx);
+  if (H < 0 || (H > 0 && !h_lr)) return LSGD_E_INVALID;
+  for (int h = 0; h < H; ++h)
+    if (!std::isfinite(h_lr[h])) return LSGD_E_INVALID;
+  for (int h = 0; h < H; ++h) {
+    lsgd_status st = do_local_step(ctx, h_lr[h],
+                                   d_loss ? d_loss + (size_t)h * ctx->cfg.K : nullptr);
+    if (st != LSGD_OK) return st;
+  }
+  return do_average(ctx);
+}
+
+lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst) {
+  LSGD_USABLE(ctx);
+  if (!d_dst || replica < -1 || replica >= ctx->cfg.K) return LSGD_E_INVALID;
+  if (replica >= 0) {
+    LSGD_CK(ctx, hipMemcpyAsync(d_dst, ctx->W() + (size_t)replica * ctx->lay.Ps,
+                                ctx->lay.P * sizeof(float),
+                                hipMemcpyDeviceToDevice, ctx->stream));
+  } else {
+    LSGD_CK(ctx, lsgd::launch_average(ctx->W(), nullptr, ctx->cfg.K, ctx->lay.P,
+                                      ctx->lay.Ps, d_dst, ctx->stream));
+  }
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_read_momentum(lsgd_ctx* ctx, int32_t replica, float* d_dst) {
+  LSGD_USABLE(ctx);
+  if (!d_dst || replica < 0 || replica >= ctx->cfg.K) return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipMemcpyAsync(d_dst, ctx->U() + (size_t)replica * ctx->lay.Ps,
+                              ctx->lay.P * sizeof(float),
+                              hipMemcpyDeviceToDevice, ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
+                              const float* d_src) {
+  LSGD_USABLE(ctx);
+  if (!d_src || replica < -1 || replica >= ctx->cfg.K) return LSGD_E_INVALID;
+  LSGD_CK(ctx, lsgd::launch_broadcast(d_src, ctx->W(), ctx->Wb(), ctx->cfg.K,
+                                      ctx->lay.P, ctx->lay.Ps, replica,
+                                      ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_get_step(lsgd_ctx* ctx, int64_t* step) {
+  if (!ctx || !step) return LSGD_E_INVALID;
+  *step = ctx->step;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_set_step(lsgd_ctx* ctx, int64_t step) {
+  LSGD_USABLE(ctx);
+  if (step < 0) return LSGD_E_INVALID;
+  ctx->step = step;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_sample_indices(lsgd_ctx* ctx, int64_t step, int32_t* d_idx) {
+  LSGD_USABLE(ctx);
+  if (!d_idx || step < 0) return LSGD_E_INVALID;
+  LSGD_CK(ctx, lsgd::launch_sample(ctx->cfg.seed, step, ctx->cfg.K, ctx->cfg.N,
+                                   ctx->cfg.B_loc, d_idx, ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_sync(lsgd_ctx* ctx) {
+  LSGD_USABLE(ctx);
+  LSGD_CK(ctx, hipStreamSynchronize(ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_destroy(lsgd_ctx* ctx) {
+  if (!ctx) return LSGD_E_INVALID;
+  delete ctx;
+  return LSGD_OK;
+}
+
+const char* lsgd_status_string(lsgd_status s) {
+  switch (s) {
+    case LSGD_OK: return "ok";
+    case LSGD_E_INVALID: return "invalid argument";
+    case LSGD_E_WORKSPACE: return "workspace too small";
+    case LSGD_E_HIP: return "HIP runtime error";
+    case LSGD_E_STATE: return "context unusable after an earlier HIP error";
+    case LSGD_E_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+const char* lsgd_last_error(const lsgd_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : "";
+}
+
+lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
+                              int32_t G, int32_t M, int32_t N, int32_t Kd,
+                              const void* d_A, int64_t lda, int64_t sA,
+                              const void* d_B, int64_t ldb, int64_t sB,
+                              float* d_C, void* stream) {
+  if ((dtype != LSGD_FP32 && dtype != LSGD_BF16) || (trans_a | trans_b) & ~1)
+    return LSGD_E_INVALID;
+  if (G < 1 || M < 1 || N < 1 || Kd < 1 || G > 65535) return LSGD_E_INVALID;
+  if (!d_A || !d_B || !d_C || sA < 0 || sB < 0) return LSGD_E_INVALID;
+  if (lda < (trans_a ? M : Kd) || ldb < (trans_b ? Kd : N)) return LSGD_E_INVALID;
+  GemmArgs a{};
+  a.G = G;
+  a.M = M;
+  a.N = N;
+  a.Kd = Kd;
+  a.A = d_A;
+  a.lda = lda;
+  a.sA = sA;
+  a.B = d_B;
+  a.ldb = ldb;
+  a.sB = sB;
+  a.C = d_C;
+  a.ldc = N;
+  a.sC = (long long)M * N;
+  hipError_t e = lsgd::launch_gemm(dtype, trans_a, trans_b, lsgd::EPI_STORE, 0, a,
+                                   (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
+}
+
+lsgd_status lsgd_replica_average(float* d_W, int32_t K, int64_t P, void* stream) {
+  if (!d_W || K < 1 || P < 0) return LSGD_E_INVALID;
+  hipError_t e = lsgd::launch_average(d_W, nullptr, K, P, P, nullptr,
+                                      (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
+}
+
+lsgd_status lsgd_sgd_update(float* d_W, float* d_U, const float* d_G, int64_t n,
+                            float lr, float momentum, float weight_decay,
+                            int32_t nesterov, void* stream) {
+  if (!d_W || !d_U || !d_G || n < 0 || (nesterov & ~1)) return LSGD_E_INVALID;
+  hipError_t e = lsgd::launch_sgd_update(d_W, d_U, d_G, n, lr, momentum,
+                                         weight_decay, nesterov,
+                                         (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,82 @@
+// Internal declarations shared by the HIP translation units of liblsgd.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lsgd {
+
+typedef uint16_t bf16_t;  // bfloat16 bit pattern
+
+// fp32 -> bf16, round to nearest even (finite inputs; overflow gives inf).
+__device__ __forceinline__ bf16_t f32_to_bf16(float x) {
+  uint32_t b = __float_as_uint(x);
+  b += 0x7FFFu + ((b >> 16) & 1u);
+  return (bf16_t)(b >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// ---------------------------------------------------------------- GEMM
+enum Epilogue : int {
+  EPI_STORE = 0,       // C = acc (fp32)
+  EPI_BIAS = 1,        // C = acc + bias[n] (fp32 logits)
+  EPI_BIAS_RELU = 2,   // C = relu(acc + bias[n]) (activation dtype)
+  EPI_RELU_MASK = 3,   // C = acc * (mask[m][n] > 0) (activation dtype)
+  EPI_SGD = 4          // fused parameter update of W[m][n] with acc as grad
+};
+
+struct GemmArgs {
+  int G, M, N, Kd;
+  // operand A: element (m, k) at A + g*sA + row(r)*lda + c, where the
+  // storage (r, c) is (m, k) for trans_a == 0 and (k, m) otherwise; row(r)
+  // is rowmap[g*sRow + r] when rowmap != nullptr, else r.
+  const void* A;
+  long long lda, sA;
+  const int32_t* rowmap;
+  long long sRow;
+  // operand B: element (k, n); storage (k, n) for trans_b == 0, (n, k) else.
+  const void* B;
+  long long ldb, sB;
+  // output / epilogue operands (leading dimension ldc, group stride sC)
+  void* C;
+  long long ldc, sC;
+  const float* bias;
+  long long sBias;
+  const void* mask;  // same layout as C (activation dtype)
+  // fused update (EPI_SGD): W, U fp32 and Wb bf16 copy share ldc / sC
+  float* W;
+  float* U;
+  bf16_t* Wb;
+  float lr, mom, wd;
+  int nesterov;
+};
+
+hipError_t launch_gemm(int dtype, int trans_a, int trans_b, int epi,
+                       int out_bf16, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- others
+hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N,
+                         int B, int32_t* idx, hipStream_t s);
+hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,
+                       int K, int B, int C, void* dZ, int dz_bf16,
+                       float* loss, hipStream_t s);
+hipError_t launch_bias_update(const void* dZ, int dz_bf16, int K, int B,
+                              int D, float* b, float* u, long long sParam,
+                              float lr, float mom, float wd, int nesterov,
+                              hipStream_t s);
+hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
+                             float lr, float mom, float wd, int nesterov,
+                             hipStream_t s);
+// K-way average of the first n elements of K rows spaced ld apart.
+hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
+                          long long ld, float* mean_out, hipStream_t s);
+hipError_t launch_broadcast(const float* src, float* W, bf16_t* Wb, int K,
+                            long long n, long long ld, int replica,
+                            hipStream_t s);
+hipError_t launch_to_bf16(const float* x, bf16_t* y, long long n,
+                          hipStream_t s);
+hipError_t launch_fill(float* x, float v, long long n, hipStream_t s);
+
+}  // namespace lsgd

@@ -1,0 +1,284 @@
+"""Python binding of liblsgd (ctypes): argument marshalling only.
+
+Every step of the local-SGD path runs in the HIP kernels behind the C ABI
+declared in include/lsgd.h. PyTorch supplies device memory and the stream.
+If the library has not been built this module raises ImportError; there is
+no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblsgd.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python -m "
+        "paper_1808_07217_amd.build` (hipcc, gfx950) before use")
+
+MAX_LAYERS = 8
+FP32, BF16 = 0, 1
+_c = ctypes
+
+
+class Config(_c.Structure):
+    _fields_ = [
+        ("model", _c.c_int32),
+        ("n_layers", _c.c_int32),
+        ("widths", _c.c_int32 * (MAX_LAYERS + 1)),
+        ("K", _c.c_int32),
+        ("B_loc", _c.c_int32),
+        ("gemm_dtype", _c.c_int32),
+        ("nesterov", _c.c_int32),
+        ("momentum", _c.c_float),
+        ("weight_decay", _c.c_float),
+        ("seed", _c.c_uint64),
+        ("N", _c.c_int64),
+    ]
+
+
+_lib = _c.CDLL(LIB_PATH)
+_P = _c.c_void_p
+_SIGS = {
+    "lsgd_param_count": [_c.POINTER(Config), _c.POINTER(_c.c_int64)],
+    "lsgd_workspace_bytes": [_c.POINTER(Config), _c.POINTER(_c.c_size_t)],
+    "lsgd_init_replicas": [_c.POINTER(Config), _P, _P, _P, _P, _c.c_size_t, _P,
+                           _c.POINTER(_P)],
+    "lsgd_local_step": [_P, _c.c_float, _P],
+    "lsgd_average": [_P],
+    "lsgd_run_round": [_P, _c.c_int32, _c.POINTER(_c.c_float), _P],
+    "lsgd_read_params": [_P, _c.c_int32, _P],
+    "lsgd_read_momentum": [_P, _c.c_int32, _P],
+    "lsgd_write_params": [_P, _c.c_int32, _P],
+    "lsgd_get_step": [_P, _c.POINTER(_c.c_int64)],
+    "lsgd_set_step": [_P, _c.c_int64],
+    "lsgd_sample_indices": [_P, _c.c_int64, _P],
+    "lsgd_sync": [_P],
+    "lsgd_destroy": [_P],
+    "lsgd_status_string": [_c.c_int],
+    "lsgd_last_error": [_P],
+    "lsgd_grouped_gemm": [_c.c_int32, _c.c_int32, _c.c_int32, _c.c_int32,
+                          _c.c_int32, _c.c_int32, _c.c_int32, _P, _c.c_int64,
+                          _c.c_int64, _P, _c.c_int64, _c.c_int64, _P, _P],
+    "lsgd_replica_average": [_P, _c.c_int32, _c.c_int64, _P],
+    "lsgd_sgd_update": [_P, _P, _P, _c.c_int64, _c.c_float, _c.c_float,
+                        _c.c_float, _c.c_int32, _P],
+}
+for _name, _args in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _c.c_int
+_lib.lsgd_status_string.restype = _c.c_char_p
+_lib.lsgd_last_error.restype = _c.c_char_p
+
+EXPORTED = tuple(_SIGS)
+
+
+class LsgdError(RuntimeError):
+    pass
+
+
+def _check(status: int, ctx=None) -> None:
+    if status != 0:
+        msg = _lib.lsgd_status_string(status).decode()
+        if ctx:
+            detail = _lib.lsgd_last_error(ctx).decode()
+            if detail:
+                msg += f" ({detail})"
+        raise LsgdError(f"liblsgd: {msg} [status {status}]")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else _c.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream) -> _c.c_void_p:
+    return _c.c_void_p(stream.cuda_stream)
+
+
+def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
+                dtype: str = "fp32", momentum: float = 0.0,
+                weight_decay: float = 0.0, nesterov: bool = False,
+                seed: int = 0) -> Config:
+    if not 2 <= len(widths) <= MAX_LAYERS + 1:
+        raise ValueError("widths must list d_0 .. d_L with 1 <= L <= 8")
+    cfg = Config()
+    cfg.model = 0
+    cfg.n_layers = len(widths) - 1
+    for i, w in enumerate(widths):
+        cfg.widths[i] = int(w)
+    cfg.K, cfg.B_loc, cfg.N = int(K), int(B_loc), int(N)
+    cfg.gemm_dtype = {"fp32": FP32, "bf16": BF16}[dtype]
+    cfg.nesterov = int(bool(nesterov))
+    cfg.momentum = float(momentum)
+    cfg.weight_decay = float(weight_decay)
+    cfg.seed = int(seed) & (2**64 - 1)
+    return cfg
+
+
+def param_count(cfg: Config) -> int:
+    out = _c.c_int64()
+    _check(_lib.lsgd_param_count(_c.byref(cfg), _c.byref(out)))
+    return out.value
+
+
+def workspace_bytes(cfg: Config) -> int:
+    out = _c.c_size_t()
+    _check(_lib.lsgd_workspace_bytes(_c.byref(cfg), _c.byref(out)))
+    return out.value
+
+
+class Replicas:
+    """K model replicas resident on one GPU (the K workers of local SGD)."""
+
+    def __init__(self, cfg: Config, X: torch.Tensor, y: torch.Tensor,
+                 w0: torch.Tensor, stream: Optional[torch.cuda.Stream] = None):
+        dev = X.device
+        if dev.type != "cuda":
+            raise ValueError("X must be a CUDA (HIP) tensor")
+        if X.dtype != torch.float32 or not X.is_contiguous() or X.dim() != 2:
+            raise ValueError("X must be a contiguous float32 [N][d_0] tensor")
+        if y.dtype != torch.int32 or y.device != dev or y.numel() != X.shape[0]:
+            raise ValueError("y must be int32 [N] on X's device")
+        if X.shape[0] != cfg.N or X.shape[1] != cfg.widths[0]:
+            raise ValueError("X shape does not match the config")
+        self.cfg = cfg
+        self.K, self.B = cfg.K, cfg.B_loc
+        self.P = param_count(cfg)
+        if w0.dtype != torch.float32 or w0.numel() != self.P or w0.device != dev:
+            raise ValueError(f"w0 must be float32 [{self.P}] on X's device")
+        self.device = dev
+        self.stream = stream or torch.cuda.current_stream(dev)
+        nbytes = workspace_bytes(cfg)
+        self._ws_raw = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
+        off = (-self._ws_raw.data_ptr()) % 256
+        self.ws = self._ws_raw[off:off + nbytes]
+        self._keep = (X, y, w0.contiguous())
+        ctx = _c.c_void_p()
+        _check(_lib.lsgd_init_replicas(
+            _c.byref(cfg), _ptr(X), _ptr(y), _ptr(self._keep[2]), _ptr(self.ws),
+            nbytes, _stream_handle(self.stream), _c.byref(ctx)))
+        self._ctx = ctx
+
+    # -- hot path --------------------------------------------------------
+    def local_step(self, lr: float, loss: Optional[torch.Tensor] = None):
+        _check(_lib.lsgd_local_step(self._ctx, float(lr), _ptr(loss)), self._ctx)
+
+    def average(self):
+        _check(_lib.lsgd_average(self._ctx), self._ctx)
+
+    def run_round(self, lrs: Sequence[float], loss: Optional[torch.Tensor] = None):
+        H = len(lrs)
+        arr = (_c.c_float * max(H, 1))(*[float(v) for v in lrs])
+        _check(_lib.lsgd_run_round(self._ctx, H, arr, _ptr(loss)), self._ctx)
+
+    # -- state -----------------------------------------------------------
+    def read_params(self, replica: int = -1, out=None) -> torch.Tensor:
+        out = out if out is not None else torch.empty(self.P, device=self.device)
+        _check(_lib.lsgd_read_params(self._ctx, int(replica), _ptr(out)), self._ctx)
+        return out
+
+    def read_momentum(self, replica: int, out=None) -> torch.Tensor:
+        out = out if out is not None else torch.empty(self.P, device=self.device)
+        _check(_lib.lsgd_read_momentum(self._ctx, int(replica), _ptr(out)), self._ctx)
+        return out
+
+    def write_params(self, src: torch.Tensor, replica: int = -1):
+        if src.dtype != torch.float32 or src.numel() != self.P:
+            raise ValueError("src must be float32 [P]")
+        _check(_lib.lsgd_write_params(self._ctx, int(replica), _ptr(src)), self._ctx)
+
+    @property
+    def step(self) -> int:
+        out = _c.c_int64()
+        _check(_lib.lsgd_get_step(self._ctx, _c.byref(out)))
+        return out.value
+
+    @step.setter
+    def step(self, s: int):
+        _check(_lib.lsgd_set_step(self._ctx, int(s)), self._ctx)
+
+    def sample_indices(self, step: int) -> torch.Tensor:
+        out = torch.empty((self.K, self.B), dtype=torch.int32, device=self.device)
+        _check(_lib.lsgd_sample_indices(self._ctx, int(step), _ptr(out)), self._ctx)
+        return out
+
+    def sync(self):
+        _check(_lib.lsgd_sync(self._ctx), self._ctx)
+
+    def close(self):
+        if getattr(self, "_ctx", None):
+            _lib.lsgd_destroy(self._ctx)
+            self._ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def run_schedule(reps: Replicas, schedule, loss: Optional[torch.Tensor] = None):
+    """Run rounds [(H_t, lr_t), ...] back to back; ``loss`` (fp32 [sum H_t][K])
+    receives the per-step, per-replica losses."""
+    row = 0
+    for H, lr in schedule:
+        reps.run_round([lr] * H, None if loss is None else loss[row:row + H])
+        row += H
+
+
+def post_local_schedule(H: int, rounds: int, lr: float, warm_rounds: int = 0,
+                        lr_after_switch: Optional[float] = None):
+    """Post-local SGD (section 3 of the paper): H_(t) = 1 for t <= t'
+    (= warm_rounds), else H; the step size switches at the same time."""
+    lr2 = lr if lr_after_switch is None or warm_rounds == 0 else lr_after_switch
+    return [(1, lr)] * warm_rounds + [(H, lr2)] * rounds
+
+
+# -- building blocks ------------------------------------------------------
+def grouped_gemm(A: torch.Tensor, B: torch.Tensor, trans_a=False, trans_b=False,
+                 out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """C[g] = op(A[g]) @ op(B[g]) on the matrix cores (fp32 or bf16 inputs,
+    fp32 accumulation and output). A, B are contiguous 3-D tensors."""
+    if A.dtype != B.dtype or A.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("A and B must both be float32 or both bfloat16")
+    if A.dim() != 3 or B.dim() != 3 or A.shape[0] != B.shape[0]:
+        raise ValueError("A, B must be [G][.][.] with the same G")
+    A, B = A.contiguous(), B.contiguous()
+    G = A.shape[0]
+    M, Kd = (A.shape[2], A.shape[1]) if trans_a else (A.shape[1], A.shape[2])
+    Kb, N = (B.shape[2], B.shape[1]) if trans_b else (B.shape[1], B.shape[2])
+    if Kb != Kd:
+        raise ValueError("inner dimensions differ")
+    out = out if out is not None else torch.empty((G, M, N), device=A.device)
+    dt = BF16 if A.dtype == torch.bfloat16 else FP32
+    _check(_lib.lsgd_grouped_gemm(
+        dt, int(trans_a), int(trans_b), G, M, N, Kd, _ptr(A), A.shape[2],
+        A.shape[1] * A.shape[2], _ptr(B), B.shape[2], B.shape[1] * B.shape[2],
+        _ptr(out), _stream_handle(torch.cuda.current_stream(A.device))))
+    return out
+
+
+def replica_average(W: torch.Tensor) -> None:
+    """In-place K-way average of a contiguous float32 [K][P] tensor."""
+    if W.dtype != torch.float32 or W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be contiguous float32 [K][P]")
+    _check(_lib.lsgd_replica_average(
+        _ptr(W), W.shape[0], W.shape[1],
+        _stream_handle(torch.cuda.current_stream(W.device))))
+
+
+def sgd_update(W, U, G, lr, momentum, weight_decay, nesterov=False) -> None:
+    """In-place fused momentum-SGD update of float32 tensors W, U with grad G."""
+    for t in (W, U, G):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("W, U, G must be contiguous float32")
+    _check(_lib.lsgd_sgd_update(
+        _ptr(W), _ptr(U), _ptr(G), W.numel(), float(lr), float(momentum),
+        float(weight_decay), int(bool(nesterov)),
+        _stream_handle(torch.cuda.current_stream(W.device))))

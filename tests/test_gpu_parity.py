@@ -1,0 +1,228 @@
+"""End-to-end parity of the HIP path with the CPU oracle, through the C ABI.
+
+Tolerances (the floating-point bar of the build):
+  * fp32 parameters: whole-vector normwise max |a - b| / max |b| <= 1e-5;
+  * fp32 losses: relative error <= 1e-3 over the trajectory;
+  * bf16 GEMM operands (fp32 master weights): losses <= 2e-2 relative;
+  * sampled indices: bit-exact (checked in the kernel tests and here through
+    the losses' data).
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wk
+from oracle import lsgd_oracle as O
+from gpu_util import make_replicas, normwise, rel, device
+
+pytestmark = pytest.mark.gpu
+
+PARAM_TOL_FP32 = 1e-5
+LOSS_TOL_FP32 = 1e-3
+LOSS_TOL_BF16 = 2e-2
+
+
+def _small(widths, dtype="fp32", nesterov=False, K=3, B=20, N=999, H=3,
+           rounds=2, momentum=0.9, wd=1e-3, lr=0.02):
+    return wk.Workload(name="small", model="mlp", widths=widths, dtype=dtype,
+                       K=K, B_loc=B, H=H, rounds=rounds, lr=lr,
+                       momentum=momentum, nesterov=nesterov, weight_decay=wd,
+                       data="custom", N=N, sample_seed=0xABCDEF + K * 7 + B)
+
+
+def _small_data(w, seed=5):
+    rng = np.random.default_rng(seed)
+    C = w.widths[-1]
+    mu = rng.standard_normal((C, w.widths[0]))
+    y = rng.integers(0, C, w.N).astype(np.int32)
+    X = (mu[y] + rng.standard_normal((w.N, w.widths[0]))).astype(np.float32)
+    w0 = np.concatenate([
+        np.concatenate([(rng.standard_normal(a * b) * np.sqrt(2.0 / a)),
+                        rng.standard_normal(b) * 0.1])
+        for a, b in wk.layer_shapes(w.widths)]).astype(np.float32)
+    return X, y, w0
+
+
+def _compare_steps(w, X, y, w0, param_tol, loss_tol, rounds=None):
+    """Run both sides round by round; compare every replica after every
+    local step and after every average."""
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss_d = torch.empty(w.K, device=device())
+    worst = 0.0
+    for t, (H, lr) in enumerate(O.schedule(w)[:rounds]):
+        for h in range(H):
+            reps.local_step(lr, loss_d)
+            want_loss = O.local_step(st, w, X, y, lr)
+            got_loss = loss_d.cpu().numpy()
+            assert np.all(rel(got_loss, want_loss) <= loss_tol), (t, h, got_loss, want_loss)
+            for k in range(w.K):
+                e = normwise(reps.read_params(k).cpu().numpy(), st.W[k])
+                worst = max(worst, e)
+                assert e <= param_tol, (t, h, k, e)
+        reps.average()
+        st.W = O.average(st.W)
+        e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
+        assert e <= param_tol, (t, "avg", e)
+        for k in (0, w.K - 1):
+            np.testing.assert_array_equal(reps.read_params(k).cpu().numpy(),
+                                          reps.read_params(0).cpu().numpy())
+    return worst
+
+
+@pytest.mark.parametrize("widths,nesterov,momentum", [
+    ((70, 48, 36, 10), False, 0.9),
+    ((70, 48, 36, 10), True, 0.9),
+    ((64, 128, 64, 10), False, 0.0),
+    ((37, 10), False, 0.5),
+    ((130, 200, 66, 100, 7), True, 0.9),
+])
+def test_small_mlp_every_step(widths, nesterov, momentum):
+    w = _small(widths, nesterov=nesterov, momentum=momentum)
+    print(f"small fp32 {widths} nesterov={nesterov}", flush=True)
+    X, y, w0 = _small_data(w)
+    _compare_steps(w, X, y, w0, PARAM_TOL_FP32, 1e-4)
+
+
+@pytest.mark.parametrize("widths", [(70, 48, 36, 10), (64, 128, 64, 10)])
+def test_small_mlp_bf16_every_step(widths):
+    w = _small(widths, dtype="bf16")
+    print(f"small bf16 {widths}", flush=True)
+    X, y, w0 = _small_data(w)
+    # bf16 operands: an operand rounded on the other side of a tie moves by
+    # 2^-8 relative; the parameter bound is the loss bound of the workload
+    _compare_steps(w, X, y, w0, 2e-3, LOSS_TOL_BF16)
+
+
+def test_softmax_regression_full_run():
+    """Workload 1 (softmax regression, K=4, H=4, 50 rounds): every step."""
+    w = wk.get("softmax_d64")
+    X, y = wk.dataset(w)
+    _compare_steps(w, X, y, wk.initial_weights(w), PARAM_TOL_FP32, LOSS_TOL_FP32)
+
+
+def test_h1_local_sgd_equals_minibatch_sgd_on_gpu():
+    """H = 1 local SGD is mini-batch SGD with batch K * B_loc (the paper's
+    special case below eq. 2): the GPU run against the oracle's separately
+    written mini-batch SGD."""
+    w = _small((70, 48, 36, 10), nesterov=True, H=1, rounds=6)
+    X, y, w0 = _small_data(w, seed=9)
+    reps = make_replicas(w, X, y, w0)
+    for _ in range(6):
+        reps.run_round([w.lr])
+    ref = O.minibatch_sgd(w, X, y, w0, steps=6, lr=w.lr)
+    assert normwise(reps.read_params(0).cpu().numpy(), ref) <= PARAM_TOL_FP32
+
+
+def test_runs_are_bitwise_deterministic():
+    w = _small((70, 48, 36, 10), nesterov=True, H=4, rounds=2)
+    X, y, w0 = _small_data(w, seed=3)
+    outs = []
+    for _ in range(2):
+        reps = make_replicas(w, X, y, w0)
+        loss = torch.empty(8, w.K, device=device())
+        reps.run_round([w.lr] * 4, loss[:4])
+        reps.run_round([w.lr] * 4, loss[4:])
+        outs.append((reps.read_params(-1).cpu().numpy(), loss.cpu().numpy()))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
+def test_run_round_equals_steps_then_average():
+    w = _small((70, 48, 36, 10), H=3, rounds=1)
+    X, y, w0 = _small_data(w, seed=4)
+    a = make_replicas(w, X, y, w0)
+    b = make_replicas(w, X, y, w0)
+    a.run_round([0.02, 0.01, 0.03])
+    for lr in (0.02, 0.01, 0.03):
+        b.local_step(lr)
+    b.average()
+    np.testing.assert_array_equal(a.read_params(-1).cpu().numpy(),
+                                  b.read_params(-1).cpu().numpy())
+    for k in range(w.K):
+        np.testing.assert_array_equal(a.read_momentum(k).cpu().numpy(),
+                                      b.read_momentum(k).cpu().numpy())
+    assert a.step == b.step == 3
+
+
+def test_momentum_buffers_are_not_averaged():
+    w = _small((70, 48, 36, 10), H=2, rounds=1)
+    X, y, w0 = _small_data(w, seed=6)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    O.run_round(st, w, X, y, 2, w.lr)
+    reps.run_round([w.lr] * 2)
+    for k in range(w.K):
+        assert normwise(reps.read_momentum(k).cpu().numpy(), st.U[k]) <= PARAM_TOL_FP32
+    u0 = reps.read_momentum(0).cpu().numpy()
+    assert not np.allclose(u0, reps.read_momentum(1).cpu().numpy())
+
+
+def test_write_params_and_step_counter_resume_exactly():
+    """Checkpoint/resume: state restored into a fresh context continues
+    bit-identically (the sampler is stateless given the step counter)."""
+    w = _small((70, 48, 36, 10), momentum=0.0, H=2, rounds=1)
+    X, y, w0 = _small_data(w, seed=8)
+    a = make_replicas(w, X, y, w0)
+    a.run_round([0.02, 0.02])
+    mid = a.read_params(-1)
+    b = make_replicas(w, X, y, w0)
+    b.write_params(mid)
+    b.step = a.step
+    a.run_round([0.02, 0.02])
+    b.run_round([0.02, 0.02])
+    np.testing.assert_array_equal(a.read_params(-1).cpu().numpy(),
+                                  b.read_params(-1).cpu().numpy())
+
+
+# --------------------------------------------------------- full-size rounds
+@pytest.fixture(scope="module")
+def img_data():
+    w = wk.get("mlp_512")
+    return wk.dataset(w)
+
+
+def test_mlp_512_first_round_full_size(img_data):
+    """Workload 2 at its real shape (K=16, B_loc=128, H=16): every replica
+    after the 16 local steps, and the average, against the oracle."""
+    w = wk.get("mlp_512")
+    X, y = img_data
+    w0 = wk.initial_weights(w)
+    print("mlp_512 round 1", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    loss = torch.empty(w.H, w.K, device=device())
+    for h in range(w.H):
+        reps.local_step(w.lr, loss[h])
+    st = O.State(w0, w.K)
+    ref_loss = np.stack([O.local_step(st, w, X, y, w.lr) for _ in range(w.H)])
+    assert np.all(rel(loss.cpu().numpy(), ref_loss) <= LOSS_TOL_FP32)
+    for k in range(w.K):
+        e = normwise(reps.read_params(k).cpu().numpy(), st.W[k])
+        assert e <= PARAM_TOL_FP32, (k, e)
+    reps.average()
+    st.W = O.average(st.W)
+    e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
+    print(f"mlp_512 round-1 averaged params normwise error {e:.3e}", flush=True)
+    assert e <= PARAM_TOL_FP32
+
+
+def test_wide_bf16_first_round_two_replicas_full_size(img_data):
+    """Workload 4 at its real shape (K=64, B_loc=64, H=8, bf16 operands):
+    replicas 0 and 63 through the first round's local steps."""
+    w = wk.get("wide_mlp_2048_bf16")
+    X, y = img_data
+    w0 = wk.initial_weights(w)
+    print("wide bf16 round 1", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    loss = torch.empty(w.H, w.K, device=device())
+    for h in range(w.H):
+        reps.local_step(w.lr, loss[h])
+    st = O.State(w0, w.K)
+    ref = np.stack([O.local_step(st, w, X, y, w.lr, replicas=[0, w.K - 1])
+                    for _ in range(w.H)])
+    got = loss.cpu().numpy()
+    for k in (0, w.K - 1):
+        assert np.all(rel(got[:, k], ref[:, k]) <= LOSS_TOL_BF16)
+        e = normwise(reps.read_params(k).cpu().numpy(), st.W[k])
+        print(f"wide bf16 replica {k} params normwise error {e:.3e}", flush=True)
+        assert e <= 2e-3

@@ -70,13 +70,6 @@ class Workload:
     def n_layers(self) -> int:
         return len(self.widths) - 1
 
-    def schedule(self):
-        """(H_t, lr_t) for every round t = 1..T, warm phase first."""
-        out = [(1, self.lr)] * self.warm_rounds
-        lr2 = self.lr_after_switch if self.warm_rounds else self.lr
-        out += [(self.H, lr2)] * self.rounds
-        return out
-
     def scaled(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
 
