@@ -1,0 +1,239 @@
+"""Throughput of the local-SGD hot path on one MI355X.
+
+One step = one local-SGD round: H local steps on every one of the K replicas
+(sample, gather, forward, loss, backward, fused update) followed by the K-way
+average. Default workload: MLP 3072-512-512-10, fp32, K=16, B_loc=128, H=16,
+heavy-ball momentum 0.9, weight decay 1e-4, synthetic 32x32x3 / 10-class
+Gaussian data (32,768 samples per round).
+
+Prints one JSON line: samples/s, the roofline position of the dominant kernel
+(timed with HIP events on the library's stream) and the CPU oracle timed on a
+bounded sample of the same workload on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
+METRIC = "aggregate samples/s per local-SGD round at 1 GPU"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20, help="timed rounds")
+    p.add_argument("--warmup", type=int, default=3, help="untimed rounds")
+    p.add_argument("--workload", default="mlp_512")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-kernel-timing", action="store_true")
+    return p.parse_args()
+
+
+def kernel_cost(tag: str, w) -> tuple:
+    """Algorithmic (flops, bytes) of one launch of the kernel at `tag`.
+
+    Bytes count each operand once: read inputs, read+write of what the
+    kernel updates; weights W and momentum U are fp32 (4 B) masters, GEMM
+    operands 4 B (fp32) or 2 B (bf16)."""
+    K, B = w.K, w.B_loc
+    d = w.widths
+    L = len(d) - 1
+    e = 2 if w.dtype == "bf16" else 4
+    P = sum(a * b + b for a, b in zip(d[:-1], d[1:]))
+    if tag == "sample":
+        return 0, K * B * 4
+    if tag == "xent":
+        return 0, K * B * d[L] * (4 + e) + K * B * 8
+    if tag == "average":
+        return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0)
+    name, l = tag.rstrip("0123456789"), int(tag[len(tag.rstrip("0123456789")):])
+    din, dout = d[l - 1], d[l]
+    mn = din * dout
+    if name == "fwd":
+        out = e if l < L else 4
+        return (2 * K * B * mn,
+                K * (B * din * e + mn * e + dout * 4 + B * dout * out))
+    if name == "dgrad":
+        return 2 * K * B * mn, K * (B * dout * e + mn * e + 2 * B * din * e)
+    if name == "wgrad_update":
+        upd = 16 + (2 if e == 2 else 0)
+        return 2 * K * B * mn, K * (B * din * e + B * dout * e + mn * upd)
+    if name == "bias_update":
+        return K * B * dout, K * (B * dout * e + dout * 16)
+    raise ValueError(tag)
+
+
+def gemm_flops_per_local_step(w) -> int:
+    d = w.widths
+    f = 0
+    for l in range(1, len(d)):
+        mn = d[l - 1] * d[l]
+        f += 2 * 2 * w.B_loc * mn                   # forward + weight grad
+        if l > 1:
+            f += 2 * w.B_loc * mn                   # input gradient
+    return f * w.K
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "elementwise.hip"):
+        with open(os.path.join(ROOT, "paper_1808_07217_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(tag: str):
+    """HBM bytes per launch of the dominant kernel from the committed PMC
+    summary, if it was taken on the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_digest") != source_digest() or t.get("tag") != tag:
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(w, X, y, w0):
+    """The CPU oracle (as it is) on one full round of the workload: H local
+    steps on all K replicas plus the average, on this host's cores."""
+    from oracle import lsgd_oracle as O
+    threads = None
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max((i.get("num_threads") or 1) for i in info) if info else 1
+    except Exception:
+        threads = os.cpu_count()
+    st = O.State(w0, w.K)
+    t0 = time.perf_counter()
+    O.run_round(st, w, X, y, w.H, w.lr)
+    dt = time.perf_counter() - t0
+    samples = w.K * w.H * w.B_loc
+    return {"value": samples / dt, "unit": "samples/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"one full round of {w.name} (H={w.H} local steps on "
+                      f"all K={w.K} replicas + average, {samples} samples) in "
+                      f"{dt:.2f} s; fp64 numpy, BLAS threads={threads}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU "
+              "path (the K workers are replicas on one device)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as wk
+    from paper_1808_07217_amd import lsgd as L
+
+    w = wk.get(args.workload)
+    X, y = wk.dataset(w)
+    w0 = wk.initial_weights(w)
+    dev = torch.device("cuda", 0)
+    cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype,
+                        momentum=w.momentum, weight_decay=w.weight_decay,
+                        nesterov=w.nesterov, seed=w.sample_seed)
+    Xd = torch.from_numpy(np.array(X)).to(dev)
+    yd = torch.from_numpy(np.array(y)).to(dev)
+    reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))
+    stream = reps.stream
+    H = w.H
+    lrs = [w.lr] * H
+    loss = torch.empty((args.warmup + args.steps + 8) * H, w.K, device=dev)
+
+    def rnd(i):
+        reps.run_round(lrs, loss[i * H:(i + 1) * H])
+
+    for i in range(args.warmup):
+        rnd(i)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            rnd(args.warmup + i)
+        ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
+    samples = w.K * H * w.B_loc
+    value = samples / (ms_per_step / 1e3)
+    l_all = loss[:(args.warmup + args.steps) * H].float().cpu().numpy()
+    if not np.all(np.isfinite(l_all)):
+        raise RuntimeError("non-finite loss in the benchmark run")
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: MLP {'-'.join(map(str, w.widths))} "
+                               f"{w.dtype}, K={w.K}, B_loc={w.B_loc}, H={H}",
+                   "K": w.K, "B_loc": w.B_loc, "H": H,
+                   "samples_per_step": samples,
+                   "momentum": w.momentum, "nesterov": w.nesterov,
+                   "weight_decay": w.weight_decay},
+    }
+    gemm_flops = gemm_flops_per_local_step(w) * H
+    out["e2e_mfma_frac"] = round(gemm_flops / (ms_per_step / 1e3) /
+                                 (PEAK_TFLOPS[w.dtype] * 1e12), 4)
+
+    if not args.no_kernel_timing:
+        # a second pass with every launch bracketed by HIP events
+        reps.profile(True)
+        base = args.warmup + args.steps
+        for i in range(min(args.steps, 8)):
+            rnd(base + i)
+        rep = reps.profile_report()
+        reps.profile(False)
+        nround = min(args.steps, 8)
+        per_round = {t: ms / nround for t, (n, ms) in rep.items()}
+        dom = max(per_round, key=per_round.get)
+        n, ms = rep[dom]
+        avg_s = ms / n / 1e3
+        flops, nbytes = kernel_cost(dom, w)
+        ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
+        if nbytes and flops / nbytes < ridge:
+            roof = {"bound": "hbm", "achieved": round(nbytes / avg_s / 1e9, 1),
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        else:
+            roof = {"bound": "mfma",
+                    "achieved": round(flops / avg_s / 1e12, 2),
+                    "peak": PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s"}
+        roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+        roof["traffic"] = traffic_for(dom)
+        roof["kernel"] = dom
+        roof["avg_launch_us"] = round(avg_s * 1e6, 2)
+        roof["algorithmic_bytes_per_launch"] = nbytes
+        roof["algorithmic_flops_per_launch"] = flops
+        out["roofline"] = roof
+        out["kernel_ms_per_step"] = {t: round(v, 4) for t, v in
+                                     sorted(per_round.items(),
+                                            key=lambda kv: -kv[1])}
+    reps.close()
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, X, y, w0)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

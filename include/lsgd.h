@@ -151,6 +151,17 @@ const char* lsgd_status_string(lsgd_status s);
 /* Text of the last error recorded on ctx ("" if none); never NULL. */
 const char* lsgd_last_error(const lsgd_ctx* ctx);
 
+/* Per-launch timing (a measurement aid, off by default): while enabled,
+ * every kernel the context launches is bracketed by two HIP events on its
+ * stream, tagged by launch site (sample, fwd<l>, xent, dgrad<l>,
+ * wgrad_update<l>, bias_update<l>, average). */
+lsgd_status lsgd_profile_enable(lsgd_ctx* ctx, int32_t enable);
+
+/* Synchronise, then write one line "tag launches total_ms" per tag into the
+ * host buffer h_buf (NUL-terminated; LSGD_E_INVALID if len is too small) and
+ * clear the records. */
+lsgd_status lsgd_profile_report(lsgd_ctx* ctx, char* h_buf, size_t len);
+
 /*
  * Building blocks, exposed for kernel-level tests and bandwidth sweeps.
  */

@@ -5,6 +5,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "../../include/lsgd.h"
 #include "kernels.h"
@@ -85,8 +86,33 @@ Layout make_layout(const lsgd_config* c) {
 
 }  // namespace
 
+// Opt-in per-launch timing: a pair of HIP events on the context's stream
+// around every kernel launch, tagged by launch site.
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  struct Rec { std::string tag; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+
+  hipError_t event(hipEvent_t* e) {
+    if (used == pool.size()) {
+      hipEvent_t ev;
+      hipError_t r = hipEventCreate(&ev);
+      if (r != hipSuccess) return r;
+      pool.push_back(ev);
+    }
+    *e = pool[used++];
+    return hipSuccess;
+  }
+  ~Profiler() {
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  }
+};
+
 struct lsgd_ctx {
   lsgd_config cfg;
+  Profiler prof;
   Layout lay;
   const float* X = nullptr;
   const int32_t* y = nullptr;
@@ -121,6 +147,22 @@ struct lsgd_ctx {
     if (e_ != hipSuccess) return (ctx)->fail(e_, #expr);    \
   } while (0)
 
+// A kernel launch, bracketed by profiling events when profiling is on.
+#define LSGD_LAUNCH(ctx, tag, expr)                                        \
+  do {                                                                     \
+    hipEvent_t a_ = nullptr, b_ = nullptr;                                 \
+    if ((ctx)->prof.on) {                                                  \
+      LSGD_CK(ctx, (ctx)->prof.event(&a_));                                \
+      LSGD_CK(ctx, (ctx)->prof.event(&b_));                                \
+      LSGD_CK(ctx, hipEventRecord(a_, (ctx)->stream));                     \
+    }                                                                      \
+    LSGD_CK(ctx, expr);                                                    \
+    if ((ctx)->prof.on) {                                                  \
+      LSGD_CK(ctx, hipEventRecord(b_, (ctx)->stream));                     \
+      (ctx)->prof.recs.push_back({std::string(tag), a_, b_});              \
+    }                                                                      \
+  } while (0)
+
 namespace {
 
 lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
@@ -135,7 +177,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   bf16_t* Wb = c->Wb();
   const void* X0 = dt ? (const void*)c->Xb() : (const void*)c->X;
 
-  LSGD_CK(c, lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
+  LSGD_LAUNCH(c, "sample", lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
 
   // forward: Z_l = A_{l-1} W_l + b_l, A_l = relu(Z_l) below the top layer
   for (int l = 1; l <= L; ++l) {
@@ -164,15 +206,17 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     a.sC = (long long)B * dout;
     if (l < L) {
       a.C = c->act(l);
-      LSGD_CK(c, lsgd::launch_gemm(dt, 0, 0, lsgd::EPI_BIAS_RELU, dt, a, s));
+      LSGD_LAUNCH(c, "fwd" + std::to_string(l),
+                  lsgd::launch_gemm(dt, 0, 0, lsgd::EPI_BIAS_RELU, dt, a, s));
     } else {
       a.C = c->Z();
-      LSGD_CK(c, lsgd::launch_gemm(dt, 0, 0, lsgd::EPI_BIAS, 0, a, s));
+      LSGD_LAUNCH(c, "fwd" + std::to_string(l),
+                  lsgd::launch_gemm(dt, 0, 0, lsgd::EPI_BIAS, 0, a, s));
     }
   }
 
-  LSGD_CK(c, lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L], c->dZ(L), dt,
-                               d_loss, s));
+  LSGD_LAUNCH(c, "xent", lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L],
+                                             c->dZ(L), dt, d_loss, s));
 
   // backward, top layer first. The input gradient of layer l reads the
   // pre-update W_l, so it is enqueued before W_l's fused update.
@@ -194,7 +238,8 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       a.ldc = din;
       a.sC = (long long)B * din;
       a.mask = c->act(l - 1);
-      LSGD_CK(c, lsgd::launch_gemm(dt, 0, 1, lsgd::EPI_RELU_MASK, dt, a, s));
+      LSGD_LAUNCH(c, "dgrad" + std::to_string(l),
+                  lsgd::launch_gemm(dt, 0, 1, lsgd::EPI_RELU_MASK, dt, a, s));
     }
     GemmArgs a{};
     a.G = K;
@@ -223,19 +268,22 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     a.mom = cf.momentum;
     a.wd = cf.weight_decay;
     a.nesterov = cf.nesterov;
-    LSGD_CK(c, lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
-    LSGD_CK(c, lsgd::launch_bias_update(c->dZ(l), dt, K, B, dout,
-                                        W + ly.offB[l - 1], U + ly.offB[l - 1],
-                                        ly.Ps, lr, cf.momentum, cf.weight_decay,
-                                        cf.nesterov, s));
+    LSGD_LAUNCH(c, "wgrad_update" + std::to_string(l),
+                lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
+    LSGD_LAUNCH(c, "bias_update" + std::to_string(l),
+                lsgd::launch_bias_update(c->dZ(l), dt, K, B, dout,
+                                         W + ly.offB[l - 1], U + ly.offB[l - 1],
+                                         ly.Ps, lr, cf.momentum, cf.weight_decay,
+                                         cf.nesterov, s));
   }
   c->step += 1;
   return LSGD_OK;
 }
 
 lsgd_status do_average(lsgd_ctx* c) {
-  LSGD_CK(c, lsgd::launch_average(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
-                                  c->lay.Ps, nullptr, c->stream));
+  LSGD_LAUNCH(c, "average",
+              lsgd::launch_average(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
+                                   c->lay.Ps, nullptr, c->stream));
   return LSGD_OK;
 }
 
@@ -400,6 +448,46 @@ const char* lsgd_status_string(lsgd_status s) {
     case LSGD_E_UNSUPPORTED: return "unsupported";
   }
   return "unknown status";
+}
+
+lsgd_status lsgd_profile_enable(lsgd_ctx* ctx, int32_t enable) {
+  LSGD_USABLE(ctx);
+  if (enable != 0 && enable != 1) return LSGD_E_INVALID;
+  ctx->prof.on = enable != 0;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_profile_report(lsgd_ctx* ctx, char* h_buf, size_t len) {
+  LSGD_USABLE(ctx);
+  if (!h_buf || len == 0) return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipStreamSynchronize(ctx->stream));
+  std::vector<std::string> tags;
+  std::vector<double> ms;
+  std::vector<long long> n;
+  for (const auto& r : ctx->prof.recs) {
+    float t = 0.f;
+    LSGD_CK(ctx, hipEventElapsedTime(&t, r.a, r.b));
+    size_t i = 0;
+    while (i < tags.size() && tags[i] != r.tag) ++i;
+    if (i == tags.size()) {
+      tags.push_back(r.tag);
+      ms.push_back(0.0);
+      n.push_back(0);
+    }
+    ms[i] += t;
+    n[i] += 1;
+  }
+  std::string out;
+  for (size_t i = 0; i < tags.size(); ++i) {
+    char line[160];
+    std::snprintf(line, sizeof line, "%s %lld %.6f\n", tags[i].c_str(), n[i], ms[i]);
+    out += line;
+  }
+  ctx->prof.recs.clear();
+  ctx->prof.used = 0;
+  if (out.size() + 1 > len) return LSGD_E_INVALID;
+  std::memcpy(h_buf, out.c_str(), out.size() + 1);
+  return LSGD_OK;
 }
 
 const char* lsgd_last_error(const lsgd_ctx* ctx) {

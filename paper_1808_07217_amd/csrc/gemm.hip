@@ -60,7 +60,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int g, int m, int n,
 }
 
 // ------------------------------------------------------------------ fp32
-template <bool AT, bool BT, int EPI, int BM, int BN>
+template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN>
 __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
                                                      int vecB) {
   constexpr int BK = 16, PAD = 4;
@@ -77,7 +77,8 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
   const float* A = (const float*)a.A + (long long)g * a.sA;
   const float* B = (const float*)a.B + (long long)g * a.sB;
-  const int32_t* rmap = a.rowmap ? a.rowmap + (long long)g * a.sRow : nullptr;
+  // GATHER: rows of A come from a row map (the sampled mini-batch indices)
+  const int32_t* rmap = GATHER ? a.rowmap + (long long)g * a.sRow : nullptr;
   const int M = a.M, N = a.N, Kd = a.Kd;
 
   float4 ra[NA], rb[NB];
@@ -102,14 +103,14 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
         const int r = q >> 2, c = k0 + (q & 3) * 4, row = m0 + r;
         ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
         if (row < M) {
-          const long long sr = rmap ? rmap[row] : row;
+          const long long sr = GATHER ? rmap[row] : row;
           ra[i] = load4(A + sr * a.lda + c, Kd - c, vecA);
         }
       } else {  // storage [Kd][M]: rows k, BM/4 float4 per row
         const int r = q / (BM / 4), c = m0 + (q % (BM / 4)) * 4, kr = k0 + r;
         ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
         if (kr < Kd) {
-          const long long sr = rmap ? rmap[kr] : kr;
+          const long long sr = GATHER ? rmap[kr] : kr;
           ra[i] = load4(A + sr * a.lda + c, M - c, vecA);
         }
       }
@@ -207,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
 }
 
 // ------------------------------------------------------------------ bf16
-template <bool AT, bool BT, int EPI, int BM, int BN>
+template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN>
 __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
                                                       int vecB) {
   constexpr int BK = 32, KP = BK + 8;  // row pitch 80 B keeps 16-B alignment
@@ -224,7 +225,8 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
   const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
   const bf16_t* A = (const bf16_t*)a.A + (long long)g * a.sA;
   const bf16_t* B = (const bf16_t*)a.B + (long long)g * a.sB;
-  const int32_t* rmap = a.rowmap ? a.rowmap + (long long)g * a.sRow : nullptr;
+  // GATHER: rows of A come from a row map (the sampled mini-batch indices)
+  const int32_t* rmap = GATHER ? a.rowmap + (long long)g * a.sRow : nullptr;
   const int M = a.M, N = a.N, Kd = a.Kd;
 
   uint4 ra[NA], rb[NB];
@@ -246,13 +248,13 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
       if constexpr (!AT) {  // [M][Kd]: 4 vectors per row
         const int r = q >> 2, c = k0 + (q & 3) * 8, row = m0 + r;
         if (row < M) {
-          const long long sr = rmap ? rmap[row] : row;
+          const long long sr = GATHER ? rmap[row] : row;
           ra[i] = load8(A + sr * a.lda + c, Kd - c, vecA);
         }
       } else {  // [Kd][M]: BM/8 vectors per row
         const int r = q / (BM / 8), c = m0 + (q % (BM / 8)) * 8, kr = k0 + r;
         if (kr < Kd) {
-          const long long sr = rmap ? rmap[kr] : kr;
+          const long long sr = GATHER ? rmap[kr] : kr;
           ra[i] = load8(A + sr * a.lda + c, M - c, vecA);
         }
       }
@@ -360,18 +362,22 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-template <bool AT, bool BT, int EPI>
+template <bool AT, bool BT, int EPI, bool GATHER = false>
 hipError_t dispatch(int dtype, const GemmArgs& a, hipStream_t s) {
+  if (GATHER != (a.rowmap != nullptr)) {
+    if (a.rowmap) return dispatch<AT, BT, EPI, true>(dtype, a, s);
+    return hipErrorInvalidValue;
+  }
   constexpr int BM = 64, BN = 64;
   dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, a.G);
   const int esz = dtype == 1 ? 8 : 4;  // elements per vector load
   const int vecA = a.lda % esz == 0 && a.sA % esz == 0 && aligned16(a.A);
   const int vecB = a.ldb % esz == 0 && a.sB % esz == 0 && aligned16(a.B);
   if (dtype == 1)
-    hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, BM, BN>), grid, dim3(kThreads),
+    hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, BM, BN>), grid, dim3(kThreads),
                        0, s, a, vecA, vecB);
   else
-    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, BM, BN>), grid, dim3(kThreads),
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, BM, BN>), grid, dim3(kThreads),
                        0, s, a, vecA, vecB);
   return hipGetLastError();
 }

@@ -62,6 +62,8 @@ _SIGS = {
     "lsgd_destroy": [_P],
     "lsgd_status_string": [_c.c_int],
     "lsgd_last_error": [_P],
+    "lsgd_profile_enable": [_P, _c.c_int32],
+    "lsgd_profile_report": [_P, _c.c_char_p, _c.c_size_t],
     "lsgd_grouped_gemm": [_c.c_int32, _c.c_int32, _c.c_int32, _c.c_int32,
                           _c.c_int32, _c.c_int32, _c.c_int32, _P, _c.c_int64,
                           _c.c_int64, _P, _c.c_int64, _c.c_int64, _P, _P],
@@ -206,6 +208,20 @@ class Replicas:
     def sample_indices(self, step: int) -> torch.Tensor:
         out = torch.empty((self.K, self.B), dtype=torch.int32, device=self.device)
         _check(_lib.lsgd_sample_indices(self._ctx, int(step), _ptr(out)), self._ctx)
+        return out
+
+    def profile(self, enable: bool = True):
+        """Bracket every launch with HIP events (see lsgd_profile_enable)."""
+        _check(_lib.lsgd_profile_enable(self._ctx, int(bool(enable))), self._ctx)
+
+    def profile_report(self) -> dict:
+        """{tag: (launches, total_ms)} since profiling was enabled; clears."""
+        buf = _c.create_string_buffer(1 << 16)
+        _check(_lib.lsgd_profile_report(self._ctx, buf, len(buf)), self._ctx)
+        out = {}
+        for line in buf.value.decode().splitlines():
+            tag, n, ms = line.split()
+            out[tag] = (int(n), float(ms))
         return out
 
     def sync(self):
