@@ -65,9 +65,10 @@ def kernel_cost(tag: str, w) -> tuple:
                 K * (B * din * e + mn * e + dout * 4 + B * dout * out))
     if name == "dgrad":
         return 2 * K * B * mn, K * (B * dout * e + mn * e + 2 * B * din * e)
-    if name == "wgrad_update":
+    if name == "wgrad_update":   # includes the fused bias gradient + update
         upd = 16 + (2 if e == 2 else 0)
-        return 2 * K * B * mn, K * (B * din * e + B * dout * e + mn * upd)
+        return (2 * K * B * mn + K * B * dout,
+                K * (B * din * e + B * dout * e + (mn + dout) * upd))
     if name == "bias_update":
         return K * B * dout, K * (B * dout * e + dout * 16)
     raise ValueError(tag)

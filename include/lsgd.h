@@ -154,7 +154,8 @@ const char* lsgd_last_error(const lsgd_ctx* ctx);
 /* Per-launch timing (a measurement aid, off by default): while enabled,
  * every kernel the context launches is bracketed by two HIP events on its
  * stream, tagged by launch site (sample, fwd<l>, xent, dgrad<l>,
- * wgrad_update<l>, bias_update<l>, average). */
+ * wgrad_update<l>, average; a split-K GEMM's tag covers both of its
+ * kernels). */
 lsgd_status lsgd_profile_enable(lsgd_ctx* ctx, int32_t enable);
 
 /* Synchronise, then write one line "tag launches total_ms" per tag into the
@@ -174,12 +175,17 @@ lsgd_status lsgd_profile_report(lsgd_ctx* ctx, char* h_buf, size_t len);
  * trans_b = 0: B_g is [Kd][N] (ldb >= N); = 1: B_g is [N][Kd] (ldb >= Kd).
  * dtype LSGD_FP32: A, B are float; LSGD_BF16: A, B are bfloat16 bit patterns
  * (uint16). C is fp32 [G][M][N] with leading dimension N, group stride M*N.
- * Group strides sA, sB are in elements. */
+ * Group strides sA, sB are in elements. splits in {2, 3, 4, 8} splits K into
+ * that many ranges whose fp32 partial sums go to d_part ([splits][G][M][N],
+ * caller owned) and are then added in ascending order; splits == 1 needs no
+ * d_part; other counts return LSGD_E_INVALID.
+ */
 lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
                               int32_t G, int32_t M, int32_t N, int32_t Kd,
                               const void* d_A, int64_t lda, int64_t sA,
                               const void* d_B, int64_t ldb, int64_t sB,
-                              float* d_C, void* stream);
+                              float* d_C, int32_t splits, float* d_part,
+                              void* stream);
 
 /* In-place K-way replica average of d_W fp32 [K][P] (the kernel behind
  * lsgd_average). */

@@ -1,5 +1,6 @@
 // C ABI and host runtime of liblsgd: workspace layout, the launch sequence
 // of one local step, the round driver and error latching.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -26,7 +27,8 @@ struct Layout {
   int64_t offW[LSGD_MAX_LAYERS] = {}, offB[LSGD_MAX_LAYERS] = {};
   size_t esz = 4;  // activation / operand element size
   // byte offsets into the workspace
-  size_t W = 0, U = 0, Wb = 0, Xb = 0, idx = 0, Z = 0;
+  size_t W = 0, U = 0, Wb = 0, Xb = 0, idx = 0, Z = 0, part = 0, rowloss = 0;
+  bool head = false;  // top layer through the fused head kernels
   size_t act[LSGD_MAX_LAYERS] = {}, dZ[LSGD_MAX_LAYERS + 1] = {};
   size_t total = 0;
 };
@@ -80,6 +82,21 @@ Layout make_layout(const lsgd_config* c) {
   for (int i = 1; i < l.L; ++i) l.act[i] = take(K * B * c->widths[i] * l.esz);
   l.Z = take(K * B * c->widths[l.L] * 4);
   for (int i = 1; i <= l.L; ++i) l.dZ[i] = take(K * B * c->widths[i] * l.esz);
+  // split-K partial sums of the forward and input-gradient GEMMs
+  size_t part = 0;
+  for (int i = 1; i <= l.L; ++i) {
+    const int din = c->widths[i - 1], dout = c->widths[i];
+    const int dt = c->gemm_dtype;
+    const size_t f = lsgd::gemm_splits(dt, c->B_loc, dout, din, c->K, lsgd::EPI_BIAS);
+    if (f > 1) part = std::max(part, f * K * B * dout);
+    if (i > 1) {
+      const size_t d = lsgd::gemm_splits(dt, c->B_loc, din, dout, c->K, lsgd::EPI_RELU_MASK);
+      if (d > 1) part = std::max(part, d * K * B * din);
+    }
+  }
+  l.part = take(part * 4);
+  l.head = c->widths[l.L] <= lsgd::kHeadMaxClasses;
+  l.rowloss = take(K * B * 4);
   l.total = t;
   return l;
 }
@@ -129,6 +146,8 @@ struct lsgd_ctx {
   int32_t* idx() const { return (int32_t*)(ws + lay.idx); }
   void* act(int l) const { return ws + lay.act[l]; }
   float* Z() const { return (float*)(ws + lay.Z); }
+  float* part() const { return (float*)(ws + lay.part); }
+  float* rowloss() const { return (float*)(ws + lay.rowloss); }
   void* dZ(int l) const { return ws + lay.dZ[l]; }
   bool bf16() const { return cfg.gemm_dtype == LSGD_BF16; }
 
@@ -180,7 +199,8 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   LSGD_LAUNCH(c, "sample", lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
 
   // forward: Z_l = A_{l-1} W_l + b_l, A_l = relu(Z_l) below the top layer
-  for (int l = 1; l <= L; ++l) {
+  const int Lg = ly.head ? L - 1 : L;  // layers through the generic GEMMs
+  for (int l = 1; l <= Lg; ++l) {
     const int din = w[l - 1], dout = w[l];
     GemmArgs a{};
     a.G = K;
@@ -204,6 +224,8 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     a.sBias = ly.Ps;
     a.ldc = dout;
     a.sC = (long long)B * dout;
+    a.splits = lsgd::gemm_splits(dt, B, dout, din, K, lsgd::EPI_BIAS);
+    a.part = c->part();
     if (l < L) {
       a.C = c->act(l);
       LSGD_LAUNCH(c, "fwd" + std::to_string(l),
@@ -215,14 +237,48 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     }
   }
 
-  LSGD_LAUNCH(c, "xent", lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L],
-                                             c->dZ(L), dt, d_loss, s));
+  lsgd::HeadArgs h{};
+  if (ly.head) {
+    h.K = K;
+    h.B = B;
+    h.D = w[L - 1];
+    h.C = w[L];
+    h.gather = L == 1;
+    h.A = L == 1 ? X0 : c->act(L - 1);
+    h.sA = (long long)B * w[L - 1];
+    h.rowmap = c->idx();
+    h.y = c->y;
+    h.W = dt ? (const void*)(Wb + ly.offW[L - 1]) : (const void*)(W + ly.offW[L - 1]);
+    h.sW = ly.Ps;
+    h.Wm = W + ly.offW[L - 1];
+    h.Um = U + ly.offW[L - 1];
+    h.Wb = dt ? Wb + ly.offW[L - 1] : nullptr;
+    h.bias = W + ly.offB[L - 1];
+    h.bias_w = W + ly.offB[L - 1];
+    h.bias_u = U + ly.offB[L - 1];
+    h.sP = ly.Ps;
+    h.dZ = c->dZ(L);
+    h.dZprev = L > 1 ? c->dZ(L - 1) : nullptr;
+    h.rowloss = c->rowloss();
+    h.loss = d_loss;
+    h.lr = lr;
+    h.mom = cf.momentum;
+    h.wd = cf.weight_decay;
+    h.nesterov = cf.nesterov;
+    // logits, loss, dZ_L and the masked input gradient of the top layer
+    LSGD_LAUNCH(c, "head_fwd", lsgd::launch_head_fwd(dt, h, s));
+    // the top layer's weight gradient reads dZ_L only: update it now
+    LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(dt, h, s));
+  } else {
+    LSGD_LAUNCH(c, "xent", lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L],
+                                               c->dZ(L), dt, d_loss, s));
+  }
 
   // backward, top layer first. The input gradient of layer l reads the
   // pre-update W_l, so it is enqueued before W_l's fused update.
-  for (int l = L; l >= 1; --l) {
+  for (int l = Lg; l >= 1; --l) {
     const int din = w[l - 1], dout = w[l];
-    if (l > 1) {
+    if (l > 1 && !(ly.head && l == L)) {
       GemmArgs a{};
       a.G = K;
       a.M = B;
@@ -238,6 +294,8 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       a.ldc = din;
       a.sC = (long long)B * din;
       a.mask = c->act(l - 1);
+      a.splits = lsgd::gemm_splits(dt, B, din, dout, K, lsgd::EPI_RELU_MASK);
+      a.part = c->part();
       LSGD_LAUNCH(c, "dgrad" + std::to_string(l),
                   lsgd::launch_gemm(dt, 0, 1, lsgd::EPI_RELU_MASK, dt, a, s));
     }
@@ -268,13 +326,12 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     a.mom = cf.momentum;
     a.wd = cf.weight_decay;
     a.nesterov = cf.nesterov;
+    a.bias_w = W + ly.offB[l - 1];
+    a.bias_u = U + ly.offB[l - 1];
+    a.sBiasP = ly.Ps;
+    a.splits = 1;
     LSGD_LAUNCH(c, "wgrad_update" + std::to_string(l),
                 lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
-    LSGD_LAUNCH(c, "bias_update" + std::to_string(l),
-                lsgd::launch_bias_update(c->dZ(l), dt, K, B, dout,
-                                         W + ly.offB[l - 1], U + ly.offB[l - 1],
-                                         ly.Ps, lr, cf.momentum, cf.weight_decay,
-                                         cf.nesterov, s));
   }
   c->step += 1;
   return LSGD_OK;
@@ -498,7 +555,11 @@ lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
                               int32_t G, int32_t M, int32_t N, int32_t Kd,
                               const void* d_A, int64_t lda, int64_t sA,
                               const void* d_B, int64_t ldb, int64_t sB,
-                              float* d_C, void* stream) {
+                              float* d_C, int32_t splits, float* d_part,
+                              void* stream) {
+  if (splits < 1 || splits > 8 || splits == 5 || splits == 6 || splits == 7 ||
+      (splits > 1 && !d_part))
+    return LSGD_E_INVALID;
   if ((dtype != LSGD_FP32 && dtype != LSGD_BF16) || (trans_a | trans_b) & ~1)
     return LSGD_E_INVALID;
   if (G < 1 || M < 1 || N < 1 || Kd < 1 || G > 65535) return LSGD_E_INVALID;
@@ -518,6 +579,8 @@ lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
   a.C = d_C;
   a.ldc = N;
   a.sC = (long long)M * N;
+  a.splits = splits;
+  a.part = d_part;
   hipError_t e = lsgd::launch_gemm(dtype, trans_a, trans_b, lsgd::EPI_STORE, 0, a,
                                    (hipStream_t)stream);
   return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;

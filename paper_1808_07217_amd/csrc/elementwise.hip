@@ -98,30 +98,6 @@ __device__ __forceinline__ void sgd(float& w, float& u, float grad, float lr,
   w = __builtin_fmaf(-lr, d, w);
 }
 
-// Bias gradient db[j] = sum_b dZ[b][j] (rows in ascending order) and its
-// update, one thread per (replica, output unit).
-__global__ void k_bias_update(const void* dZ, int dz_bf16, int B, int D,
-                              float* bias, float* mom_buf, long long sParam,
-                              float lr, float mom, float wd, int nesterov) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  const int k = blockIdx.y;
-  if (j >= D) return;
-  float s = 0.f;
-  const long long base = (long long)k * B * D + j;
-  if (dz_bf16) {
-    const bf16_t* p = (const bf16_t*)dZ + base;
-    for (int b = 0; b < B; ++b) s += bf16_to_f32(p[(long long)b * D]);
-  } else {
-    const float* p = (const float*)dZ + base;
-    for (int b = 0; b < B; ++b) s += p[(long long)b * D];
-  }
-  const long long o = (long long)k * sParam + j;
-  float w = bias[o], u = mom_buf[o];
-  sgd(w, u, s, lr, mom, wd, nesterov);
-  bias[o] = w;
-  mom_buf[o] = u;
-}
-
 __global__ void k_sgd_update4(float4* W, float4* U, const float4* G,
                               long long n4, float lr, float mom, float wd,
                               int nesterov) {
@@ -300,16 +276,6 @@ hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,
                        hipStream_t s) {
   hipLaunchKernelGGL(k_xent, dim3(K), dim3(256), 0, s, Z, y, idx, B, C, dZ,
                      dz_bf16, loss);
-  return hipGetLastError();
-}
-
-hipError_t launch_bias_update(const void* dZ, int dz_bf16, int K, int B, int D,
-                              float* b, float* u, long long sParam, float lr,
-                              float mom, float wd, int nesterov,
-                              hipStream_t s) {
-  dim3 grid((D + 255) / 256, K);
-  hipLaunchKernelGGL(k_bias_update, grid, dim3(256), 0, s, dZ, dz_bf16, B, D, b,
-                     u, sParam, lr, mom, wd, nesterov);
   return hipGetLastError();
 }
 

@@ -4,19 +4,28 @@
 // eq. 2 of the paper: forward Z = A W (+ bias, ReLU), the input gradient
 // dA = dZ W^T (masked by the ReLU derivative), and the weight gradient
 // G = A^T dZ, whose epilogue applies the local momentum-SGD update directly so
-// the gradient never goes to memory.
+// the gradient never goes to memory; the same kernel sums dZ over the batch
+// for the bias gradient and updates the bias.
 //
-// Block tile BM x BN x BK, 256 threads = 4 wavefronts in a 2 x 2 layout, each
-// wave owning (BM/2) x (BN/2) as 32 x 32 MFMA blocks. Operands are staged
-// global -> registers -> LDS with a double-buffered LDS ring: the next slab's
-// global loads are in flight while the current slab feeds the MFMAs.
+// Block tile BM x BN, K slabs of BK, 256 threads = 4 wavefronts in a 2 x 2
+// layout, each wave owning (BM/2) x (BN/2) as 32 x 32 MFMA blocks. Operands go
+// global -> registers -> LDS through a double-buffered LDS ring: the next
+// slab's global loads are in flight while the current slab feeds the MFMAs.
 //
-//  fp32: v_mfma_f32_32x32x2f32, BK = 16. LDS holds k-major tiles As[k][m],
+//  fp32: v_mfma_f32_32x32x2f32, BK = 32. LDS holds k-major tiles As[k][m],
 //        Bs[k][n]; lane l feeds A[m = l%32][k = l/32], B[k = l/32][n = l%32].
 //  bf16: v_mfma_f32_32x32x16_bf16, BK = 32. LDS holds k-contiguous rows
 //        As[m][k], Bs[n][k]; lane l feeds 8 consecutive k starting at
 //        8*(l/32) for row/column l%32.
 //  Both: accumulator register v of lane l is C[8*(v/4) + 4*(l/32) + v%4][l%32].
+//
+// Work distribution: a 1-D grid of G * S * tilesM * tilesN workgroups. The
+// hardware deals consecutive workgroup ids round-robin to the 8 XCDs (each
+// with its own L2), so the id is remapped to give every XCD a contiguous range
+// of tiles: the tiles of one replica then share that XCD's L2.
+// Split-K (S > 1) gives skinny GEMMs enough workgroups: split s covers K range
+// [s*kchunk, (s+1)*kchunk) and writes a raw fp32 partial; a second kernel sums
+// the S partials in ascending s and applies the epilogue.
 #include "kernels.h"
 
 namespace lsgd {
@@ -26,30 +35,55 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kThreads = 256;
+constexpr int kXcds = 8;
 
+struct Tile {
+  int g, s, m0, n0;
+};
+
+__device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int BM, int BN) {
+  const int tn = (a.N + BN - 1) / BN, tm = (a.M + BM - 1) / BM;
+  const int per_split = tn * tm, per_g = per_split * a.splits;
+  const int total = per_g * a.G;
+  const int p = blockIdx.x;
+  int l = (total % kXcds == 0) ? (p % kXcds) * (total / kXcds) + p / kXcds : p;
+  Tile t;
+  t.g = l / per_g;
+  l -= t.g * per_g;
+  t.s = l / per_split;
+  l -= t.s * per_split;
+  t.m0 = (l / tn) * BM;
+  t.n0 = (l % tn) * BN;
+  return t;
+}
+
+__device__ __forceinline__ void sgd_step(float& w, float& u, float grad,
+                                         const GemmArgs& a) {
+  const float g = __builtin_fmaf(a.wd, w, grad);
+  u = __builtin_fmaf(a.mom, u, g);
+  const float d = a.nesterov ? __builtin_fmaf(a.mom, u, g) : u;
+  w = __builtin_fmaf(-a.lr, d, w);
+}
+
+// Epilogue applied to a finished value of C[g][m][n]. OUTBF: activations are
+// bf16 (bf16 workloads) and so are the mask operand and the output.
 template <int EPI, bool OUTBF>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, int g, int m, int n,
-                                         float acc) {
+__device__ __forceinline__ void finish(const GemmArgs& a, int g, int m, int n,
+                                       float v) {
   const long long o = (long long)g * a.sC + (long long)m * a.ldc + n;
   if constexpr (EPI == EPI_SGD) {
-    float w = a.W[o];
-    float u = a.U[o];
-    float gr = __builtin_fmaf(a.wd, w, acc);
-    u = __builtin_fmaf(a.mom, u, gr);
-    float d = a.nesterov ? __builtin_fmaf(a.mom, u, gr) : u;
-    w = __builtin_fmaf(-a.lr, d, w);
+    float w = a.W[o], u = a.U[o];
+    sgd_step(w, u, v, a);
     a.W[o] = w;
     a.U[o] = u;
     if (a.Wb) a.Wb[o] = f32_to_bf16(w);
-    return;
   } else {
-    float v = acc;
     if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_RELU)
       v += a.bias[(long long)g * a.sBias + n];
     if constexpr (EPI == EPI_BIAS_RELU) v = v > 0.f ? v : 0.f;
     if constexpr (EPI == EPI_RELU_MASK) {
-      float mk = OUTBF ? bf16_to_f32(((const bf16_t*)a.mask)[o])
-                       : ((const float*)a.mask)[o];
+      const float mk = OUTBF ? bf16_to_f32(((const bf16_t*)a.mask)[o])
+                             : ((const float*)a.mask)[o];
       v = mk > 0.f ? v : 0.f;
     }
     if constexpr (OUTBF)
@@ -59,32 +93,224 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int g, int m, int n,
   }
 }
 
+template <int EPI, bool OUTBF>
+__device__ __forceinline__ void emit(const GemmArgs& a, const Tile& t, int m,
+                                     int n, float v) {
+  if (a.splits > 1)
+    a.part[(((long long)t.s * a.G + t.g) * a.M + m) * a.N + n] = v;
+  else
+    finish<EPI, OUTBF>(a, t.g, m, n, v);
+}
+
+// Bias of the weight-gradient workgroups with m0 == 0: db[n] = sum_b dZ[b][n]
+// in ascending b, then the same update as the weights.
+__device__ __forceinline__ void bias_update(const GemmArgs& a, const Tile& t,
+                                            int n, float colsum) {
+  const long long o = (long long)t.g * a.sBiasP + n;
+  float w = a.bias_w[o], u = a.bias_u[o];
+  sgd_step(w, u, colsum, a);
+  a.bias_w[o] = w;
+  a.bias_u[o] = u;
+}
+
+// Epilogue over one wave's FM x FN fragment of 32 x 32 blocks, one block at
+// a time. The operands the epilogue reads (W and U of the update, the ReLU
+// mask) are loaded for the whole block before anything is stored, so those
+// loads are in flight together instead of each waiting behind the previous
+// element's stores (the compiler must assume the buffers may alias).
+// Register v of a block sits at row 8*(v/4) + (v%4) below the lane's first
+// row and in the lane's column: a 32-bit offset from one base per block.
+template <int EPI, bool OUTBF, int FM, int FN>
+__device__ __forceinline__ void epilogue_fragment(const GemmArgs& a, const Tile& t,
+                                                  floatx16 (&acc)[FM][FN],
+                                                  int mb, int nb, int lk, int lr) {
+  const int M = a.M, N = a.N;
+  if (EPI != EPI_SGD && a.splits > 1) {  // raw partial sums, [s][g][M][N]
+    float* P = a.part + ((long long)t.s * a.G + t.g) * a.M * a.N;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int m1 = mb + i * 32 + lk * 4, n = nb + j * 32 + lr;
+        float* base = P + (long long)m1 * N + n;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int dr = (v >> 2) * 8 + (v & 3);
+          if (m1 + dr < M && n < N) base[dr * N] = acc[i][j][v];
+        }
+      }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int m1 = mb + i * 32 + lk * 4, n = nb + j * 32 + lr;
+      const long long o1 = (long long)t.g * a.sC + (long long)m1 * a.ldc + n;
+      const int ldc = (int)a.ldc;
+      bool ok[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) ok[v] = m1 + (v >> 2) * 8 + (v & 3) < M && n < N;
+      if constexpr (EPI == EPI_SGD) {
+        float* Wp = a.W + o1;
+        float* Up = a.U + o1;
+        float wv[16], uv[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int dr = ((v >> 2) * 8 + (v & 3)) * ldc;
+          wv[v] = ok[v] ? Wp[dr] : 0.f;
+          uv[v] = ok[v] ? Up[dr] : 0.f;
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          if (!ok[v]) continue;
+          const int dr = ((v >> 2) * 8 + (v & 3)) * ldc;
+          sgd_step(wv[v], uv[v], acc[i][j][v], a);
+          Wp[dr] = wv[v];
+          Up[dr] = uv[v];
+          if (a.Wb) a.Wb[o1 + dr] = f32_to_bf16(wv[v]);
+        }
+      } else if constexpr (EPI == EPI_RELU_MASK) {
+        float mk[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int dr = ((v >> 2) * 8 + (v & 3)) * ldc;
+          mk[v] = 0.f;
+          if (ok[v])
+            mk[v] = OUTBF ? bf16_to_f32(((const bf16_t*)a.mask)[o1 + dr])
+                          : ((const float*)a.mask)[o1 + dr];
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          if (!ok[v]) continue;
+          const int dr = ((v >> 2) * 8 + (v & 3)) * ldc;
+          const float r = mk[v] > 0.f ? acc[i][j][v] : 0.f;
+          if constexpr (OUTBF)
+            ((bf16_t*)a.C)[o1 + dr] = f32_to_bf16(r);
+          else
+            ((float*)a.C)[o1 + dr] = r;
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (ok[v]) finish<EPI, OUTBF>(a, t.g, m1 + (v >> 2) * 8 + (v & 3), n, acc[i][j][v]);
+      }
+    }
+}
+
+// Vectorised update epilogue (EPI_SGD, ldc % 4 == 0): the accumulator tile
+// goes through LDS, half of the rows at a time, so that every thread then
+// updates whole float4 runs of W and U along n -- fully coalesced rows. The
+// W/U reads of half 0 are issued at kernel entry (they overlap the MFMA
+// loop) and those of half 1 before half 0's results go through LDS.
+template <int BM, int BN>
+struct SgdVec {
+  static constexpr int CP = BN + 4;                      // LDS pitch
+  static constexpr int PER = (BM / 2) * BN / 4 / kThreads;  // float4 per thread
+  static_assert(PER >= 1 && (BM / 2) * BN / 4 % kThreads == 0, "tile too small");
+
+  __device__ static void locate(const GemmArgs& a, const Tile& t, int half, int p,
+                                int& r, int& c, long long& off, bool& ok) {
+    const int idx = (int)threadIdx.x + p * kThreads;
+    r = idx / (BN / 4);
+    c = (idx % (BN / 4)) * 4;
+    const int m = t.m0 + half * (BM / 2) + r, n = t.n0 + c;
+    ok = m < a.M && n < a.N;
+    off = (long long)t.g * a.sC + (long long)m * a.ldc + n;
+  }
+  __device__ static void fetch(const GemmArgs& a, const Tile& t, int half,
+                               float4 (&wv)[PER], float4 (&uv)[PER]) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      int r, c;
+      long long off;
+      bool ok;
+      locate(a, t, half, p, r, c, off, ok);
+      if (ok) {
+        wv[p] = *(const float4*)(a.W + off);
+        uv[p] = *(const float4*)(a.U + off);
+      }
+    }
+  }
+  template <int FM, int FN>
+  __device__ static void run(const GemmArgs& a, const Tile& t,
+                             floatx16 (&acc)[FM][FN], float* smem, int wave,
+                             int lk, int lr, float4 (&wv)[PER], float4 (&uv)[PER]) {
+    const int wn0 = (wave & 1) * (BN / 2);
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      if (half == 1) fetch(a, t, 1, wv, uv);
+      __syncthreads();
+      if ((wave >> 1) == half) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const int r = i * 32 + (v >> 2) * 8 + lk * 4 + (v & 3);
+              smem[r * CP + wn0 + j * 32 + lr] = acc[i][j][v];
+            }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int p = 0; p < PER; ++p) {
+        int r, c;
+        long long off;
+        bool ok;
+        locate(a, t, half, p, r, c, off, ok);
+        if (!ok) continue;
+        const float4 gr = *(const float4*)&smem[r * CP + c];
+        float4 w = wv[p], u = uv[p];
+        sgd_step(w.x, u.x, gr.x, a);
+        sgd_step(w.y, u.y, gr.y, a);
+        sgd_step(w.z, u.z, gr.z, a);
+        sgd_step(w.w, u.w, gr.w, a);
+        *(float4*)(a.W + off) = w;
+        *(float4*)(a.U + off) = u;
+        if (a.Wb) {
+          const uint32_t lo = f32_to_bf16(w.x) | ((uint32_t)f32_to_bf16(w.y) << 16);
+          const uint32_t hi = f32_to_bf16(w.z) | ((uint32_t)f32_to_bf16(w.w) << 16);
+          *(uint2*)(a.Wb + off) = make_uint2(lo, hi);
+        }
+      }
+    }
+  }
+};
+
 // ------------------------------------------------------------------ fp32
-template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN>
+template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN, int BK>
 __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
-                                                     int vecB) {
-  constexpr int BK = 16, PAD = 4;
+                                                     int vecB, int vecC) {
+  // pitch: transposing stores (k-contiguous source) use pitch = 2 mod 8 to
+  // spread banks; direct float4 stores need a 16-byte aligned pitch
+  constexpr int PA = AT ? BM + 4 : BM + 2;
+  constexpr int PB = BT ? BN + 2 : BN + 4;
   constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  constexpr int KV = BK / 4;                  // float4 per k-contiguous row
   constexpr int NA = BM * BK / 4 / kThreads;  // float4 loads per thread
   constexpr int NB = BN * BK / 4 / kThreads;
   static_assert(NA >= 1 && NB >= 1, "tile too small for 256 threads");
-  __shared__ float As[2][BK][BM + PAD];
-  __shared__ float Bs[2][BK][BN + PAD];
+  constexpr int OPER = 2 * BK * (PA + PB);
+  constexpr int EPIF = EPI == EPI_SGD ? (BM / 2) * (BN + 4) : 0;
+  __shared__ __attribute__((aligned(16))) float smem[OPER > EPIF ? OPER : EPIF];
+  auto As = reinterpret_cast<float (*)[BK][PA]>(smem);
+  auto Bs = reinterpret_cast<float (*)[BK][PB]>(smem + 2 * BK * PA);
 
-  const int g = blockIdx.z;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const Tile t = decode_tile(a, BM, BN);
+  const int g = t.g, m0 = t.m0, n0 = t.n0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
   const float* A = (const float*)a.A + (long long)g * a.sA;
   const float* B = (const float*)a.B + (long long)g * a.sB;
   // GATHER: rows of A come from a row map (the sampled mini-batch indices)
   const int32_t* rmap = GATHER ? a.rowmap + (long long)g * a.sRow : nullptr;
-  const int M = a.M, N = a.N, Kd = a.Kd;
+  const int M = a.M, N = a.N;
+  const int kbeg = t.s * a.kchunk;
+  const int kend = min(a.Kd, kbeg + a.kchunk);
 
   float4 ra[NA], rb[NB];
 
-  // Load 4 consecutive elements of storage row `row` starting at column
-  // `col`; `avail` elements are valid, the rest read as zero.
   auto load4 = [](const float* p, int avail, int vec) -> float4 {
     if (vec && avail >= 4) return *(const float4*)p;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -99,17 +325,16 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int q = tid + i * kThreads;
-      if constexpr (!AT) {  // storage [M][Kd]: rows m, 4 float4 per row
-        const int r = q >> 2, c = k0 + (q & 3) * 4, row = m0 + r;
-        ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if constexpr (!AT) {  // storage [M][Kd]: rows m, KV float4 per row
+        const int r = q / KV, c = k0 + (q % KV) * 4, row = m0 + r;
         if (row < M) {
           const long long sr = GATHER ? rmap[row] : row;
-          ra[i] = load4(A + sr * a.lda + c, Kd - c, vecA);
+          ra[i] = load4(A + sr * a.lda + c, kend - c, vecA);
         }
       } else {  // storage [Kd][M]: rows k, BM/4 float4 per row
         const int r = q / (BM / 4), c = m0 + (q % (BM / 4)) * 4, kr = k0 + r;
-        ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (kr < Kd) {
+        if (kr < kend) {
           const long long sr = GATHER ? rmap[kr] : kr;
           ra[i] = load4(A + sr * a.lda + c, M - c, vecA);
         }
@@ -118,14 +343,13 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int q = tid + i * kThreads;
+      rb[i] = make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (BT) {  // storage [N][Kd]
-        const int r = q >> 2, c = k0 + (q & 3) * 4, row = n0 + r;
-        rb[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row < N) rb[i] = load4(B + (long long)row * a.ldb + c, Kd - c, vecB);
+        const int r = q / KV, c = k0 + (q % KV) * 4, row = n0 + r;
+        if (row < N) rb[i] = load4(B + (long long)row * a.ldb + c, kend - c, vecB);
       } else {  // storage [Kd][N]
         const int r = q / (BN / 4), c = n0 + (q % (BN / 4)) * 4, kr = k0 + r;
-        rb[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (kr < Kd) rb[i] = load4(B + (long long)kr * a.ldb + c, N - c, vecB);
+        if (kr < kend) rb[i] = load4(B + (long long)kr * a.ldb + c, N - c, vecB);
       }
     }
   };
@@ -135,7 +359,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
     for (int i = 0; i < NA; ++i) {
       const int q = tid + i * kThreads;
       if constexpr (!AT) {
-        const int r = q >> 2, kq = (q & 3) * 4;
+        const int r = q / KV, kq = (q % KV) * 4;
         As[buf][kq + 0][r] = ra[i].x;
         As[buf][kq + 1][r] = ra[i].y;
         As[buf][kq + 2][r] = ra[i].z;
@@ -149,7 +373,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
     for (int i = 0; i < NB; ++i) {
       const int q = tid + i * kThreads;
       if constexpr (BT) {
-        const int r = q >> 2, kq = (q & 3) * 4;
+        const int r = q / KV, kq = (q % KV) * 4;
         Bs[buf][kq + 0][r] = rb[i].x;
         Bs[buf][kq + 1][r] = rb[i].y;
         Bs[buf][kq + 2][r] = rb[i].z;
@@ -169,14 +393,24 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int nk = (Kd + BK - 1) / BK;
-  gload(0);
-  lstore(0);
+  const bool do_bias = EPI == EPI_SGD && a.bias_w && m0 == 0;
+  float colsum = 0.f;
+  // EPI_SGD: W/U of the first half tile are read while the MFMAs run
+  using SV = SgdVec<BM, BN>;
+  float4 wpre[EPI == EPI_SGD ? SV::PER : 1], upre[EPI == EPI_SGD ? SV::PER : 1];
+  if constexpr (EPI == EPI_SGD) {
+    if (vecC) SV::fetch(a, t, 0, wpre, upre);
+  }
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  if (nk > 0) {
+    gload(kbeg);
+    lstore(0);
+  }
   __syncthreads();
   const int lk = lane >> 5, lr = lane & 31;
-  for (int t = 0; t < nk; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < nk) gload((t + 1) * BK);
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 2) {
       float av[FM], bv[FN];
@@ -191,26 +425,29 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j],
                                                            acc[i][j], 0, 0, 0);
     }
-    if (t + 1 < nk) lstore(buf ^ 1);
+    if (do_bias && tid < BN) {
+#pragma unroll 8
+      for (int k = 0; k < BK; ++k) colsum += Bs[buf][k][tid];
+    }
+    if (it + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
   }
 
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm0 + i * 32 + (v >> 2) * 8 + lk * 4 + (v & 3);
-        const int n = n0 + wn0 + j * 32 + lr;
-        if (m < M && n < N) epilogue<EPI, false>(a, g, m, n, acc[i][j][v]);
-      }
+  if constexpr (EPI == EPI_SGD) {
+    if (vecC)
+      SV::template run<FM, FN>(a, t, acc, smem, wave, lk, lr, wpre, upre);
+    else
+      epilogue_fragment<EPI, false, FM, FN>(a, t, acc, m0 + wm0, n0 + wn0, lk, lr);
+  } else {
+    epilogue_fragment<EPI, false, FM, FN>(a, t, acc, m0 + wm0, n0 + wn0, lk, lr);
+  }
+  if (do_bias && tid < BN && n0 + tid < N) bias_update(a, t, n0 + tid, colsum);
 }
 
 // ------------------------------------------------------------------ bf16
 template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN>
 __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
-                                                      int vecB) {
+                                                      int vecB, int vecC) {
   constexpr int BK = 32, KP = BK + 8;  // row pitch 80 B keeps 16-B alignment
   constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
   constexpr int NA = BM * BK / 8 / kThreads;  // 8-element vectors per thread
@@ -219,25 +456,26 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BM][KP];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN][KP];
 
-  const int g = blockIdx.z;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const Tile t = decode_tile(a, BM, BN);
+  const int g = t.g, m0 = t.m0, n0 = t.n0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
   const bf16_t* A = (const bf16_t*)a.A + (long long)g * a.sA;
   const bf16_t* B = (const bf16_t*)a.B + (long long)g * a.sB;
-  // GATHER: rows of A come from a row map (the sampled mini-batch indices)
   const int32_t* rmap = GATHER ? a.rowmap + (long long)g * a.sRow : nullptr;
-  const int M = a.M, N = a.N, Kd = a.Kd;
+  const int M = a.M, N = a.N;
+  const int kbeg = t.s * a.kchunk;
+  const int kend = min(a.Kd, kbeg + a.kchunk);
 
   uint4 ra[NA], rb[NB];
 
   auto load8 = [](const bf16_t* p, int avail, int vec) -> uint4 {
     if (vec && avail >= 8) return *(const uint4*)p;
-    uint16_t t[8];
+    uint16_t h[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) t[e] = e < avail ? p[e] : (uint16_t)0;
-    return make_uint4(t[0] | ((uint32_t)t[1] << 16), t[2] | ((uint32_t)t[3] << 16),
-                      t[4] | ((uint32_t)t[5] << 16), t[6] | ((uint32_t)t[7] << 16));
+    for (int e = 0; e < 8; ++e) h[e] = e < avail ? p[e] : (uint16_t)0;
+    return make_uint4(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
+                      h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16));
   };
 
   auto gload = [&](int k0) {
@@ -249,11 +487,11 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
         const int r = q >> 2, c = k0 + (q & 3) * 8, row = m0 + r;
         if (row < M) {
           const long long sr = GATHER ? rmap[row] : row;
-          ra[i] = load8(A + sr * a.lda + c, Kd - c, vecA);
+          ra[i] = load8(A + sr * a.lda + c, kend - c, vecA);
         }
       } else {  // [Kd][M]: BM/8 vectors per row
         const int r = q / (BM / 8), c = m0 + (q % (BM / 8)) * 8, kr = k0 + r;
-        if (kr < Kd) {
+        if (kr < kend) {
           const long long sr = GATHER ? rmap[kr] : kr;
           ra[i] = load8(A + sr * a.lda + c, M - c, vecA);
         }
@@ -265,10 +503,10 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
       rb[i] = make_uint4(0, 0, 0, 0);
       if constexpr (BT) {  // [N][Kd]
         const int r = q >> 2, c = k0 + (q & 3) * 8, row = n0 + r;
-        if (row < N) rb[i] = load8(B + (long long)row * a.ldb + c, Kd - c, vecB);
+        if (row < N) rb[i] = load8(B + (long long)row * a.ldb + c, kend - c, vecB);
       } else {  // [Kd][N]
         const int r = q / (BN / 8), c = n0 + (q % (BN / 8)) * 8, kr = k0 + r;
-        if (kr < Kd) rb[i] = load8(B + (long long)kr * a.ldb + c, N - c, vecB);
+        if (kr < kend) rb[i] = load8(B + (long long)kr * a.ldb + c, N - c, vecB);
       }
     }
   };
@@ -315,14 +553,18 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int nk = (Kd + BK - 1) / BK;
-  gload(0);
-  lstore(0);
+  const bool do_bias = EPI == EPI_SGD && a.bias_w && m0 == 0;
+  float colsum = 0.f;
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  if (nk > 0) {
+    gload(kbeg);
+    lstore(0);
+  }
   __syncthreads();
   const int lk = lane >> 5, lr = lane & 31;
-  for (int t = 0; t < nk; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < nk) gload((t + 1) * BK);
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       bf16x8 av[FM], bv[FN];
@@ -339,55 +581,115 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j],
                                                               acc[i][j], 0, 0, 0);
     }
-    if (t + 1 < nk) lstore(buf ^ 1);
+    if (do_bias && tid < BN) {
+#pragma unroll 8
+      for (int k = 0; k < BK; ++k) colsum += bf16_to_f32(Bs[buf][tid][k]);
+    }
+    if (it + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
   }
 
+  constexpr bool OUTBF = EPI == EPI_BIAS_RELU || EPI == EPI_RELU_MASK;
+  epilogue_fragment<EPI, OUTBF, FM, FN>(a, t, acc, m0 + wm0, n0 + wn0, lk, lr);
+  if (do_bias && tid < BN && n0 + tid < N) bias_update(a, t, n0 + tid, colsum);
+}
+
+// ------------------------------------------------------------------ split-K
+// C[g][m][n] = epilogue(sum_{s=0}^{S-1} part[s][g][m][n]), s ascending. S is
+// a template argument so all S loads are issued before the sum.
+template <int EPI, bool OUTBF, int S>
+__global__ void k_splitk_reduce(GemmArgs a) {
+  const long long MN = (long long)a.M * a.N, total = MN * a.G;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    float p[S];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+    for (int s = 0; s < S; ++s) p[s] = a.part[i + s * total];
+    float v = p[0];
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm0 + i * 32 + (v >> 2) * 8 + lk * 4 + (v & 3);
-        const int n = n0 + wn0 + j * 32 + lr;
-        if (m < M && n < N) {
-          if constexpr (EPI == EPI_BIAS_RELU || EPI == EPI_RELU_MASK)
-            epilogue<EPI, true>(a, g, m, n, acc[i][j][v]);
-          else
-            epilogue<EPI, false>(a, g, m, n, acc[i][j][v]);
-        }
-      }
+    for (int s = 1; s < S; ++s) v += p[s];
+    const int g = (int)(i / MN);
+    const long long r = i - g * MN;
+    finish<EPI, OUTBF>(a, g, (int)(r / a.N), (int)(r % a.N), v);
+  }
+}
+
+template <int EPI, bool OUTBF>
+hipError_t launch_reduce(const GemmArgs& a, hipStream_t s) {
+  const long long n = (long long)a.G * a.M * a.N;
+  const int blocks = (int)((n + 255) / 256 < 8192 ? (n + 255) / 256 : 8192);
+  switch (a.splits) {
+    case 2: hipLaunchKernelGGL((k_splitk_reduce<EPI, OUTBF, 2>), dim3(blocks), dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_splitk_reduce<EPI, OUTBF, 4>), dim3(blocks), dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_splitk_reduce<EPI, OUTBF, 8>), dim3(blocks), dim3(256), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_splitk_reduce<EPI, OUTBF, 3>), dim3(blocks), dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-template <bool AT, bool BT, int EPI, bool GATHER = false>
-hipError_t dispatch(int dtype, const GemmArgs& a, hipStream_t s) {
-  if (GATHER != (a.rowmap != nullptr)) {
-    if (a.rowmap) return dispatch<AT, BT, EPI, true>(dtype, a, s);
-    return hipErrorInvalidValue;
-  }
-  constexpr int BM = 64, BN = 64;
-  dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, a.G);
+// Tile shape for a problem: 128 x 128 (four MFMA chains per wave) when both
+// output dimensions allow it on the fp32 path, else 64 x 64.
+bool big_tile(int dtype, int M, int N) { return dtype == 0 && M >= 128 && N >= 128; }
+
+template <bool AT, bool BT, int EPI, bool GATHER>
+hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
+  const bool big = big_tile(dtype, a.M, a.N);
+  const int BM = big ? 128 : 64, BN = BM;
+  const long long tiles = (long long)((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM) * a.G;
+  const long long total = tiles * a.splits;
+  if (total > 0x7fffffffLL) return hipErrorInvalidValue;
   const int esz = dtype == 1 ? 8 : 4;  // elements per vector load
   const int vecA = a.lda % esz == 0 && a.sA % esz == 0 && aligned16(a.A);
   const int vecB = a.ldb % esz == 0 && a.sB % esz == 0 && aligned16(a.B);
+  const int vecC = EPI == EPI_SGD && a.ldc % 4 == 0 && a.sC % 4 == 0 &&
+                   aligned16(a.W) && aligned16(a.U) &&
+                   (a.Wb == nullptr || ((uintptr_t)a.Wb & 7u) == 0);
   if (dtype == 1)
-    hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, BM, BN>), grid, dim3(kThreads),
-                       0, s, a, vecA, vecB);
+    hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, 64, 64>), dim3(total),
+                       dim3(kThreads), 0, s, a, vecA, vecB, vecC);
+  else if (big)
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, 16>), dim3(total),
+                       dim3(kThreads), 0, s, a, vecA, vecB, vecC);
   else
-    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, BM, BN>), grid, dim3(kThreads),
-                       0, s, a, vecA, vecB);
-  return hipGetLastError();
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 64, 64, 32>), dim3(total),
+                       dim3(kThreads), 0, s, a, vecA, vecB, vecC);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  constexpr bool OUTBF_ACT = EPI == EPI_BIAS_RELU || EPI == EPI_RELU_MASK;
+  if (dtype == 1 && OUTBF_ACT) return launch_reduce<EPI, true>(a, s);
+  return launch_reduce<EPI, false>(a, s);
+}
+
+template <bool AT, bool BT, int EPI>
+hipError_t dispatch(int dtype, const GemmArgs& a, hipStream_t s) {
+  if (a.rowmap) return run<AT, BT, EPI, true>(dtype, a, s);
+  return run<AT, BT, EPI, false>(dtype, a, s);
 }
 
 }  // namespace
 
+int gemm_splits(int dtype, int M, int N, int Kd, int G, int epi) {
+  if (epi == EPI_SGD) return 1;
+  const int T = big_tile(dtype, M, N) ? 128 : 64;
+  const long long tiles = (long long)((N + T - 1) / T) * ((M + T - 1) / T) * G;
+  int s = 1;
+  // up to 8 splits while the grid stays within ~4 workgroups per CU and every
+  // split keeps at least 128 of K
+  while (s < 8 && tiles * s * 2 <= 1024 && Kd / (s * 2) >= 128) s *= 2;
+  return s;
+}
+
 hipError_t launch_gemm(int dtype, int trans_a, int trans_b, int epi,
-                       int out_bf16, const GemmArgs& a, hipStream_t s) {
-  if (a.G <= 0 || a.M <= 0 || a.N <= 0 || a.Kd <= 0) return hipSuccess;
-  if (a.G > 65535) return hipErrorInvalidValue;
+                       int out_bf16, const GemmArgs& args, hipStream_t s) {
+  if (args.G <= 0 || args.M <= 0 || args.N <= 0 || args.Kd <= 0) return hipSuccess;
+  GemmArgs a = args;
+  if (a.splits < 1) a.splits = 1;
+  if (a.splits > 1 && (a.part == nullptr || epi == EPI_SGD)) return hipErrorInvalidValue;
+  a.kchunk = (a.Kd + a.splits - 1) / a.splits;
+  a.kchunk = (a.kchunk + 31) / 32 * 32;
   // activations are bf16 exactly when the operands are
   if ((epi == EPI_BIAS_RELU || epi == EPI_RELU_MASK) && out_bf16 != (dtype == 1))
     return hipErrorInvalidValue;

@@ -1,0 +1,339 @@
+// The output layer of the network with few classes (C <= 32), fused around
+// the loss: the mean mini-batch cross-entropy whose gradient is the bracket of
+// eq. 2 in the paper.
+//
+// k_head_fwd: one wavefront per sample row b of replica k. Lanes stride over
+//   the D inputs to form the C logits, reduced across the wave by a fixed xor
+//   butterfly; then softmax cross-entropy (stable form), dZ = (p - onehot)/B,
+//   and, below the top layer, the input gradient dA[d] = sum_c dZ[c] W[d][c]
+//   masked by the ReLU derivative (A > 0).
+// k_head_wgrad: one workgroup per (replica, 64 inputs d): dW[d][c] =
+//   sum_b A[b][d] dZ[b][c] in ascending b, fused with the momentum-SGD update;
+//   workgroup 0 of each replica also updates the bias (sum_b dZ[b][c]) and
+//   reduces the per-row losses in ascending b.
+#include "kernels.h"
+
+namespace lsgd {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float ld(const T* p, long long i);
+template <>
+__device__ __forceinline__ float ld<float>(const float* p, long long i) {
+  return p[i];
+}
+template <>
+__device__ __forceinline__ float ld<bf16_t>(const bf16_t* p, long long i) {
+  return bf16_to_f32(p[i]);
+}
+__device__ __forceinline__ void st(float* p, long long i, float v) { p[i] = v; }
+__device__ __forceinline__ void st(bf16_t* p, long long i, float v) {
+  p[i] = f32_to_bf16(v);
+}
+__device__ __forceinline__ float round_like(float v, const float*) { return v; }
+__device__ __forceinline__ float round_like(float v, const bf16_t*) {
+  return bf16_to_f32(f32_to_bf16(v));
+}
+
+// dst[i] = src[base + i] for i < n by the 256 threads of the workgroup, eight
+// loads in flight per thread before the LDS stores.
+template <typename T>
+__device__ __forceinline__ void stage(float* dst, const T* src, long long base,
+                                      int n) {
+  for (int i0 = 0; i0 < n; i0 += 8 * 256) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 256 + (int)threadIdx.x;
+      v[u] = i < n ? ld(src, base + i) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * 256 + (int)threadIdx.x;
+      if (i < n) dst[i] = v[u];
+    }
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ void sgd_step(float& w, float& u, float grad,
+                                         const HeadArgs& h) {
+  const float g = __builtin_fmaf(h.wd, w, grad);
+  u = __builtin_fmaf(h.mom, u, g);
+  const float d = h.nesterov ? __builtin_fmaf(h.mom, u, g) : u;
+  w = __builtin_fmaf(-h.lr, d, w);
+}
+
+// Rows of W_L staged in LDS per pass: W chunk [DCH][C] plus nothing else.
+template <int CMAX>
+constexpr int head_chunk() { return CMAX <= 16 ? 1024 : 512; }
+
+template <typename T, int CMAX, bool GATHER>
+__global__ __launch_bounds__(256) void k_head_fwd(HeadArgs h) {
+  constexpr int RPW = 2;             // sample rows per wavefront
+  constexpr int DCH = head_chunk<CMAX>();
+  __shared__ float Ws[DCH * CMAX];
+  const int k = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int D = h.D, C = h.C;
+  const T* Wg = (const T*)h.W + (long long)k * h.sW;
+  const T* arow[RPW];
+  long long rr[RPW];
+  bool live[RPW];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int row = (blockIdx.x * 4 + wave) * RPW + q;
+    live[q] = row < h.B;
+    rr[q] = (long long)k * h.B + (live[q] ? row : 0);
+    arow[q] = GATHER ? (const T*)h.A + (long long)h.rowmap[rr[q]] * D
+                     : (const T*)h.A + (long long)k * h.sA +
+                           (long long)(live[q] ? row : 0) * D;
+  }
+
+  float z[RPW][CMAX];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q)
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) z[q][c] = 0.f;
+  for (int d0 = 0; d0 < D; d0 += DCH) {
+    const int nd = min(DCH, D - d0);
+    __syncthreads();
+    stage(Ws, Wg, (long long)d0 * C, nd * C);
+    __syncthreads();
+    // four strides of 64 per pass: all loads first, then the FMAs
+    for (int db = 0; db < nd; db += 256) {
+      float av[4][RPW];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int d = db + u * 64 + lane;
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) av[u][q] = d < nd ? ld(arow[q], d0 + d) : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int d = db + u * 64 + lane;
+        if (d >= nd) continue;
+#pragma unroll
+        for (int c = 0; c < CMAX; ++c) {
+          if (c >= C) continue;
+          const float wdc = Ws[d * C + c];
+#pragma unroll
+          for (int q = 0; q < RPW; ++q) z[q][c] = __builtin_fmaf(av[u][q], wdc, z[q][c]);
+        }
+      }
+    }
+  }
+  const float* bias = h.bias + (long long)k * h.sP;
+  const float invB = 1.0f / (float)h.B;
+  float dz[RPW][CMAX];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c)
+      if (c < C) z[q][c] = wave_sum(z[q][c]) + bias[c];
+    // softmax cross-entropy, identical in every lane
+    const int lab = h.y[h.rowmap[rr[q]]];
+    float m = z[q][0];
+#pragma unroll
+    for (int c = 1; c < CMAX; ++c)
+      if (c < C) m = fmaxf(m, z[q][c]);
+    float s = 0.f, rest = 0.f, zy = 0.f;
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c)
+      if (c < C) {
+        const float e = __expf(z[q][c] - m);
+        s += e;
+        if (c != lab) rest += e;
+        else zy = z[q][c];
+      }
+    const float loss = zy >= m ? log1pf(rest) : (m - zy) + logf(s);
+    const float inv_s = 1.0f / s;
+    float mine = 0.f;
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) {
+      dz[q][c] = 0.f;
+      if (c < C) {
+        const float p = __expf(z[q][c] - m) * inv_s;
+        dz[q][c] = round_like((p - (c == lab ? 1.f : 0.f)) * invB, (const T*)nullptr);
+        if (c == lane) mine = dz[q][c];
+      }
+    }
+    if (live[q]) {
+      if (lane < C) st((T*)h.dZ, rr[q] * C + lane, mine);
+      if (lane == 0) h.rowloss[rr[q]] = loss;
+    }
+  }
+
+  if (!h.dZprev) return;  // uniform over the workgroup
+  // input gradient of the top layer, ReLU-masked: needs W_L again
+  for (int d0 = 0; d0 < D; d0 += DCH) {
+    const int nd = min(DCH, D - d0);
+    if (D > DCH) {  // the chunk in LDS is not the whole of W_L
+      __syncthreads();
+      stage(Ws, Wg, (long long)d0 * C, nd * C);
+      __syncthreads();
+    }
+    for (int db = 0; db < nd; db += 256) {
+      float mk[4][RPW];  // the ReLU mask operand, loaded up front
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int d = db + u * 64 + lane;
+#pragma unroll
+        for (int q = 0; q < RPW; ++q)
+          mk[u][q] = d < nd && live[q] ? ld(arow[q], d0 + d) : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int d = db + u * 64 + lane;
+        if (d >= nd) continue;
+        float v[RPW];
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) v[q] = 0.f;
+#pragma unroll
+        for (int c = 0; c < CMAX; ++c) {
+          if (c >= C) continue;
+          const float wdc = Ws[d * C + c];
+#pragma unroll
+          for (int q = 0; q < RPW; ++q) v[q] = __builtin_fmaf(dz[q][c], wdc, v[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < RPW; ++q)
+          if (live[q])
+            st((T*)h.dZprev + rr[q] * D, d0 + d, mk[u][q] > 0.f ? v[q] : 0.f);
+      }
+    }
+  }
+}
+
+template <typename T, int CMAX, bool GATHER>
+__global__ __launch_bounds__(256) void k_head_wgrad(HeadArgs h) {
+  constexpr int RB = 64;  // batch rows staged in LDS per pass
+  constexpr int CJ = (CMAX + 3) / 4;
+  __shared__ float dzs[RB * CMAX];
+  __shared__ float As[RB][65];
+  __shared__ float red[256];
+  const int k = blockIdx.y;
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const int D = h.D, C = h.C, B = h.B;
+  const int dbase = blockIdx.x * 64, d = dbase + lane;
+  const T* dZ = (const T*)h.dZ + (long long)k * B * C;
+  const bool first = blockIdx.x == 0;
+
+  float acc[CJ];
+#pragma unroll
+  for (int j = 0; j < CJ; ++j) acc[j] = 0.f;
+  float bsum = 0.f;  // bias gradient of class threadIdx.x (first workgroup)
+  for (int b0 = 0; b0 < B; b0 += RB) {
+    const int nb = min(RB, B - b0);
+    __syncthreads();
+    stage(dzs, dZ, (long long)b0 * C, nb * C);
+    // A[b0 + r][dbase .. dbase + 63]: each wave loads whole 64-wide rows,
+    // eight rows per batch with every load issued before the LDS stores
+    for (int r0 = grp; r0 < nb; r0 += 32) {
+      long long base[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = r0 + 4 * u;
+        const long long rr = (long long)k * B + b0 + (r < nb ? r : 0);
+        base[u] = GATHER ? (long long)h.rowmap[rr] * D
+                         : (long long)k * h.sA + (long long)(b0 + (r < nb ? r : 0)) * D;
+      }
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[u] = (r0 + 4 * u < nb && d < D) ? ld((const T*)h.A, base[u] + d) : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (r0 + 4 * u < nb) As[r0 + 4 * u][lane] = v[u];
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int b = 0; b < nb; ++b) {
+      const float av = As[b][lane];
+#pragma unroll
+      for (int j = 0; j < CJ; ++j) {
+        const int c = grp + 4 * j;
+        if (c < C) acc[j] = __builtin_fmaf(av, dzs[b * C + c], acc[j]);
+      }
+    }
+    if (first && (int)threadIdx.x < C)
+      for (int b = 0; b < nb; ++b) bsum += dzs[b * C + threadIdx.x];
+  }
+  if (d < D) {
+#pragma unroll
+    for (int j = 0; j < CJ; ++j) {
+      const int c = grp + 4 * j;
+      if (c >= C) continue;
+      const long long o = (long long)k * h.sP + (long long)d * C + c;
+      float w = h.Wm[o], u = h.Um[o];
+      sgd_step(w, u, acc[j], h);
+      h.Wm[o] = w;
+      h.Um[o] = u;
+      if (h.Wb) h.Wb[o] = f32_to_bf16(w);
+    }
+  }
+  if (!first) return;  // uniform over the workgroup
+  if ((int)threadIdx.x < C) {
+    const long long o = (long long)k * h.sP + threadIdx.x;
+    float w = h.bias_w[o], u = h.bias_u[o];
+    sgd_step(w, u, bsum, h);
+    h.bias_w[o] = w;
+    h.bias_u[o] = u;
+  }
+  // mean loss of replica k: per-thread strided partial sums, then a fixed tree
+  const float* rl = h.rowloss + (long long)k * B;
+  float part = 0.f;
+  for (int b = threadIdx.x; b < B; b += 256) part += rl[b];
+  red[threadIdx.x] = part;
+  __syncthreads();
+  for (int w2 = 128; w2 > 0; w2 >>= 1) {
+    if ((int)threadIdx.x < w2) red[threadIdx.x] += red[threadIdx.x + w2];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && h.loss) h.loss[k] = red[0] / (float)B;
+}
+
+template <typename T, int CMAX>
+hipError_t launch_pair(const HeadArgs& h, hipStream_t s, int which) {
+  const bool gather = h.gather != 0;  // the top layer is layer 1
+  if (which == 0) {
+    dim3 grid((h.B + 7) / 8, h.K);  // 4 waves x 2 rows per workgroup
+    if (gather)
+      hipLaunchKernelGGL((k_head_fwd<T, CMAX, true>), grid, dim3(256), 0, s, h);
+    else
+      hipLaunchKernelGGL((k_head_fwd<T, CMAX, false>), grid, dim3(256), 0, s, h);
+  } else {
+    dim3 grid((h.D + 63) / 64, h.K);
+    if (gather)
+      hipLaunchKernelGGL((k_head_wgrad<T, CMAX, true>), grid, dim3(256), 0, s, h);
+    else
+      hipLaunchKernelGGL((k_head_wgrad<T, CMAX, false>), grid, dim3(256), 0, s, h);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_head(int dtype, const HeadArgs& h, hipStream_t s, int which) {
+  if (h.C < 1 || h.C > kHeadMaxClasses) return hipErrorInvalidValue;
+  if (h.K > 65535 || h.B < 1 || h.D < 1) return hipErrorInvalidValue;
+  if (dtype == 1)
+    return h.C <= 16 ? launch_pair<bf16_t, 16>(h, s, which)
+                     : launch_pair<bf16_t, 32>(h, s, which);
+  return h.C <= 16 ? launch_pair<float, 16>(h, s, which)
+                   : launch_pair<float, 32>(h, s, which);
+}
+
+}  // namespace
+
+hipError_t launch_head_fwd(int dtype, const HeadArgs& h, hipStream_t s) {
+  return launch_head(dtype, h, s, 0);
+}
+hipError_t launch_head_wgrad(int dtype, const HeadArgs& h, hipStream_t s) {
+  return launch_head(dtype, h, s, 1);
+}
+
+}  // namespace lsgd

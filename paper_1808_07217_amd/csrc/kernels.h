@@ -51,10 +51,52 @@ struct GemmArgs {
   bf16_t* Wb;
   float lr, mom, wd;
   int nesterov;
+  // EPI_SGD: when bias_w != nullptr the kernel also forms the bias gradient
+  // sum_k B[k][n] and updates bias_w / bias_u (group stride sBiasP)
+  float* bias_w;
+  float* bias_u;
+  long long sBiasP;
+  // split-K: `splits` partial sums of K range kchunk each, written to `part`
+  // ([splits][G][M][N] fp32) and reduced by a second kernel
+  int splits;
+  int kchunk;  // set by launch_gemm
+  float* part;
 };
+
+// Split count launch_gemm would like for a problem (1 = no split-K).
+int gemm_splits(int dtype, int M, int N, int Kd, int G, int epi);
 
 hipError_t launch_gemm(int dtype, int trans_a, int trans_b, int epi,
                        int out_bf16, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- head
+// Output layer with few classes, fused around the loss (head.hip).
+constexpr int kHeadMaxClasses = 32;
+struct HeadArgs {
+  int K, B, D, C;            // replicas, batch, inputs, classes
+  const void* A;             // layer input: activations [K][B][D] (group
+  long long sA;              //   stride sA) or, if gather, dataset rows
+  int gather;                //   selected by rowmap
+  const int32_t* rowmap;     // sampled indices [K][B]
+  const int32_t* y;          // labels [N]
+  const void* W;             // W_L [D][C] operand (fp32 master or bf16 copy)
+  long long sW;              //   group stride
+  float* Wm;                 // W_L master, momentum, bf16 copy (update)
+  float* Um;
+  bf16_t* Wb;
+  float* bias;               // b_L (read by the forward pass)
+  float* bias_w;             // b_L and its momentum (update)
+  float* bias_u;
+  long long sP;              // replica stride of the parameter buffers
+  void* dZ;                  // [K][B][C] out (activation dtype)
+  void* dZprev;              // [K][B][D] masked input gradient, or nullptr
+  float* rowloss;            // [K][B]
+  float* loss;               // [K] or nullptr
+  float lr, mom, wd;
+  int nesterov;
+};
+hipError_t launch_head_fwd(int dtype, const HeadArgs& h, hipStream_t s);
+hipError_t launch_head_wgrad(int dtype, const HeadArgs& h, hipStream_t s);
 
 // ---------------------------------------------------------------- others
 hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N,
@@ -62,10 +104,6 @@ hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N,
 hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,
                        int K, int B, int C, void* dZ, int dz_bf16,
                        float* loss, hipStream_t s);
-hipError_t launch_bias_update(const void* dZ, int dz_bf16, int K, int B,
-                              int D, float* b, float* u, long long sParam,
-                              float lr, float mom, float wd, int nesterov,
-                              hipStream_t s);
 hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
                              float lr, float mom, float wd, int nesterov,
                              hipStream_t s);

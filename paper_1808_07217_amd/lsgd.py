@@ -66,7 +66,8 @@ _SIGS = {
     "lsgd_profile_report": [_P, _c.c_char_p, _c.c_size_t],
     "lsgd_grouped_gemm": [_c.c_int32, _c.c_int32, _c.c_int32, _c.c_int32,
                           _c.c_int32, _c.c_int32, _c.c_int32, _P, _c.c_int64,
-                          _c.c_int64, _P, _c.c_int64, _c.c_int64, _P, _P],
+                          _c.c_int64, _P, _c.c_int64, _c.c_int64, _P,
+                          _c.c_int32, _P, _P],
     "lsgd_replica_average": [_P, _c.c_int32, _c.c_int64, _P],
     "lsgd_sgd_update": [_P, _P, _P, _c.c_int64, _c.c_float, _c.c_float,
                         _c.c_float, _c.c_int32, _P],
@@ -258,9 +259,10 @@ def post_local_schedule(H: int, rounds: int, lr: float, warm_rounds: int = 0,
 
 # -- building blocks ------------------------------------------------------
 def grouped_gemm(A: torch.Tensor, B: torch.Tensor, trans_a=False, trans_b=False,
-                 out: Optional[torch.Tensor] = None) -> torch.Tensor:
+                 out: Optional[torch.Tensor] = None, splits: int = 1) -> torch.Tensor:
     """C[g] = op(A[g]) @ op(B[g]) on the matrix cores (fp32 or bf16 inputs,
-    fp32 accumulation and output). A, B are contiguous 3-D tensors."""
+    fp32 accumulation and output). A, B are contiguous 3-D tensors; splits > 1
+    runs the split-K path."""
     if A.dtype != B.dtype or A.dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("A and B must both be float32 or both bfloat16")
     if A.dim() != 3 or B.dim() != 3 or A.shape[0] != B.shape[0]:
@@ -273,10 +275,13 @@ def grouped_gemm(A: torch.Tensor, B: torch.Tensor, trans_a=False, trans_b=False,
         raise ValueError("inner dimensions differ")
     out = out if out is not None else torch.empty((G, M, N), device=A.device)
     dt = BF16 if A.dtype == torch.bfloat16 else FP32
+    part = (torch.empty((splits, G, M, N), device=A.device) if splits > 1
+            else None)
     _check(_lib.lsgd_grouped_gemm(
         dt, int(trans_a), int(trans_b), G, M, N, Kd, _ptr(A), A.shape[2],
         A.shape[1] * A.shape[2], _ptr(B), B.shape[2], B.shape[1] * B.shape[2],
-        _ptr(out), _stream_handle(torch.cuda.current_stream(A.device))))
+        _ptr(out), int(splits), _ptr(part),
+        _stream_handle(torch.cuda.current_stream(A.device))))
     return out
 
 

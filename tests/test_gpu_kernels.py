@@ -44,19 +44,20 @@ GEMM_SHAPES = [(3, 70, 45, 37), (2, 64, 64, 16), (1, 1, 1, 1), (2, 33, 10, 130),
                (2, 3072, 512, 128), (1, 96, 200, 3072)]
 
 
+@pytest.mark.parametrize("splits", [1, 3])
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 @pytest.mark.parametrize("shape", GEMM_SHAPES)
-def test_grouped_gemm_error_bound(dtype, ta, tb, shape):
+def test_grouped_gemm_error_bound(dtype, ta, tb, shape, splits):
     L = _lsgd()
     G, M, N, Kd = shape
-    print(f"gemm {dtype} ta={ta} tb={tb} {shape}", flush=True)
+    print(f"gemm {dtype} ta={ta} tb={tb} {shape} splits={splits}", flush=True)
     rng = np.random.default_rng(M * 7 + N * 3 + Kd + ta * 2 + tb)
     A = rng.standard_normal((G, Kd, M) if ta else (G, M, Kd)).astype(np.float32)
     B = rng.standard_normal((G, N, Kd) if tb else (G, Kd, N)).astype(np.float32)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     Ad, Bd = to_dev(A).to(tdt), to_dev(B).to(tdt)
-    C = L.grouped_gemm(Ad, Bd, bool(ta), bool(tb)).cpu().numpy().astype(np.float64)
+    C = L.grouped_gemm(Ad, Bd, bool(ta), bool(tb), splits=splits).cpu().numpy().astype(np.float64)
     A64 = Ad.to(torch.float64).cpu().numpy()   # the exact operand values used
     B64 = Bd.to(torch.float64).cpu().numpy()
     opA = A64.transpose(0, 2, 1) if ta else A64
