@@ -17,7 +17,11 @@
  *    and unmodified by the caller until lsgd_destroy.
  *  - Work is enqueued asynchronously on the stream given at init (a
  *    hipStream_t passed as void*, NULL = the null stream). Results are valid
- *    once that stream has been synchronised (lsgd_sync does it).
+ *    once that stream has been synchronised (lsgd_sync does it). Inside a
+ *    local step, weight updates that feed nothing else in the step may run on
+ *    two internal streams of default priority; they are joined back into the
+ *    given stream before the step's last command, so stream order on the
+ *    given stream still covers all of the step's work.
  *  - Every call returns a status. Argument errors return LSGD_E_INVALID and
  *    change nothing. A failed HIP call returns LSGD_E_HIP and latches: from
  *    then on every call on that context returns LSGD_E_STATE until destroy.

@@ -130,6 +130,11 @@ struct Profiler {
 struct lsgd_ctx {
   lsgd_config cfg;
   Profiler prof;
+  // side streams for weight updates that do not feed the rest of the step
+  // (default priority), with fork/join events; created at init
+  hipStream_t side[2] = {nullptr, nullptr};
+  hipEvent_t fork[2] = {nullptr, nullptr}, join[2] = {nullptr, nullptr};
+  bool use_side = false;
   Layout lay;
   const float* X = nullptr;
   const int32_t* y = nullptr;
@@ -151,6 +156,17 @@ struct lsgd_ctx {
   void* dZ(int l) const { return ws + lay.dZ[l]; }
   bool bf16() const { return cfg.gemm_dtype == LSGD_BF16; }
 
+  ~lsgd_ctx() {
+    for (int i = 0; i < 2; ++i) {
+      if (side[i]) {
+        (void)hipStreamSynchronize(side[i]);
+        (void)hipStreamDestroy(side[i]);
+      }
+      if (fork[i]) (void)hipEventDestroy(fork[i]);
+      if (join[i]) (void)hipEventDestroy(join[i]);
+    }
+  }
+
   lsgd_status fail(hipError_t e, const char* what) {
     latched = LSGD_E_HIP;
     char buf[256];
@@ -166,21 +182,23 @@ struct lsgd_ctx {
     if (e_ != hipSuccess) return (ctx)->fail(e_, #expr);    \
   } while (0)
 
-// A kernel launch, bracketed by profiling events when profiling is on.
-#define LSGD_LAUNCH(ctx, tag, expr)                                        \
+// A kernel launch on stream `st`, bracketed by profiling events on that
+// stream when profiling is on.
+#define LSGD_LAUNCH_ON(ctx, st, tag, expr)                                 \
   do {                                                                     \
     hipEvent_t a_ = nullptr, b_ = nullptr;                                 \
     if ((ctx)->prof.on) {                                                  \
       LSGD_CK(ctx, (ctx)->prof.event(&a_));                                \
       LSGD_CK(ctx, (ctx)->prof.event(&b_));                                \
-      LSGD_CK(ctx, hipEventRecord(a_, (ctx)->stream));                     \
+      LSGD_CK(ctx, hipEventRecord(a_, (st)));                              \
     }                                                                      \
     LSGD_CK(ctx, expr);                                                    \
     if ((ctx)->prof.on) {                                                  \
-      LSGD_CK(ctx, hipEventRecord(b_, (ctx)->stream));                     \
+      LSGD_CK(ctx, hipEventRecord(b_, (st)));                              \
       (ctx)->prof.recs.push_back({std::string(tag), a_, b_});              \
     }                                                                      \
   } while (0)
+#define LSGD_LAUNCH(ctx, tag, expr) LSGD_LAUNCH_ON(ctx, (ctx)->stream, tag, expr)
 
 namespace {
 
@@ -267,8 +285,17 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     h.nesterov = cf.nesterov;
     // logits, loss, dZ_L and the masked input gradient of the top layer
     LSGD_LAUNCH(c, "head_fwd", lsgd::launch_head_fwd(dt, h, s));
-    // the top layer's weight gradient reads dZ_L only: update it now
-    LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(dt, h, s));
+    // the top layer's weight gradient feeds nothing else in this step: it
+    // runs on side stream 0 while the backward pass continues
+    if (c->use_side) {
+      LSGD_CK(c, hipEventRecord(c->fork[0], s));
+      LSGD_CK(c, hipStreamWaitEvent(c->side[0], c->fork[0], 0));
+      LSGD_LAUNCH_ON(c, c->side[0], "head_wgrad",
+                     lsgd::launch_head_wgrad(dt, h, c->side[0]));
+      LSGD_CK(c, hipEventRecord(c->join[0], c->side[0]));
+    } else {
+      LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(dt, h, s));
+    }
   } else {
     LSGD_LAUNCH(c, "xent", lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L],
                                                c->dZ(L), dt, d_loss, s));
@@ -330,8 +357,22 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     a.bias_u = U + ly.offB[l - 1];
     a.sBiasP = ly.Ps;
     a.splits = 1;
-    LSGD_LAUNCH(c, "wgrad_update" + std::to_string(l),
-                lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
+    if (c->use_side && l > 1) {
+      // after its input gradient, layer l's update only has to finish by the
+      // end of the step: side stream 1, overlapping the layers below
+      LSGD_CK(c, hipEventRecord(c->fork[1], s));
+      LSGD_CK(c, hipStreamWaitEvent(c->side[1], c->fork[1], 0));
+      LSGD_LAUNCH_ON(c, c->side[1], "wgrad_update" + std::to_string(l),
+                     lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, c->side[1]));
+    } else {
+      LSGD_LAUNCH(c, "wgrad_update" + std::to_string(l),
+                  lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
+    }
+  }
+  if (c->use_side) {  // join: the step ends when all of its updates have
+    LSGD_CK(c, hipEventRecord(c->join[1], c->side[1]));
+    LSGD_CK(c, hipStreamWaitEvent(s, c->join[0], 0));
+    LSGD_CK(c, hipStreamWaitEvent(s, c->join[1], 0));
   }
   c->step += 1;
   return LSGD_OK;
@@ -396,6 +437,16 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
   if (c->bf16())
     check(lsgd::launch_to_bf16(d_X, c->Xb(), (long long)cfg->N * cfg->widths[0],
                                c->stream), "dataset to bf16");
+  // side streams pay off once there is a hidden layer (an update that can
+  // overlap the rest of the backward pass)
+  if (st == LSGD_OK && ly.head && ly.L >= 2) {
+    for (int i = 0; i < 2; ++i) {
+      check(hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking), "side stream");
+      check(hipEventCreateWithFlags(&c->fork[i], hipEventDisableTiming), "fork event");
+      check(hipEventCreateWithFlags(&c->join[i], hipEventDisableTiming), "join event");
+    }
+    c->use_side = st == LSGD_OK;
+  }
   if (st != LSGD_OK) {
     delete c;
     return st;
