@@ -248,18 +248,30 @@ def local_step(state, wl, X, y, lr, replicas=None):
     K = state.W.shape[0]
     ks = range(K) if replicas is None else replicas
     losses = np.full(K, np.nan)
-    mask = decay_mask(wl.widths)
+    mask = model_decay_mask(wl)
     for k in ks:
         idx = sample_indices(wl.sample_seed, state.step, k, K, wl.N, wl.B_loc)
         A0 = np.asarray(X[idx], np.float64)
-        loss, grad = loss_and_grad(state.W[k], wl.widths, A0, y[idx],
-                                   bf16=(wl.dtype == "bf16"))
+        loss, grad = model_loss_and_grad(wl, state.W[k], A0, y[idx])
         state.W[k], state.U[k] = sgd_update(
             state.W[k], state.U[k], grad, lr, wl.momentum, wl.weight_decay,
             wl.nesterov, mask)
         losses[k] = loss
     state.step += 1
     return losses
+
+
+def model_loss_and_grad(wl, w, A0, y):
+    """Loss and gradient of the workload's model on one mini-batch."""
+    if wl.model == "resnet20":
+        return resnet_loss_and_grad(w, resnet_arch(), A0, y)
+    return loss_and_grad(w, wl.widths, A0, y, bf16=(wl.dtype == "bf16"))
+
+
+def model_decay_mask(wl):
+    if wl.model == "resnet20":
+        return resnet_decay_mask(resnet_arch())
+    return decay_mask(wl.widths)
 
 
 def run_round(state, wl, X, y, H, lr):
@@ -302,15 +314,199 @@ def minibatch_sgd(wl, X, y, w0, steps, lr):
     Used only as the comparator of the H = 1 special case."""
     w = np.asarray(w0, np.float64).copy()
     u = np.zeros_like(w)
-    mask = decay_mask(wl.widths)
+    mask = model_decay_mask(wl)
     for s in range(steps):
         idx = np.concatenate([
             sample_indices(wl.sample_seed, s, k, wl.K, wl.N, wl.B_loc)
             for k in range(wl.K)])
-        _, grad = loss_and_grad(w, wl.widths, np.asarray(X[idx], np.float64),
-                                y[idx], bf16=(wl.dtype == "bf16"))
+        _, grad = model_loss_and_grad(wl, w, np.asarray(X[idx], np.float64), y[idx])
         g = grad + wl.weight_decay * mask * w
         u = wl.momentum * u + g
         d = g + wl.momentum * u if wl.nesterov else u
         w = w - lr * d
     return w
+
+
+# --------------------------------------------------------------------------
+# ResNet-20-shaped network (the CIFAR ResNet of the appendix on models and
+# Table 5: 0.27M parameters, 0.041 G multiply-adds per image). NHWC images;
+# 3x3 convolutions, padding 1; per-worker batch normalisation (training-mode
+# batch statistics, the per-worker BN of the CIFAR setup paragraph); option-A
+# shortcuts (subsample, zero-pad channels); global average pool; FC classifier.
+# --------------------------------------------------------------------------
+BN_EPS = 1e-5
+
+
+def resnet_arch(side=32, cin=3, base=16, blocks=3, classes=10):
+    return dict(side=side, cin=cin, base=base, blocks=blocks, classes=classes)
+
+
+def resnet_convs(arch):
+    """[(name, c_in, c_out, stride)] of every 3x3 convolution, in order."""
+    out = [("conv1", arch["cin"], arch["base"], 1)]
+    c = arch["base"]
+    for s in range(3):
+        co = arch["base"] * 2**s
+        for b in range(arch["blocks"]):
+            stride = 2 if (s > 0 and b == 0) else 1
+            out.append((f"s{s}b{b}a", c, co, stride))
+            out.append((f"s{s}b{b}b", co, co, 1))
+            c = co
+    return out
+
+
+def resnet_layout(arch):
+    """[(name, shape, decays)] of the flat parameter vector, in order: per
+    convolution its weight [3][3][c_in][c_out] then BN gamma and beta; then
+    the classifier weight [c][classes] and bias."""
+    out = []
+    for name, ci, co, _ in resnet_convs(arch):
+        out += [(name + ".w", (3, 3, ci, co), True), (name + ".g", (co,), False),
+                (name + ".be", (co,), False)]
+    c = arch["base"] * 4
+    out += [("fc.w", (c, arch["classes"]), True), ("fc.b", (arch["classes"],), True)]
+    return out
+
+
+def resnet_unpack(w, arch):
+    out, o = {}, 0
+    for name, shape, _ in resnet_layout(arch):
+        n = int(np.prod(shape))
+        out[name] = w[o:o + n].reshape(shape)
+        o += n
+    assert o == w.size
+    return out
+
+
+def resnet_decay_mask(arch):
+    return np.concatenate([np.full(int(np.prod(s)), 1.0 if d else 0.0)
+                           for _, s, d in resnet_layout(arch)])
+
+
+def _im2col(x, stride):
+    """x [B][H][W][C] -> patches [B][Ho][Wo][3][3][C] (zero padding 1)."""
+    xp = np.pad(x, ((0, 0), (1, 1), (1, 1), (0, 0)))
+    win = np.lib.stride_tricks.sliding_window_view(xp, (3, 3), axis=(1, 2))
+    win = win[:, ::stride, ::stride]               # [B][Ho][Wo][C][3][3]
+    return np.ascontiguousarray(win.transpose(0, 1, 2, 4, 5, 3))
+
+
+def conv3x3(x, W, stride):
+    """Convolution with weight W [3][3][c_in][c_out]; returns (y, patches)."""
+    cols = _im2col(x, stride)
+    B, Ho, Wo = cols.shape[:3]
+    y = cols.reshape(B * Ho * Wo, -1) @ W.reshape(-1, W.shape[3])
+    return y.reshape(B, Ho, Wo, W.shape[3]), cols
+
+
+def conv3x3_backward(dy, cols, W, x_shape, stride):
+    """Gradients of conv3x3 w.r.t. its weight and its input."""
+    B, Ho, Wo, co = dy.shape
+    d2 = dy.reshape(-1, co)
+    dW = (cols.reshape(d2.shape[0], -1).T @ d2).reshape(W.shape)
+    dcols = (d2 @ W.reshape(-1, co).T).reshape(B, Ho, Wo, 3, 3, -1)
+    H, Wd = x_shape[1], x_shape[2]
+    dxp = np.zeros((B, H + 2, Wd + 2, x_shape[3]))
+    for kh in range(3):
+        for kw in range(3):
+            dxp[:, kh:kh + stride * Ho:stride, kw:kw + stride * Wo:stride, :] += \
+                dcols[:, :, :, kh, kw, :]
+    return dW, dxp[:, 1:H + 1, 1:Wd + 1, :]
+
+
+def batchnorm(x, g, be):
+    """Training-mode BN over (batch, height, width), biased variance."""
+    mu = x.mean(axis=(0, 1, 2))
+    var = ((x - mu) ** 2).mean(axis=(0, 1, 2))
+    inv = 1.0 / np.sqrt(var + BN_EPS)
+    xh = (x - mu) * inv
+    return g * xh + be, (xh, inv, g)
+
+
+def batchnorm_backward(dy, cache):
+    xh, inv, g = cache
+    dbe = dy.sum(axis=(0, 1, 2))
+    dg = (dy * xh).sum(axis=(0, 1, 2))
+    dx = g * inv * (dy - dy.mean(axis=(0, 1, 2)) - xh * (dy * xh).mean(axis=(0, 1, 2)))
+    return dx, dg, dbe
+
+
+def _shortcut(x, co):
+    """Option A: every second pixel, channels zero-padded to co."""
+    s = x[:, ::2, ::2, :]
+    return np.concatenate([s, np.zeros(s.shape[:3] + (co - s.shape[3],))], axis=3)
+
+
+def resnet_loss_and_grad(w, arch, A0, y):
+    """Mean mini-batch loss and flat gradient; A0 [B][side*side*cin] NHWC."""
+    p = resnet_unpack(np.asarray(w, np.float64), arch)
+    B = A0.shape[0]
+    x = np.asarray(A0, np.float64).reshape(B, arch["side"], arch["side"], arch["cin"])
+    convs = resnet_convs(arch)
+    tape = []
+
+    def cbr(x, name, stride, relu):
+        y, cols = conv3x3(x, p[name + ".w"], stride)
+        z, bc = batchnorm(y, p[name + ".g"], p[name + ".be"])
+        tape.append((name, x.shape, stride, cols, bc))
+        return np.maximum(z, 0.0) if relu else z, z
+
+    h, _ = cbr(x, "conv1", 1, True)
+    blocks = []  # (input, pre-activation of the output) per block
+    for i in range(1, len(convs), 2):
+        name_a, ci, co, stride = convs[i]
+        name_b = convs[i + 1][0]
+        a, za = cbr(h, name_a, stride, True)
+        b, _ = cbr(a, name_b, 1, False)
+        sc = h if (stride == 1 and ci == co) else _shortcut(h, co)
+        out = b + sc
+        blocks.append((h, za, out, stride, ci, co))
+        h = np.maximum(out, 0.0)
+    feat = h.mean(axis=(1, 2))                           # global average pool
+    z = feat @ p["fc.w"] + p["fc.b"]
+    loss, prob = cross_entropy(z, y)
+    dz = prob.copy()
+    dz[np.arange(B), y] -= 1.0
+    dz /= B
+
+    g = {"fc.w": feat.T @ dz, "fc.b": dz.sum(axis=0)}
+    dh = np.broadcast_to((dz @ p["fc.w"].T)[:, None, None, :], h.shape) / (h.shape[1] * h.shape[2])
+    t = len(tape) - 1
+    for (hin, za, out, stride, ci, co) in reversed(blocks):
+        dout = dh * (out > 0.0)
+        # second convolution of the block (no ReLU after its BN)
+        name_b, xs_b, st_b, cols_b, bc_b = tape[t]
+        dyb, g[name_b + ".g"], g[name_b + ".be"] = batchnorm_backward(dout, bc_b)
+        g[name_b + ".w"], da = conv3x3_backward(dyb, cols_b, p[name_b + ".w"], xs_b, st_b)
+        t -= 1
+        name_a, xs_a, st_a, cols_a, bc_a = tape[t]
+        dza = da * (za > 0.0)
+        dya, g[name_a + ".g"], g[name_a + ".be"] = batchnorm_backward(dza, bc_a)
+        g[name_a + ".w"], dx = conv3x3_backward(dya, cols_a, p[name_a + ".w"], xs_a, st_a)
+        t -= 1
+        if stride == 1 and ci == co:
+            dx = dx + dout
+        else:
+            dsc = np.zeros_like(hin)
+            dsc[:, ::2, ::2, :] = dout[..., :ci]
+            dx = dx + dsc
+        dh = dx
+    name, xs, st, cols, bc = tape[0]
+    # conv1 output went through ReLU: its mask is the block-0 input > 0
+    dz1 = dh * (blocks[0][0] > 0.0)
+    dy1, g[name + ".g"], g[name + ".be"] = batchnorm_backward(dz1, bc)
+    g[name + ".w"], _ = conv3x3_backward(dy1, cols, p[name + ".w"], xs, st)
+    flat = np.concatenate([g[n].ravel() for n, _, _ in resnet_layout(arch)])
+    return float(loss.mean()), flat
+
+
+def resnet_param_count(arch):
+    return sum(int(np.prod(s)) for _, s, _ in resnet_layout(arch))
+
+
+def resnet_macs_per_image(arch):
+    side, macs = arch["side"], 0
+    for _, ci, co, stride in resnet_convs(arch):
+        side //= stride
+        macs += side * side * 9 * ci * co
+    return macs + arch["base"] * 4 * arch["classes"]

@@ -1,0 +1,45 @@
+"""Whole-run loss trajectories of the HIP path against the oracle's.
+
+The expected trajectories in tests/golden/trajectory_<name>.json were written
+by tests/golden/make_trajectories.py, which runs only the CPU oracle on the
+seeded inputs. Every local step of every round is compared: the mean over the
+K replicas of the mini-batch loss, relative error 1e-3 (fp32) or 2e-2 (bf16
+GEMM operands).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wk
+from gpu_util import make_replicas, rel, device
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CASES = [("mlp_512", 1e-3), ("postlocal_mlp_512", 1e-3)]
+
+
+@pytest.mark.parametrize("name,tol", CASES)
+def test_full_run_loss_trajectory(name, tol):
+    from paper_1808_07217_amd import lsgd as L
+    with open(os.path.join(HERE, "golden", f"trajectory_{name}.json")) as f:
+        gold = json.load(f)["per_round_step_mean_loss"]
+    w = wk.get(name)
+    sched = L.post_local_schedule(w.H, w.rounds, w.lr, w.warm_rounds,
+                                  w.lr_after_switch)
+    assert [H for H, _ in sched] == [len(r) for r in gold]
+    print(f"{name}: {len(sched)} rounds, {sum(H for H, _ in sched)} local steps",
+          flush=True)
+    reps = make_replicas(w)
+    loss = torch.empty(sum(H for H, _ in sched), w.K, device=device())
+    L.run_schedule(reps, sched, loss)
+    got = loss.cpu().numpy().mean(axis=1)
+    want = np.concatenate([np.asarray(r) for r in gold])
+    err = rel(got, want)
+    print(f"{name}: max relative loss error {err.max():.3e} at step "
+          f"{int(err.argmax())}; final loss {got[-1]:.5g} vs {want[-1]:.5g}",
+          flush=True)
+    assert np.all(err <= tol)

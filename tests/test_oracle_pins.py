@@ -367,3 +367,75 @@ def test_loss_decreases_on_every_workload_first_rounds():
     _, traj = O.run(wl, X, y, wk.initial_weights(wl), rounds=10)
     means = [t.mean() for t in traj]
     assert means[-1] < 0.2 * means[0]
+
+
+# ------------------------------------------------------------------ ResNet-20
+def test_resnet20_shape_matches_table5():
+    """Table 5: ResNet-20 (CIFAR-10) has 0.27 M parameters and 0.041 G
+    multiply-adds per image; the network built here has 269,722 and
+    40,551,040."""
+    a = O.resnet_arch()
+    assert O.resnet_param_count(a) == 269722
+    assert O.resnet_macs_per_image(a) == 40551040
+    assert round(O.resnet_param_count(a) / 1e6, 2) == 0.27
+    assert round(O.resnet_macs_per_image(a) / 1e9, 3) == 0.041
+    assert len(O.resnet_convs(a)) == 19          # 1 + 3 stages x 3 blocks x 2
+
+
+def test_conv3x3_against_direct_loops():
+    rng = np.random.default_rng(21)
+    for stride in (1, 2):
+        x = rng.standard_normal((2, 5, 6, 3))
+        W = rng.standard_normal((3, 3, 3, 4))
+        y, _ = O.conv3x3(x, W, stride)
+        Ho, Wo = (5 + 2 - 3) // stride + 1, (6 + 2 - 3) // stride + 1
+        assert y.shape == (2, Ho, Wo, 4)
+        ref = np.zeros_like(y)
+        for b in range(2):
+            for i in range(Ho):
+                for j in range(Wo):
+                    for kh in range(3):
+                        for kw in range(3):
+                            r, c = i * stride + kh - 1, j * stride + kw - 1
+                            if 0 <= r < 5 and 0 <= c < 6:
+                                ref[b, i, j] += x[b, r, c] @ W[kh, kw]
+        np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_batchnorm_normalises_per_channel():
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((4, 3, 3, 5)) * 3 + 2
+    y, _ = O.batchnorm(x, np.ones(5), np.zeros(5))
+    np.testing.assert_allclose(y.mean(axis=(0, 1, 2)), 0, atol=1e-12)
+    var = x.var(axis=(0, 1, 2))
+    np.testing.assert_allclose(y.var(axis=(0, 1, 2)), var / (var + O.BN_EPS), rtol=1e-10)
+
+
+def test_resnet_gradient_matches_central_differences():
+    """Tiny ResNet (4x4 images, channels 2/4/8, one block per stage): every
+    parameter, including BN scales and shifts, stride-2 convolutions and the
+    zero-padded shortcuts."""
+    a = O.resnet_arch(side=4, cin=2, base=2, blocks=1, classes=3)
+    P = O.resnet_param_count(a)
+    rng = np.random.default_rng(23)
+    w = rng.standard_normal(P) * 0.5
+    A0 = rng.standard_normal((6, 4 * 4 * 2))
+    y = rng.integers(0, 3, 6)
+    _, g = O.resnet_loss_and_grad(w, a, A0, y)
+    eps = 1e-6
+    fd = np.empty(P)
+    for i in range(P):
+        wp, wm = w.copy(), w.copy()
+        wp[i] += eps
+        wm[i] -= eps
+        fd[i] = (O.resnet_loss_and_grad(wp, a, A0, y)[0] -
+                 O.resnet_loss_and_grad(wm, a, A0, y)[0]) / (2 * eps)
+    assert np.max(np.abs(fd - g)) <= 1e-6 * max(1.0, np.max(np.abs(g)))
+
+
+def test_resnet_decay_mask_exempts_batchnorm():
+    a = O.resnet_arch()
+    m = O.resnet_decay_mask(a)
+    n_bn = sum(int(np.prod(s)) for nme, s, _ in O.resnet_layout(a)
+               if nme.endswith(".g") or nme.endswith(".be"))
+    assert m.size == 269722 and int((m == 0).sum()) == n_bn == 2 * (16 * 7 + 32 * 6 + 64 * 6)

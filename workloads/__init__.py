@@ -103,6 +103,12 @@ WORKLOADS = {
         dtype="bf16", K=64, B_loc=64, H=8, rounds=10, lr=0.001,
         momentum=0.9, nesterov=False, weight_decay=1e-4, **_IMG,
         data_seed=201, init_seed=402, sample_seed=0x5EED0004),
+    # ResNet-20-shaped CNN, fp32, per-worker BN, heavy-ball momentum
+    "resnet20": Workload(
+        name="resnet20", model="resnet20", widths=(3072, 10), dtype="fp32",
+        K=16, B_loc=128, H=16, rounds=5, lr=0.05, momentum=0.9,
+        nesterov=False, weight_decay=1e-4, data="img3072_nhwc", N=50000,
+        data_seed=201, init_seed=502, sample_seed=0x5EED0005),
 }
 
 
@@ -115,7 +121,9 @@ def layer_shapes(widths) -> list:
     return [(widths[i], widths[i + 1]) for i in range(len(widths) - 1)]
 
 
-def param_count(widths) -> int:
+def param_count(widths, model: str = "mlp") -> int:
+    if model == "resnet20":
+        return sum(int(np.prod(s)) for _, s in resnet_tensors(classes=widths[-1]))
     return sum(a * b + b for a, b in layer_shapes(widths))
 
 
@@ -140,6 +148,13 @@ def _dataset_cached(kind: str, N: int, seed: int):
         std = Xc.std(axis=(0, 2), keepdims=True)
         Xc -= mean
         Xc /= std
+    elif kind == "img3072_nhwc":
+        # the same images, stored as [N][32][32][3] (channel innermost)
+        Xc, y32 = _dataset_cached("img3072", N, seed)
+        X = np.ascontiguousarray(
+            Xc.reshape(N, 3, 32, 32).transpose(0, 2, 3, 1)).reshape(N, 3072)
+        X.setflags(write=False)
+        return X, y32
     else:
         raise ValueError(f"unknown dataset kind {kind!r}")
     X32 = np.ascontiguousarray(X, dtype=np.float32)
@@ -154,14 +169,49 @@ def dataset(w: Workload):
     return _dataset_cached(w.data, w.N, w.data_seed)
 
 
+RESNET_STAGES = (16, 32, 64)   # channels of the three stages
+
+
+def resnet_tensors(blocks: int = 3, cin: int = 3, classes: int = 10):
+    """[(kind, shape)] of the ResNet-20 parameter vector, in order: per 3x3
+    convolution its weight [3][3][c_in][c_out] ("conv"), BN scale ("bn_g")
+    and shift ("bn_b"); then the classifier weight [64][classes] ("fc_w")
+    and bias ("fc_b"). Convolutions: the stem, then per stage and block two
+    convolutions (the first of stages 2 and 3 has stride 2)."""
+    out, c = [], RESNET_STAGES[0]
+    convs = [(cin, c)]
+    for co in RESNET_STAGES:
+        for _ in range(blocks):
+            convs += [(c, co), (co, co)]
+            c = co
+    for ci, co in convs:
+        out += [("conv", (3, 3, ci, co)), ("bn_g", (co,)), ("bn_b", (co,))]
+    out += [("fc_w", (RESNET_STAGES[-1], classes)), ("fc_b", (classes,))]
+    return out
+
+
 def initial_weights(w: Workload) -> np.ndarray:
     """The shared starting point w_(0), flat fp32 `[P]` in the layout above.
 
     Hidden layers: He normal, std sqrt(2 / fan_in); the classifier layer:
     N(0, 0.01^2); biases 0 (initialisation paragraph of the appendix on
-    models).
+    models). ResNet: convolutions He normal with fan_in = 9 c_in, BN scale 1
+    and shift 0, classifier as above.
     """
     rng = np.random.Generator(np.random.PCG64(w.init_seed))
+    if w.model == "resnet20":
+        parts = []
+        for kind, shape in resnet_tensors():
+            n = int(np.prod(shape))
+            if kind == "conv":
+                parts.append(np.sqrt(2.0 / (9 * shape[2])) * rng.standard_normal(n))
+            elif kind == "fc_w":
+                parts.append(0.01 * rng.standard_normal(n))
+            elif kind == "bn_g":
+                parts.append(np.ones(n))
+            else:
+                parts.append(np.zeros(n))
+        return np.concatenate(parts).astype(np.float32)
     parts = []
     shapes = layer_shapes(w.widths)
     for li, (din, dout) in enumerate(shapes):
