@@ -147,7 +147,7 @@ def main():
     dev = torch.device("cuda", 0)
     cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype,
                         momentum=w.momentum, weight_decay=w.weight_decay,
-                        nesterov=w.nesterov, seed=w.sample_seed)
+                        nesterov=w.nesterov, seed=w.sample_seed, model=w.model)
     Xd = torch.from_numpy(np.array(X)).to(dev)
     yd = torch.from_numpy(np.array(y)).to(dev)
     reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))

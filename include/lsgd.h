@@ -53,7 +53,18 @@ typedef enum lsgd_status {
   LSGD_E_UNSUPPORTED = 5  /* valid request this build does not implement */
 } lsgd_status;
 
-enum { LSGD_MODEL_MLP = 0 };      /* ReLU MLP; L = 1 is softmax regression */
+/* LSGD_MODEL_MLP: ReLU MLP with widths d_0 .. d_L (L = 1 is softmax
+ * regression). LSGD_MODEL_RESNET20: the CIFAR ResNet-20 of the paper's Table 5
+ * on 32x32x3 NHWC images (widths[0] = 3072, widths[1] = classes <= 32,
+ * n_layers = 1, fp32): a 3x3 stem convolution to 16 channels, three stages of
+ * three basic blocks at 16/32/64 channels (stride 2 entering stages 2 and 3,
+ * option-A shortcuts: subsample and zero-pad channels), batch normalisation
+ * with per-replica batch statistics after every convolution (no weight decay
+ * on its scale and shift), global average pooling and a 64 -> classes
+ * classifier. Parameter layout: per convolution in order its weight
+ * [3][3][c_in][c_out], BN scale [c_out], BN shift [c_out]; then the
+ * classifier weight [64][classes] and bias [classes]. */
+enum { LSGD_MODEL_MLP = 0, LSGD_MODEL_RESNET20 = 1 };
 enum { LSGD_FP32 = 0, LSGD_BF16 = 1 };
 #define LSGD_MAX_LAYERS 8
 
@@ -64,7 +75,7 @@ enum { LSGD_FP32 = 0, LSGD_BF16 = 1 };
  * post-local SGD stay on the host.
  */
 typedef struct lsgd_config {
-  int32_t model;                          /* LSGD_MODEL_MLP */
+  int32_t model;                          /* LSGD_MODEL_MLP / _RESNET20 */
   int32_t n_layers;                       /* L, 1..LSGD_MAX_LAYERS */
   int32_t widths[LSGD_MAX_LAYERS + 1];    /* d_0 (features) .. d_L (classes) */
   int32_t K;                              /* workers = replicas, >= 1 */

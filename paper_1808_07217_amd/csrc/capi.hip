@@ -21,8 +21,26 @@ constexpr int64_t kReplicaPad = 64;  // replica stride in elements: 256 B
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// ResNet-20 plan: the 19 convolutions (stem; 3 stages x 3 blocks x 2) with
+// their geometry, parameter offsets and activation buffers.
+struct ConvSpec {
+  int Cin, Cout, stride, H, W, Ho, Wo;
+  int64_t offW, offG, offB;  // weight [9*Cin][Cout], BN scale, BN shift
+  size_t y, act;             // pre-BN output, post-BN activation (ReLU'd)
+};
+constexpr int kResConvs = 19;
+struct ResPlan {
+  ConvSpec cv[kResConvs];
+  int64_t offFcW = 0, offFcB = 0;
+  int classes = 0, feat = 64, side_out = 8;
+  size_t featb = 0, dfeat = 0, dzh = 0, gbuf[4] = {}, mu = 0, inv = 0, coef = 0,
+         bnpart = 0, wpart = 0, wt = 0;
+};
+
 struct Layout {
   int L = 0;
+  bool resnet = false;
+  ResPlan rp;
   int64_t P = 0, Ps = 0;
   int64_t offW[LSGD_MAX_LAYERS] = {}, offB[LSGD_MAX_LAYERS] = {};
   size_t esz = 4;  // activation / operand element size
@@ -35,7 +53,13 @@ struct Layout {
 
 bool valid_config(const lsgd_config* c) {
   if (!c) return false;
-  if (c->model != LSGD_MODEL_MLP) return false;
+  if (c->model == LSGD_MODEL_RESNET20) {
+    if (c->n_layers != 1 || c->widths[0] != 3072 || c->widths[1] < 2 ||
+        c->widths[1] > lsgd::kHeadMaxClasses || c->gemm_dtype != LSGD_FP32)
+      return false;
+  } else if (c->model != LSGD_MODEL_MLP) {
+    return false;
+  }
   if (c->n_layers < 1 || c->n_layers > LSGD_MAX_LAYERS) return false;
   for (int i = 0; i <= c->n_layers; ++i)
     if (c->widths[i] < 1 || c->widths[i] > (1 << 20)) return false;
@@ -51,7 +75,80 @@ bool valid_config(const lsgd_config* c) {
   return true;
 }
 
+Layout make_resnet_layout(const lsgd_config* c) {
+  Layout l;
+  l.resnet = true;
+  l.L = 1;
+  ResPlan& r = l.rp;
+  r.classes = c->widths[1];
+  const int stages[3] = {16, 32, 64};
+  int n = 0, ci = 3, side = 32;
+  r.cv[n++] = {3, 16, 1, 32, 32, 32, 32, 0, 0, 0, 0, 0};
+  ci = 16;
+  for (int st = 0; st < 3; ++st) {
+    for (int b = 0; b < 3; ++b) {
+      const int co = stages[st], stride = (st > 0 && b == 0) ? 2 : 1;
+      const int so = side / stride;
+      r.cv[n++] = {ci, co, stride, side, side, so, so, 0, 0, 0, 0, 0};
+      r.cv[n++] = {co, co, 1, so, so, so, so, 0, 0, 0, 0, 0};
+      ci = co;
+      side = so;
+    }
+  }
+  int64_t o = 0;
+  for (int i = 0; i < kResConvs; ++i) {
+    r.cv[i].offW = o;
+    o += 9LL * r.cv[i].Cin * r.cv[i].Cout;
+    r.cv[i].offG = o;
+    o += r.cv[i].Cout;
+    r.cv[i].offB = o;
+    o += r.cv[i].Cout;
+  }
+  r.offFcW = o;
+  o += 64LL * r.classes;
+  r.offFcB = o;
+  o += r.classes;
+  l.P = o;
+  l.Ps = (o + kReplicaPad - 1) / kReplicaPad * kReplicaPad;
+  const size_t K = c->K, B = c->B_loc;
+  size_t t = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = t;
+    t = align_up(t + bytes, kAlign);
+    return at;
+  };
+  l.W = take(K * l.Ps * 4);
+  l.U = take(K * l.Ps * 4);
+  l.idx = take(K * B * 4);
+  l.rowloss = take(K * B * 4);
+  size_t maxact = 0, maxpart = 0, maxbn = 0, maxwt = 0;
+  for (int i = 0; i < kResConvs; ++i) {
+    const ConvSpec& q = r.cv[i];
+    const size_t sz = K * B * q.Ho * q.Wo * q.Cout * 4;
+    r.cv[i].y = take(sz);
+    r.cv[i].act = take(sz);
+    maxact = std::max(maxact, std::max(sz, K * B * q.H * q.W * q.Cin * 4));
+    maxpart = std::max(maxpart, (size_t)lsgd::conv_wgrad_splits(c->B_loc, q.Ho, q.Wo) *
+                                    K * 9 * q.Cin * q.Cout * 4);
+    maxbn = std::max(maxbn, K * lsgd::bn_chunks(c->B_loc * q.Ho * q.Wo) * q.Cout * 2 * 8);
+    maxwt = std::max(maxwt, K * 9 * q.Cin * q.Cout * 4);
+  }
+  r.featb = take(K * B * 64 * 4);
+  r.dfeat = take(K * B * 64 * 4);
+  r.dzh = take(K * B * r.classes * 4);
+  for (int i = 0; i < 4; ++i) r.gbuf[i] = take(maxact);
+  r.mu = take(kResConvs * K * 64 * 4);
+  r.inv = take(kResConvs * K * 64 * 4);
+  r.coef = take(K * 64 * 3 * 4);
+  r.bnpart = take(maxbn);
+  r.wpart = take(maxpart);
+  r.wt = take(maxwt);
+  l.total = t;
+  return l;
+}
+
 Layout make_layout(const lsgd_config* c) {
+  if (c->model == LSGD_MODEL_RESNET20) return make_resnet_layout(c);
   Layout l;
   l.L = c->n_layers;
   int64_t o = 0;
@@ -202,7 +299,10 @@ struct lsgd_ctx {
 
 namespace {
 
+lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss);
+
 lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
+  if (c->lay.resnet) return do_local_step_resnet(c, lr, d_loss);
   const lsgd_config& cf = c->cfg;
   const Layout& ly = c->lay;
   const int K = cf.K, B = cf.B_loc, L = ly.L;
@@ -374,6 +474,182 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_CK(c, hipStreamWaitEvent(s, c->join[0], 0));
     LSGD_CK(c, hipStreamWaitEvent(s, c->join[1], 0));
   }
+  c->step += 1;
+  return LSGD_OK;
+}
+
+lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
+  const lsgd_config& cf = c->cfg;
+  const ResPlan& r = c->lay.rp;
+  const int K = cf.K, B = cf.B_loc;
+  const long long Ps = c->lay.Ps;
+  const hipStream_t s = c->stream;
+  float* W = c->W();
+  float* U = c->U();
+  auto F = [&](size_t off) { return (float*)(c->ws + off); };
+  float* mu = F(r.mu);
+  float* inv = F(r.inv);
+  double* bnpart = (double*)(c->ws + r.bnpart);
+  auto geom = [&](int i) {
+    const ConvSpec& q = r.cv[i];
+    lsgd::ConvGeom g{};
+    g.G = K;
+    g.Bt = B;
+    g.H = q.H;
+    g.W = q.W;
+    g.Cin = q.Cin;
+    g.Ho = q.Ho;
+    g.Wo = q.Wo;
+    g.Cout = q.Cout;
+    g.stride = q.stride;
+    g.sx = (long long)B * q.H * q.W * q.Cin;
+    g.Wk = W + q.offW;
+    g.sW = Ps;
+    return g;
+  };
+  auto rows = [&](int i) { return B * r.cv[i].Ho * r.cv[i].Wo; };
+
+  LSGD_LAUNCH(c, "sample", lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
+
+  // forward: stem, then blocks (a: conv-BN-ReLU, b: conv-BN + shortcut, ReLU)
+  for (int i = 0; i < kResConvs; ++i) {
+    const ConvSpec& q = r.cv[i];
+    lsgd::ConvGeom g = geom(i);
+    const float* xin = nullptr;  // input activation of conv i
+    if (i == 0) {
+      g.x = c->X;
+      g.sx = 0;
+      g.rowmap = c->idx();
+    } else {
+      xin = F(r.cv[i - 1].act);
+      g.x = xin;
+    }
+    g.out = F(q.y);
+    LSGD_LAUNCH(c, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, s));
+    float* mi = mu + (size_t)i * K * 64;
+    float* ii = inv + (size_t)i * K * 64;
+    LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
+                                                     mi, ii, s));
+    int mode = 0;
+    const float* blk_in = nullptr;
+    int cin_blk = 0;
+    if (i > 0 && i % 2 == 0) {  // second convolution of a block
+      const ConvSpec& qa = r.cv[i - 1];
+      blk_in = F(r.cv[i - 2].act);
+      cin_blk = qa.Cin;
+      mode = (qa.stride == 1 && qa.Cin == q.Cout) ? 1 : 2;
+    }
+    LSGD_LAUNCH(c, "bn_apply", lsgd::launch_bn_apply(F(q.y), K, rows(i), q.Cout, mi, ii,
+                                                     W + q.offG, W + q.offB, Ps, mode,
+                                                     blk_in, q.Ho, q.Wo, cin_blk,
+                                                     F(q.act), s));
+  }
+
+  // head: global average pool, classifier, loss
+  const ConvSpec& last = r.cv[kResConvs - 1];
+  const int S = last.Ho * last.Wo;
+  LSGD_LAUNCH(c, "gap", lsgd::launch_gap(F(last.act), K * B, S, 64, F(r.featb), false,
+                                         nullptr, nullptr, s));
+  lsgd::HeadArgs h{};
+  h.K = K;
+  h.B = B;
+  h.D = 64;
+  h.C = r.classes;
+  h.gather = 0;
+  h.A = F(r.featb);
+  h.sA = (long long)B * 64;
+  h.rowmap = c->idx();
+  h.y = c->y;
+  h.W = W + r.offFcW;
+  h.sW = Ps;
+  h.Wm = W + r.offFcW;
+  h.Um = U + r.offFcW;
+  h.bias = W + r.offFcB;
+  h.bias_w = W + r.offFcB;
+  h.bias_u = U + r.offFcB;
+  h.sP = Ps;
+  h.dZ = F(r.dzh);
+  h.dZprev = F(r.dfeat);
+  h.nomask = 1;
+  h.rowloss = c->rowloss();
+  h.loss = d_loss;
+  h.lr = lr;
+  h.mom = cf.momentum;
+  h.wd = cf.weight_decay;
+  h.nesterov = cf.nesterov;
+  LSGD_LAUNCH(c, "head_fwd", lsgd::launch_head_fwd(0, h, s));
+  LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(0, h, s));
+
+  // backward
+  float* gb[4] = {F(r.gbuf[0]), F(r.gbuf[1]), F(r.gbuf[2]), F(r.gbuf[3])};
+  float* coef = F(r.coef);
+  float* wpart = F(r.wpart);
+  float* wt = F(r.wt);
+  LSGD_LAUNCH(c, "gap_bwd", lsgd::launch_gap(nullptr, K * B, S, 64, nullptr, true,
+                                             F(r.dfeat), gb[0], s));
+  int cur = 0;  // gb[cur] holds the gradient of the current block output
+  // BN backward (coefficients, gamma/beta update, input gradient into dy)
+  auto bn_bwd = [&](int i, const float* gup, const float* maskv, float* dy) {
+    const ConvSpec& q = r.cv[i];
+    return lsgd::launch_bn_backward(F(q.y), gup, maskv, K, rows(i), q.Cout, bnpart,
+                                    mu + (size_t)i * K * 64, inv + (size_t)i * K * 64,
+                                    coef, W + q.offG, W + q.offB, U + q.offG,
+                                    U + q.offB, Ps, lr, cf.momentum, cf.nesterov, dy, s);
+  };
+  // weight gradient of conv i from its input x and output gradient dy, then
+  // the update (after any input gradient that reads the old weight)
+  auto wgrad = [&](int i, const float* x, const float* dy) -> hipError_t {
+    const ConvSpec& q = r.cv[i];
+    lsgd::ConvGeom g = geom(i);
+    if (i == 0) {
+      g.x = c->X;
+      g.sx = 0;
+      g.rowmap = c->idx();
+    } else {
+      g.x = x;
+    }
+    g.dy = dy;
+    g.out = wpart;
+    hipError_t e = lsgd::launch_conv(lsgd::CONV_WGRAD_MODE, g, s);
+    if (e != hipSuccess) return e;
+    return lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo), K,
+                                     9 * q.Cin * q.Cout, W + q.offW, U + q.offW, Ps, lr,
+                                     cf.momentum, cf.weight_decay, cf.nesterov, s);
+  };
+  // input gradient of conv i (old weight, channels swapped per tap)
+  auto dgrad = [&](int i, const float* dy, float* dx) -> hipError_t {
+    const ConvSpec& q = r.cv[i];
+    hipError_t e = lsgd::launch_conv_wt(W + q.offW, Ps, K, q.Cin, q.Cout, wt, s);
+    if (e != hipSuccess) return e;
+    lsgd::ConvGeom g = geom(i);
+    g.dy = dy;
+    g.Wk = wt;
+    g.sW = 9LL * q.Cin * q.Cout;
+    g.out = dx;
+    return lsgd::launch_conv(lsgd::CONV_DGRAD_MODE, g, s);
+  };
+  for (int blk = 8; blk >= 0; --blk) {
+    const int ia = 2 * blk + 1, ib = 2 * blk + 2;
+    const ConvSpec& qa = r.cv[ia];
+    const float* h_in = F(r.cv[ia - 1].act);
+    const int nxt = cur == 0 ? 3 : 0;
+    // second convolution: its output went through the shortcut add and ReLU
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1]));
+    LSGD_LAUNCH(c, "conv_dgrad", dgrad(ib, gb[1], gb[2]));
+    LSGD_LAUNCH(c, "conv_wgrad", wgrad(ib, F(r.cv[ia].act), gb[1]));
+    // first convolution: ReLU'd BN output
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], F(r.cv[ia].act), gb[1]));
+    LSGD_LAUNCH(c, "conv_dgrad", dgrad(ia, gb[1], gb[nxt]));
+    LSGD_LAUNCH(c, "conv_wgrad", wgrad(ia, h_in, gb[1]));
+    // the shortcut's share of the block-output gradient
+    const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
+    LSGD_LAUNCH(c, "shortcut_bwd",
+                lsgd::launch_shortcut_grad(gb[nxt], gb[cur], F(r.cv[ib].act), K, B,
+                                           qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
+    cur = nxt;
+  }
+  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], F(r.cv[0].act), gb[1]));
+  LSGD_LAUNCH(c, "conv_wgrad", wgrad(0, nullptr, gb[1]));
   c->step += 1;
   return LSGD_OK;
 }

@@ -204,7 +204,8 @@ __global__ __launch_bounds__(256) void k_head_fwd(HeadArgs h) {
 #pragma unroll
         for (int q = 0; q < RPW; ++q)
           if (live[q])
-            st((T*)h.dZprev + rr[q] * D, d0 + d, mk[u][q] > 0.f ? v[q] : 0.f);
+            st((T*)h.dZprev + rr[q] * D, d0 + d,
+               (h.nomask || mk[u][q] > 0.f) ? v[q] : 0.f);
       }
     }
   }

@@ -94,9 +94,53 @@ struct HeadArgs {
   float* loss;               // [K] or nullptr
   float lr, mom, wd;
   int nesterov;
+  int nomask;                // dZprev without the ReLU mask (pooled inputs)
 };
 hipError_t launch_head_fwd(int dtype, const HeadArgs& h, hipStream_t s);
 hipError_t launch_head_wgrad(int dtype, const HeadArgs& h, hipStream_t s);
+
+// ---------------------------------------------------------------- ResNet
+// 3x3 convolution geometry of one launch (resnet.hip). x: input activations
+// [G][Bt][H][W][Cin] with group stride sx, or with a row map the dataset
+// rows (images) selected per replica; dy: output gradient
+// [G][Bt][Ho][Wo][Cout]; Wk: [9*Cin][Cout] (forward, weight gradient) or the
+// swapped copy [9*Cout][Cin] (input gradient), group stride sW; out: forward
+// y, input gradient dx, or the weight gradient's split partials.
+struct ConvGeom {
+  int G, Bt, H, W, Cin, Ho, Wo, Cout, stride;
+  const float* x;
+  long long sx;
+  const int32_t* rowmap;
+  const float* dy;
+  const float* Wk;
+  long long sW;
+  float* out;
+};
+enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
+int conv_wgrad_splits(int Bt, int Ho, int Wo);
+int bn_chunks(int R);
+hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st);
+hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, float* W,
+                               float* U, long long sP, float lr, float mom, float wd,
+                               int nesterov, hipStream_t st);
+hipError_t launch_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
+                          float* Wt, hipStream_t st);
+hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
+                           float* mu, float* inv, hipStream_t st);
+hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
+                           const float* inv, const float* gamma, const float* beta,
+                           long long sP, int mode, const float* xin, int Ho, int Wo,
+                           int Cin, float* out, hipStream_t st);
+hipError_t launch_bn_backward(const float* y, const float* gup, const float* maskv,
+                              int G, int R, int C, double* part, const float* mu,
+                              const float* inv, float* coef, float* gamma, float* beta,
+                              float* ug, float* ub, long long sP, float lr, float mom,
+                              int nesterov, float* dy, hipStream_t st);
+hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
+                                int G, int Bt, int H, int W, int Cin, int Cout,
+                                int mode, hipStream_t st);
+hipError_t launch_gap(const float* h, int rows, int S, int C, float* feat, bool bwd,
+                      const float* dfeat, float* dh, hipStream_t st);
 
 // ---------------------------------------------------------------- others
 hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N,

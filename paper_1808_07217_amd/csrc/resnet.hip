@@ -1,0 +1,596 @@
+// Kernels of the ResNet-20-shaped network (the CIFAR ResNet of the paper's
+// model appendix and Table 5), per replica, NHWC activations:
+//
+//  * 3x3 convolutions (padding 1, stride 1 or 2) as implicit GEMMs on the
+//    fp32 matrix cores. The operand loader maps GEMM coordinates to tensor
+//    addresses on the fly -- no im2col buffer:
+//      forward      y[m][co]  = sum_k x(m, k) W[k][co],       k = (kh, kw, ci)
+//      input grad   dx[m][ci] = sum_k dy(m, k) Wt[k][ci],     k = (kh, kw, co)
+//      weight grad  dW[k][co] = sum_m x(m, k) dy[m][co]       (split over m)
+//    where x(m, k) is the padded input at output position m and tap (kh, kw),
+//    dy(m, k) the output gradient that reaches input position m through tap
+//    (kh, kw), and Wt the weight with (ci, co) swapped.
+//  * batch normalisation with batch statistics per replica (the per-worker BN
+//    of the CIFAR setup): fp64 partial sums per row chunk, reduced in a fixed
+//    order, so the statistics are deterministic;
+//  * ReLU, the option-A shortcut (every second pixel, channels zero-padded),
+//    global average pooling.
+#include "kernels.h"
+
+namespace lsgd {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+constexpr int kT = 256;
+
+// ------------------------------------------------------------ conv GEMM
+enum ConvMode : int {
+  CONV_FWD = CONV_FWD_MODE,
+  CONV_DGRAD = CONV_DGRAD_MODE,
+  CONV_WGRAD = CONV_WGRAD_MODE
+};
+
+// Geometry seen by one launch. For CONV_FWD / CONV_WGRAD the "input" is x
+// (H x W x Cin) and the output y (Ho x Wo x Cout); for CONV_DGRAD the roles
+// are as in the forward convolution (x is the input whose gradient is
+// produced).
+struct ConvArgs {
+  int G, Bt;             // replicas, images per replica
+  int H, W, Cin, Ho, Wo, Cout, stride;
+  const float* x;        // input activations [G][Bt][H][W][Cin], or dataset
+  long long sx;          //   group stride (0 with a row map)
+  const int32_t* rowmap; // sampled image indices [G][Bt] (first convolution)
+  const float* dy;       // output gradient [G][Bt][Ho][Wo][Cout]
+  const float* Wk;       // weights: [9*Cin][Cout] (fwd, wgrad), [9*Cout][Cin] (dgrad)
+  long long sW;          //   group stride
+  float* out;            // fwd: y; dgrad: dx; wgrad: partials [S][G][9Cin][Cout]
+  int splits, mchunk;    // wgrad split over the m = (b, oh, ow) rows
+};
+
+// Pointer to element (m, k) of the forward operand x(m, k), nullptr if the
+// tap falls into the padding.
+__device__ __forceinline__ const float* fwd_addr(const ConvArgs& c, int g, int m,
+                                                 int k) {
+  const int HWo = c.Ho * c.Wo;
+  const int b = m / HWo, p = m - b * HWo;
+  const int oh = p / c.Wo, ow = p - oh * c.Wo;
+  const int tap = k / c.Cin, ci = k - tap * c.Cin;
+  const int kh = tap / 3, kw = tap - kh * 3;
+  const int ih = oh * c.stride + kh - 1, iw = ow * c.stride + kw - 1;
+  if (ih < 0 || ih >= c.H || iw < 0 || iw >= c.W) return nullptr;
+  const long long img = c.rowmap ? (long long)c.rowmap[(long long)g * c.Bt + b] * c.H * c.W * c.Cin
+                                 : (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
+  return c.x + img + ((long long)ih * c.W + iw) * c.Cin + ci;
+}
+
+// Pointer to element (m, k) of the input-gradient operand dy(m, k): the
+// output position whose tap (kh, kw) reads input position m.
+__device__ __forceinline__ const float* dgrad_addr(const ConvArgs& c, int g, int m,
+                                                   int k) {
+  const int HW = c.H * c.W;
+  const int b = m / HW, p = m - b * HW;
+  const int h = p / c.W, w = p - h * c.W;
+  const int tap = k / c.Cout, co = k - tap * c.Cout;
+  const int kh = tap / 3, kw = tap - kh * 3;
+  const int th = h + 1 - kh, tw = w + 1 - kw;
+  if (th < 0 || tw < 0 || th % c.stride || tw % c.stride) return nullptr;
+  const int oh = th / c.stride, ow = tw / c.stride;
+  if (oh >= c.Ho || ow >= c.Wo) return nullptr;
+  return c.dy + ((long long)g * c.Bt + b) * c.Ho * c.Wo * c.Cout +
+         ((long long)oh * c.Wo + ow) * c.Cout + co;
+}
+
+// Four consecutive k of one row: one float4 when they share the tap (the
+// channel count is a multiple of 4), else element by element.
+template <int MODE>
+__device__ __forceinline__ float4 load_row4(const ConvArgs& c, int g, int m, int k,
+                                            int kmax, bool vec) {
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (vec && k + 3 < kmax) {
+    const float* p = MODE == CONV_DGRAD ? dgrad_addr(c, g, m, k) : fwd_addr(c, g, m, k);
+    if (p) v = *(const float4*)p;
+    return v;
+  }
+  float t[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (k + e >= kmax) break;
+    const float* p = MODE == CONV_DGRAD ? dgrad_addr(c, g, m, k + e)
+                                        : fwd_addr(c, g, m, k + e);
+    if (p) t[e] = *p;
+  }
+  return make_float4(t[0], t[1], t[2], t[3]);
+}
+
+// 64 x 64 output tile, 4 waves of 32 x 32 (v_mfma_f32_32x32x2f32), BK = 16,
+// double-buffered LDS. Forward / input gradient: rows = spatial positions,
+// columns = output channels (masked to the true count). Weight gradient:
+// rows = (kh, kw, ci), columns = output channels, reduction over a chunk of
+// spatial positions.
+template <int MODE>
+__global__ __launch_bounds__(kT) void k_conv_gemm(ConvArgs c, int vec) {
+  constexpr int BM = 64, BN = 64, BK = 16;
+  constexpr bool AT = MODE == CONV_WGRAD;
+  constexpr int PA = AT ? BM + 4 : BM + 2, PB = BN + 4;
+  __shared__ __attribute__((aligned(16))) float As[2][BK][PA];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK][PB];
+
+  // GEMM shape of this mode
+  const int Mg = MODE == CONV_FWD ? c.Bt * c.Ho * c.Wo
+               : MODE == CONV_DGRAD ? c.Bt * c.H * c.W : 9 * c.Cin;
+  const int Ng = MODE == CONV_DGRAD ? c.Cin : c.Cout;
+  const int Kg = MODE == CONV_FWD ? 9 * c.Cin
+               : MODE == CONV_DGRAD ? 9 * c.Cout : c.Bt * c.Ho * c.Wo;
+  const int tm = (Mg + BM - 1) / BM, tn = (Ng + BN - 1) / BN;
+  int l = blockIdx.x;
+  const int n0 = (l % tn) * BN;
+  l /= tn;
+  const int m0 = (l % tm) * BM;
+  l /= tm;
+  const int s = AT ? l % c.splits : 0;
+  const int g = AT ? l / c.splits : l;
+  const int kbeg = AT ? s * c.mchunk : 0;
+  const int kend = AT ? min(Kg, kbeg + c.mchunk) : Kg;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+  const int lk = lane >> 5, lr = lane & 31;
+  const float* Wg = c.Wk + (long long)g * c.sW;
+
+  float4 ra, rb;
+  auto gload = [&](int k0) {
+    // A: one float4 per thread
+    if constexpr (!AT) {  // rows m (BM of them), 4 float4 of k per row
+      const int r = tid >> 2, kq = k0 + (tid & 3) * 4, m = m0 + r;
+      ra = m < Mg ? load_row4<MODE>(c, g, m, kq, kend, vec) : make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {              // rows k = spatial m, columns i = (kh, kw, ci)
+      const int r = tid >> 4, i0 = m0 + (tid & 15) * 4, kr = k0 + r;
+      ra = kr < kend ? load_row4<CONV_FWD>(c, g, kr, i0, Mg, vec) : make_float4(0.f, 0.f, 0.f, 0.f);
+      // load_row4's bound is on the column here (i < 9*Cin)
+    }
+    // B: [K][N] row-major, 16 rows x 64 columns, one float4 per thread
+    {
+      const int r = tid >> 4, cq = n0 + (tid & 15) * 4, kr = k0 + r;
+      rb = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (kr < kend) {
+        const float* row;
+        if constexpr (AT)
+          row = c.dy + ((long long)g * c.Bt * c.Ho * c.Wo + kr) * c.Cout;
+        else
+          row = Wg + (long long)kr * Ng;
+        float t[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t[e] = cq + e < Ng ? row[cq + e] : 0.f;
+        rb = make_float4(t[0], t[1], t[2], t[3]);
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+    if constexpr (!AT) {
+      const int r = tid >> 2, kq = (tid & 3) * 4;
+      As[buf][kq + 0][r] = ra.x;
+      As[buf][kq + 1][r] = ra.y;
+      As[buf][kq + 2][r] = ra.z;
+      As[buf][kq + 3][r] = ra.w;
+    } else {
+      *(float4*)&As[buf][tid >> 4][(tid & 15) * 4] = ra;
+    }
+    *(float4*)&Bs[buf][tid >> 4][(tid & 15) * 4] = rb;
+  };
+
+  floatx16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  if (nk > 0) {
+    gload(kbeg);
+    lstore(0);
+  }
+  __syncthreads();
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 2)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[buf][kk + lk][wm0 + lr],
+                                                 Bs[buf][kk + lk][wn0 + lr], acc,
+                                                 0, 0, 0);
+    if (it + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  const int n = n0 + wn0 + lr;
+  float* out = AT ? c.out + ((long long)s * c.G + g) * Mg * Ng
+                  : c.out + (long long)g * Mg * Ng;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int m = m0 + wm0 + (v >> 2) * 8 + lk * 4 + (v & 3);
+    if (m < Mg && n < Ng) out[(long long)m * Ng + n] = acc[v];
+  }
+}
+
+// Weight gradient: sum the S partials (ascending s) and apply the update to
+// the [9*Cin][Cout] weight of every replica.
+template <int S>
+__global__ void k_conv_wupdate(const float* part, int G, int n, float* W, float* U,
+                               long long sP, float lr, float mom, float wd,
+                               int nesterov) {
+  const long long total = (long long)G * n;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    float p[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) p[s] = part[i + s * total];
+    float grad = p[0];
+#pragma unroll
+    for (int s = 1; s < S; ++s) grad += p[s];
+    const int g = (int)(i / n);
+    const long long o = (long long)g * sP + (i - (long long)g * n);
+    float w = W[o], u = U[o];
+    const float gr = __builtin_fmaf(wd, w, grad);
+    u = __builtin_fmaf(mom, u, gr);
+    const float d = nesterov ? __builtin_fmaf(mom, u, gr) : u;
+    w = __builtin_fmaf(-lr, d, w);
+    W[o] = w;
+    U[o] = u;
+  }
+}
+
+// Wt[g][(kh, kw, co)][ci] = W[g][(kh, kw, ci)][co]: the weight of the input
+// gradient (channels swapped per tap).
+__global__ void k_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
+                          float* Wt) {
+  const int n = 9 * Cin * Cout;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+       i < (long long)G * n; i += (long long)gridDim.x * blockDim.x) {
+    const int g = (int)(i / n), r = (int)(i % n);
+    const int tap = r / (Cout * Cin), rem = r % (Cout * Cin);
+    const int co = rem / Cin, ci = rem % Cin;
+    Wt[i] = W[(long long)g * sP + ((long long)tap * Cin + ci) * Cout + co];
+  }
+}
+
+// ------------------------------------------------------------ batch norm
+// Partial sums of one row chunk per workgroup, fp64: for the forward pass
+// sum(y) and sum(y^2); for the backward pass sum(dz) and sum(dz * xhat),
+// where dz = upstream gradient (masked by `maskv > 0` when given) and
+// xhat = (y - mu) * inv. Channel count C divides 256.
+constexpr int kChunkRows = 1024;
+
+__global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
+                                                   const float* gup, const float* maskv,
+                                                   const float* mu, const float* inv,
+                                                   double* part, int nchunk) {
+  __shared__ double red[2][kT];
+  const int g = blockIdx.y, ch = blockIdx.x;
+  const int c = threadIdx.x % C, lane_r = threadIdx.x / C, rstep = kT / C;
+  const long long base = (long long)g * R * C;
+  const int r0 = ch * kChunkRows, r1 = min(R, r0 + kChunkRows);
+  const bool bwd = gup != nullptr;
+  const float m_c = bwd ? mu[g * C + c] : 0.f, i_c = bwd ? inv[g * C + c] : 0.f;
+  double s0 = 0.0, s1 = 0.0;
+  for (int rb = r0 + lane_r; rb < r1; rb += 4 * rstep) {
+    float yv[4], gv[4], mv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = rb + u * rstep;
+      const long long o = base + (long long)r * C + c;
+      yv[u] = r < r1 ? y[o] : 0.f;
+      gv[u] = (bwd && r < r1) ? gup[o] : 0.f;
+      mv[u] = (maskv && r < r1) ? maskv[o] : 1.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (rb + u * rstep >= r1) continue;
+      if (!bwd) {
+        s0 += (double)yv[u];
+        s1 += (double)yv[u] * (double)yv[u];
+      } else {
+        const float dz = mv[u] > 0.f ? gv[u] : 0.f;
+        const float xh = (yv[u] - m_c) * i_c;
+        s0 += (double)dz;
+        s1 += (double)dz * (double)xh;
+      }
+    }
+  }
+  red[0][threadIdx.x] = s0;
+  red[1][threadIdx.x] = s1;
+  __syncthreads();
+  for (int w = kT / 2; w >= C; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + w];
+      red[1][threadIdx.x] += red[1][threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if ((int)threadIdx.x < C) {
+    double* p = part + (((long long)g * nchunk + ch) * C + threadIdx.x) * 2;
+    p[0] = red[0][threadIdx.x];
+    p[1] = red[1][threadIdx.x];
+  }
+}
+
+// Forward: mu, inv = 1/sqrt(var + eps) from the partials (chunks in order).
+// Backward: the input-gradient coefficients and the update of gamma, beta:
+//   dbeta = sum dz, dgamma = sum dz*xhat,
+//   dy = gamma*inv*(dz - dbeta/R - xhat*dgamma/R)  -> coef = (gamma*inv,
+//   dbeta/R, dgamma/R); then gamma, beta take a momentum-SGD step (no decay).
+__global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int R,
+                              float* mu, float* inv, float* coef, float* gamma,
+                              float* beta, float* ug, float* ub, long long sP,
+                              float lr, float mom, int nesterov, float eps) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= G * C) return;
+  const int g = i / C, c = i % C;
+  double s0 = 0.0, s1 = 0.0;
+  for (int ch = 0; ch < nchunk; ++ch) {
+    const double* p = part + (((long long)g * nchunk + ch) * C + c) * 2;
+    s0 += p[0];
+    s1 += p[1];
+  }
+  if (coef == nullptr) {  // forward statistics
+    const double m = s0 / R;
+    double var = s1 / R - m * m;
+    if (var < 0.0) var = 0.0;
+    mu[i] = (float)m;
+    inv[i] = (float)(1.0 / sqrt(var + (double)eps));
+    return;
+  }
+  const long long o = (long long)g * sP + c;
+  float gm = gamma[o], bt = beta[o];
+  coef[i * 3 + 0] = gm * inv[i];
+  coef[i * 3 + 1] = (float)(s0 / R);
+  coef[i * 3 + 2] = (float)(s1 / R);
+  float u = ug[o];
+  const float dgm = (float)s1;
+  u = __builtin_fmaf(mom, u, dgm);
+  float d = nesterov ? __builtin_fmaf(mom, u, dgm) : u;
+  gamma[o] = __builtin_fmaf(-lr, d, gm);
+  ug[o] = u;
+  u = ub[o];
+  const float dbt = (float)s0;
+  u = __builtin_fmaf(mom, u, dbt);
+  d = nesterov ? __builtin_fmaf(mom, u, dbt) : u;
+  beta[o] = __builtin_fmaf(-lr, d, bt);
+  ub[o] = u;
+}
+
+// z = gamma*(y - mu)*inv + beta; then one of
+//   mode 0: out = relu(z)
+//   mode 1: out = relu(z + x_in)               (identity shortcut)
+//   mode 2: out = relu(z + shortcutA(x_in))    (stride-2 option-A shortcut)
+__global__ void k_bn_apply(const float* y, int R, int C, const float* mu,
+                           const float* inv, const float* gamma, const float* beta,
+                           long long sP, int G, int mode, const float* xin,
+                           int Ho, int Wo, int Cin, float* out) {
+  const long long total = (long long)G * R * C;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % C);
+    const long long r = i / C;
+    const int g = (int)(r / R);
+    const float z = gamma[(long long)g * sP + c] * (y[i] - mu[g * C + c]) * inv[g * C + c] +
+                    beta[(long long)g * sP + c];
+    float v = z;
+    if (mode == 1) {
+      v += xin[i];
+    } else if (mode == 2) {
+      if (c < Cin) {
+        const long long rr = r - (long long)g * R;   // (b, oh, ow) in replica g
+        const int HWo = Ho * Wo;
+        const int b = (int)(rr / HWo), p = (int)(rr % HWo);
+        const int oh = p / Wo, ow = p % Wo;
+        const int H = 2 * Ho, W = 2 * Wo;
+        v += xin[(((long long)g * (R / HWo) + b) * H * W +
+                  (long long)(2 * oh) * W + 2 * ow) * Cin + c];
+      }
+    }
+    out[i] = v > 0.f ? v : 0.f;
+  }
+}
+
+// dy = coef0 * (dz - coef1 - xhat * coef2) with dz = gup masked by maskv > 0
+// and xhat = (y - mu) * inv.
+__global__ void k_bn_bwd_apply(const float* y, const float* gup, const float* maskv,
+                               int R, int C, int G, const float* mu, const float* inv,
+                               const float* coef, float* dy) {
+  const long long total = (long long)G * R * C;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % C);
+    const int g = (int)(i / ((long long)R * C));
+    const int gc = g * C + c;
+    const float dz = maskv[i] > 0.f ? gup[i] : 0.f;
+    const float xh = (y[i] - mu[gc]) * inv[gc];
+    dy[i] = coef[gc * 3] * (dz - coef[gc * 3 + 1] - xh * coef[gc * 3 + 2]);
+  }
+}
+
+// Gradient reaching a block's input: dx (from the first convolution of the
+// block) plus the shortcut's share of g = dh_out masked by h_out > 0:
+// identity (mode 1) or option A (mode 2: even pixels, first Cin channels).
+__global__ void k_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
+                                int G, int Bt, int H, int W, int Cin, int Cout,
+                                int mode) {
+  const long long total = (long long)G * Bt * H * W * Cin;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    if (mode == 1) {
+      dx[i] += h_out[i] > 0.f ? dh_out[i] : 0.f;
+      continue;
+    }
+    const int ci = (int)(i % Cin);
+    const long long pix = i / Cin;          // (g, b, h, w)
+    const int w = (int)(pix % W);
+    const int h = (int)((pix / W) % H);
+    if ((h & 1) || (w & 1)) continue;
+    const long long gb = pix / ((long long)H * W);
+    const int Ho = H / 2, Wo = W / 2;
+    const long long o = ((gb * Ho + h / 2) * Wo + w / 2) * Cout + ci;
+    dx[i] += h_out[o] > 0.f ? dh_out[o] : 0.f;
+  }
+}
+
+// Global average pool [G*Bt][S][C] -> [G*Bt][C] (sum in ascending position).
+__global__ void k_gap(const float* h, int rows, int S, int C, float* feat) {
+  const long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (i >= (long long)rows * C) return;
+  const long long r = i / C;
+  const int c = (int)(i % C);
+  float s = 0.f;
+  for (int p = 0; p < S; ++p) s += h[(r * S + p) * C + c];
+  feat[i] = s / (float)S;
+}
+
+// dh[r][p][c] = dfeat[r][c] / S (the pool's gradient).
+__global__ void k_gap_bwd(const float* dfeat, int rows, int S, int C, float* dh) {
+  const long long total = (long long)rows * S * C;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % C);
+    const long long r = i / ((long long)S * C);
+    dh[i] = dfeat[r * C + c] / (float)S;
+  }
+}
+
+int blocks_for(long long n) {
+  long long b = (n + kT - 1) / kT;
+  return (int)(b < 1 ? 1 : (b > 16384 ? 16384 : b));
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ launchers
+int conv_wgrad_splits(int Bt, int Ho, int Wo) {
+  const int rows = Bt * Ho * Wo;
+  int s = 1;
+  while (s < 64 && rows / (2 * s) >= 1024) s *= 2;
+  return s;
+}
+
+hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
+  ConvArgs c{};
+  c.G = q.G;
+  c.Bt = q.Bt;
+  c.H = q.H;
+  c.W = q.W;
+  c.Cin = q.Cin;
+  c.Ho = q.Ho;
+  c.Wo = q.Wo;
+  c.Cout = q.Cout;
+  c.stride = q.stride;
+  c.x = q.x;
+  c.sx = q.sx;
+  c.rowmap = q.rowmap;
+  c.dy = q.dy;
+  c.Wk = q.Wk;
+  c.sW = q.sW;
+  c.out = q.out;
+  const int Mg = mode == CONV_FWD ? q.Bt * q.Ho * q.Wo
+               : mode == CONV_DGRAD ? q.Bt * q.H * q.W : 9 * q.Cin;
+  const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
+  const long long tiles = (long long)((Mg + 63) / 64) * ((Ng + 63) / 64);
+  const int vec = (mode == CONV_DGRAD ? q.Cout : q.Cin) % 4 == 0 &&
+                  ((uintptr_t)q.x & 15) == 0 && ((uintptr_t)q.dy & 15) == 0;
+  if (mode == CONV_WGRAD) {
+    c.splits = conv_wgrad_splits(q.Bt, q.Ho, q.Wo);
+    const int rows = q.Bt * q.Ho * q.Wo;
+    c.mchunk = ((rows + c.splits - 1) / c.splits + 15) / 16 * 16;
+    hipLaunchKernelGGL(k_conv_gemm<CONV_WGRAD>, dim3(tiles * c.splits * q.G), dim3(kT),
+                       0, st, c, vec);
+  } else if (mode == CONV_FWD) {
+    hipLaunchKernelGGL(k_conv_gemm<CONV_FWD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
+  } else {
+    hipLaunchKernelGGL(k_conv_gemm<CONV_DGRAD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, float* W,
+                               float* U, long long sP, float lr, float mom, float wd,
+                               int nesterov, hipStream_t st) {
+  const int b = blocks_for((long long)G * n);
+#define LSGD_WU(S)                                                                   \
+  case S:                                                                            \
+    hipLaunchKernelGGL(k_conv_wupdate<S>, dim3(b), dim3(kT), 0, st, part, G, n, W, U, \
+                       sP, lr, mom, wd, nesterov);                                   \
+    break;
+  switch (splits) {
+    LSGD_WU(1)
+    LSGD_WU(2)
+    LSGD_WU(4)
+    LSGD_WU(8)
+    LSGD_WU(16)
+    LSGD_WU(32)
+    LSGD_WU(64)
+    default: return hipErrorInvalidValue;
+  }
+#undef LSGD_WU
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
+                          float* Wt, hipStream_t st) {
+  hipLaunchKernelGGL(k_conv_wt, dim3(blocks_for((long long)G * 9 * Cin * Cout)), dim3(kT),
+                     0, st, W, sP, G, Cin, Cout, Wt);
+  return hipGetLastError();
+}
+
+int bn_chunks(int R) { return (R + kChunkRows - 1) / kChunkRows; }
+
+hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
+                           float* mu, float* inv, hipStream_t st) {
+  const int nch = bn_chunks(R);
+  hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
+                     nullptr, nullptr, nullptr, part, nch);
+  hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
+                     nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
+                     nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
+                           const float* inv, const float* gamma, const float* beta,
+                           long long sP, int mode, const float* xin, int Ho, int Wo,
+                           int Cin, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_bn_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0, st,
+                     y, R, C, mu, inv, gamma, beta, sP, G, mode, xin, Ho, Wo, Cin, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_backward(const float* y, const float* gup, const float* maskv,
+                              int G, int R, int C, double* part, const float* mu,
+                              const float* inv, float* coef, float* gamma, float* beta,
+                              float* ug, float* ub, long long sP, float lr, float mom,
+                              int nesterov, float* dy, hipStream_t st) {
+  const int nch = bn_chunks(R);
+  hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
+                     mu, inv, part, nch);
+  hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
+                     nch, G, C, R, (float*)mu, (float*)inv, coef, gamma, beta, ug, ub,
+                     sP, lr, mom, nesterov, 1e-5f);
+  hipLaunchKernelGGL(k_bn_bwd_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0,
+                     st, y, gup, maskv, R, C, G, mu, inv, coef, dy);
+  return hipGetLastError();
+}
+
+hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
+                                int G, int Bt, int H, int W, int Cin, int Cout,
+                                int mode, hipStream_t st) {
+  hipLaunchKernelGGL(k_shortcut_grad, dim3(blocks_for((long long)G * Bt * H * W * Cin)),
+                     dim3(kT), 0, st, dx, dh_out, h_out, G, Bt, H, W, Cin, Cout, mode);
+  return hipGetLastError();
+}
+
+hipError_t launch_gap(const float* h, int rows, int S, int C, float* feat, bool bwd,
+                      const float* dfeat, float* dh, hipStream_t st) {
+  if (!bwd)
+    hipLaunchKernelGGL(k_gap, dim3((rows * C + 255) / 256), dim3(256), 0, st, h, rows, S,
+                       C, feat);
+  else
+    hipLaunchKernelGGL(k_gap_bwd, dim3(blocks_for((long long)rows * S * C)), dim3(kT), 0,
+                       st, dfeat, rows, S, C, dh);
+  return hipGetLastError();
+}
+
+}  // namespace lsgd

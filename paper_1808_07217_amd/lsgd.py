@@ -23,6 +23,7 @@ if not os.path.exists(LIB_PATH):
 
 MAX_LAYERS = 8
 FP32, BF16 = 0, 1
+MODELS = {"mlp": 0, "resnet20": 1}
 _c = ctypes
 
 
@@ -107,11 +108,12 @@ def _stream_handle(stream) -> _c.c_void_p:
 def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
                 dtype: str = "fp32", momentum: float = 0.0,
                 weight_decay: float = 0.0, nesterov: bool = False,
-                seed: int = 0) -> Config:
+                seed: int = 0, model: str = "mlp") -> Config:
+    """widths: d_0 .. d_L for the MLP; (3072, classes) for resnet20."""
     if not 2 <= len(widths) <= MAX_LAYERS + 1:
         raise ValueError("widths must list d_0 .. d_L with 1 <= L <= 8")
     cfg = Config()
-    cfg.model = 0
+    cfg.model = MODELS[model]
     cfg.n_layers = len(widths) - 1
     for i, w in enumerate(widths):
         cfg.widths[i] = int(w)
