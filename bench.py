@@ -52,10 +52,14 @@ def kernel_cost(tag: str, w) -> tuple:
     P = sum(a * b + b for a, b in zip(d[:-1], d[1:]))
     if tag == "sample":
         return 0, K * B * 4
+    if w.model != "mlp":
+        return None, None
     if tag == "xent":
         return 0, K * B * d[L] * (4 + e) + K * B * 8
     if tag == "average":
         return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0)
+    if w.model != "mlp" or not tag[-1:].isdigit():
+        return None, None        # no per-kernel accounting for this kernel
     name, l = tag.rstrip("0123456789"), int(tag[len(tag.rstrip("0123456789")):])
     din, dout = d[l - 1], d[l]
     mn = din * dout
@@ -74,7 +78,14 @@ def kernel_cost(tag: str, w) -> tuple:
     raise ValueError(tag)
 
 
+# ResNet-20 multiply-adds per image: forward 40,551,040 (Table 5's 0.041 G);
+# the weight gradient repeats them; the input gradient skips the stem.
+RESNET20_MACS, RESNET20_STEM_MACS = 40551040, 32 * 32 * 27 * 16
+
+
 def gemm_flops_per_local_step(w) -> int:
+    if w.model == "resnet20":
+        return 2 * (3 * RESNET20_MACS - RESNET20_STEM_MACS) * w.B_loc * w.K
     d = w.widths
     f = 0
     for l in range(1, len(d)):
@@ -186,8 +197,9 @@ def main():
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: MLP {'-'.join(map(str, w.widths))} "
-                               f"{w.dtype}, K={w.K}, B_loc={w.B_loc}, H={H}",
+        "config": {"workload": (f"{w.name}: MLP {'-'.join(map(str, w.widths))} "
+                                if w.model == "mlp" else f"{w.name}: ResNet-20 ")
+                               + f"{w.dtype}, K={w.K}, B_loc={w.B_loc}, H={H}",
                    "K": w.K, "B_loc": w.B_loc, "H": H,
                    "samples_per_step": samples,
                    "momentum": w.momentum, "nesterov": w.nesterov,
@@ -211,6 +223,7 @@ def main():
         n, ms = rep[dom]
         avg_s = ms / n / 1e3
         flops, nbytes = kernel_cost(dom, w)
+    if not args.no_kernel_timing and flops is not None:
         ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
         if nbytes and flops / nbytes < ridge:
             roof = {"bound": "hbm", "achieved": round(nbytes / avg_s / 1e9, 1),
@@ -226,6 +239,7 @@ def main():
         roof["algorithmic_bytes_per_launch"] = nbytes
         roof["algorithmic_flops_per_launch"] = flops
         out["roofline"] = roof
+    if not args.no_kernel_timing:
         out["kernel_ms_per_step"] = {t: round(v, 4) for t, v in
                                      sorted(per_round.items(),
                                             key=lambda kv: -kv[1])}

@@ -309,7 +309,24 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   const int kbeg = t.s * a.kchunk;
   const int kend = min(a.Kd, kbeg + a.kchunk);
 
-  float4 ra[NA], rb[NB];
+  // two register sets: slab t+2 is loaded while slab t computes and slab t+1
+  // waits in LDS, so each load has two compute phases to arrive
+  float4 ra[2][NA], rb[2][NB];
+  // gathered rows: the forward operand's rows are fixed per thread, so their
+  // dataset indices are read once; the weight gradient walks its rows per
+  // slab, so the workgroup's indices are staged in LDS
+  long long srow[AT ? 1 : NA];
+  __shared__ int32_t srmap[AT && GATHER ? 512 : 1];
+  if constexpr (!AT) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int row = m0 + (tid + i * kThreads) / KV;
+      srow[i] = GATHER ? (row < M ? rmap[row] : 0) : row;
+    }
+  } else if constexpr (GATHER) {
+    for (int i = tid; i < 512 && kbeg + i < kend; i += kThreads) srmap[i] = rmap[kbeg + i];
+    __syncthreads();
+  }
 
   auto load4 = [](const float* p, int avail, int vec) -> float4 {
     if (vec && avail >= 4) return *(const float4*)p;
@@ -321,52 +338,50 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
     return v;
   };
 
-  auto gload = [&](int k0) {
+  auto gload = [&](int k0, int set) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int q = tid + i * kThreads;
-      ra[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      ra[set][i] = make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (!AT) {  // storage [M][Kd]: rows m, KV float4 per row
         const int r = q / KV, c = k0 + (q % KV) * 4, row = m0 + r;
-        if (row < M) {
-          const long long sr = GATHER ? rmap[row] : row;
-          ra[i] = load4(A + sr * a.lda + c, kend - c, vecA);
-        }
+        if (row < M && c < kend) ra[set][i] = load4(A + srow[i] * a.lda + c, kend - c, vecA);
       } else {  // storage [Kd][M]: rows k, BM/4 float4 per row
         const int r = q / (BM / 4), c = m0 + (q % (BM / 4)) * 4, kr = k0 + r;
         if (kr < kend) {
-          const long long sr = GATHER ? rmap[kr] : kr;
-          ra[i] = load4(A + sr * a.lda + c, M - c, vecA);
+          const long long sr = GATHER ? srmap[kr - kbeg] : kr;
+          ra[set][i] = load4(A + sr * a.lda + c, M - c, vecA);
         }
       }
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int q = tid + i * kThreads;
-      rb[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      rb[set][i] = make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (BT) {  // storage [N][Kd]
         const int r = q / KV, c = k0 + (q % KV) * 4, row = n0 + r;
-        if (row < N) rb[i] = load4(B + (long long)row * a.ldb + c, kend - c, vecB);
+        if (row < N && c < kend)
+          rb[set][i] = load4(B + (long long)row * a.ldb + c, kend - c, vecB);
       } else {  // storage [Kd][N]
         const int r = q / (BN / 4), c = n0 + (q % (BN / 4)) * 4, kr = k0 + r;
-        if (kr < kend) rb[i] = load4(B + (long long)kr * a.ldb + c, N - c, vecB);
+        if (kr < kend) rb[set][i] = load4(B + (long long)kr * a.ldb + c, N - c, vecB);
       }
     }
   };
 
-  auto lstore = [&](int buf) {
+  auto lstore = [&](int buf, int set) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int q = tid + i * kThreads;
       if constexpr (!AT) {
         const int r = q / KV, kq = (q % KV) * 4;
-        As[buf][kq + 0][r] = ra[i].x;
-        As[buf][kq + 1][r] = ra[i].y;
-        As[buf][kq + 2][r] = ra[i].z;
-        As[buf][kq + 3][r] = ra[i].w;
+        As[buf][kq + 0][r] = ra[set][i].x;
+        As[buf][kq + 1][r] = ra[set][i].y;
+        As[buf][kq + 2][r] = ra[set][i].z;
+        As[buf][kq + 3][r] = ra[set][i].w;
       } else {
         const int r = q / (BM / 4), c = (q % (BM / 4)) * 4;
-        *(float4*)&As[buf][r][c] = ra[i];
+        *(float4*)&As[buf][r][c] = ra[set][i];
       }
     }
 #pragma unroll
@@ -374,13 +389,13 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
       const int q = tid + i * kThreads;
       if constexpr (BT) {
         const int r = q / KV, kq = (q % KV) * 4;
-        Bs[buf][kq + 0][r] = rb[i].x;
-        Bs[buf][kq + 1][r] = rb[i].y;
-        Bs[buf][kq + 2][r] = rb[i].z;
-        Bs[buf][kq + 3][r] = rb[i].w;
+        Bs[buf][kq + 0][r] = rb[set][i].x;
+        Bs[buf][kq + 1][r] = rb[set][i].y;
+        Bs[buf][kq + 2][r] = rb[set][i].z;
+        Bs[buf][kq + 3][r] = rb[set][i].w;
       } else {
         const int r = q / (BN / 4), c = (q % (BN / 4)) * 4;
-        *(float4*)&Bs[buf][r][c] = rb[i];
+        *(float4*)&Bs[buf][r][c] = rb[set][i];
       }
     }
   };
@@ -402,15 +417,8 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
     if (vecC) SV::fetch(a, t, 0, wpre, upre);
   }
   const int nk = (kend - kbeg + BK - 1) / BK;
-  if (nk > 0) {
-    gload(kbeg);
-    lstore(0);
-  }
-  __syncthreads();
   const int lk = lane >> 5, lr = lane & 31;
-  for (int it = 0; it < nk; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 2) {
       float av[FM], bv[FN];
@@ -429,9 +437,24 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
 #pragma unroll 8
       for (int k = 0; k < BK; ++k) colsum += Bs[buf][k][tid];
     }
-    if (it + 1 < nk) lstore(buf ^ 1);
+  };
+  // slab t lives in LDS buffer t % 2 and register set t % 2
+  if (nk > 0) gload(kbeg, 0);
+  if (nk > 1) gload(kbeg + BK, 1);
+  if (nk > 0) lstore(0, 0);
+  __syncthreads();
+  int it = 0;
+  for (; it + 1 < nk; it += 2) {
+    if (it + 2 < nk) gload(kbeg + (it + 2) * BK, 0);
+    compute(0);
+    lstore(1, 1);
+    __syncthreads();
+    if (it + 3 < nk) gload(kbeg + (it + 3) * BK, 1);
+    compute(1);
+    if (it + 2 < nk) lstore(0, 0);
     __syncthreads();
   }
+  if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
 
   if constexpr (EPI == EPI_SGD) {
     if (vecC)

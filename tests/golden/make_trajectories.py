@@ -21,7 +21,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 import workloads as wk  # noqa: E402
 from oracle import lsgd_oracle as O  # noqa: E402
 
-FULL_RUNS = ["mlp_512", "postlocal_mlp_512", "wide_mlp_2048_bf16"]
+FULL_RUNS = ["mlp_512", "postlocal_mlp_512", "wide_mlp_2048_bf16", "resnet20"]
 
 
 def trajectory(name):
