@@ -316,7 +316,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   // dataset indices are read once; the weight gradient walks its rows per
   // slab, so the workgroup's indices are staged in LDS
   long long srow[AT ? 1 : NA];
-  __shared__ int32_t srmap[AT && GATHER ? 512 : 1];
+  __shared__ int32_t srmap[AT && GATHER ? 512 : 1];  // beyond: read rmap
   if constexpr (!AT) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
@@ -349,7 +349,8 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
       } else {  // storage [Kd][M]: rows k, BM/4 float4 per row
         const int r = q / (BM / 4), c = m0 + (q % (BM / 4)) * 4, kr = k0 + r;
         if (kr < kend) {
-          const long long sr = GATHER ? srmap[kr - kbeg] : kr;
+          const long long sr =
+              GATHER ? (kr - kbeg < 512 ? srmap[kr - kbeg] : rmap[kr]) : kr;
           ra[set][i] = load4(A + sr * a.lda + c, M - c, vecA);
         }
       }

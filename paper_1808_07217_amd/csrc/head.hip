@@ -299,6 +299,132 @@ __global__ __launch_bounds__(256) void k_head_wgrad(HeadArgs h) {
   if (threadIdx.x == 0 && h.loss) h.loss[k] = red[0] / (float)B;
 }
 
+// Register-resident variant for fp32, a class count fixed at compile time,
+// D % 256 == 0 and D <= 512: lane l
+// owns inputs d = 256 j + 4 l .. +3 (j < D / 256) of two sample rows and the
+// matching rows W_L[d][0..C-1]; all of them are loaded in one batch, so the
+// logits, the loss, dZ and the masked input gradient cost one memory round
+// trip. The loss and gradient formulas are those of k_head_fwd; only the
+// split of the logit sums over lanes differs (each lane's inputs in ascending
+// d, then the same xor butterfly).
+template <int C, int NJ>
+__global__ __launch_bounds__(256) void k_head_fwd_vec(HeadArgs h) {
+  constexpr int RPW = 2;
+  const int k = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int D = h.D;
+  const float* Wg = (const float*)h.W + (long long)k * h.sW;
+  long long rr[RPW];
+  bool live[RPW];
+  float4 a[RPW][NJ];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int row = (blockIdx.x * 4 + wave) * RPW + q;
+    live[q] = row < h.B;
+    rr[q] = (long long)k * h.B + (live[q] ? row : 0);
+    const float* arow = (const float*)h.A + (long long)k * h.sA +
+                        (long long)(live[q] ? row : 0) * D;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) a[q][j] = *(const float4*)(arow + 256 * j + 4 * lane);
+  }
+  // W rows d .. d+3 are 4*C consecutive floats (C float4 when C is even)
+  static_assert(C % 2 == 0 && C <= 16, "class count");
+  float wr[NJ][4 * C];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const float* wp = Wg + (long long)(256 * j + 4 * lane) * C;
+#pragma unroll
+    for (int v = 0; v < C; ++v) {
+      const float4 t = *(const float4*)(wp + 4 * v);
+      wr[j][4 * v] = t.x;
+      wr[j][4 * v + 1] = t.y;
+      wr[j][4 * v + 2] = t.z;
+      wr[j][4 * v + 3] = t.w;
+    }
+  }
+  float z[RPW][C];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q)
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      float acc = 0.f;
+      {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          acc = __builtin_fmaf(a[q][j].x, wr[j][0 * C + c], acc);
+          acc = __builtin_fmaf(a[q][j].y, wr[j][1 * C + c], acc);
+          acc = __builtin_fmaf(a[q][j].z, wr[j][2 * C + c], acc);
+          acc = __builtin_fmaf(a[q][j].w, wr[j][3 * C + c], acc);
+        }
+      }
+      z[q][c] = acc;
+    }
+  const float* bias = h.bias + (long long)k * h.sP;
+  const float invB = 1.0f / (float)h.B;
+  float dz[RPW][C];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      z[q][c] = wave_sum(z[q][c]) + bias[c];
+    const int lab = h.y[h.rowmap[rr[q]]];
+    float m = z[q][0];
+#pragma unroll
+    for (int c = 1; c < C; ++c)
+      m = fmaxf(m, z[q][c]);
+    float sum = 0.f, rest = 0.f, zy = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      {
+        const float e = __expf(z[q][c] - m);
+        sum += e;
+        if (c != lab) rest += e;
+        else zy = z[q][c];
+      }
+    const float loss = zy >= m ? log1pf(rest) : (m - zy) + logf(sum);
+    const float inv_s = 1.0f / sum;
+    float mine = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      dz[q][c] = 0.f;
+      {
+        const float p = __expf(z[q][c] - m) * inv_s;
+        dz[q][c] = (p - (c == lab ? 1.f : 0.f)) * invB;
+        if (c == lane) mine = dz[q][c];
+      }
+    }
+    if (live[q]) {
+      if (lane < C) ((float*)h.dZ)[rr[q] * C + lane] = mine;
+      if (lane == 0) h.rowloss[rr[q]] = loss;
+    }
+  }
+  if (!h.dZprev) return;
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    if (!live[q]) continue;
+    float* out = (float*)h.dZprev + rr[q] * D;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float acc = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+          acc = __builtin_fmaf(dz[q][c], wr[j][e * C + c], acc);
+        v[e] = acc;
+      }
+      const float4 av = a[q][j];
+      float4 o;
+      o.x = (h.nomask || av.x > 0.f) ? v[0] : 0.f;
+      o.y = (h.nomask || av.y > 0.f) ? v[1] : 0.f;
+      o.z = (h.nomask || av.z > 0.f) ? v[2] : 0.f;
+      o.w = (h.nomask || av.w > 0.f) ? v[3] : 0.f;
+      *(float4*)(out + 256 * j + 4 * lane) = o;
+    }
+  }
+}
+
 template <typename T, int CMAX>
 hipError_t launch_pair(const HeadArgs& h, hipStream_t s, int which) {
   const bool gather = h.gather != 0;  // the top layer is layer 1
@@ -318,9 +444,22 @@ hipError_t launch_pair(const HeadArgs& h, hipStream_t s, int which) {
   return hipGetLastError();
 }
 
+bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
 hipError_t launch_head(int dtype, const HeadArgs& h, hipStream_t s, int which) {
   if (h.C < 1 || h.C > kHeadMaxClasses) return hipErrorInvalidValue;
   if (h.K > 65535 || h.B < 1 || h.D < 1) return hipErrorInvalidValue;
+  // register-resident forward when the shapes and alignment allow it
+  if (which == 0 && dtype == 0 && !h.gather && h.C == 10 && h.D % 256 == 0 &&
+      h.D <= 512 && h.sA % 4 == 0 && h.sW % 4 == 0 && al16(h.A) && al16(h.W) &&
+      (h.dZprev == nullptr || al16(h.dZprev))) {
+    dim3 grid((h.B + 7) / 8, h.K);
+    if (h.D == 256)
+      hipLaunchKernelGGL((k_head_fwd_vec<10, 1>), grid, dim3(256), 0, s, h);
+    else
+      hipLaunchKernelGGL((k_head_fwd_vec<10, 2>), grid, dim3(256), 0, s, h);
+    return hipGetLastError();
+  }
   if (dtype == 1)
     return h.C <= 16 ? launch_pair<bf16_t, 16>(h, s, which)
                      : launch_pair<bf16_t, 32>(h, s, which);

@@ -78,10 +78,20 @@ def _compare_steps(w, X, y, w0, param_tol, loss_tol, rounds=None):
     ((130, 200, 66, 100, 7), True, 0.9),
     ((50, 24, 20), False, 0.9),        # 17..32 classes: wider head variant
     ((40, 33, 45), True, 0.9),         # > 32 classes: generic GEMM + loss path
+    ((100, 256, 10), False, 0.9),      # register-resident head, 256 inputs
+    ((48, 512, 512, 10), True, 0.9),   # register-resident head, 512 inputs
 ])
 def test_small_mlp_every_step(widths, nesterov, momentum):
     w = _small(widths, nesterov=nesterov, momentum=momentum)
     print(f"small fp32 {widths} nesterov={nesterov}", flush=True)
+    X, y, w0 = _small_data(w)
+    _compare_steps(w, X, y, w0, PARAM_TOL_FP32, 1e-4)
+
+
+def test_batch_larger_than_the_gathered_row_cache():
+    """A local batch of 600 rows (the weight-gradient kernel caches 512
+    gathered row indices in LDS and reads the rest from memory)."""
+    w = _small((70, 36, 10), B=600, N=5000, K=2, H=2, rounds=1, lr=0.01)
     X, y, w0 = _small_data(w)
     _compare_steps(w, X, y, w0, PARAM_TOL_FP32, 1e-4)
 
