@@ -36,6 +36,10 @@ def parse():
     p.add_argument("--workload", default="mlp_512")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-kernel-timing", action="store_true")
+    p.add_argument("--traffic-from", metavar="DIR",
+                   help="no GPU run: turn the rocprofv3 FETCH_SIZE / "
+                        "WRITE_SIZE passes under DIR (fetch/, write/) into "
+                        f"{os.path.relpath(TRAFFIC_FILE, ROOT)}")
     return p.parse_args()
 
 
@@ -58,6 +62,10 @@ def kernel_cost(tag: str, w) -> tuple:
         return 0, K * B * d[L] * (4 + e) + K * B * 8
     if tag == "average":
         return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0)
+    if tag == "wgrad_update":   # one launch over every generic layer
+        Lg = L - 1 if d[L] <= 32 else L   # the top layer has its own kernels
+        costs = [kernel_cost(f"wgrad_update{l}", w) for l in range(1, Lg + 1)]
+        return sum(c[0] for c in costs), sum(c[1] for c in costs)
     if w.model != "mlp" or not tag[-1:].isdigit():
         return None, None        # no per-kernel accounting for this kernel
     name, l = tag.rstrip("0123456789"), int(tag[len(tag.rstrip("0123456789")):])
@@ -98,7 +106,7 @@ def gemm_flops_per_local_step(w) -> int:
 
 def source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("gemm.hip", "elementwise.hip"):
+    for f in ("kernels.h", "gemm.hip", "elementwise.hip"):
         with open(os.path.join(ROOT, "paper_1808_07217_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -115,6 +123,64 @@ def traffic_for(tag: str):
     if t.get("source_digest") != source_digest() or t.get("tag") != tag:
         return None
     return t.get("bytes_per_launch")
+
+
+# Kernel (as rocprofv3 names it) behind a launch tag of the MLP workloads:
+# the persistent fused weight-gradient + update kernel over the hidden
+# layers, and the K-way average, the copy-like kernel used to scale the
+# counters.
+TAG_KERNEL = {
+    "wgrad_update": "gemm_f32_sgd_ws<",
+    "average": "k_average4<",
+}
+
+
+def _counter_means(path: str, counter: str) -> dict:
+    """{kernel name: mean counter value (KiB) per dispatch} from one
+    rocprofv3 --pmc pass (its *_counter_collection.csv)."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"),
+                      recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {path}")
+    acc = {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def write_traffic(pmc_dir: str, w) -> dict:
+    """HBM bytes per launch of the dominant kernel from two counter passes,
+    each scaled by what the same counter reads for the K-way average, whose
+    traffic is known exactly (K P fp32 words read and written)."""
+    def pick(table, key):
+        hits = [v for k, v in table.items() if key in k]
+        if len(hits) != 1:
+            raise SystemExit(f"{key!r} matches {len(hits)} kernels")
+        return hits[0] * 1024.0
+    fetch = _counter_means(os.path.join(pmc_dir, "fetch"), "FETCH_SIZE")
+    write = _counter_means(os.path.join(pmc_dir, "write"), "WRITE_SIZE")
+    P = sum(a * b + b for a, b in zip(w.widths[:-1], w.widths[1:]))
+    avg_bytes = 4.0 * w.K * P
+    f_scale = avg_bytes / pick(fetch, TAG_KERNEL["average"])
+    w_scale = avg_bytes / pick(write, TAG_KERNEL["average"])
+    tag = "wgrad_update"
+    rd = pick(fetch, TAG_KERNEL[tag]) * f_scale
+    wr = pick(write, TAG_KERNEL[tag]) * w_scale
+    out = {"tag": tag, "kernel": TAG_KERNEL[tag], "workload": w.name,
+           "source_digest": source_digest(),
+           "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+           "read_bytes_per_launch": round(rd), "write_bytes_per_launch": round(wr),
+           "bytes_per_launch": round(rd + wr),
+           "algorithmic_bytes_per_launch": kernel_cost(tag, w)[1]}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    return out
 
 
 def cpu_baseline(w, X, y, w0):
@@ -142,6 +208,10 @@ def cpu_baseline(w, X, y, w0):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        import workloads as wk
+        print(json.dumps(write_traffic(args.traffic_from, wk.get(args.workload))))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU "
               "path (the K workers are replicas on one device)", file=sys.stderr)
@@ -170,8 +240,26 @@ def main():
     def rnd(i):
         reps.run_round(lrs, loss[i * H:(i + 1) * H])
 
+    # Warmup. The rounds after the first bracket every launch with HIP events
+    # (per-kernel breakdown, and the dominant kernel); the timed rounds then
+    # bracket two of the dominant kernel's launches per round (each bracket
+    # costs the stream some microseconds), on the stream it is launched on.
+    timing = not args.no_kernel_timing and args.warmup >= 1
+    prof_rounds = 0
     for i in range(args.warmup):
+        if timing and (i >= 1 or args.warmup == 1):
+            reps.profile(True)
+            prof_rounds += 1
         rnd(i)
+    dom = None
+    if timing:
+        rep = reps.profile_report()
+        reps.profile(False)
+        per_round = {t: ms / prof_rounds for t, (n, ms) in rep.items()}
+        dom = max(per_round, key=per_round.get)
+        per_round_launches = rep[dom][0] // prof_rounds
+        reps.profile_select(dom, every=max(1, per_round_launches // 2))
+        reps.profile(True)
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -182,6 +270,12 @@ def main():
             rnd(args.warmup + i)
         ev1.record(stream)
     torch.cuda.synchronize()
+    if timing:
+        n, ms = reps.profile_report()[dom]
+        reps.profile(False)
+        reps.profile_select(None)
+        avg_s = ms / n / 1e3
+        flops, nbytes = kernel_cost(dom, w)
     wall = time.perf_counter() - t0
     gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
@@ -209,21 +303,7 @@ def main():
     out["e2e_mfma_frac"] = round(gemm_flops / (ms_per_step / 1e3) /
                                  (PEAK_TFLOPS[w.dtype] * 1e12), 4)
 
-    if not args.no_kernel_timing:
-        # a second pass with every launch bracketed by HIP events
-        reps.profile(True)
-        base = args.warmup + args.steps
-        for i in range(min(args.steps, 8)):
-            rnd(base + i)
-        rep = reps.profile_report()
-        reps.profile(False)
-        nround = min(args.steps, 8)
-        per_round = {t: ms / nround for t, (n, ms) in rep.items()}
-        dom = max(per_round, key=per_round.get)
-        n, ms = rep[dom]
-        avg_s = ms / n / 1e3
-        flops, nbytes = kernel_cost(dom, w)
-    if not args.no_kernel_timing and flops is not None:
+    if timing and flops is not None:
         ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
         if nbytes and flops / nbytes < ridge:
             roof = {"bound": "hbm", "achieved": round(nbytes / avg_s / 1e9, 1),
@@ -236,10 +316,12 @@ def main():
         roof["traffic"] = traffic_for(dom)
         roof["kernel"] = dom
         roof["avg_launch_us"] = round(avg_s * 1e6, 2)
+        roof["launches_timed"] = n
         roof["algorithmic_bytes_per_launch"] = nbytes
         roof["algorithmic_flops_per_launch"] = flops
         out["roofline"] = roof
-    if not args.no_kernel_timing:
+    if timing:
+        # from the event-bracketed warmup rounds
         out["kernel_ms_per_step"] = {t: round(v, 4) for t, v in
                                      sorted(per_round.items(),
                                             key=lambda kv: -kv[1])}

@@ -173,6 +173,15 @@ const char* lsgd_last_error(const lsgd_ctx* ctx);
  * kernels). */
 lsgd_status lsgd_profile_enable(lsgd_ctx* ctx, int32_t enable);
 
+/* Restrict the bracketing to launches tagged `tag` (host string, at most 64
+ * characters, copied; NULL or "" selects every launch again), and of those
+ * to the 1st, (every+1)-th, (2 every+1)-th ... counted from this call, so
+ * that one kernel can be timed inside a run at a sampling rate that leaves
+ * the run's own speed nearly undisturbed (each bracket costs some
+ * microseconds of stream time). LSGD_E_INVALID for a longer tag or
+ * every < 1. */
+lsgd_status lsgd_profile_select(lsgd_ctx* ctx, const char* tag, int32_t every);
+
 /* Synchronise, then write one line "tag launches total_ms" per tag into the
  * host buffer h_buf (NUL-terminated; LSGD_E_INVALID if len is too small) and
  * clear the records. */

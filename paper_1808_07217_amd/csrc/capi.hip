@@ -204,6 +204,9 @@ Layout make_layout(const lsgd_config* c) {
 // around every kernel launch, tagged by launch site.
 struct Profiler {
   bool on = false;
+  std::string only;  // non-empty: bracket only launches with this tag,
+  int every = 1;     // and of those only every `every`-th
+  long long seen = 0;
   std::vector<hipEvent_t> pool;
   size_t used = 0;
   struct Rec { std::string tag; hipEvent_t a, b; };
@@ -212,12 +215,18 @@ struct Profiler {
   hipError_t event(hipEvent_t* e) {
     if (used == pool.size()) {
       hipEvent_t ev;
-      hipError_t r = hipEventCreate(&ev);
+      // timing only: no system-scope fence (and its cache writeback) at
+      // each record, so the bracketed kernels run as they would unobserved
+      hipError_t r = hipEventCreateWithFlags(&ev, hipEventDisableSystemFence);
       if (r != hipSuccess) return r;
       pool.push_back(ev);
     }
     *e = pool[used++];
     return hipSuccess;
+  }
+  bool wants(const std::string& tag) {
+    if (only.empty()) return true;
+    return tag == only && seen++ % every == 0;
   }
   ~Profiler() {
     for (hipEvent_t e : pool) (void)hipEventDestroy(e);
@@ -280,17 +289,18 @@ struct lsgd_ctx {
   } while (0)
 
 // A kernel launch on stream `st`, bracketed by profiling events on that
-// stream when profiling is on.
+// stream when profiling is on (and the tag is selected).
 #define LSGD_LAUNCH_ON(ctx, st, tag, expr)                                 \
   do {                                                                     \
     hipEvent_t a_ = nullptr, b_ = nullptr;                                 \
-    if ((ctx)->prof.on) {                                                  \
+    const bool p_ = (ctx)->prof.on && (ctx)->prof.wants(tag);              \
+    if (p_) {                                                              \
       LSGD_CK(ctx, (ctx)->prof.event(&a_));                                \
       LSGD_CK(ctx, (ctx)->prof.event(&b_));                                \
       LSGD_CK(ctx, hipEventRecord(a_, (st)));                              \
     }                                                                      \
     LSGD_CK(ctx, expr);                                                    \
-    if ((ctx)->prof.on) {                                                  \
+    if (p_) {                                                              \
       LSGD_CK(ctx, hipEventRecord(b_, (st)));                              \
       (ctx)->prof.recs.push_back({std::string(tag), a_, b_});              \
     }                                                                      \
@@ -300,6 +310,52 @@ struct lsgd_ctx {
 namespace {
 
 lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss);
+
+// Tiles (128 x 128) from which one persistent launch over all hidden layers
+// updates beats per-layer launches (about four per compute unit).
+constexpr int kMergedMinTiles = 1024;
+
+// Weight gradient of layer l fused with its momentum-SGD step and the bias
+// step: G_l = A_{l-1}^T dZ_l over the batch, per replica.
+GemmArgs wgrad_args(const lsgd_ctx* c, int l, float lr) {
+  const lsgd_config& cf = c->cfg;
+  const Layout& ly = c->lay;
+  const int K = cf.K, B = cf.B_loc;
+  const int din = cf.widths[l - 1], dout = cf.widths[l];
+  const bool dt = c->bf16();
+  GemmArgs a{};
+  a.G = K;
+  a.M = din;
+  a.N = dout;
+  a.Kd = B;
+  if (l == 1) {
+    a.A = dt ? (const void*)c->Xb() : (const void*)c->X;
+    a.sA = 0;
+    a.rowmap = c->idx();
+    a.sRow = B;
+  } else {
+    a.A = c->act(l - 1);
+    a.sA = (long long)B * din;
+  }
+  a.lda = din;
+  a.B = c->dZ(l);
+  a.ldb = dout;
+  a.sB = (long long)B * dout;
+  a.ldc = dout;
+  a.sC = ly.Ps;
+  a.W = c->W() + ly.offW[l - 1];
+  a.U = c->U() + ly.offW[l - 1];
+  a.Wb = dt ? c->Wb() + ly.offW[l - 1] : nullptr;
+  a.lr = lr;
+  a.mom = cf.momentum;
+  a.wd = cf.weight_decay;
+  a.nesterov = cf.nesterov;
+  a.bias_w = c->W() + ly.offB[l - 1];
+  a.bias_u = c->U() + ly.offB[l - 1];
+  a.sBiasP = ly.Ps;
+  a.splits = 1;
+  return a;
+}
 
 lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   if (c->lay.resnet) return do_local_step_resnet(c, lr, d_loss);
@@ -402,7 +458,19 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   }
 
   // backward, top layer first. The input gradient of layer l reads the
-  // pre-update W_l, so it is enqueued before W_l's fused update.
+  // pre-update W_l, so it is enqueued before W_l's fused update. When every
+  // hidden layer's update fits the persistent update kernel and together
+  // they fill the chip, the input gradients go first and one launch then
+  // updates all of those layers (their tiles in one list).
+  GemmArgs upd[lsgd::kWsMaxProblems];
+  int nupd = 0;
+  bool merged = false;
+  if (Lg >= 1 && Lg <= lsgd::kWsMaxProblems) {
+    for (int l = 1; l <= Lg; ++l) upd[l - 1] = wgrad_args(c, l, lr);
+    const int tiles = lsgd::gemm_sgd_multi_tiles(dt, upd, Lg);
+    merged = tiles >= kMergedMinTiles;
+    nupd = Lg;
+  }
   for (int l = Lg; l >= 1; --l) {
     const int din = w[l - 1], dout = w[l];
     if (l > 1 && !(ly.head && l == L)) {
@@ -426,37 +494,8 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       LSGD_LAUNCH(c, "dgrad" + std::to_string(l),
                   lsgd::launch_gemm(dt, 0, 1, lsgd::EPI_RELU_MASK, dt, a, s));
     }
-    GemmArgs a{};
-    a.G = K;
-    a.M = din;
-    a.N = dout;
-    a.Kd = B;
-    if (l == 1) {
-      a.A = X0;
-      a.sA = 0;
-      a.rowmap = c->idx();
-      a.sRow = B;
-    } else {
-      a.A = c->act(l - 1);
-      a.sA = (long long)B * din;
-    }
-    a.lda = din;
-    a.B = c->dZ(l);
-    a.ldb = dout;
-    a.sB = (long long)B * dout;
-    a.ldc = dout;
-    a.sC = ly.Ps;
-    a.W = W + ly.offW[l - 1];
-    a.U = U + ly.offW[l - 1];
-    a.Wb = dt ? Wb + ly.offW[l - 1] : nullptr;
-    a.lr = lr;
-    a.mom = cf.momentum;
-    a.wd = cf.weight_decay;
-    a.nesterov = cf.nesterov;
-    a.bias_w = W + ly.offB[l - 1];
-    a.bias_u = U + ly.offB[l - 1];
-    a.sBiasP = ly.Ps;
-    a.splits = 1;
+    if (merged) continue;
+    const GemmArgs a = wgrad_args(c, l, lr);
     if (c->use_side && l > 1) {
       // after its input gradient, layer l's update only has to finish by the
       // end of the step: side stream 1, overlapping the layers below
@@ -469,6 +508,8 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
                   lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
     }
   }
+  if (merged)
+    LSGD_LAUNCH(c, "wgrad_update", lsgd::launch_gemm_sgd_multi(dt, upd, nupd, s));
   if (c->use_side) {  // join: the step ends when all of its updates have
     LSGD_CK(c, hipEventRecord(c->join[1], c->side[1]));
     LSGD_CK(c, hipStreamWaitEvent(s, c->join[0], 0));
@@ -838,6 +879,15 @@ lsgd_status lsgd_profile_enable(lsgd_ctx* ctx, int32_t enable) {
   LSGD_USABLE(ctx);
   if (enable != 0 && enable != 1) return LSGD_E_INVALID;
   ctx->prof.on = enable != 0;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_profile_select(lsgd_ctx* ctx, const char* tag, int32_t every) {
+  LSGD_USABLE(ctx);
+  if ((tag && std::strlen(tag) > 64) || every < 1) return LSGD_E_INVALID;
+  ctx->prof.only = tag ? tag : "";
+  ctx->prof.every = every;
+  ctx->prof.seen = 0;
   return LSGD_OK;
 }
 

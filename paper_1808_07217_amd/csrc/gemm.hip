@@ -468,6 +468,267 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   if (do_bias && tid < BN && n0 + tid < N) bias_update(a, t, n0 + tid, colsum);
 }
 
+// ------------------------------------------------- fp32 update, specialised
+// Fused weight gradient + momentum-SGD update over the 128 x 128 tiles of one
+// or several layers (a list of problems whose tiles are concatenated). A
+// workgroup of 8 wavefronts stays resident and walks its share of the tile
+// list; its waves have two roles that run concurrently:
+//   MFMA waves 0-3 each compute a 64 x 64 quarter of tile j. A lane loads its
+//     operands straight from global memory as float2 pairs along m (resp. n);
+//     the two halves of a pair feed two different 32 x 32 MFMA blocks, so
+//     block i's MFMA row r is m = 2 r + i (columns likewise) and no LDS
+//     staging (and so no barrier among the MFMA waves) is needed. A ring of
+//     D k-pairs of registers keeps D loads in flight.
+//   Update waves 4-7 apply the SGD step to tile j-1 from the gradient tile
+//     in LDS (float4 runs along n: coalesced W/U rows), then issue the W/U
+//     reads of tile j, which arrive while tile j's MFMAs run.
+// Two workgroup barriers per tile hand the LDS gradient buffer over. The
+// HBM-bound update of one tile thus overlaps the MFMA phase of the next,
+// where separate workgroups doing both phases in turn fall into step and
+// alternate between compute-only and memory-only periods across the chip.
+// Every problem needs M % 128 == 0, N % 128 == 0, 8-byte aligned operand
+// rows, 16-byte aligned W/U rows and (gathered rows) Kd <= 512; all share
+// lr, momentum, weight decay and Nesterov.
+constexpr int kWsThreads = 512;
+constexpr int kWsMaxRows = 512;
+constexpr int kWsDepth = 8;        // k-pairs of operands in flight per lane
+constexpr int kWsMinTiles = 1024;  // below: one tile per workgroup is as good
+constexpr int kWsUnrolledRows = 128;  // batch size given a fully unrolled k loop
+
+struct WsArgs {
+  GemmArgs p[kWsMaxProblems];
+  int start[kWsMaxProblems + 1];  // first tile of each problem; [np] = total
+  int np;
+};
+
+struct WsTile {
+  int pi, g, m0, n0;
+};
+
+__device__ __forceinline__ bool ws_tile(const WsArgs& w, int j, WsTile& t) {
+  const int total = w.start[w.np];
+  const int p = blockIdx.x, nwg = gridDim.x;
+  int l;
+  if (total % kXcds == 0 && nwg % kXcds == 0) {
+    // XCD x = p % 8 owns tiles [x * total/8, (x+1) * total/8)
+    const int chunk = total / kXcds, q = p / kXcds + j * (nwg / kXcds);
+    if (q >= chunk) return false;
+    l = (p % kXcds) * chunk + q;
+  } else {
+    const long long ll = p + (long long)j * nwg;
+    if (ll >= total) return false;
+    l = (int)ll;
+  }
+  int pi = 0;
+  while (pi + 1 < w.np && l >= w.start[pi + 1]) ++pi;
+  l -= w.start[pi];
+  const int tn = w.p[pi].N / 128, per_g = tn * (w.p[pi].M / 128);
+  t.pi = pi;
+  t.g = l / per_g;
+  l -= t.g * per_g;
+  t.m0 = (l / tn) * 128;
+  t.n0 = (l % tn) * 128;
+  return true;
+}
+
+// Row list (sampled dataset indices) of a gathered tile: thread t < 256 of
+// the MFMA role holds entries t and t + 256 (clamped to the last row).
+struct WsRows {
+  int32_t r0, r1;
+};
+__device__ __forceinline__ WsRows ws_rows_load(const WsArgs& w, const WsTile& t) {
+  const GemmArgs& a = w.p[t.pi];
+  const int32_t* rm = a.rowmap + (long long)t.g * a.sRow;
+  const int last = a.Kd - 1, i = threadIdx.x;
+  return WsRows{rm[min(i, last)], rm[min(i + 256, last)]};
+}
+__device__ __forceinline__ void ws_rows_store(int32_t* buf, const WsRows& r) {
+  buf[threadIdx.x] = r.r0;
+  buf[threadIdx.x + 256] = r.r1;
+}
+
+// Both roles walk the same tile list and execute the same barriers: one
+// before the first tile, then two per tile.
+template <int D>
+__global__ __launch_bounds__(kWsThreads) void gemm_f32_sgd_ws(WsArgs w) {
+  constexpr int T = 128, CP = T + 4;  // gradient tile pitch (16-byte rows)
+  constexpr int PER = T * T / 4 / 256;  // float4 per update thread
+  __shared__ __attribute__((aligned(16))) float Gs[T * CP];
+  // row lists, double-buffered: tile j reads buffer j % 2 while the MFMA
+  // role writes tile j+1's list into the other one after its k loop
+  __shared__ int32_t srmap[2][kWsMaxRows];
+  // wave index as a scalar: the role branch below is uniform per wave
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  WsTile cur, prev;
+  bool prev_ok = false;
+
+  if (wave < 4) {
+    // ---- MFMA role: gradient tile j into LDS
+    const int lk = lane >> 5, lr = lane & 31;
+    const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * 64;
+    {
+      WsTile t0;
+      if (ws_tile(w, 0, t0) && w.p[t0.pi].rowmap) ws_rows_store(srmap[0], ws_rows_load(w, t0));
+    }
+    __syncthreads();  // row list of the first tile
+    for (int j = 0;; ++j) {
+      const bool ok = ws_tile(w, j, cur);  // uniform over the workgroup
+      if (!ok && !prev_ok) break;
+      floatx16 acc[2][2];
+      if (ok) {
+        // next tile's row list: issued now, stored after the k loop
+        WsTile nxt;
+        const bool nxt_rows = ws_tile(w, j + 1, nxt) && w.p[nxt.pi].rowmap;
+        WsRows nr{0, 0};
+        if (nxt_rows) nr = ws_rows_load(w, nxt);
+
+        const GemmArgs& a = w.p[cur.pi];
+        const int Kd = a.Kd, nblk = ((Kd + 1) / 2 + D - 1) / D;
+        const bool gather = a.rowmap != nullptr;
+        const int32_t* srm = srmap[j & 1];
+        const float* A = (const float*)a.A + (long long)cur.g * a.sA + cur.m0 + wm0 + 2 * lr;
+        const float* B = (const float*)a.B + (long long)cur.g * a.sB + cur.n0 + wn0 + 2 * lr;
+        const long long lda = a.lda, ldb = a.ldb;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][jj][v] = 0.f;
+        // k = 2 kp + lk; rows past the end are clamped to the last one here
+        // and their values replaced by zero at use, so the loads carry no
+        // branches and stay countable in flight
+        float2 ra[D], rb[D];
+        auto load = [&](int kp, float2& x, float2& y) {
+          const int k = min(2 * kp + lk, Kd - 1);
+          const int sr = srm[min(k, kWsMaxRows - 1)];
+          const long long row = gather ? (long long)sr : (long long)k;
+          x = *(const float2*)(A + row * lda);
+          y = *(const float2*)(B + (long long)k * ldb);
+        };
+#pragma unroll
+        for (int d = 0; d < D; ++d) load(d, ra[d], rb[d]);
+        float cs0 = 0.f, cs1 = 0.f;
+        auto slot = [&](int kp, int d) {
+          const bool live = 2 * kp + lk < Kd;
+          const float a0 = live ? ra[d].x : 0.f, a1 = live ? ra[d].y : 0.f;
+          const float b0 = live ? rb[d].x : 0.f, b1 = live ? rb[d].y : 0.f;
+          acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+          acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+          acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+          acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+          cs0 += b0;
+          cs1 += b1;
+          load(kp + D, ra[d], rb[d]);
+          // keep each refill right behind its slot's MFMAs: left alone, the
+          // scheduler sinks the refills to the end of the block, where they
+          // have no time left to arrive
+          __builtin_amdgcn_sched_barrier(0);
+        };
+        if (Kd == kWsUnrolledRows) {
+          // straight-line code: the wait before each slot's MFMAs counts
+          // exactly the D - 1 younger refills, which a runtime loop's
+          // back edge hides from the compiler (it then waits for all)
+#pragma unroll
+          for (int kp = 0; kp < kWsUnrolledRows / 2; ++kp) slot(kp, kp % D);
+        } else {
+          for (int blk = 0; blk < nblk; ++blk) {
+#pragma unroll
+            for (int d = 0; d < D; ++d) slot(blk * D + d, d);
+          }
+        }
+        if (nxt_rows) ws_rows_store(srmap[(j + 1) & 1], nr);
+        if (a.bias_w && cur.m0 == 0 && wm0 == 0) {
+          // lanes < 32 summed the even batch rows, lanes >= 32 the odd ones
+          cs0 += __shfl_xor(cs0, 32, 64);
+          cs1 += __shfl_xor(cs1, 32, 64);
+          if (lk == 0) {
+            Tile bt;
+            bt.g = cur.g;
+            const int n = cur.n0 + wn0 + 2 * lr;
+            bias_update(a, bt, n, cs0);
+            bias_update(a, bt, n + 1, cs1);
+          }
+        }
+      }
+      __syncthreads();  // the update role has consumed gradient tile j-1
+      if (ok) {
+        // accumulator v of block (i, jj): row 8(v/4) + 4 lk + v%4, column lr
+        // of the block, i.e. tile row wm0 + 2 R + i, column wn0 + 2 lr + jj
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int R = (v >> 2) * 8 + lk * 4 + (v & 3);
+            *(float2*)&Gs[(wm0 + 2 * R + i) * CP + wn0 + 2 * lr] =
+                make_float2(acc[i][0][v], acc[i][1][v]);
+          }
+      }
+      __syncthreads();  // gradient tile j (and tile j+1's row list) in LDS
+      prev_ok = ok;
+    }
+  } else {
+    // ---- update role: SGD step of tile j-1, then tile j's W/U reads
+    const int u = (int)threadIdx.x - 256;
+    float4 wv[PER], uv[PER];
+    __syncthreads();  // row list of the first tile
+    for (int j = 0;; ++j) {
+      const bool ok = ws_tile(w, j, cur);
+      if (!ok && !prev_ok) break;
+      if (prev_ok) {
+        const GemmArgs& a = w.p[prev.pi];
+#pragma unroll
+        for (int p = 0; p < PER; ++p) {
+          const int r = u / 32 + 8 * p, c = (u % 32) * 4;
+          const long long off = (long long)prev.g * a.sC +
+                                (long long)(prev.m0 + r) * a.ldc + prev.n0 + c;
+          const float4 gr = *(const float4*)&Gs[r * CP + c];
+          float4 wq = wv[p], uq = uv[p];
+          sgd_step(wq.x, uq.x, gr.x, a);
+          sgd_step(wq.y, uq.y, gr.y, a);
+          sgd_step(wq.z, uq.z, gr.z, a);
+          sgd_step(wq.w, uq.w, gr.w, a);
+          *(float4*)(a.W + off) = wq;
+          *(float4*)(a.U + off) = uq;
+          if (a.Wb) {
+            const uint32_t lo = f32_to_bf16(wq.x) | ((uint32_t)f32_to_bf16(wq.y) << 16);
+            const uint32_t hi = f32_to_bf16(wq.z) | ((uint32_t)f32_to_bf16(wq.w) << 16);
+            *(uint2*)(a.Wb + off) = make_uint2(lo, hi);
+          }
+        }
+      }
+      if (ok) {
+        const GemmArgs& a = w.p[cur.pi];
+#pragma unroll
+        for (int p = 0; p < PER; ++p) {
+          const int r = u / 32 + 8 * p, c = (u % 32) * 4;
+          const long long off = (long long)cur.g * a.sC +
+                                (long long)(cur.m0 + r) * a.ldc + cur.n0 + c;
+          wv[p] = *(const float4*)(a.W + off);
+          uv[p] = *(const float4*)(a.U + off);
+        }
+      }
+      __syncthreads();  // gradient tile j-1 consumed
+      __syncthreads();  // gradient tile j is in LDS
+      prev = cur;
+      prev_ok = ok;
+    }
+  }
+}
+
+// Shape and alignment rules of the specialised kernel for one problem.
+bool ws_eligible(int dtype, const GemmArgs& a) {
+  auto al = [](const void* p, uintptr_t m) { return ((uintptr_t)p & m) == 0; };
+  return dtype == 0 && a.splits <= 1 && a.G > 0 && a.M > 0 && a.N > 0 && a.Kd > 0 &&
+         a.M % 128 == 0 && a.N % 128 == 0 &&
+         (a.rowmap == nullptr || a.Kd <= kWsMaxRows) &&
+         a.lda % 2 == 0 && a.sA % 2 == 0 && al(a.A, 7) &&
+         a.ldb % 2 == 0 && a.sB % 2 == 0 && al(a.B, 7) &&
+         a.ldc % 4 == 0 && a.sC % 4 == 0 && al(a.W, 15) && al(a.U, 15) &&
+         (a.Wb == nullptr || al(a.Wb, 7));
+}
+
 // ------------------------------------------------------------------ bf16
 template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN>
 __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
@@ -658,8 +919,81 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 // output dimensions allow it on the fp32 path, else 64 x 64.
 bool big_tile(int dtype, int M, int N) { return dtype == 0 && M >= 128 && N >= 128; }
 
+// Compute units and resident specialised-update workgroups per CU on the
+// current device, queried once per device.
+hipError_t ws_grid(long long tiles, int& grid) {
+  struct Shape {
+    int cus = 0, per_cu = 0;
+  };
+  static Shape cache[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (cache[dev].cus == 0) {
+    Shape sh;
+    e = hipDeviceGetAttribute(&sh.cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &sh.per_cu, reinterpret_cast<const void*>(gemm_f32_sgd_ws<kWsDepth>),
+        kWsThreads, 0);
+    if (e != hipSuccess) return e;
+    if (sh.per_cu < 1) sh.per_cu = 1;
+    cache[dev] = sh;
+  }
+  long long g = (long long)cache[dev].cus * cache[dev].per_cu;
+  if (g > tiles) g = tiles;
+  if (g >= kXcds) g -= g % kXcds;
+  grid = (int)g;
+  return hipSuccess;
+}
+
+}  // namespace
+
+int gemm_sgd_multi_tiles(int dtype, const GemmArgs* list, int n) {
+  if (n < 1 || n > kWsMaxProblems) return -1;
+  long long total = 0;
+  for (int i = 0; i < n; ++i) {
+    if (!ws_eligible(dtype, list[i])) return -1;
+    total += (long long)(list[i].M / 128) * (list[i].N / 128) * list[i].G;
+  }
+  return total < (1LL << 30) ? (int)total : -1;
+}
+
+hipError_t launch_gemm_sgd_multi(int dtype, const GemmArgs* list, int n,
+                                 hipStream_t s) {
+  const int total = gemm_sgd_multi_tiles(dtype, list, n);
+  if (total < 0) return hipErrorInvalidValue;
+  if (total == 0) return hipSuccess;
+  WsArgs w{};
+  w.np = n;
+  w.start[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    w.p[i] = list[i];
+    w.p[i].splits = 1;
+    w.start[i + 1] = w.start[i] + (list[i].M / 128) * (list[i].N / 128) * list[i].G;
+    if (i > 0 && (list[i].lr != list[0].lr || list[i].mom != list[0].mom ||
+                  list[i].wd != list[0].wd || list[i].nesterov != list[0].nesterov))
+      return hipErrorInvalidValue;
+  }
+  int grid = 0;
+  hipError_t e = ws_grid(total, grid);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((gemm_f32_sgd_ws<kWsDepth>), dim3(grid), dim3(kWsThreads), 0,
+                     s, w);
+  return hipGetLastError();
+}
+
+namespace {
+
 template <bool AT, bool BT, int EPI, bool GATHER>
 hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
+  if constexpr (AT && !BT && EPI == EPI_SGD) {
+    // one large layer: the specialised update kernel with a one-item list
+    if (ws_eligible(dtype, a) &&
+        (long long)(a.M / 128) * (a.N / 128) * a.G >= kWsMinTiles)
+      return launch_gemm_sgd_multi(dtype, &a, 1, s);
+  }
   const bool big = big_tile(dtype, a.M, a.N);
   const int BM = big ? 128 : 64, BN = BM;
   const long long tiles = (long long)((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM) * a.G;

@@ -69,6 +69,16 @@ int gemm_splits(int dtype, int M, int N, int Kd, int G, int epi);
 hipError_t launch_gemm(int dtype, int trans_a, int trans_b, int epi,
                        int out_bf16, const GemmArgs& a, hipStream_t s);
 
+// Fused weight gradient + update (trans_a = 1, trans_b = 0, EPI_SGD) of up to
+// kWsMaxProblems layers in one persistent launch, their tiles concatenated.
+// gemm_sgd_multi_tiles: the list's total 128 x 128 tile count, or -1 when a
+// problem does not fit the kernel (fp32, M and N multiples of 128, aligned
+// rows, at most 512 gathered rows).
+constexpr int kWsMaxProblems = 8;
+int gemm_sgd_multi_tiles(int dtype, const GemmArgs* list, int n);
+hipError_t launch_gemm_sgd_multi(int dtype, const GemmArgs* list, int n,
+                                 hipStream_t s);
+
 // ---------------------------------------------------------------- head
 // Output layer with few classes, fused around the loss (head.hip).
 constexpr int kHeadMaxClasses = 32;

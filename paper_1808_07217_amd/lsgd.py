@@ -64,6 +64,7 @@ _SIGS = {
     "lsgd_status_string": [_c.c_int],
     "lsgd_last_error": [_P],
     "lsgd_profile_enable": [_P, _c.c_int32],
+    "lsgd_profile_select": [_P, _c.c_char_p, _c.c_int32],
     "lsgd_profile_report": [_P, _c.c_char_p, _c.c_size_t],
     "lsgd_grouped_gemm": [_c.c_int32, _c.c_int32, _c.c_int32, _c.c_int32,
                           _c.c_int32, _c.c_int32, _c.c_int32, _P, _c.c_int64,
@@ -216,6 +217,13 @@ class Replicas:
     def profile(self, enable: bool = True):
         """Bracket every launch with HIP events (see lsgd_profile_enable)."""
         _check(_lib.lsgd_profile_enable(self._ctx, int(bool(enable))), self._ctx)
+
+    def profile_select(self, tag: Optional[str] = None, every: int = 1):
+        """Bracket only every ``every``-th launch tagged ``tag`` (None: all
+        launches)."""
+        _check(_lib.lsgd_profile_select(
+            self._ctx, None if tag is None else tag.encode(), int(every)),
+            self._ctx)
 
     def profile_report(self) -> dict:
         """{tag: (launches, total_ms)} since profiling was enabled; clears."""

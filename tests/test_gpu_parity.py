@@ -96,6 +96,30 @@ def test_batch_larger_than_the_gathered_row_cache():
     _compare_steps(w, X, y, w0, PARAM_TOL_FP32, 1e-4)
 
 
+@pytest.mark.parametrize("widths,K,B,nesterov,seed", [
+    ((256, 2048, 10), 32, 21, False, 5),       # gathered rows, 1024 tiles
+    ((384, 384, 384, 10), 115, 9, True, 6),    # both layers; 1035 tiles, odd batch
+    ((64, 1024, 1024, 10), 16, 20, False, 5),  # activation rows, 1024 tiles
+    ((512, 1024, 512, 10), 16, 128, True, 5),  # 128-row batch: unrolled k loop
+])
+def test_persistent_update_kernel_shapes(widths, K, B, nesterov, seed):
+    """Layers with 1024 or more 128 x 128 weight tiles take the persistent
+    weight-gradient + update kernel (MFMA and update wavefronts working on
+    consecutive tiles); every replica after every step.
+
+    The data seeds keep every ReLU pre-activation of these runs clear of
+    zero at fp32 resolution: perturbing the oracle's own initial weights by
+    1e-7 (relative) moves every replica's parameters by at most ~3e-7. (With
+    seed 5 the 115-replica case puts one hidden unit of replica 32 on the
+    kink at the fourth step, where the same perturbation moves the fp64
+    oracle by 2.45e-4 -- an fp32 result can legitimately differ there.)"""
+    w = _small(widths, nesterov=nesterov, K=K, B=B, N=max(999, 4 * K), H=2,
+               rounds=2, lr=0.01)
+    print(f"persistent update {widths} K={K} B={B}", flush=True)
+    X, y, w0 = _small_data(w, seed=seed)
+    _compare_steps(w, X, y, w0, PARAM_TOL_FP32, 1e-4)
+
+
 @pytest.mark.parametrize("widths", [(70, 48, 36, 10), (64, 128, 64, 10),
                                     (72, 20), (40, 33, 45)])
 def test_small_mlp_bf16_every_step(widths):
