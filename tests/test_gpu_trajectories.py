@@ -19,7 +19,8 @@ from gpu_util import make_replicas, rel, device
 pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-CASES = [("mlp_512", 1e-3), ("postlocal_mlp_512", 1e-3)]
+CASES = [("mlp_512", 1e-3), ("postlocal_mlp_512", 1e-3),
+         ("wide_mlp_2048_bf16", 2e-2)]
 
 
 @pytest.mark.parametrize("name,tol", CASES)
