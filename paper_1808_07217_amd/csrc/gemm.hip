@@ -37,6 +37,18 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;
 
+// float4 moves through a native vector type: copying HIP's float4 struct
+// straight from memory becomes a memcpy, which keeps register arrays of it
+// in scratch memory
+typedef float v4f __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ldg4(const float* p) {
+  const v4f v = *(const v4f*)p;
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void sts4(float* p, const float4& v) {
+  *(v4f*)p = v4f{v.x, v.y, v.z, v.w};
+}
+
 struct Tile {
   int g, s, m0, n0;
 };
@@ -279,7 +291,12 @@ struct SgdVec {
 };
 
 // ------------------------------------------------------------------ fp32
-template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN, int BK>
+// FULL: every tile is whole, every split covers whole BK slabs and the
+// operands allow float4 loads (checked at launch). The loads then carry no
+// bounds branches and the prefetch of slabs past the end is clamped to the
+// last slab instead of skipped, so the compiler can count the loads in
+// flight and wait only for the register set it is about to store.
+template <bool AT, bool BT, int EPI, bool GATHER, int BM, int BN, int BK, bool FULL>
 __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
                                                      int vecB, int vecC) {
   // pitch: transposing stores (k-contiguous source) use pitch = 2 mod 8 to
@@ -310,8 +327,9 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   const int kend = min(a.Kd, kbeg + a.kchunk);
 
   // two register sets: slab t+2 is loaded while slab t computes and slab t+1
-  // waits in LDS, so each load has two compute phases to arrive
-  float4 ra[2][NA], rb[2][NB];
+  // waits in LDS, so each load has two compute phases to arrive (separate
+  // arrays, not one indexed by the set: that index ends up in scratch)
+  float4 ra0[NA], rb0[NB], ra1[NA], rb1[NB];
   // gathered rows: the forward operand's rows are fixed per thread, so their
   // dataset indices are read once; the weight gradient walks its rows per
   // slab, so the workgroup's indices are staged in LDS
@@ -338,51 +356,74 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
     return v;
   };
 
-  auto gload = [&](int k0, int set) {
+  auto gload = [&](int k0, float4(&xa)[NA], float4(&xb)[NB]) __attribute__((always_inline)) {
+    if constexpr (FULL) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const int q = tid + i * kThreads;
+        if constexpr (!AT) {
+          xa[i] = ldg4(A + srow[i] * a.lda + k0 + (q % KV) * 4);
+        } else {
+          const int r = q / (BM / 4), kr = k0 + r;
+          const long long sr =
+              GATHER ? (kr - kbeg < 512 ? srmap[kr - kbeg] : rmap[kr]) : kr;
+          xa[i] = ldg4(A + sr * a.lda + m0 + (q % (BM / 4)) * 4);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int q = tid + i * kThreads;
+        if constexpr (BT)
+          xb[i] = ldg4(B + (long long)(n0 + q / KV) * a.ldb + k0 + (q % KV) * 4);
+        else
+          xb[i] = ldg4(B + (long long)(k0 + q / (BN / 4)) * a.ldb + n0 + (q % (BN / 4)) * 4);
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int q = tid + i * kThreads;
-      ra[set][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      xa[i] = make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (!AT) {  // storage [M][Kd]: rows m, KV float4 per row
         const int r = q / KV, c = k0 + (q % KV) * 4, row = m0 + r;
-        if (row < M && c < kend) ra[set][i] = load4(A + srow[i] * a.lda + c, kend - c, vecA);
+        if (row < M && c < kend) xa[i] = load4(A + srow[i] * a.lda + c, kend - c, vecA);
       } else {  // storage [Kd][M]: rows k, BM/4 float4 per row
         const int r = q / (BM / 4), c = m0 + (q % (BM / 4)) * 4, kr = k0 + r;
         if (kr < kend) {
           const long long sr =
               GATHER ? (kr - kbeg < 512 ? srmap[kr - kbeg] : rmap[kr]) : kr;
-          ra[set][i] = load4(A + sr * a.lda + c, M - c, vecA);
+          xa[i] = load4(A + sr * a.lda + c, M - c, vecA);
         }
       }
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int q = tid + i * kThreads;
-      rb[set][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      xb[i] = make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (BT) {  // storage [N][Kd]
         const int r = q / KV, c = k0 + (q % KV) * 4, row = n0 + r;
         if (row < N && c < kend)
-          rb[set][i] = load4(B + (long long)row * a.ldb + c, kend - c, vecB);
+          xb[i] = load4(B + (long long)row * a.ldb + c, kend - c, vecB);
       } else {  // storage [Kd][N]
         const int r = q / (BN / 4), c = n0 + (q % (BN / 4)) * 4, kr = k0 + r;
-        if (kr < kend) rb[set][i] = load4(B + (long long)kr * a.ldb + c, N - c, vecB);
+        if (kr < kend) xb[i] = load4(B + (long long)kr * a.ldb + c, N - c, vecB);
       }
     }
   };
 
-  auto lstore = [&](int buf, int set) {
+  auto lstore = [&](int buf, const float4(&xa)[NA], const float4(&xb)[NB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int q = tid + i * kThreads;
       if constexpr (!AT) {
         const int r = q / KV, kq = (q % KV) * 4;
-        As[buf][kq + 0][r] = ra[set][i].x;
-        As[buf][kq + 1][r] = ra[set][i].y;
-        As[buf][kq + 2][r] = ra[set][i].z;
-        As[buf][kq + 3][r] = ra[set][i].w;
+        As[buf][kq + 0][r] = xa[i].x;
+        As[buf][kq + 1][r] = xa[i].y;
+        As[buf][kq + 2][r] = xa[i].z;
+        As[buf][kq + 3][r] = xa[i].w;
       } else {
         const int r = q / (BM / 4), c = (q % (BM / 4)) * 4;
-        *(float4*)&As[buf][r][c] = ra[set][i];
+        sts4(&As[buf][r][c], xa[i]);
       }
     }
 #pragma unroll
@@ -390,13 +431,13 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
       const int q = tid + i * kThreads;
       if constexpr (BT) {
         const int r = q / KV, kq = (q % KV) * 4;
-        Bs[buf][kq + 0][r] = rb[set][i].x;
-        Bs[buf][kq + 1][r] = rb[set][i].y;
-        Bs[buf][kq + 2][r] = rb[set][i].z;
-        Bs[buf][kq + 3][r] = rb[set][i].w;
+        Bs[buf][kq + 0][r] = xb[i].x;
+        Bs[buf][kq + 1][r] = xb[i].y;
+        Bs[buf][kq + 2][r] = xb[i].z;
+        Bs[buf][kq + 3][r] = xb[i].w;
       } else {
         const int r = q / (BN / 4), c = (q % (BN / 4)) * 4;
-        *(float4*)&Bs[buf][r][c] = rb[set][i];
+        sts4(&Bs[buf][r][c], xb[i]);
       }
     }
   };
@@ -419,7 +460,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   }
   const int nk = (kend - kbeg + BK - 1) / BK;
   const int lk = lane >> 5, lr = lane & 31;
-  auto compute = [&](int buf) {
+  auto compute = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 2) {
       float av[FM], bv[FN];
@@ -440,20 +481,41 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
     }
   };
   // slab t lives in LDS buffer t % 2 and register set t % 2
-  if (nk > 0) gload(kbeg, 0);
-  if (nk > 1) gload(kbeg + BK, 1);
-  if (nk > 0) lstore(0, 0);
-  __syncthreads();
   int it = 0;
-  for (; it + 1 < nk; it += 2) {
-    if (it + 2 < nk) gload(kbeg + (it + 2) * BK, 0);
-    compute(0);
-    lstore(1, 1);
+  if constexpr (FULL) {
+    // nk >= 1; prefetches past the last slab reload it (unused)
+    auto slab = [&](int t) __attribute__((always_inline)) { return kbeg + min(t, nk - 1) * BK; };
+    gload(slab(0), ra0, rb0);
+    gload(slab(1), ra1, rb1);
+    lstore(0, ra0, rb0);
     __syncthreads();
-    if (it + 3 < nk) gload(kbeg + (it + 3) * BK, 1);
-    compute(1);
-    if (it + 2 < nk) lstore(0, 0);
+    for (; it + 1 < nk; it += 2) {
+      gload(slab(it + 2), ra0, rb0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, ra1, rb1);
+      __syncthreads();
+      gload(slab(it + 3), ra1, rb1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      lstore(0, ra0, rb0);
+      __syncthreads();
+    }
+  } else {
+    if (nk > 0) gload(kbeg, ra0, rb0);
+    if (nk > 1) gload(kbeg + BK, ra1, rb1);
+    if (nk > 0) lstore(0, ra0, rb0);
     __syncthreads();
+    for (; it + 1 < nk; it += 2) {
+      if (it + 2 < nk) gload(kbeg + (it + 2) * BK, ra0, rb0);
+      compute(0);
+      lstore(1, ra1, rb1);
+      __syncthreads();
+      if (it + 3 < nk) gload(kbeg + (it + 3) * BK, ra1, rb1);
+      compute(1);
+      if (it + 2 < nk) lstore(0, ra0, rb0);
+      __syncthreads();
+    }
   }
   if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
 
@@ -986,6 +1048,12 @@ hipError_t launch_gemm_sgd_multi(int dtype, const GemmArgs* list, int n,
 
 namespace {
 
+// Whole tiles, whole slabs per split, vector loads: the FULL kernel variant.
+bool full(const GemmArgs& a, int T, int BK, int vecA, int vecB, int vecC) {
+  return vecA && vecB && a.M % T == 0 && a.N % T == 0 && a.kchunk % BK == 0 &&
+         (long long)a.kchunk * a.splits == a.Kd && (vecC || a.W == nullptr);
+}
+
 template <bool AT, bool BT, int EPI, bool GATHER>
 hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
   if constexpr (AT && !BT && EPI == EPI_SGD) {
@@ -1008,11 +1076,17 @@ hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
   if (dtype == 1)
     hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, 64, 64>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
+  else if (big && full(a, 128, 16, vecA, vecB, vecC))
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, 16, true>), dim3(total),
+                       dim3(kThreads), 0, s, a, vecA, vecB, vecC);
   else if (big)
-    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, 16>), dim3(total),
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, 16, false>), dim3(total),
+                       dim3(kThreads), 0, s, a, vecA, vecB, vecC);
+  else if (full(a, 64, 32, vecA, vecB, vecC))
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 64, 64, 32, true>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
   else
-    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 64, 64, 32>), dim3(total),
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 64, 64, 32, false>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
