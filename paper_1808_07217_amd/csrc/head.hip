@@ -299,6 +299,108 @@ __global__ __launch_bounds__(256) void k_head_wgrad(HeadArgs h) {
   if (threadIdx.x == 0 && h.loss) h.loss[k] = red[0] / (float)B;
 }
 
+// Weight gradient of the output layer in one memory round trip (fp32,
+// C <= CM, D % 64 == 0, B <= 128): workgroup (x, k) owns inputs
+// d = 64 x .. 64 x + 63 of replica k. Every load -- the activations A[b][d]
+// of the lane's d for the group's rows b = grp + 4 r, dZ, this slice of W_L
+// and U_L, the per-row losses -- is issued up front. Each of the 4 thread
+// groups sums its quarter of the batch (rows grp, grp + 4, ... ascending);
+// the four partials are then added in group order and the SGD step applied.
+// Workgroup 0 of each replica also updates the bias and reduces the loss.
+template <int CM, bool GATHER>
+__global__ __launch_bounds__(256) void k_head_wgrad_vec(HeadArgs h) {
+  constexpr int RPG = 32;                 // rows per group: B <= 128
+  constexpr int WPT = (64 * CM + 255) / 256;  // weights per thread
+  constexpr int ZPT = (128 * CM + 255) / 256; // dZ values per thread
+  __shared__ float dzs[128 * CM];
+  __shared__ float part[4][64][CM + 1];
+  __shared__ float red[256];
+  const int k = blockIdx.y;
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const int D = h.D, C = h.C, B = h.B;
+  const int dbase = blockIdx.x * 64, d = dbase + lane;
+  const bool first = blockIdx.x == 0;
+  const float* dZ = (const float*)h.dZ + (long long)k * B * C;
+
+  // 1. all loads in flight together (clamped indices, values masked at use)
+  float av[RPG];
+#pragma unroll
+  for (int r = 0; r < RPG; ++r) {
+    const int b = min(grp + 4 * r, B - 1);
+    const long long row = GATHER ? (long long)h.rowmap[(long long)k * B + b]
+                                 : (long long)k * (h.sA / D) + b;
+    av[r] = ((const float*)h.A)[row * D + d];
+  }
+  float zv[ZPT];
+#pragma unroll
+  for (int q = 0; q < ZPT; ++q) zv[q] = dZ[min((int)threadIdx.x + 256 * q, B * C - 1)];
+  float wv[WPT], uv[WPT];
+  const long long wbase = (long long)k * h.sP + (long long)dbase * C;
+#pragma unroll
+  for (int q = 0; q < WPT; ++q) {
+    const int e = min((int)threadIdx.x + 256 * q, 64 * C - 1);
+    wv[q] = h.Wm[wbase + e];
+    uv[q] = h.Um[wbase + e];
+  }
+  const float rl = first ? h.rowloss[(long long)k * B + min((int)threadIdx.x, B - 1)] : 0.f;
+
+  // 2. dZ to LDS
+#pragma unroll
+  for (int q = 0; q < ZPT; ++q) {
+    const int i = (int)threadIdx.x + 256 * q;
+    if (i < B * C) dzs[i] = zv[q];
+  }
+  __syncthreads();
+
+  // 3. this group's rows
+  float acc[CM];
+#pragma unroll
+  for (int c = 0; c < CM; ++c) acc[c] = 0.f;
+#pragma unroll
+  for (int r = 0; r < RPG; ++r) {
+    const int b = grp + 4 * r;
+    if (b < B) {
+#pragma unroll
+      for (int c = 0; c < CM; ++c)
+        if (c < C) acc[c] = __builtin_fmaf(av[r], dzs[b * C + c], acc[c]);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CM; ++c) part[grp][lane][c] = acc[c];
+  __syncthreads();
+
+  // 4. partials in group order, SGD step on W_L[d][c]
+#pragma unroll
+  for (int q = 0; q < WPT; ++q) {
+    const int e = (int)threadIdx.x + 256 * q;
+    if (e < 64 * C) {
+      const int dl = e / C, c = e - dl * C;
+      const float g = ((part[0][dl][c] + part[1][dl][c]) + part[2][dl][c]) + part[3][dl][c];
+      float w = wv[q], u = uv[q];
+      sgd_step(w, u, g, h);
+      h.Wm[wbase + e] = w;
+      h.Um[wbase + e] = u;
+    }
+  }
+  if (!first) return;  // uniform over the workgroup
+  if ((int)threadIdx.x < C) {
+    float bsum = 0.f;
+    for (int b = 0; b < B; ++b) bsum += dzs[b * C + threadIdx.x];
+    const long long o = (long long)k * h.sP + threadIdx.x;
+    float w = h.bias_w[o], u = h.bias_u[o];
+    sgd_step(w, u, bsum, h);
+    h.bias_w[o] = w;
+    h.bias_u[o] = u;
+  }
+  red[threadIdx.x] = (int)threadIdx.x < B ? rl : 0.f;
+  __syncthreads();
+  for (int w2 = 128; w2 > 0; w2 >>= 1) {
+    if ((int)threadIdx.x < w2) red[threadIdx.x] += red[threadIdx.x + w2];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && h.loss) h.loss[k] = red[0] / (float)B;
+}
+
 // Register-resident variant for fp32, a class count fixed at compile time,
 // D % 256 == 0 and D <= 512: lane l
 // owns inputs d = 256 j + 4 l .. +3 (j < D / 256) of two sample rows and the
@@ -458,6 +560,20 @@ hipError_t launch_head(int dtype, const HeadArgs& h, hipStream_t s, int which) {
       hipLaunchKernelGGL((k_head_fwd_vec<10, 1>), grid, dim3(256), 0, s, h);
     else
       hipLaunchKernelGGL((k_head_fwd_vec<10, 2>), grid, dim3(256), 0, s, h);
+    return hipGetLastError();
+  }
+  // one-round-trip weight gradient: fp32, up to 16 classes, 64-input slices
+  if (which == 1 && dtype == 0 && h.C <= 16 && h.D % 64 == 0 && h.B <= 128 &&
+      h.Wb == nullptr && (h.gather || h.sA % h.D == 0)) {
+    dim3 grid(h.D / 64, h.K);
+    if (h.C == 10 && h.gather)
+      hipLaunchKernelGGL((k_head_wgrad_vec<10, true>), grid, dim3(256), 0, s, h);
+    else if (h.C == 10)
+      hipLaunchKernelGGL((k_head_wgrad_vec<10, false>), grid, dim3(256), 0, s, h);
+    else if (h.gather)
+      hipLaunchKernelGGL((k_head_wgrad_vec<16, true>), grid, dim3(256), 0, s, h);
+    else
+      hipLaunchKernelGGL((k_head_wgrad_vec<16, false>), grid, dim3(256), 0, s, h);
     return hipGetLastError();
   }
   if (dtype == 1)

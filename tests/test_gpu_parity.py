@@ -80,6 +80,8 @@ def _compare_steps(w, X, y, w0, param_tol, loss_tol, rounds=None):
     ((40, 33, 45), True, 0.9),         # > 32 classes: generic GEMM + loss path
     ((100, 256, 10), False, 0.9),      # register-resident head, 256 inputs
     ((48, 512, 512, 10), True, 0.9),   # register-resident head, 512 inputs
+    ((64, 64, 13), True, 0.9),         # one-pass head weight gradient, 13 classes
+    ((128, 16), False, 0.9),           # the same, gathered rows, 16 classes
 ])
 def test_small_mlp_every_step(widths, nesterov, momentum):
     w = _small(widths, nesterov=nesterov, momentum=momentum)
