@@ -691,9 +691,44 @@ __global__ __launch_bounds__(kWsThreads) void gemm_f32_sgd_ws(WsArgs w) {
         if (Kd == kWsUnrolledRows) {
           // straight-line code: the wait before each slot's MFMAs counts
           // exactly the D - 1 younger refills, which a runtime loop's
-          // back edge hides from the compiler (it then waits for all)
+          // back edge hides from the compiler (it then waits for all).
+          // The 128 row indices sit in two registers per lane (rows lane
+          // and lane + 64); a refill takes its row with a readlane at a
+          // compile-time lane instead of waiting on an LDS read between
+          // MFMAs.
+          static_assert(kWsUnrolledRows == 128, "two index registers per lane");
+          constexpr int NKP = kWsUnrolledRows / 2;
+          const int r_lo = srm[lane], r_hi = srm[lane + 64];
+          // B rows walk with one running pointer (per-k addresses hoisted
+          // out of the unrolled loop would take two registers each)
+          const float* bq = B + (long long)(2 * D + lk) * ldb;
+          const long long bstep = 2 * ldb;
 #pragma unroll
-          for (int kp = 0; kp < kWsUnrolledRows / 2; ++kp) slot(kp, kp % D);
+          for (int kp = 0; kp < NKP; ++kp) {
+            const int d = kp % D;
+            const float a0 = ra[d].x, a1 = ra[d].y, b0 = rb[d].x, b1 = rb[d].y;
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+            if (kp + D < NKP) {
+              // refill of this slot with k-pair kp + D: its row index by
+              // readlane at a compile-time lane, issued between the MFMAs
+              const int ke = 2 * (kp + D);
+              const int src = ke < 64 ? r_lo : r_hi;
+              const int se = __builtin_amdgcn_readlane(src, ke & 63);
+              const int so = __builtin_amdgcn_readlane(src, (ke + 1) & 63);
+              const long long row = gather ? (long long)(lk ? so : se) : (long long)(ke + lk);
+              ra[d] = *(const float2*)(A + row * lda);
+            }
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+            if (kp + D < NKP) {
+              rb[d] = *(const float2*)bq;
+              bq += bstep;
+            }
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            cs0 += b0;
+            cs1 += b1;
+            __builtin_amdgcn_sched_barrier(0);
+          }
         } else {
           for (int blk = 0; blk < nblk; ++blk) {
 #pragma unroll
@@ -1048,6 +1083,12 @@ hipError_t launch_gemm_sgd_multi(int dtype, const GemmArgs* list, int n,
 
 namespace {
 
+// k slab of the whole-tile 128 x 128 variant. 32 would halve the barriers
+// per k but doubles the prefetch registers and LDS; measured on the 512-wide
+// MLP it is slower, and costs the update epilogue an occupancy step.
+template <int EPI>
+constexpr int kBigFullBK = 16;
+
 // Whole tiles, whole slabs per split, vector loads: the FULL kernel variant.
 bool full(const GemmArgs& a, int T, int BK, int vecA, int vecB, int vecC) {
   return vecA && vecB && a.M % T == 0 && a.N % T == 0 && a.kchunk % BK == 0 &&
@@ -1076,8 +1117,8 @@ hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
   if (dtype == 1)
     hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, 64, 64>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
-  else if (big && full(a, 128, 16, vecA, vecB, vecC))
-    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, 16, true>), dim3(total),
+  else if (big && full(a, 128, kBigFullBK<EPI>, vecA, vecB, vecC))
+    hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, kBigFullBK<EPI>, true>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
   else if (big)
     hipLaunchKernelGGL((gemm_f32<AT, BT, EPI, GATHER, 128, 128, 16, false>), dim3(total),
