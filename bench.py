@@ -36,6 +36,9 @@ def parse():
     p.add_argument("--workload", default="mlp_512")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-kernel-timing", action="store_true")
+    p.add_argument("--sweep", action="store_true",
+                   help="HBM sweep of the K-way average and the fused update "
+                        "from 64 MB to 4 GB working sets (one JSON line per size)")
     p.add_argument("--traffic-from", metavar="DIR",
                    help="no GPU run: turn the rocprofv3 FETCH_SIZE / "
                         "WRITE_SIZE passes under DIR (fetch/, write/) into "
@@ -183,6 +186,56 @@ def write_traffic(pmc_dir: str, w) -> dict:
     return out
 
 
+def sweep():
+    """Achieved bandwidth of the two HBM-bound building blocks against the
+    working-set size. Sets up to ~256 MB can stay in the 256 MB Infinity
+    Cache between repetitions, so only the larger sizes measure HBM itself."""
+    import torch
+    from paper_1808_07217_amd import lsgd as L
+    dev = torch.device("cuda", 0)
+    K = 16
+    for mb in (64, 128, 256, 512, 1024, 2048, 4096):
+        nbytes = mb << 20
+        P = nbytes // (4 * K) // 64 * 64
+        W = torch.randn(K, P, device=dev)
+        reps = 20 if mb <= 1024 else 8
+        L.replica_average(W)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            L.replica_average(W)
+        e1.record()
+        torch.cuda.synchronize()
+        t_avg = e0.elapsed_time(e1) / reps / 1e3
+        avg_bytes = 2 * K * P * 4                # read and write [K][P]
+        del W
+        n = nbytes // (3 * 4) // 64 * 64          # W, U, G of n floats
+        Wt = torch.randn(n, device=dev)
+        Ut = torch.zeros(n, device=dev)
+        Gt = torch.randn(n, device=dev)
+        L.sgd_update(Wt, Ut, Gt, 1e-3, 0.9, 1e-4)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            L.sgd_update(Wt, Ut, Gt, 1e-3, 0.9, 1e-4)
+        e1.record()
+        torch.cuda.synchronize()
+        t_upd = e0.elapsed_time(e1) / reps / 1e3
+        upd_bytes = 20 * n                        # read W, U, G; write W, U
+        del Wt, Ut, Gt
+        torch.cuda.empty_cache()
+        print(json.dumps({
+            "working_set_MB": mb,
+            "average": {"K": K, "P": P, "us": round(t_avg * 1e6, 2),
+                        "GB/s": round(avg_bytes / t_avg / 1e9, 1),
+                        "frac_hbm": round(avg_bytes / t_avg / 1e9 / PEAK_HBM_GBS, 4)},
+            "sgd_update": {"n": n, "us": round(t_upd * 1e6, 2),
+                           "GB/s": round(upd_bytes / t_upd / 1e9, 1),
+                           "frac_hbm": round(upd_bytes / t_upd / 1e9 / PEAK_HBM_GBS, 4)},
+        }), flush=True)
+
+
 def cpu_baseline(w, X, y, w0):
     """The CPU oracle (as it is) on one full round of the workload: H local
     steps on all K replicas plus the average, on this host's cores."""
@@ -208,6 +261,9 @@ def cpu_baseline(w, X, y, w0):
 
 def main():
     args = parse()
+    if args.sweep:
+        sweep()
+        return
     if args.traffic_from:
         import workloads as wk
         print(json.dumps(write_traffic(args.traffic_from, wk.get(args.workload))))
@@ -270,14 +326,34 @@ def main():
             rnd(args.warmup + i)
         ev1.record(stream)
     torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    phases = None
+    if w.warm_rounds > 0:
+        # post-local SGD: the H = 1 warm phase (one average per local step)
+        # timed on its own; the headline above is the H-step phase
+        nw = min(w.warm_rounds, 100)
+        reps.profile(False)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            p0 = torch.cuda.Event(enable_timing=True)
+            p1 = torch.cuda.Event(enable_timing=True)
+            p0.record(stream)
+            tw = time.perf_counter()
+            for _ in range(nw):
+                reps.run_round([w.lr], loss[:1])
+            p1.record(stream)
+        torch.cuda.synchronize()
+        ms_h1 = max(p0.elapsed_time(p1), (time.perf_counter() - tw) * 1e3) / nw
+        phases = {"H1": {"rounds_timed": nw, "samples_per_round": w.K * w.B_loc,
+                         "ms_per_round": round(ms_h1, 4),
+                         "samples_per_s": round(w.K * w.B_loc / (ms_h1 / 1e3), 1)}}
     if timing:
         n, ms = reps.profile_report()[dom]
         reps.profile(False)
         reps.profile_select(None)
         avg_s = ms / n / 1e3
         flops, nbytes = kernel_cost(dom, w)
-    wall = time.perf_counter() - t0
-    gpu_ms = ev0.elapsed_time(ev1)
     ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
     samples = w.K * H * w.B_loc
     value = samples / (ms_per_step / 1e3)
@@ -299,6 +375,11 @@ def main():
                    "momentum": w.momentum, "nesterov": w.nesterov,
                    "weight_decay": w.weight_decay},
     }
+    if phases is not None:
+        phases[f"H{H}"] = {"samples_per_round": samples,
+                           "ms_per_round": round(ms_per_step, 4),
+                           "samples_per_s": round(value, 1)}
+        out["phases"] = phases
     gemm_flops = gemm_flops_per_local_step(w) * H
     out["e2e_mfma_frac"] = round(gemm_flops / (ms_per_step / 1e3) /
                                  (PEAK_TFLOPS[w.dtype] * 1e12), 4)

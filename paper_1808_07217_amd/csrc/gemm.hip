@@ -555,7 +555,6 @@ constexpr int kWsThreads = 512;
 constexpr int kWsMaxRows = 512;
 constexpr int kWsDepth = 8;        // k-pairs of operands in flight per lane
 constexpr int kWsMinTiles = 1024;  // below: one tile per workgroup is as good
-constexpr int kWsUnrolledRows = 128;  // batch size given a fully unrolled k loop
 
 struct WsArgs {
   GemmArgs p[kWsMaxProblems];
@@ -609,10 +608,140 @@ __device__ __forceinline__ void ws_rows_store(int32_t* buf, const WsRows& r) {
   buf[threadIdx.x + 256] = r.r1;
 }
 
+// Operand pairs of the MFMA role: two consecutive fp32 values (float2), or
+// two consecutive bf16 values in one 32-bit word, widened to fp32 at use
+// (bf16 x bf16 products are exact in fp32, so the fp32 MFMA computes what a
+// bf16 MFMA with fp32 accumulation does, up to the order of the sums).
+template <bool BF>
+struct WsOp;
+template <>
+struct WsOp<false> {
+  using E = float;
+  using P = float2;
+  __device__ static P ld(const E* p) { return *(const float2*)p; }
+  __device__ static float lo(P v) { return v.x; }
+  __device__ static float hi(P v) { return v.y; }
+};
+template <>
+struct WsOp<true> {
+  using E = bf16_t;
+  using P = uint32_t;
+  __device__ static P ld(const E* p) { return *(const uint32_t*)p; }
+  __device__ static float lo(P v) { return __uint_as_float(v << 16); }
+  __device__ static float hi(P v) { return __uint_as_float(v & 0xffff0000u); }
+};
+
+// k loop of one MFMA wave over a tile (its 64 x 64 quarter): rows
+// k = 2 kp + lk, kp < nkp. A points at column m0 + wm0 + 2 lr of row 0
+// (gathered: row srm[k]), B at column n0 + wn0 + 2 lr of row 0.
+template <bool BF, int D>
+struct WsK {
+  using Op = WsOp<BF>;
+  using E = typename Op::E;
+  using P = typename Op::P;
+
+  __device__ static void mfma(floatx16 (&acc)[2][2], P ra, P rb, float& cs0, float& cs1) {
+    const float a0 = Op::lo(ra), a1 = Op::hi(ra), b0 = Op::lo(rb), b1 = Op::hi(rb);
+    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+    cs0 += b0;
+    cs1 += b1;
+  }
+
+  // Any batch size. Rows past the end are clamped to the last one and their
+  // values replaced by zero at use, so the loads carry no branches and stay
+  // countable in flight; a runtime loop's back edge still makes the compiler
+  // wait for all of them at the top of each block.
+  __device__ static void generic(floatx16 (&acc)[2][2], const E* A, const E* B,
+                                 long long lda, long long ldb, int Kd, bool gather,
+                                 const int32_t* srm, int lk, float& cs0, float& cs1) {
+    P ra[D], rb[D];
+    auto load = [&](int kp, P& x, P& y) __attribute__((always_inline)) {
+      const int k = min(2 * kp + lk, Kd - 1);
+      const int sr = srm[min(k, kWsMaxRows - 1)];
+      const long long row = gather ? (long long)sr : (long long)k;
+      x = Op::ld(A + row * lda);
+      y = Op::ld(B + (long long)k * ldb);
+    };
+#pragma unroll
+    for (int d = 0; d < D; ++d) load(d, ra[d], rb[d]);
+    const int nblk = ((Kd + 1) / 2 + D - 1) / D;
+    for (int blk = 0; blk < nblk; ++blk) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int kp = blk * D + d;
+        const bool live = 2 * kp + lk < Kd;
+        const P za = live ? ra[d] : P{}, zb = live ? rb[d] : P{};
+        mfma(acc, za, zb, cs0, cs1);
+        load(kp + D, ra[d], rb[d]);
+        // keep each refill right behind its slot's MFMAs: left alone, the
+        // scheduler sinks the refills to the end of the block, where they
+        // have no time left to arrive
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+
+  // ROWS (64 or 128) rows in straight-line code: the wait before each slot's
+  // MFMAs counts exactly the D - 1 younger refills. The row indices sit in
+  // ROWS / 64 registers per lane (rows lane, lane + 64) and a refill takes
+  // its row by readlane at a compile-time lane instead of waiting on an LDS
+  // read between MFMAs; B rows walk with one running pointer.
+  template <int ROWS>
+  __device__ static void unrolled(floatx16 (&acc)[2][2], const E* A, const E* B,
+                                  long long lda, long long ldb, bool gather,
+                                  const int32_t* srm, int lane, int lk, float& cs0,
+                                  float& cs1) {
+    static_assert(ROWS == 64 || ROWS == 128, "one or two index registers per lane");
+    constexpr int NKP = ROWS / 2;
+    P ra[D], rb[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int k = 2 * d + lk;
+      const long long row = gather ? (long long)srm[k] : (long long)k;
+      ra[d] = Op::ld(A + row * lda);
+      rb[d] = Op::ld(B + (long long)k * ldb);
+    }
+    const int r_lo = srm[lane], r_hi = ROWS > 64 ? srm[lane + 64] : 0;
+    const E* bq = B + (long long)(2 * D + lk) * ldb;
+    const long long bstep = 2 * ldb;
+#pragma unroll
+    for (int kp = 0; kp < NKP; ++kp) {
+      const int d = kp % D;
+      const P ca = ra[d], cb = rb[d];
+      const float a0 = Op::lo(ca), a1 = Op::hi(ca), b0 = Op::lo(cb), b1 = Op::hi(cb);
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+      if (kp + D < NKP) {
+        // refill of this slot with k-pair kp + D, between the MFMAs
+        const int ke = 2 * (kp + D);
+        const int src = ke < 64 ? r_lo : r_hi;
+        const int se = __builtin_amdgcn_readlane(src, ke & 63);
+        const int so = __builtin_amdgcn_readlane(src, (ke + 1) & 63);
+        const long long row = gather ? (long long)(lk ? so : se) : (long long)(ke + lk);
+        ra[d] = Op::ld(A + row * lda);
+      }
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+      if (kp + D < NKP) {
+        rb[d] = Op::ld(bq);
+        bq += bstep;
+      }
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+      cs0 += b0;
+      cs1 += b1;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+};
+
 // Both roles walk the same tile list and execute the same barriers: one
 // before the first tile, then two per tile.
-template <int D>
+template <bool BF, int D>
 __global__ __launch_bounds__(kWsThreads) void gemm_f32_sgd_ws(WsArgs w) {
+  using K = WsK<BF, D>;
+  using E = typename K::E;
   constexpr int T = 128, CP = T + 4;  // gradient tile pitch (16-byte rows)
   constexpr int PER = T * T / 4 / 256;  // float4 per update thread
   __shared__ __attribute__((aligned(16))) float Gs[T * CP];
@@ -646,95 +775,24 @@ __global__ __launch_bounds__(kWsThreads) void gemm_f32_sgd_ws(WsArgs w) {
         if (nxt_rows) nr = ws_rows_load(w, nxt);
 
         const GemmArgs& a = w.p[cur.pi];
-        const int Kd = a.Kd, nblk = ((Kd + 1) / 2 + D - 1) / D;
+        const int Kd = a.Kd;
         const bool gather = a.rowmap != nullptr;
         const int32_t* srm = srmap[j & 1];
-        const float* A = (const float*)a.A + (long long)cur.g * a.sA + cur.m0 + wm0 + 2 * lr;
-        const float* B = (const float*)a.B + (long long)cur.g * a.sB + cur.n0 + wn0 + 2 * lr;
-        const long long lda = a.lda, ldb = a.ldb;
+        const E* A = (const E*)a.A + (long long)cur.g * a.sA + cur.m0 + wm0 + 2 * lr;
+        const E* B = (const E*)a.B + (long long)cur.g * a.sB + cur.n0 + wn0 + 2 * lr;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][jj][v] = 0.f;
-        // k = 2 kp + lk; rows past the end are clamped to the last one here
-        // and their values replaced by zero at use, so the loads carry no
-        // branches and stay countable in flight
-        float2 ra[D], rb[D];
-        auto load = [&](int kp, float2& x, float2& y) {
-          const int k = min(2 * kp + lk, Kd - 1);
-          const int sr = srm[min(k, kWsMaxRows - 1)];
-          const long long row = gather ? (long long)sr : (long long)k;
-          x = *(const float2*)(A + row * lda);
-          y = *(const float2*)(B + (long long)k * ldb);
-        };
-#pragma unroll
-        for (int d = 0; d < D; ++d) load(d, ra[d], rb[d]);
         float cs0 = 0.f, cs1 = 0.f;
-        auto slot = [&](int kp, int d) {
-          const bool live = 2 * kp + lk < Kd;
-          const float a0 = live ? ra[d].x : 0.f, a1 = live ? ra[d].y : 0.f;
-          const float b0 = live ? rb[d].x : 0.f, b1 = live ? rb[d].y : 0.f;
-          acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-          acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-          acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-          acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
-          cs0 += b0;
-          cs1 += b1;
-          load(kp + D, ra[d], rb[d]);
-          // keep each refill right behind its slot's MFMAs: left alone, the
-          // scheduler sinks the refills to the end of the block, where they
-          // have no time left to arrive
-          __builtin_amdgcn_sched_barrier(0);
-        };
-        if (Kd == kWsUnrolledRows) {
-          // straight-line code: the wait before each slot's MFMAs counts
-          // exactly the D - 1 younger refills, which a runtime loop's
-          // back edge hides from the compiler (it then waits for all).
-          // The 128 row indices sit in two registers per lane (rows lane
-          // and lane + 64); a refill takes its row with a readlane at a
-          // compile-time lane instead of waiting on an LDS read between
-          // MFMAs.
-          static_assert(kWsUnrolledRows == 128, "two index registers per lane");
-          constexpr int NKP = kWsUnrolledRows / 2;
-          const int r_lo = srm[lane], r_hi = srm[lane + 64];
-          // B rows walk with one running pointer (per-k addresses hoisted
-          // out of the unrolled loop would take two registers each)
-          const float* bq = B + (long long)(2 * D + lk) * ldb;
-          const long long bstep = 2 * ldb;
-#pragma unroll
-          for (int kp = 0; kp < NKP; ++kp) {
-            const int d = kp % D;
-            const float a0 = ra[d].x, a1 = ra[d].y, b0 = rb[d].x, b1 = rb[d].y;
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-            if (kp + D < NKP) {
-              // refill of this slot with k-pair kp + D: its row index by
-              // readlane at a compile-time lane, issued between the MFMAs
-              const int ke = 2 * (kp + D);
-              const int src = ke < 64 ? r_lo : r_hi;
-              const int se = __builtin_amdgcn_readlane(src, ke & 63);
-              const int so = __builtin_amdgcn_readlane(src, (ke + 1) & 63);
-              const long long row = gather ? (long long)(lk ? so : se) : (long long)(ke + lk);
-              ra[d] = *(const float2*)(A + row * lda);
-            }
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-            if (kp + D < NKP) {
-              rb[d] = *(const float2*)bq;
-              bq += bstep;
-            }
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
-            cs0 += b0;
-            cs1 += b1;
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        } else {
-          for (int blk = 0; blk < nblk; ++blk) {
-#pragma unroll
-            for (int d = 0; d < D; ++d) slot(blk * D + d, d);
-          }
-        }
+        if (Kd == 128)
+          K::template unrolled<128>(acc, A, B, a.lda, a.ldb, gather, srm, lane, lk, cs0, cs1);
+        else if (Kd == 64)
+          K::template unrolled<64>(acc, A, B, a.lda, a.ldb, gather, srm, lane, lk, cs0, cs1);
+        else
+          K::generic(acc, A, B, a.lda, a.ldb, Kd, gather, srm, lk, cs0, cs1);
         if (nxt_rows) ws_rows_store(srmap[(j + 1) & 1], nr);
         if (a.bias_w && cur.m0 == 0 && wm0 == 0) {
           // lanes < 32 summed the even batch rows, lanes >= 32 the odd ones
@@ -815,13 +873,15 @@ __global__ __launch_bounds__(kWsThreads) void gemm_f32_sgd_ws(WsArgs w) {
 }
 
 // Shape and alignment rules of the specialised kernel for one problem.
+// fp32 operands are read as float2, bf16 operands as pairs in one 32-bit word.
 bool ws_eligible(int dtype, const GemmArgs& a) {
   auto al = [](const void* p, uintptr_t m) { return ((uintptr_t)p & m) == 0; };
-  return dtype == 0 && a.splits <= 1 && a.G > 0 && a.M > 0 && a.N > 0 && a.Kd > 0 &&
-         a.M % 128 == 0 && a.N % 128 == 0 &&
+  const uintptr_t pair = dtype == 0 ? 7 : 3;
+  return (dtype == 0 || dtype == 1) && a.splits <= 1 && a.G > 0 && a.M > 0 &&
+         a.N > 0 && a.Kd > 0 && a.M % 128 == 0 && a.N % 128 == 0 &&
          (a.rowmap == nullptr || a.Kd <= kWsMaxRows) &&
-         a.lda % 2 == 0 && a.sA % 2 == 0 && al(a.A, 7) &&
-         a.ldb % 2 == 0 && a.sB % 2 == 0 && al(a.B, 7) &&
+         a.lda % 2 == 0 && a.sA % 2 == 0 && al(a.A, pair) &&
+         a.ldb % 2 == 0 && a.sB % 2 == 0 && al(a.B, pair) &&
          a.ldc % 4 == 0 && a.sC % 4 == 0 && al(a.W, 15) && al(a.U, 15) &&
          (a.Wb == nullptr || al(a.Wb, 7));
 }
@@ -1018,6 +1078,7 @@ bool big_tile(int dtype, int M, int N) { return dtype == 0 && M >= 128 && N >= 1
 
 // Compute units and resident specialised-update workgroups per CU on the
 // current device, queried once per device.
+template <bool BF>
 hipError_t ws_grid(long long tiles, int& grid) {
   struct Shape {
     int cus = 0, per_cu = 0;
@@ -1032,7 +1093,7 @@ hipError_t ws_grid(long long tiles, int& grid) {
     e = hipDeviceGetAttribute(&sh.cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &sh.per_cu, reinterpret_cast<const void*>(gemm_f32_sgd_ws<kWsDepth>),
+        &sh.per_cu, reinterpret_cast<const void*>(gemm_f32_sgd_ws<BF, kWsDepth>),
         kWsThreads, 0);
     if (e != hipSuccess) return e;
     if (sh.per_cu < 1) sh.per_cu = 1;
@@ -1074,10 +1135,14 @@ hipError_t launch_gemm_sgd_multi(int dtype, const GemmArgs* list, int n,
       return hipErrorInvalidValue;
   }
   int grid = 0;
-  hipError_t e = ws_grid(total, grid);
+  hipError_t e = dtype == 1 ? ws_grid<true>(total, grid) : ws_grid<false>(total, grid);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((gemm_f32_sgd_ws<kWsDepth>), dim3(grid), dim3(kWsThreads), 0,
-                     s, w);
+  if (dtype == 1)
+    hipLaunchKernelGGL((gemm_f32_sgd_ws<true, kWsDepth>), dim3(grid), dim3(kWsThreads),
+                       0, s, w);
+  else
+    hipLaunchKernelGGL((gemm_f32_sgd_ws<false, kWsDepth>), dim3(grid), dim3(kWsThreads),
+                       0, s, w);
   return hipGetLastError();
 }
 

@@ -122,6 +122,21 @@ def test_persistent_update_kernel_shapes(widths, K, B, nesterov, seed):
     _compare_steps(w, X, y, w0, PARAM_TOL_FP32, 1e-4)
 
 
+@pytest.mark.parametrize("widths,K,B", [
+    ((256, 2048, 10), 32, 21),        # gathered bf16 rows, runtime k loop
+    ((512, 1024, 512, 10), 16, 64),   # both layers, unrolled 64-row k loop
+])
+def test_persistent_update_kernel_bf16(widths, K, B):
+    """bf16 GEMM operands through the persistent update kernel (bf16 pairs
+    widened to fp32 for the MFMAs; fp32 master weights and momentum, bf16
+    weight copy written by the update), every replica after every step."""
+    w = _small(widths, dtype="bf16", K=K, B=B, N=max(999, 4 * K), H=2,
+               rounds=2, lr=0.01)
+    print(f"persistent update bf16 {widths} K={K} B={B}", flush=True)
+    X, y, w0 = _small_data(w)
+    _compare_steps(w, X, y, w0, 2e-3, LOSS_TOL_BF16)
+
+
 @pytest.mark.parametrize("widths", [(70, 48, 36, 10), (64, 128, 64, 10),
                                     (72, 20), (40, 33, 45)])
 def test_small_mlp_bf16_every_step(widths):
