@@ -41,6 +41,7 @@ constexpr int kXcds = 8;
 // straight from memory becomes a memcpy, which keeps register arrays of it
 // in scratch memory
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float4 ldg4(const float* p) {
   const v4f v = *(const v4f*)p;
   return make_float4(v.x, v.y, v.z, v.w);
@@ -1036,6 +1037,108 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16(GemmArgs a, int vecA,
   if (do_bias && tid < BN && n0 + tid < N) bias_update(a, t, n0 + tid, colsum);
 }
 
+// bf16 operands, whole 64 x 64 tiles, A stored [M][Kd] (forward and input
+// gradient): a HBM-bound contraction at small M, so the point is to keep
+// many weight bytes in flight. Two register sets of branch-free 16-byte
+// loads (slab t+2 is loaded while slab t computes and slab t+1 waits in
+// LDS), BK = 64, prefetches past the end clamped to the last slab.
+template <bool BT, int EPI, bool GATHER>
+__global__ __launch_bounds__(kThreads) void gemm_bf16_full(GemmArgs a) {
+  constexpr int BM = 64, BN = 64, BK = 64, KP = BK + 8;  // 144-B rows
+  constexpr int FM = 1, FN = 1;
+  constexpr int NA = BM * BK / 8 / kThreads, NB = BN * BK / 8 / kThreads;
+  static_assert(NA == 2 && NB == 2, "tile shape");
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM][KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN][KP];
+
+  const Tile t = decode_tile(a, BM, BN);
+  const int g = t.g, m0 = t.m0, n0 = t.n0;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+  const bf16_t* A = (const bf16_t*)a.A + (long long)g * a.sA;
+  const bf16_t* B = (const bf16_t*)a.B + (long long)g * a.sB;
+  const int kbeg = t.s * a.kchunk;
+  const int nk = a.kchunk / BK;
+  // rows of A are fixed per thread: resolve the gathered indices once
+  long long arow[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int row = m0 + (tid + i * kThreads) / (BK / 8);
+    arow[i] = (GATHER ? (long long)a.rowmap[(long long)g * a.sRow + row] : (long long)row) * a.lda;
+  }
+  auto gload = [&](int k0, u32x4(&xa)[NA], u32x4(&xb)[NB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int q = tid + i * kThreads;
+      xa[i] = *(const u32x4*)(A + arow[i] + k0 + (q % (BK / 8)) * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int q = tid + i * kThreads;
+      if constexpr (BT)  // [N][Kd]
+        xb[i] = *(const u32x4*)(B + (long long)(n0 + q / (BK / 8)) * a.ldb + k0 + (q % (BK / 8)) * 8);
+      else  // [Kd][N]
+        xb[i] = *(const u32x4*)(B + (long long)(k0 + q / (BN / 8)) * a.ldb + n0 + (q % (BN / 8)) * 8);
+    }
+  };
+  auto lstore = [&](int buf, const u32x4(&xa)[NA], const u32x4(&xb)[NB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int q = tid + i * kThreads;
+      *(u32x4*)&As[buf][q / (BK / 8)][(q % (BK / 8)) * 8] = xa[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int q = tid + i * kThreads;
+      if constexpr (BT) {
+        *(u32x4*)&Bs[buf][q / (BK / 8)][(q % (BK / 8)) * 8] = xb[i];
+      } else {  // k row r, 8 consecutive n: transpose into Bs[n][k]
+        const int r = q / (BN / 8), c = (q % (BN / 8)) * 8;
+        const uint32_t wds[4] = {xb[i].x, xb[i].y, xb[i].z, xb[i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          Bs[buf][c + 2 * e][r] = (bf16_t)(wds[e] & 0xFFFFu);
+          Bs[buf][c + 2 * e + 1][r] = (bf16_t)(wds[e] >> 16);
+        }
+      }
+    }
+  };
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[0][0][v] = 0.f;
+  const int lk = lane >> 5, lr = lane & 31;
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      const bf16x8 av = *(const bf16x8*)&As[buf][wm0 + lr][kk + lk * 8];
+      const bf16x8 bv = *(const bf16x8*)&Bs[buf][wn0 + lr][kk + lk * 8];
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc[0][0], 0, 0, 0);
+    }
+  };
+  u32x4 ra0[NA], rb0[NB], ra1[NA], rb1[NB];
+  auto slab = [&](int s) __attribute__((always_inline)) { return kbeg + min(s, nk - 1) * BK; };
+  gload(slab(0), ra0, rb0);
+  gload(slab(1), ra1, rb1);
+  lstore(0, ra0, rb0);
+  __syncthreads();
+  int it = 0;
+  for (; it + 1 < nk; it += 2) {
+    gload(slab(it + 2), ra0, rb0);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);
+    lstore(1, ra1, rb1);
+    __syncthreads();
+    gload(slab(it + 3), ra1, rb1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);
+    lstore(0, ra0, rb0);
+    __syncthreads();
+  }
+  if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
+  constexpr bool OUTBF = EPI == EPI_BIAS_RELU || EPI == EPI_RELU_MASK;
+  epilogue_fragment<EPI, OUTBF, FM, FN>(a, t, acc, m0 + wm0, n0 + wn0, lk, lr);
+}
+
 // ------------------------------------------------------------------ split-K
 // C[g][m][n] = epilogue(sum_{s=0}^{S-1} part[s][g][m][n]), s ascending. S is
 // a template argument so all S loads are issued before the sum.
@@ -1179,6 +1282,17 @@ hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
   const int vecC = EPI == EPI_SGD && a.ldc % 4 == 0 && a.sC % 4 == 0 &&
                    aligned16(a.W) && aligned16(a.U) &&
                    (a.Wb == nullptr || ((uintptr_t)a.Wb & 7u) == 0);
+  if constexpr (!AT && EPI != EPI_SGD) {
+    if (dtype == 1 && vecA && vecB && a.M % 64 == 0 && a.N % 64 == 0 &&
+        a.kchunk % 64 == 0 && (long long)a.kchunk * a.splits == a.Kd) {
+      hipLaunchKernelGGL((gemm_bf16_full<BT, EPI, GATHER>), dim3(total), dim3(kThreads),
+                         0, s, a);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess || a.splits == 1) return e;
+      constexpr bool OUTBF_ACT = EPI == EPI_BIAS_RELU || EPI == EPI_RELU_MASK;
+      return launch_reduce<EPI, OUTBF_ACT>(a, s);
+    }
+  }
   if (dtype == 1)
     hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, 64, 64>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
