@@ -209,6 +209,152 @@ __global__ __launch_bounds__(kT) void k_conv_gemm(ConvArgs c, int vec) {
   }
 }
 
+// Forward / input-gradient convolution for reduction channel counts that
+// are multiples of 16 (every convolution after the first): the output tile
+// is 256 spatial rows x all BN (= 16, 32 or 64) channels, so no MFMA lane is
+// spent on channels that do not exist. A k slab of 16 is one tap (kh, kw)
+// and 16 consecutive channels, so a thread decodes its rows (image, output
+// position) once and each slab only moves the tap; padding and the stride-2
+// parity become a validity mask (address clamped, value zeroed), and the
+// loads carry no branches. Two register sets: slab t+2 is in flight while
+// slab t computes. Each wave owns 64 rows as 16 x 16 blocks of
+// v_mfma_f32_16x16x4f32 (lane l: A[m = l%16][k = l/16], B[k = l/16][n = l%16],
+// accumulator v at C[4 (l/16) + v][l%16]).
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int MODE, int BN>
+__global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
+  static_assert(MODE == CONV_FWD || MODE == CONV_DGRAD, "row-tiled modes");
+  constexpr int BM = 256, BK = 16, PK = BK + 4;  // 80-byte A rows in LDS
+  constexpr int NBL = BN / 16;                    // 16-wide column blocks
+  constexpr int RPT = BM * BK / 4 / kT;           // A float4 per thread (4)
+  constexpr int BQ = BK * BN / 4;                 // B float4 per slab
+  __shared__ __attribute__((aligned(16))) float As[2][BM][PK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + 4];
+
+  const int Cr = MODE == CONV_FWD ? c.Cin : c.Cout;  // reduction channels
+  const int HWo = MODE == CONV_FWD ? c.Ho * c.Wo : c.H * c.W;
+  const int Mg = c.Bt * HWo;
+  const int tiles = (Mg + BM - 1) / BM;
+  const int g = blockIdx.x / tiles, m0 = (blockIdx.x - g * tiles) * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kq = (tid & 3) * 4;  // this thread's 4 channels of the slab
+  const float* Bw = c.Wk + (long long)g * c.sW;  // [9 Cr][BN]
+
+  // rows of this thread: r = tid / 4 + 64 i
+  long long base[RPT];  // image (or output-gradient image) base, elements
+  int ya[RPT], xa[RPT];
+  bool rok[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int m = m0 + (tid >> 2) + 64 * i;
+    rok[i] = m < Mg;
+    const int mm = rok[i] ? m : 0;
+    const int b = mm / HWo, p = mm - b * HWo;
+    if constexpr (MODE == CONV_FWD) {
+      const int oh = p / c.Wo, ow = p - oh * c.Wo;
+      ya[i] = oh * c.stride - 1;  // input row of tap kh: ya + kh
+      xa[i] = ow * c.stride - 1;
+      base[i] = c.rowmap ? (long long)c.rowmap[(long long)g * c.Bt + b] * c.H * c.W * c.Cin
+                         : (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
+    } else {
+      const int h = p / c.W, w = p - h * c.W;
+      ya[i] = h + 1;  // output-gradient row of tap kh: (ya - kh) / stride
+      xa[i] = w + 1;
+      base[i] = ((long long)g * c.Bt + b) * c.Ho * c.Wo * c.Cout;
+    }
+  }
+  const float* src = MODE == CONV_FWD ? c.x : c.dy;
+  const int nk = 9 * Cr / BK;
+  auto gload = [&](int s, v4f(&xa4)[RPT], v4f& xb) __attribute__((always_inline)) {
+    const int tap = s / (Cr / BK), ch0 = (s - tap * (Cr / BK)) * BK + kq;
+    const int kh = tap / 3, kw = tap - kh * 3;
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      int yy, xx;
+      bool ok;
+      if constexpr (MODE == CONV_FWD) {
+        yy = ya[i] + kh;
+        xx = xa[i] + kw;
+        ok = rok[i] && yy >= 0 && yy < c.H && xx >= 0 && xx < c.W;
+        yy = ok ? yy : 0;
+        xx = ok ? xx : 0;
+        xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.W + xx) * c.Cin + ch0);
+      } else {
+        const int th = ya[i] - kh, tw = xa[i] - kw;
+        const int oh = c.stride == 1 ? th : th >> 1, ow = c.stride == 1 ? tw : tw >> 1;
+        ok = rok[i] && th >= 0 && tw >= 0 && oh < c.Ho && ow < c.Wo &&
+             (c.stride == 1 || ((th | tw) & 1) == 0);
+        yy = ok ? oh : 0;
+        xx = ok ? ow : 0;
+        xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.Wo + xx) * c.Cout + ch0);
+      }
+      if (!ok) xa4[i] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    const int bq = min(tid, BQ - 1);
+    xb = *(const v4f*)(Bw + (long long)(s * BK + bq / (BN / 4)) * BN + (bq % (BN / 4)) * 4);
+  };
+  auto lstore = [&](int buf, const v4f(&xa4)[RPT], const v4f& xb) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] = xa4[i];
+    if (tid < BQ) *(v4f*)&Bs[buf][tid / (BN / 4)][(tid % (BN / 4)) * 4] = xb;
+  };
+  floatx4 acc[4][NBL];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < NBL; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int lq = lane >> 4, lm = lane & 15;
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 4) {
+      float av[4], bv[NBL];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[buf][wave * 64 + i * 16 + lm][kk + lq];
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) bv[j] = Bs[buf][kk + lq][j * 16 + lm];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < NBL; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  };
+  v4f ra0[RPT], ra1[RPT], rb0, rb1;
+  auto slab = [&](int t) __attribute__((always_inline)) { return min(t, nk - 1); };
+  gload(slab(0), ra0, rb0);
+  gload(slab(1), ra1, rb1);
+  lstore(0, ra0, rb0);
+  __syncthreads();
+  int it = 0;
+  for (; it + 1 < nk; it += 2) {
+    gload(slab(it + 2), ra0, rb0);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);
+    lstore(1, ra1, rb1);
+    __syncthreads();
+    gload(slab(it + 3), ra1, rb1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);
+    lstore(0, ra0, rb0);
+    __syncthreads();
+  }
+  if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
+
+  float* out = c.out + (long long)g * Mg * BN;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int m = m0 + wave * 64 + i * 16 + lq * 4 + v;
+      if (m < Mg) {
+#pragma unroll
+        for (int j = 0; j < NBL; ++j) out[(long long)m * BN + j * 16 + lm] = acc[i][j][v];
+      }
+    }
+}
+
 // Weight gradient: sum the S partials (ascending s) and apply the update to
 // the [9*Cin][Cout] weight of every replica.
 template <int S>
@@ -498,10 +644,35 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
     c.mchunk = ((rows + c.splits - 1) / c.splits + 15) / 16 * 16;
     hipLaunchKernelGGL(k_conv_gemm<CONV_WGRAD>, dim3(tiles * c.splits * q.G), dim3(kT),
                        0, st, c, vec);
-  } else if (mode == CONV_FWD) {
-    hipLaunchKernelGGL(k_conv_gemm<CONV_FWD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
   } else {
-    hipLaunchKernelGGL(k_conv_gemm<CONV_DGRAD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
+    // row-tiled kernel: reduction channels a multiple of 16, output channels
+    // 16 / 32 / 64, 16-byte aligned tensors
+    const int Cr = mode == CONV_FWD ? q.Cin : q.Cout;
+    const bool rows = Cr % 16 == 0 && (Ng == 16 || Ng == 32 || Ng == 64) &&
+                      (q.stride == 1 || q.stride == 2) && ((uintptr_t)q.Wk & 15) == 0 &&
+                      (q.sW % 4 == 0) && (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0
+                                                           : ((uintptr_t)q.dy & 15) == 0) &&
+                      (mode == CONV_DGRAD || q.rowmap || q.sx % 4 == 0);
+    if (rows) {
+      const long long rt = (long long)((Mg + 255) / 256) * q.G;
+      if (rt > 0x7fffffffLL) return hipErrorInvalidValue;
+#define LSGD_ROWS(MD, NB)                                                              \
+  hipLaunchKernelGGL((k_conv_rows<MD, NB>), dim3((unsigned)rt), dim3(kT), 0, st, c)
+      if (mode == CONV_FWD) {
+        if (Ng == 16) LSGD_ROWS(CONV_FWD, 16);
+        else if (Ng == 32) LSGD_ROWS(CONV_FWD, 32);
+        else LSGD_ROWS(CONV_FWD, 64);
+      } else {
+        if (Ng == 16) LSGD_ROWS(CONV_DGRAD, 16);
+        else if (Ng == 32) LSGD_ROWS(CONV_DGRAD, 32);
+        else LSGD_ROWS(CONV_DGRAD, 64);
+      }
+#undef LSGD_ROWS
+    } else if (mode == CONV_FWD) {
+      hipLaunchKernelGGL(k_conv_gemm<CONV_FWD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
+    } else {
+      hipLaunchKernelGGL(k_conv_gemm<CONV_DGRAD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
+    }
   }
   return hipGetLastError();
 }
