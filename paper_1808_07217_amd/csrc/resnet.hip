@@ -355,6 +355,142 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
 }
 
+// Weight gradient of a convolution with 16 / 32 / 64 channels in and out:
+// workgroup (replica g, tap t, split s) forms the partial
+//   dW[t][ci][co] = sum over output positions p of chunk s of
+//                   x(p shifted by tap t)[ci] * dy[p][co]
+// for all CI x CO channels of the tap. Slabs of 64 consecutive positions
+// (64 divides H_o W_o, so a slab lies in one image) go through LDS with
+// float4 loads of whole channel rows (padding taps masked to zero); each of
+// the 4 waves takes 16 positions of the slab and accumulates the full
+// CI x CO block on v_mfma_f32_16x16x4f32. The four waves' sums are added in
+// wave order at the end. Partials land in [S][G][9 CI][CO] as for the GEMM
+// form, reduced over s by k_conv_wupdate.
+template <int CI, int CO>
+__global__ __launch_bounds__(kT) void k_conv_wgrad_rows(ConvArgs c) {
+  constexpr int SP = 64;                       // positions per slab
+  constexpr int XQ = SP * CI / 4, DQ = SP * CO / 4;
+  constexpr int XPT = (XQ + kT - 1) / kT, DPT = (DQ + kT - 1) / kT;
+  constexpr int MB = CI / 16, NB = CO / 16;
+  constexpr int XP = CI + 4, DP = CO + 4;      // LDS pitches (16-byte rows)
+  constexpr int LDSF = 2 * SP * XP + 2 * SP * DP;
+  static_assert(4 * CI * CO <= LDSF, "wave reduction fits the slab buffers");
+  __shared__ __attribute__((aligned(16))) float lds[LDSF];
+  float* Xs = lds;                  // [2][SP][XP]
+  float* Ds = lds + 2 * SP * XP;    // [2][SP][DP]
+
+  const int S = c.splits;
+  int l = blockIdx.x;
+  const int sp = l % S;
+  l /= S;
+  const int tap = l % 9, g = l / 9;
+  const int kh = tap / 3, kw = tap - kh * 3;
+  const int HWo = c.Ho * c.Wo, rows = c.Bt * HWo;
+  const int kbeg = sp * c.mchunk, kend = min(rows, kbeg + c.mchunk);
+  const int nsl = kend > kbeg ? (kend - kbeg) / SP : 0;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lq = lane >> 4, lm = lane & 15;
+
+  auto gload = [&](int j, v4f(&xr)[XPT], v4f(&dr)[DPT]) __attribute__((always_inline)) {
+    const int p0 = kbeg + j * SP;
+    const int b = p0 / HWo, pl0 = p0 - b * HWo;
+    const long long img = (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+      const int q = min(tid + kT * i, XQ - 1);
+      const int pos = q / (CI / 4), c4 = (q - pos * (CI / 4)) * 4;
+      const int pl = pl0 + pos, oh = pl / c.Wo, ow = pl - oh * c.Wo;
+      const int ih = oh * c.stride + kh - 1, iw = ow * c.stride + kw - 1;
+      const bool ok = ih >= 0 && ih < c.H && iw >= 0 && iw < c.W;
+      const long long o = img + ((long long)(ok ? ih : 0) * c.W + (ok ? iw : 0)) * c.Cin + c4;
+      xr[i] = *(const v4f*)(c.x + o);
+      if (!ok) xr[i] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+    const long long drow = ((long long)g * c.Bt + b) * HWo + pl0;
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int q = min(tid + kT * i, DQ - 1);
+      const int pos = q / (CO / 4), c4 = (q - pos * (CO / 4)) * 4;
+      dr[i] = *(const v4f*)(c.dy + (drow + pos) * c.Cout + c4);
+    }
+  };
+  auto lstore = [&](int buf, const v4f(&xr)[XPT], const v4f(&dr)[DPT]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+      const int q = tid + kT * i;
+      if (q < XQ) {
+        const int pos = q / (CI / 4), c4 = (q - pos * (CI / 4)) * 4;
+        *(v4f*)&Xs[(buf * SP + pos) * XP + c4] = xr[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int q = tid + kT * i;
+      if (q < DQ) {
+        const int pos = q / (CO / 4), c4 = (q - pos * (CO / 4)) * 4;
+        *(v4f*)&Ds[(buf * SP + pos) * DP + c4] = dr[i];
+      }
+    }
+  };
+  floatx4 acc[MB][NB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int pos = wave * 16 + kk * 4 + lq;
+      float av[MB], bv[NB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) av[i] = Xs[(buf * SP + pos) * XP + i * 16 + lm];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) bv[j] = Ds[(buf * SP + pos) * DP + j * 16 + lm];
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  };
+  if (nsl > 0) {
+    v4f xr0[XPT], xr1[XPT], dr0[DPT], dr1[DPT];
+    auto slab = [&](int t) __attribute__((always_inline)) { return min(t, nsl - 1); };
+    gload(slab(0), xr0, dr0);
+    gload(slab(1), xr1, dr1);
+    lstore(0, xr0, dr0);
+    __syncthreads();
+    int it = 0;
+    for (; it + 1 < nsl; it += 2) {
+      gload(slab(it + 2), xr0, dr0);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, xr1, dr1);
+      __syncthreads();
+      gload(slab(it + 3), xr1, dr1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      lstore(0, xr0, dr0);
+      __syncthreads();
+    }
+    if (it < nsl) compute(0);
+  }
+  // the four waves' sums, added in wave order: block (i, j) register v of
+  // lane l is dW[16 i + 4 (l/16) + v][16 j + l%16]
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        lds[wave * CI * CO + (i * 16 + lq * 4 + v) * CO + j * 16 + lm] = acc[i][j][v];
+  __syncthreads();
+  float* out = c.out + ((long long)sp * c.G + g) * 9 * CI * CO + (long long)tap * CI * CO;
+  for (int e = tid; e < CI * CO; e += kT)
+    out[e] = ((lds[e] + lds[CI * CO + e]) + lds[2 * CI * CO + e]) + lds[3 * CI * CO + e];
+}
+
 // Weight gradient: sum the S partials (ascending s) and apply the update to
 // the [9*Cin][Cout] weight of every replica.
 template <int S>
@@ -641,6 +777,26 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   if (mode == CONV_WGRAD) {
     c.splits = conv_wgrad_splits(q.Bt, q.Ho, q.Wo);
     const int rows = q.Bt * q.Ho * q.Wo;
+    auto chan = [](int v) { return v == 16 || v == 32 || v == 64; };
+    const bool rowsk = chan(q.Cin) && chan(q.Cout) && q.Cout >= q.Cin && !q.rowmap &&
+                       (q.Ho * q.Wo) % 64 == 0 && ((uintptr_t)q.x & 15) == 0 &&
+                       ((uintptr_t)q.dy & 15) == 0 && q.sx % 4 == 0;
+    if (rowsk) {
+      // whole 64-position slabs per split
+      c.mchunk = ((rows + c.splits - 1) / c.splits + 63) / 64 * 64;
+      const dim3 grid((unsigned)(q.G * 9 * c.splits));
+#define LSGD_WG(CI, CO)                                                                \
+  if (q.Cin == CI && q.Cout == CO) {                                                   \
+    hipLaunchKernelGGL((k_conv_wgrad_rows<CI, CO>), grid, dim3(kT), 0, st, c);         \
+    return hipGetLastError();                                                          \
+  }
+      LSGD_WG(16, 16)
+      LSGD_WG(16, 32)
+      LSGD_WG(32, 32)
+      LSGD_WG(32, 64)
+      LSGD_WG(64, 64)
+#undef LSGD_WG
+    }
     c.mchunk = ((rows + c.splits - 1) / c.splits + 15) / 16 * 16;
     hipLaunchKernelGGL(k_conv_gemm<CONV_WGRAD>, dim3(tiles * c.splits * q.G), dim3(kT),
                        0, st, c, vec);
