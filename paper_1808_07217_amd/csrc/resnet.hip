@@ -688,6 +688,173 @@ __global__ void k_bn_bwd_apply(const float* y, const float* gup, const float* ma
   }
 }
 
+// ---- float4 forms of the BN passes (channel count C a power of two >= 16):
+// the replica is the grid's y coordinate and a thread owns 4 consecutive
+// channels of one row, so the channel is a mask of the index and no 64-bit
+// division is left in the inner work.
+
+// Partial sums as k_bn_partial (same chunks, same fp64 sums per channel;
+// rows of a chunk interleaved over the 1024 / C row lanes of a workgroup,
+// then added in a fixed tree).
+__global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C,
+                                                    const float* gup, const float* maskv,
+                                                    const float* mu, const float* inv,
+                                                    double* part, int nchunk) {
+  __shared__ double red[2][4][kT];
+  const int g = blockIdx.y, ch = blockIdx.x;
+  const int cq = C / 4;  // threads per row
+  const int c0 = (threadIdx.x % cq) * 4, lane_r = threadIdx.x / cq, rstep = kT / cq;
+  const long long base = (long long)g * R * C;
+  const int r0 = ch * kChunkRows, r1 = min(R, r0 + kChunkRows);
+  const bool bwd = gup != nullptr;
+  float m_c[4], i_c[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    m_c[e] = bwd ? mu[g * C + c0 + e] : 0.f;
+    i_c[e] = bwd ? inv[g * C + c0 + e] : 0.f;
+  }
+  double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int rb = r0 + lane_r; rb < r1; rb += 4 * rstep) {
+    v4f yv[4], gv[4], mv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = min(rb + u * rstep, r1 - 1);
+      const long long o = base + (long long)r * C + c0;
+      yv[u] = *(const v4f*)(y + o);
+      gv[u] = bwd ? *(const v4f*)(gup + o) : v4f{0.f, 0.f, 0.f, 0.f};
+      mv[u] = maskv ? *(const v4f*)(maskv + o) : v4f{1.f, 1.f, 1.f, 1.f};
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (rb + u * rstep >= r1) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (!bwd) {
+          s0[e] += (double)yv[u][e];
+          s1[e] += (double)yv[u][e] * (double)yv[u][e];
+        } else {
+          const float dz = mv[u][e] > 0.f ? gv[u][e] : 0.f;
+          const float xh = (yv[u][e] - m_c[e]) * i_c[e];
+          s0[e] += (double)dz;
+          s1[e] += (double)dz * (double)xh;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    red[0][e][threadIdx.x] = s0[e];
+    red[1][e][threadIdx.x] = s1[e];
+  }
+  __syncthreads();
+  for (int w = kT / 2; w >= cq; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        red[0][e][threadIdx.x] += red[0][e][threadIdx.x + w];
+        red[1][e][threadIdx.x] += red[1][e][threadIdx.x + w];
+      }
+    }
+    __syncthreads();
+  }
+  if ((int)threadIdx.x < cq) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      double* p = part + (((long long)g * nchunk + ch) * C + c0 + e) * 2;
+      p[0] = red[0][e][threadIdx.x];
+      p[1] = red[1][e][threadIdx.x];
+    }
+  }
+}
+
+// k_bn_apply, 4 channels per thread.
+__global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, int cshift,
+                                                  const float* mu, const float* inv,
+                                                  const float* gamma, const float* beta,
+                                                  long long sP, int mode, const float* xin,
+                                                  int Ho, int Wo, int Cin, float* out) {
+  const int g = blockIdx.y;
+  const int j = blockIdx.x * kT + threadIdx.x;
+  if (j >= R * C / 4) return;
+  const int e4 = 4 * j, c0 = e4 & (C - 1), r = e4 >> cshift;
+  const long long o = (long long)g * R * C + e4;
+  const v4f yv = *(const v4f*)(y + o);
+  v4f xv = v4f{0.f, 0.f, 0.f, 0.f};
+  if (mode == 1) {
+    xv = *(const v4f*)(xin + o);
+  } else if (mode == 2 && c0 < Cin) {
+    const int HWo = Ho * Wo, b = r / HWo, p = r - b * HWo;
+    const int oh = p / Wo, ow = p - oh * Wo;
+    const int H = 2 * Ho, W = 2 * Wo, Bt = R / HWo;
+    xv = *(const v4f*)(xin + (((long long)g * Bt + b) * H * W + (long long)(2 * oh) * W +
+                              2 * ow) * Cin + c0);
+  }
+  v4f res;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int c = c0 + e;
+    const float z = gamma[(long long)g * sP + c] * (yv[e] - mu[g * C + c]) * inv[g * C + c] +
+                    beta[(long long)g * sP + c];
+    const float v = z + xv[e];
+    res[e] = v > 0.f ? v : 0.f;
+  }
+  *(v4f*)(out + o) = res;
+}
+
+// k_bn_bwd_apply, 4 channels per thread.
+__global__ __launch_bounds__(kT) void k_bn_bwd_apply4(const float* y, const float* gup,
+                                                      const float* maskv, int R, int C,
+                                                      const float* mu, const float* inv,
+                                                      const float* coef, float* dy) {
+  const int g = blockIdx.y;
+  const int j = blockIdx.x * kT + threadIdx.x;
+  if (j >= R * C / 4) return;
+  const int e4 = 4 * j, c0 = e4 & (C - 1);
+  const long long o = (long long)g * R * C + e4;
+  const v4f yv = *(const v4f*)(y + o), gv = *(const v4f*)(gup + o),
+            mv = *(const v4f*)(maskv + o);
+  v4f res;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int gc = g * C + c0 + e;
+    const float dz = mv[e] > 0.f ? gv[e] : 0.f;
+    const float xh = (yv[e] - mu[gc]) * inv[gc];
+    res[e] = coef[gc * 3] * (dz - coef[gc * 3 + 1] - xh * coef[gc * 3 + 2]);
+  }
+  *(v4f*)(dy + o) = res;
+}
+
+// k_shortcut_grad, 4 channels per thread. Identity: every element of dx.
+// Option A: one thread per (output position, 4 of the first Cin channels),
+// adding to the even input pixel it was taken from.
+__global__ __launch_bounds__(kT) void k_shortcut_grad4(float* dx, const float* dh_out,
+                                                       const float* h_out, int Bt, int H,
+                                                       int W, int Cin, int Cout, int mode) {
+  const int g = blockIdx.y;
+  const int j = blockIdx.x * kT + threadIdx.x;
+  if (mode == 1) {
+    if (j >= Bt * H * W * Cin / 4) return;
+    const long long o = (long long)g * Bt * H * W * Cin + 4 * j;
+    v4f d = *(const v4f*)(dx + o);
+    const v4f a = *(const v4f*)(h_out + o), gq = *(const v4f*)(dh_out + o);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) d[e] += a[e] > 0.f ? gq[e] : 0.f;
+    *(v4f*)(dx + o) = d;
+    return;
+  }
+  const int Ho = H / 2, Wo = W / 2, cq = Cin / 4;
+  if (j >= Bt * Ho * Wo * cq) return;
+  const int c0 = (j % cq) * 4, pos = j / cq;  // pos = (b, oh, ow)
+  const int b = pos / (Ho * Wo), p = pos - b * Ho * Wo, oh = p / Wo, ow = p - oh * Wo;
+  const long long oo = ((long long)g * Bt * Ho * Wo + pos) * Cout + c0;
+  const long long oi = (((long long)g * Bt + b) * H * W + (long long)(2 * oh) * W + 2 * ow) * Cin + c0;
+  v4f d = *(const v4f*)(dx + oi);
+  const v4f a = *(const v4f*)(h_out + oo), gq = *(const v4f*)(dh_out + oo);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) d[e] += a[e] > 0.f ? gq[e] : 0.f;
+  *(v4f*)(dx + oi) = d;
+}
+
 // Gradient reaching a block's input: dx (from the first convolution of the
 // block) plus the shortcut's share of g = dh_out masked by h_out > 0:
 // identity (mode 1) or option A (mode 2: even pixels, first Cin channels).
@@ -863,13 +1030,26 @@ hipError_t launch_conv_wt(const float* W, long long sP, int G, int Cin, int Cout
   return hipGetLastError();
 }
 
+// Channel counts the float4 BN forms take: powers of two from 16, aligned.
+int bn_vec_shift(int C) {
+  if (C < 16 || (C & (C - 1))) return -1;
+  int s = 0;
+  while ((1 << s) < C) ++s;
+  return s;
+}
+bool al16p(const void* p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
+
 int bn_chunks(int R) { return (R + kChunkRows - 1) / kChunkRows; }
 
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
                            float* mu, float* inv, hipStream_t st) {
   const int nch = bn_chunks(R);
-  hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
-                     nullptr, nullptr, nullptr, part, nch);
+  if (bn_vec_shift(C) >= 0 && al16p(y) && (long long)R * C < (1LL << 31) && G <= 65535)
+    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
+                       nullptr, nullptr, nullptr, part, nch);
+  else
+    hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
+                       nullptr, nullptr, nullptr, part, nch);
   hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
                      nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
                      nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
@@ -880,6 +1060,13 @@ hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
                            int Cin, float* out, hipStream_t st) {
+  const int cs = bn_vec_shift(C);
+  if (cs >= 0 && al16p(y) && al16p(out) && al16p(xin) && Cin % 4 == 0 &&
+      (long long)R * C < (1LL << 31) && G <= 65535) {
+    hipLaunchKernelGGL(k_bn_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0, st,
+                       y, R, C, cs, mu, inv, gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_bn_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0, st,
                      y, R, C, mu, inv, gamma, beta, sP, G, mode, xin, Ho, Wo, Cin, out);
   return hipGetLastError();
@@ -891,19 +1078,38 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
                               float* ug, float* ub, long long sP, float lr, float mom,
                               int nesterov, float* dy, hipStream_t st) {
   const int nch = bn_chunks(R);
-  hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
-                     mu, inv, part, nch);
+  const bool v4 = bn_vec_shift(C) >= 0 && al16p(y) && al16p(gup) && al16p(maskv) &&
+                  al16p(dy) && maskv != nullptr && (long long)R * C < (1LL << 31) &&
+                  G <= 65535;
+  if (v4)
+    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
+                       mu, inv, part, nch);
+  else
+    hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
+                       mu, inv, part, nch);
   hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
                      nch, G, C, R, (float*)mu, (float*)inv, coef, gamma, beta, ug, ub,
                      sP, lr, mom, nesterov, 1e-5f);
-  hipLaunchKernelGGL(k_bn_bwd_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0,
-                     st, y, gup, maskv, R, C, G, mu, inv, coef, dy);
+  if (v4)
+    hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
+                       st, y, gup, maskv, R, C, mu, inv, coef, dy);
+  else
+    hipLaunchKernelGGL(k_bn_bwd_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0,
+                       st, y, gup, maskv, R, C, G, mu, inv, coef, dy);
   return hipGetLastError();
 }
 
 hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
                                 int G, int Bt, int H, int W, int Cin, int Cout,
                                 int mode, hipStream_t st) {
+  if (Cin % 4 == 0 && Cout % 4 == 0 && al16p(dx) && al16p(dh_out) && al16p(h_out) &&
+      (long long)Bt * H * W * Cin < (1LL << 31) && G <= 65535 && H % 2 == 0 && W % 2 == 0) {
+    const long long n4 = mode == 1 ? (long long)Bt * H * W * Cin / 4
+                                   : (long long)Bt * (H / 2) * (W / 2) * (Cin / 4);
+    hipLaunchKernelGGL(k_shortcut_grad4, dim3((unsigned)((n4 + kT - 1) / kT), G), dim3(kT),
+                       0, st, dx, dh_out, h_out, Bt, H, W, Cin, Cout, mode);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_shortcut_grad, dim3(blocks_for((long long)G * Bt * H * W * Cin)),
                      dim3(kT), 0, st, dx, dh_out, h_out, G, Bt, H, W, Cin, Cout, mode);
   return hipGetLastError();
