@@ -637,6 +637,64 @@ __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int 
   ub[o] = u;
 }
 
+// k_bn_finalize with the chunk sums spread over a workgroup per replica:
+// lane q of channel c adds chunks q, q + L, q + 2L, ... (L = 256 / C lanes,
+// ascending), then the lanes are added in a fixed tree; thread c < C then
+// finalises as k_bn_finalize does.
+__global__ __launch_bounds__(kT) void k_bn_finalize_wg(
+    const double* part, int nchunk, int C, int R, float* mu, float* inv, float* coef,
+    float* gamma, float* beta, float* ug, float* ub, long long sP, float lr, float mom,
+    int nesterov, float eps) {
+  __shared__ double red[2][kT];
+  const int g = blockIdx.x, t = threadIdx.x;
+  const int L = kT / C, c = t % C, q = t / C;
+  double s0 = 0.0, s1 = 0.0;
+  for (int ch = q; ch < nchunk; ch += L) {
+    const double* p = part + (((long long)g * nchunk + ch) * C + c) * 2;
+    s0 += p[0];
+    s1 += p[1];
+  }
+  red[0][t] = s0;
+  red[1][t] = s1;
+  __syncthreads();
+  for (int w = kT / 2; w >= C; w >>= 1) {
+    if (t < w) {
+      red[0][t] += red[0][t + w];
+      red[1][t] += red[1][t + w];
+    }
+    __syncthreads();
+  }
+  if (t >= C) return;
+  s0 = red[0][t];
+  s1 = red[1][t];
+  const int i = g * C + c;
+  if (coef == nullptr) {  // forward statistics
+    const double m = s0 / R;
+    double var = s1 / R - m * m;
+    if (var < 0.0) var = 0.0;
+    mu[i] = (float)m;
+    inv[i] = (float)(1.0 / sqrt(var + (double)eps));
+    return;
+  }
+  const long long o = (long long)g * sP + c;
+  float gm = gamma[o], bt = beta[o];
+  coef[i * 3 + 0] = gm * inv[i];
+  coef[i * 3 + 1] = (float)(s0 / R);
+  coef[i * 3 + 2] = (float)(s1 / R);
+  float u = ug[o];
+  const float dgm = (float)s1;
+  u = __builtin_fmaf(mom, u, dgm);
+  float d = nesterov ? __builtin_fmaf(mom, u, dgm) : u;
+  gamma[o] = __builtin_fmaf(-lr, d, gm);
+  ug[o] = u;
+  u = ub[o];
+  const float dbt = (float)s0;
+  u = __builtin_fmaf(mom, u, dbt);
+  d = nesterov ? __builtin_fmaf(mom, u, dbt) : u;
+  beta[o] = __builtin_fmaf(-lr, d, bt);
+  ub[o] = u;
+}
+
 // z = gamma*(y - mu)*inv + beta; then one of
 //   mode 0: out = relu(z)
 //   mode 1: out = relu(z + x_in)               (identity shortcut)
@@ -1050,9 +1108,14 @@ hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
   else
     hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
                        nullptr, nullptr, nullptr, part, nch);
-  hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
-                     nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
-                     nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
+  if (bn_vec_shift(C) >= 0 && C <= kT)
+    hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R, mu,
+                       inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
+                       1e-5f);
+  else
+    hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
+                       nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
+                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
   return hipGetLastError();
 }
 
@@ -1087,9 +1150,14 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
   else
     hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
                        mu, inv, part, nch);
-  hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
-                     nch, G, C, R, (float*)mu, (float*)inv, coef, gamma, beta, ug, ub,
-                     sP, lr, mom, nesterov, 1e-5f);
+  if (bn_vec_shift(C) >= 0 && C <= kT)
+    hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
+                       (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
+                       nesterov, 1e-5f);
+  else
+    hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
+                       nch, G, C, R, (float*)mu, (float*)inv, coef, gamma, beta, ug, ub,
+                       sP, lr, mom, nesterov, 1e-5f);
   if (v4)
     hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
                        st, y, gup, maskv, R, C, mu, inv, coef, dy);
