@@ -355,6 +355,97 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
 }
 
+// Stride-1 convolution with 16 channels in and out on 32-wide images (the
+// first stage): workgroup (g, b, band) computes 8 output rows x 32 columns x
+// 16 channels. The input rows h0-1 .. h0+8 (zero-padded) and the 144 x 16
+// weights go to LDS once and all 9 taps read shifted views of the tile, so
+// each input value is fetched from memory about 1.25 times rather than once
+// per tap. Input gradient: the same convolution applied to dy with the
+// kernel flipped -- tap (kh, kw) uses weight row (2-kh, 2-kw) -- read from
+// the transposed copy Wt[(kh, kw, co)][ci]. Wave w owns output rows
+// h0 + 2w, h0 + 2w + 1 as four 16 x 16 blocks of v_mfma_f32_16x16x4f32.
+template <int MODE>
+__global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
+  constexpr int C = 16, CP = C + 4;          // 80-byte pixel pitch in LDS
+  constexpr int W = 32, BH = 8;
+  constexpr int TW = W + 2, TH = BH + 2;
+  constexpr int TQ = TH * TW * (C / 4);      // float4 of the input tile
+  constexpr int WQ = 9 * C * (C / 4);        // float4 of the weights
+  constexpr int TPT = (TQ + kT - 1) / kT, WPT = (WQ + kT - 1) / kT;
+  __shared__ __attribute__((aligned(16))) float T[TH * TW * CP];
+  __shared__ __attribute__((aligned(16))) float Ws[9 * C * CP];
+  const int H = c.H, bands = H / BH;
+  int l = blockIdx.x;
+  const int band = l % bands;
+  l /= bands;
+  const int b = l % c.Bt, g = l / c.Bt;
+  const int h0 = band * BH;
+  const float* src = MODE == CONV_FWD
+                         ? c.x + (long long)g * c.sx + (long long)b * H * W * C
+                         : c.dy + ((long long)g * c.Bt + b) * H * W * C;
+  const float* Wg = c.Wk + (long long)g * c.sW;
+  // every load issued before the LDS stores (clamped addresses, zero-masked)
+  v4f tv[TPT], wv[WPT];
+#pragma unroll
+  for (int i = 0; i < TPT; ++i) {
+    const int q = min((int)threadIdx.x + kT * i, TQ - 1);
+    const int pix = q >> 2, c4 = (q & 3) * 4;
+    const int tr = pix / TW, tc = pix - tr * TW;
+    const int ih = h0 - 1 + tr, iw = tc - 1;
+    const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
+    tv[i] = *(const v4f*)(src + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
+    if (!ok) tv[i] = v4f{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int q = min((int)threadIdx.x + kT * i, WQ - 1);
+    const int row = q >> 2, c4 = (q & 3) * 4;
+    const int tap = row / C, r = row - tap * C;
+    const int srow = MODE == CONV_FWD ? row : (8 - tap) * C + r;
+    wv[i] = *(const v4f*)(Wg + (long long)srow * C + c4);
+  }
+#pragma unroll
+  for (int i = 0; i < TPT; ++i) {
+    const int q = (int)threadIdx.x + kT * i;
+    if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = tv[i];
+  }
+#pragma unroll
+  for (int i = 0; i < WPT; ++i) {
+    const int q = (int)threadIdx.x + kT * i;
+    if (q < WQ) *(v4f*)&Ws[(q >> 2) * CP + (q & 3) * 4] = wv[i];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lq = lane >> 4, lm = lane & 15;
+  floatx4 acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap) {
+    const int kh = tap / 3, kw = tap - kh * 3;
+#pragma unroll
+    for (int cq = 0; cq < 4; ++cq) {
+      const int ci = cq * 4 + lq;
+      const float bv = Ws[(tap * C + ci) * CP + lm];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // output (row 2w + i/2, col 16 (i%2) + lm) reads tile (row + kh, col + kw)
+        const int tr = 2 * wave + (i >> 1) + kh, tc = 16 * (i & 1) + lm + kw;
+        const float av = T[(tr * TW + tc) * CP + ci];
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i], 0, 0, 0);
+      }
+    }
+  }
+  float* out = c.out + ((long long)g * c.Bt + b) * H * W * C;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
+      out[((long long)row * W + col) * C + lm] = acc[i][v];
+    }
+}
+
 // Weight gradient of a convolution with 16 / 32 / 64 channels in and out:
 // workgroup (replica g, tap t, split s) forms the partial
 //   dW[t][ci][co] = sum over output positions p of chunk s of
@@ -1034,7 +1125,19 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
                       (q.sW % 4 == 0) && (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0
                                                            : ((uintptr_t)q.dy & 15) == 0) &&
                       (mode == CONV_DGRAD || q.rowmap || q.sx % 4 == 0);
-    if (rows) {
+    const bool halo = q.Cin == 16 && q.Cout == 16 && q.stride == 1 && q.W == 32 &&
+                      q.Wo == 32 && q.H == q.Ho && q.H % 8 == 0 && !q.rowmap &&
+                      ((uintptr_t)q.Wk & 15) == 0 && q.sW % 4 == 0 &&
+                      ((uintptr_t)(mode == CONV_FWD ? q.x : q.dy) & 15) == 0 &&
+                      (mode == CONV_DGRAD || q.sx % 4 == 0);
+    if (halo) {
+      const long long nb = (long long)q.G * q.Bt * (q.H / 8);
+      if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
+      if (mode == CONV_FWD)
+        hipLaunchKernelGGL((k_conv_halo16<CONV_FWD>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+      else
+        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+    } else if (rows) {
       const long long rt = (long long)((Mg + 255) / 256) * q.G;
       if (rt > 0x7fffffffLL) return hipErrorInvalidValue;
 #define LSGD_ROWS(MD, NB)                                                              \
