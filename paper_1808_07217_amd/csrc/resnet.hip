@@ -446,6 +446,91 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
     }
 }
 
+// Weight gradient of the first-stage 16 -> 16 stride-1 convolution (32-wide
+// images) from the same halo tiles: workgroup (g, split s) walks its bands
+// of 8 x 32 output positions; per band the input rows h0-1 .. h0+8 and the
+// band's output gradients go to LDS, and each wave takes 64 of the 256
+// positions and accumulates all nine taps' 16 x 16 blocks
+//   dW[tap][ci][co] += x(p shifted by tap)[ci] * dy[p][co].
+// The four waves' sums are added in wave order; the partial lands in
+// [S][G][144][16] for k_conv_wupdate.
+__global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
+  constexpr int C = 16, CP = C + 4;
+  constexpr int W = 32, BH = 8, TW = W + 2, TH = BH + 2;
+  constexpr int TQ = TH * TW * (C / 4), DQ = BH * W * (C / 4);
+  constexpr int TPT = (TQ + kT - 1) / kT, DPT = DQ / kT;
+  static_assert(DQ % kT == 0, "band gradient tile");
+  // one array: the input tile, the band's gradients, and at the end the
+  // four waves' sums in the same space
+  __shared__ __attribute__((aligned(16))) float lds[TH * TW * CP + BH * W * CP];
+  float* T = lds;
+  float* Dsh = lds + TH * TW * CP;
+  const int H = c.H, bpi = H / BH;               // bands per image
+  const int S = c.splits, sp = blockIdx.x % S, g = blockIdx.x / S;
+  const int nb = c.Bt * bpi, per = (nb + S - 1) / S;
+  const int bb = sp * per, be = min(nb, bb + per);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lq = lane >> 4, lm = lane & 15;
+  floatx4 acc[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int bd = bb; bd < be; ++bd) {
+    const int b = bd / bpi, h0 = (bd - b * bpi) * BH;
+    const float* xs = c.x + (long long)g * c.sx + (long long)b * H * W * C;
+    const float* ds = c.dy + (((long long)g * c.Bt + b) * H + h0) * W * C;
+    v4f tv[TPT], dv[DPT];
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int q = min((int)threadIdx.x + kT * i, TQ - 1);
+      const int pix = q >> 2, c4 = (q & 3) * 4;
+      const int tr = pix / TW, tc = pix - tr * TW;
+      const int ih = h0 - 1 + tr, iw = tc - 1;
+      const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
+      tv[i] = *(const v4f*)(xs + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
+      if (!ok) tv[i] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) dv[i] = *(const v4f*)(ds + 4 * ((int)threadIdx.x + kT * i));
+    __syncthreads();  // the previous band's tiles are no longer read
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int q = (int)threadIdx.x + kT * i;
+      if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = tv[i];
+    }
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int q = (int)threadIdx.x + kT * i;
+      *(v4f*)&Dsh[(q >> 2) * CP + (q & 3) * 4] = dv[i];
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int ks = 0; ks < 16; ++ks) {
+      // position of this lane's k: row 2w + ks/8, column 4 (ks%8) + lq
+      const int pr = 2 * wave + (ks >> 3), pc = 4 * (ks & 7) + lq;
+      const float bv = Dsh[(pr * W + pc) * CP + lm];
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int kh = t / 3, kw = t - kh * 3;
+        const float av = T[((pr + kh) * TW + pc + kw) * CP + lm];
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t], 0, 0, 0);
+      }
+    }
+  }
+  // waves in order; block t register v of lane l: dW[t][4 (l/16) + v][l%16]
+  __syncthreads();
+  float* red = lds;  // 4 x 144 x 16 floats fit the tile space (6800 + 5120)
+  static_assert(4 * 9 * C * C <= TH * TW * CP + BH * W * CP, "reduction space");
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      red[wave * 9 * C * C + (t * C + lq * 4 + v) * C + lm] = acc[t][v];
+  __syncthreads();
+  float* out = c.out + ((long long)sp * c.G + g) * 9 * C * C;
+  for (int e = threadIdx.x; e < 9 * C * C; e += kT)
+    out[e] = ((red[e] + red[9 * C * C + e]) + red[2 * 9 * C * C + e]) + red[3 * 9 * C * C + e];
+}
+
 // Weight gradient of a convolution with 16 / 32 / 64 channels in and out:
 // workgroup (replica g, tap t, split s) forms the partial
 //   dW[t][ci][co] = sum over output positions p of chunk s of
@@ -1097,6 +1182,15 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
     const bool rowsk = chan(q.Cin) && chan(q.Cout) && q.Cout >= q.Cin && !q.rowmap &&
                        (q.Ho * q.Wo) % 64 == 0 && ((uintptr_t)q.x & 15) == 0 &&
                        ((uintptr_t)q.dy & 15) == 0 && q.sx % 4 == 0;
+    const bool halo = q.Cin == 16 && q.Cout == 16 && q.stride == 1 && q.W == 32 &&
+                      q.Wo == 32 && q.H == q.Ho && q.H % 8 == 0 && !q.rowmap &&
+                      ((uintptr_t)q.x & 15) == 0 && ((uintptr_t)q.dy & 15) == 0 &&
+                      q.sx % 4 == 0;
+    if (halo) {
+      hipLaunchKernelGGL(k_conv_wgrad_halo16, dim3((unsigned)(q.G * c.splits)), dim3(kT), 0,
+                         st, c);
+      return hipGetLastError();
+    }
     if (rowsk) {
       // whole 64-position slabs per split
       c.mchunk = ((rows + c.splits - 1) / c.splits + 63) / 64 * 64;
