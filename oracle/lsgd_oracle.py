@@ -227,6 +227,21 @@ def average_delta_form(W_start, W_end):
     return np.broadcast_to(wbar, D.shape).copy()
 
 
+def average_blocks(W, Kb):
+    """Hierarchical local SGD's block synchronisation (Appendix D, the
+    hierarchical local SGD equation, middle line; Algorithm 5's inner
+    all-reduce, read as a plain mean like the global one): replicas are
+    grouped into blocks of Kb consecutive workers and every replica is
+    replaced by the mean of its block. W: [K][P], K a multiple of Kb."""
+    W = np.asarray(W, np.float64)
+    K = W.shape[0]
+    if Kb < 1 or K % Kb:
+        raise ValueError("the block size must divide K")
+    blocks = W.reshape(K // Kb, Kb, -1)
+    means = blocks.sum(axis=1) / Kb
+    return np.repeat(means, Kb, axis=0)
+
+
 # --------------------------------------------------------------------------
 # Drivers
 # --------------------------------------------------------------------------
@@ -280,6 +295,20 @@ def run_round(state, wl, X, y, H, lr):
     losses = np.stack([local_step(state, wl, X, y, lr) for _ in range(H)])
     state.W = average(state.W)
     return losses
+
+
+def run_hierarchical_round(state, wl, X, y, H, Hb, Kb, lr):
+    """One outer round of hierarchical local SGD (Appendix D, Algorithm 5):
+    Hb block rounds, each H local steps on every replica followed by the
+    block average over Kb consecutive replicas, then the global average.
+    Momentum buffers stay local. Returns the [Hb * H][K] losses."""
+    losses = []
+    for _ in range(Hb):
+        for _ in range(H):
+            losses.append(local_step(state, wl, X, y, lr))
+        state.W = average_blocks(state.W, Kb)
+    state.W = average(state.W)
+    return np.stack(losses)
 
 
 def schedule(wl):

@@ -361,6 +361,83 @@ def test_replicas_are_independent_between_averages():
     np.testing.assert_array_equal(b.W[0], np.asarray(w0, float))
 
 
+# ---------------------------------------------------- hierarchical local SGD
+@pytest.mark.parametrize("K,Kb", [(8, 1), (8, 2), (8, 4), (8, 8), (6, 3)])
+def test_block_average_structure(K, Kb):
+    """Block synchronisation (Appendix D): members of a block of Kb
+    consecutive workers become equal, the mean over all workers is kept,
+    Kb = 1 is the identity, Kb = K is the global average, and a second block
+    average changes nothing."""
+    W = np.random.default_rng(K * 10 + Kb).standard_normal((K, 37))
+    A = O.average_blocks(W, Kb)
+    for b in range(K // Kb):
+        blk = A[b * Kb:(b + 1) * Kb]
+        np.testing.assert_array_equal(blk, np.broadcast_to(blk[0], blk.shape))
+    np.testing.assert_allclose(A.mean(0), W.mean(0), rtol=1e-13, atol=1e-15)
+    if Kb == 1:
+        np.testing.assert_array_equal(A, W)
+    if Kb == K:
+        np.testing.assert_allclose(A, O.average(W), rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(O.average_blocks(A, Kb), A, rtol=1e-14, atol=1e-15)
+    if 1 < Kb < K:  # different blocks differ before the global average
+        assert not np.allclose(A[0], A[Kb])
+    with pytest.raises(ValueError):
+        O.average_blocks(W, 5)
+
+
+@pytest.mark.parametrize("nesterov", [False, True])
+def test_hierarchical_limits_are_local_sgd(nesterov):
+    """Appendix D's limits, against the separately pinned local SGD rounds:
+    K' = K makes every block step a global average (H^b rounds of local SGD
+    with period H); K' = 1 leaves only the global average (one round of
+    H * H^b local steps); H^b = 1 is one round of period H for any K' --
+    the mean of equal-sized block means is the global mean."""
+    wl = _small(nesterov, 0.9, K=8, H=2, B=6, rounds=1)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(21).standard_normal(wk.param_count(wl.widths)) * 0.1
+    H, Hb = 2, 3
+
+    def pair():
+        return O.State(w0, wl.K), O.State(w0, wl.K)
+
+    a, b = pair()
+    O.run_hierarchical_round(a, wl, X, y, H, Hb, wl.K, wl.lr)
+    for _ in range(Hb):
+        O.run_round(b, wl, X, y, H, wl.lr)
+    np.testing.assert_allclose(a.W, b.W, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(a.U, b.U, rtol=1e-12, atol=1e-14)
+
+    a, b = pair()
+    O.run_hierarchical_round(a, wl, X, y, H, Hb, 1, wl.lr)
+    O.run_round(b, wl, X, y, H * Hb, wl.lr)
+    np.testing.assert_allclose(a.W, b.W, rtol=1e-12, atol=1e-14)
+
+    for Kb in (2, 4):
+        a, b = pair()
+        O.run_hierarchical_round(a, wl, X, y, H, 1, Kb, wl.lr)
+        O.run_round(b, wl, X, y, H, wl.lr)
+        np.testing.assert_allclose(a.W, b.W, rtol=1e-12, atol=1e-14)
+
+
+def test_hierarchical_round_blocks_between_global_averages():
+    """Within an outer round, the blocks evolve separately: after the first
+    block step, workers of one block agree and the blocks differ; after the
+    round every worker holds the global mean, and buffers stay local."""
+    wl = _small(False, 0.9, K=8, H=2, B=6, rounds=1)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(22).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st = O.State(w0, wl.K)
+    for _ in range(2):
+        O.local_step(st, wl, X, y, wl.lr)
+    blk = O.average_blocks(st.W, 4)
+    np.testing.assert_array_equal(blk[0], blk[3])
+    assert not np.allclose(blk[0], blk[4])
+    st2 = O.State(w0, wl.K)
+    O.run_hierarchical_round(st2, wl, X, y, 2, 2, 4, wl.lr)
+    np.testing.assert_array_equal(st2.W, np.broadcast_to(st2.W[0], st2.W.shape))
+    assert not np.allclose(st2.U[0], st2.U[1])
+
+
 def test_loss_decreases_on_every_workload_first_rounds():
     wl = wk.get("softmax_d64")
     X, y = wk.dataset(wl)
