@@ -131,6 +131,30 @@ lsgd_status lsgd_average(lsgd_ctx* ctx);
 lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
                            float* d_loss);
 
+/*
+ * Block synchronisation of hierarchical local SGD (Appendix D, the
+ * hierarchical local SGD equation; the inner all-reduce of Algorithm 5):
+ * replicas 0..K-1 form K/Kb blocks of Kb consecutive replicas and each
+ * replica becomes the mean of its block, summed in the same fixed tree as
+ * lsgd_average (within the block). Momentum buffers are left as they are.
+ * Kb must divide K, else LSGD_E_INVALID; Kb == K is lsgd_average (bit for
+ * bit), Kb == 1 changes nothing.
+ */
+lsgd_status lsgd_average_blocks(lsgd_ctx* ctx, int32_t Kb);
+
+/*
+ * One outer round of hierarchical local SGD (Algorithm 5): Hb times, run H
+ * local steps then the block synchronisation over blocks of Kb replicas;
+ * the last block synchronisation is replaced by the global average
+ * (lsgd_average), to which it is identical in exact arithmetic. h_lr: host
+ * array of H * Hb step sizes in step order. d_loss: fp32 [Hb * H][K] or
+ * NULL. Kb must divide K; H >= 0, Hb >= 1, else LSGD_E_INVALID. Hb == 1 is
+ * lsgd_run_round; Kb == K runs Hb plain rounds of period H.
+ */
+lsgd_status lsgd_run_hierarchical_round(lsgd_ctx* ctx, int32_t H, int32_t Hb,
+                                        int32_t Kb, const float* h_lr,
+                                        float* d_loss);
+
 /* Copy replica `replica`'s parameters (or, for replica == -1, their mean by
  * the same tree as lsgd_average, without changing state) to d_dst fp32 [P]. */
 lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst);
@@ -215,6 +239,12 @@ lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
  * lsgd_average). */
 lsgd_status lsgd_replica_average(float* d_W, int32_t K, int64_t P,
                                  void* stream);
+
+/* In-place block average of d_W fp32 [K][P]: each of the K/Kb groups of Kb
+ * consecutive rows is replaced by its mean (the kernel behind
+ * lsgd_average_blocks). Kb must divide K, else LSGD_E_INVALID. */
+lsgd_status lsgd_replica_average_blocks(float* d_W, int32_t K, int32_t Kb,
+                                        int64_t P, void* stream);
 
 /* Fused update over n elements (the kernel behind the parameter update of
  * lsgd_local_step): g = d_G + wd * w; u = m u + g; d = nesterov ? g + m u

@@ -702,6 +702,16 @@ lsgd_status do_average(lsgd_ctx* c) {
   return LSGD_OK;
 }
 
+lsgd_status do_average_blocks(lsgd_ctx* c, int Kb) {
+  if (Kb == c->cfg.K) return do_average(c);
+  if (Kb == 1) return LSGD_OK;  // every block holds one replica
+  LSGD_LAUNCH(c, "average_blocks",
+              lsgd::launch_average_blocks(c->W(), c->Wb(), Kb, c->cfg.K / Kb,
+                                          c->lay.Ps, c->lay.Ps, nullptr,
+                                          c->stream));
+  return LSGD_OK;
+}
+
 #define LSGD_USABLE(ctx)                                   \
   do {                                                     \
     if (!(ctx)) return LSGD_E_INVALID;                     \
@@ -795,6 +805,36 @@ lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
     if (st != LSGD_OK) return st;
   }
   return do_average(ctx);
+}
+
+lsgd_status lsgd_average_blocks(lsgd_ctx* ctx, int32_t Kb) {
+  LSGD_USABLE(ctx);
+  if (Kb < 1 || ctx->cfg.K % Kb) return LSGD_E_INVALID;
+  return do_average_blocks(ctx, Kb);
+}
+
+lsgd_status lsgd_run_hierarchical_round(lsgd_ctx* ctx, int32_t H, int32_t Hb,
+                                        int32_t Kb, const float* h_lr,
+                                        float* d_loss) {
+  LSGD_USABLE(ctx);
+  if (H < 0 || Hb < 1 || Kb < 1 || ctx->cfg.K % Kb) return LSGD_E_INVALID;
+  const long long steps = (long long)H * Hb;
+  if (steps > 0 && !h_lr) return LSGD_E_INVALID;
+  for (long long h = 0; h < steps; ++h)
+    if (!std::isfinite(h_lr[h])) return LSGD_E_INVALID;
+  for (int b = 0; b < Hb; ++b) {
+    for (int h = 0; h < H; ++h) {
+      const long long t = (long long)b * H + h;
+      lsgd_status st = do_local_step(
+          ctx, h_lr[t], d_loss ? d_loss + (size_t)t * ctx->cfg.K : nullptr);
+      if (st != LSGD_OK) return st;
+    }
+    // the last block synchronisation is absorbed by the global one: the
+    // mean of equal-sized block means is the global mean
+    lsgd_status st = b + 1 < Hb ? do_average_blocks(ctx, Kb) : do_average(ctx);
+    if (st != LSGD_OK) return st;
+  }
+  return LSGD_OK;
 }
 
 lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst) {
@@ -967,6 +1007,14 @@ lsgd_status lsgd_replica_average(float* d_W, int32_t K, int64_t P, void* stream)
   if (!d_W || K < 1 || P < 0) return LSGD_E_INVALID;
   hipError_t e = lsgd::launch_average(d_W, nullptr, K, P, P, nullptr,
                                       (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
+}
+
+lsgd_status lsgd_replica_average_blocks(float* d_W, int32_t K, int32_t Kb,
+                                       int64_t P, void* stream) {
+  if (!d_W || K < 1 || Kb < 1 || K % Kb || P < 0) return LSGD_E_INVALID;
+  hipError_t e = lsgd::launch_average_blocks(d_W, nullptr, Kb, K / Kb, P, P,
+                                             nullptr, (hipStream_t)stream);
   return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
 }
 

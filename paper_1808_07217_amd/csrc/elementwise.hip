@@ -184,10 +184,14 @@ __device__ __forceinline__ void store_bf16x4(bf16_t* p, float4 v) {
 }
 
 // Vectorised average: thread i owns elements 4i .. 4i+3 of every replica.
+// The grid's y index picks a block of K consecutive replicas (hierarchical
+// averaging; a single block is the global average).
 // mean_out != nullptr: write the mean there and leave W untouched.
 template <int KT>
 __global__ void k_average4(float* W, bf16_t* Wb, int K, long long n,
                            long long ld, float* mean_out) {
+  W += blockIdx.y * (long long)K * ld;
+  if (Wb) Wb += blockIdx.y * (long long)K * ld;
   const long long n4 = n / 4;
   const float4* W4 = (const float4*)W;
   const long long stride = ld / 4;
@@ -212,6 +216,8 @@ __global__ void k_average4(float* W, bf16_t* Wb, int K, long long n,
 
 __global__ void k_average1(float* W, bf16_t* Wb, int K, long long n,
                            long long ld, float* mean_out) {
+  W += blockIdx.y * (long long)K * ld;
+  if (Wb) Wb += blockIdx.y * (long long)K * ld;
   for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
        i += (long long)gridDim.x * blockDim.x) {
     const float mean = tree_sum_rt<float>(W + i, ld, K) / (float)K;
@@ -297,18 +303,21 @@ hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
   return hipGetLastError();
 }
 
-hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
-                          long long ld, float* mean_out, hipStream_t s) {
-  if (n <= 0 || K <= 0) return hipSuccess;
+hipError_t launch_average_blocks(float* W, bf16_t* Wb, int Kb, int blocks,
+                                 long long n, long long ld, float* mean_out,
+                                 hipStream_t s) {
+  if (n <= 0 || Kb <= 0 || blocks <= 0) return hipSuccess;
+  if (blocks > 65535 || (mean_out && blocks != 1)) return hipErrorInvalidValue;
+  const int K = Kb;
   const bool vec = n % 4 == 0 && ld % 4 == 0 && aligned16(W) &&
                    (mean_out == nullptr || aligned16(mean_out)) &&
                    (Wb == nullptr || ((uintptr_t)Wb & 7u) == 0);
   if (!vec) {
-    hipLaunchKernelGGL(k_average1, dim3(grid_for(n, 256)), dim3(256), 0, s, W,
-                       Wb, K, n, ld, mean_out);
+    hipLaunchKernelGGL(k_average1, dim3(grid_for(n, 256), blocks), dim3(256),
+                       0, s, W, Wb, K, n, ld, mean_out);
     return hipGetLastError();
   }
-  const dim3 grid(grid_for(n / 4, 256)), block(256);
+  const dim3 grid(grid_for(n / 4, 256), blocks), block(256);
 #define LSGD_AVG_CASE(KK)                                                    \
   case KK:                                                                   \
     hipLaunchKernelGGL(k_average4<KK>, grid, block, 0, s, W, Wb, K, n, ld,   \
@@ -329,6 +338,11 @@ hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
   }
 #undef LSGD_AVG_CASE
   return hipGetLastError();
+}
+
+hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
+                          long long ld, float* mean_out, hipStream_t s) {
+  return launch_average_blocks(W, Wb, K, 1, n, ld, mean_out, s);
 }
 
 hipError_t launch_broadcast(const float* src, float* W, bf16_t* Wb, int K,

@@ -164,6 +164,11 @@ hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
 // K-way average of the first n elements of K rows spaced ld apart.
 hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
                           long long ld, float* mean_out, hipStream_t s);
+// The same average within each of `blocks` groups of Kb consecutive rows
+// (mean_out only with blocks == 1).
+hipError_t launch_average_blocks(float* W, bf16_t* Wb, int Kb, int blocks,
+                                 long long n, long long ld, float* mean_out,
+                                 hipStream_t s);
 hipError_t launch_broadcast(const float* src, float* W, bf16_t* Wb, int K,
                             long long n, long long ld, int replica,
                             hipStream_t s);

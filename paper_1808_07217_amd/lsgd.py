@@ -53,6 +53,9 @@ _SIGS = {
     "lsgd_local_step": [_P, _c.c_float, _P],
     "lsgd_average": [_P],
     "lsgd_run_round": [_P, _c.c_int32, _c.POINTER(_c.c_float), _P],
+    "lsgd_average_blocks": [_P, _c.c_int32],
+    "lsgd_run_hierarchical_round": [_P, _c.c_int32, _c.c_int32, _c.c_int32,
+                                    _c.POINTER(_c.c_float), _P],
     "lsgd_read_params": [_P, _c.c_int32, _P],
     "lsgd_read_momentum": [_P, _c.c_int32, _P],
     "lsgd_write_params": [_P, _c.c_int32, _P],
@@ -71,6 +74,7 @@ _SIGS = {
                           _c.c_int64, _P, _c.c_int64, _c.c_int64, _P,
                           _c.c_int32, _P, _P],
     "lsgd_replica_average": [_P, _c.c_int32, _c.c_int64, _P],
+    "lsgd_replica_average_blocks": [_P, _c.c_int32, _c.c_int32, _c.c_int64, _P],
     "lsgd_sgd_update": [_P, _P, _P, _c.c_int64, _c.c_float, _c.c_float,
                         _c.c_float, _c.c_int32, _P],
 }
@@ -182,6 +186,23 @@ class Replicas:
         H = len(lrs)
         arr = (_c.c_float * max(H, 1))(*[float(v) for v in lrs])
         _check(_lib.lsgd_run_round(self._ctx, H, arr, _ptr(loss)), self._ctx)
+
+    def average_blocks(self, Kb: int):
+        """Hierarchical block synchronisation: each block of Kb consecutive
+        replicas takes its mean."""
+        _check(_lib.lsgd_average_blocks(self._ctx, int(Kb)), self._ctx)
+
+    def run_hierarchical_round(self, H: int, Hb: int, Kb: int,
+                               lrs: Sequence[float],
+                               loss: Optional[torch.Tensor] = None):
+        """Hb x (H local steps, block average over blocks of Kb), then the
+        global average; ``lrs`` holds the H * Hb step sizes."""
+        if len(lrs) != H * Hb:
+            raise ValueError("lrs must hold H * Hb step sizes")
+        arr = (_c.c_float * max(1, len(lrs)))(*[float(v) for v in lrs])
+        _check(_lib.lsgd_run_hierarchical_round(self._ctx, int(H), int(Hb),
+                                                int(Kb), arr, _ptr(loss)),
+               self._ctx)
 
     # -- state -----------------------------------------------------------
     def read_params(self, replica: int = -1, out=None) -> torch.Tensor:
@@ -301,6 +322,16 @@ def replica_average(W: torch.Tensor) -> None:
         raise ValueError("W must be contiguous float32 [K][P]")
     _check(_lib.lsgd_replica_average(
         _ptr(W), W.shape[0], W.shape[1],
+        _stream_handle(torch.cuda.current_stream(W.device))))
+
+
+def replica_average_blocks(W: torch.Tensor, Kb: int) -> None:
+    """In-place average within each block of Kb consecutive rows of a
+    contiguous float32 [K][P] tensor."""
+    if W.dtype != torch.float32 or W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be contiguous float32 [K][P]")
+    _check(_lib.lsgd_replica_average_blocks(
+        _ptr(W), W.shape[0], int(Kb), W.shape[1],
         _stream_handle(torch.cuda.current_stream(W.device))))
 
 

@@ -72,6 +72,13 @@ def test_null_context_calls_fail_cleanly():
     from paper_1808_07217_amd import lsgd as L
     lib = L._lib
     assert lib.lsgd_average(None) == 1
+    assert lib.lsgd_average_blocks(None, 1) == 1
+    assert lib.lsgd_run_hierarchical_round(None, 1, 1, 1, None, None) == 1
+    assert lib.lsgd_replica_average_blocks(None, 4, 2, 8, None) == 1
+    # a block size that does not divide K is refused before any launch
+    fake = ctypes.c_void_p(256)
+    assert lib.lsgd_replica_average_blocks(fake, 6, 4, 8, None) == 1
+    assert lib.lsgd_replica_average_blocks(fake, 6, 0, 8, None) == 1
     assert lib.lsgd_local_step(None, ctypes.c_float(0.1), None) == 1
     assert lib.lsgd_destroy(None) == 1
     for s in range(7):

@@ -112,6 +112,43 @@ def test_average_of_identical_replicas_is_identity(K):
     np.testing.assert_array_equal(Wd.cpu().numpy()[0], w)
 
 
+@pytest.mark.parametrize("K,Kb,P", [(16, 4, 1841162 + 6), (16, 2, 4099),
+                                    (8, 8, 1027), (8, 1, 650), (6, 3, 7),
+                                    (64, 16, 10001), (12, 4, 5), (10, 5, 4096)])
+def test_replica_average_blocks(K, Kb, P):
+    """Hierarchical block synchronisation: each block of Kb consecutive rows
+    is replaced by its mean, bit-exact against the same fp32 tree within the
+    block and within the pairwise bound of the oracle's block mean."""
+    L = _lsgd()
+    print(f"block average K={K} Kb={Kb} P={P}", flush=True)
+    rng = np.random.default_rng(K * 100 + Kb * 10 + P)
+    W = rng.standard_normal((K, P)).astype(np.float32)
+    Wd = to_dev(W)
+    L.replica_average_blocks(Wd, Kb)
+    got = Wd.cpu().numpy()
+    ref = O.average_blocks(W.astype(np.float64), Kb)
+    depth = int(np.ceil(np.log2(Kb))) if Kb > 1 else 0
+    for b in range(K // Kb):
+        rows = W[b * Kb:(b + 1) * Kb]
+        want = (_tree_f32(list(rows)) / np.float32(Kb)).astype(np.float32)
+        for k in range(b * Kb, (b + 1) * Kb):
+            np.testing.assert_array_equal(got[k], want)
+        bound = (gamma(depth) * np.abs(rows).astype(np.float64).sum(0) / Kb
+                 + U32 * np.abs(ref[b * Kb]))
+        assert np.all(np.abs(got[b * Kb] - ref[b * Kb]) <= bound + 1e-45)
+    if Kb == K:
+        Wd2 = to_dev(W)
+        L.replica_average(Wd2)
+        np.testing.assert_array_equal(Wd2.cpu().numpy(), got)
+
+
+def test_replica_average_blocks_rejects_a_block_size_not_dividing_k():
+    L = _lsgd()
+    Wd = to_dev(np.zeros((6, 8), np.float32))
+    with pytest.raises(L.LsgdError):
+        L.replica_average_blocks(Wd, 4)
+
+
 # ------------------------------------------------------------------ update
 @pytest.mark.parametrize("nesterov", [False, True])
 @pytest.mark.parametrize("n", [1, 3, 4099, 1 << 20])

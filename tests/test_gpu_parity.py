@@ -229,6 +229,116 @@ def test_write_params_and_step_counter_resume_exactly():
                                   b.read_params(-1).cpu().numpy())
 
 
+# ----------------------------------------------------- hierarchical local SGD
+@pytest.mark.parametrize("K,Kb,nesterov", [(8, 4, False), (6, 3, True),
+                                           (8, 2, False)])
+def test_hierarchical_round_matches_oracle_step_by_step(K, Kb, nesterov):
+    """Appendix D / Algorithm 5 on both sides: every replica after every local
+    step and after every block average, then the global average; and the
+    fused round entry point against the oracle's whole round."""
+    w = _small((70, 48, 36, 10), K=K, B=12, nesterov=nesterov, rounds=1)
+    X, y, w0 = _small_data(w, seed=9 + K)
+    H, Hb = 2, 3
+    print(f"hierarchical K={K} Kb={Kb} H={H} Hb={Hb}", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss_d = torch.empty(w.K, device=device())
+    for b in range(Hb):
+        for h in range(H):
+            reps.local_step(w.lr, loss_d)
+            want = O.local_step(st, w, X, y, w.lr)
+            assert np.all(rel(loss_d.cpu().numpy(), want) <= LOSS_TOL_FP32), (b, h)
+            for k in range(w.K):
+                e = normwise(reps.read_params(k).cpu().numpy(), st.W[k])
+                assert e <= PARAM_TOL_FP32, (b, h, k, e)
+        reps.average_blocks(Kb)
+        st.W = O.average_blocks(st.W, Kb)
+        got = [reps.read_params(k).cpu().numpy() for k in range(w.K)]
+        for k in range(w.K):
+            e = normwise(got[k], st.W[k])
+            assert e <= PARAM_TOL_FP32, (b, "block", k, e)
+            np.testing.assert_array_equal(got[k], got[k - k % Kb])
+        assert not np.array_equal(got[0], got[Kb])
+    reps.average()
+    st.W = O.average(st.W)
+    e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
+    assert e <= PARAM_TOL_FP32, ("global", e)
+
+    # the fused entry point over a whole round
+    a = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(H * Hb, w.K, device=device())
+    a.run_hierarchical_round(H, Hb, Kb, [w.lr] * (H * Hb), loss)
+    want = O.run_hierarchical_round(st, w, X, y, H, Hb, Kb, w.lr)
+    assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32)
+    for k in (0, w.K - 1):
+        e = normwise(a.read_params(k).cpu().numpy(), st.W[k])
+        assert e <= PARAM_TOL_FP32, ("fused", k, e)
+    for k in range(w.K):
+        e = normwise(a.read_momentum(k).cpu().numpy(), st.U[k])
+        assert e <= PARAM_TOL_FP32, ("momentum", k, e)
+    assert a.step == H * Hb
+
+
+def test_hierarchical_round_reduces_to_local_sgd_bit_for_bit():
+    """The limits of Appendix D on the GPU, launch for launch: H^b = 1 is one
+    local SGD round; K' = K is H^b rounds of period H; K' = 1 is one round
+    of H * H^b steps; and the fused round equals its steps with the block
+    averages in between and the global average at the end."""
+    w = _small((70, 48, 36, 10), K=8, B=12, rounds=1)
+    X, y, w0 = _small_data(w, seed=31)
+    lrs = [0.02, 0.01, 0.03, 0.02, 0.015, 0.025]
+
+    def final(r):
+        return (r.read_params(-1).cpu().numpy(),
+                np.stack([r.read_momentum(k).cpu().numpy() for k in range(w.K)]))
+
+    def same(a, b):
+        for x, z in zip(final(a), final(b)):
+            np.testing.assert_array_equal(x, z)
+
+    a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+    a.run_hierarchical_round(6, 1, 4, lrs)
+    b.run_round(lrs)
+    same(a, b)
+
+    a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+    a.run_hierarchical_round(2, 3, w.K, lrs)
+    for i in range(3):
+        b.run_round(lrs[2 * i:2 * i + 2])
+    same(a, b)
+
+    a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+    a.run_hierarchical_round(3, 2, 1, lrs)
+    b.run_round(lrs)
+    same(a, b)
+
+    a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+    a.run_hierarchical_round(2, 3, 2, lrs)
+    for i in range(3):
+        b.local_step(lrs[2 * i])
+        b.local_step(lrs[2 * i + 1])
+        if i < 2:
+            b.average_blocks(2)
+    b.average()
+    same(a, b)
+
+
+def test_hierarchical_round_rejects_bad_blocks():
+    from paper_1808_07217_amd import lsgd as L
+    w = _small((70, 48, 36, 10), K=6, B=12, rounds=1)
+    X, y, w0 = _small_data(w, seed=3)
+    reps = make_replicas(w, X, y, w0)
+    for Kb in (0, 4, 7):
+        with pytest.raises(L.LsgdError):
+            reps.average_blocks(Kb)
+        with pytest.raises(L.LsgdError):
+            reps.run_hierarchical_round(1, 2, Kb, [0.01, 0.01])
+    with pytest.raises(L.LsgdError):
+        reps.run_hierarchical_round(1, 0, 3, [])
+    assert reps.step == 0
+
+
 # --------------------------------------------------------- full-size rounds
 @pytest.fixture(scope="module")
 def img_data():
@@ -268,6 +378,26 @@ def test_mlp_512_first_round_full_size(img_data):
     st.W = O.average(st.W)
     e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
     print(f"mlp_512 round-1 averaged params normwise error {e:.3e}", flush=True)
+    assert e <= PARAM_TOL_FP32
+
+
+def test_mlp_512_hierarchical_round_full_size(img_data):
+    """Workload 2's shape (K=16, B_loc=128) as hierarchical local SGD with
+    blocks of K'=4 replicas, H=4, H^b=2: the losses of all eight steps and
+    the averaged model after the outer round against the oracle."""
+    w = wk.get("mlp_512")
+    X, y = img_data
+    w0 = wk.initial_weights(w)
+    H, Hb, Kb = 4, 2, 4
+    print("mlp_512 hierarchical round", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(H * Hb, w.K, device=device())
+    reps.run_hierarchical_round(H, Hb, Kb, [w.lr] * (H * Hb), loss)
+    want = O.run_hierarchical_round(st, w, X, y, H, Hb, Kb, w.lr)
+    assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32)
+    e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
+    print(f"mlp_512 hierarchical round params normwise error {e:.3e}", flush=True)
     assert e <= PARAM_TOL_FP32
 
 
