@@ -63,7 +63,7 @@ def kernel_cost(tag: str, w) -> tuple:
         return None, None
     if tag == "xent":
         return 0, K * B * d[L] * (4 + e) + K * B * 8
-    if tag == "average":
+    if tag in ("average", "average_blocks"):   # same traffic per launch
         return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0)
     if tag == "wgrad_update":   # one launch over every generic layer
         Lg = L - 1 if d[L] <= 32 else L   # the top layer has its own kernels
@@ -249,14 +249,19 @@ def cpu_baseline(w, X, y, w0):
         threads = os.cpu_count()
     st = O.State(w0, w.K)
     t0 = time.perf_counter()
-    O.run_round(st, w, X, y, w.H, w.lr)
+    if w.Kb > 0:
+        O.run_hierarchical_round(st, w, X, y, w.H, w.Hb, w.Kb, w.lr)
+        what = (f"H^b={w.Hb} x (H={w.H} local steps on all K={w.K} replicas "
+                f"+ block average over K'={w.Kb}) + global average")
+    else:
+        O.run_round(st, w, X, y, w.H, w.lr)
+        what = f"H={w.H} local steps on all K={w.K} replicas + average"
     dt = time.perf_counter() - t0
-    samples = w.K * w.H * w.B_loc
+    samples = w.K * w.H * w.Hb * w.B_loc
     return {"value": samples / dt, "unit": "samples/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"one full round of {w.name} (H={w.H} local steps on "
-                      f"all K={w.K} replicas + average, {samples} samples) in "
-                      f"{dt:.2f} s; fp64 numpy, BLAS threads={threads}"}
+            "sample": f"one full round of {w.name} ({what}, {samples} samples) "
+                      f"in {dt:.2f} s; fp64 numpy, BLAS threads={threads}"}
 
 
 def main():
@@ -289,12 +294,17 @@ def main():
     yd = torch.from_numpy(np.array(y)).to(dev)
     reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))
     stream = reps.stream
-    H = w.H
+    hier = w.Kb > 0
+    H = w.H * w.Hb            # local steps per (outer) round
     lrs = [w.lr] * H
     loss = torch.empty((args.warmup + args.steps + 8) * H, w.K, device=dev)
 
     def rnd(i):
-        reps.run_round(lrs, loss[i * H:(i + 1) * H])
+        if hier:   # H^b x (H local steps, block average), global average
+            reps.run_hierarchical_round(w.H, w.Hb, w.Kb, lrs,
+                                        loss[i * H:(i + 1) * H])
+        else:
+            reps.run_round(lrs, loss[i * H:(i + 1) * H])
 
     # Warmup. The rounds after the first bracket every launch with HIP events
     # (per-kernel breakdown, and the dominant kernel); the timed rounds then
@@ -369,8 +379,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": (f"{w.name}: MLP {'-'.join(map(str, w.widths))} "
                                 if w.model == "mlp" else f"{w.name}: ResNet-20 ")
-                               + f"{w.dtype}, K={w.K}, B_loc={w.B_loc}, H={H}",
+                               + f"{w.dtype}, K={w.K}, B_loc={w.B_loc}, "
+                               + (f"K'={w.Kb}, H={w.H}, H^b={w.Hb}" if hier
+                                  else f"H={H}"),
                    "K": w.K, "B_loc": w.B_loc, "H": H,
+                   **({"K_block": w.Kb, "H_block": w.Hb} if hier else {}),
                    "samples_per_step": samples,
                    "momentum": w.momentum, "nesterov": w.nesterov,
                    "weight_decay": w.weight_decay},

@@ -44,7 +44,9 @@ class Workload:
     ``warm_rounds`` is the post-local switch point t': rounds 1..t' run with
     one local step each (mini-batch SGD), later rounds run ``H`` local steps.
     ``lr_after_switch`` is the step size used after the switch (equal to
-    ``lr`` when there is no switch).
+    ``lr`` when there is no switch). ``Kb`` > 0 makes it hierarchical local
+    SGD (Appendix D): blocks of ``Kb`` consecutive workers average every
+    ``H`` steps, all workers every ``H * Hb`` steps (one outer round).
     """
     name: str
     model: str                 # "mlp" (softmax regression is the 1-layer MLP)
@@ -65,6 +67,8 @@ class Workload:
     data_seed: int = 0
     init_seed: int = 0
     sample_seed: int = 0
+    Kb: int = 0                # hierarchical block size K' (0: none)
+    Hb: int = 1                # block rounds per global average, H^b
 
     @property
     def n_layers(self) -> int:
@@ -103,6 +107,14 @@ WORKLOADS = {
         dtype="bf16", K=64, B_loc=64, H=8, rounds=10, lr=0.001,
         momentum=0.9, nesterov=False, weight_decay=1e-4, **_IMG,
         data_seed=201, init_seed=402, sample_seed=0x5EED0004),
+    # hierarchical local SGD on the same MLP: 8 blocks of K'=2 workers (the
+    # 8 x 2 topology of Appendix D's tables), block average every H=4 steps,
+    # global average every H * H^b = 16 steps
+    "hier_mlp_512": Workload(
+        name="hier_mlp_512", model="mlp", widths=(3072, 512, 512, 10),
+        dtype="fp32", K=16, B_loc=128, H=4, rounds=20, lr=0.001,
+        momentum=0.9, nesterov=False, weight_decay=1e-4, Kb=2, Hb=4, **_IMG,
+        data_seed=201, init_seed=202, sample_seed=0x5EED0006),
     # ResNet-20-shaped CNN, fp32, per-worker BN, heavy-ball momentum
     "resnet20": Workload(
         name="resnet20", model="resnet20", widths=(3072, 10), dtype="fp32",
