@@ -227,6 +227,39 @@ def average_delta_form(W_start, W_end):
     return np.broadcast_to(wbar, D.shape).copy()
 
 
+def average_global_momentum(W, w_sync, u_global, m_global, lr):
+    """Synchronisation of local SGD with global momentum (momentum appendix,
+    the paragraph on local SGD with global momentum; with local momentum on
+    as well it is the hybrid scheme of the next paragraph). The round's
+    model differences Delta^k = w_(t) - w^k_(t)+H, averaged over the workers
+    and divided by the step size, feed a momentum buffer u held with the
+    synchronised model:
+        u_(t)   = m_g u_(t-1) + (1/lr) (1/K) sum_k Delta^k,
+        w_(t+1) = w_(t) - lr u_(t).
+    W: [K][P] replicas at the end of the round; w_sync = w_(t). Returns
+    (every replica set to w_(t+1), w_(t+1), u_(t)). With m_g = 0 this is the
+    plain average up to rounding."""
+    W = np.asarray(W, np.float64)
+    w_sync = np.asarray(w_sync, np.float64)
+    deltas = w_sync[None, :] - W
+    u = m_global * np.asarray(u_global, np.float64) + deltas.sum(axis=0) / W.shape[0] / lr
+    w = w_sync - lr * u
+    return np.broadcast_to(w, W.shape).copy(), w.copy(), u
+
+
+def synchronise(state, wl, lr):
+    """The global synchronisation at the end of a round: the plain average of
+    eq. (2), or the global-momentum form when the workload sets a global
+    momentum factor (read with the step size of the round's local steps)."""
+    m_g = getattr(wl, "global_momentum", 0.0)
+    if m_g:
+        state.W, state.w_sync, state.u_global = average_global_momentum(
+            state.W, state.w_sync, state.u_global, m_g, lr)
+    else:
+        state.W = average(state.W)
+        state.w_sync = state.W[0].copy()
+
+
 def average_blocks(W, Kb):
     """Hierarchical local SGD's block synchronisation (Appendix D, the
     hierarchical local SGD equation, middle line; Algorithm 5's inner
@@ -246,12 +279,15 @@ def average_blocks(W, Kb):
 # Drivers
 # --------------------------------------------------------------------------
 class State:
-    """K replicas w^k, their momentum buffers u^k, and the step counter."""
+    """K replicas w^k, their momentum buffers u^k, and the step counter; for
+    global momentum also the synchronised model w_(t) and its buffer u."""
 
     def __init__(self, w0, K):
         self.W = np.repeat(np.asarray(w0, np.float64)[None, :], K, axis=0)
         self.U = np.zeros_like(self.W)
         self.step = 0
+        self.w_sync = np.asarray(w0, np.float64).copy()
+        self.u_global = np.zeros_like(self.w_sync)
 
 
 def local_step(state, wl, X, y, lr, replicas=None):
@@ -290,10 +326,10 @@ def model_decay_mask(wl):
 
 
 def run_round(state, wl, X, y, H, lr):
-    """H local steps on every replica, then the average; returns [H][K]
-    losses."""
+    """H local steps on every replica, then the synchronisation (the average,
+    or its global-momentum form); returns [H][K] losses."""
     losses = np.stack([local_step(state, wl, X, y, lr) for _ in range(H)])
-    state.W = average(state.W)
+    synchronise(state, wl, lr)
     return losses
 
 
@@ -307,7 +343,7 @@ def run_hierarchical_round(state, wl, X, y, H, Hb, Kb, lr):
         for _ in range(H):
             losses.append(local_step(state, wl, X, y, lr))
         state.W = average_blocks(state.W, Kb)
-    state.W = average(state.W)
+    synchronise(state, wl, lr)
     return np.stack(losses)
 
 

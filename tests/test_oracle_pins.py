@@ -438,6 +438,68 @@ def test_hierarchical_round_blocks_between_global_averages():
     assert not np.allclose(st2.U[0], st2.U[1])
 
 
+# ------------------------------------------------- global / hybrid momentum
+def test_global_momentum_average_closed_forms():
+    """The global-momentum synchronisation against its rearranged closed
+    forms: with all replicas starting the round at w_(t), the new model is
+    the plain mean minus lr * m_g * u_(t-1), and the buffer gains the mean
+    model change over lr. m_g = 0 is the plain average of eq. (2)."""
+    rng = np.random.default_rng(41)
+    K, P, lr, mg = 5, 33, 0.05, 0.7
+    W = rng.standard_normal((K, P))
+    w_sync = rng.standard_normal(P)
+    u = rng.standard_normal(P)
+    Wn, wn, un = O.average_global_momentum(W, w_sync, u, mg, lr)
+    mean = W.mean(axis=0)
+    np.testing.assert_allclose(wn, mean - lr * mg * u, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(un, mg * u + (w_sync - mean) / lr, rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(Wn, np.broadcast_to(wn, (K, P)))
+    W0, _, _ = O.average_global_momentum(W, w_sync, u, 0.0, lr)
+    np.testing.assert_allclose(W0, O.average(W), rtol=1e-12, atol=1e-13)
+
+
+def test_global_momentum_h1_is_minibatch_heavy_ball():
+    """H = 1 without local momentum: the mean model change over lr is the
+    mean gradient (coupled decay included), so local SGD with global
+    momentum m_g is mini-batch SGD with heavy-ball momentum m_g on the
+    union batch -- the block-momentum view of the global-momentum
+    paragraph."""
+    base = _small(False, 0.0, H=1, rounds=6)
+    X, y = wk.dataset(base)
+    w0 = np.random.default_rng(42).standard_normal(wk.param_count(base.widths)) * 0.1
+    for mg in (0.5, 0.9):
+        st, _ = O.run(base.scaled(global_momentum=mg), X, y, w0)
+        ref = O.minibatch_sgd(base.scaled(momentum=mg), X, y, w0, steps=6, lr=base.lr)
+        np.testing.assert_allclose(st.W[0], ref, rtol=1e-10, atol=1e-12)
+        assert not np.allclose(st.W[0], O.minibatch_sgd(base, X, y, w0, 6, base.lr))
+
+
+def test_hybrid_momentum_first_round_and_buffers():
+    """Hybrid momentum (local buffers plus the global one): the global buffer
+    starts at zero, so the first round ends at the plain average; from the
+    second round on the models differ by -lr * m_g * u_(1), with u_(1) the
+    first round's mean model change over lr. Local buffers stay local."""
+    wl = _small(True, 0.9, H=3, rounds=2)
+    hyb = wl.scaled(global_momentum=0.4)
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(43).standard_normal(wk.param_count(wl.widths)) * 0.1
+    a, b = O.State(w0, wl.K), O.State(w0, wl.K)
+    O.run_round(a, hyb, X, y, 3, wl.lr)
+    O.run_round(b, wl, X, y, 3, wl.lr)
+    np.testing.assert_allclose(a.W, b.W, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(a.u_global, (w0 - b.W[0]) / wl.lr, rtol=1e-10, atol=1e-10)
+    np.testing.assert_array_equal(a.U, b.U)
+    assert not np.allclose(a.U[0], a.U[1])
+    # second round from the same start: the end models differ by the momentum term
+    c = O.State(w0, wl.K)
+    c.W, c.U, c.step = a.W.copy(), a.U.copy(), a.step
+    c.w_sync = a.w_sync.copy()
+    O.run_round(a, hyb, X, y, 3, wl.lr)
+    O.run_round(c, wl, X, y, 3, wl.lr)
+    np.testing.assert_allclose(a.W[0], c.W[0] - wl.lr * 0.4 * (w0 - b.W[0]) / wl.lr,
+                               rtol=1e-9, atol=1e-12)
+
+
 def test_loss_decreases_on_every_workload_first_rounds():
     wl = wk.get("softmax_d64")
     X, y = wk.dataset(wl)

@@ -69,6 +69,7 @@ class Workload:
     sample_seed: int = 0
     Kb: int = 0                # hierarchical block size K' (0: none)
     Hb: int = 1                # block rounds per global average, H^b
+    global_momentum: float = 0.0   # m_g at the global average (0: plain mean)
 
     @property
     def n_layers(self) -> int:
