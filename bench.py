@@ -64,7 +64,8 @@ def kernel_cost(tag: str, w) -> tuple:
     if tag == "xent":
         return 0, K * B * d[L] * (4 + e) + K * B * 8
     if tag in ("average", "average_blocks"):   # same traffic per launch
-        return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0)
+        gm = 16 * P if w.global_momentum else 0  # w_sync and u read + written
+        return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0) + gm
     if tag == "wgrad_update":   # one launch over every generic layer
         Lg = L - 1 if d[L] <= 32 else L   # the top layer has its own kernels
         costs = [kernel_cost(f"wgrad_update{l}", w) for l in range(1, Lg + 1)]
@@ -255,7 +256,9 @@ def cpu_baseline(w, X, y, w0):
                 f"+ block average over K'={w.Kb}) + global average")
     else:
         O.run_round(st, w, X, y, w.H, w.lr)
-        what = f"H={w.H} local steps on all K={w.K} replicas + average"
+        what = (f"H={w.H} local steps on all K={w.K} replicas + "
+                + ("synchronisation with global momentum" if w.global_momentum
+                   else "average"))
     dt = time.perf_counter() - t0
     samples = w.K * w.H * w.Hb * w.B_loc
     return {"value": samples / dt, "unit": "samples/s", "cores": threads,
@@ -289,7 +292,8 @@ def main():
     dev = torch.device("cuda", 0)
     cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype,
                         momentum=w.momentum, weight_decay=w.weight_decay,
-                        nesterov=w.nesterov, seed=w.sample_seed, model=w.model)
+                        nesterov=w.nesterov, seed=w.sample_seed, model=w.model,
+                        global_momentum=w.global_momentum)
     Xd = torch.from_numpy(np.array(X)).to(dev)
     yd = torch.from_numpy(np.array(y)).to(dev)
     reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))
@@ -386,7 +390,9 @@ def main():
                    **({"K_block": w.Kb, "H_block": w.Hb} if hier else {}),
                    "samples_per_step": samples,
                    "momentum": w.momentum, "nesterov": w.nesterov,
-                   "weight_decay": w.weight_decay},
+                   "weight_decay": w.weight_decay,
+                   **({"global_momentum": w.global_momentum}
+                      if w.global_momentum else {})},
     }
     if phases is not None:
         phases[f"H{H}"] = {"samples_per_round": samples,

@@ -84,6 +84,8 @@ typedef struct lsgd_config {
   int32_t nesterov;                       /* 0 heavy ball, 1 Nesterov */
   float momentum;                         /* m in [0, 1) */
   float weight_decay;                     /* coupled L2 on weights and biases */
+  float global_momentum;                  /* m_g in [0, 1) at the global
+                                             synchronisation; 0: plain mean */
   uint64_t seed;                          /* Philox4x32-10 key for sampling */
   int64_t N;                              /* dataset rows, >= K */
 } lsgd_config;
@@ -123,11 +125,29 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
 lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss);
 
 /* Synchronisation of eq. 2: every replica becomes (1/K) sum_k w^k, summed in
- * a fixed pairwise tree over k. Momentum buffers are left as they are. */
+ * a fixed pairwise tree over k. Momentum buffers are left as they are.
+ * LSGD_E_INVALID when the configuration sets a global momentum factor (that
+ * synchronisation needs the step size: lsgd_synchronise). */
 lsgd_status lsgd_average(lsgd_ctx* ctx);
 
+/*
+ * The end-of-round synchronisation. With global_momentum == 0 it is
+ * lsgd_average (lr unused). Otherwise it is local SGD with global momentum
+ * (the momentum appendix's paragraph on global momentum; with local
+ * momentum also on, its hybrid scheme): with w_s the model of the previous
+ * synchronisation (w0 at init) and u the global buffer (0 at init),
+ *   mean = (1/K) sum_k w^k  (the tree of lsgd_average),
+ *   u = m_g u + (w_s - mean) / lr,   w_s = w_s - lr u,   every w^k := w_s.
+ * The paper's (1/K) sum_k (w_s - w^k) is computed as w_s - mean. lr is the
+ * step size of the round's local steps; lr must be finite, and non-zero
+ * when m_g != 0, else LSGD_E_INVALID.
+ */
+lsgd_status lsgd_synchronise(lsgd_ctx* ctx, float lr);
+
 /* H local steps with step sizes h_lr[0..H-1] (host array), then
- * lsgd_average. d_loss: fp32 [H][K] or NULL. */
+ * lsgd_synchronise(ctx, h_lr[H-1]) (lsgd_average without global momentum).
+ * d_loss: fp32 [H][K] or NULL. With global momentum, H == 0 or a zero last
+ * step size is LSGD_E_INVALID. */
 lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
                            float* d_loss);
 
@@ -145,8 +165,10 @@ lsgd_status lsgd_average_blocks(lsgd_ctx* ctx, int32_t Kb);
 /*
  * One outer round of hierarchical local SGD (Algorithm 5): Hb times, run H
  * local steps then the block synchronisation over blocks of Kb replicas;
- * the last block synchronisation is replaced by the global average
- * (lsgd_average), to which it is identical in exact arithmetic. h_lr: host
+ * the last block synchronisation is replaced by the global synchronisation
+ * (lsgd_synchronise with the last step size; lsgd_average without global
+ * momentum), which the plain block mean would not change in exact
+ * arithmetic. h_lr: host
  * array of H * Hb step sizes in step order. d_loss: fp32 [Hb * H][K] or
  * NULL. Kb must divide K; H >= 0, Hb >= 1, else LSGD_E_INVALID. Hb == 1 is
  * lsgd_run_round; Kb == K runs Hb plain rounds of period H.
@@ -162,8 +184,16 @@ lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst);
 /* Copy replica `replica`'s momentum buffer to d_dst fp32 [P]. */
 lsgd_status lsgd_read_momentum(lsgd_ctx* ctx, int32_t replica, float* d_dst);
 
+/* Copy the global momentum buffer u to d_dst fp32 [P] / overwrite it from
+ * d_src fp32 [P] (checkpoint and resume; the synchronised model w_s is set
+ * by lsgd_write_params with replica == -1). LSGD_E_INVALID without global
+ * momentum. */
+lsgd_status lsgd_read_global_momentum(lsgd_ctx* ctx, float* d_dst);
+lsgd_status lsgd_write_global_momentum(lsgd_ctx* ctx, const float* d_src);
+
 /* Overwrite replica `replica` (or all replicas for -1) with d_src fp32 [P]
- * (and the bf16 operand copy). For checkpoint restore and tests. */
+ * (and the bf16 operand copy). For checkpoint restore and tests. With global
+ * momentum, replica == -1 also sets the synchronised model w_s. */
 lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
                               const float* d_src);
 
@@ -239,6 +269,16 @@ lsgd_status lsgd_grouped_gemm(int32_t dtype, int32_t trans_a, int32_t trans_b,
  * lsgd_average). */
 lsgd_status lsgd_replica_average(float* d_W, int32_t K, int64_t P,
                                  void* stream);
+
+/* The global-momentum synchronisation of lsgd_synchronise on plain arrays:
+ * d_W fp32 [K][P] replicas (all set to the new model), d_wsync fp32 [P] the
+ * previous synchronised model and d_ug fp32 [P] the global buffer, both
+ * updated in place. m_global in [0, 1), lr finite and non-zero, else
+ * LSGD_E_INVALID. */
+lsgd_status lsgd_replica_average_global_momentum(float* d_W, int32_t K,
+                                                 int64_t P, float* d_wsync,
+                                                 float* d_ug, float m_global,
+                                                 float lr, void* stream);
 
 /* In-place block average of d_W fp32 [K][P]: each of the K/Kb groups of Kb
  * consecutive rows is replaced by its mean (the kernel behind

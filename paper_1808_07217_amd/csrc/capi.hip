@@ -46,6 +46,7 @@ struct Layout {
   size_t esz = 4;  // activation / operand element size
   // byte offsets into the workspace
   size_t W = 0, U = 0, Wb = 0, Xb = 0, idx = 0, Z = 0, part = 0, rowloss = 0;
+  size_t Wsync = 0, Ug = 0;  // global momentum: model at the last sync, buffer
   bool head = false;  // top layer through the fused head kernels
   size_t act[LSGD_MAX_LAYERS] = {}, dZ[LSGD_MAX_LAYERS + 1] = {};
   size_t total = 0;
@@ -71,6 +72,9 @@ bool valid_config(const lsgd_config* c) {
   if (!std::isfinite(c->momentum) || c->momentum < 0.f || c->momentum >= 1.f)
     return false;
   if (!std::isfinite(c->weight_decay) || c->weight_decay < 0.f) return false;
+  if (!std::isfinite(c->global_momentum) || c->global_momentum < 0.f ||
+      c->global_momentum >= 1.f)
+    return false;
   if (c->N < c->K || c->N > (int64_t)INT32_MAX) return false;
   return true;
 }
@@ -119,6 +123,10 @@ Layout make_resnet_layout(const lsgd_config* c) {
   };
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
+  if (c->global_momentum != 0.f) {
+    l.Wsync = take(l.Ps * 4);
+    l.Ug = take(l.Ps * 4);
+  }
   l.idx = take(K * B * 4);
   l.rowloss = take(K * B * 4);
   size_t maxact = 0, maxpart = 0, maxbn = 0, maxwt = 0;
@@ -171,6 +179,10 @@ Layout make_layout(const lsgd_config* c) {
   };
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
+  if (c->global_momentum != 0.f) {
+    l.Wsync = take(l.Ps * 4);
+    l.Ug = take(l.Ps * 4);
+  }
   if (bf) {
     l.Wb = take(K * l.Ps * 2);
     l.Xb = take((size_t)c->N * c->widths[0] * 2);
@@ -252,6 +264,9 @@ struct lsgd_ctx {
 
   float* W() const { return (float*)(ws + lay.W); }
   float* U() const { return (float*)(ws + lay.U); }
+  bool gm() const { return cfg.global_momentum != 0.f; }
+  float* Wsync() const { return gm() ? (float*)(ws + lay.Wsync) : nullptr; }
+  float* Ug() const { return gm() ? (float*)(ws + lay.Ug) : nullptr; }
   bf16_t* Wb() const { return bf16() ? (bf16_t*)(ws + lay.Wb) : nullptr; }
   bf16_t* Xb() const { return (bf16_t*)(ws + lay.Xb); }
   int32_t* idx() const { return (int32_t*)(ws + lay.idx); }
@@ -702,6 +717,17 @@ lsgd_status do_average(lsgd_ctx* c) {
   return LSGD_OK;
 }
 
+// The end-of-round synchronisation: the plain average, or with a global
+// momentum factor its momentum form at step size lr.
+lsgd_status do_synchronise(lsgd_ctx* c, float lr) {
+  if (!c->gm()) return do_average(c);
+  LSGD_LAUNCH(c, "average",
+              lsgd::launch_average_gm(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
+                                      c->lay.Ps, c->Wsync(), c->Ug(),
+                                      c->cfg.global_momentum, lr, c->stream));
+  return LSGD_OK;
+}
+
 lsgd_status do_average_blocks(lsgd_ctx* c, int Kb) {
   if (Kb == c->cfg.K) return do_average(c);
   if (Kb == 1) return LSGD_OK;  // every block holds one replica
@@ -761,6 +787,12 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
   check(lsgd::launch_fill(c->U(), 0.f, (long long)K * ly.Ps, c->stream), "fill U");
   check(lsgd::launch_broadcast(d_w0, c->W(), c->Wb(), K, ly.P, ly.Ps, -1,
                                c->stream), "broadcast w0");
+  if (c->gm()) {  // w_(0) is the first synchronised model; the buffer is 0
+    check(lsgd::launch_fill(c->Wsync(), 0.f, ly.Ps, c->stream), "fill w_sync");
+    check(lsgd::launch_fill(c->Ug(), 0.f, ly.Ps, c->stream), "fill u_global");
+    check(lsgd::launch_broadcast(d_w0, c->Wsync(), nullptr, 1, ly.P, ly.Ps, -1,
+                                 c->stream), "w_sync := w0");
+  }
   if (c->bf16())
     check(lsgd::launch_to_bf16(d_X, c->Xb(), (long long)cfg->N * cfg->widths[0],
                                c->stream), "dataset to bf16");
@@ -790,7 +822,14 @@ lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss) {
 
 lsgd_status lsgd_average(lsgd_ctx* ctx) {
   LSGD_USABLE(ctx);
+  if (ctx->gm()) return LSGD_E_INVALID;  // needs the step size: lsgd_synchronise
   return do_average(ctx);
+}
+
+lsgd_status lsgd_synchronise(lsgd_ctx* ctx, float lr) {
+  LSGD_USABLE(ctx);
+  if (!std::isfinite(lr) || (ctx->gm() && lr == 0.f)) return LSGD_E_INVALID;
+  return do_synchronise(ctx, lr);
 }
 
 lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
@@ -799,12 +838,13 @@ lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
   if (H < 0 || (H > 0 && !h_lr)) return LSGD_E_INVALID;
   for (int h = 0; h < H; ++h)
     if (!std::isfinite(h_lr[h])) return LSGD_E_INVALID;
+  if (ctx->gm() && (H == 0 || h_lr[H - 1] == 0.f)) return LSGD_E_INVALID;
   for (int h = 0; h < H; ++h) {
     lsgd_status st = do_local_step(ctx, h_lr[h],
                                    d_loss ? d_loss + (size_t)h * ctx->cfg.K : nullptr);
     if (st != LSGD_OK) return st;
   }
-  return do_average(ctx);
+  return do_synchronise(ctx, H > 0 ? h_lr[H - 1] : 0.f);
 }
 
 lsgd_status lsgd_average_blocks(lsgd_ctx* ctx, int32_t Kb) {
@@ -818,6 +858,7 @@ lsgd_status lsgd_run_hierarchical_round(lsgd_ctx* ctx, int32_t H, int32_t Hb,
                                         float* d_loss) {
   LSGD_USABLE(ctx);
   if (H < 0 || Hb < 1 || Kb < 1 || ctx->cfg.K % Kb) return LSGD_E_INVALID;
+  if (ctx->gm() && H == 0) return LSGD_E_INVALID;  // no step size to sync with
   const long long steps = (long long)H * Hb;
   if (steps > 0 && !h_lr) return LSGD_E_INVALID;
   for (long long h = 0; h < steps; ++h)
@@ -831,7 +872,8 @@ lsgd_status lsgd_run_hierarchical_round(lsgd_ctx* ctx, int32_t H, int32_t Hb,
     }
     // the last block synchronisation is absorbed by the global one: the
     // mean of equal-sized block means is the global mean
-    lsgd_status st = b + 1 < Hb ? do_average_blocks(ctx, Kb) : do_average(ctx);
+    lsgd_status st = b + 1 < Hb ? do_average_blocks(ctx, Kb)
+                                : do_synchronise(ctx, h_lr[steps - 1]);
     if (st != LSGD_OK) return st;
   }
   return LSGD_OK;
@@ -867,6 +909,25 @@ lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
   LSGD_CK(ctx, lsgd::launch_broadcast(d_src, ctx->W(), ctx->Wb(), ctx->cfg.K,
                                       ctx->lay.P, ctx->lay.Ps, replica,
                                       ctx->stream));
+  if (replica == -1 && ctx->gm())  // the written model is the synchronised one
+    LSGD_CK(ctx, lsgd::launch_broadcast(d_src, ctx->Wsync(), nullptr, 1,
+                                        ctx->lay.P, ctx->lay.Ps, -1, ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_read_global_momentum(lsgd_ctx* ctx, float* d_dst) {
+  LSGD_USABLE(ctx);
+  if (!d_dst || !ctx->gm()) return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipMemcpyAsync(d_dst, ctx->Ug(), ctx->lay.P * sizeof(float),
+                              hipMemcpyDeviceToDevice, ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_write_global_momentum(lsgd_ctx* ctx, const float* d_src) {
+  LSGD_USABLE(ctx);
+  if (!d_src || !ctx->gm()) return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipMemcpyAsync(ctx->Ug(), d_src, ctx->lay.P * sizeof(float),
+                              hipMemcpyDeviceToDevice, ctx->stream));
   return LSGD_OK;
 }
 
@@ -1015,6 +1076,18 @@ lsgd_status lsgd_replica_average_blocks(float* d_W, int32_t K, int32_t Kb,
   if (!d_W || K < 1 || Kb < 1 || K % Kb || P < 0) return LSGD_E_INVALID;
   hipError_t e = lsgd::launch_average_blocks(d_W, nullptr, Kb, K / Kb, P, P,
                                              nullptr, (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
+}
+
+lsgd_status lsgd_replica_average_global_momentum(float* d_W, int32_t K,
+                                                 int64_t P, float* d_wsync,
+                                                 float* d_ug, float m_global,
+                                                 float lr, void* stream) {
+  if (!d_W || !d_wsync || !d_ug || K < 1 || P < 0 || !std::isfinite(m_global) ||
+      m_global < 0.f || m_global >= 1.f || !std::isfinite(lr) || lr == 0.f)
+    return LSGD_E_INVALID;
+  hipError_t e = lsgd::launch_average_gm(d_W, nullptr, K, P, P, d_wsync, d_ug,
+                                         m_global, lr, (hipStream_t)stream);
   return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
 }
 

@@ -214,6 +214,62 @@ __global__ void k_average4(float* W, bf16_t* Wb, int K, long long n,
   }
 }
 
+// Synchronisation with global momentum: the replica mean (the tree of
+// k_average4), then u = mg u + (ws - mean) / lr and ws = ws - lr u, where ws
+// holds the model of the previous synchronisation; every replica gets ws.
+__device__ __forceinline__ float gm_step(float mean, float& ws, float& u,
+                                         float mg, float lr) {
+  u = mg * u + (ws - mean) / lr;
+  ws = ws - lr * u;
+  return ws;
+}
+
+template <int KT>
+__global__ void k_average_gm4(float* W, bf16_t* Wb, int K, long long n,
+                              long long ld, float* ws, float* ug, float mg,
+                              float lr) {
+  const long long n4 = n / 4;
+  const float4* W4 = (const float4*)W;
+  const long long stride = ld / 4;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n4;
+       i += (long long)gridDim.x * blockDim.x) {
+    float4 s;
+    if constexpr (KT > 0)
+      s = Tree<KT, float4>::sum(W4 + i, stride);
+    else
+      s = tree_sum_rt<float4>(W4 + i, stride, K);
+    const float4 mean = div4(s, (float)K);
+    float4 w = ((float4*)ws)[i], u = ((float4*)ug)[i];
+    gm_step(mean.x, w.x, u.x, mg, lr);
+    gm_step(mean.y, w.y, u.y, mg, lr);
+    gm_step(mean.z, w.z, u.z, mg, lr);
+    gm_step(mean.w, w.w, u.w, mg, lr);
+    ((float4*)ws)[i] = w;
+    ((float4*)ug)[i] = u;
+    for (int k = 0; k < K; ++k) {
+      ((float4*)W)[k * stride + i] = w;
+      if (Wb) store_bf16x4(Wb + k * ld + 4 * i, w);
+    }
+  }
+}
+
+__global__ void k_average_gm1(float* W, bf16_t* Wb, int K, long long n,
+                              long long ld, float* ws, float* ug, float mg,
+                              float lr) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x) {
+    const float mean = tree_sum_rt<float>(W + i, ld, K) / (float)K;
+    float w = ws[i], u = ug[i];
+    gm_step(mean, w, u, mg, lr);
+    ws[i] = w;
+    ug[i] = u;
+    for (int k = 0; k < K; ++k) {
+      W[k * ld + i] = w;
+      if (Wb) Wb[k * ld + i] = f32_to_bf16(w);
+    }
+  }
+}
+
 __global__ void k_average1(float* W, bf16_t* Wb, int K, long long n,
                            long long ld, float* mean_out) {
   W += blockIdx.y * (long long)K * ld;
@@ -343,6 +399,39 @@ hipError_t launch_average_blocks(float* W, bf16_t* Wb, int Kb, int blocks,
 hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
                           long long ld, float* mean_out, hipStream_t s) {
   return launch_average_blocks(W, Wb, K, 1, n, ld, mean_out, s);
+}
+
+hipError_t launch_average_gm(float* W, bf16_t* Wb, int K, long long n,
+                             long long ld, float* ws, float* ug, float mg,
+                             float lr, hipStream_t s) {
+  if (n <= 0 || K <= 0) return hipSuccess;
+  const bool vec = n % 4 == 0 && ld % 4 == 0 && aligned16(W) && aligned16(ws) &&
+                   aligned16(ug) && (Wb == nullptr || ((uintptr_t)Wb & 7u) == 0);
+  if (!vec) {
+    hipLaunchKernelGGL(k_average_gm1, dim3(grid_for(n, 256)), dim3(256), 0, s,
+                       W, Wb, K, n, ld, ws, ug, mg, lr);
+    return hipGetLastError();
+  }
+  const dim3 grid(grid_for(n / 4, 256)), block(256);
+#define LSGD_AVG_GM_CASE(KK)                                                 \
+  case KK:                                                                   \
+    hipLaunchKernelGGL(k_average_gm4<KK>, grid, block, 0, s, W, Wb, K, n, ld, \
+                       ws, ug, mg, lr);                                      \
+    break;
+  switch (K) {
+    LSGD_AVG_GM_CASE(1)
+    LSGD_AVG_GM_CASE(2)
+    LSGD_AVG_GM_CASE(4)
+    LSGD_AVG_GM_CASE(8)
+    LSGD_AVG_GM_CASE(16)
+    LSGD_AVG_GM_CASE(32)
+    LSGD_AVG_GM_CASE(64)
+    default:
+      hipLaunchKernelGGL(k_average_gm4<0>, grid, block, 0, s, W, Wb, K, n, ld,
+                         ws, ug, mg, lr);
+  }
+#undef LSGD_AVG_GM_CASE
+  return hipGetLastError();
 }
 
 hipError_t launch_broadcast(const float* src, float* W, bf16_t* Wb, int K,

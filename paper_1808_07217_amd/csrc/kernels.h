@@ -164,6 +164,12 @@ hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
 // K-way average of the first n elements of K rows spaced ld apart.
 hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
                           long long ld, float* mean_out, hipStream_t s);
+// The K-way average with global momentum: mean of the K rows, then
+// ug = mg ug + (ws - mean) / lr, ws -= lr ug, and every row := ws (ws, ug:
+// [n] fp32, updated in place).
+hipError_t launch_average_gm(float* W, bf16_t* Wb, int K, long long n,
+                             long long ld, float* ws, float* ug, float mg,
+                             float lr, hipStream_t s);
 // The same average within each of `blocks` groups of Kb consecutive rows
 // (mean_out only with blocks == 1).
 hipError_t launch_average_blocks(float* W, bf16_t* Wb, int Kb, int blocks,

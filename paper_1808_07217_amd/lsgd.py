@@ -38,6 +38,7 @@ class Config(_c.Structure):
         ("nesterov", _c.c_int32),
         ("momentum", _c.c_float),
         ("weight_decay", _c.c_float),
+        ("global_momentum", _c.c_float),
         ("seed", _c.c_uint64),
         ("N", _c.c_int64),
     ]
@@ -54,6 +55,11 @@ _SIGS = {
     "lsgd_average": [_P],
     "lsgd_run_round": [_P, _c.c_int32, _c.POINTER(_c.c_float), _P],
     "lsgd_average_blocks": [_P, _c.c_int32],
+    "lsgd_synchronise": [_P, _c.c_float],
+    "lsgd_read_global_momentum": [_P, _P],
+    "lsgd_write_global_momentum": [_P, _P],
+    "lsgd_replica_average_global_momentum": [_P, _c.c_int32, _c.c_int64, _P, _P,
+                                             _c.c_float, _c.c_float, _P],
     "lsgd_run_hierarchical_round": [_P, _c.c_int32, _c.c_int32, _c.c_int32,
                                     _c.POINTER(_c.c_float), _P],
     "lsgd_read_params": [_P, _c.c_int32, _P],
@@ -113,7 +119,8 @@ def _stream_handle(stream) -> _c.c_void_p:
 def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
                 dtype: str = "fp32", momentum: float = 0.0,
                 weight_decay: float = 0.0, nesterov: bool = False,
-                seed: int = 0, model: str = "mlp") -> Config:
+                seed: int = 0, model: str = "mlp",
+                global_momentum: float = 0.0) -> Config:
     """widths: d_0 .. d_L for the MLP; (3072, classes) for resnet20."""
     if not 2 <= len(widths) <= MAX_LAYERS + 1:
         raise ValueError("widths must list d_0 .. d_L with 1 <= L <= 8")
@@ -127,6 +134,7 @@ def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
     cfg.nesterov = int(bool(nesterov))
     cfg.momentum = float(momentum)
     cfg.weight_decay = float(weight_decay)
+    cfg.global_momentum = float(global_momentum)
     cfg.seed = int(seed) & (2**64 - 1)
     return cfg
 
@@ -187,6 +195,11 @@ class Replicas:
         arr = (_c.c_float * max(H, 1))(*[float(v) for v in lrs])
         _check(_lib.lsgd_run_round(self._ctx, H, arr, _ptr(loss)), self._ctx)
 
+    def synchronise(self, lr: float):
+        """End-of-round synchronisation: the average, or with a global
+        momentum factor its momentum form at step size ``lr``."""
+        _check(_lib.lsgd_synchronise(self._ctx, float(lr)), self._ctx)
+
     def average_blocks(self, Kb: int):
         """Hierarchical block synchronisation: each block of Kb consecutive
         replicas takes its mean."""
@@ -209,6 +222,17 @@ class Replicas:
         out = out if out is not None else torch.empty(self.P, device=self.device)
         _check(_lib.lsgd_read_params(self._ctx, int(replica), _ptr(out)), self._ctx)
         return out
+
+    def read_global_momentum(self, out=None) -> torch.Tensor:
+        out = out if out is not None else torch.empty(self.P, device=self.device)
+        _check(_lib.lsgd_read_global_momentum(self._ctx, _ptr(out)), self._ctx)
+        return out
+
+    def write_global_momentum(self, src: torch.Tensor):
+        src = src.contiguous()
+        if src.dtype != torch.float32 or src.numel() != self.P:
+            raise ValueError("src must be float32 with P elements")
+        _check(_lib.lsgd_write_global_momentum(self._ctx, _ptr(src)), self._ctx)
 
     def read_momentum(self, replica: int, out=None) -> torch.Tensor:
         out = out if out is not None else torch.empty(self.P, device=self.device)
@@ -332,6 +356,22 @@ def replica_average_blocks(W: torch.Tensor, Kb: int) -> None:
         raise ValueError("W must be contiguous float32 [K][P]")
     _check(_lib.lsgd_replica_average_blocks(
         _ptr(W), W.shape[0], int(Kb), W.shape[1],
+        _stream_handle(torch.cuda.current_stream(W.device))))
+
+
+def replica_average_global_momentum(W: torch.Tensor, w_sync: torch.Tensor,
+                                    u_global: torch.Tensor, m_global: float,
+                                    lr: float) -> None:
+    """In place: W [K][P] := the global-momentum synchronisation of its rows;
+    w_sync and u_global ([P] float32) are updated."""
+    for t in (W, w_sync, u_global):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous float32")
+    if W.dim() != 2 or w_sync.numel() != W.shape[1] or u_global.numel() != W.shape[1]:
+        raise ValueError("W must be [K][P], w_sync and u_global [P]")
+    _check(_lib.lsgd_replica_average_global_momentum(
+        _ptr(W), W.shape[0], W.shape[1], _ptr(w_sync), _ptr(u_global),
+        float(m_global), float(lr),
         _stream_handle(torch.cuda.current_stream(W.device))))
 
 

@@ -52,13 +52,15 @@ def test_known_parameter_counts():
 @pytest.mark.parametrize("bad", [
     dict(K=0), dict(B_loc=0), dict(N=3, K=4), dict(widths=(64,)),
     dict(momentum=1.0), dict(momentum=-0.1), dict(weight_decay=-1.0),
-    dict(widths=(64, 1)),
+    dict(widths=(64, 1)), dict(global_momentum=1.0),
+    dict(global_momentum=-0.5), dict(global_momentum=float("nan")),
 ])
 def test_invalid_configs_are_rejected(bad):
     from paper_1808_07217_amd import lsgd as L
     kw = dict(widths=(64, 10), K=4, B_loc=32, N=4096)
     kw.update(bad)
-    opt = {k: kw.pop(k) for k in ("momentum", "weight_decay") if k in kw}
+    opt = {k: kw.pop(k) for k in ("momentum", "weight_decay", "global_momentum")
+           if k in kw}
     if len(kw["widths"]) < 2:
         with pytest.raises(ValueError):
             L.make_config(**kw, **opt)
@@ -75,10 +77,19 @@ def test_null_context_calls_fail_cleanly():
     assert lib.lsgd_average_blocks(None, 1) == 1
     assert lib.lsgd_run_hierarchical_round(None, 1, 1, 1, None, None) == 1
     assert lib.lsgd_replica_average_blocks(None, 4, 2, 8, None) == 1
+    assert lib.lsgd_synchronise(None, ctypes.c_float(0.1)) == 1
+    assert lib.lsgd_read_global_momentum(None, None) == 1
+    assert lib.lsgd_write_global_momentum(None, None) == 1
+    assert lib.lsgd_replica_average_global_momentum(
+        None, 4, 8, None, None, ctypes.c_float(0.5), ctypes.c_float(0.1), None) == 1
     # a block size that does not divide K is refused before any launch
     fake = ctypes.c_void_p(256)
     assert lib.lsgd_replica_average_blocks(fake, 6, 4, 8, None) == 1
     assert lib.lsgd_replica_average_blocks(fake, 6, 0, 8, None) == 1
+    # a global momentum factor outside [0, 1) or a zero step size likewise
+    for mg, lr in ((1.0, 0.1), (-0.1, 0.1), (0.5, 0.0)):
+        assert lib.lsgd_replica_average_global_momentum(
+            fake, 4, 8, fake, fake, ctypes.c_float(mg), ctypes.c_float(lr), None) == 1
     assert lib.lsgd_local_step(None, ctypes.c_float(0.1), None) == 1
     assert lib.lsgd_destroy(None) == 1
     for s in range(7):

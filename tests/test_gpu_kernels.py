@@ -149,6 +149,39 @@ def test_replica_average_blocks_rejects_a_block_size_not_dividing_k():
         L.replica_average_blocks(Wd, 4)
 
 
+@pytest.mark.parametrize("K,P,mg,lr", [(16, 1841162 + 6, 0.3, 0.001),
+                                       (4, 650, 0.9, 0.1), (5, 1027, 0.5, 0.02),
+                                       (1, 7, 0.0, 0.05), (64, 4100, 0.7, 0.01)])
+def test_replica_average_global_momentum(K, P, mg, lr):
+    """Global-momentum synchronisation against the oracle, elementwise within
+    an fp32 bound: the mean by the K-way tree (gamma_depth of sum |w| / K),
+    then a handful of roundings on the difference, the buffer and the step,
+    each at most u times the magnitudes involved."""
+    L = _lsgd()
+    print(f"global momentum average K={K} P={P} mg={mg}", flush=True)
+    rng = np.random.default_rng(K * 31 + P)
+    ws = rng.standard_normal(P).astype(np.float32)
+    W = (ws[None] + 0.01 * rng.standard_normal((K, P))).astype(np.float32)
+    u = (rng.standard_normal(P) * 0.5).astype(np.float32)
+    Wd, wsd, ud = to_dev(W), to_dev(ws), to_dev(u)
+    L.replica_average_global_momentum(Wd, wsd, ud, mg, lr)
+    W_got, ws_got, u_got = (t.cpu().numpy().astype(np.float64) for t in (Wd, wsd, ud))
+    W_ref, ws_ref, u_ref = O.average_global_momentum(
+        W.astype(np.float64), ws.astype(np.float64), u.astype(np.float64), mg, lr)
+    assert np.all(W_got == W_got[0:1])
+    np.testing.assert_array_equal(W_got[0], ws_got)
+    depth = int(np.ceil(np.log2(K))) if K > 1 else 0
+    a = np.abs
+    e_mean = gamma(depth + 1) * a(W).astype(np.float64).sum(0) / K
+    mean = W.astype(np.float64).mean(0)
+    e_u = 2 * (e_mean / lr + 4 * U32 * (a(mg * u) + a(ws - mean) / lr + a(u_ref)
+                                         + a(ws) / lr))
+    e_w = 2 * (e_mean + 4 * U32 * (a(ws) + a(ws - mean) + a(ws_ref)
+                                   + lr * a(mg * u) + lr * a(u_ref)))
+    assert np.all(a(u_got - u_ref) <= e_u), np.max(a(u_got - u_ref) / e_u)
+    assert np.all(a(ws_got - ws_ref) <= e_w), np.max(a(ws_got - ws_ref) / e_w)
+
+
 # ------------------------------------------------------------------ update
 @pytest.mark.parametrize("nesterov", [False, True])
 @pytest.mark.parametrize("n", [1, 3, 4099, 1 << 20])

@@ -339,6 +339,95 @@ def test_hierarchical_round_rejects_bad_blocks():
     assert reps.step == 0
 
 
+# -------------------------------------------------- global / hybrid momentum
+def _sync_error(reps, st, w):
+    """Model-space errors after a synchronisation: the replicas' model, and
+    the global buffer's step lr * u (the buffer itself is a model change
+    divided by the step size, so its own relative error carries the model's
+    cancellation; in model space it is held to the parameter bar)."""
+    got = reps.read_params(0).cpu().numpy()
+    e_w = normwise(got, st.W[0])
+    du = np.abs(reps.read_global_momentum().cpu().numpy().astype(np.float64)
+                - st.u_global)
+    e_u = float(np.max(du) * w.lr / np.max(np.abs(st.W[0])))
+    return e_w, e_u
+
+
+@pytest.mark.parametrize("mg,momentum,nesterov", [(0.5, 0.0, False),
+                                                  (0.3, 0.9, False),
+                                                  (0.9, 0.9, True)])
+def test_global_momentum_rounds_match_oracle(mg, momentum, nesterov):
+    """Local SGD with global momentum (local momentum 0) and the hybrid
+    scheme (local heavy ball or Nesterov plus the global buffer): every
+    replica and the global buffer after each of four rounds, the losses of
+    every step."""
+    w = _small((70, 48, 36, 10), K=4, B=12, H=3, rounds=4, momentum=momentum,
+               nesterov=nesterov).scaled(global_momentum=mg)
+    X, y, w0 = _small_data(w, seed=50)
+    print(f"global momentum mg={mg} local m={momentum} nesterov={nesterov}", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(w.H, w.K, device=device())
+    for t in range(w.rounds):
+        reps.run_round([w.lr] * w.H, loss)
+        want = O.run_round(st, w, X, y, w.H, w.lr)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        e_w, e_u = _sync_error(reps, st, w)
+        assert e_w <= PARAM_TOL_FP32, (t, e_w)
+        assert e_u <= PARAM_TOL_FP32, (t, e_u)
+        for k in range(1, w.K):
+            np.testing.assert_array_equal(reps.read_params(k).cpu().numpy(),
+                                          reps.read_params(0).cpu().numpy())
+
+
+def test_global_momentum_h1_is_minibatch_heavy_ball_on_the_gpu():
+    """H = 1, no local momentum: the GPU run equals the oracle's mini-batch
+    SGD with heavy-ball momentum m_g on the union batch."""
+    w = _small((70, 48, 36, 10), K=4, B=12, H=1, rounds=6,
+               momentum=0.0).scaled(global_momentum=0.8)
+    X, y, w0 = _small_data(w, seed=51)
+    reps = make_replicas(w, X, y, w0)
+    for _ in range(6):
+        reps.run_round([w.lr])
+    ref = O.minibatch_sgd(w.scaled(momentum=0.8), X, y, w0, steps=6, lr=w.lr)
+    assert normwise(reps.read_params(-1).cpu().numpy(), ref) <= PARAM_TOL_FP32
+
+
+def test_global_momentum_entry_points_and_resume():
+    """lsgd_average is refused once a global factor is set (the
+    synchronisation needs the step size), synchronise() equals the end of
+    run_round bit for bit, and a context restored from the synchronised
+    model, the global buffer and the step counter continues bit-identically
+    (no local momentum, so the local buffers carry nothing over)."""
+    from paper_1808_07217_amd import lsgd as L
+    w = _small((70, 48, 36, 10), K=4, B=12, H=2, rounds=1,
+               momentum=0.0).scaled(global_momentum=0.6)
+    X, y, w0 = _small_data(w, seed=52)
+    a = make_replicas(w, X, y, w0)
+    with pytest.raises(L.LsgdError):
+        a.average()
+    with pytest.raises(L.LsgdError):
+        a.run_round([])
+    b = make_replicas(w, X, y, w0)
+    a.run_round([0.02, 0.03])
+    b.local_step(0.02)
+    b.local_step(0.03)
+    b.synchronise(0.03)
+    np.testing.assert_array_equal(a.read_params(-1).cpu().numpy(),
+                                  b.read_params(-1).cpu().numpy())
+    np.testing.assert_array_equal(a.read_global_momentum().cpu().numpy(),
+                                  b.read_global_momentum().cpu().numpy())
+    a.run_round([0.02, 0.02])          # a second round so that u != 0 matters
+    c = make_replicas(w, X, y, w0)
+    c.write_params(a.read_params(0))
+    c.write_global_momentum(a.read_global_momentum())
+    c.step = a.step
+    a.run_round([0.02, 0.02])
+    c.run_round([0.02, 0.02])
+    np.testing.assert_array_equal(a.read_params(-1).cpu().numpy(),
+                                  c.read_params(-1).cpu().numpy())
+
+
 # --------------------------------------------------------- full-size rounds
 @pytest.fixture(scope="module")
 def img_data():
@@ -399,6 +488,25 @@ def test_mlp_512_hierarchical_round_full_size(img_data):
     e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
     print(f"mlp_512 hierarchical round params normwise error {e:.3e}", flush=True)
     assert e <= PARAM_TOL_FP32
+
+
+def test_mlp_512_hybrid_momentum_two_rounds_full_size(img_data):
+    """Workload 2's shape with hybrid momentum (local heavy ball 0.9, global
+    0.3): two rounds of 16 steps, so the global buffer acts in the second."""
+    w = wk.get("mlp_512").scaled(global_momentum=0.3)
+    X, y = img_data
+    w0 = wk.initial_weights(w)
+    print("mlp_512 hybrid momentum, two rounds", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(w.H, w.K, device=device())
+    for t in range(2):
+        reps.run_round([w.lr] * w.H, loss)
+        want = O.run_round(st, w, X, y, w.H, w.lr)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        e_w, e_u = _sync_error(reps, st, w)
+        print(f"round {t + 1}: params {e_w:.3e}, lr * u {e_u:.3e}", flush=True)
+        assert e_w <= PARAM_TOL_FP32 and e_u <= PARAM_TOL_FP32, (t, e_w, e_u)
 
 
 def test_wide_bf16_first_round_two_replicas_full_size(img_data):

@@ -116,6 +116,14 @@ WORKLOADS = {
         dtype="fp32", K=16, B_loc=128, H=4, rounds=20, lr=0.001,
         momentum=0.9, nesterov=False, weight_decay=1e-4, Kb=2, Hb=4, **_IMG,
         data_seed=201, init_seed=202, sample_seed=0x5EED0006),
+    # hybrid momentum on the same MLP: local heavy ball 0.9 plus a global
+    # buffer with factor 0.3 at every synchronisation (the momentum
+    # appendix's local/global grid, at one of its well-behaved settings)
+    "hybrid_mlp_512": Workload(
+        name="hybrid_mlp_512", model="mlp", widths=(3072, 512, 512, 10),
+        dtype="fp32", K=16, B_loc=128, H=16, rounds=20, lr=0.001,
+        momentum=0.9, nesterov=False, weight_decay=1e-4, global_momentum=0.3,
+        **_IMG, data_seed=201, init_seed=202, sample_seed=0x5EED0007),
     # ResNet-20-shaped CNN, fp32, per-worker BN, heavy-ball momentum
     "resnet20": Workload(
         name="resnet20", model="resnet20", widths=(3072, 10), dtype="fp32",
