@@ -200,11 +200,17 @@ def decay_mask(widths):
 # appendix on local SGD with momentum; Nesterov, no dampening, weight decay
 # from the CIFAR hyper-parameter paragraph)
 # --------------------------------------------------------------------------
-def sgd_update(w, u, grad, lr, momentum, weight_decay, nesterov, wd_mask=1.0):
-    """One local step on one replica: returns (w_new, u_new)."""
+def sgd_update(w, u, grad, lr, momentum, weight_decay, nesterov, wd_mask=1.0,
+               sign_step=False):
+    """One local step on one replica: returns (w_new, u_new). With
+    ``sign_step`` the replica moves by the sign of its update direction (the
+    local step of the signSGD variant, Algorithm 3: the direction may
+    include weight decay and momentum); sign(0) = 0."""
     g = grad + (weight_decay * wd_mask) * w
     u = momentum * u + g
     d = g + momentum * u if nesterov else u
+    if sign_step:
+        d = np.sign(d)
     return w - lr * d, u
 
 
@@ -247,12 +253,52 @@ def average_global_momentum(W, w_sync, u_global, m_global, lr):
     return np.broadcast_to(w, W.shape).copy(), w.copy(), u
 
 
+def compress_sign(delta):
+    """The compressor of Algorithms 3 and 4: the sign vector s = sign(delta)
+    (sign(0) = 0) and the scale p = ||delta||_1 / d, d the model size."""
+    delta = np.asarray(delta, np.float64)
+    return np.sign(delta), np.abs(delta).sum() / delta.size
+
+
+def average_sign_compressed(W, w_sync, E=None):
+    """Sign-compressed synchronisation (Algorithm 3's; Algorithm 4's when the
+    error memories E are given). Each worker's model difference
+    Delta^k = w_(t) - w^k_(t)+H, plus e^k for Algorithm 4, is sent as
+    s^k p^k; the new synchronised model is w_(t) - (1/K) sum_k s^k p^k.
+    Algorithm 4 keeps what the message missed, e^k = Delta^k - s^k p^k
+    (error feedback: the memory holds the part of the corrected difference
+    that was not transmitted). Returns (every replica set to w_(t+1),
+    w_(t+1), new E or None)."""
+    W = np.asarray(W, np.float64)
+    w_sync = np.asarray(w_sync, np.float64)
+    K = W.shape[0]
+    sent = np.zeros_like(W)
+    newE = None if E is None else np.zeros_like(W)
+    for k in range(K):
+        delta = w_sync - W[k]
+        if E is not None:
+            delta = delta + E[k]
+        s, p = compress_sign(delta)
+        sent[k] = s * p
+        if E is not None:
+            newE[k] = delta - sent[k]
+    w = w_sync - sent.sum(axis=0) / K
+    return np.broadcast_to(w, W.shape).copy(), w.copy(), newE
+
+
 def synchronise(state, wl, lr):
     """The global synchronisation at the end of a round: the plain average of
-    eq. (2), or the global-momentum form when the workload sets a global
-    momentum factor (read with the step size of the round's local steps)."""
+    eq. (2); the global-momentum form when the workload sets a global
+    momentum factor (read with the step size of the round's local steps);
+    the sign-compressed forms of Algorithms 3 ("sign") and 4 ("ef_sign")."""
     m_g = getattr(wl, "global_momentum", 0.0)
-    if m_g:
+    scheme = getattr(wl, "scheme", "local")
+    if scheme in ("sign", "ef_sign"):
+        state.W, state.w_sync, E = average_sign_compressed(
+            state.W, state.w_sync, state.E if scheme == "ef_sign" else None)
+        if E is not None:
+            state.E = E
+    elif m_g:
         state.W, state.w_sync, state.u_global = average_global_momentum(
             state.W, state.w_sync, state.u_global, m_g, lr)
     else:
@@ -288,6 +334,7 @@ class State:
         self.step = 0
         self.w_sync = np.asarray(w0, np.float64).copy()
         self.u_global = np.zeros_like(self.w_sync)
+        self.E = np.zeros_like(self.W)     # error memories e^k (Algorithm 4)
 
 
 def local_step(state, wl, X, y, lr, replicas=None):
@@ -306,7 +353,7 @@ def local_step(state, wl, X, y, lr, replicas=None):
         loss, grad = model_loss_and_grad(wl, state.W[k], A0, y[idx])
         state.W[k], state.U[k] = sgd_update(
             state.W[k], state.U[k], grad, lr, wl.momentum, wl.weight_decay,
-            wl.nesterov, mask)
+            wl.nesterov, mask, sign_step=getattr(wl, "scheme", "local") == "sign")
         losses[k] = loss
     state.step += 1
     return losses

@@ -500,6 +500,109 @@ def test_hybrid_momentum_first_round_and_buffers():
                                rtol=1e-9, atol=1e-12)
 
 
+# ------------------------------------------- sign-compressed synchronisation
+def test_sign_compressor_properties():
+    """sign(0) = 0 and zeros count in the model size d; a difference whose
+    entries share one magnitude passes unchanged; without zeros the message
+    keeps the l1 norm and its residual is orthogonal to the sign vector
+    (p = ||delta||_1 / d is then the l2-optimal scale of s)."""
+    s_, p_ = O.compress_sign(np.array([2.0, 0.0, -2.0, 0.0]))
+    np.testing.assert_array_equal(s_, [1.0, 0.0, -1.0, 0.0])
+    assert p_ == 1.0
+    rng = np.random.default_rng(61)
+    flat = 0.25 * np.where(rng.random(1000) < 0.5, -1.0, 1.0)
+    s_, p_ = O.compress_sign(flat)
+    np.testing.assert_array_equal(s_ * p_, flat)
+    delta = rng.standard_normal(997)
+    s_, p_ = O.compress_sign(delta)
+    np.testing.assert_allclose(np.abs(s_ * p_).sum(), np.abs(delta).sum(), rtol=1e-13)
+    np.testing.assert_allclose(np.dot(s_, delta - s_ * p_), 0.0, atol=1e-10)
+    c = np.dot(s_, delta) / np.dot(s_, s_)
+    np.testing.assert_allclose(c, p_, rtol=1e-13)
+
+
+def test_sign_sync_without_memory_and_constant_magnitudes_is_the_average():
+    """If every worker's difference has one magnitude per worker and no
+    zeros, Algorithm 3's synchronisation is exactly the plain average."""
+    rng = np.random.default_rng(62)
+    K, P = 4, 64
+    w_sync = rng.standard_normal(P)
+    mags = np.array([0.5, 0.25, 0.125, 0.0625])
+    W = w_sync[None] - mags[:, None] * np.where(rng.random((K, P)) < 0.5, -1.0, 1.0)
+    Wn, wn, E = O.average_sign_compressed(W, w_sync)
+    assert E is None
+    np.testing.assert_allclose(Wn, O.average(W), rtol=0, atol=1e-15)
+
+
+def test_alg3_h1_is_signsgd_with_sign_averaging():
+    """Algorithm 3 at H' = 1: each worker's round moves by lr * sign(d^k)
+    exactly, so its message is that move and the synchronisation takes the
+    average of the workers' signs -- signSGD with an average instead of a
+    majority vote over signs, as the appendix on compression says. The
+    reference below writes that update directly."""
+    wl = _small(True, 0.9, K=4, H=1, B=8, rounds=5).scaled(scheme="sign")
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(63).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st, _ = O.run(wl, X, y, w0)
+    w = w0.copy()
+    u = np.zeros((wl.K, w.size))
+    for s in range(5):
+        signs = []
+        for k in range(wl.K):
+            idx = O.sample_indices(wl.sample_seed, s, k, wl.K, wl.N, wl.B_loc)
+            _, grad = O.model_loss_and_grad(wl, w, np.asarray(X[idx], np.float64), y[idx])
+            g = grad + wl.weight_decay * w
+            u[k] = wl.momentum * u[k] + g
+            signs.append(np.sign(g + wl.momentum * u[k]))
+        w = w - wl.lr * np.mean(signs, axis=0)
+    np.testing.assert_allclose(st.W[0], w, rtol=1e-12, atol=1e-13)
+
+
+def test_alg4_local_steps_are_plain_and_memory_feeds_back():
+    """Algorithm 4: the local steps are plain SGD steps (the replicas before
+    the synchronisation equal those of local SGD), the memories start at 0,
+    and error feedback telescopes: the model minus the mean memory moves by
+    exactly the uncompressed mean model change of every round. Each memory
+    is orthogonal to its sign vector and shorter than the corrected
+    difference it came from."""
+    wl = _small(False, 0.9, K=4, H=3, B=8, rounds=1).scaled(scheme="ef_sign")
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(64).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st, plain = O.State(w0, wl.K), O.State(w0, wl.K)
+    tilde = st.w_sync - st.E.mean(axis=0)
+    for t in range(4):
+        for _ in range(3):
+            O.local_step(st, wl, X, y, wl.lr)
+            if t == 0:
+                O.local_step(plain, wl.scaled(scheme="local"), X, y, wl.lr)
+        if t == 0:
+            np.testing.assert_array_equal(st.W, plain.W)
+            assert not np.any(st.E)
+        w_start, W_end, E_old = st.w_sync.copy(), st.W.copy(), st.E.copy()
+        O.synchronise(st, wl, wl.lr)
+        new_tilde = st.w_sync - st.E.mean(axis=0)
+        np.testing.assert_allclose(new_tilde, tilde - (w_start - W_end.mean(axis=0)),
+                                   rtol=1e-11, atol=1e-13)
+        tilde = new_tilde
+        for k in range(wl.K):
+            delta = w_start - W_end[k] + E_old[k]
+            s_ = np.sign(delta)
+            np.testing.assert_allclose(np.dot(s_, st.E[k]), 0.0, atol=1e-12)
+            assert np.linalg.norm(st.E[k]) < np.linalg.norm(delta)
+        np.testing.assert_array_equal(st.W, np.broadcast_to(st.w_sync, st.W.shape))
+
+
+def test_alg3_local_steps_move_by_signs():
+    """Algorithm 3's local step moves every coordinate by exactly lr (the
+    update direction has no zero entries here), unlike the plain step."""
+    wl = _small(True, 0.9, K=2, H=1, B=8, rounds=1).scaled(scheme="sign")
+    X, y = wk.dataset(wl)
+    w0 = np.random.default_rng(65).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st = O.State(w0, wl.K)
+    O.local_step(st, wl, X, y, wl.lr)
+    np.testing.assert_allclose(np.abs(st.W - w0[None]), wl.lr, rtol=1e-9)
+
+
 def test_loss_decreases_on_every_workload_first_rounds():
     wl = wk.get("softmax_d64")
     X, y = wk.dataset(wl)

@@ -70,6 +70,7 @@ class Workload:
     Kb: int = 0                # hierarchical block size K' (0: none)
     Hb: int = 1                # block rounds per global average, H^b
     global_momentum: float = 0.0   # m_g at the global average (0: plain mean)
+    scheme: str = "local"      # "local"; "sign" (Algorithm 3); "ef_sign" (4)
 
     @property
     def n_layers(self) -> int:
