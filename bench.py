@@ -66,6 +66,10 @@ def kernel_cost(tag: str, w) -> tuple:
     if tag in ("average", "average_blocks"):   # same traffic per launch
         gm = 16 * P if w.global_momentum else 0  # w_sync and u read + written
         return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0) + gm
+    if tag == "sign_sync":   # two passes: l1 + packed signs, then apply
+        if w.scheme == "ef_sign":   # W, e read twice, written once
+            return 0, 24 * K * P + 8 * P
+        return 0, 8 * K * P + K * P // 2 + 8 * P
     if tag == "wgrad_update":   # one launch over every generic layer
         Lg = L - 1 if d[L] <= 32 else L   # the top layer has its own kernels
         costs = [kernel_cost(f"wgrad_update{l}", w) for l in range(1, Lg + 1)]
@@ -258,6 +262,7 @@ def cpu_baseline(w, X, y, w0):
         O.run_round(st, w, X, y, w.H, w.lr)
         what = (f"H={w.H} local steps on all K={w.K} replicas + "
                 + ("synchronisation with global momentum" if w.global_momentum
+                   else f"{w.scheme} synchronisation" if w.scheme != "local"
                    else "average"))
     dt = time.perf_counter() - t0
     samples = w.K * w.H * w.Hb * w.B_loc
@@ -293,7 +298,7 @@ def main():
     cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype,
                         momentum=w.momentum, weight_decay=w.weight_decay,
                         nesterov=w.nesterov, seed=w.sample_seed, model=w.model,
-                        global_momentum=w.global_momentum)
+                        global_momentum=w.global_momentum, scheme=w.scheme)
     Xd = torch.from_numpy(np.array(X)).to(dev)
     yd = torch.from_numpy(np.array(y)).to(dev)
     reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))
@@ -391,6 +396,7 @@ def main():
                    "samples_per_step": samples,
                    "momentum": w.momentum, "nesterov": w.nesterov,
                    "weight_decay": w.weight_decay,
+                   **({"scheme": w.scheme} if w.scheme != "local" else {}),
                    **({"global_momentum": w.global_momentum}
                       if w.global_momentum else {})},
     }

@@ -66,6 +66,20 @@ typedef enum lsgd_status {
  * classifier weight [64][classes] and bias [classes]. */
 enum { LSGD_MODEL_MLP = 0, LSGD_MODEL_RESNET20 = 1 };
 enum { LSGD_FP32 = 0, LSGD_BF16 = 1 };
+/* Local-step / synchronisation scheme (the appendix on compression):
+ * LSGD_SCHEME_LOCAL   plain local steps, plain mean (eq. 2);
+ * LSGD_SCHEME_SIGN    Algorithm 3: local steps move by sign(d) (d the update
+ *                     direction after weight decay and momentum, sign(0) =
+ *                     0); the synchronisation sends each worker's model
+ *                     difference Delta^k = w_s - w^k as sign(Delta^k) *
+ *                     ||Delta^k||_1 / P and sets every replica to
+ *                     w_s - (1/K) sum_k of those messages;
+ * LSGD_SCHEME_EF_SIGN Algorithm 4: plain local steps; the synchronisation
+ *                     compresses Delta^k + e^k the same way and keeps the
+ *                     error memory e^k = Delta^k + e^k - message (e^k = 0 at
+ *                     init, per worker, never averaged).
+ * w_s is the model of the previous synchronisation (w0 at init). */
+enum { LSGD_SCHEME_LOCAL = 0, LSGD_SCHEME_SIGN = 1, LSGD_SCHEME_EF_SIGN = 2 };
 #define LSGD_MAX_LAYERS 8
 
 /*
@@ -86,6 +100,8 @@ typedef struct lsgd_config {
   float weight_decay;                     /* coupled L2 on weights and biases */
   float global_momentum;                  /* m_g in [0, 1) at the global
                                              synchronisation; 0: plain mean */
+  int32_t scheme;                         /* LSGD_SCHEME_*; a sign scheme
+                                             needs global_momentum == 0 */
   uint64_t seed;                          /* Philox4x32-10 key for sampling */
   int64_t N;                              /* dataset rows, >= K */
 } lsgd_config;
@@ -126,13 +142,14 @@ lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss);
 
 /* Synchronisation of eq. 2: every replica becomes (1/K) sum_k w^k, summed in
  * a fixed pairwise tree over k. Momentum buffers are left as they are.
- * LSGD_E_INVALID when the configuration sets a global momentum factor (that
- * synchronisation needs the step size: lsgd_synchronise). */
+ * LSGD_E_INVALID when the configuration sets a global momentum factor or a
+ * sign scheme (those synchronise through lsgd_synchronise). */
 lsgd_status lsgd_average(lsgd_ctx* ctx);
 
 /*
- * The end-of-round synchronisation. With global_momentum == 0 it is
- * lsgd_average (lr unused). Otherwise it is local SGD with global momentum
+ * The end-of-round synchronisation. With a sign scheme it is the
+ * sign-compressed synchronisation of Algorithm 3 or 4 (lr unused; see
+ * LSGD_SCHEME_*). With global_momentum == 0 it is lsgd_average (lr unused). Otherwise it is local SGD with global momentum
  * (the momentum appendix's paragraph on global momentum; with local
  * momentum also on, its hybrid scheme): with w_s the model of the previous
  * synchronisation (w0 at init) and u the global buffer (0 at init),
@@ -190,6 +207,13 @@ lsgd_status lsgd_read_momentum(lsgd_ctx* ctx, int32_t replica, float* d_dst);
  * momentum. */
 lsgd_status lsgd_read_global_momentum(lsgd_ctx* ctx, float* d_dst);
 lsgd_status lsgd_write_global_momentum(lsgd_ctx* ctx, const float* d_src);
+
+/* Copy replica `replica`'s error memory e^k (LSGD_SCHEME_EF_SIGN) to d_dst
+ * fp32 [P] / overwrite it from d_src fp32 [P]. LSGD_E_INVALID for other
+ * schemes or a replica outside [0, K). */
+lsgd_status lsgd_read_error_memory(lsgd_ctx* ctx, int32_t replica, float* d_dst);
+lsgd_status lsgd_write_error_memory(lsgd_ctx* ctx, int32_t replica,
+                                    const float* d_src);
 
 /* Overwrite replica `replica` (or all replicas for -1) with d_src fp32 [P]
  * (and the bf16 operand copy). For checkpoint restore and tests. With global
@@ -280,6 +304,23 @@ lsgd_status lsgd_replica_average_global_momentum(float* d_W, int32_t K,
                                                  float* d_ug, float m_global,
                                                  float lr, void* stream);
 
+/* Scratch bytes lsgd_replica_sign_sync needs for K rows of P elements
+ * (P % 4 == 0, else LSGD_E_INVALID). */
+lsgd_status lsgd_sign_sync_scratch_bytes(int32_t K, int64_t P, size_t* bytes);
+
+/* The sign-compressed synchronisation of lsgd_synchronise on plain arrays:
+ * d_W fp32 [K][P] replicas (all set to the new model), d_wsync fp32 [P] the
+ * previous synchronised model (updated), d_E fp32 [K][P] the error memories
+ * (updated; Algorithm 4) or NULL (Algorithm 3). d_scratch: caller-owned
+ * device memory of lsgd_sign_sync_scratch_bytes (LSGD_E_WORKSPACE if
+ * smaller). Pointers 16-byte aligned and P % 4 == 0, else LSGD_E_INVALID.
+ * Summation orders: each |delta| partial in fp64 over fixed chunks of 8192
+ * elements, chunks added in a fixed order; messages added over k in
+ * ascending order in fp32. */
+lsgd_status lsgd_replica_sign_sync(float* d_W, int32_t K, int64_t P,
+                                   float* d_wsync, float* d_E, void* d_scratch,
+                                   size_t scratch_bytes, void* stream);
+
 /* In-place block average of d_W fp32 [K][P]: each of the K/Kb groups of Kb
  * consecutive rows is replaced by its mean (the kernel behind
  * lsgd_average_blocks). Kb must divide K, else LSGD_E_INVALID. */
@@ -287,8 +328,9 @@ lsgd_status lsgd_replica_average_blocks(float* d_W, int32_t K, int32_t Kb,
                                         int64_t P, void* stream);
 
 /* Fused update over n elements (the kernel behind the parameter update of
- * lsgd_local_step): g = d_G + wd * w; u = m u + g; d = nesterov ? g + m u
- * : u; w -= lr * d. d_W, d_U updated in place. */
+ * lsgd_local_step): g = d_G + wd * w; u = m u + g; d = (nesterov & 1) ?
+ * g + m u : u; with nesterov & 2, d = sign(d) (the sign step); w -= lr * d.
+ * d_W, d_U updated in place. nesterov outside [0, 3]: LSGD_E_INVALID. */
 lsgd_status lsgd_sgd_update(float* d_W, float* d_U, const float* d_G,
                             int64_t n, float lr, float momentum,
                             float weight_decay, int32_t nesterov,

@@ -46,11 +46,18 @@ struct Layout {
   size_t esz = 4;  // activation / operand element size
   // byte offsets into the workspace
   size_t W = 0, U = 0, Wb = 0, Xb = 0, idx = 0, Z = 0, part = 0, rowloss = 0;
-  size_t Wsync = 0, Ug = 0;  // global momentum: model at the last sync, buffer
+  size_t Wsync = 0, Ug = 0;  // model at the last sync; global momentum buffer
+  size_t E = 0, sign = 0, sign_bytes = 0;  // error memories; sign-sync scratch
   bool head = false;  // top layer through the fused head kernels
   size_t act[LSGD_MAX_LAYERS] = {}, dZ[LSGD_MAX_LAYERS + 1] = {};
   size_t total = 0;
 };
+
+// The local step's mode bits: Nesterov, and the sign step of Algorithm 3.
+int upd_mode(const lsgd_config& cf) {
+  return (cf.nesterov ? lsgd::kModeNesterov : 0) |
+         (cf.scheme == LSGD_SCHEME_SIGN ? lsgd::kModeSign : 0);
+}
 
 bool valid_config(const lsgd_config* c) {
   if (!c) return false;
@@ -75,6 +82,8 @@ bool valid_config(const lsgd_config* c) {
   if (!std::isfinite(c->global_momentum) || c->global_momentum < 0.f ||
       c->global_momentum >= 1.f)
     return false;
+  if (c->scheme < LSGD_SCHEME_LOCAL || c->scheme > LSGD_SCHEME_EF_SIGN) return false;
+  if (c->scheme != LSGD_SCHEME_LOCAL && c->global_momentum != 0.f) return false;
   if (c->N < c->K || c->N > (int64_t)INT32_MAX) return false;
   return true;
 }
@@ -123,9 +132,13 @@ Layout make_resnet_layout(const lsgd_config* c) {
   };
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
-  if (c->global_momentum != 0.f) {
+  if (c->global_momentum != 0.f || c->scheme != LSGD_SCHEME_LOCAL)
     l.Wsync = take(l.Ps * 4);
-    l.Ug = take(l.Ps * 4);
+  if (c->global_momentum != 0.f) l.Ug = take(l.Ps * 4);
+  if (c->scheme == LSGD_SCHEME_EF_SIGN) l.E = take(K * l.Ps * 4);
+  if (c->scheme != LSGD_SCHEME_LOCAL) {
+    l.sign_bytes = lsgd::sign_sync_scratch_bytes((int)K, l.Ps);
+    l.sign = take(l.sign_bytes);
   }
   l.idx = take(K * B * 4);
   l.rowloss = take(K * B * 4);
@@ -179,9 +192,13 @@ Layout make_layout(const lsgd_config* c) {
   };
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
-  if (c->global_momentum != 0.f) {
+  if (c->global_momentum != 0.f || c->scheme != LSGD_SCHEME_LOCAL)
     l.Wsync = take(l.Ps * 4);
-    l.Ug = take(l.Ps * 4);
+  if (c->global_momentum != 0.f) l.Ug = take(l.Ps * 4);
+  if (c->scheme == LSGD_SCHEME_EF_SIGN) l.E = take(K * l.Ps * 4);
+  if (c->scheme != LSGD_SCHEME_LOCAL) {
+    l.sign_bytes = lsgd::sign_sync_scratch_bytes((int)K, l.Ps);
+    l.sign = take(l.sign_bytes);
   }
   if (bf) {
     l.Wb = take(K * l.Ps * 2);
@@ -265,8 +282,15 @@ struct lsgd_ctx {
   float* W() const { return (float*)(ws + lay.W); }
   float* U() const { return (float*)(ws + lay.U); }
   bool gm() const { return cfg.global_momentum != 0.f; }
-  float* Wsync() const { return gm() ? (float*)(ws + lay.Wsync) : nullptr; }
+  bool signed_sync() const { return cfg.scheme != LSGD_SCHEME_LOCAL; }
+  bool ef() const { return cfg.scheme == LSGD_SCHEME_EF_SIGN; }
+  // w_s, the model of the previous synchronisation (global momentum and
+  // the sign-compressed schemes keep it)
+  float* Wsync() const {
+    return gm() || signed_sync() ? (float*)(ws + lay.Wsync) : nullptr;
+  }
   float* Ug() const { return gm() ? (float*)(ws + lay.Ug) : nullptr; }
+  float* E() const { return ef() ? (float*)(ws + lay.E) : nullptr; }
   bf16_t* Wb() const { return bf16() ? (bf16_t*)(ws + lay.Wb) : nullptr; }
   bf16_t* Xb() const { return (bf16_t*)(ws + lay.Xb); }
   int32_t* idx() const { return (int32_t*)(ws + lay.idx); }
@@ -364,7 +388,7 @@ GemmArgs wgrad_args(const lsgd_ctx* c, int l, float lr) {
   a.lr = lr;
   a.mom = cf.momentum;
   a.wd = cf.weight_decay;
-  a.nesterov = cf.nesterov;
+  a.nesterov = upd_mode(cf);
   a.bias_w = c->W() + ly.offB[l - 1];
   a.bias_u = c->U() + ly.offB[l - 1];
   a.sBiasP = ly.Ps;
@@ -453,7 +477,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     h.lr = lr;
     h.mom = cf.momentum;
     h.wd = cf.weight_decay;
-    h.nesterov = cf.nesterov;
+    h.nesterov = upd_mode(cf);
     // logits, loss, dZ_L and the masked input gradient of the top layer
     LSGD_LAUNCH(c, "head_fwd", lsgd::launch_head_fwd(dt, h, s));
     // the top layer's weight gradient feeds nothing else in this step: it
@@ -632,7 +656,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   h.lr = lr;
   h.mom = cf.momentum;
   h.wd = cf.weight_decay;
-  h.nesterov = cf.nesterov;
+  h.nesterov = upd_mode(cf);
   LSGD_LAUNCH(c, "head_fwd", lsgd::launch_head_fwd(0, h, s));
   LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(0, h, s));
 
@@ -650,7 +674,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     return lsgd::launch_bn_backward(F(q.y), gup, maskv, K, rows(i), q.Cout, bnpart,
                                     mu + (size_t)i * K * 64, inv + (size_t)i * K * 64,
                                     coef, W + q.offG, W + q.offB, U + q.offG,
-                                    U + q.offB, Ps, lr, cf.momentum, cf.nesterov, dy, s);
+                                    U + q.offB, Ps, lr, cf.momentum, upd_mode(cf), dy, s);
   };
   // weight gradient of conv i from its input x and output gradient dy, then
   // the update (after any input gradient that reads the old weight)
@@ -670,7 +694,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     if (e != hipSuccess) return e;
     return lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo), K,
                                      9 * q.Cin * q.Cout, W + q.offW, U + q.offW, Ps, lr,
-                                     cf.momentum, cf.weight_decay, cf.nesterov, s);
+                                     cf.momentum, cf.weight_decay, upd_mode(cf), s);
   };
   // input gradient of conv i (old weight, channels swapped per tap)
   auto dgrad = [&](int i, const float* dy, float* dx) -> hipError_t {
@@ -720,6 +744,14 @@ lsgd_status do_average(lsgd_ctx* c) {
 // The end-of-round synchronisation: the plain average, or with a global
 // momentum factor its momentum form at step size lr.
 lsgd_status do_synchronise(lsgd_ctx* c, float lr) {
+  if (c->signed_sync()) {
+    LSGD_LAUNCH(c, "sign_sync",
+                lsgd::launch_sign_sync(c->W(), c->Wb(), c->E(), c->Wsync(),
+                                       c->cfg.K, c->lay.P, c->lay.Ps,
+                                       c->ws + c->lay.sign, c->lay.sign_bytes,
+                                       c->stream));
+    return LSGD_OK;
+  }
   if (!c->gm()) return do_average(c);
   LSGD_LAUNCH(c, "average",
               lsgd::launch_average_gm(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
@@ -787,12 +819,15 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
   check(lsgd::launch_fill(c->U(), 0.f, (long long)K * ly.Ps, c->stream), "fill U");
   check(lsgd::launch_broadcast(d_w0, c->W(), c->Wb(), K, ly.P, ly.Ps, -1,
                                c->stream), "broadcast w0");
-  if (c->gm()) {  // w_(0) is the first synchronised model; the buffer is 0
+  if (c->Wsync()) {  // w_(0) is the first synchronised model
     check(lsgd::launch_fill(c->Wsync(), 0.f, ly.Ps, c->stream), "fill w_sync");
-    check(lsgd::launch_fill(c->Ug(), 0.f, ly.Ps, c->stream), "fill u_global");
     check(lsgd::launch_broadcast(d_w0, c->Wsync(), nullptr, 1, ly.P, ly.Ps, -1,
                                  c->stream), "w_sync := w0");
   }
+  if (c->gm())  // the global buffer starts at 0
+    check(lsgd::launch_fill(c->Ug(), 0.f, ly.Ps, c->stream), "fill u_global");
+  if (c->ef())  // and so do the error memories
+    check(lsgd::launch_fill(c->E(), 0.f, (long long)K * ly.Ps, c->stream), "fill e");
   if (c->bf16())
     check(lsgd::launch_to_bf16(d_X, c->Xb(), (long long)cfg->N * cfg->widths[0],
                                c->stream), "dataset to bf16");
@@ -822,7 +857,9 @@ lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss) {
 
 lsgd_status lsgd_average(lsgd_ctx* ctx) {
   LSGD_USABLE(ctx);
-  if (ctx->gm()) return LSGD_E_INVALID;  // needs the step size: lsgd_synchronise
+  // global momentum needs the step size, the sign schemes compress: both
+  // synchronise through lsgd_synchronise
+  if (ctx->gm() || ctx->signed_sync()) return LSGD_E_INVALID;
   return do_average(ctx);
 }
 
@@ -909,9 +946,30 @@ lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
   LSGD_CK(ctx, lsgd::launch_broadcast(d_src, ctx->W(), ctx->Wb(), ctx->cfg.K,
                                       ctx->lay.P, ctx->lay.Ps, replica,
                                       ctx->stream));
-  if (replica == -1 && ctx->gm())  // the written model is the synchronised one
+  if (replica == -1 && ctx->Wsync())  // the written model is the synchronised one
     LSGD_CK(ctx, lsgd::launch_broadcast(d_src, ctx->Wsync(), nullptr, 1,
                                         ctx->lay.P, ctx->lay.Ps, -1, ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_read_error_memory(lsgd_ctx* ctx, int32_t replica, float* d_dst) {
+  LSGD_USABLE(ctx);
+  if (!d_dst || !ctx->ef() || replica < 0 || replica >= ctx->cfg.K)
+    return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipMemcpyAsync(d_dst, ctx->E() + (size_t)replica * ctx->lay.Ps,
+                              ctx->lay.P * sizeof(float), hipMemcpyDeviceToDevice,
+                              ctx->stream));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_write_error_memory(lsgd_ctx* ctx, int32_t replica,
+                                    const float* d_src) {
+  LSGD_USABLE(ctx);
+  if (!d_src || !ctx->ef() || replica < 0 || replica >= ctx->cfg.K)
+    return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipMemcpyAsync(ctx->E() + (size_t)replica * ctx->lay.Ps, d_src,
+                              ctx->lay.P * sizeof(float), hipMemcpyDeviceToDevice,
+                              ctx->stream));
   return LSGD_OK;
 }
 
@@ -1091,10 +1149,29 @@ lsgd_status lsgd_replica_average_global_momentum(float* d_W, int32_t K,
   return e == hipSuccess ? LSGD_OK : LSGD_E_HIP;
 }
 
+lsgd_status lsgd_sign_sync_scratch_bytes(int32_t K, int64_t P, size_t* bytes) {
+  if (!bytes || K < 1 || P < 0 || P % 4) return LSGD_E_INVALID;
+  *bytes = lsgd::sign_sync_scratch_bytes(K, P);
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_replica_sign_sync(float* d_W, int32_t K, int64_t P,
+                                   float* d_wsync, float* d_E, void* d_scratch,
+                                   size_t scratch_bytes, void* stream) {
+  if (!d_W || !d_wsync || !d_scratch || K < 1 || P < 0 || P % 4)
+    return LSGD_E_INVALID;
+  if (scratch_bytes < lsgd::sign_sync_scratch_bytes(K, P)) return LSGD_E_WORKSPACE;
+  hipError_t e = lsgd::launch_sign_sync(d_W, nullptr, d_E, d_wsync, K, P, P,
+                                        d_scratch, scratch_bytes,
+                                        (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : (e == hipErrorInvalidValue ? LSGD_E_INVALID
+                                                                : LSGD_E_HIP);
+}
+
 lsgd_status lsgd_sgd_update(float* d_W, float* d_U, const float* d_G, int64_t n,
                             float lr, float momentum, float weight_decay,
                             int32_t nesterov, void* stream) {
-  if (!d_W || !d_U || !d_G || n < 0 || (nesterov & ~1)) return LSGD_E_INVALID;
+  if (!d_W || !d_U || !d_G || n < 0 || (nesterov & ~3)) return LSGD_E_INVALID;
   hipError_t e = lsgd::launch_sgd_update(d_W, d_U, d_G, n, lr, momentum,
                                          weight_decay, nesterov,
                                          (hipStream_t)stream);

@@ -94,7 +94,7 @@ __device__ __forceinline__ void sgd(float& w, float& u, float grad, float lr,
                                     float mom, float wd, int nesterov) {
   const float g = __builtin_fmaf(wd, w, grad);
   u = __builtin_fmaf(mom, u, g);
-  const float d = nesterov ? __builtin_fmaf(mom, u, g) : u;
+  const float d = step_dir(u, g, mom, nesterov);
   w = __builtin_fmaf(-lr, d, w);
 }
 

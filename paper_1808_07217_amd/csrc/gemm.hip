@@ -74,7 +74,7 @@ __device__ __forceinline__ void sgd_step(float& w, float& u, float grad,
                                          const GemmArgs& a) {
   const float g = __builtin_fmaf(a.wd, w, grad);
   u = __builtin_fmaf(a.mom, u, g);
-  const float d = a.nesterov ? __builtin_fmaf(a.mom, u, g) : u;
+  const float d = step_dir(u, g, a.mom, a.nesterov);
   w = __builtin_fmaf(-a.lr, d, w);
 }
 

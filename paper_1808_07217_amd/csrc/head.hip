@@ -65,7 +65,7 @@ __device__ __forceinline__ void sgd_step(float& w, float& u, float grad,
                                          const HeadArgs& h) {
   const float g = __builtin_fmaf(h.wd, w, grad);
   u = __builtin_fmaf(h.mom, u, g);
-  const float d = h.nesterov ? __builtin_fmaf(h.mom, u, g) : u;
+  const float d = step_dir(u, g, h.mom, h.nesterov);
   w = __builtin_fmaf(-h.lr, d, w);
 }
 

@@ -6,6 +6,18 @@
 
 namespace lsgd {
 
+// Local-step mode, carried in the `nesterov` field of the update arguments:
+// bit 0 Nesterov (d = g + m u) instead of heavy ball (d = u); bit 1 moves
+// by sign(d) (the signSGD local step), sign(0) = 0.
+constexpr int kModeNesterov = 1, kModeSign = 2;
+
+__device__ __forceinline__ float step_dir(float u, float g, float mom, int mode) {
+  float d = (mode & kModeNesterov) ? __builtin_fmaf(mom, u, g) : u;
+  if (mode & kModeSign) d = d > 0.f ? 1.f : (d < 0.f ? -1.f : 0.f);
+  return d;
+}
+
+
 typedef uint16_t bf16_t;  // bfloat16 bit pattern
 
 // fp32 -> bf16, round to nearest even (finite inputs; overflow gives inf).
@@ -170,6 +182,15 @@ hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
 hipError_t launch_average_gm(float* W, bf16_t* Wb, int K, long long n,
                              long long ld, float* ws, float* ug, float mg,
                              float lr, hipStream_t s);
+// Sign-compressed synchronisation (compress.hip): W fp32 [K][Ps] replicas
+// (the first P elements of each row are the model), ws fp32 [Ps] the model
+// of the previous synchronisation (updated), E fp32 [K][Ps] error memories
+// or nullptr (Algorithm 4 / 3), Wb the bf16 copy or nullptr. Ps % 4 == 0,
+// 16-byte aligned buffers; scratch of sign_sync_scratch_bytes(K, Ps).
+size_t sign_sync_scratch_bytes(int K, long long Ps);
+hipError_t launch_sign_sync(float* W, bf16_t* Wb, float* E, float* ws, int K,
+                            long long P, long long Ps, void* scratch,
+                            size_t scratch_bytes, hipStream_t s);
 // The same average within each of `blocks` groups of Kb consecutive rows
 // (mean_out only with blocks == 1).
 hipError_t launch_average_blocks(float* W, bf16_t* Wb, int Kb, int blocks,

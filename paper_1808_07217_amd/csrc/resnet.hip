@@ -687,7 +687,7 @@ __global__ void k_conv_wupdate(const float* part, int G, int n, float* W, float*
     float w = W[o], u = U[o];
     const float gr = __builtin_fmaf(wd, w, grad);
     u = __builtin_fmaf(mom, u, gr);
-    const float d = nesterov ? __builtin_fmaf(mom, u, gr) : u;
+    const float d = step_dir(u, gr, mom, nesterov);
     w = __builtin_fmaf(-lr, d, w);
     W[o] = w;
     U[o] = u;
@@ -802,13 +802,13 @@ __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int 
   float u = ug[o];
   const float dgm = (float)s1;
   u = __builtin_fmaf(mom, u, dgm);
-  float d = nesterov ? __builtin_fmaf(mom, u, dgm) : u;
+  float d = step_dir(u, dgm, mom, nesterov);
   gamma[o] = __builtin_fmaf(-lr, d, gm);
   ug[o] = u;
   u = ub[o];
   const float dbt = (float)s0;
   u = __builtin_fmaf(mom, u, dbt);
-  d = nesterov ? __builtin_fmaf(mom, u, dbt) : u;
+  d = step_dir(u, dbt, mom, nesterov);
   beta[o] = __builtin_fmaf(-lr, d, bt);
   ub[o] = u;
 }
@@ -860,13 +860,13 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
   float u = ug[o];
   const float dgm = (float)s1;
   u = __builtin_fmaf(mom, u, dgm);
-  float d = nesterov ? __builtin_fmaf(mom, u, dgm) : u;
+  float d = step_dir(u, dgm, mom, nesterov);
   gamma[o] = __builtin_fmaf(-lr, d, gm);
   ug[o] = u;
   u = ub[o];
   const float dbt = (float)s0;
   u = __builtin_fmaf(mom, u, dbt);
-  d = nesterov ? __builtin_fmaf(mom, u, dbt) : u;
+  d = step_dir(u, dbt, mom, nesterov);
   beta[o] = __builtin_fmaf(-lr, d, bt);
   ub[o] = u;
 }

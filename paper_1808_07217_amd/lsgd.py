@@ -24,6 +24,7 @@ if not os.path.exists(LIB_PATH):
 MAX_LAYERS = 8
 FP32, BF16 = 0, 1
 MODELS = {"mlp": 0, "resnet20": 1}
+SCHEMES = {"local": 0, "sign": 1, "ef_sign": 2}
 _c = ctypes
 
 
@@ -39,6 +40,7 @@ class Config(_c.Structure):
         ("momentum", _c.c_float),
         ("weight_decay", _c.c_float),
         ("global_momentum", _c.c_float),
+        ("scheme", _c.c_int32),
         ("seed", _c.c_uint64),
         ("N", _c.c_int64),
     ]
@@ -56,6 +58,11 @@ _SIGS = {
     "lsgd_run_round": [_P, _c.c_int32, _c.POINTER(_c.c_float), _P],
     "lsgd_average_blocks": [_P, _c.c_int32],
     "lsgd_synchronise": [_P, _c.c_float],
+    "lsgd_read_error_memory": [_P, _c.c_int32, _P],
+    "lsgd_write_error_memory": [_P, _c.c_int32, _P],
+    "lsgd_sign_sync_scratch_bytes": [_c.c_int32, _c.c_int64, _P],
+    "lsgd_replica_sign_sync": [_P, _c.c_int32, _c.c_int64, _P, _P, _P,
+                               _c.c_size_t, _P],
     "lsgd_read_global_momentum": [_P, _P],
     "lsgd_write_global_momentum": [_P, _P],
     "lsgd_replica_average_global_momentum": [_P, _c.c_int32, _c.c_int64, _P, _P,
@@ -120,7 +127,7 @@ def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
                 dtype: str = "fp32", momentum: float = 0.0,
                 weight_decay: float = 0.0, nesterov: bool = False,
                 seed: int = 0, model: str = "mlp",
-                global_momentum: float = 0.0) -> Config:
+                global_momentum: float = 0.0, scheme: str = "local") -> Config:
     """widths: d_0 .. d_L for the MLP; (3072, classes) for resnet20."""
     if not 2 <= len(widths) <= MAX_LAYERS + 1:
         raise ValueError("widths must list d_0 .. d_L with 1 <= L <= 8")
@@ -135,6 +142,7 @@ def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
     cfg.momentum = float(momentum)
     cfg.weight_decay = float(weight_decay)
     cfg.global_momentum = float(global_momentum)
+    cfg.scheme = SCHEMES[scheme]
     cfg.seed = int(seed) & (2**64 - 1)
     return cfg
 
@@ -233,6 +241,19 @@ class Replicas:
         if src.dtype != torch.float32 or src.numel() != self.P:
             raise ValueError("src must be float32 with P elements")
         _check(_lib.lsgd_write_global_momentum(self._ctx, _ptr(src)), self._ctx)
+
+    def read_error_memory(self, replica: int, out=None) -> torch.Tensor:
+        out = out if out is not None else torch.empty(self.P, device=self.device)
+        _check(_lib.lsgd_read_error_memory(self._ctx, int(replica), _ptr(out)),
+               self._ctx)
+        return out
+
+    def write_error_memory(self, replica: int, src: torch.Tensor):
+        src = src.contiguous()
+        if src.dtype != torch.float32 or src.numel() != self.P:
+            raise ValueError("src must be float32 with P elements")
+        _check(_lib.lsgd_write_error_memory(self._ctx, int(replica), _ptr(src)),
+               self._ctx)
 
     def read_momentum(self, replica: int, out=None) -> torch.Tensor:
         out = out if out is not None else torch.empty(self.P, device=self.device)
@@ -375,12 +396,35 @@ def replica_average_global_momentum(W: torch.Tensor, w_sync: torch.Tensor,
         _stream_handle(torch.cuda.current_stream(W.device))))
 
 
-def sgd_update(W, U, G, lr, momentum, weight_decay, nesterov=False) -> None:
-    """In-place fused momentum-SGD update of float32 tensors W, U with grad G."""
+def replica_sign_sync(W: torch.Tensor, w_sync: torch.Tensor,
+                      E: Optional[torch.Tensor] = None) -> None:
+    """In place: the sign-compressed synchronisation of the rows of W [K][P]
+    (Algorithm 3; Algorithm 4 with the error memories E [K][P]); w_sync [P]
+    is updated. P must be a multiple of 4."""
+    ts = (W, w_sync) if E is None else (W, w_sync, E)
+    for t in ts:
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous float32")
+    if W.dim() != 2 or w_sync.numel() != W.shape[1] or (
+            E is not None and E.shape != W.shape):
+        raise ValueError("W, E must be [K][P] and w_sync [P]")
+    K, P = W.shape
+    nb = _c.c_size_t()
+    _check(_lib.lsgd_sign_sync_scratch_bytes(K, P, _c.byref(nb)))
+    scratch = torch.empty(max(1, nb.value), dtype=torch.uint8, device=W.device)
+    _check(_lib.lsgd_replica_sign_sync(
+        _ptr(W), K, P, _ptr(w_sync), _ptr(E), _ptr(scratch), nb.value,
+        _stream_handle(torch.cuda.current_stream(W.device))))
+
+
+def sgd_update(W, U, G, lr, momentum, weight_decay, nesterov=False,
+               sign_step=False) -> None:
+    """In-place fused momentum-SGD update of float32 tensors W, U with grad G
+    (``sign_step``: move by the sign of the direction, Algorithm 3)."""
     for t in (W, U, G):
         if t.dtype != torch.float32 or not t.is_contiguous():
             raise ValueError("W, U, G must be contiguous float32")
     _check(_lib.lsgd_sgd_update(
         _ptr(W), _ptr(U), _ptr(G), W.numel(), float(lr), float(momentum),
-        float(weight_decay), int(bool(nesterov)),
+        float(weight_decay), int(bool(nesterov)) | (2 if sign_step else 0),
         _stream_handle(torch.cuda.current_stream(W.device))))

@@ -54,6 +54,7 @@ def test_known_parameter_counts():
     dict(momentum=1.0), dict(momentum=-0.1), dict(weight_decay=-1.0),
     dict(widths=(64, 1)), dict(global_momentum=1.0),
     dict(global_momentum=-0.5), dict(global_momentum=float("nan")),
+    dict(scheme=3), dict(scheme=-1), dict(scheme=1, global_momentum=0.5),
 ])
 def test_invalid_configs_are_rejected(bad):
     from paper_1808_07217_amd import lsgd as L
@@ -61,11 +62,13 @@ def test_invalid_configs_are_rejected(bad):
     kw.update(bad)
     opt = {k: kw.pop(k) for k in ("momentum", "weight_decay", "global_momentum")
            if k in kw}
+    scheme = kw.pop("scheme", 0)
     if len(kw["widths"]) < 2:
         with pytest.raises(ValueError):
             L.make_config(**kw, **opt)
         return
     cfg = L.make_config(**kw, **opt)
+    cfg.scheme = scheme
     with pytest.raises(L.LsgdError, match="invalid argument"):
         L.param_count(cfg)
 
@@ -78,6 +81,14 @@ def test_null_context_calls_fail_cleanly():
     assert lib.lsgd_run_hierarchical_round(None, 1, 1, 1, None, None) == 1
     assert lib.lsgd_replica_average_blocks(None, 4, 2, 8, None) == 1
     assert lib.lsgd_synchronise(None, ctypes.c_float(0.1)) == 1
+    assert lib.lsgd_read_error_memory(None, 0, None) == 1
+    assert lib.lsgd_write_error_memory(None, 0, None) == 1
+    assert lib.lsgd_replica_sign_sync(None, 4, 8, None, None, None, 0, None) == 1
+    nb = ctypes.c_size_t()
+    assert lib.lsgd_sign_sync_scratch_bytes(4, 6, ctypes.byref(nb)) == 1  # P % 4
+    assert lib.lsgd_sign_sync_scratch_bytes(4, 8192, ctypes.byref(nb)) == 0
+    # 2 bits per element, one fp64 partial per 8192-element chunk, K scales
+    assert nb.value == 4 * 8192 * 2 // 8 + 256 + 256
     assert lib.lsgd_read_global_momentum(None, None) == 1
     assert lib.lsgd_write_global_momentum(None, None) == 1
     assert lib.lsgd_replica_average_global_momentum(

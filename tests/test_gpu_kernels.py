@@ -182,7 +182,91 @@ def test_replica_average_global_momentum(K, P, mg, lr):
     assert np.all(a(ws_got - ws_ref) <= e_w), np.max(a(ws_got - ws_ref) / e_w)
 
 
+# ------------------------------------------------- sign-compressed sync
+@pytest.mark.parametrize("K,P,ef", [(16, 1841168, False), (16, 1841168, True),
+                                    (4, 8192 + 4, False), (3, 260, True),
+                                    (1, 4, False), (64, 10004, True)])
+def test_replica_sign_sync(K, P, ef):
+    """Sign-compressed synchronisation (Algorithm 3; Algorithm 4 with the
+    memories). Signs are decided in fp32 on the kernel's documented
+    arithmetic ((w_s - w) + e), so the test takes them from the same fp32
+    expression: a wrong or missed sign would move an element by at least
+    p / K, far outside the rounding bound checked here. Against the fp64
+    oracle, elements whose exact difference is within fp32 rounding of zero
+    (possible only with memories) may carry either sign. Exact zeros
+    (replica elements equal to w_s) must give sign 0."""
+    L = _lsgd()
+    print(f"sign sync K={K} P={P} ef={ef}", flush=True)
+    rng = np.random.default_rng(K * 7 + P + ef)
+    ws = rng.standard_normal(P).astype(np.float32)
+    W = (ws[None] + 0.01 * rng.standard_normal((K, P))).astype(np.float32)
+    W = np.where(rng.random((K, P)) < 0.05, ws[None], W).astype(np.float32)
+    E = (0.003 * rng.standard_normal((K, P))).astype(np.float32) if ef else None
+    Wd, wsd = to_dev(W), to_dev(ws)
+    Ed = to_dev(E) if ef else None
+    L.replica_sign_sync(Wd, wsd, Ed)
+    got_w = wsd.cpu().numpy().astype(np.float64)
+    assert np.all(Wd.cpu().numpy() == wsd.cpu().numpy()[None])
+
+    d32 = (ws[None] - W) + E if ef else ws[None] - W          # fp32 decisions
+    p64 = np.abs(d32).astype(np.float64).sum(axis=1) / P
+    msgs = np.sign(d32).astype(np.float64) * p64[:, None]
+    mine = ws.astype(np.float64) - msgs.sum(axis=0) / K
+    bound = 4 * U32 * (np.abs(ws) + np.abs(msgs).sum(axis=0) / K) + 1e-30
+    assert np.max(bound) < 0.5 * p64.min() / K       # one flipped sign shows
+    assert np.all(np.abs(got_w - mine) <= bound), np.max(np.abs(got_w - mine) / bound)
+    if ef:
+        got_E = Ed.cpu().numpy().astype(np.float64)
+        e_mine = d32.astype(np.float64) - msgs
+        assert np.all(np.abs(got_E - e_mine) <= 4 * U32 * (np.abs(d32) + p64[:, None]))
+
+    # the fp64 oracle
+    W64, ws64 = W.astype(np.float64), ws.astype(np.float64)
+    _, w_ref, E_ref = O.average_sign_compressed(W64, ws64, None if E is None
+                                                else E.astype(np.float64))
+    d64 = ws64[None] - W64 + (0 if E is None else E)
+    amb = np.abs(d64) <= 4 * U32 * (np.abs(ws64[None] - W64) +
+                                    (0 if E is None else np.abs(E)))
+    if not ef:
+        assert not amb[np.abs(d64) > 0].any()      # differences of fp32 values
+    allow = bound + 4 * U32 * np.abs(w_ref) + (2 * p64[:, None] * amb).sum(axis=0) / K
+    assert np.all(np.abs(got_w - w_ref) <= allow)
+    assert np.array_equal(np.sign(d32) == 0, d64 == 0) or ef
+
+
 # ------------------------------------------------------------------ update
+@pytest.mark.parametrize("nesterov", [False, True])
+def test_sgd_update_sign_step(nesterov):
+    """The signSGD local step: every element moves by exactly lr * sign(d)
+    (one fp32 rounding of w -+ lr), the buffer as in the plain step; where d
+    is within fp32 rounding of zero either move (or none) is valid."""
+    L = _lsgd()
+    n = 1 << 16
+    rng = np.random.default_rng(77 + nesterov)
+    w, u, g = (rng.standard_normal(n).astype(np.float32) for _ in range(3))
+    g[:64] = -1e-4 * w[:64] - 0.9 * u[:64]       # directions near zero
+    Wd, Ud, Gd = to_dev(w), to_dev(u), to_dev(g)
+    L.sgd_update(Wd, Ud, Gd, 0.01, 0.9, 1e-4, nesterov, sign_step=True)
+    w2, u2 = O.sgd_update(w.astype(float), u.astype(float), g.astype(float),
+                          0.01, 0.9, 1e-4, nesterov, sign_step=True)
+    _, u_plain = O.sgd_update(w.astype(float), u.astype(float), g.astype(float),
+                              0.01, 0.9, 1e-4, nesterov)
+    gw = Wd.cpu().numpy().astype(np.float64)
+    np.testing.assert_allclose(Ud.cpu().numpy(), u_plain, rtol=0,
+                               atol=float(np.max(4 * U32 * (np.abs(u) + np.abs(g) + np.abs(w)))))
+    gg = g + 1e-4 * w
+    uu = 0.9 * u.astype(float) + gg
+    d = gg + 0.9 * uu if nesterov else uu
+    scale = np.abs(gg) + np.abs(uu) * (1.9 if nesterov else 1.0) + np.abs(w)
+    clear = np.abs(d) > 8 * U32 * scale
+    assert clear.sum() > n - 200
+    np.testing.assert_allclose(gw[clear], w2[clear], rtol=0,
+                               atol=float(np.max(U32 * np.abs(w2))) * 2)
+    moved = np.abs(gw[~clear] - w[~clear])
+    assert np.all((moved <= 2 * U32 * np.abs(w[~clear])) |
+                  (np.abs(moved - 0.01) <= 4 * U32 * (np.abs(w[~clear]) + 0.01)))
+
+
 @pytest.mark.parametrize("nesterov", [False, True])
 @pytest.mark.parametrize("n", [1, 3, 4099, 1 << 20])
 def test_sgd_update_matches_oracle(nesterov, n):

@@ -428,6 +428,101 @@ def test_global_momentum_entry_points_and_resume():
                                   c.read_params(-1).cpu().numpy())
 
 
+# ------------------------------------- sign-compressed synchronisation
+def _sign_sync_allowance(st_W, w_sync, E, amb_abs):
+    """Per element, the largest change that sign decisions on near-zero
+    differences can make: 2 p^k / K summed over the workers whose corrected
+    difference there is within ``amb_abs`` of zero (either sign, or none,
+    is a valid decision there)."""
+    K = st_W.shape[0]
+    d = w_sync[None] - st_W + (0 if E is None else E)
+    p = np.abs(d).sum(axis=1) / d.shape[1]
+    amb = np.abs(d) <= amb_abs
+    return (2 * p[:, None] * amb).sum(axis=0) / K, amb
+
+
+@pytest.mark.parametrize("scheme,H,nesterov", [("ef_sign", 3, False),
+                                               ("ef_sign", 1, True),
+                                               ("sign", 1, True),
+                                               ("sign", 1, False)])
+def test_sign_schemes_rounds_match_oracle(scheme, H, nesterov):
+    """Algorithms 3 (sign local steps, H' = 1) and 4 (EF-signSGD) over four
+    rounds: the synchronised model, the error memories (in model space,
+    against max |w|) and every loss."""
+    w = _small((70, 48, 36, 10), K=4, B=12, H=H, rounds=4,
+               nesterov=nesterov).scaled(scheme=scheme)
+    X, y, w0 = _small_data(w, seed=70)
+    print(f"{scheme} H={H} nesterov={nesterov}", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(H, w.K, device=device())
+    for t in range(4):
+        reps.run_round([w.lr] * H, loss)
+        want = O.run_round(st, w, X, y, H, w.lr)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        e = normwise(reps.read_params(0).cpu().numpy(), st.W[0])
+        assert e <= PARAM_TOL_FP32, (t, e)
+        if scheme == "ef_sign":
+            scale = np.max(np.abs(st.W[0]))
+            for k in range(w.K):
+                de = np.max(np.abs(reps.read_error_memory(k).cpu().numpy() - st.E[k]))
+                assert de <= PARAM_TOL_FP32 * scale, (t, k, de / scale)
+
+
+def test_signsgd_round_with_cancelling_steps():
+    """Algorithm 3 with H' = 4: coordinates whose four sign steps cancel have
+    an exactly zero model difference in exact arithmetic, but w - lr + lr
+    leaves a rounding residue (in fp32 on the GPU, in fp64 in the oracle)
+    whose sign is noise on both sides. Elsewhere the synchronised model
+    matches the oracle elementwise; at cancelled coordinates it stays within
+    the change such noise can make."""
+    w = _small((70, 48, 36, 10), K=4, B=12, H=4, rounds=1,
+               nesterov=True).scaled(scheme="sign")
+    X, y, w0 = _small_data(w, seed=71)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(4, w.K, device=device())
+    reps.run_round([w.lr] * 4, loss)
+    want = [O.local_step(st, w, X, y, w.lr) for _ in range(4)]
+    assert np.all(rel(loss.cpu().numpy(), np.stack(want)) <= LOSS_TOL_FP32)
+    allow, amb = _sign_sync_allowance(st.W, st.w_sync, None, 0.5 * w.lr)
+    print(f"cancelled coordinates: {amb.mean():.3%}", flush=True)
+    assert amb.any()
+    O.synchronise(st, w, w.lr)
+    got = reps.read_params(0).cpu().numpy()
+    err = np.abs(got - st.W[0])
+    tol = PARAM_TOL_FP32 * np.max(np.abs(st.W[0]))
+    assert np.all(err <= tol + allow)
+    assert np.max(err[allow == 0]) <= tol
+
+
+def test_sign_scheme_entry_points_and_resume():
+    """Sign schemes synchronise through lsgd_synchronise (lsgd_average is
+    refused); EF-signSGD resumes bit-identically from the synchronised model
+    and the memories (no local momentum, so the buffers carry nothing)."""
+    from paper_1808_07217_amd import lsgd as L
+    w = _small((70, 48, 36, 10), K=4, B=12, H=2, rounds=1,
+               momentum=0.0).scaled(scheme="ef_sign")
+    X, y, w0 = _small_data(w, seed=72)
+    a = make_replicas(w, X, y, w0)
+    with pytest.raises(L.LsgdError):
+        a.average()
+    a.run_round([0.02, 0.02])
+    a.run_round([0.02, 0.02])
+    c = make_replicas(w, X, y, w0)
+    c.write_params(a.read_params(0))
+    for k in range(w.K):
+        c.write_error_memory(k, a.read_error_memory(k))
+    c.step = a.step
+    a.run_round([0.02, 0.02])
+    c.run_round([0.02, 0.02])
+    np.testing.assert_array_equal(a.read_params(-1).cpu().numpy(),
+                                  c.read_params(-1).cpu().numpy())
+    for k in range(w.K):
+        np.testing.assert_array_equal(a.read_error_memory(k).cpu().numpy(),
+                                      c.read_error_memory(k).cpu().numpy())
+
+
 # --------------------------------------------------------- full-size rounds
 @pytest.fixture(scope="module")
 def img_data():
@@ -507,6 +602,74 @@ def test_mlp_512_hybrid_momentum_two_rounds_full_size(img_data):
         e_w, e_u = _sync_error(reps, st, w)
         print(f"round {t + 1}: params {e_w:.3e}, lr * u {e_u:.3e}", flush=True)
         assert e_w <= PARAM_TOL_FP32 and e_u <= PARAM_TOL_FP32, (t, e_w, e_u)
+
+
+def test_mlp_512_ef_signsgd_first_round_full_size(img_data):
+    """Workload 2's shape under Algorithm 4, one round of 16 plain local
+    steps. Before the synchronisation the replicas carry fp32 rounding
+    amplified over 16 steps (held to 5e-5 of max |w| per replica in the
+    plain run); where a worker's difference is that close to zero its sign
+    is not determined, and the synchronised model may differ there by the
+    change such signs can make. Elsewhere it matches the oracle
+    elementwise."""
+    w = wk.get("mlp_512").scaled(scheme="ef_sign")
+    X, y = img_data
+    w0 = wk.initial_weights(w)
+    print("mlp_512 ef_sign round 1", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(w.H, w.K, device=device())
+    reps.run_round([w.lr] * w.H, loss)
+    want = [O.local_step(st, w, X, y, w.lr) for _ in range(w.H)]
+    assert np.all(rel(loss.cpu().numpy(), np.stack(want)) <= LOSS_TOL_FP32)
+    near = 5e-5 * np.max(np.abs(st.W), axis=1, keepdims=True)
+    allow, amb = _sign_sync_allowance(st.W, st.w_sync, None, near)
+    O.synchronise(st, w, w.lr)
+    got = reps.read_params(0).cpu().numpy()
+    err = np.abs(got - st.W[0])
+    tol = PARAM_TOL_FP32 * np.max(np.abs(st.W[0]))
+    print(f"undetermined signs: {amb.mean():.3%}; max error off them "
+          f"{np.max(err[allow == 0]) / np.max(np.abs(st.W[0])):.3e}", flush=True)
+    assert np.all(err <= tol + allow)
+    assert np.max(err[allow == 0]) <= tol
+
+
+def test_mlp_512_signsgd_first_round_full_size(img_data):
+    """Workload 2's shape under Algorithm 3 at H' = 1 (one sign step per
+    worker, then the compressed synchronisation). The first step's
+    direction is the gradient plus decay at w0 on both sides; where it is
+    within 1e-5 of the largest direction entry of its replica, fp32 and fp64
+    may take different signs (the GEMM's rounding is of that order), and the
+    synchronised model may differ there by 2 p / K per such worker.
+    Elsewhere it matches the oracle elementwise. (Over many sign steps such
+    decisions compound, so longer runs are compared on small cases.)"""
+    w = wk.get("mlp_512").scaled(scheme="sign", H=1)
+    X, y = img_data
+    w0 = wk.initial_weights(w)
+    print("mlp_512 sign H'=1 round 1", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    loss = torch.empty(1, w.K, device=device())
+    reps.run_round([w.lr], loss)
+    st = O.State(w0, w.K)
+    want = O.local_step(st, w, X, y, w.lr)
+    assert np.all(rel(loss.cpu().numpy()[0], want) <= LOSS_TOL_FP32)
+    # the oracle's first directions d^k = grad + wd * w0 (u starts at 0)
+    amb = np.zeros((w.K, st.W.shape[1]), bool)
+    for k in range(w.K):
+        idx = O.sample_indices(w.sample_seed, 0, k, w.K, w.N, w.B_loc)
+        _, g = O.model_loss_and_grad(w, w0.astype(np.float64),
+                                     np.asarray(X[idx], np.float64), y[idx])
+        d = g + w.weight_decay * w0
+        amb[k] = np.abs(d) <= 1e-5 * np.max(np.abs(d))
+    p = np.abs(st.w_sync[None] - st.W).sum(axis=1) / st.W.shape[1]
+    allow = (2 * p[:, None] * amb).sum(axis=0) / w.K
+    O.synchronise(st, w, w.lr)
+    got = reps.read_params(0).cpu().numpy()
+    err = np.abs(got - st.W[0])
+    tol = PARAM_TOL_FP32 * np.max(np.abs(st.W[0]))
+    print(f"undetermined directions: {amb.mean():.4%}", flush=True)
+    assert np.all(err <= tol + allow)
+    assert np.max(err[allow == 0]) <= tol
 
 
 def test_wide_bf16_first_round_two_replicas_full_size(img_data):

@@ -125,6 +125,20 @@ WORKLOADS = {
         dtype="fp32", K=16, B_loc=128, H=16, rounds=20, lr=0.001,
         momentum=0.9, nesterov=False, weight_decay=1e-4, global_momentum=0.3,
         **_IMG, data_seed=201, init_seed=202, sample_seed=0x5EED0007),
+    # (post-)local SGD with sign compression on the same MLP, Nesterov and
+    # weight decay on the local steps as the compression appendix used:
+    # Algorithm 3 (sign local steps; a small step size since every
+    # coordinate moves by it) and Algorithm 4 (EF-signSGD)
+    "signsgd_mlp_512": Workload(
+        name="signsgd_mlp_512", model="mlp", widths=(3072, 512, 512, 10),
+        dtype="fp32", K=16, B_loc=128, H=16, rounds=20, lr=0.0001,
+        momentum=0.9, nesterov=True, weight_decay=1e-4, scheme="sign",
+        **_IMG, data_seed=201, init_seed=202, sample_seed=0x5EED0008),
+    "efsign_mlp_512": Workload(
+        name="efsign_mlp_512", model="mlp", widths=(3072, 512, 512, 10),
+        dtype="fp32", K=16, B_loc=128, H=16, rounds=20, lr=0.001,
+        momentum=0.9, nesterov=True, weight_decay=1e-4, scheme="ef_sign",
+        **_IMG, data_seed=201, init_seed=202, sample_seed=0x5EED0009),
     # ResNet-20-shaped CNN, fp32, per-worker BN, heavy-ball momentum
     "resnet20": Workload(
         name="resnet20", model="resnet20", widths=(3072, 10), dtype="fp32",
