@@ -98,6 +98,85 @@ def sample_indices(seed: int, step: int, k: int, K: int, N: int, B: int):
     return lo + ((u * np.uint64(n)) >> np.uint64(32)).astype(np.int64)
 
 
+# Per-epoch global reshuffle (the CIFAR training procedure: the data is
+# partitioned disjointly among the workers and reshuffled globally every
+# epoch; each worker then takes its local mini-batches from its part).
+# The permutation of epoch e is a counter-based pseudo-random permutation:
+# a balanced Feistel network (Luby and Rackoff) on 2m-bit words, 4^m >= N,
+# whose round function is word 0 of Philox4x32-10 at counter
+# (right half, round, e, SHUFFLE_STREAM), restricted to [0, N) by cycle
+# walking (Black and Rogaway): values >= N are permuted again until they
+# fall in range.
+SHUFFLE_STREAM = 0x5348464C
+FEISTEL_ROUNDS = 4
+
+
+def feistel_bits(N: int) -> int:
+    """Half width m: the smallest m >= 1 with 4^m >= N."""
+    m = 1
+    while (1 << (2 * m)) < N:
+        m += 1
+    return m
+
+
+def feistel(x, m: int, seed: int, epoch: int):
+    """The Feistel permutation of [0, 4^m) applied to the array ``x``."""
+    x = np.asarray(x, np.uint64)
+    mask = np.uint64((1 << m) - 1)
+    left, right = x >> np.uint64(m), x & mask
+    for r in range(FEISTEL_ROUNDS):
+        f = philox4x32_10((right, np.full_like(right, r),
+                           np.full_like(right, epoch & 0xFFFFFFFF),
+                           np.full_like(right, SHUFFLE_STREAM)),
+                          (seed & 0xFFFFFFFF, seed >> 32))[0]
+        left, right = right, left ^ (f & mask)
+    return (left << np.uint64(m)) | right
+
+
+def epoch_permutation(positions, N: int, seed: int, epoch: int):
+    """pi_e(q) for the array of positions q in [0, N)."""
+    m = feistel_bits(N)
+    y = feistel(np.asarray(positions, np.uint64), m, seed, epoch)
+    out = y.copy()
+    todo = out >= np.uint64(N)
+    while todo.any():
+        out[todo] = feistel(out[todo], m, seed, epoch)
+        todo = out >= np.uint64(N)
+    return out.astype(np.int64)
+
+
+def steps_per_epoch(K: int, N: int, B: int) -> int:
+    """Whole local mini-batches per epoch: every worker's part holds at least
+    floor(N / K) rows, of which floor(floor(N / K) / B) batches are taken
+    (the rest of a part is left for that epoch; the next reshuffle moves
+    every row to a random place)."""
+    return (N // K) // B
+
+
+def sample_indices_epoch(seed: int, step: int, k: int, K: int, N: int, B: int):
+    """I^k for local step ``step`` under the per-epoch reshuffle: epoch
+    e = step // S, batch j = step % S (S = steps_per_epoch); worker k's part
+    of epoch e is pi_e restricted to its slice [lo_k, hi_k) of positions, and
+    batch j is positions lo_k + jB .. lo_k + jB + B - 1 of it (without
+    replacement within the epoch)."""
+    S = steps_per_epoch(K, N, B)
+    if S < 1:
+        raise ValueError("a worker's part must hold at least one batch")
+    e, j = divmod(step, S)
+    lo, _ = shard(k, K, N)
+    q = lo + j * B + np.arange(B, dtype=np.int64)
+    return epoch_permutation(q, N, seed, e)
+
+
+def worker_indices(wl, step: int, k: int):
+    """The index set of worker k at a local step, by the workload's
+    sampler ("iid": with replacement from a fixed shard; "epoch": the
+    per-epoch reshuffled partition)."""
+    if getattr(wl, "sampler", "iid") == "epoch":
+        return sample_indices_epoch(wl.sample_seed, step, k, wl.K, wl.N, wl.B_loc)
+    return sample_indices(wl.sample_seed, step, k, wl.K, wl.N, wl.B_loc)
+
+
 # --------------------------------------------------------------------------
 # bfloat16 rounding (operand precision of the bf16 workload)
 # --------------------------------------------------------------------------
@@ -348,7 +427,7 @@ def local_step(state, wl, X, y, lr, replicas=None):
     losses = np.full(K, np.nan)
     mask = model_decay_mask(wl)
     for k in ks:
-        idx = sample_indices(wl.sample_seed, state.step, k, K, wl.N, wl.B_loc)
+        idx = worker_indices(wl, state.step, k)
         A0 = np.asarray(X[idx], np.float64)
         loss, grad = model_loss_and_grad(wl, state.W[k], A0, y[idx])
         state.W[k], state.U[k] = sgd_update(
@@ -374,9 +453,14 @@ def model_decay_mask(wl):
 
 def run_round(state, wl, X, y, H, lr):
     """H local steps on every replica, then the synchronisation (the average,
-    or its global-momentum form); returns [H][K] losses."""
-    losses = np.stack([local_step(state, wl, X, y, lr) for _ in range(H)])
-    synchronise(state, wl, lr)
+    or its global-momentum form); returns [H][K] losses. ``lr`` is one step
+    size for the round or a list of H, one per local step (the
+    synchronisation uses the last)."""
+    lrs = list(lr) if np.ndim(lr) else [lr] * H
+    if len(lrs) != H:
+        raise ValueError("one step size per local step")
+    losses = np.stack([local_step(state, wl, X, y, a) for a in lrs])
+    synchronise(state, wl, lrs[-1] if lrs else lr)
     return losses
 
 
@@ -406,6 +490,73 @@ def schedule(wl):
     return out
 
 
+# --------------------------------------------------------------------------
+# Schedules of the training procedure (host side): the large-batch learning
+# rate schemes (linear scaling and gradual warm-up), the step decay at 50%
+# and 75% of the sample budget, and the local-step warm-up strategies.
+# --------------------------------------------------------------------------
+def goyal_lr(step: int, lr: float, scale: float, warmup_steps: int) -> float:
+    """Step size of local step ``step`` (0-based) under the large-batch
+    schemes: the target lr * scale (the linear scaling rule), reached from lr
+    by a constant increment per iteration, (target - lr) / warmup_steps. With
+    warmup_steps = 5 N / (K B) (five epochs) this is the appendix's
+    increment. warmup_steps = 0: the target from the start."""
+    target = lr * scale
+    if warmup_steps <= 0 or step >= warmup_steps:
+        return target
+    return lr + step * (target - lr) / warmup_steps
+
+
+def decay_factor(step: int, samples_per_step: int, total_samples: int,
+                 milestones=(0.5, 0.75), factor: float = 0.1) -> float:
+    """The step decay of the CIFAR procedure: the step size is divided by 10
+    once the run has accessed 50% of its sample budget and again at 75%;
+    ``step`` local steps (of samples_per_step samples over all workers) have
+    been taken before the step in question."""
+    f = 1.0
+    for m in milestones:
+        if step * samples_per_step >= m * total_samples:
+            f *= factor
+    return f
+
+
+def local_steps_of_epoch(epoch: int, H: int, kind, warmup_epochs: int) -> int:
+    """Local-step warm-up (the appendix on it and the ImageNet runs): during
+    the first ``warmup_epochs`` epochs H grows from 1 -- "linear": by equal
+    increments, 1 + floor((H - 1) e / W); "exponential": doubling, min(H, 2^e)
+    (H = 8 over three epochs gives 1, 2, 4, as in the ImageNet runs);
+    "constant": 1 throughout -- and is H afterwards."""
+    if kind is None or epoch >= warmup_epochs:
+        return H
+    if kind == "linear":
+        return 1 + ((H - 1) * epoch) // warmup_epochs
+    if kind == "exponential":
+        return min(H, 2 ** epoch)
+    if kind == "constant":
+        return 1
+    raise ValueError(kind)
+
+
+def schedule_rounds(total_steps: int, steps_per_ep: int, H: int, lr_of_step,
+                    h_kind=None, h_warmup_epochs: int = 0,
+                    switch_step=None):
+    """The rounds of a run as [(H_t, [step size of each of its steps])]: a
+    round's H_t is that of the epoch in which it starts (local-step warm-up),
+    or -- post-local SGD -- 1 before ``switch_step`` and H from it on; the
+    last round is cut so that the run takes exactly ``total_steps`` local
+    steps (every method accesses the same number of samples)."""
+    rounds, s = [], 0
+    while s < total_steps:
+        if switch_step is not None:
+            Ht = 1 if s < switch_step else H
+        else:
+            Ht = local_steps_of_epoch(s // steps_per_ep, H, h_kind, h_warmup_epochs)
+        Ht = min(Ht, total_steps - s)
+        rounds.append((Ht, [lr_of_step(s + h) for h in range(Ht)]))
+        s += Ht
+    return rounds
+
+
 def run(wl, X, y, w0, rounds=None):
     """Whole (post-)local SGD run (Algorithm 2; Algorithm 1 when t' = 0).
 
@@ -429,7 +580,7 @@ def minibatch_sgd(wl, X, y, w0, steps, lr):
     mask = model_decay_mask(wl)
     for s in range(steps):
         idx = np.concatenate([
-            sample_indices(wl.sample_seed, s, k, wl.K, wl.N, wl.B_loc)
+            worker_indices(wl, s, k)
             for k in range(wl.K)])
         _, grad = model_loss_and_grad(wl, w, np.asarray(X[idx], np.float64), y[idx])
         g = grad + wl.weight_decay * mask * w

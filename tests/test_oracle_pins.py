@@ -278,6 +278,18 @@ def test_h1_local_sgd_is_minibatch_sgd(nesterov, momentum):
     np.testing.assert_allclose(st.W[0], ref, rtol=1e-12, atol=1e-13)
 
 
+def test_h1_local_sgd_is_minibatch_sgd_with_the_epoch_sampler():
+    """The same identity with the per-epoch reshuffled partition, across an
+    epoch boundary (the union batch is drawn without replacement)."""
+    wl = _small(False, 0.9, K=4, H=1, B=8, rounds=40).scaled(sampler="epoch", N=400)
+    X, y = wk.dataset(wl)
+    assert O.steps_per_epoch(wl.K, wl.N, wl.B_loc) < 40
+    w0 = np.random.default_rng(5).standard_normal(wk.param_count(wl.widths)) * 0.1
+    st, _ = O.run(wl, X, y, w0)
+    ref = O.minibatch_sgd(wl, X, y, w0, steps=40, lr=wl.lr)
+    np.testing.assert_allclose(st.W[0], ref, rtol=1e-11, atol=1e-12)
+
+
 def test_single_worker_is_sequential_sgd():
     wl = _small(False, 0.9, K=1, H=4, rounds=3)
     X, y = wk.dataset(wl)
@@ -601,6 +613,140 @@ def test_alg3_local_steps_move_by_signs():
     st = O.State(w0, wl.K)
     O.local_step(st, wl, X, y, wl.lr)
     np.testing.assert_allclose(np.abs(st.W - w0[None]), wl.lr, rtol=1e-9)
+
+
+# ------------------------------------------- per-epoch reshuffle sampler
+def _feistel_inverse(y, m, seed, epoch):
+    """Undo the Feistel rounds (the network run backwards): a separate
+    derivation, so the forward map is checked to be the permutation its
+    definition says."""
+    y = np.asarray(y, np.uint64)
+    mask = np.uint64((1 << m) - 1)
+    left, right = y >> np.uint64(m), y & mask
+    for r in reversed(range(O.FEISTEL_ROUNDS)):
+        f = O.philox4x32_10((left, np.full_like(left, r),
+                             np.full_like(left, epoch & 0xFFFFFFFF),
+                             np.full_like(left, O.SHUFFLE_STREAM)),
+                            (seed & 0xFFFFFFFF, seed >> 32))[0]
+        left, right = right ^ (f & mask), left
+    return (left << np.uint64(m)) | right
+
+
+@pytest.mark.parametrize("m", [1, 2, 3, 5, 8])
+def test_feistel_is_a_permutation_with_its_inverse(m):
+    for seed, epoch in ((0, 0), (2**64 - 1, 7), (12345, 2**31 + 5)):
+        x = np.arange(1 << (2 * m), dtype=np.uint64)
+        y = O.feistel(x, m, seed, epoch)
+        assert np.array_equal(np.sort(y), x)
+        assert np.array_equal(_feistel_inverse(y, m, seed, epoch), x)
+        if m >= 3:
+            assert not np.array_equal(y, x)
+
+
+@pytest.mark.parametrize("N", [1, 2, 3, 5, 17, 1000, 4097, 50000])
+def test_epoch_permutation_is_a_bijection_of_the_rows(N):
+    for epoch in (0, 1, 99):
+        pi = O.epoch_permutation(np.arange(N), N, 0x5EED, epoch)
+        assert np.array_equal(np.sort(pi), np.arange(N))
+    if N >= 17:
+        a = O.epoch_permutation(np.arange(N), N, 0x5EED, 0)
+        assert not np.array_equal(a, O.epoch_permutation(np.arange(N), N, 0x5EED, 1))
+        assert not np.array_equal(a, O.epoch_permutation(np.arange(N), N, 0x5EEE, 0))
+
+
+def test_epoch_sampler_partitions_each_epoch_disjointly():
+    """Within an epoch no row is drawn twice across workers and steps, every
+    worker's batches come from its part of that epoch's permutation, and the
+    next epoch reshuffles (the parts change)."""
+    K, N, B, seed = 4, 1000, 32, 99
+    S = O.steps_per_epoch(K, N, B)
+    assert S == 7
+    for e in (0, 1):
+        drawn = np.concatenate([O.sample_indices_epoch(seed, e * S + j, k, K, N, B)
+                                for k in range(K) for j in range(S)])
+        assert drawn.size == K * S * B == np.unique(drawn).size
+        assert drawn.min() >= 0 and drawn.max() < N
+        pi = O.epoch_permutation(np.arange(N), N, seed, e)
+        for k in range(K):
+            lo, hi = O.shard(k, K, N)
+            mine = np.concatenate([O.sample_indices_epoch(seed, e * S + j, k, K, N, B)
+                                   for j in range(S)])
+            assert set(mine) <= set(pi[lo:hi])
+    part0 = set(O.sample_indices_epoch(seed, 0, 0, K, N, B))
+    part1 = set(O.sample_indices_epoch(seed, S, 0, K, N, B))
+    assert part0 != part1
+    with pytest.raises(ValueError):
+        O.sample_indices_epoch(seed, 0, 0, 8, 100, 32)
+
+
+def test_epoch_permutation_places_a_row_uniformly():
+    """Over many epochs, row 0 lands in each of the N positions about
+    equally often (chi-square)."""
+    from scipy.stats import chisquare
+    N, E = 10, 5000
+    pos = np.array([int(np.argmax(O.epoch_permutation(np.arange(N), N, 7, e) == 0))
+                    for e in range(E)])
+    counts = np.bincount(pos, minlength=N)
+    assert chisquare(counts).pvalue > 1e-4
+
+
+# ------------------------------------------------------------- schedules
+def test_goyal_warmup_matches_the_appendix_increment():
+    """Five epochs of N / (K n) iterations from lr to k * lr with the
+    appendix's per-iteration increment (k_hat lr - lr) / (5 N / (K n))."""
+    K, n, S = 16, 128, 24
+    N = S * K * n
+    lr, scale = 0.1, K * n / 128
+    warm = 5 * N // (K * n)
+    inc = (scale * lr - lr) / (5 * N / (K * n))
+    for s in (0, 1, 7, warm - 1):
+        assert O.goyal_lr(s, lr, scale, warm) == pytest.approx(lr + s * inc, rel=1e-15)
+    assert O.goyal_lr(warm, lr, scale, warm) == scale * lr
+    assert O.goyal_lr(10 * warm, lr, scale, warm) == scale * lr
+    assert O.goyal_lr(0, lr, scale, 0) == scale * lr
+
+
+def test_step_decay_at_half_and_three_quarters_of_the_samples():
+    spp, T = 2048, 2048 * 100
+    f = [O.decay_factor(s, spp, T) for s in range(100)]
+    assert f[:50] == [1.0] * 50
+    assert all(v == pytest.approx(0.1) for v in f[50:75])
+    assert all(v == pytest.approx(0.01) for v in f[75:])
+
+
+def test_local_step_warmup_kinds():
+    """The ImageNet example (fixture) for the exponential warm-up; linear
+    and constant warm-up by their definitions' end points and monotonicity."""
+    path = os.path.join(os.path.dirname(__file__), "golden", "local_step_warmup_imagenet.txt")
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        head, tail = line.split(":")
+        kind, H, W = head.split()
+        want = [int(v) for v in tail.split()]
+        got = [O.local_steps_of_epoch(e, int(H), kind, int(W)) for e in range(len(want))]
+        assert got == want
+    lin = [O.local_steps_of_epoch(e, 16, "linear", 4) for e in range(6)]
+    assert lin == [1, 4, 8, 12, 16, 16]
+    assert [O.local_steps_of_epoch(e, 16, "constant", 3) for e in range(5)] == [1, 1, 1, 16, 16]
+    assert [O.local_steps_of_epoch(e, 16, None, 3) for e in range(3)] == [16] * 3
+
+
+@pytest.mark.parametrize("kind", [None, "linear", "exponential", "constant"])
+def test_schedule_rounds_keep_the_sample_budget(kind):
+    S, total, H = 24, 24 * 10 + 5, 16
+    rounds = O.schedule_rounds(total, S, H, lambda s: 0.1 * (s + 1), h_kind=kind,
+                               h_warmup_epochs=3)
+    assert sum(h for h, _ in rounds) == total
+    s = 0
+    for h, lrs in rounds:
+        want = O.local_steps_of_epoch(s // S, H, kind, 3)
+        assert h == want or (h < want and s + h == total)
+        assert lrs == [0.1 * (s + i + 1) for i in range(h)]
+        s += h
+    pl = O.schedule_rounds(total, S, H, lambda s: 1.0, switch_step=100)
+    assert [h for h, _ in pl[:100]] == [1] * 100 and pl[100][0] == H
+    assert sum(h for h, _ in pl) == total
 
 
 def test_loss_decreases_on_every_workload_first_rounds():

@@ -71,6 +71,7 @@ class Workload:
     Hb: int = 1                # block rounds per global average, H^b
     global_momentum: float = 0.0   # m_g at the global average (0: plain mean)
     scheme: str = "local"      # "local"; "sign" (Algorithm 3); "ef_sign" (4)
+    sampler: str = "iid"       # "iid" (fixed shards); "epoch" (reshuffled)
 
     @property
     def n_layers(self) -> int:
