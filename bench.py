@@ -298,7 +298,8 @@ def main():
     cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype,
                         momentum=w.momentum, weight_decay=w.weight_decay,
                         nesterov=w.nesterov, seed=w.sample_seed, model=w.model,
-                        global_momentum=w.global_momentum, scheme=w.scheme)
+                        global_momentum=w.global_momentum, scheme=w.scheme,
+                        sampler=w.sampler)
     Xd = torch.from_numpy(np.array(X)).to(dev)
     yd = torch.from_numpy(np.array(y)).to(dev)
     reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))
@@ -397,6 +398,7 @@ def main():
                    "momentum": w.momentum, "nesterov": w.nesterov,
                    "weight_decay": w.weight_decay,
                    **({"scheme": w.scheme} if w.scheme != "local" else {}),
+                   **({"sampler": w.sampler} if w.sampler != "iid" else {}),
                    **({"global_momentum": w.global_momentum}
                       if w.global_momentum else {})},
     }

@@ -80,6 +80,25 @@ enum { LSGD_FP32 = 0, LSGD_BF16 = 1 };
  *                     init, per worker, never averaged).
  * w_s is the model of the previous synchronisation (w0 at init). */
 enum { LSGD_SCHEME_LOCAL = 0, LSGD_SCHEME_SIGN = 1, LSGD_SCHEME_EF_SIGN = 2 };
+/* Index sampler. With n_k = floor((k+1)N/K) - floor(kN/K) rows in worker
+ * k's slice [floor(kN/K), floor((k+1)N/K)):
+ * LSGD_SAMPLER_IID    every local step draws B_loc rows i.i.d. with
+ *                     replacement from the worker's fixed slice (eq. 1's
+ *                     sampling from the local data): Philox4x32-10, key
+ *                     (seed lo, seed hi), counter (j / 4, s lo, k, s hi),
+ *                     slot j takes word j mod 4, u -> lo + floor(u n_k / 2^32);
+ * LSGD_SAMPLER_EPOCH  the data is repartitioned by a fresh global permutation
+ *                     every epoch (the CIFAR training procedure): with
+ *                     S = floor(floor(N / K) / B_loc) batches per epoch
+ *                     (must be >= 1), step s is batch j = s mod S of epoch
+ *                     e = s / S and takes rows pi_e(lo_k + j B_loc + b),
+ *                     b < B_loc. pi_e is a 4-round balanced Feistel network on
+ *                     2m-bit words (m the smallest >= 1 with 4^m >= N; left
+ *                     half the high m bits; round r maps (L, R) to
+ *                     (R, L xor (F_r(R) & (2^m - 1)))), F_r(R) word 0 of
+ *                     Philox4x32-10 at counter (R, r, e, 0x5348464C) with the
+ *                     same key, restricted to [0, N) by cycle walking. */
+enum { LSGD_SAMPLER_IID = 0, LSGD_SAMPLER_EPOCH = 1 };
 #define LSGD_MAX_LAYERS 8
 
 /*
@@ -102,6 +121,7 @@ typedef struct lsgd_config {
                                              synchronisation; 0: plain mean */
   int32_t scheme;                         /* LSGD_SCHEME_*; a sign scheme
                                              needs global_momentum == 0 */
+  int32_t sampler;                        /* LSGD_SAMPLER_* */
   uint64_t seed;                          /* Philox4x32-10 key for sampling */
   int64_t N;                              /* dataset rows, >= K */
 } lsgd_config;
@@ -225,11 +245,8 @@ lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
 lsgd_status lsgd_get_step(lsgd_ctx* ctx, int64_t* step);
 lsgd_status lsgd_set_step(lsgd_ctx* ctx, int64_t step);
 
-/* The indices the sampler draws at local step `step`: int32 [K][B_loc],
- * i.i.d. uniform over worker k's shard [floor(kN/K), floor((k+1)N/K)),
- * Philox4x32-10 with key (seed low, seed high) and counter
- * (j / 4, step low, k, step high), word j mod 4, mapped by
- * lo + floor(u * n / 2^32). */
+/* The indices the configured sampler (LSGD_SAMPLER_*) draws at local step
+ * `step`: int32 [K][B_loc] into d_idx. */
 lsgd_status lsgd_sample_indices(lsgd_ctx* ctx, int64_t step, int32_t* d_idx);
 
 /* Synchronise the context's stream; returns the latched status. */

@@ -83,6 +83,8 @@ bool valid_config(const lsgd_config* c) {
       c->global_momentum >= 1.f)
     return false;
   if (c->scheme < LSGD_SCHEME_LOCAL || c->scheme > LSGD_SCHEME_EF_SIGN) return false;
+  if (c->sampler != LSGD_SAMPLER_IID && c->sampler != LSGD_SAMPLER_EPOCH) return false;
+  if (c->sampler == LSGD_SAMPLER_EPOCH && (c->N / c->K) / c->B_loc < 1) return false;
   if (c->scheme != LSGD_SCHEME_LOCAL && c->global_momentum != 0.f) return false;
   if (c->N < c->K || c->N > (int64_t)INT32_MAX) return false;
   return true;
@@ -350,6 +352,14 @@ namespace {
 
 lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss);
 
+// The index sets of local step `step` by the configured sampler.
+hipError_t sample(const lsgd_ctx* c, int64_t step, int32_t* idx, hipStream_t s) {
+  const lsgd_config& cf = c->cfg;
+  if (cf.sampler == LSGD_SAMPLER_EPOCH)
+    return lsgd::launch_sample_epoch(cf.seed, step, cf.K, cf.N, cf.B_loc, idx, s);
+  return lsgd::launch_sample(cf.seed, step, cf.K, cf.N, cf.B_loc, idx, s);
+}
+
 // Tiles (128 x 128) from which one persistent launch over all hidden layers
 // updates beats per-layer launches (about four per compute unit).
 constexpr int kMergedMinTiles = 1024;
@@ -409,7 +419,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   bf16_t* Wb = c->Wb();
   const void* X0 = dt ? (const void*)c->Xb() : (const void*)c->X;
 
-  LSGD_LAUNCH(c, "sample", lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
+  LSGD_LAUNCH(c, "sample", sample(c, c->step, c->idx(), s));
 
   // forward: Z_l = A_{l-1} W_l + b_l, A_l = relu(Z_l) below the top layer
   const int Lg = ly.head ? L - 1 : L;  // layers through the generic GEMMs
@@ -589,7 +599,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   };
   auto rows = [&](int i) { return B * r.cv[i].Ho * r.cv[i].Wo; };
 
-  LSGD_LAUNCH(c, "sample", lsgd::launch_sample(cf.seed, c->step, K, cf.N, B, c->idx(), s));
+  LSGD_LAUNCH(c, "sample", sample(c, c->step, c->idx(), s));
 
   // forward: stem, then blocks (a: conv-BN-ReLU, b: conv-BN + shortcut, ReLU)
   for (int i = 0; i < kResConvs; ++i) {
@@ -1005,8 +1015,7 @@ lsgd_status lsgd_set_step(lsgd_ctx* ctx, int64_t step) {
 lsgd_status lsgd_sample_indices(lsgd_ctx* ctx, int64_t step, int32_t* d_idx) {
   LSGD_USABLE(ctx);
   if (!d_idx || step < 0) return LSGD_E_INVALID;
-  LSGD_CK(ctx, lsgd::launch_sample(ctx->cfg.seed, step, ctx->cfg.K, ctx->cfg.N,
-                                   ctx->cfg.B_loc, d_idx, ctx->stream));
+  LSGD_CK(ctx, sample(ctx, step, d_idx, ctx->stream));
   return LSGD_OK;
 }
 

@@ -44,6 +44,48 @@ __global__ void k_sample(uint32_t key0, uint32_t key1, uint32_t s_lo,
   }
 }
 
+// Per-epoch reshuffled partition. Epoch e's permutation of [0, N) is a
+// balanced Feistel network on 2m-bit words (4^m >= N) whose four round
+// functions are word 0 of Philox4x32-10 at counter (right half, round, e,
+// kShuffleStream), restricted to [0, N) by cycle walking: an image >= N is
+// permuted again. The walk ends on the first in-range value of the cycle
+// through the start, after about 4^m / N steps on average; a cap far above
+// any plausible walk returns the position itself (still a valid row), so
+// the kernel always finishes and a parity test would show the failure.
+constexpr uint32_t kShuffleStream = 0x5348464Cu;
+constexpr int kCycleWalkCap = 1 << 12;
+
+__device__ __forceinline__ uint32_t feistel4(uint32_t x, int m, uint32_t mask,
+                                             uint32_t k0, uint32_t k1,
+                                             uint32_t e) {
+  uint32_t left = x >> m, right = x & mask;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint4 f = philox4x32_10(make_uint4(right, (uint32_t)r, e, kShuffleStream), k0, k1);
+    const uint32_t t = left ^ (f.x & mask);
+    left = right;
+    right = t;
+  }
+  return (left << m) | right;
+}
+
+// One thread per (worker k = blockIdx.y, slot b): row pi_e(lo_k + jB + b).
+__global__ void k_sample_epoch(uint32_t key0, uint32_t key1, uint32_t e, long long j,
+                               int K, long long N, int B, int m, int32_t* idx) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  const int k = blockIdx.y;
+  if (b >= B) return;
+  const uint32_t mask = (1u << m) - 1u;
+  const uint32_t q = (uint32_t)((long long)k * N / K + j * B + b);
+  uint32_t y = feistel4(q, m, mask, key0, key1, e);
+  int walk = 0;
+  while (y >= (uint64_t)N && walk < kCycleWalkCap) {
+    y = feistel4(y, m, mask, key0, key1, e);
+    ++walk;
+  }
+  idx[(long long)k * B + b] = (int32_t)(y < (uint64_t)N ? y : q);
+}
+
 // ------------------------------------------------------------------ loss
 // Softmax cross-entropy over C classes for the B rows of replica k
 // (blockIdx.x): dZ = (softmax(z) - onehot(y)) / B and the mean loss, summed
@@ -334,6 +376,20 @@ hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N, int B,
   hipLaunchKernelGGL(k_sample, grid, dim3(64), 0, s, (uint32_t)seed,
                      (uint32_t)(seed >> 32), (uint32_t)step,
                      (uint32_t)((uint64_t)step >> 32), K, (long long)N, B, idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_epoch(uint64_t seed, int64_t step, int K, int64_t N,
+                               int B, int32_t* idx, hipStream_t s) {
+  const long long S = (N / K) / B;  // batches per worker and epoch
+  if (S < 1 || N > 0x7fffffffLL) return hipErrorInvalidValue;
+  int m = 1;
+  while ((1LL << (2 * m)) < N) ++m;
+  const long long e = step / S, j = step % S;
+  dim3 grid((B + 63) / 64, K);
+  hipLaunchKernelGGL(k_sample_epoch, grid, dim3(64), 0, s, (uint32_t)seed,
+                     (uint32_t)(seed >> 32), (uint32_t)e, j, K, (long long)N, B,
+                     m, idx);
   return hipGetLastError();
 }
 

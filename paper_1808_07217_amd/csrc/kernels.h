@@ -165,6 +165,10 @@ hipError_t launch_gap(const float* h, int rows, int S, int C, float* feat, bool 
                       const float* dfeat, float* dh, hipStream_t st);
 
 // ---------------------------------------------------------------- others
+// The per-epoch reshuffled partition sampler (epoch = step / S, batch
+// step % S with S = floor(floor(N / K) / B) >= 1, else hipErrorInvalidValue).
+hipError_t launch_sample_epoch(uint64_t seed, int64_t step, int K, int64_t N,
+                               int B, int32_t* idx, hipStream_t s);
 hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N,
                          int B, int32_t* idx, hipStream_t s);
 hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,

@@ -25,6 +25,7 @@ MAX_LAYERS = 8
 FP32, BF16 = 0, 1
 MODELS = {"mlp": 0, "resnet20": 1}
 SCHEMES = {"local": 0, "sign": 1, "ef_sign": 2}
+SAMPLERS = {"iid": 0, "epoch": 1}
 _c = ctypes
 
 
@@ -41,6 +42,7 @@ class Config(_c.Structure):
         ("weight_decay", _c.c_float),
         ("global_momentum", _c.c_float),
         ("scheme", _c.c_int32),
+        ("sampler", _c.c_int32),
         ("seed", _c.c_uint64),
         ("N", _c.c_int64),
     ]
@@ -127,7 +129,8 @@ def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
                 dtype: str = "fp32", momentum: float = 0.0,
                 weight_decay: float = 0.0, nesterov: bool = False,
                 seed: int = 0, model: str = "mlp",
-                global_momentum: float = 0.0, scheme: str = "local") -> Config:
+                global_momentum: float = 0.0, scheme: str = "local",
+                sampler: str = "iid") -> Config:
     """widths: d_0 .. d_L for the MLP; (3072, classes) for resnet20."""
     if not 2 <= len(widths) <= MAX_LAYERS + 1:
         raise ValueError("widths must list d_0 .. d_L with 1 <= L <= 8")
@@ -143,6 +146,7 @@ def make_config(widths: Sequence[int], K: int, B_loc: int, N: int, *,
     cfg.weight_decay = float(weight_decay)
     cfg.global_momentum = float(global_momentum)
     cfg.scheme = SCHEMES[scheme]
+    cfg.sampler = SAMPLERS[sampler]
     cfg.seed = int(seed) & (2**64 - 1)
     return cfg
 

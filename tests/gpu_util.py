@@ -47,7 +47,8 @@ def make_replicas(w, X=None, y=None, w0=None):
     cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype,
                         momentum=w.momentum, weight_decay=w.weight_decay,
                         nesterov=w.nesterov, seed=w.sample_seed, model=w.model,
-                        global_momentum=w.global_momentum, scheme=w.scheme)
+                        global_momentum=w.global_momentum, scheme=w.scheme,
+                        sampler=w.sampler)
     Xd = to_dev(np.asarray(X, np.float32))
     yd = to_dev(np.asarray(y, np.int32))
     wd = to_dev(np.asarray(w0, np.float32))

@@ -38,6 +38,33 @@ def test_sampler_bit_exact(K, N, B, seed):
         np.testing.assert_array_equal(got, want)
 
 
+@pytest.mark.parametrize("K,N,B,seed", [
+    (4, 4096, 32, 0x5EED0001), (16, 50000, 128, 0x5EED0002),
+    (64, 50000, 64, 0x5EED0004), (3, 10, 3, 1), (1, 7, 7, 2**64 - 1),
+    (5, 1000, 4, 77), (2, 2**31 - 1, 13, 12345),
+])
+def test_epoch_sampler_bit_exact(K, N, B, seed):
+    """The per-epoch reshuffled partition: every index of every worker at
+    steps on both sides of epoch boundaries, against the oracle's Feistel
+    permutation; within an epoch no row repeats."""
+    L = _lsgd()
+    print(f"epoch sampler K={K} N={N} B={B}", flush=True)
+    cfg = L.make_config((1, 2), K, B, N, seed=seed, sampler="epoch")
+    X = torch.empty((N, 1), device=device())
+    y = torch.empty(N, dtype=torch.int32, device=device())
+    w0 = torch.zeros(L.param_count(cfg), device=device())
+    reps = L.Replicas(cfg, X, y, w0)
+    S = O.steps_per_epoch(K, N, B)
+    for step in sorted({0, 1, S - 1, S, S + 1, 5 * S + 2, 123456, 2**32 + 11}):
+        got = reps.sample_indices(step).cpu().numpy()
+        want = np.stack([O.sample_indices_epoch(seed, step, k, K, N, B) for k in range(K)])
+        np.testing.assert_array_equal(got, want)
+    if S <= 64:
+        epoch = np.concatenate([reps.sample_indices(j).cpu().numpy().ravel()
+                                for j in range(S)])
+        assert np.unique(epoch).size == epoch.size
+
+
 # ------------------------------------------------------------------ GEMM
 GEMM_SHAPES = [(3, 70, 45, 37), (2, 64, 64, 16), (1, 1, 1, 1), (2, 33, 10, 130),
                (4, 128, 512, 512), (2, 128, 10, 512), (2, 512, 10, 128),

@@ -523,6 +523,47 @@ def test_sign_scheme_entry_points_and_resume():
                                       c.read_error_memory(k).cpu().numpy())
 
 
+# ------------------------------------------------ training-procedure schedules
+@pytest.mark.parametrize("post_local,kind", [(False, "exponential"), (True, None)])
+def test_cifar_plan_with_the_epoch_sampler_matches_oracle(post_local, kind):
+    """The CIFAR procedure on a small MLP: the per-epoch reshuffled
+    partition, linear scaling with a gradual warm-up, the 50% / 75% decay,
+    and rounds from post-local SGD's switch or an exponential local-step
+    warm-up (rounds of 1, 2, 4, then 8 steps). Step sizes vary inside
+    rounds. Every round's synchronised model and every loss against the
+    oracle driven by its own schedule functions."""
+    from paper_1808_07217_amd import schedules as S
+    w = _small((70, 48, 36, 10), K=4, B=8, N=400, H=8, rounds=1,
+               lr=0.01).scaled(sampler="epoch")
+    X, y, w0 = _small_data(w, seed=80)
+    K, B, N, epochs = w.K, w.B_loc, w.N, 6
+    plan = S.cifar_plan(K=K, B=B, N=N, epochs=epochs, base_lr=w.lr, H=8, ref_batch=16,
+                        lr_warmup_epochs=1, post_local=post_local, warmup=kind,
+                        warmup_epochs=3)
+    spe = O.steps_per_epoch(K, N, B)
+    total = epochs * spe
+
+    def f(s):
+        return (O.goyal_lr(s, w.lr, K * B / 16, spe) *
+                O.decay_factor(s, K * B, total * K * B))
+    switch = (next(s for s in range(total) if O.decay_factor(s, K * B, total * K * B) < 1)
+              if post_local else None)
+    oracle_plan = O.schedule_rounds(total, spe, 8, f, h_kind=kind, h_warmup_epochs=3,
+                                    switch_step=switch)
+    assert [h for h, _ in plan] == [h for h, _ in oracle_plan]
+    print(f"plan: {len(plan)} rounds, H {sorted(set(h for h, _ in plan))}", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    for t, ((h, lrs), (_, lrs_o)) in enumerate(zip(plan, oracle_plan)):
+        loss = torch.empty(h, w.K, device=device())
+        reps.run_round(lrs, loss)
+        want = O.run_round(st, w, X, y, h, lrs_o)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        e = normwise(reps.read_params(0).cpu().numpy(), st.W[0])
+        assert e <= PARAM_TOL_FP32, (t, e)
+    assert reps.step == total
+
+
 # --------------------------------------------------------- full-size rounds
 @pytest.fixture(scope="module")
 def img_data():

@@ -140,6 +140,13 @@ WORKLOADS = {
         dtype="fp32", K=16, B_loc=128, H=16, rounds=20, lr=0.001,
         momentum=0.9, nesterov=True, weight_decay=1e-4, scheme="ef_sign",
         **_IMG, data_seed=201, init_seed=202, sample_seed=0x5EED0009),
+    # the same MLP round with the per-epoch reshuffled partition sampler
+    # (the CIFAR procedure's data handling) instead of i.i.d. draws
+    "epoch_mlp_512": Workload(
+        name="epoch_mlp_512", model="mlp", widths=(3072, 512, 512, 10),
+        dtype="fp32", K=16, B_loc=128, H=16, rounds=20, lr=0.001,
+        momentum=0.9, nesterov=False, weight_decay=1e-4, sampler="epoch",
+        **_IMG, data_seed=201, init_seed=202, sample_seed=0x5EED000A),
     # ResNet-20-shaped CNN, fp32, per-worker BN, heavy-ball momentum
     "resnet20": Workload(
         name="resnet20", model="resnet20", widths=(3072, 10), dtype="fp32",
