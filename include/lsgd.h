@@ -218,8 +218,12 @@ lsgd_status lsgd_run_hierarchical_round(lsgd_ctx* ctx, int32_t H, int32_t Hb,
  * the same tree as lsgd_average, without changing state) to d_dst fp32 [P]. */
 lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst);
 
-/* Copy replica `replica`'s momentum buffer to d_dst fp32 [P]. */
+/* Copy replica `replica`'s momentum buffer to d_dst fp32 [P] / overwrite it
+ * from d_src fp32 [P] (checkpoint and resume). replica outside [0, K):
+ * LSGD_E_INVALID. */
 lsgd_status lsgd_read_momentum(lsgd_ctx* ctx, int32_t replica, float* d_dst);
+lsgd_status lsgd_write_momentum(lsgd_ctx* ctx, int32_t replica,
+                                const float* d_src);
 
 /* Copy the global momentum buffer u to d_dst fp32 [P] / overwrite it from
  * d_src fp32 [P] (checkpoint and resume; the synchronised model w_s is set

@@ -983,6 +983,16 @@ lsgd_status lsgd_write_error_memory(lsgd_ctx* ctx, int32_t replica,
   return LSGD_OK;
 }
 
+lsgd_status lsgd_write_momentum(lsgd_ctx* ctx, int32_t replica,
+                                const float* d_src) {
+  LSGD_USABLE(ctx);
+  if (!d_src || replica < 0 || replica >= ctx->cfg.K) return LSGD_E_INVALID;
+  LSGD_CK(ctx, hipMemcpyAsync(ctx->U() + (size_t)replica * ctx->lay.Ps, d_src,
+                              ctx->lay.P * sizeof(float), hipMemcpyDeviceToDevice,
+                              ctx->stream));
+  return LSGD_OK;
+}
+
 lsgd_status lsgd_read_global_momentum(lsgd_ctx* ctx, float* d_dst) {
   LSGD_USABLE(ctx);
   if (!d_dst || !ctx->gm()) return LSGD_E_INVALID;

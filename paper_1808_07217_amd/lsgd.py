@@ -61,6 +61,7 @@ _SIGS = {
     "lsgd_average_blocks": [_P, _c.c_int32],
     "lsgd_synchronise": [_P, _c.c_float],
     "lsgd_read_error_memory": [_P, _c.c_int32, _P],
+    "lsgd_write_momentum": [_P, _c.c_int32, _P],
     "lsgd_write_error_memory": [_P, _c.c_int32, _P],
     "lsgd_sign_sync_scratch_bytes": [_c.c_int32, _c.c_int64, _P],
     "lsgd_replica_sign_sync": [_P, _c.c_int32, _c.c_int64, _P, _P, _P,
@@ -245,6 +246,12 @@ class Replicas:
         if src.dtype != torch.float32 or src.numel() != self.P:
             raise ValueError("src must be float32 with P elements")
         _check(_lib.lsgd_write_global_momentum(self._ctx, _ptr(src)), self._ctx)
+
+    def write_momentum(self, replica: int, src: torch.Tensor):
+        src = src.contiguous()
+        if src.dtype != torch.float32 or src.numel() != self.P:
+            raise ValueError("src must be float32 with P elements")
+        _check(_lib.lsgd_write_momentum(self._ctx, int(replica), _ptr(src)), self._ctx)
 
     def read_error_memory(self, replica: int, out=None) -> torch.Tensor:
         out = out if out is not None else torch.empty(self.P, device=self.device)

@@ -82,6 +82,7 @@ def test_null_context_calls_fail_cleanly():
     assert lib.lsgd_replica_average_blocks(None, 4, 2, 8, None) == 1
     assert lib.lsgd_synchronise(None, ctypes.c_float(0.1)) == 1
     assert lib.lsgd_read_error_memory(None, 0, None) == 1
+    assert lib.lsgd_write_momentum(None, 0, None) == 1
     assert lib.lsgd_write_error_memory(None, 0, None) == 1
     assert lib.lsgd_replica_sign_sync(None, 4, 8, None, None, None, 0, None) == 1
     nb = ctypes.c_size_t()

@@ -523,6 +523,30 @@ def test_sign_scheme_entry_points_and_resume():
                                       c.read_error_memory(k).cpu().numpy())
 
 
+def test_full_state_checkpoint_resumes_bit_exactly():
+    """Checkpoint and resume with every piece of state: the synchronised
+    model, each replica's momentum buffer (Nesterov, heavy-ball buffers
+    carry over rounds), and the step counter. A fresh context restored from
+    them continues bit-identically, replicas and buffers alike."""
+    w = _small((70, 48, 36, 10), K=4, B=12, H=3, rounds=1, nesterov=True)
+    X, y, w0 = _small_data(w, seed=90)
+    a = make_replicas(w, X, y, w0)
+    a.run_round([0.02] * 3)
+    a.run_round([0.01] * 3)
+    c = make_replicas(w, X, y, w0)
+    c.write_params(a.read_params(0))
+    for k in range(w.K):
+        c.write_momentum(k, a.read_momentum(k))
+    c.step = a.step
+    for r in (a, c):
+        r.run_round([0.015, 0.02, 0.01])
+    for k in range(w.K):
+        np.testing.assert_array_equal(a.read_params(k).cpu().numpy(),
+                                      c.read_params(k).cpu().numpy())
+        np.testing.assert_array_equal(a.read_momentum(k).cpu().numpy(),
+                                      c.read_momentum(k).cpu().numpy())
+
+
 # ------------------------------------------------ training-procedure schedules
 @pytest.mark.parametrize("post_local,kind", [(False, "exponential"), (True, None)])
 def test_cifar_plan_with_the_epoch_sampler_matches_oracle(post_local, kind):
