@@ -1177,7 +1177,16 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Tile shape for a problem: 128 x 128 (four MFMA chains per wave) when both
 // output dimensions allow it on the fp32 path, else 64 x 64.
-bool big_tile(int dtype, int M, int N) { return dtype == 0 && M >= 128 && N >= 128; }
+// 128 x 128 fp32 tiles when they fill the chip (256 or more) or the inner
+// dimension is long enough for split-K to amortise them; otherwise 64 x 64
+// tiles without split-K. Measured on the 512-wide MLP: its 512-deep layer
+// GEMMs (64 big tiles) take 18 us as 64 x 64 tiles against 25 us as split-K
+// 128 x 128 tiles plus the reduction; the 3072-deep first layer is fastest
+// as 128 x 128 tiles split four ways.
+bool big_tile(int dtype, int M, int N, int G, int Kd) {
+  if (dtype != 0 || M < 128 || N < 128) return false;
+  return (long long)(M / 128) * (N / 128) * G >= 256 || Kd >= 2048;
+}
 
 // Compute units and resident specialised-update workgroups per CU on the
 // current device, queried once per device.
@@ -1271,7 +1280,7 @@ hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
         (long long)(a.M / 128) * (a.N / 128) * a.G >= kWsMinTiles)
       return launch_gemm_sgd_multi(dtype, &a, 1, s);
   }
-  const bool big = big_tile(dtype, a.M, a.N);
+  const bool big = big_tile(dtype, a.M, a.N, a.G, a.Kd);
   const int BM = big ? 128 : 64, BN = BM;
   const long long tiles = (long long)((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM) * a.G;
   const long long total = tiles * a.splits;
@@ -1325,12 +1334,12 @@ hipError_t dispatch(int dtype, const GemmArgs& a, hipStream_t s) {
 
 int gemm_splits(int dtype, int M, int N, int Kd, int G, int epi) {
   if (epi == EPI_SGD) return 1;
-  const int T = big_tile(dtype, M, N) ? 128 : 64;
+  const int T = big_tile(dtype, M, N, G, Kd) ? 128 : 64;
   const long long tiles = (long long)((N + T - 1) / T) * ((M + T - 1) / T) * G;
   int s = 1;
-  // up to 8 splits while the grid stays within ~4 workgroups per CU and every
-  // split keeps at least 128 of K
-  while (s < 8 && tiles * s * 2 <= 1024 && Kd / (s * 2) >= 128) s *= 2;
+  // up to 8 splits while the grid has fewer workgroups than compute units
+  // and every split keeps at least 128 of K
+  while (s < 8 && tiles * s < 256 && Kd / (s * 2) >= 128) s *= 2;
   return s;
 }
 
