@@ -355,6 +355,125 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
 }
 
+// The stem: a 3 x 3 stride-1 convolution of a 3-channel 32 x 32 image (read
+// through the row map, or at group stride sx) to 16 channels. The image goes
+// to LDS once as a zero-padded 34 x 34 x 3 tile; taps t = (kh, kw, ci) index
+// the 27 rows of the [27][16] weight.
+constexpr int kStemSide = 32, kStemTile = kStemSide + 2, kStemCin = 3, kStemCout = 16;
+constexpr int kStemTaps = 9 * kStemCin;
+
+__device__ __forceinline__ const float* stem_image(const ConvArgs& c, int g, int b) {
+  const long long img = (long long)kStemSide * kStemSide * kStemCin;
+  return c.rowmap ? c.x + (long long)c.rowmap[(long long)g * c.Bt + b] * img
+                  : c.x + (long long)g * c.sx + (long long)b * img;
+}
+
+// Zero the tile, then scatter the image's 768 float4 into its interior.
+__device__ __forceinline__ void stem_stage(float* T, const float* src) {
+  constexpr int NT = kStemTile * kStemTile * kStemCin;
+  constexpr int Q = kStemSide * kStemSide * kStemCin / 4;
+  static_assert(Q % kT == 0, "whole float4 rounds");
+  v4f v[Q / kT];
+#pragma unroll
+  for (int i = 0; i < Q / kT; ++i) v[i] = *(const v4f*)(src + 4 * (threadIdx.x + kT * i));
+  for (int i = threadIdx.x; i < NT; i += kT) T[i] = 0.f;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < Q / kT; ++i) {
+    const int e0 = 4 * (threadIdx.x + kT * i);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = e0 + j, pix = e / kStemCin, ci = e - pix * kStemCin;
+      const int h = pix / kStemSide, w = pix - h * kStemSide;
+      T[((h + 1) * kStemTile + w + 1) * kStemCin + ci] = v[i][j];
+    }
+  }
+  __syncthreads();
+}
+
+// Tap t's input value for output position (h, w) from the tile; 0 for t >= 27.
+__device__ __forceinline__ float stem_tap(const float* T, int t, int h, int w) {
+  const int tt = t < kStemTaps ? t : 0;
+  const int kh = tt / 9, kw = (tt / 3) % 3, ci = tt % 3;
+  const float v = T[((h + kh) * kStemTile + w + kw) * kStemCin + ci];
+  return t < kStemTaps ? v : 0.f;
+}
+
+// Forward, one workgroup per (replica, image): y^T = W^T X^T as
+// v_mfma_f32_16x16x4f32 blocks of 16 output channels x 16 positions over
+// 7 steps of 4 taps (the 28th tap is zero). Lane l holds channels
+// 4 (l / 16) .. + 3 of position l % 16 of its block, one float4 store.
+__global__ __launch_bounds__(kT) void k_conv_stem_fwd(ConvArgs c) {
+  __shared__ float T[kStemTile * kStemTile * kStemCin];
+  const int g = blockIdx.x / c.Bt, b = blockIdx.x - g * c.Bt;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lq = lane >> 4, lm = lane & 15;
+  const float* Wg = c.Wk + (long long)g * c.sW;
+  float wa[7];
+#pragma unroll
+  for (int ks = 0; ks < 7; ++ks) {
+    const int t = 4 * ks + lq;
+    wa[ks] = t < kStemTaps ? Wg[t * kStemCout + lm] : 0.f;
+  }
+  stem_stage(T, stem_image(c, g, b));
+  float* out = c.out + ((long long)g * c.Bt + b) * kStemSide * kStemSide * kStemCout;
+  // wave w: rows 8w .. 8w+7, two blocks of 16 columns each
+#pragma unroll 2
+  for (int blk = 0; blk < 16; ++blk) {
+    const int h = 8 * wave + (blk >> 1), w = 16 * (blk & 1) + lm;
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 7; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[ks], stem_tap(T, 4 * ks + lq, h, w),
+                                                 acc, 0, 0, 0);
+    *(v4f*)(out + (h * kStemSide + 16 * (blk & 1) + lm) * kStemCout + 4 * lq) =
+        v4f{acc[0], acc[1], acc[2], acc[3]};
+  }
+}
+
+// Weight gradient, workgroup (replica g, split s) over the s-th run of
+// whole images (c.mchunk positions, a multiple of 1024):
+//   dW[t][co] = sum_p x(p, tap t) dy[p][co]
+// as two 16 x 16 blocks of taps (0-15, 16-31; taps 27-31 zero) x 16 output
+// channels, 4 positions per v_mfma_f32_16x16x4f32 step. Wave w takes rows
+// 8w .. 8w+7 of every image; the four waves' sums are added in wave order
+// into the partial [S][G][27][16] for k_conv_wupdate.
+__global__ __launch_bounds__(kT) void k_conv_wgrad_stem(ConvArgs c) {
+  __shared__ float T[kStemTile * kStemTile * kStemCin];
+  __shared__ float R[4][2 * 16 * 16];
+  const int g = blockIdx.x / c.splits, s = blockIdx.x - g * c.splits;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lq = lane >> 4, lm = lane & 15;
+  constexpr int HW = kStemSide * kStemSide;
+  const int img0 = s * (c.mchunk / HW), nimg = c.mchunk / HW;
+  floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < nimg && img0 + i < c.Bt; ++i) {
+    const int b = img0 + i;
+    if (i) __syncthreads();  // every wave is done with the previous tile
+    stem_stage(T, stem_image(c, g, b));
+    const float* dy = c.dy + ((long long)g * c.Bt + b) * HW * kStemCout;
+#pragma unroll 4
+    for (int q = 0; q < 64; ++q) {
+      const int p = 256 * wave + 4 * q + lq;   // this lane's position
+      const int h = p >> 5, w = p & 31;
+      const float bv = dy[(long long)p * kStemCout + lm];
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(stem_tap(T, lm, h, w), bv, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(stem_tap(T, 16 + lm, h, w), bv, acc1,
+                                                  0, 0, 0);
+    }
+  }
+  // C[4 (l/16) + v][l % 16]: rows are taps, columns output channels
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    R[wave][(4 * lq + v) * 16 + lm] = acc0[v];
+    R[wave][256 + (4 * lq + v) * 16 + lm] = acc1[v];
+  }
+  __syncthreads();
+  float* part = c.out + ((long long)s * c.G + g) * kStemTaps * kStemCout;
+  for (int e = threadIdx.x; e < kStemTaps * kStemCout; e += kT)
+    part[e] = ((R[0][e] + R[1][e]) + R[2][e]) + R[3][e];
+}
+
 // Stride-1 convolution with 16 channels in and out on 32-wide images (the
 // first stage): workgroup (g, b, band) computes 8 output rows x 32 columns x
 // 16 channels. The input rows h0-1 .. h0+8 (zero-padded) and the 144 x 16
@@ -1144,6 +1263,15 @@ int blocks_for(long long n) {
 }  // namespace
 
 // ------------------------------------------------------------ launchers
+// The stem shape the dedicated kernels take: 3 -> 16 channels, stride 1,
+// 32 x 32, 16-byte aligned image rows (3072 floats) and output.
+static bool stem_shape(const ConvGeom& q) {
+  return q.Cin == kStemCin && q.Cout == kStemCout && q.stride == 1 && q.H == kStemSide &&
+         q.W == kStemSide && q.Ho == kStemSide && q.Wo == kStemSide &&
+         ((uintptr_t)q.x & 15) == 0 && ((uintptr_t)q.dy & 15) == 0 &&
+         ((uintptr_t)q.out & 15) == 0 && (q.rowmap || q.sx % 4 == 0);
+}
+
 int conv_wgrad_splits(int Bt, int Ho, int Wo) {
   const int rows = Bt * Ho * Wo;
   int s = 1;
@@ -1191,6 +1319,12 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
                          st, c);
       return hipGetLastError();
     }
+    if (stem_shape(q) && rows % (c.splits * kStemSide * kStemSide) == 0) {
+      c.mchunk = rows / c.splits;  // whole images per split
+      hipLaunchKernelGGL(k_conv_wgrad_stem, dim3((unsigned)(q.G * c.splits)), dim3(kT), 0,
+                         st, c);
+      return hipGetLastError();
+    }
     if (rowsk) {
       // whole 64-position slabs per split
       c.mchunk = ((rows + c.splits - 1) / c.splits + 63) / 64 * 64;
@@ -1224,6 +1358,12 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
                       ((uintptr_t)q.Wk & 15) == 0 && q.sW % 4 == 0 &&
                       ((uintptr_t)(mode == CONV_FWD ? q.x : q.dy) & 15) == 0 &&
                       (mode == CONV_DGRAD || q.sx % 4 == 0);
+    if (mode == CONV_FWD && stem_shape(q)) {
+      const long long nb = (long long)q.G * q.Bt;
+      if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
+      hipLaunchKernelGGL(k_conv_stem_fwd, dim3((unsigned)nb), dim3(kT), 0, st, c);
+      return hipGetLastError();
+    }
     if (halo) {
       const long long nb = (long long)q.G * q.Bt * (q.H / 8);
       if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
