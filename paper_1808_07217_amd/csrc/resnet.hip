@@ -220,12 +220,20 @@ __global__ __launch_bounds__(kT) void k_conv_gemm(ConvArgs c, int vec) {
 // slab t computes. Each wave owns 64 rows as 16 x 16 blocks of
 // v_mfma_f32_16x16x4f32 (lane l: A[m = l%16][k = l/16], B[k = l/16][n = l%16],
 // accumulator v at C[4 (l/16) + v][l%16]).
+//
+// P2 (input gradient of a stride-2 convolution, H = 2 Ho, W = 2 Wo): an
+// input position (2i + ph, 2j + pw) only receives taps with kh = 1 (ph = 0)
+// or kh in {0, 2} (ph = 1), and likewise for kw -- 1, 2, 2 or 4 of the nine
+// by parity class. The rows are ordered (class, image, i, j) so that every
+// 256-row tile lies in one class (Bt Ho Wo a multiple of 256) and its slabs
+// run over that class's taps only.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-template <int MODE, int BN>
+template <int MODE, int BN, bool P2 = false>
 __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   static_assert(MODE == CONV_FWD || MODE == CONV_DGRAD, "row-tiled modes");
+  static_assert(!P2 || MODE == CONV_DGRAD, "parity classes are an input-gradient form");
   constexpr int BM = 256, BK = 16, PK = BK + 4;  // 80-byte A rows in LDS
   constexpr int NBL = BN / 16;                    // 16-wide column blocks
   constexpr int RPT = BM * BK / 4 / kT;           // A float4 per thread (4)
@@ -241,6 +249,10 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kq = (tid & 3) * 4;  // this thread's 4 channels of the slab
   const float* Bw = c.Wk + (long long)g * c.sW;  // [9 Cr][BN]
+  // P2: this tile's parity class and the slab count of its taps
+  const int HWq = c.Ho * c.Wo, cls_rows = c.Bt * HWq;
+  const int cls = P2 ? m0 / cls_rows : 0, ph = cls >> 1, pw = cls & 1;
+  const int nkw = P2 && pw ? 2 : 1, ntap = P2 ? (ph ? 2 : 1) * nkw : 9;
 
   // rows of this thread: r = tid / 4 + 64 i
   long long base[RPT];  // image (or output-gradient image) base, elements
@@ -258,6 +270,13 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       xa[i] = ow * c.stride - 1;
       base[i] = c.rowmap ? (long long)c.rowmap[(long long)g * c.Bt + b] * c.H * c.W * c.Cin
                          : (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
+    } else if constexpr (P2) {
+      const int rem = mm - cls * cls_rows;
+      const int bb = rem / HWq, q = rem - bb * HWq;
+      const int ii = q / c.Wo, jj = q - ii * c.Wo;
+      ya[i] = 2 * ii + ph + 1;
+      xa[i] = 2 * jj + pw + 1;
+      base[i] = ((long long)g * c.Bt + bb) * c.Ho * c.Wo * c.Cout;
     } else {
       const int h = p / c.W, w = p - h * c.W;
       ya[i] = h + 1;  // output-gradient row of tap kh: (ya - kh) / stride
@@ -266,10 +285,19 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
   }
   const float* src = MODE == CONV_FWD ? c.x : c.dy;
-  const int nk = 9 * Cr / BK;
+  const int nk = ntap * Cr / BK;
   auto gload = [&](int s, v4f(&xa4)[RPT], v4f& xb) __attribute__((always_inline)) {
-    const int tap = s / (Cr / BK), ch0 = (s - tap * (Cr / BK)) * BK + kq;
-    const int kh = tap / 3, kw = tap - kh * 3;
+    const int ti = s / (Cr / BK), ch0 = (s - ti * (Cr / BK)) * BK + kq;
+    int kh, kw;
+    if constexpr (P2) {  // the class's taps: kh = 1 or {0, 2}, kw likewise
+      const int th = ti / nkw, tw = ti - th * nkw;
+      kh = ph ? 2 * th : 1;
+      kw = pw ? 2 * tw : 1;
+    } else {
+      kh = ti / 3;
+      kw = ti - kh * 3;
+    }
+    const int tap = kh * 3 + kw;
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       int yy, xx;
@@ -293,7 +321,8 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       if (!ok) xa4[i] = v4f{0.f, 0.f, 0.f, 0.f};
     }
     const int bq = min(tid, BQ - 1);
-    xb = *(const v4f*)(Bw + (long long)(s * BK + bq / (BN / 4)) * BN + (bq % (BN / 4)) * 4);
+    const int wrow = tap * Cr + (s - ti * (Cr / BK)) * BK;  // slab's first weight row
+    xb = *(const v4f*)(Bw + (long long)(wrow + bq / (BN / 4)) * BN + (bq % (BN / 4)) * 4);
   };
   auto lstore = [&](int buf, const v4f(&xa4)[RPT], const v4f& xb) __attribute__((always_inline)) {
 #pragma unroll
@@ -349,8 +378,15 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     for (int v = 0; v < 4; ++v) {
       const int m = m0 + wave * 64 + i * 16 + lq * 4 + v;
       if (m < Mg) {
+        long long row = m;
+        if constexpr (P2) {  // back to (image, h, w) order
+          const int rem = m - cls * cls_rows;
+          const int bb = rem / HWq, q = rem - bb * HWq;
+          const int ii = q / c.Wo, jj = q - ii * c.Wo;
+          row = ((long long)bb * c.H + 2 * ii + ph) * c.W + 2 * jj + pw;
+        }
 #pragma unroll
-        for (int j = 0; j < NBL; ++j) out[(long long)m * BN + j * 16 + lm] = acc[i][j][v];
+        for (int j = 0; j < NBL; ++j) out[row * BN + j * 16 + lm] = acc[i][j][v];
       }
     }
 }
@@ -1380,6 +1416,15 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
         if (Ng == 16) LSGD_ROWS(CONV_FWD, 16);
         else if (Ng == 32) LSGD_ROWS(CONV_FWD, 32);
         else LSGD_ROWS(CONV_FWD, 64);
+      } else if (q.stride == 2 && q.H == 2 * q.Ho && q.W == 2 * q.Wo &&
+                 ((long long)q.Bt * q.Ho * q.Wo) % 256 == 0) {
+        // input gradient of a stride-2 convolution by parity class
+#define LSGD_ROWS2(NB)                                                                 \
+  hipLaunchKernelGGL((k_conv_rows<CONV_DGRAD, NB, true>), dim3((unsigned)rt), dim3(kT), 0, st, c)
+        if (Ng == 16) LSGD_ROWS2(16);
+        else if (Ng == 32) LSGD_ROWS2(32);
+        else LSGD_ROWS2(64);
+#undef LSGD_ROWS2
       } else {
         if (Ng == 16) LSGD_ROWS(CONV_DGRAD, 16);
         else if (Ng == 32) LSGD_ROWS(CONV_DGRAD, 32);
