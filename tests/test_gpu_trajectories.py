@@ -4,7 +4,8 @@ The expected trajectories in tests/golden/trajectory_<name>.json were written
 by tests/golden/make_trajectories.py, which runs only the CPU oracle on the
 seeded inputs. Every local step of every round is compared: the mean over the
 K replicas of the mini-batch loss, relative error 1e-3 (fp32) or 2e-2 (bf16
-GEMM operands).
+GEMM operands), widened where the oracle's own trajectory is sensitive
+(below).
 """
 import json
 import os
@@ -20,7 +21,14 @@ pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CASES = [("mlp_512", 1e-3), ("postlocal_mlp_512", 1e-3),
-         ("wide_mlp_2048_bf16", 2e-2)]
+         ("wide_mlp_2048_bf16", 2e-2), ("resnet20", 1e-3)]
+# How far an fp32 run may legitimately drift from the fp64 oracle grows with
+# the trajectory's own sensitivity: where a golden run from initial weights
+# perturbed by 1e-7 (relative; trajectory_<name>_perturbed.json, also the
+# oracle's) has moved by rel_p, the bar is max(tol, ENVELOPE * running max of
+# rel_p). ResNet-20's batch-normalised descent amplifies a 1e-7 perturbation
+# to 3e-2 by the end of its five rounds.
+ENVELOPE = 4.0
 
 
 @pytest.mark.parametrize("name,tol", CASES)
@@ -40,7 +48,14 @@ def test_full_run_loss_trajectory(name, tol):
     got = loss.cpu().numpy().mean(axis=1)
     want = np.concatenate([np.asarray(r) for r in gold])
     err = rel(got, want)
+    bar = np.full_like(err, tol)
+    pert = os.path.join(HERE, "golden", f"trajectory_{name}_perturbed.json")
+    if os.path.exists(pert):
+        with open(pert) as f:
+            moved = np.concatenate([np.asarray(r) for r in
+                                    json.load(f)["per_round_step_mean_loss"]])
+        bar = np.maximum(bar, ENVELOPE * np.maximum.accumulate(rel(moved, want)))
     print(f"{name}: max relative loss error {err.max():.3e} at step "
-          f"{int(err.argmax())}; final loss {got[-1]:.5g} vs {want[-1]:.5g}",
-          flush=True)
-    assert np.all(err <= tol)
+          f"{int(err.argmax())} (bar there {bar[err.argmax()]:.3e}); final loss "
+          f"{got[-1]:.5g} vs {want[-1]:.5g}", flush=True)
+    assert np.all(err <= bar), int(np.argmax(err / bar))
