@@ -780,6 +780,47 @@ lsgd_status do_average_blocks(lsgd_ctx* c, int Kb) {
   return LSGD_OK;
 }
 
+// A whole round of softmax regression (one fp32 layer, plain local SGD and
+// averaging) in one launch when the replicas fit in LDS.
+bool tiny_round_ok(const lsgd_ctx* c, int H) {
+  const lsgd_config& cf = c->cfg;
+  return cf.model == LSGD_MODEL_MLP && cf.n_layers == 1 && cf.gemm_dtype == LSGD_FP32 &&
+         cf.scheme == LSGD_SCHEME_LOCAL && cf.global_momentum == 0.f &&
+         lsgd::tiny_round_fits(cf.K, cf.B_loc, cf.widths[0], cf.widths[1], H);
+}
+
+lsgd_status do_tiny_round(lsgd_ctx* c, int H, const float* h_lr, float* d_loss) {
+  const lsgd_config& cf = c->cfg;
+  lsgd::TinyArgs a{};
+  a.X = c->X;
+  a.y = c->y;
+  a.W = c->W();
+  a.U = c->U();
+  a.loss = d_loss;
+  a.N = cf.N;
+  a.Ps = c->lay.Ps;
+  a.step0 = c->step;
+  a.K = cf.K;
+  a.B = cf.B_loc;
+  a.D = cf.widths[0];
+  a.C = cf.widths[1];
+  a.H = H;
+  a.key0 = (uint32_t)cf.seed;
+  a.key1 = (uint32_t)(cf.seed >> 32);
+  a.mom = cf.momentum;
+  a.wd = cf.weight_decay;
+  a.mode = upd_mode(cf);
+  if (cf.sampler == LSGD_SAMPLER_EPOCH) {
+    a.S = (cf.N / cf.K) / cf.B_loc;
+    a.m = 1;
+    while ((1LL << (2 * a.m)) < cf.N) ++a.m;
+  }
+  for (int h = 0; h < H; ++h) a.lr[h] = h_lr[h];
+  LSGD_LAUNCH(c, "tiny_round", lsgd::launch_tiny_round(a, c->stream));
+  c->step += H;
+  return LSGD_OK;
+}
+
 #define LSGD_USABLE(ctx)                                   \
   do {                                                     \
     if (!(ctx)) return LSGD_E_INVALID;                     \
@@ -886,6 +927,7 @@ lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
   for (int h = 0; h < H; ++h)
     if (!std::isfinite(h_lr[h])) return LSGD_E_INVALID;
   if (ctx->gm() && (H == 0 || h_lr[H - 1] == 0.f)) return LSGD_E_INVALID;
+  if (tiny_round_ok(ctx, H)) return do_tiny_round(ctx, H, h_lr, d_loss);
   for (int h = 0; h < H; ++h) {
     lsgd_status st = do_local_step(ctx, h_lr[h],
                                    d_loss ? d_loss + (size_t)h * ctx->cfg.K : nullptr);

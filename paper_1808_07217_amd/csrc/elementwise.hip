@@ -2,26 +2,10 @@
 // sampling, softmax cross-entropy, bias gradient + update, the fused
 // momentum-SGD update, and the K-way replica average.
 #include "kernels.h"
+#include "device_common.h"
 
 namespace lsgd {
 namespace {
-
-// ------------------------------------------------------------------ Philox
-// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
-// 32x32->64-bit multiplies with a Weyl-sequence key schedule.
-__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r) {
-      k0 += 0x9E3779B9u;
-      k1 += 0xBB67AE85u;
-    }
-    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
-  }
-  return c;
-}
 
 // One thread per (worker k, group of 4 slots): a Philox block gives the four
 // uniform words of slots 4q .. 4q+3 of worker k at local step `step`.
@@ -44,46 +28,14 @@ __global__ void k_sample(uint32_t key0, uint32_t key1, uint32_t s_lo,
   }
 }
 
-// Per-epoch reshuffled partition. Epoch e's permutation of [0, N) is a
-// balanced Feistel network on 2m-bit words (4^m >= N) whose four round
-// functions are word 0 of Philox4x32-10 at counter (right half, round, e,
-// kShuffleStream), restricted to [0, N) by cycle walking: an image >= N is
-// permuted again. The walk ends on the first in-range value of the cycle
-// through the start, after about 4^m / N steps on average; a cap far above
-// any plausible walk returns the position itself (still a valid row), so
-// the kernel always finishes and a parity test would show the failure.
-constexpr uint32_t kShuffleStream = 0x5348464Cu;
-constexpr int kCycleWalkCap = 1 << 12;
-
-__device__ __forceinline__ uint32_t feistel4(uint32_t x, int m, uint32_t mask,
-                                             uint32_t k0, uint32_t k1,
-                                             uint32_t e) {
-  uint32_t left = x >> m, right = x & mask;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const uint4 f = philox4x32_10(make_uint4(right, (uint32_t)r, e, kShuffleStream), k0, k1);
-    const uint32_t t = left ^ (f.x & mask);
-    left = right;
-    right = t;
-  }
-  return (left << m) | right;
-}
-
 // One thread per (worker k = blockIdx.y, slot b): row pi_e(lo_k + jB + b).
 __global__ void k_sample_epoch(uint32_t key0, uint32_t key1, uint32_t e, long long j,
                                int K, long long N, int B, int m, int32_t* idx) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   const int k = blockIdx.y;
   if (b >= B) return;
-  const uint32_t mask = (1u << m) - 1u;
   const uint32_t q = (uint32_t)((long long)k * N / K + j * B + b);
-  uint32_t y = feistel4(q, m, mask, key0, key1, e);
-  int walk = 0;
-  while (y >= (uint64_t)N && walk < kCycleWalkCap) {
-    y = feistel4(y, m, mask, key0, key1, e);
-    ++walk;
-  }
-  idx[(long long)k * B + b] = (int32_t)(y < (uint64_t)N ? y : q);
+  idx[(long long)k * B + b] = epoch_row(q, N, m, key0, key1, e);
 }
 
 // ------------------------------------------------------------------ loss

@@ -186,6 +186,27 @@ hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
 hipError_t launch_average_gm(float* W, bf16_t* Wb, int K, long long n,
                              long long ld, float* ws, float* ug, float mg,
                              float lr, hipStream_t s);
+// Single-launch round for softmax regression (tiny.hip): every replica and
+// its buffer live in LDS for the H steps and the average.
+constexpr int kTinyMaxC = 32, kTinyMaxH = 64;
+constexpr size_t kTinyMaxLds = 160 * 1024;
+struct TinyArgs {
+  const float* X;      // [N][D]
+  const int32_t* y;    // [N]
+  float* W;            // [K][Ps] replicas (read, then the averaged model)
+  float* U;            // [K][Ps] momentum buffers
+  float* loss;         // [H][K] or nullptr
+  long long N, Ps, step0;
+  long long S;         // batches per epoch of the reshuffle sampler; 0: i.i.d.
+  int K, B, D, C, H, m;
+  uint32_t key0, key1;
+  float mom, wd;
+  int mode;            // kModeNesterov | kModeSign
+  float lr[kTinyMaxH];
+};
+size_t tiny_round_lds_bytes(int K, int B, int D, int C);
+bool tiny_round_fits(int K, int B, int D, int C, int H);
+hipError_t launch_tiny_round(const TinyArgs& a, hipStream_t s);
 // Sign-compressed synchronisation (compress.hip): W fp32 [K][Ps] replicas
 // (the first P elements of each row are the model), ws fp32 [Ps] the model
 // of the previous synchronisation (updated), E fp32 [K][Ps] error memories

@@ -1,0 +1,296 @@
+// One launch per local-SGD round for softmax regression (one layer, fp32)
+// when every replica and its momentum buffer fit in LDS: H local steps on all
+// K replicas followed by the K-way average (eq. 2, Algorithm 1's round), in
+// one workgroup. Small problems are bound by launch latency, not by work --
+// the multi-kernel round of such a problem is 13 launches for H = 4 -- so the
+// whole round runs from LDS with no launch between its steps.
+//
+// Workgroup layout: four waves; replica k belongs to wave k mod 4. Per local
+// step and replica, its wave
+//   samples B indices (the configured sampler),
+//   forwards its rows (lane = row: C logits, the weight read from LDS by
+//     broadcast), takes the stable softmax cross-entropy and
+//     dZ = (softmax - onehot) / B into LDS, the mean loss by a fixed
+//     butterfly,
+//   forms dW[i][c] = sum_b x[b][i] dZ[b][c] in ascending b (lane = input
+//     feature) and db[c], and applies the momentum-SGD step to the replica
+//     in LDS.
+// Then the replicas are averaged in the replica-average tree order and
+// replicas and buffers are written back.
+#include "kernels.h"
+#include "device_common.h"
+
+namespace lsgd {
+namespace {
+
+constexpr int kTinyThreads = 256;
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Per-step scratch of one wave: dZ [B][C], the sampled row indices [B] and
+// the rows themselves [B][D | 1].
+__device__ __forceinline__ float wave_sum_fixed(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// CM >= C: classes padded to a compile-time count. Weights, buffers and dZ
+// sit in LDS at a row pitch of CM (padded entries zero, so they stay zero
+// through every update), the hot loops run over all CM columns with float4
+// LDS reads, and the padded logits are masked to -inf: no loop branches on
+// the class count.
+template <int CM>
+__global__ __launch_bounds__(kTinyThreads) void k_tiny_round(TinyArgs a) {
+  extern __shared__ float lds[];
+  const int K = a.K, B = a.B, D = a.D, C = a.C, P = D * C + C;
+  const int PL = (D + 1) * CM;              // a replica in LDS: D rows + bias row
+  float* Wl = lds;                          // [K][D + 1][CM]
+  float* Ul = Wl + (long long)K * PL;       // [K][D + 1][CM]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int XP = D | 1;  // odd row pitch: lane-per-row reads miss no bank
+  const int WS = (B * CM + B + B * XP + 3) & ~3;  // per-wave scratch, float4-aligned
+  float* dz = Ul + (long long)K * PL + wave * WS;     // this wave's [B][CM]
+  int32_t* rows = (int32_t*)(dz + B * CM);                            // [B]
+  float* xs = dz + B * CM + B;                                        // [B][XP] its rows
+
+#pragma unroll 8
+  for (int e = threadIdx.x; e < K * PL; e += kTinyThreads) {
+    const int k = e / PL, q = e - k * PL, i = q / CM, c = q - i * CM;
+    const long long g = (long long)k * a.Ps + i * C + c;
+    const bool ok = c < C;
+    Wl[e] = ok ? a.W[g] : 0.f;
+    Ul[e] = ok ? a.U[g] : 0.f;
+  }
+  __syncthreads();
+
+  const float invB = 1.0f / (float)B;
+  const int slots = (K + 3) / 4;
+  for (int h = 0; h < a.H; ++h) {
+    const long long step = a.step0 + h;
+    const float lr = a.lr[h];
+    for (int r = 0; r < slots; ++r) {
+      // every wave passes the same barriers; waves without a replica in this
+      // slot (k >= K) skip the work between them
+      const int k = 4 * r + wave;
+      const bool mine = k < K;
+      float* W = Wl + (long long)(mine ? k : 0) * PL;
+      float* U = Ul + (long long)(mine ? k : 0) * PL;
+      const long long lo = (long long)k * a.N / K;
+      if (mine) {
+        // sampling
+        if (a.S > 0) {  // per-epoch reshuffled partition
+          const long long ep = step / a.S, j = step - ep * a.S;
+          for (int b = lane; b < B; b += 64)
+            rows[b] = epoch_row((uint32_t)(lo + j * B + b), a.N, a.m, a.key0, a.key1,
+                                (uint32_t)ep);
+        } else {        // i.i.d. from the worker's shard
+          const uint64_t n = (uint64_t)((long long)(k + 1) * a.N / K - lo);
+          for (int q = lane; 4 * q < B; q += 64) {
+            const uint4 u = philox4x32_10(
+                make_uint4((uint32_t)q, (uint32_t)step, (uint32_t)k,
+                           (uint32_t)((uint64_t)step >> 32)), a.key0, a.key1);
+            const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (4 * q + e < B)
+                rows[4 * q + e] = (int32_t)(lo + (long long)(((uint64_t)w4[e] * n) >> 32));
+          }
+        }
+      }
+      __syncthreads();
+      if (mine) {
+        // the batch's rows into LDS, every load in flight before any store
+        if ((D & 3) == 0) {
+          const int D4 = D >> 2;
+#pragma unroll 8
+          for (int e = lane; e < B * D4; e += 64) {
+            const int b = e / D4, i4 = e - b * D4;
+            const v4f v = *(const v4f*)(a.X + (long long)rows[b] * D + 4 * i4);
+            float* d = xs + b * XP + 4 * i4;
+            d[0] = v[0];
+            d[1] = v[1];
+            d[2] = v[2];
+            d[3] = v[3];
+          }
+        } else {
+#pragma unroll 8
+          for (int e = lane; e < B * D; e += 64) {
+            const int b = e / D, i = e - b * D;
+            xs[b * XP + i] = a.X[(long long)rows[b] * D + i];
+          }
+        }
+      }
+      __syncthreads();
+      if (mine) {
+        // forward, loss, dZ: lane = row
+        float lsum = 0.f;
+        for (int b0 = 0; b0 < B; b0 += 64) {
+          const int b = b0 + lane;
+          const bool live = b < B;
+          const int row = live ? rows[b] : rows[0];
+          const int lab = a.y[row];   // issued before the forward loop
+          const float* x = xs + (live ? b : 0) * XP;
+          float z[CM];
+#pragma unroll
+          for (int c = 0; c < CM; ++c) z[c] = 0.f;
+#pragma unroll 4
+          for (int i = 0; i < D; ++i) {
+            const float xi = x[i];
+#pragma unroll
+            for (int c4 = 0; c4 < CM; c4 += 4) {
+              const v4f wv = *(const v4f*)(W + i * CM + c4);
+#pragma unroll
+              for (int j = 0; j < 4; ++j) z[c4 + j] = __builtin_fmaf(xi, wv[j], z[c4 + j]);
+            }
+          }
+          float m = -INFINITY;
+#pragma unroll
+          for (int c = 0; c < CM; ++c) {
+            z[c] = c < C ? z[c] + W[D * CM + c] : -INFINITY;
+            m = fmaxf(m, z[c]);
+          }
+          float s = 0.f, rest = 0.f, zy = 0.f;
+#pragma unroll
+          for (int c = 0; c < CM; ++c) {
+            const float e = __expf(z[c] - m);   // 0 for the padded classes
+            s += e;
+            rest += c != lab ? e : 0.f;
+            zy = c == lab ? z[c] : zy;
+          }
+          const float loss = zy >= m ? log1pf(rest) : (m - zy) + logf(s);
+          const float inv_s = 1.0f / s;
+          if (live) {
+#pragma unroll
+            for (int c4 = 0; c4 < CM; c4 += 4) {
+              v4f v;
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                v[j] = (__expf(z[c4 + j] - m) * inv_s - (c4 + j == lab ? 1.f : 0.f)) * invB;
+              *(v4f*)(dz + b * CM + c4) = v;
+            }
+            lsum += loss;
+          }
+        }
+        lsum = wave_sum_fixed(lsum);
+        if (lane == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
+      }
+      __syncthreads();
+      if (mine) {
+        // weight gradient and update: lane = input feature (and the bias row
+        // as feature D, whose "input" is 1)
+        for (int i0 = 0; i0 <= D; i0 += 64) {
+          const int i = i0 + lane;
+          if (i <= D) {
+            float g[CM];
+#pragma unroll
+            for (int c = 0; c < CM; ++c) g[c] = 0.f;
+#pragma unroll 4
+            for (int b = 0; b < B; ++b) {
+              const float xi = i < D ? xs[b * XP + i] : 1.f;
+#pragma unroll
+              for (int c4 = 0; c4 < CM; c4 += 4) {
+                const v4f dv = *(const v4f*)(dz + b * CM + c4);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) g[c4 + j] = __builtin_fmaf(xi, dv[j], g[c4 + j]);
+              }
+            }
+            const float wd = a.wd;   // coupled decay on weights and biases alike
+#pragma unroll
+            for (int c4 = 0; c4 < CM; c4 += 4) {
+              v4f w = *(v4f*)(W + i * CM + c4), u = *(v4f*)(U + i * CM + c4);
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const float gg = __builtin_fmaf(wd, w[j], g[c4 + j]);
+                u[j] = __builtin_fmaf(a.mom, u[j], gg);
+                w[j] = __builtin_fmaf(-lr, step_dir(u[j], gg, a.mom, a.mode), w[j]);
+              }
+              *(v4f*)(W + i * CM + c4) = w;
+              *(v4f*)(U + i * CM + c4) = u;
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // the K-way average, every replica := mean; then write back
+  for (int p = threadIdx.x; p < P; p += kTinyThreads) {
+    const int i = p / C, c = p - i * C;
+    const float mean = tree_sum_f(Wl + i * CM + c, PL, K) / (float)K;
+    for (int k = 0; k < K; ++k) a.W[k * a.Ps + p] = mean;
+  }
+#pragma unroll 4
+  for (int e = threadIdx.x; e < K * P; e += kTinyThreads) {
+    const int k = e / P, p = e - k * P, i = p / C, c = p - i * C;
+    a.U[k * a.Ps + p] = Ul[(long long)k * PL + i * CM + c];
+  }
+}
+
+}  // namespace
+
+int tiny_classes(int C) { return C <= 8 ? 8 : C <= 16 ? 16 : 32; }
+
+size_t tiny_round_lds_bytes(int K, int B, int D, int C) {
+  const int CM = tiny_classes(C);
+  const long long wave = ((long long)B * CM + B + (long long)B * (D | 1) + 3) & ~3LL;
+  return (size_t)(2LL * K * (D + 1) * CM + 4LL * wave) * sizeof(float);
+}
+
+// The kernel's dynamic LDS above the default 64 KB: requested once per
+// device and instance (gfx950 compute units hold 160 KB).
+template <int CM>
+hipError_t allow_lds(size_t bytes) {
+  static bool done[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= 64) return e != hipSuccess ? e : hipErrorInvalidDevice;
+  if (bytes <= 64 * 1024 || done[dev]) return hipSuccess;
+  e = hipFuncSetAttribute((const void*)k_tiny_round<CM>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)kTinyMaxLds);
+  if (e == hipSuccess) done[dev] = true;
+  return e;
+}
+
+// LDS one workgroup may opt in to on the current device (cached per device).
+size_t tiny_lds_limit() {
+  static size_t limit[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!limit[dev]) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeSharedMemPerBlockOptin, dev) != hipSuccess ||
+        v <= 0)
+      v = 64 * 1024;
+    limit[dev] = (size_t)v;
+  }
+  return limit[dev];
+}
+
+bool tiny_round_fits(int K, int B, int D, int C, int H) {
+  if (K < 1 || B < 1 || D < 1 || C < 2 || C > kTinyMaxC || H < 1 || H > kTinyMaxH)
+    return false;
+  const size_t lds = tiny_round_lds_bytes(K, B, D, C);
+  return lds <= kTinyMaxLds && lds <= tiny_lds_limit();
+}
+
+hipError_t launch_tiny_round(const TinyArgs& a, hipStream_t s) {
+  if (!tiny_round_fits(a.K, a.B, a.D, a.C, a.H)) return hipErrorInvalidValue;
+  const size_t lds = tiny_round_lds_bytes(a.K, a.B, a.D, a.C);
+  hipError_t e;
+  switch (tiny_classes(a.C)) {
+    case 8:
+      if ((e = allow_lds<8>(lds)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_tiny_round<8>, dim3(1), dim3(kTinyThreads), lds, s, a);
+      break;
+    case 16:
+      if ((e = allow_lds<16>(lds)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_tiny_round<16>, dim3(1), dim3(kTinyThreads), lds, s, a);
+      break;
+    default:
+      if ((e = allow_lds<32>(lds)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_tiny_round<32>, dim3(1), dim3(kTinyThreads), lds, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace lsgd

@@ -155,6 +155,61 @@ def test_softmax_regression_full_run():
     _compare_steps(w, X, y, wk.initial_weights(w), PARAM_TOL_FP32, LOSS_TOL_FP32)
 
 
+def test_softmax_regression_single_launch_rounds():
+    """Workload 1 through lsgd_run_round, which runs each round of softmax
+    regression as one launch (replicas and buffers in LDS): all 50 rounds'
+    averaged models and every step's losses against the oracle."""
+    w = wk.get("softmax_d64")
+    X, y = wk.dataset(w)
+    reps = make_replicas(w, X, y)
+    reps.profile(True)
+    st = O.State(wk.initial_weights(w), w.K)
+    loss = torch.empty(w.H, w.K, device=device())
+    worst = 0.0
+    for t in range(w.rounds):
+        reps.run_round([w.lr] * w.H, loss)
+        want = O.run_round(st, w, X, y, w.H, w.lr)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        e = normwise(reps.read_params(0).cpu().numpy(), st.W[0])
+        worst = max(worst, e)
+        assert e <= PARAM_TOL_FP32, (t, e)
+    print(f"softmax single-launch rounds: worst params {worst:.3e}", flush=True)
+    assert set(reps.profile_report()) == {"tiny_round"}
+
+
+@pytest.mark.parametrize("K,B,nesterov,momentum,sampler", [
+    (5, 70, False, 0.9, "iid"), (3, 20, True, 0.9, "epoch"),
+    (8, 8, False, 0.0, "iid"), (1, 33, True, 0.5, "epoch")])
+def test_single_launch_round_variants(K, B, nesterov, momentum, sampler):
+    """The single-launch round on ragged shapes: more replicas than waves
+    (idle waves in the last slot), batches beyond one wave of rows, both
+    samplers, heavy ball / Nesterov / plain SGD, step sizes changing inside a
+    round; every round against the oracle, and against the step-by-step
+    multi-kernel path within fp32 rounding."""
+    w = _small((24, 7), K=K, B=B, N=600, H=3, rounds=4, momentum=momentum,
+               nesterov=nesterov, lr=0.05).scaled(sampler=sampler)
+    X, y, w0 = _small_data(w, seed=K + B)
+    lrs = [0.05, 0.03, 0.04]
+    a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+    a.profile(True)          # to see which path ran the rounds
+    st = O.State(w0, w.K)
+    loss = torch.empty(3, w.K, device=device())
+    for t in range(4):
+        a.run_round(lrs, loss)
+        for lr in lrs:
+            b.local_step(lr)
+        b.average()
+        want = O.run_round(st, w, X, y, 3, lrs)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        got = a.read_params(0).cpu().numpy()
+        assert normwise(got, st.W[0]) <= PARAM_TOL_FP32, t
+        assert normwise(got, b.read_params(0).cpu().numpy()) <= 1e-6, t
+        for k in range(w.K):
+            assert normwise(a.read_momentum(k).cpu().numpy(), st.U[k]) <= PARAM_TOL_FP32
+    assert a.step == b.step == 12
+    assert set(a.profile_report()) == {"tiny_round"}
+
+
 def test_h1_local_sgd_equals_minibatch_sgd_on_gpu():
     """H = 1 local SGD is mini-batch SGD with batch K * B_loc (the paper's
     special case below eq. 2): the GPU run against the oracle's separately
