@@ -56,3 +56,43 @@ def test_resnet20_full_shape_first_steps():
     print("resnet20 full shape", flush=True)
     _, _, worst = _compare(w, X, y, wk.initial_weights(w), 2, [0, w.K - 1], 1e-5, 1e-3)
     print(f"resnet20 full shape: worst error {worst:.3e}", flush=True)
+
+
+@pytest.mark.parametrize("variant", ["hybrid_epoch", "ef_sign"])
+def test_resnet20_round_with_the_newer_schemes(variant):
+    """ResNet-20 (K = 2, B = 128, a 4096-image subset) for one round of two
+    local steps under hybrid momentum (local 0.9, global 0.3) with the
+    per-epoch reshuffle sampler, and under EF-signSGD: the synchronised
+    model against the oracle (for EF-signSGD, elements whose corrected
+    difference is within the replicas' own fp32 error of zero may take
+    either sign, as on the MLP)."""
+    base = wk.get("resnet20")
+    w = base.scaled(K=2, N=4096, H=2)
+    w = (w.scaled(global_momentum=0.3, sampler="epoch") if variant == "hybrid_epoch"
+         else w.scaled(scheme="ef_sign", nesterov=True))
+    X, y = wk.dataset(base)
+    X, y = np.ascontiguousarray(X[:4096]), np.ascontiguousarray(y[:4096])
+    w0 = wk.initial_weights(w)
+    print(f"resnet20 {variant}", flush=True)
+    reps = make_replicas(w, X, y, w0)
+    st = O.State(w0, w.K)
+    loss = torch.empty(2, w.K, device=device())
+    reps.run_round([w.lr] * 2, loss)
+    want = [O.local_step(st, w, X, y, w.lr) for _ in range(2)]
+    assert np.all(rel(loss.cpu().numpy(), np.stack(want)) <= 1e-4)
+    scale = np.max(np.abs(st.W))
+    if variant == "ef_sign":
+        d = st.w_sync[None] - st.W
+        p = np.abs(d).sum(axis=1) / d.shape[1]
+        amb = np.abs(d) <= 1e-5 * scale
+        allow = (2 * p[:, None] * amb).sum(axis=0) / w.K
+    O.synchronise(st, w, w.lr)
+    got = reps.read_params(0).cpu().numpy()
+    err = np.abs(got - st.W[0])
+    if variant == "ef_sign":
+        assert np.all(err <= 1e-5 * scale + allow)
+        assert np.max(err[allow == 0]) <= 1e-5 * scale
+    else:
+        assert normwise(got, st.W[0]) <= 1e-5
+        u = reps.read_global_momentum().cpu().numpy()
+        assert np.max(np.abs(u - st.u_global)) * w.lr <= 1e-5 * scale
