@@ -154,6 +154,8 @@ Layout make_resnet_layout(const lsgd_config* c) {
     maxpart = std::max(maxpart, (size_t)lsgd::conv_wgrad_splits(c->B_loc, q.Ho, q.Wo) *
                                     K * 9 * q.Cin * q.Cout * 4);
     maxbn = std::max(maxbn, K * lsgd::bn_chunks(c->B_loc * q.Ho * q.Wo) * q.Cout * 2 * 8);
+    // the forward convolutions' statistics: one partial per 256 output rows
+    maxbn = std::max(maxbn, K * ((size_t)c->B_loc * q.Ho * q.Wo / 256 + 1) * q.Cout * 2 * 8);
     maxwt = std::max(maxwt, K * 9 * q.Cin * q.Cout * 4);
   }
   r.featb = take(K * B * 64 * 4);
@@ -615,11 +617,19 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
       g.x = xin;
     }
     g.out = F(q.y);
+    // the convolution writes its BN statistics per 256-row chunk where its
+    // kernel can; otherwise a separate pass reads the output
+    const bool fused = lsgd::conv_fwd_stats(g) && rows(i) % 256 == 0;
+    g.stats = fused ? bnpart : nullptr;
     LSGD_LAUNCH(c, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, s));
     float* mi = mu + (size_t)i * K * 64;
     float* ii = inv + (size_t)i * K * 64;
-    LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
-                                                     mi, ii, s));
+    if (fused)
+      LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_finalize_chunks(bnpart, rows(i) / 256, K,
+                                                                 rows(i), q.Cout, mi, ii, s));
+    else
+      LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
+                                                       mi, ii, s));
     int mode = 0;
     const float* blk_in = nullptr;
     int cin_blk = 0;

@@ -137,9 +137,16 @@ struct ConvGeom {
   const float* Wk;
   long long sW;
   float* out;
+  double* stats;  // forward: BN statistics per 256-row chunk (see conv_fwd_stats)
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
 int conv_wgrad_splits(int Bt, int Ho, int Wo);
+// Whether the forward convolution of q writes its output's BN statistics
+// (per 256-row chunk, [G][R/256][Cout][2] doubles: sum, sum of squares) when
+// q.stats is set; the caller then finalises with launch_bn_finalize_chunks.
+bool conv_fwd_stats(const ConvGeom& q);
+hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
+                                     float* mu, float* inv, hipStream_t st);
 int bn_chunks(int R);
 hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st);
 hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, float* W,

@@ -45,7 +45,21 @@ struct ConvArgs {
   long long sW;          //   group stride
   float* out;            // fwd: y; dgrad: dx; wgrad: partials [S][G][9Cin][Cout]
   int splits, mchunk;    // wgrad split over the m = (b, oh, ow) rows
+  double* stats;         // fwd: per 256-row chunk q of replica g, (sum y, sum y^2)
+                         //   per channel at [g][q][Cout][2], or nullptr
 };
+
+// BN statistics of a forward tile: lane partial sums (s0, s1) of one channel,
+// added over the lanes xor-ed by `mask_bits` (a fixed butterfly), written by
+// the lanes whose masked bits are zero.
+__device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int width_bits,
+                                                int first_bit) {
+  for (int b = 0; b < width_bits; ++b) {
+    const int off = 1 << (first_bit + b);
+    s0 += __shfl_xor(s0, off, 64);
+    s1 += __shfl_xor(s1, off, 64);
+  }
+}
 
 // Pointer to element (m, k) of the forward operand x(m, k), nullptr if the
 // tap falls into the padding.
@@ -372,6 +386,37 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
 
   float* out = c.out + (long long)g * Mg * BN;
+  if constexpr (MODE == CONV_FWD) {
+    // BN statistics of the tile's 256 rows (one chunk; Mg is a multiple of
+    // 256): each wave's 64 rows by a lane butterfly, the four waves in order
+    if (c.stats) {
+      __shared__ double red[4][BN][2];
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) {
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const double y = (double)acc[i][j][v];
+            s0 += y;
+            s1 += y * y;
+          }
+        stats_butterfly(s0, s1, 2, 4);  // the four row groups lq
+        if (lq == 0) {
+          red[wave][j * 16 + lm][0] = s0;
+          red[wave][j * 16 + lm][1] = s1;
+        }
+      }
+      __syncthreads();
+      if (tid < BN) {
+        double* d = c.stats + (((long long)g * (Mg / 256) + m0 / 256) * BN + tid) * 2;
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+          d[e] = ((red[0][tid][e] + red[1][tid][e]) + red[2][tid][e]) + red[3][tid][e];
+      }
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -453,17 +498,41 @@ __global__ __launch_bounds__(kT) void k_conv_stem_fwd(ConvArgs c) {
   }
   stem_stage(T, stem_image(c, g, b));
   float* out = c.out + ((long long)g * c.Bt + b) * kStemSide * kStemSide * kStemCout;
-  // wave w: rows 8w .. 8w+7, two blocks of 16 columns each
-#pragma unroll 2
-  for (int blk = 0; blk < 16; ++blk) {
-    const int h = 8 * wave + (blk >> 1), w = 16 * (blk & 1) + lm;
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  // wave w: rows 8w .. 8w+7 (256 positions: one BN statistics chunk), two
+  // blocks of 16 columns each
+  double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int ch = 0; ch < 4; ++ch) {
 #pragma unroll
-    for (int ks = 0; ks < 7; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[ks], stem_tap(T, 4 * ks + lq, h, w),
-                                                 acc, 0, 0, 0);
-    *(v4f*)(out + (h * kStemSide + 16 * (blk & 1) + lm) * kStemCout + 4 * lq) =
-        v4f{acc[0], acc[1], acc[2], acc[3]};
+    for (int bb = 0; bb < 4; ++bb) {
+      const int blk = 4 * ch + bb;
+      const int h = 8 * wave + (blk >> 1), w = 16 * (blk & 1) + lm;
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 7; ++ks)
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[ks], stem_tap(T, 4 * ks + lq, h, w),
+                                                   acc, 0, 0, 0);
+      *(v4f*)(out + (h * kStemSide + 16 * (blk & 1) + lm) * kStemCout + 4 * lq) =
+          v4f{acc[0], acc[1], acc[2], acc[3]};
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const double y = (double)acc[v];
+        s0[v] += y;
+        s1[v] += y * y;
+      }
+    }
+  }
+  if (c.stats) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) stats_butterfly(s0[v], s1[v], 4, 0);  // the 16 positions
+    if (lm == 0) {
+      const long long q = (long long)b * 4 + wave;
+      double* d = c.stats + ((long long)g * c.Bt * 4 + q) * kStemCout * 2;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        d[(4 * lq + v) * 2] = s0[v];
+        d[(4 * lq + v) * 2 + 1] = s1[v];
+      }
+    }
   }
 }
 
@@ -599,6 +668,34 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
       const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
       out[((long long)row * W + col) * C + lm] = acc[i][v];
     }
+  if (MODE == CONV_FWD && c.stats) {
+    // BN statistics of the band (8 x 32 = 256 positions: one chunk): each
+    // wave's two rows by a lane butterfly, the four waves in order
+    __shared__ double red[4][C][2];
+    double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const double y = (double)acc[i][v];
+        s0 += y;
+        s1 += y * y;
+      }
+    stats_butterfly(s0, s1, 2, 4);
+    if (lq == 0) {
+      red[wave][lm][0] = s0;
+      red[wave][lm][1] = s1;
+    }
+    __syncthreads();
+    if (threadIdx.x < C) {
+      const int t = threadIdx.x;
+      const long long q = (long long)b * bands + band;
+      double* d = c.stats + (((long long)g * c.Bt * bands + q) * C + t) * 2;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+        d[e] = ((red[0][t][e] + red[1][t][e]) + red[2][t][e]) + red[3][t][e];
+    }
+  }
 }
 
 // Weight gradient of the first-stage 16 -> 16 stride-1 convolution (32-wide
@@ -980,6 +1077,7 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
   const int g = blockIdx.x, t = threadIdx.x;
   const int L = kT / C, c = t % C, q = t / C;
   double s0 = 0.0, s1 = 0.0;
+#pragma unroll 8
   for (int ch = q; ch < nchunk; ch += L) {
     const double* p = part + (((long long)g * nchunk + ch) * C + c) * 2;
     s0 += p[0];
@@ -1308,6 +1406,30 @@ static bool stem_shape(const ConvGeom& q) {
          ((uintptr_t)q.out & 15) == 0 && (q.rowmap || q.sx % 4 == 0);
 }
 
+// Row-tiled kernel: reduction channels a multiple of 16, output channels
+// 16 / 32 / 64, 16-byte aligned tensors.
+static bool rows_shape(const ConvGeom& q, int mode) {
+  const int Cr = mode == CONV_FWD ? q.Cin : q.Cout;
+  const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
+  return Cr % 16 == 0 && (Ng == 16 || Ng == 32 || Ng == 64) &&
+         (q.stride == 1 || q.stride == 2) && ((uintptr_t)q.Wk & 15) == 0 && (q.sW % 4 == 0) &&
+         (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0 : ((uintptr_t)q.dy & 15) == 0) &&
+         (mode == CONV_DGRAD || q.rowmap || q.sx % 4 == 0);
+}
+
+// Halo-tile kernel: the first stage's 16 -> 16 stride-1 convolutions.
+static bool halo_shape(const ConvGeom& q, int mode) {
+  return q.Cin == 16 && q.Cout == 16 && q.stride == 1 && q.W == 32 && q.Wo == 32 &&
+         q.H == q.Ho && q.H % 8 == 0 && !q.rowmap && ((uintptr_t)q.Wk & 15) == 0 &&
+         q.sW % 4 == 0 && ((uintptr_t)(mode == CONV_FWD ? q.x : q.dy) & 15) == 0 &&
+         (mode == CONV_DGRAD || q.sx % 4 == 0);
+}
+
+bool conv_fwd_stats(const ConvGeom& q) {
+  if (stem_shape(q) || halo_shape(q, CONV_FWD)) return true;
+  return rows_shape(q, CONV_FWD) && ((long long)q.Bt * q.Ho * q.Wo) % 256 == 0;
+}
+
 int conv_wgrad_splits(int Bt, int Ho, int Wo) {
   const int rows = Bt * Ho * Wo;
   int s = 1;
@@ -1333,6 +1455,7 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   c.Wk = q.Wk;
   c.sW = q.sW;
   c.out = q.out;
+  c.stats = mode == CONV_FWD ? q.stats : nullptr;
   const int Mg = mode == CONV_FWD ? q.Bt * q.Ho * q.Wo
                : mode == CONV_DGRAD ? q.Bt * q.H * q.W : 9 * q.Cin;
   const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
@@ -1381,19 +1504,7 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
     hipLaunchKernelGGL(k_conv_gemm<CONV_WGRAD>, dim3(tiles * c.splits * q.G), dim3(kT),
                        0, st, c, vec);
   } else {
-    // row-tiled kernel: reduction channels a multiple of 16, output channels
-    // 16 / 32 / 64, 16-byte aligned tensors
-    const int Cr = mode == CONV_FWD ? q.Cin : q.Cout;
-    const bool rows = Cr % 16 == 0 && (Ng == 16 || Ng == 32 || Ng == 64) &&
-                      (q.stride == 1 || q.stride == 2) && ((uintptr_t)q.Wk & 15) == 0 &&
-                      (q.sW % 4 == 0) && (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0
-                                                           : ((uintptr_t)q.dy & 15) == 0) &&
-                      (mode == CONV_DGRAD || q.rowmap || q.sx % 4 == 0);
-    const bool halo = q.Cin == 16 && q.Cout == 16 && q.stride == 1 && q.W == 32 &&
-                      q.Wo == 32 && q.H == q.Ho && q.H % 8 == 0 && !q.rowmap &&
-                      ((uintptr_t)q.Wk & 15) == 0 && q.sW % 4 == 0 &&
-                      ((uintptr_t)(mode == CONV_FWD ? q.x : q.dy) & 15) == 0 &&
-                      (mode == CONV_DGRAD || q.sx % 4 == 0);
+    const bool rows = rows_shape(q, mode), halo = halo_shape(q, mode);
     if (mode == CONV_FWD && stem_shape(q)) {
       const long long nb = (long long)q.G * q.Bt;
       if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -1497,6 +1608,19 @@ hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
   else
     hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
                        nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
+                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
+                                     float* mu, float* inv, hipStream_t st) {
+  if (bn_vec_shift(C) >= 0 && C <= kT)
+    hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nchunk, C, R, mu,
+                       inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
+                       1e-5f);
+  else
+    hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
+                       nchunk, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
                        nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
   return hipGetLastError();
 }
