@@ -164,7 +164,7 @@ Layout make_resnet_layout(const lsgd_config* c) {
   for (int i = 0; i < 4; ++i) r.gbuf[i] = take(maxact);
   r.mu = take(kResConvs * K * 64 * 4);
   r.inv = take(kResConvs * K * 64 * 4);
-  r.coef = take(K * 64 * 3 * 4);
+  r.coef = take(K * 64 * 5 * 4);
   r.bnpart = take(maxbn);
   r.wpart = take(maxpart);
   r.wt = take(maxwt);
@@ -737,8 +737,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1]));
     LSGD_LAUNCH(c, "conv_dgrad", dgrad(ib, gb[1], gb[2]));
     LSGD_LAUNCH(c, "conv_wgrad", wgrad(ib, F(r.cv[ia].act), gb[1]));
-    // first convolution: ReLU'd BN output
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], F(r.cv[ia].act), gb[1]));
+    // first convolution: ReLU'd BN output, the mask recomputed from its input
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[1]));
     LSGD_LAUNCH(c, "conv_dgrad", dgrad(ia, gb[1], gb[nxt]));
     LSGD_LAUNCH(c, "conv_wgrad", wgrad(ia, h_in, gb[1]));
     // the shortcut's share of the block-output gradient
@@ -748,7 +748,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                            qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
     cur = nxt;
   }
-  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], F(r.cv[0].act), gb[1]));
+  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1]));
   LSGD_LAUNCH(c, "conv_wgrad", wgrad(0, nullptr, gb[1]));
   c->step += 1;
   return LSGD_OK;

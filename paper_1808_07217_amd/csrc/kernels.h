@@ -160,6 +160,10 @@ hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
                            int Cin, float* out, hipStream_t st);
+// BN backward with the gamma/beta step: the upstream gradient gup is masked
+// by maskv > 0 (the post-ReLU activation) or, with maskv null, by the sign of
+// the recomputed pre-ReLU BN output (a BN-ReLU with no shortcut add). coef
+// holds 5 floats per (replica, channel).
 hipError_t launch_bn_backward(const float* y, const float* gup, const float* maskv,
                               int G, int R, int C, double* part, const float* mu,
                               const float* inv, float* coef, float* gamma, float* beta,

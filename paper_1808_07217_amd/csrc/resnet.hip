@@ -963,14 +963,27 @@ __global__ void k_conv_wt(const float* W, long long sP, int G, int Cin, int Cout
 // ------------------------------------------------------------ batch norm
 // Partial sums of one row chunk per workgroup, fp64: for the forward pass
 // sum(y) and sum(y^2); for the backward pass sum(dz) and sum(dz * xhat),
-// where dz = upstream gradient (masked by `maskv > 0` when given) and
+// where dz = upstream gradient masked by the ReLU derivative -- `maskv > 0`
+// when given, else bn_z(gamma, y, mu, inv, beta) > 0 -- and
 // xhat = (y - mu) * inv. Channel count C divides 256.
 constexpr int kChunkRows = 1024;
+
+// The shifted, scaled BN output z = gamma * (y - mu) * inv + beta in one fixed
+// rounding order: the forward pass takes relu(z) (+ the shortcut) with it, and
+// the backward pass of a convolution followed by BN-ReLU alone recomputes the
+// ReLU mask z > 0 with it instead of reading the activation back.
+__device__ __forceinline__ float bn_z(float gm, float y, float m, float iv, float bt) {
+  return __builtin_fmaf(gm * (y - m), iv, bt);
+}
+// Backward coefficients per (replica g, channel c), field f at
+// coef[f * G * C + g * C + c]: gamma * inv, dbeta / R, dgamma / R, and gamma,
+// beta as they were before this step's update.
 
 __global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
                                                    const float* gup, const float* maskv,
                                                    const float* mu, const float* inv,
-                                                   double* part, int nchunk) {
+                                                   const float* gamma, const float* beta,
+                                                   long long sP, double* part, int nchunk) {
   __shared__ double red[2][kT];
   const int g = blockIdx.y, ch = blockIdx.x;
   const int c = threadIdx.x % C, lane_r = threadIdx.x / C, rstep = kT / C;
@@ -978,6 +991,9 @@ __global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
   const int r0 = ch * kChunkRows, r1 = min(R, r0 + kChunkRows);
   const bool bwd = gup != nullptr;
   const float m_c = bwd ? mu[g * C + c] : 0.f, i_c = bwd ? inv[g * C + c] : 0.f;
+  const bool zmask = bwd && maskv == nullptr;
+  const float g_c = zmask ? gamma[(long long)g * sP + c] : 0.f;
+  const float b_c = zmask ? beta[(long long)g * sP + c] : 0.f;
   double s0 = 0.0, s1 = 0.0;
   for (int rb = r0 + lane_r; rb < r1; rb += 4 * rstep) {
     float yv[4], gv[4], mv[4];
@@ -996,7 +1012,8 @@ __global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
         s0 += (double)yv[u];
         s1 += (double)yv[u] * (double)yv[u];
       } else {
-        const float dz = mv[u] > 0.f ? gv[u] : 0.f;
+        const bool on = zmask ? bn_z(g_c, yv[u], m_c, i_c, b_c) > 0.f : mv[u] > 0.f;
+        const float dz = on ? gv[u] : 0.f;
         const float xh = (yv[u] - m_c) * i_c;
         s0 += (double)dz;
         s1 += (double)dz * (double)xh;
@@ -1024,7 +1041,8 @@ __global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
 // Backward: the input-gradient coefficients and the update of gamma, beta:
 //   dbeta = sum dz, dgamma = sum dz*xhat,
 //   dy = gamma*inv*(dz - dbeta/R - xhat*dgamma/R)  -> coef = (gamma*inv,
-//   dbeta/R, dgamma/R); then gamma, beta take a momentum-SGD step (no decay).
+//   dbeta/R, dgamma/R, gamma, beta); then gamma, beta take a momentum-SGD step
+//   (no decay).
 __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int R,
                               float* mu, float* inv, float* coef, float* gamma,
                               float* beta, float* ug, float* ub, long long sP,
@@ -1048,9 +1066,12 @@ __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int 
   }
   const long long o = (long long)g * sP + c;
   float gm = gamma[o], bt = beta[o];
-  coef[i * 3 + 0] = gm * inv[i];
-  coef[i * 3 + 1] = (float)(s0 / R);
-  coef[i * 3 + 2] = (float)(s1 / R);
+  const int GC = G * C;
+  coef[i] = gm * inv[i];
+  coef[GC + i] = (float)(s0 / R);
+  coef[2 * GC + i] = (float)(s1 / R);
+  coef[3 * GC + i] = gm;
+  coef[4 * GC + i] = bt;
   float u = ug[o];
   const float dgm = (float)s1;
   u = __builtin_fmaf(mom, u, dgm);
@@ -1107,9 +1128,12 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
   }
   const long long o = (long long)g * sP + c;
   float gm = gamma[o], bt = beta[o];
-  coef[i * 3 + 0] = gm * inv[i];
-  coef[i * 3 + 1] = (float)(s0 / R);
-  coef[i * 3 + 2] = (float)(s1 / R);
+  const int GC = (int)gridDim.x * C;
+  coef[i] = gm * inv[i];
+  coef[GC + i] = (float)(s0 / R);
+  coef[2 * GC + i] = (float)(s1 / R);
+  coef[3 * GC + i] = gm;
+  coef[4 * GC + i] = bt;
   float u = ug[o];
   const float dgm = (float)s1;
   u = __builtin_fmaf(mom, u, dgm);
@@ -1138,8 +1162,8 @@ __global__ void k_bn_apply(const float* y, int R, int C, const float* mu,
     const int c = (int)(i % C);
     const long long r = i / C;
     const int g = (int)(r / R);
-    const float z = gamma[(long long)g * sP + c] * (y[i] - mu[g * C + c]) * inv[g * C + c] +
-                    beta[(long long)g * sP + c];
+    const float z = bn_z(gamma[(long long)g * sP + c], y[i], mu[g * C + c], inv[g * C + c],
+                         beta[(long long)g * sP + c]);
     float v = z;
     if (mode == 1) {
       v += xin[i];
@@ -1159,7 +1183,8 @@ __global__ void k_bn_apply(const float* y, int R, int C, const float* mu,
 }
 
 // dy = coef0 * (dz - coef1 - xhat * coef2) with dz = gup masked by maskv > 0
-// and xhat = (y - mu) * inv.
+// (without maskv: by bn_z > 0 from the pre-update gamma, beta in coef) and
+// xhat = (y - mu) * inv.
 __global__ void k_bn_bwd_apply(const float* y, const float* gup, const float* maskv,
                                int R, int C, int G, const float* mu, const float* inv,
                                const float* coef, float* dy) {
@@ -1169,9 +1194,13 @@ __global__ void k_bn_bwd_apply(const float* y, const float* gup, const float* ma
     const int c = (int)(i % C);
     const int g = (int)(i / ((long long)R * C));
     const int gc = g * C + c;
-    const float dz = maskv[i] > 0.f ? gup[i] : 0.f;
+    const long long GC = (long long)G * C;
+    const float* cf = coef + gc;
+    const bool on = maskv ? maskv[i] > 0.f
+                          : bn_z(cf[3 * GC], y[i], mu[gc], inv[gc], cf[4 * GC]) > 0.f;
+    const float dz = on ? gup[i] : 0.f;
     const float xh = (y[i] - mu[gc]) * inv[gc];
-    dy[i] = coef[gc * 3] * (dz - coef[gc * 3 + 1] - xh * coef[gc * 3 + 2]);
+    dy[i] = cf[0] * (dz - cf[GC] - xh * cf[2 * GC]);
   }
 }
 
@@ -1186,7 +1215,9 @@ __global__ void k_bn_bwd_apply(const float* y, const float* gup, const float* ma
 __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C,
                                                     const float* gup, const float* maskv,
                                                     const float* mu, const float* inv,
-                                                    double* part, int nchunk) {
+                                                    const float* gamma, const float* beta,
+                                                    long long sP, double* part,
+                                                    int nchunk) {
   __shared__ double red[2][4][kT];
   const int g = blockIdx.y, ch = blockIdx.x;
   const int cq = C / 4;  // threads per row
@@ -1194,11 +1225,14 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
   const long long base = (long long)g * R * C;
   const int r0 = ch * kChunkRows, r1 = min(R, r0 + kChunkRows);
   const bool bwd = gup != nullptr;
-  float m_c[4], i_c[4];
+  const bool zmask = bwd && maskv == nullptr;
+  float m_c[4], i_c[4], g_c[4], b_c[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     m_c[e] = bwd ? mu[g * C + c0 + e] : 0.f;
     i_c[e] = bwd ? inv[g * C + c0 + e] : 0.f;
+    g_c[e] = zmask ? gamma[(long long)g * sP + c0 + e] : 0.f;
+    b_c[e] = zmask ? beta[(long long)g * sP + c0 + e] : 0.f;
   }
   double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
   for (int rb = r0 + lane_r; rb < r1; rb += 4 * rstep) {
@@ -1210,6 +1244,10 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
       yv[u] = *(const v4f*)(y + o);
       gv[u] = bwd ? *(const v4f*)(gup + o) : v4f{0.f, 0.f, 0.f, 0.f};
       mv[u] = maskv ? *(const v4f*)(maskv + o) : v4f{1.f, 1.f, 1.f, 1.f};
+      if (zmask) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mv[u][e] = bn_z(g_c[e], yv[u][e], m_c[e], i_c[e], b_c[e]);
+      }
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -1254,7 +1292,9 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
   }
 }
 
-// k_bn_apply, 4 channels per thread.
+// k_bn_apply, 4 channels per thread; mu, inv (and gamma, beta when PV) read
+// as float4.
+template <bool PV>
 __global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, int cshift,
                                                   const float* mu, const float* inv,
                                                   const float* gamma, const float* beta,
@@ -1276,13 +1316,22 @@ __global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, 
     xv = *(const v4f*)(xin + (((long long)g * Bt + b) * H * W + (long long)(2 * oh) * W +
                               2 * ow) * Cin + c0);
   }
+  const v4f m4 = *(const v4f*)(mu + g * C + c0), i4 = *(const v4f*)(inv + g * C + c0);
+  v4f g4, b4;
+  if constexpr (PV) {
+    g4 = *(const v4f*)(gamma + (long long)g * sP + c0);
+    b4 = *(const v4f*)(beta + (long long)g * sP + c0);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      g4[e] = gamma[(long long)g * sP + c0 + e];
+      b4[e] = beta[(long long)g * sP + c0 + e];
+    }
+  }
   v4f res;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const int c = c0 + e;
-    const float z = gamma[(long long)g * sP + c] * (yv[e] - mu[g * C + c]) * inv[g * C + c] +
-                    beta[(long long)g * sP + c];
-    const float v = z + xv[e];
+    const float v = bn_z(g4[e], yv[e], m4[e], i4[e], b4[e]) + xv[e];
     res[e] = v > 0.f ? v : 0.f;
   }
   *(v4f*)(out + o) = res;
@@ -1298,15 +1347,25 @@ __global__ __launch_bounds__(kT) void k_bn_bwd_apply4(const float* y, const floa
   if (j >= R * C / 4) return;
   const int e4 = 4 * j, c0 = e4 & (C - 1);
   const long long o = (long long)g * R * C + e4;
-  const v4f yv = *(const v4f*)(y + o), gv = *(const v4f*)(gup + o),
-            mv = *(const v4f*)(maskv + o);
+  const int gc = g * C + c0, GC = (int)gridDim.y * C;
+  const v4f yv = *(const v4f*)(y + o), gv = *(const v4f*)(gup + o);
+  const v4f m4 = *(const v4f*)(mu + gc), i4 = *(const v4f*)(inv + gc);
+  const v4f k0 = *(const v4f*)(coef + gc), k1 = *(const v4f*)(coef + GC + gc),
+            k2 = *(const v4f*)(coef + 2 * GC + gc);
+  v4f mv;
+  if (maskv) {
+    mv = *(const v4f*)(maskv + o);
+  } else {
+    const v4f k3 = *(const v4f*)(coef + 3 * GC + gc), k4 = *(const v4f*)(coef + 4 * GC + gc);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mv[e] = bn_z(k3[e], yv[e], m4[e], i4[e], k4[e]);
+  }
   v4f res;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const int gc = g * C + c0 + e;
     const float dz = mv[e] > 0.f ? gv[e] : 0.f;
-    const float xh = (yv[e] - mu[gc]) * inv[gc];
-    res[e] = coef[gc * 3] * (dz - coef[gc * 3 + 1] - xh * coef[gc * 3 + 2]);
+    const float xh = (yv[e] - m4[e]) * i4[e];
+    res[e] = k0[e] * (dz - k1[e] - xh * k2[e]);
   }
   *(v4f*)(dy + o) = res;
 }
@@ -1597,10 +1656,10 @@ hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
   const int nch = bn_chunks(R);
   if (bn_vec_shift(C) >= 0 && al16p(y) && (long long)R * C < (1LL << 31) && G <= 65535)
     hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
-                       nullptr, nullptr, nullptr, part, nch);
+                       nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, part, nch);
   else
     hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
-                       nullptr, nullptr, nullptr, part, nch);
+                       nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, part, nch);
   if (bn_vec_shift(C) >= 0 && C <= kT)
     hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R, mu,
                        inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
@@ -1630,10 +1689,15 @@ hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
                            int Cin, float* out, hipStream_t st) {
   const int cs = bn_vec_shift(C);
-  if (cs >= 0 && al16p(y) && al16p(out) && al16p(xin) && Cin % 4 == 0 &&
-      (long long)R * C < (1LL << 31) && G <= 65535) {
-    hipLaunchKernelGGL(k_bn_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0, st,
-                       y, R, C, cs, mu, inv, gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
+  if (cs >= 0 && al16p(y) && al16p(out) && al16p(xin) && al16p(mu) && al16p(inv) &&
+      Cin % 4 == 0 && (long long)R * C < (1LL << 31) && G <= 65535) {
+    const dim3 grid((R * C / 4 + kT - 1) / kT, G);
+    if (sP % 4 == 0 && al16p(gamma) && al16p(beta))
+      hipLaunchKernelGGL(k_bn_apply4<true>, grid, dim3(kT), 0, st, y, R, C, cs, mu, inv,
+                         gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
+    else
+      hipLaunchKernelGGL(k_bn_apply4<false>, grid, dim3(kT), 0, st, y, R, C, cs, mu, inv,
+                         gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_bn_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0, st,
@@ -1648,14 +1712,14 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
                               int nesterov, float* dy, hipStream_t st) {
   const int nch = bn_chunks(R);
   const bool v4 = bn_vec_shift(C) >= 0 && al16p(y) && al16p(gup) && al16p(maskv) &&
-                  al16p(dy) && maskv != nullptr && (long long)R * C < (1LL << 31) &&
-                  G <= 65535;
+                  al16p(dy) && al16p(mu) && al16p(inv) && al16p(coef) &&
+                  (long long)R * C < (1LL << 31) && G <= 65535;
   if (v4)
     hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
-                       mu, inv, part, nch);
+                       mu, inv, gamma, beta, sP, part, nch);
   else
     hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
-                       mu, inv, part, nch);
+                       mu, inv, gamma, beta, sP, part, nch);
   if (bn_vec_shift(C) >= 0 && C <= kT)
     hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
                        (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
