@@ -527,6 +527,150 @@ __global__ __launch_bounds__(256) void k_head_fwd_vec(HeadArgs h) {
   }
 }
 
+// bf16 form: the bf16 copy of W_L and bf16 activations, a class count C
+// fixed at compile time and D = 512 NJ. The replica's W_L ([D][C] bf16, D C / 8
+// 16-byte words) is copied into LDS unchanged, every word loaded before the
+// first is stored; lane l of a wave owns inputs d = 512 j + 8 l .. +7 of two
+// sample rows, loaded in the same batch. The logits, the loss, dZ and the
+// masked input gradient then need no further global read. Formulas and
+// rounding points (dZ and the input gradient rounded to bf16) are those of
+// k_head_fwd; each lane adds its inputs in ascending d before the xor
+// butterfly.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) {
+  return __uint_as_float(w & 0xFFFF0000u);
+}
+__device__ __forceinline__ float bf16_at(const uint4& v, int e) {
+  const uint32_t w = e < 2 ? v.x : (e < 4 ? v.y : (e < 6 ? v.z : v.w));
+  return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+}
+
+template <int C, int NJ>
+__global__ __launch_bounds__(256) void k_head_fwd_bf16(HeadArgs h) {
+  constexpr int RPW = 2;
+  constexpr int D = 512 * NJ;
+  constexpr int WV = D * C / 8;            // 16-byte words of W_L
+  constexpr int WPT = (WV + 255) / 256;    // per thread
+  __shared__ uint4 Ws[WV];
+  const int k = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint4* Wg = (const uint4*)((const bf16_t*)h.W + (long long)k * h.sW);
+  uint4 wv[WPT];
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int i = u * 256 + (int)threadIdx.x;
+    wv[u] = i < WV ? Wg[i] : make_uint4(0u, 0u, 0u, 0u);
+  }
+  long long rr[RPW];
+  bool live[RPW];
+  uint4 a[RPW][NJ];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int row = (blockIdx.x * 4 + wave) * RPW + q;
+    live[q] = row < h.B;
+    rr[q] = (long long)k * h.B + (live[q] ? row : 0);
+    const bf16_t* arow = (const bf16_t*)h.A + (long long)k * h.sA +
+                         (long long)(live[q] ? row : 0) * D;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) a[q][j] = *(const uint4*)(arow + 512 * j + 8 * lane);
+  }
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int i = u * 256 + (int)threadIdx.x;
+    if (i < WV) Ws[i] = wv[u];
+  }
+  __syncthreads();
+  // W_L[d][c] for the lane's d = 512 j + 8 l + t: element t C + c of the C
+  // words starting at word (64 j + l) C
+  float z[RPW][C];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q)
+#pragma unroll
+    for (int c = 0; c < C; ++c) z[q][c] = 0.f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    uint4 w[C];
+#pragma unroll
+    for (int v = 0; v < C; ++v) w[v] = Ws[(64 * j + lane) * C + v];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const int e = t * C + c;
+        const float wdc = bf16_at(w[e / 8], e % 8);
+#pragma unroll
+        for (int q = 0; q < RPW; ++q)
+          z[q][c] = __builtin_fmaf(bf16_at(a[q][j], t), wdc, z[q][c]);
+      }
+    __builtin_amdgcn_sched_barrier(0);  // one slice of W_L in registers at a time
+  }
+  const float* bias = h.bias + (long long)k * h.sP;
+  const float invB = 1.0f / (float)h.B;
+  float dz[RPW][C];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+#pragma unroll
+    for (int c = 0; c < C; ++c) z[q][c] = wave_sum(z[q][c]) + bias[c];
+    const int lab = h.y[h.rowmap[rr[q]]];
+    float m = z[q][0];
+#pragma unroll
+    for (int c = 1; c < C; ++c) m = fmaxf(m, z[q][c]);
+    float sum = 0.f, rest = 0.f, zy = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float e = __expf(z[q][c] - m);
+      sum += e;
+      if (c != lab) rest += e;
+      else zy = z[q][c];
+    }
+    const float loss = zy >= m ? log1pf(rest) : (m - zy) + logf(sum);
+    const float inv_s = 1.0f / sum;
+    float mine = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float p = __expf(z[q][c] - m) * inv_s;
+      dz[q][c] = round_like((p - (c == lab ? 1.f : 0.f)) * invB, (const bf16_t*)nullptr);
+      if (c == lane) mine = dz[q][c];
+    }
+    if (live[q]) {
+      if (lane < C) ((bf16_t*)h.dZ)[rr[q] * C + lane] = f32_to_bf16(mine);
+      if (lane == 0) h.rowloss[rr[q]] = loss;
+    }
+  }
+  if (!h.dZprev) return;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    uint4 w[C];
+#pragma unroll
+    for (int v = 0; v < C; ++v) w[v] = Ws[(64 * j + lane) * C + v];
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      if (!live[q]) continue;
+      uint32_t o[4];
+#pragma unroll
+      for (int t2 = 0; t2 < 4; ++t2) {
+        uint32_t pair = 0u;
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+          const int t = 2 * t2 + hb;
+          float acc = 0.f;
+#pragma unroll
+          for (int c = 0; c < C; ++c) {
+            const int e = t * C + c;
+            acc = __builtin_fmaf(dz[q][c], bf16_at(w[e / 8], e % 8), acc);
+          }
+          const float out = (h.nomask || bf16_at(a[q][j], t) > 0.f) ? acc : 0.f;
+          pair |= (uint32_t)f32_to_bf16(out) << (16 * hb);
+        }
+        o[t2] = pair;
+      }
+      *(uint4*)((bf16_t*)h.dZprev + rr[q] * D + 512 * j + 8 * lane) =
+          make_uint4(o[0], o[1], o[2], o[3]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 template <typename T, int CMAX>
 hipError_t launch_pair(const HeadArgs& h, hipStream_t s, int which) {
   const bool gather = h.gather != 0;  // the top layer is layer 1
@@ -560,6 +704,19 @@ hipError_t launch_head(int dtype, const HeadArgs& h, hipStream_t s, int which) {
       hipLaunchKernelGGL((k_head_fwd_vec<10, 1>), grid, dim3(256), 0, s, h);
     else
       hipLaunchKernelGGL((k_head_fwd_vec<10, 2>), grid, dim3(256), 0, s, h);
+    return hipGetLastError();
+  }
+  // the same for bf16 operands, D a multiple of 512 up to 2048
+  if (which == 0 && dtype == 1 && !h.gather && h.C == 10 && h.D % 512 == 0 &&
+      h.D <= 2048 && h.sA % 8 == 0 && h.sW % 8 == 0 && al16(h.A) && al16(h.W) &&
+      (h.dZprev == nullptr || al16(h.dZprev))) {
+    dim3 grid((h.B + 7) / 8, h.K);
+    switch (h.D / 512) {
+      case 1: hipLaunchKernelGGL((k_head_fwd_bf16<10, 1>), grid, dim3(256), 0, s, h); break;
+      case 2: hipLaunchKernelGGL((k_head_fwd_bf16<10, 2>), grid, dim3(256), 0, s, h); break;
+      case 3: hipLaunchKernelGGL((k_head_fwd_bf16<10, 3>), grid, dim3(256), 0, s, h); break;
+      default: hipLaunchKernelGGL((k_head_fwd_bf16<10, 4>), grid, dim3(256), 0, s, h); break;
+    }
     return hipGetLastError();
   }
   // one-round-trip weight gradient: fp32, up to 16 classes, 64-input slices

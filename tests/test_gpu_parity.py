@@ -138,7 +138,10 @@ def test_persistent_update_kernel_bf16(widths, K, B):
 
 
 @pytest.mark.parametrize("widths", [(70, 48, 36, 10), (64, 128, 64, 10),
-                                    (72, 20), (40, 33, 45)])
+                                    (72, 20), (40, 33, 45),
+                                    # 10 classes over 512 / 1536 bf16 inputs:
+                                    # the head forward with W_L in LDS
+                                    (48, 512, 10), (40, 64, 1536, 10)])
 def test_small_mlp_bf16_every_step(widths):
     w = _small(widths, dtype="bf16")
     print(f"small bf16 {widths}", flush=True)
