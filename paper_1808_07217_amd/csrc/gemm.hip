@@ -531,6 +531,155 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GemmArgs a, int vecA,
   if (do_bias && tid < BN && n0 + tid < N) bias_update(a, t, n0 + tid, colsum);
 }
 
+// Two k halves per workgroup (fp32, A not transposed, whole tiles, no update
+// epilogue): 512 threads, threads 256 h .. 256 h + 255 run gemm_f32's FULL
+// pipeline over half h of the workgroup's k range (an even number of BK
+// slabs) with an LDS ring of their own. Each SIMD then holds two MFMA
+// wavefronts, one per half, and one's LDS and barrier waits are covered by
+// the other's MFMAs. At the end half 1 hands its accumulators over through
+// LDS and half 0 forms (first half) + (second half) and runs the epilogue.
+template <bool BT, int EPI, bool GATHER, int BM, int BN, int BK>
+__global__ __launch_bounds__(2 * kThreads) void gemm_f32_kh2(GemmArgs a) {
+  constexpr int PA = BM + 2;  // As[k][m], transposing stores
+  constexpr int PB = BT ? BN + 2 : BN + 4;
+  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  constexpr int KV = BK / 4;
+  constexpr int NA = BM * BK / 4 / kThreads, NB = BN * BK / 4 / kThreads;
+  static_assert(NA >= 1 && NB >= 1, "tile too small for 256 threads per half");
+  constexpr int HALF = 2 * BK * (PA + PB);  // floats of one half's ring
+  constexpr int XCH = BM * BN;              // accumulator hand-over
+  __shared__ __attribute__((aligned(16))) float smem[2 * HALF > XCH ? 2 * HALF : XCH];
+  const int h = threadIdx.x >> 8, tid = threadIdx.x & (kThreads - 1);
+  auto As = reinterpret_cast<float (*)[BK][PA]>(smem + h * HALF);
+  auto Bs = reinterpret_cast<float (*)[BK][PB]>(smem + h * HALF + 2 * BK * PA);
+
+  const Tile t = decode_tile(a, BM, BN);
+  const int g = t.g, m0 = t.m0, n0 = t.n0;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
+  const float* A = (const float*)a.A + (long long)g * a.sA;
+  const float* B = (const float*)a.B + (long long)g * a.sB;
+  const int32_t* rmap = GATHER ? a.rowmap + (long long)g * a.sRow : nullptr;
+  const int nk = a.kchunk / BK / 2;  // slabs per half
+  const int kbeg = t.s * a.kchunk + h * nk * BK;
+
+  long long srow[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int row = m0 + (tid + i * kThreads) / KV;
+    srow[i] = GATHER ? rmap[row] : row;
+  }
+  auto gload = [&](int k0, float4(&xa)[NA], float4(&xb)[NB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int q = tid + i * kThreads;
+      xa[i] = ldg4(A + srow[i] * a.lda + k0 + (q % KV) * 4);
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int q = tid + i * kThreads;
+      if constexpr (BT)
+        xb[i] = ldg4(B + (long long)(n0 + q / KV) * a.ldb + k0 + (q % KV) * 4);
+      else
+        xb[i] = ldg4(B + (long long)(k0 + q / (BN / 4)) * a.ldb + n0 + (q % (BN / 4)) * 4);
+    }
+  };
+  auto lstore = [&](int buf, const float4(&xa)[NA], const float4(&xb)[NB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int q = tid + i * kThreads;
+      const int r = q / KV, kq = (q % KV) * 4;
+      As[buf][kq + 0][r] = xa[i].x;
+      As[buf][kq + 1][r] = xa[i].y;
+      As[buf][kq + 2][r] = xa[i].z;
+      As[buf][kq + 3][r] = xa[i].w;
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int q = tid + i * kThreads;
+      if constexpr (BT) {
+        const int r = q / KV, kq = (q % KV) * 4;
+        Bs[buf][kq + 0][r] = xb[i].x;
+        Bs[buf][kq + 1][r] = xb[i].y;
+        Bs[buf][kq + 2][r] = xb[i].z;
+        Bs[buf][kq + 3][r] = xb[i].w;
+      } else {
+        const int r = q / (BN / 4), c = (q % (BN / 4)) * 4;
+        sts4(&Bs[buf][r][c], xb[i]);
+      }
+    }
+  };
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  const int lk = lane >> 5, lr = lane & 31;
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 2) {
+      float av[FM], bv[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) av[i] = As[buf][kk + lk][wm0 + i * 32 + lr];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bv[j] = Bs[buf][kk + lk][wn0 + j * 32 + lr];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  };
+  // slab t of this half: LDS buffer t % 2, register set t % 2; prefetches
+  // past the last slab reload it (unused)
+  float4 ra0[NA], rb0[NB], ra1[NA], rb1[NB];
+  auto slab = [&](int s) __attribute__((always_inline)) { return kbeg + min(s, nk - 1) * BK; };
+  gload(slab(0), ra0, rb0);
+  gload(slab(1), ra1, rb1);
+  lstore(0, ra0, rb0);
+  __syncthreads();
+  int it = 0;
+  for (; it + 1 < nk; it += 2) {
+    gload(slab(it + 2), ra0, rb0);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(0);
+    lstore(1, ra1, rb1);
+    __syncthreads();
+    gload(slab(it + 3), ra1, rb1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);
+    lstore(0, ra0, rb0);
+    __syncthreads();
+  }
+  if (it < nk) compute(0);  // odd slab count per half: the last is in buffer 0
+
+  // hand-over: register v of block (i, j) of wave w and lane l at
+  // ((((w FM + i) FN + j) 16 + v) 64 + l)
+  __syncthreads();  // both halves' operand reads are done
+  if (h == 1) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          smem[(((wave * FM + i) * FN + j) * 16 + v) * 64 + lane] = acc[i][j][v];
+  }
+  __syncthreads();
+  if (h == 1) return;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        acc[i][j][v] += smem[(((wave * FM + i) * FN + j) * 16 + v) * 64 + lane];
+  epilogue_fragment<EPI, false, FM, FN>(a, t, acc, m0 + wm0, n0 + wn0, lk, lr);
+}
+
+
 // ------------------------------------------------- fp32 update, specialised
 // Fused weight gradient + momentum-SGD update over the 128 x 128 tiles of one
 // or several layers (a list of problems whose tiles are concatenated). A
@@ -1302,7 +1451,22 @@ hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
       return launch_reduce<EPI, OUTBF_ACT>(a, s);
     }
   }
-  if (dtype == 1)
+  // two k halves per workgroup (an even number of slabs per split)
+  bool kh2 = false;
+  if constexpr (!AT && EPI != EPI_SGD) {
+    const int bk = big ? kBigFullBK<EPI> : 32;
+    kh2 = dtype == 0 && full(a, BM, bk, vecA, vecB, vecC) && a.kchunk >= 2 * bk &&
+          a.kchunk % (2 * bk) == 0;
+    if (kh2 && big)
+      hipLaunchKernelGGL((gemm_f32_kh2<BT, EPI, GATHER, 128, 128, kBigFullBK<EPI>>),
+                         dim3(total), dim3(2 * kThreads), 0, s, a);
+    else if (kh2)
+      hipLaunchKernelGGL((gemm_f32_kh2<BT, EPI, GATHER, 64, 64, 32>), dim3(total),
+                         dim3(2 * kThreads), 0, s, a);
+  }
+  if (kh2)
+    ;
+  else if (dtype == 1)
     hipLaunchKernelGGL((gemm_bf16<AT, BT, EPI, GATHER, 64, 64>), dim3(total),
                        dim3(kThreads), 0, s, a, vecA, vecB, vecC);
   else if (big && full(a, 128, kBigFullBK<EPI>, vecA, vecB, vecC))

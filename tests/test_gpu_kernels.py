@@ -94,6 +94,29 @@ def test_grouped_gemm_error_bound(dtype, ta, tb, shape, splits):
     assert np.all(np.abs(C - ref) <= bound), np.max(np.abs(C - ref) / bound)
 
 
+# whole-tile fp32 shapes with an even number of k slabs per split: the
+# kernel with two k halves per workgroup (64 x 64 tiles with 32-deep slabs,
+# or 128 x 128 tiles with 16-deep slabs once the inner dimension reaches
+# 2048), including an odd slab count per half (192 = 2 x 3 x 32)
+@pytest.mark.parametrize("tb", [0, 1])
+@pytest.mark.parametrize("shape,splits", [((16, 128, 512, 512), 1), ((16, 128, 512, 512), 2),
+                                          ((2, 64, 128, 192), 1), ((2, 256, 256, 3072), 1),
+                                          ((2, 128, 256, 2048), 4)])
+def test_grouped_gemm_two_k_halves(shape, splits, tb):
+    L = _lsgd()
+    G, M, N, Kd = shape
+    print(f"gemm two k halves {shape} splits={splits} tb={tb}", flush=True)
+    rng = np.random.default_rng(G + M + N + Kd + splits + tb)
+    A = rng.standard_normal((G, M, Kd)).astype(np.float32)
+    B = rng.standard_normal((G, N, Kd) if tb else (G, Kd, N)).astype(np.float32)
+    C = L.grouped_gemm(to_dev(A), to_dev(B), False, bool(tb), splits=splits)
+    C = C.cpu().numpy().astype(np.float64)
+    opB = B.astype(np.float64).transpose(0, 2, 1) if tb else B.astype(np.float64)
+    ref = A.astype(np.float64) @ opB
+    bound = gamma(Kd + 1) * (np.abs(A.astype(np.float64)) @ np.abs(opB)) + 1e-30
+    assert np.all(np.abs(C - ref) <= bound), np.max(np.abs(C - ref) / bound)
+
+
 # ------------------------------------------------------------------ average
 def _tree_f32(rows):
     """The kernel's documented order in fp32: split at the largest power of
