@@ -241,9 +241,12 @@ def sweep():
         }), flush=True)
 
 
-def cpu_baseline(w, X, y, w0):
-    """The CPU oracle (as it is) on one full round of the workload: H local
-    steps on all K replicas plus the average, on this host's cores."""
+def cpu_baseline(w, X, y, w0, min_seconds: float = 10.0):
+    """The CPU oracle (as it is) on a bounded sample of the workload, repeated
+    until about `min_seconds` of CPU work: whole rounds (H local steps on all
+    K replicas plus the synchronisation) where one takes a few seconds; one
+    local step of replica 0 where a round would take minutes (ResNet-20, the
+    2048-wide MLP)."""
     from oracle import lsgd_oracle as O
     threads = None
     try:
@@ -253,23 +256,38 @@ def cpu_baseline(w, X, y, w0):
     except Exception:
         threads = os.cpu_count()
     st = O.State(w0, w.K)
-    t0 = time.perf_counter()
-    if w.Kb > 0:
-        O.run_hierarchical_round(st, w, X, y, w.H, w.Hb, w.Kb, w.lr)
-        what = (f"H^b={w.Hb} x (H={w.H} local steps on all K={w.K} replicas "
+    per_step = w.model == "resnet20" or w.dtype == "bf16"
+    if per_step:
+        what = f"one local step of replica 0 ({w.B_loc} samples)"
+        unit = w.B_loc
+    elif w.Kb > 0:
+        what = (f"one round: H^b={w.Hb} x (H={w.H} local steps on all K={w.K} replicas "
                 f"+ block average over K'={w.Kb}) + global average")
+        unit = w.K * w.H * w.Hb * w.B_loc
     else:
-        O.run_round(st, w, X, y, w.H, w.lr)
-        what = (f"H={w.H} local steps on all K={w.K} replicas + "
+        what = (f"one round: H={w.H} local steps on all K={w.K} replicas + "
                 + ("synchronisation with global momentum" if w.global_momentum
                    else f"{w.scheme} synchronisation" if w.scheme != "local"
                    else "average"))
-    dt = time.perf_counter() - t0
-    samples = w.K * w.H * w.Hb * w.B_loc
+        unit = w.K * w.H * w.Hb * w.B_loc
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        if per_step:
+            O.local_step(st, w, X, y, w.lr, replicas=[0])
+        elif w.Kb > 0:
+            O.run_hierarchical_round(st, w, X, y, w.H, w.Hb, w.Kb, w.lr)
+        else:
+            O.run_round(st, w, X, y, w.H, w.lr)
+        n += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    samples = n * unit
     return {"value": samples / dt, "unit": "samples/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"one full round of {w.name} ({what}, {samples} samples) "
-                      f"in {dt:.2f} s; fp64 numpy, BLAS threads={threads}"}
+            "sample": f"{n} x {what} of {w.name}: {samples} samples in {dt:.2f} s; "
+                      f"fp64 numpy, BLAS threads={threads}"}
 
 
 def main():
