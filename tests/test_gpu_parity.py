@@ -257,6 +257,36 @@ def test_run_round_equals_steps_then_average():
     assert a.step == b.step == 3
 
 
+def test_single_worker_rounds_are_plain_sgd():
+    """K = 1: the average of one replica is that replica (bit for bit), so a
+    round is H steps of mini-batch SGD with momentum on the one worker; against
+    the oracle, and against the same steps taken one by one."""
+    w = _small((70, 48, 36, 10), K=1, B=20, H=3, rounds=2, nesterov=True)
+    X, y, w0 = _small_data(w, seed=81)
+    a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+    st = O.State(w0, 1)
+    loss = torch.empty(3, 1, device=device())
+    for t in range(2):
+        a.run_round([0.02, 0.01, 0.03], loss)
+        for lr in (0.02, 0.01, 0.03):
+            b.local_step(lr)
+        want = O.run_round(st, w, X, y, 3, [0.02, 0.01, 0.03])
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), t
+        np.testing.assert_array_equal(a.read_params(0).cpu().numpy(),
+                                      b.read_params(0).cpu().numpy())
+        assert normwise(a.read_params(0).cpu().numpy(), st.W[0]) <= PARAM_TOL_FP32
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_smallest_batch(dtype):
+    """B_loc = 4, the smallest batch the boundary accepts (one row group per
+    sampler call): every step against the oracle."""
+    w = _small((36, 24, 10), K=3, B=4, H=2, rounds=2, dtype=dtype)
+    X, y, w0 = _small_data(w, seed=83)
+    tol = PARAM_TOL_FP32 if dtype == "fp32" else 2e-3
+    _compare_steps(w, X, y, w0, tol, LOSS_TOL_FP32 if dtype == "fp32" else LOSS_TOL_BF16)
+
+
 def test_momentum_buffers_are_not_averaged():
     w = _small((70, 48, 36, 10), H=2, rounds=1)
     X, y, w0 = _small_data(w, seed=6)
