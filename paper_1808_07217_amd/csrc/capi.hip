@@ -46,6 +46,7 @@ struct Layout {
   size_t esz = 4;  // activation / operand element size
   // byte offsets into the workspace
   size_t W = 0, U = 0, Wb = 0, Xb = 0, idx = 0, Z = 0, part = 0, rowloss = 0;
+  size_t idx2 = 0;  // second index buffer: the next step's rows, sampled early
   size_t Wsync = 0, Ug = 0;  // model at the last sync; global momentum buffer
   size_t E = 0, sign = 0, sign_bytes = 0;  // error memories; sign-sync scratch
   bool head = false;  // top layer through the fused head kernels
@@ -209,6 +210,7 @@ Layout make_layout(const lsgd_config* c) {
     l.Xb = take((size_t)c->N * c->widths[0] * 2);
   }
   l.idx = take(K * B * 4);
+  l.idx2 = take(K * B * 4);
   for (int i = 1; i < l.L; ++i) l.act[i] = take(K * B * c->widths[i] * l.esz);
   l.Z = take(K * B * c->widths[l.L] * 4);
   for (int i = 1; i <= l.L; ++i) l.dZ[i] = take(K * B * c->widths[i] * l.esz);
@@ -297,7 +299,13 @@ struct lsgd_ctx {
   float* E() const { return ef() ? (float*)(ws + lay.E) : nullptr; }
   bf16_t* Wb() const { return bf16() ? (bf16_t*)(ws + lay.Wb) : nullptr; }
   bf16_t* Xb() const { return (bf16_t*)(ws + lay.Xb); }
-  int32_t* idx() const { return (int32_t*)(ws + lay.idx); }
+  // Sampled rows of the current step. The MLP step samples the next step's
+  // rows on side stream 0 into the other buffer (idx_next); `presampled` is
+  // the step they belong to (-1: none), and the buffers swap when it starts.
+  int idx_alt = 0;
+  int64_t presampled = -1;
+  int32_t* idx() const { return (int32_t*)(ws + (idx_alt ? lay.idx2 : lay.idx)); }
+  int32_t* idx_next() const { return (int32_t*)(ws + (idx_alt ? lay.idx : lay.idx2)); }
   void* act(int l) const { return ws + lay.act[l]; }
   float* Z() const { return (float*)(ws + lay.Z); }
   float* part() const { return (float*)(ws + lay.part); }
@@ -421,7 +429,13 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   bf16_t* Wb = c->Wb();
   const void* X0 = dt ? (const void*)c->Xb() : (const void*)c->X;
 
-  LSGD_LAUNCH(c, "sample", sample(c, c->step, c->idx(), s));
+  // this step's rows: sampled by the step before on the side stream, or now
+  if (c->presampled == c->step && c->lay.idx2 != 0)
+    c->idx_alt ^= 1;
+  else
+    LSGD_LAUNCH(c, "sample", sample(c, c->step, c->idx(), s));
+  c->presampled = -1;
+  bool presample = false;
 
   // forward: Z_l = A_{l-1} W_l + b_l, A_l = relu(Z_l) below the top layer
   const int Lg = ly.head ? L - 1 : L;  // layers through the generic GEMMs
@@ -499,6 +513,14 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       LSGD_CK(c, hipStreamWaitEvent(c->side[0], c->fork[0], 0));
       LSGD_LAUNCH_ON(c, c->side[0], "head_wgrad",
                      lsgd::launch_head_wgrad(dt, h, c->side[0]));
+      // the next step's rows, off the critical path, into the buffer this
+      // step does not read (its previous rows' readers, the step before,
+      // precede head_fwd, after which this stream runs)
+      if (c->lay.idx2 != 0) {
+        LSGD_LAUNCH_ON(c, c->side[0], "sample",
+                       sample(c, c->step + 1, c->idx_next(), c->side[0]));
+        presample = true;
+      }
       LSGD_CK(c, hipEventRecord(c->join[0], c->side[0]));
     } else {
       LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(dt, h, s));
@@ -567,6 +589,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_CK(c, hipStreamWaitEvent(s, c->join[1], 0));
   }
   c->step += 1;
+  if (presample) c->presampled = c->step;
   return LSGD_OK;
 }
 
@@ -1071,6 +1094,7 @@ lsgd_status lsgd_set_step(lsgd_ctx* ctx, int64_t step) {
   LSGD_USABLE(ctx);
   if (step < 0) return LSGD_E_INVALID;
   ctx->step = step;
+  ctx->presampled = -1;
   return LSGD_OK;
 }
 
