@@ -120,15 +120,17 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for(tag: str):
+def traffic_for(tag: str, workload: str):
     """HBM bytes per launch of the dominant kernel from the committed PMC
-    summary, if it was taken on the current kernel sources."""
+    summary, if it was taken on this workload and the current kernel
+    sources."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_digest") != source_digest() or t.get("tag") != tag:
+    if (t.get("source_digest") != source_digest() or t.get("tag") != tag
+            or t.get("workload") != workload):
         return None
     return t.get("bytes_per_launch")
 
@@ -439,7 +441,7 @@ def main():
                     "achieved": round(flops / avg_s / 1e12, 2),
                     "peak": PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s"}
         roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-        roof["traffic"] = traffic_for(dom)
+        roof["traffic"] = traffic_for(dom, w.name)
         roof["kernel"] = dom
         roof["avg_launch_us"] = round(avg_s * 1e6, 2)
         roof["launches_timed"] = n
