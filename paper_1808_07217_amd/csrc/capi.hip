@@ -436,6 +436,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_LAUNCH(c, "sample", sample(c, c->step, c->idx(), s));
   c->presampled = -1;
   bool presample = false;
+  bool side0 = false, side1 = false;  // work forked onto the side streams
 
   // forward: Z_l = A_{l-1} W_l + b_l, A_l = relu(Z_l) below the top layer
   const int Lg = ly.head ? L - 1 : L;  // layers through the generic GEMMs
@@ -522,6 +523,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
         presample = true;
       }
       LSGD_CK(c, hipEventRecord(c->join[0], c->side[0]));
+      side0 = true;
     } else {
       LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(dt, h, s));
     }
@@ -576,6 +578,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       LSGD_CK(c, hipStreamWaitEvent(c->side[1], c->fork[1], 0));
       LSGD_LAUNCH_ON(c, c->side[1], "wgrad_update" + std::to_string(l),
                      lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, c->side[1]));
+      side1 = true;
     } else {
       LSGD_LAUNCH(c, "wgrad_update" + std::to_string(l),
                   lsgd::launch_gemm(dt, 1, 0, lsgd::EPI_SGD, 0, a, s));
@@ -583,9 +586,11 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   }
   if (merged)
     LSGD_LAUNCH(c, "wgrad_update", lsgd::launch_gemm_sgd_multi(dt, upd, nupd, s));
-  if (c->use_side) {  // join: the step ends when all of its updates have
+  // join: the step ends when all of its updates have; a side stream with no
+  // work this step is not waited for (each wait costs the stream some µs)
+  if (side0) LSGD_CK(c, hipStreamWaitEvent(s, c->join[0], 0));
+  if (side1) {
     LSGD_CK(c, hipEventRecord(c->join[1], c->side[1]));
-    LSGD_CK(c, hipStreamWaitEvent(s, c->join[0], 0));
     LSGD_CK(c, hipStreamWaitEvent(s, c->join[1], 0));
   }
   c->step += 1;
