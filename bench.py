@@ -357,17 +357,18 @@ def main():
         reps.profile_select(dom, every=max(1, per_round_launches // 2))
         reps.profile(True)
     torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # one event per round boundary: the total and the per-round spread
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     with torch.cuda.stream(stream):
-        ev0.record(stream)
+        evs[0].record(stream)
         t0 = time.perf_counter()
         for i in range(args.steps):
             rnd(args.warmup + i)
-        ev1.record(stream)
+            evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    gpu_ms = ev0.elapsed_time(ev1)
+    gpu_ms = evs[0].elapsed_time(evs[-1])
+    round_ms = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     phases = None
     if w.warm_rounds > 0:
         # post-local SGD: the H = 1 warm phase (one average per local step)
@@ -427,6 +428,8 @@ def main():
                            "ms_per_round": round(ms_per_step, 4),
                            "samples_per_s": round(value, 1)}
         out["phases"] = phases
+    out["round_ms"] = {"median": round(float(np.median(round_ms)), 4),
+                       "min": round(round_ms[0], 4), "max": round(round_ms[-1], 4)}
     gemm_flops = gemm_flops_per_local_step(w) * H
     out["e2e_mfma_frac"] = round(gemm_flops / (ms_per_step / 1e3) /
                                  (PEAK_TFLOPS[w.dtype] * 1e12), 4)
@@ -453,6 +456,19 @@ def main():
         out["kernel_ms_per_step"] = {t: round(v, 4) for t, v in
                                      sorted(per_round.items(),
                                             key=lambda kv: -kv[1])}
+        # matrix-core fraction of each GEMM-carrying launch tag (algorithmic
+        # flops over its bracketed time, against the dtype's dense peak)
+        mf = {}
+        for t, ms in per_round.items():
+            try:
+                f, _ = kernel_cost(t, w)
+            except ValueError:
+                f = None
+            if f and ms > 0:
+                launches = rep[t][0] / prof_rounds
+                mf[t] = round(f * launches / (ms / 1e3) / (PEAK_TFLOPS[w.dtype] * 1e12), 4)
+        if mf:
+            out["kernel_mfma_frac"] = mf
     reps.close()
 
     if not args.no_cpu_baseline:
