@@ -226,6 +226,266 @@ __global__ __launch_bounds__(kTinyThreads) void k_tiny_round(TinyArgs a) {
   }
 }
 
+// The same round with a group of 256 threads per replica (up to four
+// replicas, 1024 threads). The rows of all H steps are sampled up front, and
+// while a step computes, the rows and labels of the next step are already in
+// flight into registers (stored to LDS after the step's last read of them),
+// so no step waits on global memory. Per step and replica the group forms
+// the logits with eight lanes per row (CM / 8 classes each; the row's max,
+// sums and label logit combined by xor butterflies over the eight lanes),
+// then the weight gradient with CM / 4 lanes per input feature (a float4 of
+// classes each, rows ascending) and the update. The mean loss adds the rows'
+// losses lane-strided in ascending order, then a fixed butterfly. The same
+// layout of replicas in LDS as k_tiny_round, the same average and write-back.
+constexpr int kWideThreads = 1024, kRepThreads = 256;
+
+__device__ __forceinline__ float xor8_sum(float v) {
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 4, 64);
+  return v;
+}
+__device__ __forceinline__ float xor8_max(float v) {
+  v = fmaxf(v, __shfl_xor(v, 1, 64));
+  v = fmaxf(v, __shfl_xor(v, 2, 64));
+  v = fmaxf(v, __shfl_xor(v, 4, 64));
+  return v;
+}
+
+// Up to 4 * 256 float4 elements of a step's batch rows (the row-major
+// [B][D] block, D % 4 == 0): element e at thread e % 256, slot e / 256.
+constexpr int kPrefetch4 = 4 * kRepThreads;
+__device__ __forceinline__ void rows_load(const float* X, const int32_t* r, int D4, int nel,
+                                          int t, v4f (&v)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = t + kRepThreads * j;
+    if (e < nel) {
+      const int b = e / D4, i4 = e - b * D4;
+      v[j] = *(const v4f*)(X + (long long)r[b] * (4 * D4) + 4 * i4);
+    }
+  }
+}
+__device__ __forceinline__ void rows_store(float* xs, int XP, int D4, int nel, int t,
+                                           const v4f (&v)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = t + kRepThreads * j;
+    if (e < nel) {
+      const int b = e / D4, i4 = e - b * D4;
+      float* d = xs + b * XP + 4 * i4;
+      d[0] = v[j][0];
+      d[1] = v[j][1];
+      d[2] = v[j][2];
+      d[3] = v[j][3];
+    }
+  }
+}
+
+template <int CM>
+__global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
+  constexpr int CPT = CM / 8;  // classes per lane in the forward
+  constexpr int NQ = CM / 4;   // lanes per input feature in the weight gradient
+  constexpr int RPP = kRepThreads / NQ;
+  extern __shared__ float lds[];
+  const int K = a.K, B = a.B, D = a.D, C = a.C, H = a.H, P = D * C + C;
+  const int PL = (D + 1) * CM;
+  float* Wl = lds;                        // [K][D + 1][CM]
+  float* Ul = Wl + (long long)K * PL;     // [K][D + 1][CM]
+  const int k = threadIdx.x / kRepThreads, t = threadIdx.x % kRepThreads;
+  const bool mine = k < K;
+  const int XP = D | 1;
+  // per replica: dZ [B][CM], labels [B], rows [B][XP], row losses [B],
+  // sampled row indices [H][B]
+  const int RS = (B * CM + 2 * B + B * XP + H * B + 3) & ~3;
+  float* dz = Ul + (long long)K * PL + (mine ? k : 0) * RS;
+  int32_t* labs = (int32_t*)(dz + B * CM);
+  float* xs = dz + B * CM + B;
+  float* lrow = xs + B * XP;
+  int32_t* rows = (int32_t*)(lrow + B);
+
+#pragma unroll 8
+  for (int e = threadIdx.x; e < K * PL; e += kWideThreads) {
+    const int kk = e / PL, q = e - kk * PL, i = q / CM, c = q - i * CM;
+    const long long g = (long long)kk * a.Ps + i * C + c;
+    const bool ok = c < C;
+    Wl[e] = ok ? a.W[g] : 0.f;
+    Ul[e] = ok ? a.U[g] : 0.f;
+  }
+  const long long lo = (long long)k * a.N / K;
+  if (mine) {  // every step's rows
+    if (a.S > 0) {  // per-epoch reshuffled partition
+      for (int e = t; e < H * B; e += kRepThreads) {
+        const int h = e / B, b = e - h * B;
+        const long long step = a.step0 + h, ep = step / a.S, j = step - ep * a.S;
+        rows[e] = epoch_row((uint32_t)(lo + j * B + b), a.N, a.m, a.key0, a.key1,
+                            (uint32_t)ep);
+      }
+    } else {        // i.i.d. from the worker's shard
+      const uint64_t n = (uint64_t)((long long)(k + 1) * a.N / K - lo);
+      const int nq = (B + 3) >> 2;
+      for (int e = t; e < H * nq; e += kRepThreads) {
+        const int h = e / nq, q = e - h * nq;
+        const long long step = a.step0 + h;
+        const uint4 u = philox4x32_10(
+            make_uint4((uint32_t)q, (uint32_t)step, (uint32_t)k,
+                       (uint32_t)((uint64_t)step >> 32)), a.key0, a.key1);
+        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (4 * q + j < B)
+            rows[h * B + 4 * q + j] = (int32_t)(lo + (long long)(((uint64_t)w4[j] * n) >> 32));
+      }
+    }
+  }
+  __syncthreads();
+
+  // the next step's batch fits four float4 per thread and its labels one
+  // per thread: prefetched during the step; otherwise staged between steps
+  const int D4 = D >> 2;
+  const bool pf = (D & 3) == 0 && B * D4 <= kPrefetch4 && B <= kRepThreads;
+  v4f pre[4];
+  int lab_next = 0;
+  auto stage_sync = [&](int h) {
+    const int32_t* r = rows + h * B;
+    if ((D & 3) == 0) {
+#pragma unroll 4
+      for (int e = t; e < B * D4; e += kRepThreads) {
+        const int b = e / D4, i4 = e - b * D4;
+        const v4f v = *(const v4f*)(a.X + (long long)r[b] * D + 4 * i4);
+        float* d = xs + b * XP + 4 * i4;
+        d[0] = v[0];
+        d[1] = v[1];
+        d[2] = v[2];
+        d[3] = v[3];
+      }
+    } else {
+#pragma unroll 4
+      for (int e = t; e < B * D; e += kRepThreads) {
+        const int b = e / D, i = e - b * D;
+        xs[b * XP + i] = a.X[(long long)r[b] * D + i];
+      }
+    }
+    for (int b = t; b < B; b += kRepThreads) labs[b] = a.y[r[b]];
+  };
+  if (mine) stage_sync(0);
+  __syncthreads();
+
+  const float invB = 1.0f / (float)B;
+  float* W = Wl + (long long)(mine ? k : 0) * PL;
+  float* U = Ul + (long long)(mine ? k : 0) * PL;
+  for (int h = 0; h < H; ++h) {
+    const float lr = a.lr[h];
+    const bool next = h + 1 < H;
+    if (mine && pf && next) {  // in flight while this step computes
+      const int32_t* r = rows + (h + 1) * B;
+      rows_load(a.X, r, D4, B * D4, t, pre);
+      if (t < B) lab_next = a.y[r[t]];
+    }
+    if (mine) {
+      // forward, loss, dZ: eight lanes per row, classes c0 .. c0 + CPT - 1
+      const int cg = t & 7, c0 = cg * CPT;
+      for (int b0 = 0; b0 < B; b0 += kRepThreads / 8) {
+        const int b = b0 + (t >> 3);
+        const bool live = b < B;
+        const int lab = labs[live ? b : 0];
+        const float* x = xs + (live ? b : 0) * XP;
+        float z[CPT];
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) z[j] = 0.f;
+#pragma unroll 4
+        for (int i = 0; i < D; ++i) {
+          const float xi = x[i];
+#pragma unroll
+          for (int j = 0; j < CPT; ++j) z[j] = __builtin_fmaf(xi, W[i * CM + c0 + j], z[j]);
+        }
+        float m = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) {
+          z[j] = c0 + j < C ? z[j] + W[D * CM + c0 + j] : -INFINITY;
+          m = fmaxf(m, z[j]);
+        }
+        m = xor8_max(m);
+        float s = 0.f, rest = 0.f, zy = -INFINITY, ev[CPT];
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) {
+          ev[j] = __expf(z[j] - m);  // 0 for the padded classes
+          s += ev[j];
+          rest += c0 + j != lab ? ev[j] : 0.f;
+          zy = c0 + j == lab ? z[j] : zy;
+        }
+        s = xor8_sum(s);
+        rest = xor8_sum(rest);
+        zy = xor8_max(zy);
+        const float inv_s = 1.0f / s;
+        if (live) {
+#pragma unroll
+          for (int j = 0; j < CPT; ++j)
+            dz[b * CM + c0 + j] = (ev[j] * inv_s - (c0 + j == lab ? 1.f : 0.f)) * invB;
+          if (cg == 0) lrow[b] = zy >= m ? log1pf(rest) : (m - zy) + logf(s);
+        }
+      }
+    }
+    __syncthreads();
+    if (mine) {
+      if (t < 64) {  // mean loss: lane-strided rows in order, then a butterfly
+        float lsum = 0.f;
+        for (int b = t; b < B; b += 64) lsum += lrow[b];
+        lsum = wave_sum_fixed(lsum);
+        if (t == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
+      }
+      // weight gradient and update: NQ lanes per input feature (and the bias
+      // row as feature D, whose input is 1), rows ascending
+      const int q4 = (t % NQ) * 4;
+      for (int i0 = 0; i0 <= D; i0 += RPP) {
+        const int i = i0 + t / NQ;
+        if (i <= D) {
+          v4f g = (v4f){0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+          for (int b = 0; b < B; ++b) {
+            const float xi = i < D ? xs[b * XP + i] : 1.f;
+            const v4f dv = *(const v4f*)(dz + b * CM + q4);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) g[j] = __builtin_fmaf(xi, dv[j], g[j]);
+          }
+          const float wd = a.wd;
+          v4f w = *(v4f*)(W + i * CM + q4), u = *(v4f*)(U + i * CM + q4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float gg = __builtin_fmaf(wd, w[j], g[j]);
+            u[j] = __builtin_fmaf(a.mom, u[j], gg);
+            w[j] = __builtin_fmaf(-lr, step_dir(u[j], gg, a.mom, a.mode), w[j]);
+          }
+          *(v4f*)(W + i * CM + q4) = w;
+          *(v4f*)(U + i * CM + q4) = u;
+        }
+      }
+    }
+    if (next) {
+      __syncthreads();  // the step's last reads of its rows and labels
+      if (mine) {
+        if (pf) {
+          rows_store(xs, XP, D4, B * D4, t, pre);
+          if (t < B) labs[t] = lab_next;
+        } else {
+          stage_sync(h + 1);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  for (int p = threadIdx.x; p < P; p += kWideThreads) {
+    const int i = p / C, c = p - i * C;
+    const float mean = tree_sum_f(Wl + i * CM + c, PL, K) / (float)K;
+    for (int kk = 0; kk < K; ++kk) a.W[kk * a.Ps + p] = mean;
+  }
+#pragma unroll 4
+  for (int e = threadIdx.x; e < K * P; e += kWideThreads) {
+    const int kk = e / P, p = e - kk * P, i = p / C, c = p - i * C;
+    a.U[kk * a.Ps + p] = Ul[(long long)kk * PL + i * CM + c];
+  }
+}
+
 }  // namespace
 
 int tiny_classes(int C) { return C <= 8 ? 8 : C <= 16 ? 16 : 32; }
@@ -235,17 +495,23 @@ size_t tiny_round_lds_bytes(int K, int B, int D, int C) {
   const long long wave = ((long long)B * CM + B + (long long)B * (D | 1) + 3) & ~3LL;
   return (size_t)(2LL * K * (D + 1) * CM + 4LL * wave) * sizeof(float);
 }
+size_t tiny_wide_lds_bytes(int K, int B, int D, int C, int H) {
+  const int CM = tiny_classes(C);
+  const long long rep =
+      ((long long)B * CM + 2LL * B + (long long)B * (D | 1) + (long long)H * B + 3) & ~3LL;
+  return (size_t)(2LL * K * (D + 1) * CM + K * rep) * sizeof(float);
+}
 
 // The kernel's dynamic LDS above the default 64 KB: requested once per
 // device and instance (gfx950 compute units hold 160 KB).
-template <int CM>
+template <int CM, bool Wide>
 hipError_t allow_lds(size_t bytes) {
   static bool done[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess || dev < 0 || dev >= 64) return e != hipSuccess ? e : hipErrorInvalidDevice;
   if (bytes <= 64 * 1024 || done[dev]) return hipSuccess;
-  e = hipFuncSetAttribute((const void*)k_tiny_round<CM>,
+  e = hipFuncSetAttribute(Wide ? (const void*)k_tiny_round_wide<CM> : (const void*)k_tiny_round<CM>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kTinyMaxLds);
   if (e == hipSuccess) done[dev] = true;
   return e;
@@ -273,24 +539,28 @@ bool tiny_round_fits(int K, int B, int D, int C, int H) {
   return lds <= kTinyMaxLds && lds <= tiny_lds_limit();
 }
 
-hipError_t launch_tiny_round(const TinyArgs& a, hipStream_t s) {
-  if (!tiny_round_fits(a.K, a.B, a.D, a.C, a.H)) return hipErrorInvalidValue;
-  const size_t lds = tiny_round_lds_bytes(a.K, a.B, a.D, a.C);
+template <int CM>
+hipError_t launch_round(const TinyArgs& a, hipStream_t s) {
   hipError_t e;
-  switch (tiny_classes(a.C)) {
-    case 8:
-      if ((e = allow_lds<8>(lds)) != hipSuccess) return e;
-      hipLaunchKernelGGL(k_tiny_round<8>, dim3(1), dim3(kTinyThreads), lds, s, a);
-      break;
-    case 16:
-      if ((e = allow_lds<16>(lds)) != hipSuccess) return e;
-      hipLaunchKernelGGL(k_tiny_round<16>, dim3(1), dim3(kTinyThreads), lds, s, a);
-      break;
-    default:
-      if ((e = allow_lds<32>(lds)) != hipSuccess) return e;
-      hipLaunchKernelGGL(k_tiny_round<32>, dim3(1), dim3(kTinyThreads), lds, s, a);
+  const size_t wide = tiny_wide_lds_bytes(a.K, a.B, a.D, a.C, a.H);
+  if (a.K * kRepThreads <= kWideThreads && wide <= kTinyMaxLds && wide <= tiny_lds_limit()) {
+    if ((e = allow_lds<CM, true>(wide)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_tiny_round_wide<CM>, dim3(1), dim3(kWideThreads), wide, s, a);
+  } else {
+    const size_t lds = tiny_round_lds_bytes(a.K, a.B, a.D, a.C);
+    if ((e = allow_lds<CM, false>(lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_tiny_round<CM>, dim3(1), dim3(kTinyThreads), lds, s, a);
   }
   return hipGetLastError();
 }
-
+// Up to four replicas take the 256-thread-per-replica kernel when its larger
+// scratch fits; otherwise the wave-per-replica kernel runs.
+hipError_t launch_tiny_round(const TinyArgs& a, hipStream_t s) {
+  if (!tiny_round_fits(a.K, a.B, a.D, a.C, a.H)) return hipErrorInvalidValue;
+  switch (tiny_classes(a.C)) {
+    case 8: return launch_round<8>(a, s);
+    case 16: return launch_round<16>(a, s);
+    default: return launch_round<32>(a, s);
+  }
+}
 }  // namespace lsgd
