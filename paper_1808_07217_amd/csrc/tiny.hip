@@ -226,30 +226,45 @@ __global__ __launch_bounds__(kTinyThreads) void k_tiny_round(TinyArgs a) {
   }
 }
 
-// The same round with a group of 256 threads per replica (up to four
-// replicas, 1024 threads). The rows of all H steps are sampled up front, and
-// while a step computes, the rows and labels of the next step are already in
-// flight into registers (stored to LDS after the step's last read of them),
-// so no step waits on global memory. Per step and replica the group forms
-// the logits with eight lanes per row (CM / 8 classes each; the row's max,
-// sums and label logit combined by xor butterflies over the eight lanes),
-// then the weight gradient with CM / 4 lanes per input feature (a float4 of
-// classes each, rows ascending) and the update. The mean loss adds the rows'
-// losses lane-strided in ascending order, then a fixed butterfly. The same
-// layout of replicas in LDS as k_tiny_round, the same average and write-back.
+// The same round with a group of 256 threads (four waves) per replica, up
+// to four replicas in 1024 threads. The rows of all H steps are sampled up
+// front, and while a step computes, the rows and labels of the next step are
+// already in flight into registers (stored to LDS after the step's last read
+// of them), so no step waits on global memory. Both contractions of a step
+// run on the matrix cores with their operands read from LDS: the logits
+// Z = X W as 16-row blocks of v_mfma_f32_16x16x4f32 over the input features,
+// and the gradient dW = X^T [dZ] (the bias row as a feature whose input is 1)
+// as 16-feature blocks over the rows, each followed by the update of its
+// block. A row's 16 classes sit on one 16-lane DPP row of the accumulator,
+// so its max, sums and label logit are DPP butterflies. The mean loss adds
+// the rows' losses lane-strided in ascending order, then a fixed butterfly.
+// The same layout of replicas in LDS as k_tiny_round, the same average and
+// write-back.
 constexpr int kWideThreads = 1024, kRepThreads = 256;
 
-__device__ __forceinline__ float xor8_sum(float v) {
-  v += __shfl_xor(v, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  v += __shfl_xor(v, 4, 64);
+// Reductions over the four lanes l % 16 + 16 q of a wave (xor 16, then xor
+// 32): each step adds two partials that both lanes of the pair form in the
+// same order, so all four lanes end with bitwise the same value.
+__device__ __forceinline__ float quad16_sum(float v) {
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
   return v;
 }
-__device__ __forceinline__ float xor8_max(float v) {
-  v = fmaxf(v, __shfl_xor(v, 1, 64));
-  v = fmaxf(v, __shfl_xor(v, 2, 64));
-  v = fmaxf(v, __shfl_xor(v, 4, 64));
-  return v;
+__device__ __forceinline__ float quad16_max(float v) {
+  float o = __shfl_xor(v, 16, 64);
+  v = o > v ? o : v;
+  o = __shfl_xor(v, 32, 64);
+  return o > v ? o : v;
+}
+
+// The replica average of k_tiny_round_wide (K <= 4) in the order of the
+// replica-average tree: ((w0 + w1) + (w2 + w3)), ((w0 + w1) + w2), ...
+__device__ __forceinline__ float tree_sum_le4(const float* p, int stride, int K) {
+  if (K == 1) return p[0];
+  const float a = p[0] + p[stride];
+  if (K == 2) return a;
+  if (K == 3) return a + p[2 * stride];
+  return a + (p[2 * stride] + p[3 * stride]);
 }
 
 // Up to 4 * 256 float4 elements of a step's batch rows (the row-major
@@ -257,13 +272,13 @@ __device__ __forceinline__ float xor8_max(float v) {
 constexpr int kPrefetch4 = 4 * kRepThreads;
 __device__ __forceinline__ void rows_load(const float* X, const int32_t* r, int D4, int nel,
                                           int t, v4f (&v)[4]) {
+  // unconditional loads (slots past the batch re-read element 0), so that
+  // all four are in flight together
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int e = t + kRepThreads * j;
-    if (e < nel) {
-      const int b = e / D4, i4 = e - b * D4;
-      v[j] = *(const v4f*)(X + (long long)r[b] * (4 * D4) + 4 * i4);
-    }
+    const int e = t + kRepThreads * j < nel ? t + kRepThreads * j : 0;
+    const int b = e / D4, i4 = e - b * D4;
+    v[j] = *(const v4f*)(X + (long long)r[b] * (4 * D4) + 4 * i4);
   }
 }
 __device__ __forceinline__ void rows_store(float* xs, int XP, int D4, int nel, int t,
@@ -284,15 +299,17 @@ __device__ __forceinline__ void rows_store(float* xs, int XP, int D4, int nel, i
 
 template <int CM>
 __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
-  constexpr int CPT = CM / 8;  // classes per lane in the forward
-  constexpr int NQ = CM / 4;   // lanes per input feature in the weight gradient
-  constexpr int RPP = kRepThreads / NQ;
+  constexpr int NCB = CM >= 16 ? CM / 16 : 1;  // blocks of 16 classes
   extern __shared__ float lds[];
   const int K = a.K, B = a.B, D = a.D, C = a.C, H = a.H, P = D * C + C;
   const int PL = (D + 1) * CM;
   float* Wl = lds;                        // [K][D + 1][CM]
   float* Ul = Wl + (long long)K * PL;     // [K][D + 1][CM]
   const int k = threadIdx.x / kRepThreads, t = threadIdx.x % kRepThreads;
+  // MFMA lane row and quarter; the wave's rank in its group, rotated by the
+  // replica so that the first waves of the four groups (the only ones with
+  // work when a phase has fewer blocks than waves) sit on different SIMDs
+  const int l16 = t & 15, lq = (t & 63) >> 4, wr = ((t >> 6) - k) & 3;
   const bool mine = k < K;
   const int XP = D | 1;
   // per replica: dZ [B][CM], labels [B], rows [B][XP], row losses [B],
@@ -380,49 +397,86 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
     if (mine && pf && next) {  // in flight while this step computes
       const int32_t* r = rows + (h + 1) * B;
       rows_load(a.X, r, D4, B * D4, t, pre);
-      if (t < B) lab_next = a.y[r[t]];
+      lab_next = a.y[r[t < B ? t : 0]];
     }
     if (mine) {
-      // forward, loss, dZ: eight lanes per row, classes c0 .. c0 + CPT - 1
-      const int cg = t & 7, c0 = cg * CPT;
-      for (int b0 = 0; b0 < B; b0 += kRepThreads / 8) {
-        const int b = b0 + (t >> 3);
-        const bool live = b < B;
-        const int lab = labs[live ? b : 0];
-        const float* x = xs + (live ? b : 0) * XP;
-        float z[CPT];
+      // forward, loss, dZ: wave rank wr takes row blocks wr, wr + 4, ... of
+      // 16 rows; Z^T = W^T X^T on v_mfma_f32_16x16x4f32 over k = input
+      // features, operands read from LDS (padded rows, features and classes
+      // read as 0), so that lane l holds classes 4 (l / 16) + j (+ 16 cb) of
+      // row l % 16: a row's softmax is one lane's classes and a butterfly
+      // over the four lanes l % 16 + 16 q
+      const int nrb = (B + 15) >> 4;
+      for (int rb = wr; rb < nrb; rb += kRepThreads / 64) {
+        const int br = rb * 16 + l16;
+        const bool rok = br < B;
+        const float* xb = xs + (rok ? br : 0) * XP;
+        v4f acc[NCB];
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) z[j] = 0.f;
-#pragma unroll 4
-        for (int i = 0; i < D; ++i) {
-          const float xi = x[i];
+        for (int cb = 0; cb < NCB; ++cb) acc[cb] = (v4f){0.f, 0.f, 0.f, 0.f};
+        // four k steps per trip (a whole trip's operands read before its
+        // MFMAs); steps past D read zeros
+        for (int k0 = 0; k0 < D; k0 += 16) {
+          float xv[4], wv4[4][NCB];
 #pragma unroll
-          for (int j = 0; j < CPT; ++j) z[j] = __builtin_fmaf(xi, W[i * CM + c0 + j], z[j]);
+          for (int u = 0; u < 4; ++u) {
+            const int kk = k0 + 4 * u + lq;
+            const bool kok = kk < D;
+            const float x = xb[kok ? kk : 0];  // addresses clamped, values zeroed
+            xv[u] = rok && kok ? x : 0.f;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+              const int c = cb * 16 + l16;
+              const float w = W[(kok ? kk : 0) * CM + (c < CM ? c : 0)];
+              wv4[u][cb] = kok && c < CM ? w : 0.f;
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb)
+              acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv4[u][cb], xv[u], acc[cb], 0, 0, 0);
         }
-        float m = -INFINITY;
+        const int lab = labs[rok ? br : 0];
+        float z[NCB][4], zl[NCB][4], m = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) {
-          z[j] = c0 + j < C ? z[j] + W[D * CM + c0 + j] : -INFINITY;
-          m = fmaxf(m, z[j]);
-        }
-        m = xor8_max(m);
-        float s = 0.f, rest = 0.f, zy = -INFINITY, ev[CPT];
+        for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) {
-          ev[j] = __expf(z[j] - m);  // 0 for the padded classes
-          s += ev[j];
-          rest += c0 + j != lab ? ev[j] : 0.f;
-          zy = c0 + j == lab ? z[j] : zy;
-        }
-        s = xor8_sum(s);
-        rest = xor8_sum(rest);
-        zy = xor8_max(zy);
-        const float inv_s = 1.0f / s;
-        if (live) {
+          for (int j = 0; j < 4; ++j) {
+            const int c = cb * 16 + 4 * lq + j;
+            zl[cb][j] = acc[cb][j] + W[D * CM + (c < C ? c : 0)];
+            z[cb][j] = c < C ? zl[cb][j] : -INFINITY;
+            m = z[cb][j] > m ? z[cb][j] : m;
+          }
+        m = quad16_max(m);
+        float s = 0.f, rest = 0.f, zy = -INFINITY;
 #pragma unroll
-          for (int j = 0; j < CPT; ++j)
-            dz[b * CM + c0 + j] = (ev[j] * inv_s - (c0 + j == lab ? 1.f : 0.f)) * invB;
-          if (cg == 0) lrow[b] = zy >= m ? log1pf(rest) : (m - zy) + logf(s);
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int c = cb * 16 + 4 * lq + j;
+            z[cb][j] = __expf(z[cb][j] - m);  // 0 for the padded classes
+            s += z[cb][j];
+            rest += c != lab ? z[cb][j] : 0.f;
+            zy = c == lab ? zl[cb][j] : zy;
+          }
+        s = quad16_sum(s);
+        rest = quad16_sum(rest);
+        zy = quad16_max(zy);
+        if (rok) {
+          const float inv_s = 1.0f / s;
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) {
+            const int c4 = cb * 16 + 4 * lq;
+            if (c4 < CM) {
+              v4f d;
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                d[j] = (z[cb][j] * inv_s - (c4 + j == lab ? 1.f : 0.f)) * invB;
+              *(v4f*)(dz + br * CM + c4) = d;
+            }
+          }
+          if (lq == 0) lrow[br] = zy >= m ? log1pf(rest) : (m - zy) + logf(s);
         }
       }
     }
@@ -434,30 +488,41 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
         lsum = wave_sum_fixed(lsum);
         if (t == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
       }
-      // weight gradient and update: NQ lanes per input feature (and the bias
-      // row as feature D, whose input is 1), rows ascending
-      const int q4 = (t % NQ) * 4;
-      for (int i0 = 0; i0 <= D; i0 += RPP) {
-        const int i = i0 + t / NQ;
-        if (i <= D) {
-          v4f g = (v4f){0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-          for (int b = 0; b < B; ++b) {
-            const float xi = i < D ? xs[b * XP + i] : 1.f;
-            const v4f dv = *(const v4f*)(dz + b * CM + q4);
+      // weight gradient and update: blocks of 16 features (the bias row as
+      // feature D, whose input is 1) x 16 classes, wave rank wr taking
+      // blocks wr, wr + 4, ...; dW = X^T dZ on v_mfma_f32_16x16x4f32 over k = rows
+      const int nib = (D + 16) >> 4;  // ceil((D + 1) / 16)
+      for (int blk = wr; blk < nib * NCB; blk += kRepThreads / 64) {
+        const int ib = blk / NCB, cb = blk - ib * NCB;
+        const int ia = ib * 16 + l16, cn = cb * 16 + l16;
+        v4f acc = (v4f){0.f, 0.f, 0.f, 0.f};
+        for (int b0 = 0; b0 < B; b0 += 16) {  // as above: rows past B read zeros
+          float av[4], bv[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) g[j] = __builtin_fmaf(xi, dv[j], g[j]);
+          for (int u = 0; u < 4; ++u) {
+            const int b = b0 + 4 * u + lq;
+            const bool bok = b < B;
+            const int bc = bok ? b : 0;
+            const float x = xs[bc * XP + (ia < D ? ia : 0)], g = dz[bc * CM + (cn < CM ? cn : 0)];
+            av[u] = !bok ? 0.f : ia < D ? x : ia == D ? 1.f : 0.f;
+            bv[u] = bok && cn < CM ? g : 0.f;
           }
-          const float wd = a.wd;
-          v4f w = *(v4f*)(W + i * CM + q4), u = *(v4f*)(U + i * CM + q4);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float gg = __builtin_fmaf(wd, w[j], g[j]);
-            u[j] = __builtin_fmaf(a.mom, u[j], gg);
-            w[j] = __builtin_fmaf(-lr, step_dir(u[j], gg, a.mom, a.mode), w[j]);
+          for (int u = 0; u < 4; ++u)
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], acc, 0, 0, 0);
+        }
+        // lane holds the gradient of features ib * 16 + 4 lq + j, class cn
+        const float wd = a.wd;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = ib * 16 + 4 * lq + j;
+          if (i <= D && cn < CM) {
+            const float w = W[i * CM + cn], u = U[i * CM + cn];
+            const float gg = __builtin_fmaf(wd, w, acc[j]);
+            const float un = __builtin_fmaf(a.mom, u, gg);
+            W[i * CM + cn] = __builtin_fmaf(-lr, step_dir(un, gg, a.mom, a.mode), w);
+            U[i * CM + cn] = un;
           }
-          *(v4f*)(W + i * CM + q4) = w;
-          *(v4f*)(U + i * CM + q4) = u;
         }
       }
     }
@@ -476,7 +541,7 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   }
   for (int p = threadIdx.x; p < P; p += kWideThreads) {
     const int i = p / C, c = p - i * C;
-    const float mean = tree_sum_f(Wl + i * CM + c, PL, K) / (float)K;
+    const float mean = tree_sum_le4(Wl + i * CM + c, PL, K) / (float)K;
     for (int kk = 0; kk < K; ++kk) a.W[kk * a.Ps + p] = mean;
   }
 #pragma unroll 4
