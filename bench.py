@@ -15,6 +15,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -25,13 +26,17 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
 METRIC = "aggregate samples/s per local-SGD round at 1 GPU"
+EVENT_GAP_MS = 0.4      # timed rounds between two HIP events: at least this long
+MAX_AUTO_STEPS = 20000
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 
 
 def parse():
     p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20, help="timed rounds")
+    p.add_argument("--steps", type=int, default=None,
+                   help="timed rounds (default 20; rounds shorter than 1 ms: "
+                        "as many as fill about 100 ms)")
     p.add_argument("--warmup", type=int, default=3, help="untimed rounds")
     p.add_argument("--workload", default="mlp_512")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -70,6 +75,13 @@ def kernel_cost(tag: str, w) -> tuple:
         if w.scheme == "ef_sign":   # W, e read twice, written once
             return 0, 24 * K * P + 8 * P
         return 0, 8 * K * P + K * P // 2 + 8 * P
+    if tag == "tiny_round" and L == 1:   # a whole round in one workgroup
+        H = w.H * w.Hb
+        D, C = d
+        flops = H * K * (2 * B * D * C + 2 * B * (D + 1) * C)   # logits + gradient
+        # batch rows + labels per step, replicas and buffers read and written
+        # once, the losses
+        return flops, H * K * B * (D * 4 + 4) + 16 * K * P + 4 * H * K
     if tag == "wgrad_update":   # one launch over every generic layer
         Lg = L - 1 if d[L] <= 32 else L   # the top layer has its own kernels
         costs = [kernel_cost(f"wgrad_update{l}", w) for l in range(1, Lg + 1)]
@@ -327,7 +339,8 @@ def main():
     hier = w.Kb > 0
     H = w.H * w.Hb            # local steps per (outer) round
     lrs = [w.lr] * H
-    loss = torch.empty((args.warmup + args.steps + 8) * H, w.K, device=dev)
+    max_steps = args.steps if args.steps is not None else MAX_AUTO_STEPS
+    loss = torch.empty((args.warmup + max_steps + 8) * H, w.K, device=dev)
 
     def rnd(i):
         if hier:   # H^b x (H local steps, block average), global average
@@ -342,11 +355,25 @@ def main():
     # costs the stream some microseconds), on the stream it is launched on.
     timing = not args.no_kernel_timing and args.warmup >= 1
     prof_rounds = 0
+    w0_ev, w1_ev = (torch.cuda.Event(enable_timing=True) for _ in range(2))
     for i in range(args.warmup):
         if timing and (i >= 1 or args.warmup == 1):
             reps.profile(True)
             prof_rounds += 1
+        if i == args.warmup - 1:
+            w0_ev.record(stream)
         rnd(i)
+    w1_ev.record(stream)
+    torch.cuda.synchronize()
+    # one warmup round's time: the number of timed rounds (when not given)
+    # and how sparsely events may sample them. An event record costs the
+    # stream a few microseconds, so short rounds are bracketed only every
+    # few rounds (events cost at most about 2% of the timed region).
+    est_ms = max(w0_ev.elapsed_time(w1_ev), 1e-3) if args.warmup >= 1 else 1.0
+    sparse = max(1, math.ceil(EVENT_GAP_MS / est_ms))
+    steps = args.steps
+    if steps is None:
+        steps = 20 if est_ms >= 1.0 else min(MAX_AUTO_STEPS, max(20, math.ceil(100.0 / est_ms)))
     dom = None
     if timing:
         rep = reps.profile_report()
@@ -354,21 +381,26 @@ def main():
         per_round = {t: ms / prof_rounds for t, (n, ms) in rep.items()}
         dom = max(per_round, key=per_round.get)
         per_round_launches = rep[dom][0] // prof_rounds
-        reps.profile_select(dom, every=max(1, per_round_launches // 2))
+        reps.profile_select(dom, every=max(1, per_round_launches // 2) if sparse == 1
+                            else per_round_launches * sparse)
         reps.profile(True)
     torch.cuda.synchronize()
-    # one event per round boundary: the total and the per-round spread
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    # an event every `sparse` round boundaries: the total and the per-round
+    # spread (blocks of `sparse` rounds)
+    bounds = sorted(set(range(0, steps, sparse)) | {steps})
+    evs = {b: torch.cuda.Event(enable_timing=True) for b in bounds}
     with torch.cuda.stream(stream):
         evs[0].record(stream)
         t0 = time.perf_counter()
-        for i in range(args.steps):
+        for i in range(steps):
             rnd(args.warmup + i)
-            evs[i + 1].record(stream)
+            if i + 1 in evs:
+                evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    gpu_ms = evs[0].elapsed_time(evs[-1])
-    round_ms = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    gpu_ms = evs[0].elapsed_time(evs[steps])
+    round_ms = sorted(evs[a].elapsed_time(evs[b]) / (b - a)
+                      for a, b in zip(bounds[:-1], bounds[1:]))
     phases = None
     if w.warm_rounds > 0:
         # post-local SGD: the H = 1 warm phase (one average per local step)
@@ -395,16 +427,16 @@ def main():
         reps.profile_select(None)
         avg_s = ms / n / 1e3
         flops, nbytes = kernel_cost(dom, w)
-    ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
+    ms_per_step = max(gpu_ms, wall * 1e3) / steps
     samples = w.K * H * w.B_loc
     value = samples / (ms_per_step / 1e3)
-    l_all = loss[:(args.warmup + args.steps) * H].float().cpu().numpy()
+    l_all = loss[:(args.warmup + steps) * H].float().cpu().numpy()
     if not np.all(np.isfinite(l_all)):
         raise RuntimeError("non-finite loss in the benchmark run")
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
         "data": "synthetic",

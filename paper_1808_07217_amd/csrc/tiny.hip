@@ -301,7 +301,7 @@ template <int CM>
 __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   constexpr int NCB = CM >= 16 ? CM / 16 : 1;  // blocks of 16 classes
   extern __shared__ float lds[];
-  const int K = a.K, B = a.B, D = a.D, C = a.C, H = a.H, P = D * C + C;
+  const int K = a.K, B = a.B, D = a.D, C = a.C, H = a.H;
   const int PL = (D + 1) * CM;
   float* Wl = lds;                        // [K][D + 1][CM]
   float* Ul = Wl + (long long)K * PL;     // [K][D + 1][CM]
@@ -312,23 +312,18 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   const int l16 = t & 15, lq = (t & 63) >> 4, wr = ((t >> 6) - k) & 3;
   const bool mine = k < K;
   const int XP = D | 1;
-  // per replica: dZ [B][CM], labels [B], rows [B][XP], row losses [B],
-  // sampled row indices [H][B]
-  const int RS = (B * CM + 2 * B + B * XP + H * B + 3) & ~3;
+  // per replica: dZ [B][CM], row losses [B], sampled row indices [H][B],
+  // then two buffers (steps of even / odd index) of labels [B] and rows
+  // [B][XP]: the next step's batch is stored while this step still reads its
+  // own
+  const int RS = (B * CM + B + H * B + 2 * (B + B * XP) + 3) & ~3;
   float* dz = Ul + (long long)K * PL + (mine ? k : 0) * RS;
-  int32_t* labs = (int32_t*)(dz + B * CM);
-  float* xs = dz + B * CM + B;
-  float* lrow = xs + B * XP;
+  float* lrow = dz + B * CM;
   int32_t* rows = (int32_t*)(lrow + B);
+  float* const buf0 = lrow + B + H * B;
+  int32_t* labs = (int32_t*)buf0;
+  float* xs = buf0 + B;
 
-#pragma unroll 8
-  for (int e = threadIdx.x; e < K * PL; e += kWideThreads) {
-    const int kk = e / PL, q = e - kk * PL, i = q / CM, c = q - i * CM;
-    const long long g = (long long)kk * a.Ps + i * C + c;
-    const bool ok = c < C;
-    Wl[e] = ok ? a.W[g] : 0.f;
-    Ul[e] = ok ? a.U[g] : 0.f;
-  }
   const long long lo = (long long)k * a.N / K;
   if (mine) {  // every step's rows
     if (a.S > 0) {  // per-epoch reshuffled partition
@@ -385,7 +380,30 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
     }
     for (int b = t; b < B; b += kRepThreads) labs[b] = a.y[r[b]];
   };
-  if (mine) stage_sync(0);
+  // step 0's rows and labels in flight together with the replicas' loads
+  if (mine && pf) {
+    rows_load(a.X, rows, D4, B * D4, t, pre);
+    lab_next = a.y[rows[t < B ? t : 0]];
+  }
+  // replica by replica over the padded layout: the row and class of an
+  // entry are a shift and a mask (CM is a power of two)
+  for (int kk = 0; kk < K; ++kk)
+#pragma unroll 2
+    for (int e = threadIdx.x; e < PL; e += kWideThreads) {
+      const int i = e / CM, c = e % CM;
+      const long long g = (long long)kk * a.Ps + i * C + (c < C ? c : 0);
+      const float w = a.W[g], u = a.U[g];
+      Wl[kk * PL + e] = c < C ? w : 0.f;
+      Ul[kk * PL + e] = c < C ? u : 0.f;
+    }
+  if (mine) {
+    if (pf) {
+      rows_store(xs, XP, D4, B * D4, t, pre);
+      if (t < B) labs[t] = lab_next;
+    } else {
+      stage_sync(0);
+    }
+  }
   __syncthreads();
 
   const float invB = 1.0f / (float)B;
@@ -394,6 +412,9 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   for (int h = 0; h < H; ++h) {
     const float lr = a.lr[h];
     const bool next = h + 1 < H;
+    float* const bufn = buf0 + ((h + 1) & 1) * (B + B * XP);  // the next step's
+    labs = (int32_t*)(buf0 + (h & 1) * (B + B * XP));
+    xs = (float*)labs + B;
     if (mine && pf && next) {  // in flight while this step computes
       const int32_t* r = rows + (h + 1) * B;
       rows_load(a.X, r, D4, B * D4, t, pre);
@@ -482,11 +503,13 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
     }
     __syncthreads();
     if (mine) {
-      if (t < 64) {  // mean loss: lane-strided rows in order, then a butterfly
+      if (wr == 3) {  // mean loss (the wave with the fewest gradient blocks):
+        // lane-strided rows in order, then a butterfly
+        const int lane = t & 63;
         float lsum = 0.f;
-        for (int b = t; b < B; b += 64) lsum += lrow[b];
+        for (int b = lane; b < B; b += 64) lsum += lrow[b];
         lsum = wave_sum_fixed(lsum);
-        if (t == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
+        if (lane == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
       }
       // weight gradient and update: blocks of 16 features (the bias row as
       // feature D, whose input is 1) x 16 classes, wave rank wr taking
@@ -526,28 +549,27 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
         }
       }
     }
-    if (next) {
-      __syncthreads();  // the step's last reads of its rows and labels
-      if (mine) {
-        if (pf) {
-          rows_store(xs, XP, D4, B * D4, t, pre);
-          if (t < B) labs[t] = lab_next;
-        } else {
-          stage_sync(h + 1);
-        }
+    if (next && mine) {  // into the other buffer, last read two steps ago
+      labs = (int32_t*)bufn;
+      xs = bufn + B;
+      if (pf) {
+        rows_store(xs, XP, D4, B * D4, t, pre);
+        if (t < B) labs[t] = lab_next;
+      } else {
+        stage_sync(h + 1);
       }
     }
     __syncthreads();
   }
-  for (int p = threadIdx.x; p < P; p += kWideThreads) {
-    const int i = p / C, c = p - i * C;
-    const float mean = tree_sum_le4(Wl + i * CM + c, PL, K) / (float)K;
-    for (int kk = 0; kk < K; ++kk) a.W[kk * a.Ps + p] = mean;
-  }
-#pragma unroll 4
-  for (int e = threadIdx.x; e < K * P; e += kWideThreads) {
-    const int kk = e / P, p = e - kk * P, i = p / C, c = p - i * C;
-    a.U[kk * a.Ps + p] = Ul[(long long)kk * PL + i * CM + c];
+  for (int e = threadIdx.x; e < PL; e += kWideThreads) {
+    const int i = e / CM, c = e % CM, p = i * C + c;
+    if (c < C) {
+      const float mean = tree_sum_le4(Wl + e, PL, K) / (float)K;
+      for (int kk = 0; kk < K; ++kk) {
+        a.W[kk * a.Ps + p] = mean;
+        a.U[kk * a.Ps + p] = Ul[kk * PL + e];
+      }
+    }
   }
 }
 
@@ -563,7 +585,7 @@ size_t tiny_round_lds_bytes(int K, int B, int D, int C) {
 size_t tiny_wide_lds_bytes(int K, int B, int D, int C, int H) {
   const int CM = tiny_classes(C);
   const long long rep =
-      ((long long)B * CM + 2LL * B + (long long)B * (D | 1) + (long long)H * B + 3) & ~3LL;
+      ((long long)B * CM + B + (long long)H * B + 2LL * (B + (long long)B * (D | 1)) + 3) & ~3LL;
   return (size_t)(2LL * K * (D + 1) * CM + K * rep) * sizeof(float);
 }
 
