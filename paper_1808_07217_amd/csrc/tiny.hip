@@ -312,15 +312,15 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   const int l16 = t & 15, lq = (t & 63) >> 4, wr = ((t >> 6) - k) & 3;
   const bool mine = k < K;
   const int XP = D | 1;
-  // per replica: dZ [B][CM], row losses [B], sampled row indices [H][B],
+  // per replica: dZ [B][CM], row loss terms [B][2], sampled row indices [H][B],
   // then two buffers (steps of even / odd index) of labels [B] and rows
   // [B][XP]: the next step's batch is stored while this step still reads its
   // own
-  const int RS = (B * CM + B + H * B + 2 * (B + B * XP) + 3) & ~3;
+  const int RS = (B * CM + 2 * B + H * B + 2 * (B + B * XP) + 3) & ~3;
   float* dz = Ul + (long long)K * PL + (mine ? k : 0) * RS;
   float* lrow = dz + B * CM;
-  int32_t* rows = (int32_t*)(lrow + B);
-  float* const buf0 = lrow + B + H * B;
+  int32_t* rows = (int32_t*)(lrow + 2 * B);
+  float* const buf0 = lrow + 2 * B + H * B;
   int32_t* labs = (int32_t*)buf0;
   float* xs = buf0 + B;
 
@@ -497,7 +497,10 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
               *(v4f*)(dz + br * CM + c4) = d;
             }
           }
-          if (lq == 0) lrow[br] = zy >= m ? log1pf(rest) : (m - zy) + logf(s);
+          if (lq == 0) {  // the loss's terms; its logarithm on the loss wave
+            lrow[2 * br] = m - zy;
+            lrow[2 * br + 1] = zy >= m ? rest : s;
+          }
         }
       }
     }
@@ -507,7 +510,10 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
         // lane-strided rows in order, then a butterfly
         const int lane = t & 63;
         float lsum = 0.f;
-        for (int b = lane; b < B; b += 64) lsum += lrow[b];
+        for (int b = lane; b < B; b += 64) {
+          const float d = lrow[2 * b], v = lrow[2 * b + 1];
+          lsum += d <= 0.f ? log1pf(v) : d + logf(v);  // d = 0: the label is the max
+        }
         lsum = wave_sum_fixed(lsum);
         if (lane == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
       }
@@ -585,7 +591,7 @@ size_t tiny_round_lds_bytes(int K, int B, int D, int C) {
 size_t tiny_wide_lds_bytes(int K, int B, int D, int C, int H) {
   const int CM = tiny_classes(C);
   const long long rep =
-      ((long long)B * CM + B + (long long)H * B + 2LL * (B + (long long)B * (D | 1)) + 3) & ~3LL;
+      ((long long)B * CM + 2LL * B + (long long)H * B + 2LL * (B + (long long)B * (D | 1)) + 3) & ~3LL;
   return (size_t)(2LL * K * (D + 1) * CM + K * rep) * sizeof(float);
 }
 
