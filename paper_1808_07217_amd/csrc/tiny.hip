@@ -5,6 +5,10 @@
 // the multi-kernel round of such a problem is 13 launches for H = 4 -- so the
 // whole round runs from LDS with no launch between its steps.
 //
+// Two kernels: k_tiny_round_wide (further down) gives each of up to four
+// replicas 256 threads and puts both products on the matrix cores;
+// k_tiny_round, for more replicas or when the former's LDS does not fit:
+//
 // Workgroup layout: four waves; replica k belongs to wave k mod 4. Per local
 // step and replica, its wave
 //   samples B indices (the configured sampler),
