@@ -231,19 +231,33 @@ __global__ __launch_bounds__(kTinyThreads) void k_tiny_round(TinyArgs a) {
 }
 
 // The same round with a group of 256 threads (four waves) per replica, up
-// to four replicas in 1024 threads. The rows of all H steps are sampled up
-// front, and while a step computes, the rows and labels of the next step are
-// already in flight into registers (stored to LDS after the step's last read
-// of them), so no step waits on global memory. Both contractions of a step
-// run on the matrix cores with their operands read from LDS: the logits
-// Z = X W as 16-row blocks of v_mfma_f32_16x16x4f32 over the input features,
-// and the gradient dW = X^T [dZ] (the bias row as a feature whose input is 1)
-// as 16-feature blocks over the rows, each followed by the update of its
-// block. A row's 16 classes sit on one 16-lane DPP row of the accumulator,
-// so its max, sums and label logit are DPP butterflies. The mean loss adds
-// the rows' losses lane-strided in ascending order, then a fixed butterfly.
-// The same layout of replicas in LDS as k_tiny_round, the same average and
-// write-back.
+// to four replicas in 1024 threads. Both contractions of a step run on the
+// matrix cores (v_mfma_f32_16x16x4f32) with their operands read from LDS:
+//   logits Z^T = W^T X^T as blocks of 16 rows, over the input features;
+//   gradient dW = X^T dZ (the bias as a feature whose input is 1) as blocks of
+//     16 features x 16 classes, over the batch rows, each block followed by
+//     the momentum step of its entries.
+// Lane l then holds four classes of row l % 16, so a row's max, sums and
+// label logit are one butterfly over four lanes; the logarithms of the row
+// losses are taken by the wave with the fewest gradient blocks, which adds
+// them lane-strided in ascending order, then by a fixed butterfly.
+//
+// LDS layout per replica (all pitches multiples of 4 floats, so that every
+// MFMA operand of the forward and every update is one float4 access):
+//   Wt, Ut [CM][DP]: class-major weights and buffers, entry (c, i) = weight
+//     of input i (i = D: the bias) for class c; columns D + 1 .. DP - 1 and
+//     classes C .. CM - 1 are zero and stay zero through every update.
+//   xs [B16][XP] (two buffers, with labels [B]): the batch rows; columns D ..
+//     XP - 1 and rows B .. B16 - 1 are zero, so the forward needs no masks.
+//   dz [B16][CM]: dZ, rows B .. B16 - 1 zero.
+// The MFMA k index is remapped (lane quarter q takes k = 4 q .. 4 q + 3 of a
+// 16-deep trip), so each lane's four k values are contiguous in LDS.
+//
+// The rows of all H steps are sampled up front; while a step computes, the
+// next step's rows and labels are in flight into registers and are stored
+// into the other buffer at the end of the step (two barriers per step). Wave
+// ranks are rotated by replica, so a phase with fewer blocks than waves
+// spreads over the four SIMDs. The average is the replica-average tree's.
 constexpr int kWideThreads = 1024, kRepThreads = 256;
 
 // Reductions over the four lanes l % 16 + 16 q of a wave (xor 16, then xor
@@ -292,13 +306,22 @@ __device__ __forceinline__ void rows_store(float* xs, int XP, int D4, int nel, i
     const int e = t + kRepThreads * j;
     if (e < nel) {
       const int b = e / D4, i4 = e - b * D4;
-      float* d = xs + b * XP + 4 * i4;
-      d[0] = v[j][0];
-      d[1] = v[j][1];
-      d[2] = v[j][2];
-      d[3] = v[j][3];
+      *(v4f*)(xs + b * XP + 4 * i4) = v[j];
     }
   }
+}
+
+// Pitches of the wide kernel's LDS layout (see above).
+__host__ __device__ inline int wide_dp(int D) {  // Wt row: >= D + 1 and >= ceil16(D)
+  const int a = (D + 4) & ~3, b = (D + 15) & ~15;
+  return a > b ? a : b;
+}
+__host__ __device__ inline int wide_xp(int D) { return ((D + 15) & ~15) + 4; }
+__host__ __device__ inline int wide_rep_floats(int B, int D, int CM, int H) {
+  const int B16 = (B + 15) & ~15;
+  const int head = (B16 * CM + 2 * B + H * B + 3) & ~3;   // dz, loss terms, rows
+  const int buf = (B16 * wide_xp(D) + B + 3) & ~3;         // xs + labels
+  return head + 2 * buf;
 }
 
 template <int CM>
@@ -306,30 +329,31 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   constexpr int NCB = CM >= 16 ? CM / 16 : 1;  // blocks of 16 classes
   extern __shared__ float lds[];
   const int K = a.K, B = a.B, D = a.D, C = a.C, H = a.H;
-  const int PL = (D + 1) * CM;
-  float* Wl = lds;                        // [K][D + 1][CM]
-  float* Ul = Wl + (long long)K * PL;     // [K][D + 1][CM]
+  const int DP = wide_dp(D), XP = wide_xp(D), B16 = (B + 15) & ~15;
+  const int PL = CM * DP;
+  float* Wl = lds;                        // [K][CM][DP]
+  float* Ul = Wl + (long long)K * PL;     // [K][CM][DP]
   const int k = threadIdx.x / kRepThreads, t = threadIdx.x % kRepThreads;
   // MFMA lane row and quarter; the wave's rank in its group, rotated by the
   // replica so that the first waves of the four groups (the only ones with
   // work when a phase has fewer blocks than waves) sit on different SIMDs
   const int l16 = t & 15, lq = (t & 63) >> 4, wr = ((t >> 6) - k) & 3;
   const bool mine = k < K;
-  const int XP = D | 1;
-  // per replica: dZ [B][CM], row loss terms [B][2], sampled row indices [H][B],
-  // then two buffers (steps of even / odd index) of labels [B] and rows
-  // [B][XP]: the next step's batch is stored while this step still reads its
-  // own
-  const int RS = (B * CM + 2 * B + H * B + 2 * (B + B * XP) + 3) & ~3;
-  float* dz = Ul + (long long)K * PL + (mine ? k : 0) * RS;
-  float* lrow = dz + B * CM;
-  int32_t* rows = (int32_t*)(lrow + 2 * B);
-  float* const buf0 = lrow + 2 * B + H * B;
-  int32_t* labs = (int32_t*)buf0;
-  float* xs = buf0 + B;
+  const int RS = wide_rep_floats(B, D, CM, H);
+  float* dz = Ul + (long long)K * PL + (mine ? k : 0) * RS;   // [B16][CM]
+  float* lrow = dz + B16 * CM;                                 // [B][2]
+  int32_t* rows = (int32_t*)(lrow + 2 * B);                    // [H][B]
+  const int BUF = (B16 * XP + B + 3) & ~3;
+  float* const buf0 = dz + ((B16 * CM + 2 * B + H * B + 3) & ~3);
+  float* xs = buf0;                                            // [B16][XP]
+  int32_t* labs = (int32_t*)(buf0 + B16 * XP);                 // [B]
 
   const long long lo = (long long)k * a.N / K;
-  if (mine) {  // every step's rows
+  if (mine) {
+    // zero padding: both row buffers and dZ's rows past the batch
+    for (int e = t; e < 2 * BUF; e += kRepThreads) buf0[e] = 0.f;
+    for (int e = B * CM + t; e < B16 * CM; e += kRepThreads) dz[e] = 0.f;
+    // every step's rows
     if (a.S > 0) {  // per-epoch reshuffled partition
       for (int e = t; e < H * B; e += kRepThreads) {
         const int h = e / B, b = e - h * B;
@@ -368,12 +392,7 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
 #pragma unroll 4
       for (int e = t; e < B * D4; e += kRepThreads) {
         const int b = e / D4, i4 = e - b * D4;
-        const v4f v = *(const v4f*)(a.X + (long long)r[b] * D + 4 * i4);
-        float* d = xs + b * XP + 4 * i4;
-        d[0] = v[0];
-        d[1] = v[1];
-        d[2] = v[2];
-        d[3] = v[3];
+        *(v4f*)(xs + b * XP + 4 * i4) = *(const v4f*)(a.X + (long long)r[b] * D + 4 * i4);
       }
     } else {
 #pragma unroll 4
@@ -389,16 +408,17 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
     rows_load(a.X, rows, D4, B * D4, t, pre);
     lab_next = a.y[rows[t < B ? t : 0]];
   }
-  // replica by replica over the padded layout: the row and class of an
-  // entry are a shift and a mask (CM is a power of two)
+  // replica by replica, input-major over the padded layout (the row and
+  // class of an entry are a shift and a mask), transposed into LDS
   for (int kk = 0; kk < K; ++kk)
 #pragma unroll 2
-    for (int e = threadIdx.x; e < PL; e += kWideThreads) {
+    for (int e = threadIdx.x; e < DP * CM; e += kWideThreads) {
       const int i = e / CM, c = e % CM;
-      const long long g = (long long)kk * a.Ps + i * C + (c < C ? c : 0);
+      const bool ok = c < C && i <= D;
+      const long long g = (long long)kk * a.Ps + (i <= D ? i : D) * C + (c < C ? c : 0);
       const float w = a.W[g], u = a.U[g];
-      Wl[kk * PL + e] = c < C ? w : 0.f;
-      Ul[kk * PL + e] = c < C ? u : 0.f;
+      Wl[kk * PL + c * DP + i] = ok ? w : 0.f;
+      Ul[kk * PL + c * DP + i] = ok ? u : 0.f;
     }
   if (mine) {
     if (pf) {
@@ -416,52 +436,39 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   for (int h = 0; h < H; ++h) {
     const float lr = a.lr[h];
     const bool next = h + 1 < H;
-    float* const bufn = buf0 + ((h + 1) & 1) * (B + B * XP);  // the next step's
-    labs = (int32_t*)(buf0 + (h & 1) * (B + B * XP));
-    xs = (float*)labs + B;
+    xs = buf0 + (h & 1) * BUF;
+    labs = (int32_t*)(xs + B16 * XP);
     if (mine && pf && next) {  // in flight while this step computes
       const int32_t* r = rows + (h + 1) * B;
       rows_load(a.X, r, D4, B * D4, t, pre);
       lab_next = a.y[r[t < B ? t : 0]];
     }
     if (mine) {
-      // forward, loss, dZ: wave rank wr takes row blocks wr, wr + 4, ... of
-      // 16 rows; Z^T = W^T X^T on v_mfma_f32_16x16x4f32 over k = input
-      // features, operands read from LDS (padded rows, features and classes
-      // read as 0), so that lane l holds classes 4 (l / 16) + j (+ 16 cb) of
-      // row l % 16: a row's softmax is one lane's classes and a butterfly
-      // over the four lanes l % 16 + 16 q
-      const int nrb = (B + 15) >> 4;
+      // forward, loss terms, dZ: wave rank wr takes row blocks wr, wr + 4, ...
+      const int nrb = B16 >> 4;
       for (int rb = wr; rb < nrb; rb += kRepThreads / 64) {
         const int br = rb * 16 + l16;
-        const bool rok = br < B;
-        const float* xb = xs + (rok ? br : 0) * XP;
+        const float* xb = xs + br * XP + 4 * lq;
         v4f acc[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[cb] = (v4f){0.f, 0.f, 0.f, 0.f};
-        // four k steps per trip (a whole trip's operands read before its
-        // MFMAs); steps past D read zeros
         for (int k0 = 0; k0 < D; k0 += 16) {
-          float xv[4], wv4[4][NCB];
+          const v4f xv = *(const v4f*)(xb + k0);
+          v4f wv[NCB];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int kk = k0 + 4 * u + lq;
-            const bool kok = kk < D;
-            const float x = xb[kok ? kk : 0];  // addresses clamped, values zeroed
-            xv[u] = rok && kok ? x : 0.f;
-#pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-              const int c = cb * 16 + l16;
-              const float w = W[(kok ? kk : 0) * CM + (c < CM ? c : 0)];
-              wv4[u][cb] = kok && c < CM ? w : 0.f;
-            }
+          for (int cb = 0; cb < NCB; ++cb) {
+            const int c = cb * 16 + l16;
+            const v4f w = *(const v4f*)(W + (c < CM ? c : 0) * DP + k0 + 4 * lq);
+            wv[cb] = c < CM ? w : (v4f){0.f, 0.f, 0.f, 0.f};
           }
 #pragma unroll
           for (int u = 0; u < 4; ++u)
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb)
-              acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv4[u][cb], xv[u], acc[cb], 0, 0, 0);
+              acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[cb][u], xv[u], acc[cb], 0, 0, 0);
         }
+        // lane holds the logits of row br, classes cb * 16 + 4 lq + j
+        const bool rok = br < B;
         const int lab = labs[rok ? br : 0];
         float z[NCB][4], zl[NCB][4], m = -INFINITY;
 #pragma unroll
@@ -469,7 +476,7 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int c = cb * 16 + 4 * lq + j;
-            zl[cb][j] = acc[cb][j] + W[D * CM + (c < C ? c : 0)];
+            zl[cb][j] = acc[cb][j] + W[(c < C ? c : 0) * DP + D];
             z[cb][j] = c < C ? zl[cb][j] : -INFINITY;
             m = z[cb][j] > m ? z[cb][j] : m;
           }
@@ -521,47 +528,47 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
         lsum = wave_sum_fixed(lsum);
         if (lane == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
       }
-      // weight gradient and update: blocks of 16 features (the bias row as
-      // feature D, whose input is 1) x 16 classes, wave rank wr taking
-      // blocks wr, wr + 4, ...; dW = X^T dZ on v_mfma_f32_16x16x4f32 over k = rows
+      // weight gradient and update: wave rank wr takes blocks wr, wr + 4, ...
       const int nib = (D + 16) >> 4;  // ceil((D + 1) / 16)
       for (int blk = wr; blk < nib * NCB; blk += kRepThreads / 64) {
         const int ib = blk / NCB, cb = blk - ib * NCB;
         const int ia = ib * 16 + l16, cn = cb * 16 + l16;
+        const int iac = ia < XP ? ia : XP - 1;     // columns D + 1 .. XP - 1 are zero
+        const int cnc = cn < CM ? cn : 0;
         v4f acc = (v4f){0.f, 0.f, 0.f, 0.f};
-        for (int b0 = 0; b0 < B; b0 += 16) {  // as above: rows past B read zeros
+        for (int b0 = 0; b0 < B; b0 += 16) {  // rows past B are zero
           float av[4], bv[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const int b = b0 + 4 * u + lq;
-            const bool bok = b < B;
-            const int bc = bok ? b : 0;
-            const float x = xs[bc * XP + (ia < D ? ia : 0)], g = dz[bc * CM + (cn < CM ? cn : 0)];
-            av[u] = !bok ? 0.f : ia < D ? x : ia == D ? 1.f : 0.f;
-            bv[u] = bok && cn < CM ? g : 0.f;
+            const int b = b0 + 4 * lq + u;
+            const float x = xs[b * XP + iac], g = dz[b * CM + cnc];
+            av[u] = ia == D ? 1.f : x;
+            bv[u] = cn < CM ? g : 0.f;
           }
 #pragma unroll
           for (int u = 0; u < 4; ++u)
             acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], acc, 0, 0, 0);
         }
-        // lane holds the gradient of features ib * 16 + 4 lq + j, class cn
-        const float wd = a.wd;
+        // lane holds the gradient of inputs ib * 16 + 4 lq + j, class cn: one
+        // float4 of Wt and Ut (padding entries get a zero gradient and stay 0)
+        const int i0 = ib * 16 + 4 * lq;
+        if (i0 < DP && cn < CM) {
+          const float wd = a.wd;
+          v4f w = *(v4f*)(W + cn * DP + i0), u = *(v4f*)(U + cn * DP + i0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int i = ib * 16 + 4 * lq + j;
-          if (i <= D && cn < CM) {
-            const float w = W[i * CM + cn], u = U[i * CM + cn];
-            const float gg = __builtin_fmaf(wd, w, acc[j]);
-            const float un = __builtin_fmaf(a.mom, u, gg);
-            W[i * CM + cn] = __builtin_fmaf(-lr, step_dir(un, gg, a.mom, a.mode), w);
-            U[i * CM + cn] = un;
+          for (int j = 0; j < 4; ++j) {
+            const float gg = __builtin_fmaf(wd, w[j], acc[j]);
+            u[j] = __builtin_fmaf(a.mom, u[j], gg);
+            w[j] = __builtin_fmaf(-lr, step_dir(u[j], gg, a.mom, a.mode), w[j]);
           }
+          *(v4f*)(W + cn * DP + i0) = w;
+          *(v4f*)(U + cn * DP + i0) = u;
         }
       }
     }
     if (next && mine) {  // into the other buffer, last read two steps ago
-      labs = (int32_t*)bufn;
-      xs = bufn + B;
+      xs = buf0 + ((h + 1) & 1) * BUF;
+      labs = (int32_t*)(xs + B16 * XP);
       if (pf) {
         rows_store(xs, XP, D4, B * D4, t, pre);
         if (t < B) labs[t] = lab_next;
@@ -571,13 +578,13 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
     }
     __syncthreads();
   }
-  for (int e = threadIdx.x; e < PL; e += kWideThreads) {
+  for (int e = threadIdx.x; e < (D + 1) * CM; e += kWideThreads) {
     const int i = e / CM, c = e % CM, p = i * C + c;
     if (c < C) {
-      const float mean = tree_sum_le4(Wl + e, PL, K) / (float)K;
+      const float mean = tree_sum_le4(Wl + c * DP + i, PL, K) / (float)K;
       for (int kk = 0; kk < K; ++kk) {
         a.W[kk * a.Ps + p] = mean;
-        a.U[kk * a.Ps + p] = Ul[kk * PL + e];
+        a.U[kk * a.Ps + p] = Ul[kk * PL + c * DP + i];
       }
     }
   }
@@ -594,9 +601,8 @@ size_t tiny_round_lds_bytes(int K, int B, int D, int C) {
 }
 size_t tiny_wide_lds_bytes(int K, int B, int D, int C, int H) {
   const int CM = tiny_classes(C);
-  const long long rep =
-      ((long long)B * CM + 2LL * B + (long long)H * B + 2LL * (B + (long long)B * (D | 1)) + 3) & ~3LL;
-  return (size_t)(2LL * K * (D + 1) * CM + K * rep) * sizeof(float);
+  return (size_t)(2LL * K * CM * wide_dp(D) + (long long)K * wide_rep_floats(B, D, CM, H)) *
+         sizeof(float);
 }
 
 // The kernel's dynamic LDS above the default 64 KB: requested once per
