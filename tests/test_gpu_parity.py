@@ -183,13 +183,15 @@ def test_softmax_regression_single_launch_rounds():
 @pytest.mark.parametrize("K,B,D,nesterov,momentum,sampler", [
     (5, 70, 24, False, 0.9, "iid"), (3, 20, 24, True, 0.9, "epoch"),
     (8, 8, 24, False, 0.0, "iid"), (1, 33, 24, True, 0.5, "epoch"),
-    (2, 200, 24, False, 0.9, "iid"), (4, 30, 23, True, 0.9, "epoch")])
+    (2, 200, 24, False, 0.9, "iid"), (4, 30, 23, True, 0.9, "epoch"),
+    (3, 20, 32, True, 0.9, "iid")])
 def test_single_launch_round_variants(K, B, D, nesterov, momentum, sampler):
     """The single-launch round on ragged shapes: more replicas than waves
     (idle waves in the last slot), batches beyond one wave of rows, up to four
     replicas with a 256-thread group each (next step's rows prefetched, or
     staged between steps for a large batch or an input width not a multiple
-    of 4), both samplers, heavy ball / Nesterov / plain SGD, step sizes
+    of 4; input widths with and without padding to the 16-deep MFMA steps),
+    both samplers, heavy ball / Nesterov / plain SGD, step sizes
     changing inside a round; every round against the oracle, and against the
     step-by-step multi-kernel path within fp32 rounding."""
     w = _small((D, 7), K=K, B=B, N=600, H=3, rounds=4, momentum=momentum,
