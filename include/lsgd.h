@@ -184,7 +184,13 @@ lsgd_status lsgd_synchronise(lsgd_ctx* ctx, float lr);
 /* H local steps with step sizes h_lr[0..H-1] (host array), then
  * lsgd_synchronise(ctx, h_lr[H-1]) (lsgd_average without global momentum).
  * d_loss: fp32 [H][K] or NULL. With global momentum, H == 0 or a zero last
- * step size is LSGD_E_INVALID. */
+ * step size is LSGD_E_INVALID.
+ * A one-layer fp32 model (softmax regression) under the plain local scheme
+ * without global momentum, with 1 <= H <= 64, at most 32 classes and all
+ * replicas and buffers within one workgroup's LDS, runs the whole round as a
+ * single launch. Its products sum in a different fixed order than the
+ * step-by-step path, so the two agree to fp32 rounding, not bit for bit;
+ * each is deterministic. */
 lsgd_status lsgd_run_round(lsgd_ctx* ctx, int32_t H, const float* h_lr,
                            float* d_loss);
 
