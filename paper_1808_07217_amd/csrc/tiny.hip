@@ -351,7 +351,8 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
   const long long lo = (long long)k * a.N / K;
   if (mine) {
     // zero padding: both row buffers and dZ's rows past the batch
-    for (int e = t; e < 2 * BUF; e += kRepThreads) buf0[e] = 0.f;
+    for (int e = 4 * t; e < 2 * BUF; e += 4 * kRepThreads)
+      *(v4f*)(buf0 + e) = (v4f){0.f, 0.f, 0.f, 0.f};
     for (int e = B * CM + t; e < B16 * CM; e += kRepThreads) dz[e] = 0.f;
     // every step's rows
     if (a.S > 0) {  // per-epoch reshuffled partition
@@ -408,18 +409,34 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
     rows_load(a.X, rows, D4, B * D4, t, pre);
     lab_next = a.y[rows[t < B ? t : 0]];
   }
-  // replica by replica, input-major over the padded layout (the row and
-  // class of an entry are a shift and a mask), transposed into LDS
-  for (int kk = 0; kk < K; ++kk)
-#pragma unroll 2
-    for (int e = threadIdx.x; e < DP * CM; e += kWideThreads) {
-      const int i = e / CM, c = e % CM;
-      const bool ok = c < C && i <= D;
-      const long long g = (long long)kk * a.Ps + (i <= D ? i : D) * C + (c < C ? c : 0);
-      const float w = a.W[g], u = a.U[g];
-      Wl[kk * PL + c * DP + i] = ok ? w : 0.f;
-      Ul[kk * PL + c * DP + i] = ok ? u : 0.f;
-    }
+  // the replicas, input-major over the padded layout (the row and class of
+  // an entry are a shift and a mask), transposed into LDS: per chunk all
+  // four replicas' loads (clamped, unconditional) before any store, so they
+  // share one round trip
+  for (int e0 = threadIdx.x; e0 < DP * CM; e0 += 2 * kWideThreads) {
+    float wv[4][2], uv[4][2];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int e = min(e0 + r * kWideThreads, DP * CM - 1), i = e / CM, c = e % CM;
+        const long long g =
+            (long long)min(kk, K - 1) * a.Ps + (i <= D ? i : D) * C + (c < C ? c : 0);
+        wv[kk][r] = a.W[g];
+        uv[kk][r] = a.U[g];
+      }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int e = e0 + r * kWideThreads, i = e / CM, c = e % CM;
+        if (kk < K && e < DP * CM) {
+          const bool ok = c < C && i <= D;
+          Wl[kk * PL + c * DP + i] = ok ? wv[kk][r] : 0.f;
+          Ul[kk * PL + c * DP + i] = ok ? uv[kk][r] : 0.f;
+        }
+      }
+  }
   if (mine) {
     if (pf) {
       rows_store(xs, XP, D4, B * D4, t, pre);
