@@ -249,7 +249,8 @@ __global__ __launch_bounds__(kTinyThreads) void k_tiny_round(TinyArgs a) {
 //     classes C .. CM - 1 are zero and stay zero through every update.
 //   xs [B16][XP] (two buffers, with labels [B]): the batch rows; columns D ..
 //     XP - 1 and rows B .. B16 - 1 are zero, so the forward needs no masks.
-//   dz [B16][CM]: dZ, rows B .. B16 - 1 zero.
+//   dz [B16][CM]: dZ, rows B .. B16 - 1 zero; the rows' loss terms [B][2];
+//     the sampled row indices of every step [H][B].
 // The MFMA k index is remapped (lane quarter q takes k = 4 q .. 4 q + 3 of a
 // 16-deep trip), so each lane's four k values are contiguous in LDS.
 //
