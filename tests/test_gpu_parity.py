@@ -180,21 +180,23 @@ def test_softmax_regression_single_launch_rounds():
     assert set(reps.profile_report()) == {"tiny_round"}
 
 
-@pytest.mark.parametrize("K,B,D,nesterov,momentum,sampler", [
-    (5, 70, 24, False, 0.9, "iid"), (3, 20, 24, True, 0.9, "epoch"),
-    (8, 8, 24, False, 0.0, "iid"), (1, 33, 24, True, 0.5, "epoch"),
-    (2, 200, 24, False, 0.9, "iid"), (4, 30, 23, True, 0.9, "epoch"),
-    (3, 20, 32, True, 0.9, "iid")])
-def test_single_launch_round_variants(K, B, D, nesterov, momentum, sampler):
+@pytest.mark.parametrize("K,B,D,C,nesterov,momentum,sampler", [
+    (5, 70, 24, 7, False, 0.9, "iid"), (3, 20, 24, 7, True, 0.9, "epoch"),
+    (8, 8, 24, 7, False, 0.0, "iid"), (1, 33, 24, 7, True, 0.5, "epoch"),
+    (2, 200, 24, 7, False, 0.9, "iid"), (4, 30, 23, 7, True, 0.9, "epoch"),
+    (3, 20, 32, 7, True, 0.9, "iid"), (4, 16, 40, 20, False, 0.9, "iid"),
+    (6, 12, 40, 20, True, 0.9, "epoch")])
+def test_single_launch_round_variants(K, B, D, C, nesterov, momentum, sampler):
     """The single-launch round on ragged shapes: more replicas than waves
     (idle waves in the last slot), batches beyond one wave of rows, up to four
     replicas with a 256-thread group each (next step's rows prefetched, or
     staged between steps for a large batch or an input width not a multiple
-    of 4; input widths with and without padding to the 16-deep MFMA steps),
-    both samplers, heavy ball / Nesterov / plain SGD, step sizes
-    changing inside a round; every round against the oracle, and against the
-    step-by-step multi-kernel path within fp32 rounding."""
-    w = _small((D, 7), K=K, B=B, N=600, H=3, rounds=4, momentum=momentum,
+    of 4; input widths with and without padding to the 16-deep MFMA steps;
+    classes padded to 8 and to 32), both samplers, heavy ball / Nesterov /
+    plain SGD, step sizes changing inside a round; every round against the
+    oracle, and against the step-by-step multi-kernel path within fp32
+    rounding."""
+    w = _small((D, C), K=K, B=B, N=600, H=3, rounds=4, momentum=momentum,
                nesterov=nesterov, lr=0.05).scaled(sampler=sampler)
     X, y, w0 = _small_data(w, seed=K + B)
     lrs = [0.05, 0.03, 0.04]
