@@ -220,6 +220,31 @@ def test_single_launch_round_variants(K, B, D, C, nesterov, momentum, sampler):
     assert set(a.profile_report()) == {"tiny_round"}
 
 
+def test_single_launch_round_longest():
+    """The longest round one launch takes (H = 64: every step's rows sampled
+    up front, the largest LDS request of the softmax shape) against the
+    oracle and the step-by-step path; H = 65 takes the multi-kernel path."""
+    w = _small((64, 10), K=4, B=32, N=2000, H=64, rounds=1, momentum=0.9,
+               nesterov=True, lr=0.02)
+    X, y, w0 = _small_data(w, seed=64)
+    for H, single in ((64, True), (65, False)):
+        a, b = make_replicas(w, X, y, w0), make_replicas(w, X, y, w0)
+        a.profile(True)
+        st = O.State(w0, w.K)
+        loss = torch.empty(H, w.K, device=device())
+        a.run_round([w.lr] * H, loss)
+        for _ in range(H):
+            b.local_step(w.lr)
+        b.average()
+        want = O.run_round(st, w, X, y, H, w.lr)
+        assert np.all(rel(loss.cpu().numpy(), want) <= LOSS_TOL_FP32), H
+        got = a.read_params(0).cpu().numpy()
+        assert normwise(got, st.W[0]) <= PARAM_TOL_FP32, H
+        assert normwise(got, b.read_params(0).cpu().numpy()) <= 1e-6, H
+        tags = set(a.profile_report())
+        assert (tags == {"tiny_round"}) == single, (H, tags)
+
+
 def test_h1_local_sgd_equals_minibatch_sgd_on_gpu():
     """H = 1 local SGD is mini-batch SGD with batch K * B_loc (the paper's
     special case below eq. 2): the GPU run against the oracle's separately
