@@ -245,6 +245,28 @@ def test_single_launch_round_longest():
         assert (tags == {"tiny_round"}) == single, (H, tags)
 
 
+@pytest.mark.parametrize("K,C", [(4, 10), (6, 20)])
+def test_single_launch_rounds_are_bitwise_deterministic(K, C):
+    """Two fresh runs of five single-launch rounds (the 256-thread kernel at
+    K = 4, the wave-per-replica kernel at K = 6): bit-identical parameters,
+    momentum buffers and losses."""
+    w = _small((64, C), K=K, B=32, N=2000, H=4, rounds=5, momentum=0.9, lr=0.05)
+    X, y, w0 = _small_data(w, seed=11)
+    outs = []
+    for _ in range(2):
+        reps = make_replicas(w, X, y, w0)
+        reps.profile(True)
+        loss = torch.empty(5 * 4, w.K, device=device())
+        for r in range(5):
+            reps.run_round([w.lr] * 4, loss[4 * r:4 * r + 4])
+        assert set(reps.profile_report()) == {"tiny_round"}
+        outs.append((reps.read_params(0).cpu().numpy(),
+                     np.stack([reps.read_momentum(k).cpu().numpy() for k in range(w.K)]),
+                     loss.cpu().numpy()))
+    for a, b in zip(outs[0], outs[1]):
+        np.testing.assert_array_equal(a, b)
+
+
 def test_h1_local_sgd_equals_minibatch_sgd_on_gpu():
     """H = 1 local SGD is mini-batch SGD with batch K * B_loc (the paper's
     special case below eq. 2): the GPU run against the oracle's separately
