@@ -383,6 +383,10 @@ def synchronise(state, wl, lr):
     else:
         state.W = average(state.W)
         state.w_sync = state.W[0].copy()
+    if getattr(state, "RS", None) is not None:
+        # BN running statistics are not trained: every scheme takes their
+        # plain mean over the workers
+        state.RS = average(state.RS)
 
 
 def average_blocks(W, Kb):
@@ -405,7 +409,9 @@ def average_blocks(W, Kb):
 # --------------------------------------------------------------------------
 class State:
     """K replicas w^k, their momentum buffers u^k, and the step counter; for
-    global momentum also the synchronised model w_(t) and its buffer u."""
+    global momentum also the synchronised model w_(t) and its buffer u; for
+    the ResNet its per-replica BN running statistics RS [K][R] (created at the
+    first local step, see resnet_running_init)."""
 
     def __init__(self, w0, K):
         self.W = np.repeat(np.asarray(w0, np.float64)[None, :], K, axis=0)
@@ -414,6 +420,7 @@ class State:
         self.w_sync = np.asarray(w0, np.float64).copy()
         self.u_global = np.zeros_like(self.w_sync)
         self.E = np.zeros_like(self.W)     # error memories e^k (Algorithm 4)
+        self.RS = None
 
 
 def local_step(state, wl, X, y, lr, replicas=None):
@@ -426,10 +433,23 @@ def local_step(state, wl, X, y, lr, replicas=None):
     ks = range(K) if replicas is None else replicas
     losses = np.full(K, np.nan)
     mask = model_decay_mask(wl)
+    resnet = wl.model == "resnet20"
+    if resnet and getattr(state, "RS", None) is None:
+        state.RS = np.repeat(resnet_running_init(resnet_arch())[None, :], K, axis=0)
     for k in ks:
         idx = worker_indices(wl, state.step, k)
         A0 = np.asarray(X[idx], np.float64)
-        loss, grad = model_loss_and_grad(wl, state.W[k], A0, y[idx])
+        if resnet:
+            # per-worker BN: replica k's running statistics follow its batches
+            stats = []
+            loss, grad = resnet_loss_and_grad(state.W[k], resnet_arch(), A0, y[idx], stats)
+            half = state.RS.shape[1] // 2
+            for (_, o, c), (mu, var, n) in zip(resnet_running_layout(resnet_arch()), stats):
+                state.RS[k, o:o + c], state.RS[k, half + o:half + o + c] = \
+                    bn_running_update(state.RS[k, o:o + c],
+                                      state.RS[k, half + o:half + o + c], mu, var, n)
+        else:
+            loss, grad = model_loss_and_grad(wl, state.W[k], A0, y[idx])
         state.W[k], state.U[k] = sgd_update(
             state.W[k], state.U[k], grad, lr, wl.momentum, wl.weight_decay,
             wl.nesterov, mask, sign_step=getattr(wl, "scheme", "local") == "sign")
@@ -474,6 +494,8 @@ def run_hierarchical_round(state, wl, X, y, H, Hb, Kb, lr):
         for _ in range(H):
             losses.append(local_step(state, wl, X, y, lr))
         state.W = average_blocks(state.W, Kb)
+        if getattr(state, "RS", None) is not None:
+            state.RS = average_blocks(state.RS, Kb)
     synchronise(state, wl, lr)
     return np.stack(losses)
 
@@ -694,14 +716,48 @@ def batchnorm_backward(dy, cache):
     return dx, dg, dbe
 
 
+BN_MOMENTUM = 0.1
+
+
+def bn_running_update(rm, rv, mean, var, n, momentum=BN_MOMENTUM):
+    """Running statistics of one BN layer after a training-mode batch (the
+    paper keeps BN per worker and is silent on its running statistics; read
+    as the usual convention of its PyTorch implementation): an exponential
+    average with factor ``momentum`` of the batch mean and of the unbiased
+    batch variance var * n / (n - 1), ``var`` being the biased variance that
+    normalised the batch over its ``n`` values per channel."""
+    return ((1.0 - momentum) * rm + momentum * mean,
+            (1.0 - momentum) * rv + momentum * var * (n / (n - 1.0)))
+
+
+def resnet_running_layout(arch):
+    """[(name, offset, channels)] of the running statistics of one replica:
+    the running means of every BN layer in convolution order, then the
+    running variances in the same order; the flat vector has 2 * sum(C)
+    entries."""
+    out, o = [], 0
+    for name, _, co, _ in resnet_convs(arch):
+        out.append((name, o, co))
+        o += co
+    return out
+
+
+def resnet_running_init(arch):
+    """Initial running statistics: means 0, variances 1."""
+    n = sum(c for _, _, c in resnet_running_layout(arch))
+    return np.concatenate([np.zeros(n), np.ones(n)])
+
+
 def _shortcut(x, co):
     """Option A: every second pixel, channels zero-padded to co."""
     s = x[:, ::2, ::2, :]
     return np.concatenate([s, np.zeros(s.shape[:3] + (co - s.shape[3],))], axis=3)
 
 
-def resnet_loss_and_grad(w, arch, A0, y):
-    """Mean mini-batch loss and flat gradient; A0 [B][side*side*cin] NHWC."""
+def resnet_loss_and_grad(w, arch, A0, y, stats=None):
+    """Mean mini-batch loss and flat gradient; A0 [B][side*side*cin] NHWC.
+    With a list ``stats``, each BN layer appends (batch mean, biased batch
+    variance, values per channel) in convolution order."""
     p = resnet_unpack(np.asarray(w, np.float64), arch)
     B = A0.shape[0]
     x = np.asarray(A0, np.float64).reshape(B, arch["side"], arch["side"], arch["cin"])
@@ -711,6 +767,10 @@ def resnet_loss_and_grad(w, arch, A0, y):
     def cbr(x, name, stride, relu):
         y, cols = conv3x3(x, p[name + ".w"], stride)
         z, bc = batchnorm(y, p[name + ".g"], p[name + ".be"])
+        if stats is not None:
+            mu = y.mean(axis=(0, 1, 2))
+            stats.append((mu, ((y - mu) ** 2).mean(axis=(0, 1, 2)),
+                          y.shape[0] * y.shape[1] * y.shape[2]))
         tape.append((name, x.shape, stride, cols, bc))
         return np.maximum(z, 0.0) if relu else z, z
 

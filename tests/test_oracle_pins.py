@@ -127,6 +127,84 @@ def test_bf16_rounding_matches_torch_on_fp32_values():
     np.testing.assert_array_equal(O.rne_bf16(x.astype(np.float64)), ref)
 
 
+def test_bf16_rounding_points_on_a_hand_computed_network():
+    """The bf16 workload's rounding points, each made visible on a 1-1-2
+    network with one sample of class 0 whose inputs sit at bf16 ties:
+      x = 1 + 2^-8 (rounds to 1), W1 = 1 + 2^-8 (to 1), b1 = 2^-9 (fp32, not
+      rounded), W2 = [1 + 2^-8, -(1/2 + 2^-9)] (to [1, -1/2]), b2 = 0.
+    By hand: z1 = 1 + 2^-9, whose ReLU rounds to 1; z2 = [1, -1/2]; with
+    s = 1 / (1 + e^1.5) = 0.18242552..., dZ2 = [-s, s], rounded to
+    [-187, 187] 2^-10; dW2 = 1 * dZ2q; db2 = dZ2q; the input gradient
+    dZ2q W2q^T = -187 * 1.5 * 2^-10 = -0.27392578125 (ReLU slope 1), rounded to
+    -140 * 2^-9 = -0.2734375 = dW1 = db1; the loss is log(1 + e^-1.5).
+    Each single change -- leaving x, W1, the hidden activation, W2 (forward
+    or input gradient) or a dZ unrounded, or taking a bias gradient before
+    its dZ's rounding -- moves at least one of these values by >= 2^-10
+    relative (x or W1 unrounded gives a hidden activation that rounds to
+    1 + 2^-7; an unrounded W2 in the input gradient gives 141 * 2^-9)."""
+    q = 2.0 ** -8
+    w = np.array([1 + q,                      # W1 [1][1]
+                  2.0 ** -9,                  # b1
+                  1 + q, -(0.5 + q / 2),      # W2 [1][2]
+                  0.0, 0.0])                  # b2
+    A0 = np.array([[1 + q]])
+    loss, g = O.loss_and_grad(w, (1, 1, 2), A0, np.array([0]), bf16=True)
+    s = 1.0 / (1.0 + math.exp(1.5))
+    assert round(s * 1024) == 187 and abs(s * 1024 - 187) > 0.1   # not a tie
+    dz2q = 187 * 2.0 ** -10
+    dz1q = -140 * 2.0 ** -9
+    want = np.array([dz1q, dz1q, -dz2q, dz2q, -dz2q, dz2q])
+    np.testing.assert_array_equal(g, want)
+    assert abs(loss - math.log1p(math.exp(-1.5))) <= 1e-15
+    # the same network without any bf16 rounding gives other values
+    _, g32 = O.loss_and_grad(w, (1, 1, 2), A0, np.array([0]), bf16=False)
+    assert np.all(np.abs(g32 - want) >= 2.0 ** -10 * np.abs(want))
+
+
+def test_bf16_rounding_points_with_a_batch_and_a_dead_unit():
+    """Two samples and two hidden units, one of them below zero for the
+    second sample (its mask and its rounded activation of 0): the bias
+    gradients are the batch sums of the rounded dZ (each already divided by
+    the batch size), the weight gradients the rounded activations times the
+    rounded dZ. Checked against the per-sample scalar formulas written out
+    here with the rounding applied at the same points."""
+    r = O.rne_bf16
+    q = 2.0 ** -8
+    X = np.array([[1 + q, -(2 + 3 * q)], [0.75 + q / 4, 1 + 3 * q]])
+    W1 = np.array([[1 + q, 0.5 + q / 2], [0.25 + q / 8, -(1 + 3 * q)]])
+    b1 = np.array([2.0 ** -9, -0.1])
+    W2 = np.array([[1.5 + q, -1.0], [-0.5 - q / 2, 0.75]])
+    b2 = np.array([0.01, -0.02])
+    y = np.array([1, 0])
+    w = np.concatenate([W1.ravel(), b1, W2.ravel(), b2])
+    loss, g = O.loss_and_grad(w, (2, 2, 2), X, y, bf16=True)
+    gW1, gb1, gW2, gb2 = np.zeros((2, 2)), np.zeros(2), np.zeros((2, 2)), np.zeros(2)
+    losses = []
+    for b in range(2):
+        xq = [r(v) for v in X[b]]
+        z1 = [sum(xq[i] * r(W1[i, j]) for i in range(2)) + b1[j] for j in range(2)]
+        hq = [r(max(v, 0.0)) for v in z1]
+        z2 = [sum(hq[i] * r(W2[i, c]) for i in range(2)) + b2[c] for c in range(2)]
+        m = max(z2)
+        e = [math.exp(v - m) for v in z2]
+        losses.append(math.log(sum(e)) + m - z2[y[b]])
+        dz2q = [r((e[c] / sum(e) - (c == y[b])) / 2) for c in range(2)]
+        for c in range(2):
+            gb2[c] += dz2q[c]
+            for i in range(2):
+                gW2[i, c] += hq[i] * dz2q[c]
+        dz1q = [r(sum(dz2q[c] * r(W2[j, c]) for c in range(2)) * (z1[j] > 0))
+                for j in range(2)]
+        for j in range(2):
+            gb1[j] += dz1q[j]
+            for i in range(2):
+                gW1[i, j] += xq[i] * dz1q[j]
+    assert z1[0] > 0 and z1[1] < 0            # the second sample's dead unit
+    want = np.concatenate([gW1.ravel(), gb1, gW2.ravel(), gb2])
+    np.testing.assert_allclose(g, want, rtol=1e-14, atol=1e-17)
+    assert abs(loss - np.mean(losses)) <= 1e-14
+
+
 # ------------------------------------------------------------------ loss
 def _exact_ce(z, y):
     with decimal.localcontext() as ctx:
@@ -827,3 +905,134 @@ def test_resnet_decay_mask_exempts_batchnorm():
     n_bn = sum(int(np.prod(s)) for nme, s, _ in O.resnet_layout(a)
                if nme.endswith(".g") or nme.endswith(".be"))
     assert m.size == 269722 and int((m == 0).sum()) == n_bn == 2 * (16 * 7 + 32 * 6 + 64 * 6)
+
+
+# --------------------------------------- ResNet against torch's autograd / BN
+def _torch_resnet(arch, w, bns=None):
+    """The CIFAR ResNet of the oracle's architecture written with torch's
+    functional ops (CPU, fp64) from the flat parameter vector, with its own
+    unpacking: per 3x3 convolution (stem, then two per block) the weight
+    [3][3][c_in][c_out], BN scale and shift; then the classifier [c][classes]
+    and bias. BN is torch's training-mode batch_norm (momentum 0.1) on
+    running-statistic buffers that persist across calls when ``bns`` (a list
+    of (running mean, running variance) pairs) is passed back in. Returns
+    (forward(x_nhwc, labels) -> mean loss, parameters as leaf tensors in
+    vector order, the BN buffers)."""
+    import torch
+    import torch.nn.functional as F
+    convs, c = [(arch["cin"], arch["base"], 1)], arch["base"]
+    for s in range(3):
+        co = arch["base"] * 2 ** s
+        for b in range(arch["blocks"]):
+            convs += [(c, co, 2 if (s > 0 and b == 0) else 1), (co, co, 1)]
+            c = co
+    params, o = [], 0
+    w = np.asarray(w, np.float64)
+
+    def take(shape):
+        nonlocal o
+        n = int(np.prod(shape))
+        t = torch.tensor(w[o:o + n].reshape(shape), dtype=torch.float64, requires_grad=True)
+        o += n
+        params.append(t)
+        return t
+    layers = [(take((3, 3, ci, co)), take((co,)), take((co,)), st) for ci, co, st in convs]
+    fcw, fcb = take((c, arch["classes"])), take((arch["classes"],))
+    assert o == w.size
+    if bns is None:
+        bns = [(torch.zeros(co, dtype=torch.float64), torch.ones(co, dtype=torch.float64))
+               for _, co, _ in convs]
+
+    def cbr(x, i):
+        Wt, g, be, st = layers[i]
+        y = F.conv2d(x, Wt.permute(3, 2, 0, 1), stride=st, padding=1)
+        return F.batch_norm(y, bns[i][0], bns[i][1], weight=g, bias=be, training=True,
+                            momentum=0.1, eps=1e-5)
+
+    def forward(x_nhwc, labels):
+        x = torch.tensor(x_nhwc, dtype=torch.float64).permute(0, 3, 1, 2)
+        h = torch.relu(cbr(x, 0))
+        for i in range(1, len(convs), 2):
+            ci, co, st = convs[i]
+            a = torch.relu(cbr(h, i))
+            b = cbr(a, i + 1)
+            sc = h if (st == 1 and ci == co) else \
+                F.pad(h[:, :, ::2, ::2], (0, 0, 0, 0, 0, co - ci))
+            h = torch.relu(b + sc)
+        z = h.mean(dim=(2, 3)) @ fcw + fcb
+        return F.cross_entropy(z, torch.tensor(labels, dtype=torch.long))
+    return forward, params, bns
+
+
+def test_resnet_loss_gradient_and_batch_statistics_match_torch():
+    """A small ResNet (8x8 images, channels 4/8/16, two blocks per stage) in
+    torch's autograd with its BatchNorm2d (training mode): the same mean loss,
+    the same gradient of every parameter, and the batch statistics the oracle
+    reports per BN layer give torch's running statistics."""
+    torch = pytest.importorskip("torch")
+    a = O.resnet_arch(side=8, cin=3, base=4, blocks=2, classes=5)
+    rng = np.random.default_rng(31)
+    P = O.resnet_param_count(a)
+    w = rng.standard_normal(P) * 0.4
+    A0 = rng.standard_normal((6, 8 * 8 * 3))
+    y = rng.integers(0, 5, 6)
+    stats = []
+    loss, g = O.resnet_loss_and_grad(w, a, A0, y, stats)
+    fwd, params, bns = _torch_resnet(a, w)
+    tl = fwd(A0.reshape(6, 8, 8, 3), y)
+    tl.backward()
+    tg = np.concatenate([p.grad.numpy().ravel() for p in params])
+    assert abs(loss - tl.item()) <= 1e-12 * abs(loss)
+    assert np.max(np.abs(g - tg)) <= 1e-10 * np.max(np.abs(tg))
+    assert len(stats) == len(bns) == 1 + 3 * 2 * 2
+    for (mu, var, n), (trm, trv) in zip(stats, bns):
+        rm, rv = O.bn_running_update(np.zeros_like(mu), np.ones_like(var), mu, var, n)
+        np.testing.assert_allclose(rm, trm.numpy(), rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(rv, trv.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_bn_running_update_closed_form():
+    """Repeating one batch T times: running mean (1 - 0.9^T) mu (from 0),
+    running variance 0.9^T + (1 - 0.9^T) var n / (n - 1) (from 1)."""
+    mu, var, n = np.array([0.3, -2.0]), np.array([1.5, 0.25]), 37
+    rm, rv = np.zeros(2), np.ones(2)
+    for _ in range(7):
+        rm, rv = O.bn_running_update(rm, rv, mu, var, n)
+    f = 0.9 ** 7
+    np.testing.assert_allclose(rm, (1 - f) * mu, rtol=1e-14)
+    np.testing.assert_allclose(rv, f + (1 - f) * var * n / (n - 1), rtol=1e-14)
+
+
+def test_resnet20_running_statistics_per_worker_and_averaged():
+    """The full ResNet-20 at 2 images per replica, K = 2, two local steps and
+    the synchronisation: each replica's running statistics equal those of a
+    torch ResNet-20 whose BatchNorm2d modules saw that replica's batches at
+    that replica's weights, and the synchronisation leaves their mean in every
+    replica."""
+    torch = pytest.importorskip("torch")
+    base = wk.get("resnet20")
+    w = base.scaled(K=2, B_loc=2, N=64, H=2, momentum=0.9)
+    X, y = wk.dataset(base)
+    X, y = np.ascontiguousarray(X[:64]), np.ascontiguousarray(y[:64])
+    st = O.State(wk.initial_weights(w), 2)
+    arch = O.resnet_arch()
+    bns = [None, None]
+    for _ in range(2):
+        W_before = st.W.copy()
+        step = st.step
+        O.local_step(st, w, X, y, w.lr)
+        for k in range(2):
+            fwd, _, bns[k] = _torch_resnet(arch, W_before[k], bns[k])
+            idx = O.worker_indices(w, step, k)
+            fwd(X[idx].reshape(2, 32, 32, 3).astype(np.float64), y[idx])
+    half = st.RS.shape[1] // 2
+    for k in range(2):
+        for (_, o, c), (trm, trv) in zip(O.resnet_running_layout(arch), bns[k]):
+            np.testing.assert_allclose(st.RS[k, o:o + c], trm.numpy(),
+                                       rtol=1e-10, atol=1e-13)
+            np.testing.assert_allclose(st.RS[k, half + o:half + o + c], trv.numpy(),
+                                       rtol=1e-10)
+    before = st.RS.copy()
+    O.synchronise(st, w, w.lr)
+    np.testing.assert_allclose(st.RS, np.repeat(before.mean(axis=0)[None], 2, axis=0),
+                               rtol=1e-15, atol=0)
