@@ -2,9 +2,12 @@
 
 One step = one local-SGD round: H local steps on every one of the K replicas
 (sample, gather, forward, loss, backward, fused update) followed by the K-way
-average. Default workload: MLP 3072-512-512-10, fp32, K=16, B_loc=128, H=16,
-heavy-ball momentum 0.9, weight decay 1e-4, synthetic 32x32x3 / 10-class
-Gaussian data (32,768 samples per round).
+average. Default workload: the ResNet-20-shaped CNN of the paper's CIFAR
+experiments (3x3 convolutions as implicit GEMMs, 16/32/64 channels, three
+basic blocks per stage, per-worker batch normalisation, global average
+pooling, 10-way classifier), fp32, K=16, B_loc=128, H=16, heavy-ball momentum
+0.9, weight decay 1e-4, synthetic 32x32x3 / 10-class Gaussian images (32,768
+samples per round). ``--workload`` selects the other workloads.
 
 Prints one JSON line: samples/s, the roofline position of the dominant kernel
 (timed with HIP events on the library's stream) and the CPU oracle timed on a
@@ -28,7 +31,11 @@ PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
 METRIC = "aggregate samples/s per local-SGD round at 1 GPU"
 EVENT_GAP_MS = 0.4      # timed rounds between two HIP events: at least this long
 MAX_AUTO_STEPS = 20000
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(PROFILES, f"traffic_counters_{workload}.json")
 
 
 def parse():
@@ -38,7 +45,7 @@ def parse():
                    help="timed rounds (default 20; rounds shorter than 1 ms: "
                         "as many as fill about 100 ms)")
     p.add_argument("--warmup", type=int, default=3, help="untimed rounds")
-    p.add_argument("--workload", default="mlp_512")
+    p.add_argument("--workload", default="resnet20")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-kernel-timing", action="store_true")
     p.add_argument("--sweep", action="store_true",
@@ -47,7 +54,10 @@ def parse():
     p.add_argument("--traffic-from", metavar="DIR",
                    help="no GPU run: turn the rocprofv3 FETCH_SIZE / "
                         "WRITE_SIZE passes under DIR (fetch/, write/) into "
-                        f"{os.path.relpath(TRAFFIC_FILE, ROOT)}")
+                        "profiles/traffic_counters_<workload>.json")
+    p.add_argument("--traffic-tag", default=None,
+                   help="with --traffic-from: the launch tag to account "
+                        "(default: the workload's dominant one)")
     return p.parse_args()
 
 
@@ -64,6 +74,15 @@ def kernel_cost(tag: str, w) -> tuple:
     P = sum(a * b + b for a, b in zip(d[:-1], d[1:]))
     if tag == "sample":
         return 0, K * B * 4
+    if w.model == "resnet20":
+        if tag in ("average", "average_bn_running"):
+            n = resnet_param_count(d[-1]) if tag == "average" else RESNET20_RUNNING
+            return K * n, K * n * 8
+        costs = resnet_step_costs(w)
+        if tag not in costs:
+            return None, None
+        launches, flops, nbytes = costs[tag]
+        return flops / launches, nbytes / launches
     if w.model != "mlp":
         return None, None
     if tag == "xent":
@@ -75,7 +94,7 @@ def kernel_cost(tag: str, w) -> tuple:
         if w.scheme == "ef_sign":   # W, e read twice, written once
             return 0, 24 * K * P + 8 * P
         return 0, 8 * K * P + K * P // 2 + 8 * P
-    if tag == "tiny_round" and L == 1:   # a whole round in one workgroup
+    if tag in ("tiny_round", "tiny_round_wide") and L == 1:   # a round in one workgroup
         H = w.H * w.Hb
         D, C = d
         flops = H * K * (2 * B * D * C + 2 * B * (D + 1) * C)   # logits + gradient
@@ -109,6 +128,76 @@ def kernel_cost(tag: str, w) -> tuple:
 # ResNet-20 multiply-adds per image: forward 40,551,040 (Table 5's 0.041 G);
 # the weight gradient repeats them; the input gradient skips the stem.
 RESNET20_MACS, RESNET20_STEM_MACS = 40551040, 32 * 32 * 27 * 16
+RESNET20_RUNNING = 2 * (16 * 7 + 32 * 6 + 64 * 6)   # BN running means + variances
+
+
+def resnet20_convs():
+    """(c_in, c_out, stride, input side, output side) of the 19 3x3
+    convolutions: the stem, then per stage three blocks of two."""
+    out, c, side = [(3, 16, 1, 32, 32)], 16, 32
+    for st, co in enumerate((16, 32, 64)):
+        for b in range(3):
+            stride = 2 if (st > 0 and b == 0) else 1
+            so = side // stride
+            out += [(c, co, stride, side, so), (co, co, 1, so, so)]
+            c, side = co, so
+    return out
+
+
+def resnet_param_count(classes: int) -> int:
+    return sum(9 * ci * co + 2 * co for ci, co, *_ in resnet20_convs()) + 64 * classes + classes
+
+
+def resnet_step_costs(w) -> dict:
+    """{launch tag: (launches, algorithmic flops, algorithmic bytes)} of one
+    ResNet-20 local step over all K replicas. Flops: 2 per multiply-add of
+    each convolution (forward, input gradient except the stem's, weight
+    gradient). Bytes: every tensor a kernel family must read or write, once
+    (fp32): activations, output gradients, weights; BN's forward apply reads
+    the pre-BN output (and the shortcut input of a block's second
+    convolution) and writes the activation; BN's backward reads the pre-BN
+    output and the upstream gradient twice (sums, then apply; plus the block
+    output for the ReLU mask after a shortcut add) and writes the input
+    gradient; the weight update reads the gradient once and reads and writes
+    the weights and momentum (20 B per weight)."""
+    K, B, C = w.K, w.B_loc, w.widths[-1]
+    convs = resnet20_convs()
+    t = {}
+
+    def add(tag, fl, by):
+        n, f0, b0 = t.get(tag, (0, 0, 0))
+        t[tag] = (n + 1, f0 + fl, b0 + by)
+    for i, (ci, co, st, si, so) in enumerate(convs):
+        x = K * B * si * si * ci * 4          # conv input
+        y = K * B * so * so * co * 4          # conv output / BN tensor
+        wt = K * 9 * ci * co * 4
+        fl = 2 * K * B * so * so * 9 * ci * co
+        add("conv_fwd", fl, x + y + wt)
+        add("bn_stats", 0, K * (B * so * so // 256) * co * 16 + K * co * 24)
+        second = i > 0 and i % 2 == 0         # second convolution of a block
+        sc = 0
+        if second:
+            cin_blk = convs[i - 1][0]
+            sc = y if (convs[i - 1][2] == 1 and cin_blk == co) else K * B * so * so * cin_blk * 4
+        add("bn_apply", 0, 2 * y + sc)
+        add("bn_bwd", 0, (7 if second else 5) * y)
+        if i > 0:
+            add("conv_wt", 0, 2 * wt)
+            add("conv_dgrad", fl, y + x + wt)
+        add("conv_wgrad", fl, x + y + wt)
+        add("conv_wupdate", 0, 5 * wt)
+        if second:
+            cin_blk, _, st_a, si_a, _ = convs[i - 1]
+            if st_a == 1 and cin_blk == co:
+                add("shortcut_bwd", 0, 4 * y)
+            else:
+                add("shortcut_bwd", 0, 4 * K * B * so * so * cin_blk * 4)
+    last = K * B * 8 * 8 * 64 * 4
+    add("gap", 0, last + K * B * 64 * 4)
+    add("gap_bwd", 0, last + K * B * 64 * 4)
+    add("head_fwd", 2 * K * B * 64 * C, K * B * (64 + 2 * C) * 4 + K * 65 * C * 4)
+    add("head_wgrad", 2 * K * B * 64 * C, K * B * (64 + C) * 4 + K * 65 * C * 16)
+    return t
 
 
 def gemm_flops_per_local_step(w) -> int:
@@ -124,83 +213,112 @@ def gemm_flops_per_local_step(w) -> int:
     return f * w.K
 
 
-def source_digest() -> str:
+def source_digest(w) -> str:
+    """Digest of the kernel sources a workload's dominant kernels come from."""
+    files = (("kernels.h", "resnet.hip", "elementwise.hip") if w.model == "resnet20"
+             else ("kernels.h", "gemm.hip", "elementwise.hip"))
     h = hashlib.sha256()
-    for f in ("kernels.h", "gemm.hip", "elementwise.hip"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_1808_07217_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def traffic_for(tag: str, workload: str):
+def traffic_for(tag: str, w):
     """HBM bytes per launch of the dominant kernel from the committed PMC
-    summary, if it was taken on this workload and the current kernel
-    sources."""
+    summary, if it was taken on this workload, this tag and the current
+    kernel sources."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(w.name)) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if (t.get("source_digest") != source_digest() or t.get("tag") != tag
-            or t.get("workload") != workload):
+    if t.get("source_digest") != source_digest(w) or t.get("tag") != tag:
         return None
     return t.get("bytes_per_launch")
 
 
-# Kernel (as rocprofv3 names it) behind a launch tag of the MLP workloads:
-# the persistent fused weight-gradient + update kernel over the hidden
-# layers, and the K-way average, the copy-like kernel used to scale the
-# counters.
-TAG_KERNEL = {
-    "wgrad_update": "gemm_f32_sgd_ws<",
-    "average": "k_average4<",
+# Kernels (as rocprofv3 names them, by name prefix) behind a launch tag: the
+# MLP's persistent fused weight-gradient + update kernel, the ResNet's
+# convolution families, and the K-way average, the copy-like kernel used to
+# scale the counters.
+TAG_KERNELS = {
+    "wgrad_update": ("gemm_f32_sgd_ws<",),
+    "average": ("k_average4<",),
+    "conv_fwd": ("k_conv_stem_fwd", "k_conv_halo16<0>", "k_conv_rows<0,"),
+    "conv_dgrad": ("k_conv_halo16<1>", "k_conv_rows<1,"),
+    "conv_wgrad": ("k_conv_wgrad_stem", "k_conv_wgrad_halo16", "k_conv_wgrad_rows<"),
+    "bn_bwd": ("k_bn_partial4", "k_bn_finalize_wg", "k_bn_bwd_apply4"),
+    "bn_apply": ("k_bn_apply4<",),
 }
 
 
-def _counter_means(path: str, counter: str) -> dict:
-    """{kernel name: mean counter value (KiB) per dispatch} from one
-    rocprofv3 --pmc pass (its *_counter_collection.csv)."""
+def _counter_rows(path: str, counter: str) -> list:
+    """[(kernel name, grid size, counter value in KiB)] per dispatch from
+    one rocprofv3 --pmc pass (its *_counter_collection.csv)."""
     import csv
     import glob
     files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"),
                       recursive=True)
     if not files:
         raise SystemExit(f"no counter_collection.csv under {path}")
-    acc = {}
+    rows = []
     for f in files:
         with open(f) as fh:
             for r in csv.DictReader(fh):
-                if r["Counter_Name"] != counter:
-                    continue
-                acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
-    return {k: sum(v) / len(v) for k, v in acc.items()}
+                if r["Counter_Name"] == counter:
+                    rows.append((r["Kernel_Name"], int(r["Grid_Size"]),
+                                 float(r["Counter_Value"])))
+    return rows
 
 
-def write_traffic(pmc_dir: str, w) -> dict:
-    """HBM bytes per launch of the dominant kernel from two counter passes,
-    each scaled by what the same counter reads for the K-way average, whose
-    traffic is known exactly (K P fp32 words read and written)."""
-    def pick(table, key):
-        hits = [v for k, v in table.items() if key in k]
-        if len(hits) != 1:
-            raise SystemExit(f"{key!r} matches {len(hits)} kernels")
-        return hits[0] * 1024.0
-    fetch = _counter_means(os.path.join(pmc_dir, "fetch"), "FETCH_SIZE")
-    write = _counter_means(os.path.join(pmc_dir, "write"), "WRITE_SIZE")
-    P = sum(a * b + b for a, b in zip(w.widths[:-1], w.widths[1:]))
-    avg_bytes = 4.0 * w.K * P
-    f_scale = avg_bytes / pick(fetch, TAG_KERNEL["average"])
-    w_scale = avg_bytes / pick(write, TAG_KERNEL["average"])
-    tag = "wgrad_update"
-    rd = pick(fetch, TAG_KERNEL[tag]) * f_scale
-    wr = pick(write, TAG_KERNEL[tag]) * w_scale
-    out = {"tag": tag, "kernel": TAG_KERNEL[tag], "workload": w.name,
-           "source_digest": source_digest(),
+def _short(name: str) -> str:
+    """A kernel's name without its namespaces and parameter list."""
+    name = name.split("(")[0] if not name.startswith("void ") else name[5:].split("(")[0]
+    return name.replace("lsgd::(anonymous namespace)::", "").replace("lsgd::", "")
+
+
+def _family_bytes(rows, prefixes) -> tuple:
+    """(dispatches, mean bytes per dispatch) over the kernels whose short
+    name starts with one of the prefixes."""
+    vals = [v for k, _, v in rows if any(_short(k).replace(" ", "").startswith(
+        p.replace(" ", "")) for p in prefixes)]
+    if not vals:
+        raise SystemExit(f"no dispatch of {prefixes}")
+    return len(vals), 1024.0 * sum(vals) / len(vals)
+
+
+def write_traffic(pmc_dir: str, w, tag: str) -> dict:
+    """HBM bytes per launch of a tag's kernels from two counter passes, each
+    scaled by what the same counter reads for the K-way average of the
+    replicas (the launch with the largest grid), whose traffic is known
+    exactly (K Ps fp32 words read and written)."""
+    fetch = _counter_rows(os.path.join(pmc_dir, "fetch"), "FETCH_SIZE")
+    write = _counter_rows(os.path.join(pmc_dir, "write"), "WRITE_SIZE")
+
+    def calib(rows):
+        avg = [(g, v) for k, g, v in rows if _short(k).startswith("k_average4<")]
+        gmax = max(g for g, _ in avg)
+        vals = [v for g, v in avg if g == gmax]
+        return 1024.0 * sum(vals) / len(vals)
+    if w.model == "resnet20":
+        P = resnet_param_count(w.widths[-1])
+    else:
+        P = sum(a * b + b for a, b in zip(w.widths[:-1], w.widths[1:]))
+    Ps = (P + 63) // 64 * 64
+    avg_bytes = 4.0 * w.K * Ps
+    f_scale = avg_bytes / calib(fetch)
+    w_scale = avg_bytes / calib(write)
+    n_f, rd = _family_bytes(fetch, TAG_KERNELS[tag])
+    n_w, wr = _family_bytes(write, TAG_KERNELS[tag])
+    rd, wr = rd * f_scale, wr * w_scale
+    out = {"tag": tag, "kernels": list(TAG_KERNELS[tag]), "workload": w.name,
+           "source_digest": source_digest(w),
            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
-           "read_bytes_per_launch": round(rd), "write_bytes_per_launch": round(wr),
-           "bytes_per_launch": round(rd + wr),
-           "algorithmic_bytes_per_launch": kernel_cost(tag, w)[1]}
-    with open(TRAFFIC_FILE, "w") as f:
+           "dispatches": n_f, "read_bytes_per_launch": round(rd),
+           "write_bytes_per_launch": round(wr), "bytes_per_launch": round(rd + wr),
+           "algorithmic_bytes_per_launch": round(kernel_cost(tag, w)[1])}
+    with open(traffic_file(w.name), "w") as f:
         json.dump(out, f, indent=1)
     return out
 
@@ -260,16 +378,17 @@ def cpu_baseline(w, X, y, w0, min_seconds: float = 10.0):
     until about `min_seconds` of CPU work: whole rounds (H local steps on all
     K replicas plus the synchronisation) where one takes a few seconds; one
     local step of replica 0 where a round would take minutes (ResNet-20, the
-    2048-wide MLP)."""
+    2048-wide MLP). Timed with the host BLAS's own thread count, then again
+    with one thread."""
     from oracle import lsgd_oracle as O
-    threads = None
     try:
         import threadpoolctl
+    except ImportError:
+        threadpoolctl = None
+    threads = None
+    if threadpoolctl is not None:
         info = threadpoolctl.threadpool_info()
         threads = max((i.get("num_threads") or 1) for i in info) if info else 1
-    except Exception:
-        threads = os.cpu_count()
-    st = O.State(w0, w.K)
     per_step = w.model == "resnet20" or w.dtype == "bf16"
     if per_step:
         what = f"one local step of replica 0 ({w.B_loc} samples)"
@@ -284,24 +403,36 @@ def cpu_baseline(w, X, y, w0, min_seconds: float = 10.0):
                    else f"{w.scheme} synchronisation" if w.scheme != "local"
                    else "average"))
         unit = w.K * w.H * w.Hb * w.B_loc
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        if per_step:
-            O.local_step(st, w, X, y, w.lr, replicas=[0])
-        elif w.Kb > 0:
-            O.run_hierarchical_round(st, w, X, y, w.H, w.Hb, w.Kb, w.lr)
-        else:
-            O.run_round(st, w, X, y, w.H, w.lr)
-        n += 1
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
-    samples = n * unit
-    return {"value": samples / dt, "unit": "samples/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{n} x {what} of {w.name}: {samples} samples in {dt:.2f} s; "
-                      f"fp64 numpy, BLAS threads={threads}"}
+
+    def timed():
+        st = O.State(w0, w.K)
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            if per_step:
+                O.local_step(st, w, X, y, w.lr, replicas=[0])
+            elif w.Kb > 0:
+                O.run_hierarchical_round(st, w, X, y, w.H, w.Hb, w.Kb, w.lr)
+            else:
+                O.run_round(st, w, X, y, w.H, w.lr)
+            n += 1
+            dt = time.perf_counter() - t0
+            if dt >= min_seconds:
+                return n, dt
+
+    n, dt = timed()
+    out = {"value": n * unit / dt, "unit": "samples/s", "cores": threads,
+           "host_cores": os.cpu_count(), "kind": "oracle",
+           "sample": f"{n} x {what} of {w.name}: {n * unit} samples in {dt:.2f} s; "
+                     f"fp64 numpy, BLAS threads={threads}, host cores={os.cpu_count()}"}
+    if threadpoolctl is not None:
+        with threadpoolctl.threadpool_limits(1):
+            n1, dt1 = timed()
+        out["single_thread"] = {"value": n1 * unit / dt1, "unit": "samples/s",
+                                "cores": 1,
+                                "sample": f"{n1} x {what}: {n1 * unit} samples in "
+                                          f"{dt1:.2f} s on one BLAS thread"}
+    return out
 
 
 def main():
@@ -311,7 +442,9 @@ def main():
         return
     if args.traffic_from:
         import workloads as wk
-        print(json.dumps(write_traffic(args.traffic_from, wk.get(args.workload))))
+        w = wk.get(args.workload)
+        tag = args.traffic_tag or ("conv_wgrad" if w.model == "resnet20" else "wgrad_update")
+        print(json.dumps(write_traffic(args.traffic_from, w, tag)))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU "
@@ -476,7 +609,7 @@ def main():
                     "achieved": round(flops / avg_s / 1e12, 2),
                     "peak": PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s"}
         roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-        roof["traffic"] = traffic_for(dom, w.name)
+        roof["traffic"] = traffic_for(dom, w)
         roof["kernel"] = dom
         roof["avg_launch_us"] = round(avg_s * 1e6, 2)
         roof["launches_timed"] = n

@@ -27,6 +27,14 @@
  *    then on every call on that context returns LSGD_E_STATE until destroy.
  *  - One context must not be used from two host threads at once. Distinct
  *    contexts are independent.
+ *  - Failure detection: every local step checks on the device, with no host
+ *    synchronisation, that each replica's mean mini-batch loss is finite; a
+ *    non-finite one sets a flag in the workspace that lsgd_sync reports as
+ *    LSGD_E_NONFINITE. The flag stays set (the context remains usable)
+ *    until lsgd_write_state restores a state or the context is destroyed.
+ *    A loss is taken at the pre-update weights, so a step whose update makes
+ *    a parameter non-finite shows up at the next step's loss; a non-finite
+ *    hidden pre-activation that a ReLU maps to 0 does not reach it.
  *
  * Flat parameter layout of one replica ([P] fp32): for each layer l = 1..L in
  * order, W_l row-major [d_{l-1}][d_l] (element (i, j) maps input i to output
@@ -50,7 +58,9 @@ typedef enum lsgd_status {
   LSGD_E_WORKSPACE = 2,   /* workspace smaller than lsgd_workspace_bytes */
   LSGD_E_HIP = 3,         /* a HIP runtime call or launch failed (latched) */
   LSGD_E_STATE = 4,       /* context unusable after an earlier HIP error */
-  LSGD_E_UNSUPPORTED = 5  /* valid request this build does not implement */
+  LSGD_E_UNSUPPORTED = 5, /* valid request this build does not implement */
+  LSGD_E_NONFINITE = 6    /* a local step's loss was not finite (sticky; see
+                             lsgd_sync) */
 } lsgd_status;
 
 /* LSGD_MODEL_MLP: ReLU MLP with widths d_0 .. d_L (L = 1 is softmax
@@ -63,7 +73,15 @@ typedef enum lsgd_status {
  * on its scale and shift), global average pooling and a 64 -> classes
  * classifier. Parameter layout: per convolution in order its weight
  * [3][3][c_in][c_out], BN scale [c_out], BN shift [c_out]; then the
- * classifier weight [64][classes] and bias [classes]. */
+ * classifier weight [64][classes] and bias [classes]. Each replica also keeps
+ * BN running statistics (they do not enter the training loss): R = 1376
+ * values, the running means of the 19 BN layers in convolution order, then
+ * their running variances; they start at 0 and 1, follow every local step as
+ * r = 0.9 r + 0.1 s (s the batch mean, or the unbiased batch variance
+ * var * n / (n - 1) over the n values per channel), and take the plain mean
+ * over the replicas at every synchronisation (over the block at a block
+ * synchronisation), whatever the scheme. They are read and written through
+ * the state blob. */
 enum { LSGD_MODEL_MLP = 0, LSGD_MODEL_RESNET20 = 1 };
 enum { LSGD_FP32 = 0, LSGD_BF16 = 1 };
 /* Local-step / synchronisation scheme (the appendix on compression):
@@ -259,8 +277,40 @@ lsgd_status lsgd_set_step(lsgd_ctx* ctx, int64_t step);
  * `step`: int32 [K][B_loc] into d_idx. */
 lsgd_status lsgd_sample_indices(lsgd_ctx* ctx, int64_t step, int32_t* d_idx);
 
-/* Synchronise the context's stream; returns the latched status. */
+/* Synchronise the context's stream; returns the latched status, else
+ * LSGD_E_NONFINITE when a local step since init (or the last
+ * lsgd_write_state) had a non-finite loss, else LSGD_OK. */
 lsgd_status lsgd_sync(lsgd_ctx* ctx);
+
+/*
+ * Checkpoint and resume: the whole training state of a context as one
+ * device blob -- what the paper's post-local runs restart from (they switch
+ * to local SGD from a mini-batch SGD checkpoint). Layout (all little-endian):
+ *   bytes 0..255: header, eight uint64 words: magic 0x3154535F4447534C
+ *     ("LSGD_ST1"), a digest of the layout (model, widths, K, P, R and the
+ *     section mask, FNV-1a), K, P, R (BN running statistics per replica; 0
+ *     for the MLP), the local step counter s, the section mask, the blob's
+ *     total bytes; the rest of the 256 bytes is unused;
+ *   then, each at the next 256-byte aligned offset and present when its mask
+ *   bit is set: bit 0 the replicas fp32 [K][P], bit 1 the momentum buffers
+ *   [K][P] (always present), bit 2 the BN running statistics [K][R]
+ *   (ResNet-20), bit 3 the synchronised model w_s [P] (global momentum and
+ *   the sign schemes), bit 4 the global momentum buffer [P] (global
+ *   momentum), bit 5 the error memories [K][P] (LSGD_SCHEME_EF_SIGN).
+ * lsgd_state_bytes gives the size for a configuration (no device needed).
+ * lsgd_read_state writes the blob to d_dst (stream-ordered, no host sync).
+ * lsgd_write_state restores it from d_src: it synchronises the stream to
+ * read the header, returns LSGD_E_INVALID without changing anything unless
+ * the header matches this context's configuration (magic, digest, K, P, R,
+ * mask, size), then overwrites every section (and the bf16 operand copy),
+ * sets s and clears the non-finite flag. d_dst / d_src: caller-owned device
+ * memory of lsgd_state_bytes bytes, 256-byte aligned, else LSGD_E_INVALID.
+ * A context resumed from a blob continues bit for bit as the one that wrote
+ * it (same configuration, dataset and step sizes).
+ */
+lsgd_status lsgd_state_bytes(const lsgd_config* cfg, size_t* bytes);
+lsgd_status lsgd_read_state(lsgd_ctx* ctx, void* d_dst);
+lsgd_status lsgd_write_state(lsgd_ctx* ctx, const void* d_src);
 
 /* Release the host context (device memory stays with the caller). */
 lsgd_status lsgd_destroy(lsgd_ctx* ctx);

@@ -35,6 +35,13 @@ struct ResPlan {
   int classes = 0, feat = 64, side_out = 8;
   size_t featb = 0, dfeat = 0, dzh = 0, gbuf[4] = {}, mu = 0, inv = 0, coef = 0,
          bnpart = 0, wpart = 0, wt = 0;
+  // BN running statistics [K][Rs] fp32: per replica the running means of
+  // every BN layer in convolution order (layer i from rsoff[i]), then the
+  // running variances in the same order (from rs_half); R = 2 rs_half
+  size_t rs = 0;
+  int rsoff[kResConvs] = {};
+  int rs_half = 0;
+  int64_t Rs = 0;
 };
 
 struct Layout {
@@ -49,6 +56,7 @@ struct Layout {
   size_t idx2 = 0;  // second index buffer: the next step's rows, sampled early
   size_t Wsync = 0, Ug = 0;  // model at the last sync; global momentum buffer
   size_t E = 0, sign = 0, sign_bytes = 0;  // error memories; sign-sync scratch
+  size_t flag = 0;    // int32: set by the loss kernels on a non-finite loss
   bool head = false;  // top layer through the fused head kernels
   size_t act[LSGD_MAX_LAYERS] = {}, dZ[LSGD_MAX_LAYERS + 1] = {};
   size_t total = 0;
@@ -135,6 +143,13 @@ Layout make_resnet_layout(const lsgd_config* c) {
   };
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
+  for (int i = 0; i < kResConvs; ++i) {
+    r.rsoff[i] = r.rs_half;
+    r.rs_half += r.cv[i].Cout;
+  }
+  r.Rs = (2 * r.rs_half + kReplicaPad - 1) / kReplicaPad * kReplicaPad;
+  r.rs = take(K * r.Rs * 4);
+  l.flag = take(4);
   if (c->global_momentum != 0.f || c->scheme != LSGD_SCHEME_LOCAL)
     l.Wsync = take(l.Ps * 4);
   if (c->global_momentum != 0.f) l.Ug = take(l.Ps * 4);
@@ -197,6 +212,7 @@ Layout make_layout(const lsgd_config* c) {
   };
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
+  l.flag = take(4);
   if (c->global_momentum != 0.f || c->scheme != LSGD_SCHEME_LOCAL)
     l.Wsync = take(l.Ps * 4);
   if (c->global_momentum != 0.f) l.Ug = take(l.Ps * 4);
@@ -287,6 +303,9 @@ struct lsgd_ctx {
 
   float* W() const { return (float*)(ws + lay.W); }
   float* U() const { return (float*)(ws + lay.U); }
+  int* flag() const { return (int*)(ws + lay.flag); }
+  // BN running statistics (ResNet), else nullptr
+  float* RS() const { return lay.resnet ? (float*)(ws + lay.rp.rs) : nullptr; }
   bool gm() const { return cfg.global_momentum != 0.f; }
   bool signed_sync() const { return cfg.scheme != LSGD_SCHEME_LOCAL; }
   bool ef() const { return cfg.scheme == LSGD_SCHEME_EF_SIGN; }
@@ -501,6 +520,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     h.dZprev = L > 1 ? c->dZ(L - 1) : nullptr;
     h.rowloss = c->rowloss();
     h.loss = d_loss;
+    h.nonfinite = c->flag();
     h.lr = lr;
     h.mom = cf.momentum;
     h.wd = cf.weight_decay;
@@ -529,7 +549,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     }
   } else {
     LSGD_LAUNCH(c, "xent", lsgd::launch_xent(c->Z(), c->y, c->idx(), K, B, w[L],
-                                               c->dZ(L), dt, d_loss, s));
+                                               c->dZ(L), dt, d_loss, c->flag(), s));
   }
 
   // backward, top layer first. The input gradient of layer l reads the
@@ -652,12 +672,16 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_LAUNCH(c, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, s));
     float* mi = mu + (size_t)i * K * 64;
     float* ii = inv + (size_t)i * K * 64;
+    // this replica's running statistics of BN layer i follow the batch
+    float* rm = c->RS() + r.rsoff[i];
+    float* rv = c->RS() + r.rs_half + r.rsoff[i];
     if (fused)
       LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_finalize_chunks(bnpart, rows(i) / 256, K,
-                                                                 rows(i), q.Cout, mi, ii, s));
+                                                                 rows(i), q.Cout, mi, ii, rm,
+                                                                 rv, r.Rs, s));
     else
       LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
-                                                       mi, ii, s));
+                                                       mi, ii, rm, rv, r.Rs, s));
     int mode = 0;
     const float* blk_in = nullptr;
     int cin_blk = 0;
@@ -701,6 +725,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   h.nomask = 1;
   h.rowloss = c->rowloss();
   h.loss = d_loss;
+  h.nonfinite = c->flag();
   h.lr = lr;
   h.mom = cf.momentum;
   h.wd = cf.weight_decay;
@@ -724,9 +749,10 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                     coef, W + q.offG, W + q.offB, U + q.offG,
                                     U + q.offB, Ps, lr, cf.momentum, upd_mode(cf), dy, s);
   };
-  // weight gradient of conv i from its input x and output gradient dy, then
-  // the update (after any input gradient that reads the old weight)
-  auto wgrad = [&](int i, const float* x, const float* dy) -> hipError_t {
+  // weight gradient of conv i from its input x and output gradient dy into
+  // per-split partials, then their fixed-order sum and the update (after
+  // any input gradient that reads the old weight)
+  auto wgrad = [&](int i, const float* x, const float* dy) -> lsgd_status {
     const ConvSpec& q = r.cv[i];
     lsgd::ConvGeom g = geom(i);
     if (i == 0) {
@@ -738,24 +764,27 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     }
     g.dy = dy;
     g.out = wpart;
-    hipError_t e = lsgd::launch_conv(lsgd::CONV_WGRAD_MODE, g, s);
-    if (e != hipSuccess) return e;
-    return lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo), K,
-                                     9 * q.Cin * q.Cout, W + q.offW, U + q.offW, Ps, lr,
-                                     cf.momentum, cf.weight_decay, upd_mode(cf), s);
+    LSGD_LAUNCH(c, "conv_wgrad", lsgd::launch_conv(lsgd::CONV_WGRAD_MODE, g, s));
+    LSGD_LAUNCH(c, "conv_wupdate",
+                lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo), K,
+                                          9 * q.Cin * q.Cout, W + q.offW, U + q.offW, Ps,
+                                          lr, cf.momentum, cf.weight_decay, upd_mode(cf),
+                                          s));
+    return LSGD_OK;
   };
   // input gradient of conv i (old weight, channels swapped per tap)
-  auto dgrad = [&](int i, const float* dy, float* dx) -> hipError_t {
+  auto dgrad = [&](int i, const float* dy, float* dx) -> lsgd_status {
     const ConvSpec& q = r.cv[i];
-    hipError_t e = lsgd::launch_conv_wt(W + q.offW, Ps, K, q.Cin, q.Cout, wt, s);
-    if (e != hipSuccess) return e;
+    LSGD_LAUNCH(c, "conv_wt", lsgd::launch_conv_wt(W + q.offW, Ps, K, q.Cin, q.Cout, wt, s));
     lsgd::ConvGeom g = geom(i);
     g.dy = dy;
     g.Wk = wt;
     g.sW = 9LL * q.Cin * q.Cout;
     g.out = dx;
-    return lsgd::launch_conv(lsgd::CONV_DGRAD_MODE, g, s);
+    LSGD_LAUNCH(c, "conv_dgrad", lsgd::launch_conv(lsgd::CONV_DGRAD_MODE, g, s));
+    return LSGD_OK;
   };
+
   for (int blk = 8; blk >= 0; --blk) {
     const int ia = 2 * blk + 1, ib = 2 * blk + 2;
     const ConvSpec& qa = r.cv[ia];
@@ -763,12 +792,12 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     const int nxt = cur == 0 ? 3 : 0;
     // second convolution: its output went through the shortcut add and ReLU
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1]));
-    LSGD_LAUNCH(c, "conv_dgrad", dgrad(ib, gb[1], gb[2]));
-    LSGD_LAUNCH(c, "conv_wgrad", wgrad(ib, F(r.cv[ia].act), gb[1]));
+    if (lsgd_status st = dgrad(ib, gb[1], gb[2])) return st;
+    if (lsgd_status st = wgrad(ib, F(r.cv[ia].act), gb[1])) return st;
     // first convolution: ReLU'd BN output, the mask recomputed from its input
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[1]));
-    LSGD_LAUNCH(c, "conv_dgrad", dgrad(ia, gb[1], gb[nxt]));
-    LSGD_LAUNCH(c, "conv_wgrad", wgrad(ia, h_in, gb[1]));
+    if (lsgd_status st = dgrad(ia, gb[1], gb[nxt])) return st;
+    if (lsgd_status st = wgrad(ia, h_in, gb[1])) return st;
     // the shortcut's share of the block-output gradient
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
     LSGD_LAUNCH(c, "shortcut_bwd",
@@ -777,8 +806,25 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     cur = nxt;
   }
   LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1]));
-  LSGD_LAUNCH(c, "conv_wgrad", wgrad(0, nullptr, gb[1]));
+  if (lsgd_status st = wgrad(0, nullptr, gb[1])) return st;
   c->step += 1;
+  return LSGD_OK;
+}
+
+// The BN running statistics (ResNet) take the plain mean over the replicas
+// (over each block of Kb for a block synchronisation) at every
+// synchronisation, whatever the scheme: they are not trained parameters.
+lsgd_status average_running_stats(lsgd_ctx* c, int Kb) {
+  if (!c->RS()) return LSGD_OK;
+  const int K = c->cfg.K;
+  const long long Rs = c->lay.rp.Rs;
+  if (Kb == K)
+    LSGD_LAUNCH(c, "average_bn_running",
+                lsgd::launch_average(c->RS(), nullptr, K, Rs, Rs, nullptr, c->stream));
+  else if (Kb > 1)
+    LSGD_LAUNCH(c, "average_bn_running",
+                lsgd::launch_average_blocks(c->RS(), nullptr, Kb, K / Kb, Rs, Rs, nullptr,
+                                            c->stream));
   return LSGD_OK;
 }
 
@@ -786,7 +832,7 @@ lsgd_status do_average(lsgd_ctx* c) {
   LSGD_LAUNCH(c, "average",
               lsgd::launch_average(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
                                    c->lay.Ps, nullptr, c->stream));
-  return LSGD_OK;
+  return average_running_stats(c, c->cfg.K);
 }
 
 // The end-of-round synchronisation: the plain average, or with a global
@@ -798,14 +844,14 @@ lsgd_status do_synchronise(lsgd_ctx* c, float lr) {
                                        c->cfg.K, c->lay.P, c->lay.Ps,
                                        c->ws + c->lay.sign, c->lay.sign_bytes,
                                        c->stream));
-    return LSGD_OK;
+    return average_running_stats(c, c->cfg.K);
   }
   if (!c->gm()) return do_average(c);
   LSGD_LAUNCH(c, "average",
               lsgd::launch_average_gm(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
                                       c->lay.Ps, c->Wsync(), c->Ug(),
                                       c->cfg.global_momentum, lr, c->stream));
-  return LSGD_OK;
+  return average_running_stats(c, c->cfg.K);
 }
 
 lsgd_status do_average_blocks(lsgd_ctx* c, int Kb) {
@@ -815,7 +861,7 @@ lsgd_status do_average_blocks(lsgd_ctx* c, int Kb) {
               lsgd::launch_average_blocks(c->W(), c->Wb(), Kb, c->cfg.K / Kb,
                                           c->lay.Ps, c->lay.Ps, nullptr,
                                           c->stream));
-  return LSGD_OK;
+  return average_running_stats(c, Kb);
 }
 
 // A whole round of softmax regression (one fp32 layer, plain local SGD and
@@ -835,6 +881,7 @@ lsgd_status do_tiny_round(lsgd_ctx* c, int H, const float* h_lr, float* d_loss) 
   a.W = c->W();
   a.U = c->U();
   a.loss = d_loss;
+  a.nonfinite = c->flag();
   a.N = cf.N;
   a.Ps = c->lay.Ps;
   a.step0 = c->step;
@@ -854,9 +901,65 @@ lsgd_status do_tiny_round(lsgd_ctx* c, int H, const float* h_lr, float* d_loss) 
     while ((1LL << (2 * a.m)) < cf.N) ++a.m;
   }
   for (int h = 0; h < H; ++h) a.lr[h] = h_lr[h];
-  LSGD_LAUNCH(c, "tiny_round", lsgd::launch_tiny_round(a, c->stream));
+  // the two kernels launch under their own tags
+  const char* tag = lsgd::tiny_round_wide(a.K, a.B, a.D, a.C, a.H) ? "tiny_round_wide"
+                                                                  : "tiny_round";
+  LSGD_LAUNCH(c, tag, lsgd::launch_tiny_round(a, c->stream));
   c->step += H;
   return LSGD_OK;
+}
+
+// The state blob of lsgd_read_state / lsgd_write_state: a header of eight
+// 64-bit words, then the sections present for the configuration, each at a
+// 256-byte aligned offset, rows of P (or R) contiguous fp32 values.
+enum { kSecW = 0, kSecU, kSecRS, kSecWsync, kSecUg, kSecE, kSecCount };
+constexpr uint64_t kStateMagic = 0x3154535F4447534CULL;  // "LSGD_ST1"
+constexpr size_t kStateHeader = 256;
+
+struct StatePlan {
+  int64_t K = 0, P = 0, R = 0;
+  uint64_t mask = 0;
+  size_t off[kSecCount] = {};
+  size_t total = 0;
+  uint64_t digest = 0;
+};
+
+uint64_t fnv1a(uint64_t h, int64_t v) {
+  for (int i = 0; i < 8; ++i) {
+    h ^= (uint64_t)((v >> (8 * i)) & 0xff);
+    h *= 0x100000001b3ULL;
+  }
+  return h;
+}
+
+StatePlan state_plan(const lsgd_config& cf, const Layout& ly) {
+  StatePlan sp;
+  sp.K = cf.K;
+  sp.P = ly.P;
+  sp.R = ly.resnet ? 2LL * ly.rp.rs_half : 0;
+  const bool gm = cf.global_momentum != 0.f, sgn = cf.scheme != LSGD_SCHEME_LOCAL;
+  const bool present[kSecCount] = {true, true, sp.R > 0, gm || sgn, gm,
+                                   cf.scheme == LSGD_SCHEME_EF_SIGN};
+  const int64_t floats[kSecCount] = {sp.K * sp.P, sp.K * sp.P, sp.K * sp.R, sp.P, sp.P,
+                                     sp.K * sp.P};
+  size_t t = kStateHeader;
+  for (int i = 0; i < kSecCount; ++i) {
+    if (!present[i]) continue;
+    sp.mask |= 1ULL << i;
+    sp.off[i] = t;
+    t = align_up(t + (size_t)floats[i] * 4, kAlign);
+  }
+  sp.total = t;
+  uint64_t h = 0xcbf29ce484222325ULL;
+  h = fnv1a(h, cf.model);
+  h = fnv1a(h, cf.n_layers);
+  for (int i = 0; i <= cf.n_layers; ++i) h = fnv1a(h, cf.widths[i]);
+  h = fnv1a(h, sp.K);
+  h = fnv1a(h, sp.P);
+  h = fnv1a(h, sp.R);
+  h = fnv1a(h, (int64_t)sp.mask);
+  sp.digest = h;
+  return sp;
 }
 
 #define LSGD_USABLE(ctx)                                   \
@@ -920,6 +1023,16 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
   if (c->bf16())
     check(lsgd::launch_to_bf16(d_X, c->Xb(), (long long)cfg->N * cfg->widths[0],
                                c->stream), "dataset to bf16");
+  check(lsgd::launch_fill((float*)c->flag(), 0.f, 1, c->stream), "clear the loss flag");
+  if (c->RS()) {  // running means 0 and variances 1, in every replica
+    const ResPlan& r = ly.rp;
+    check(lsgd::launch_fill(c->RS(), 0.f, (long long)K * r.Rs, c->stream), "fill RS");
+    check(lsgd::launch_fill(c->RS() + r.rs_half, 1.f, r.rs_half, c->stream),
+          "running variances := 1");
+    if (K > 1)  // rows 1..K-1 from row 0
+      check(lsgd::launch_copy_rows(c->RS() + r.Rs, r.Rs, c->RS(), 0, r.Rs, K - 1,
+                                   c->stream), "running statistics to every replica");
+  }
   // side streams pay off once there is a hidden layer (an update that can
   // overlap the rest of the backward pass)
   if (st == LSGD_OK && ly.head && ly.L >= 2) {
@@ -1089,6 +1202,93 @@ lsgd_status lsgd_write_global_momentum(lsgd_ctx* ctx, const float* d_src) {
   return LSGD_OK;
 }
 
+lsgd_status lsgd_state_bytes(const lsgd_config* cfg, size_t* bytes) {
+  if (!valid_config(cfg) || !bytes) return LSGD_E_INVALID;
+  *bytes = state_plan(*cfg, make_layout(cfg)).total;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_read_state(lsgd_ctx* ctx, void* d_dst) {
+  LSGD_USABLE(ctx);
+  if (!d_dst || ((uintptr_t)d_dst) % kAlign) return LSGD_E_INVALID;
+  const StatePlan sp = state_plan(ctx->cfg, ctx->lay);
+  char* dst = (char*)d_dst;
+  lsgd::Words8 h{};
+  h.w[0] = kStateMagic;
+  h.w[1] = sp.digest;
+  h.w[2] = (uint64_t)sp.K;
+  h.w[3] = (uint64_t)sp.P;
+  h.w[4] = (uint64_t)sp.R;
+  h.w[5] = (uint64_t)ctx->step;
+  h.w[6] = sp.mask;
+  h.w[7] = (uint64_t)sp.total;
+  const hipStream_t s = ctx->stream;
+  const long long P = sp.P, Ps = ctx->lay.Ps;
+  LSGD_CK(ctx, lsgd::launch_put_words(dst, h, s));
+  // the rest of the header and the alignment gaps are zeros, so that equal
+  // states give equal blobs
+  LSGD_CK(ctx, lsgd::launch_fill((float*)(dst + 64), 0.f, (kStateHeader - 64) / 4, s));
+  const int64_t nfl[kSecCount] = {sp.K * P, sp.K * P, sp.K * sp.R, P, P, sp.K * P};
+  for (int i = 0; i < kSecCount; ++i) {
+    if (!(sp.mask >> i & 1)) continue;
+    size_t next = sp.total;
+    for (int j = i + 1; j < kSecCount; ++j)
+      if (sp.mask >> j & 1) {
+        next = sp.off[j];
+        break;
+      }
+    const size_t end = sp.off[i] + (size_t)nfl[i] * 4;
+    if (next > end) LSGD_CK(ctx, lsgd::launch_fill((float*)(dst + end), 0.f, (next - end) / 4, s));
+  }
+  auto rows = [&](int sec, const float* src, long long n, long long pitch, int k) {
+    return lsgd::launch_copy_rows((float*)(dst + sp.off[sec]), n, src, pitch, n, k, s);
+  };
+  LSGD_CK(ctx, rows(kSecW, ctx->W(), P, Ps, sp.K));
+  LSGD_CK(ctx, rows(kSecU, ctx->U(), P, Ps, sp.K));
+  if (sp.mask & (1u << kSecRS)) LSGD_CK(ctx, rows(kSecRS, ctx->RS(), sp.R, ctx->lay.rp.Rs, sp.K));
+  if (sp.mask & (1u << kSecWsync)) LSGD_CK(ctx, rows(kSecWsync, ctx->Wsync(), P, Ps, 1));
+  if (sp.mask & (1u << kSecUg)) LSGD_CK(ctx, rows(kSecUg, ctx->Ug(), P, Ps, 1));
+  if (sp.mask & (1u << kSecE)) LSGD_CK(ctx, rows(kSecE, ctx->E(), P, Ps, sp.K));
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_write_state(lsgd_ctx* ctx, const void* d_src) {
+  LSGD_USABLE(ctx);
+  if (!d_src || ((uintptr_t)d_src) % kAlign) return LSGD_E_INVALID;
+  const StatePlan sp = state_plan(ctx->cfg, ctx->lay);
+  const hipStream_t s = ctx->stream;
+  // the header decides whether the blob fits this context: read it first
+  uint64_t h[8] = {};
+  LSGD_CK(ctx, hipMemcpyAsync(h, d_src, sizeof h, hipMemcpyDeviceToHost, s));
+  LSGD_CK(ctx, hipStreamSynchronize(s));
+  if (h[0] != kStateMagic || h[1] != sp.digest || h[2] != (uint64_t)sp.K ||
+      h[3] != (uint64_t)sp.P || h[4] != (uint64_t)sp.R || h[6] != sp.mask ||
+      h[7] != (uint64_t)sp.total || (int64_t)h[5] < 0)
+    return LSGD_E_INVALID;
+  const char* src = (const char*)d_src;
+  const long long P = sp.P, Ps = ctx->lay.Ps;
+  auto sec = [&](int i) { return (const float*)(src + sp.off[i]); };
+  // replicas through the broadcast kernel, which also refreshes the bf16 copy
+  for (int k = 0; k < sp.K; ++k)
+    LSGD_CK(ctx, lsgd::launch_broadcast(sec(kSecW) + (size_t)k * P, ctx->W(), ctx->Wb(),
+                                        (int)sp.K, P, Ps, k, s));
+  LSGD_CK(ctx, lsgd::launch_copy_rows(ctx->U(), Ps, sec(kSecU), P, P, (int)sp.K, s));
+  if (sp.mask & (1u << kSecRS))
+    LSGD_CK(ctx, lsgd::launch_copy_rows(ctx->RS(), ctx->lay.rp.Rs, sec(kSecRS), sp.R, sp.R,
+                                        (int)sp.K, s));
+  if (sp.mask & (1u << kSecWsync))
+    LSGD_CK(ctx, lsgd::launch_copy_rows(ctx->Wsync(), Ps, sec(kSecWsync), P, P, 1, s));
+  if (sp.mask & (1u << kSecUg))
+    LSGD_CK(ctx, lsgd::launch_copy_rows(ctx->Ug(), Ps, sec(kSecUg), P, P, 1, s));
+  if (sp.mask & (1u << kSecE))
+    LSGD_CK(ctx, lsgd::launch_copy_rows(ctx->E(), Ps, sec(kSecE), P, P, (int)sp.K, s));
+  // a restored state starts without a non-finite loss on record
+  LSGD_CK(ctx, lsgd::launch_fill((float*)ctx->flag(), 0.f, 1, s));
+  ctx->step = (int64_t)h[5];
+  ctx->presampled = -1;
+  return LSGD_OK;
+}
+
 lsgd_status lsgd_get_step(lsgd_ctx* ctx, int64_t* step) {
   if (!ctx || !step) return LSGD_E_INVALID;
   *step = ctx->step;
@@ -1113,7 +1313,9 @@ lsgd_status lsgd_sample_indices(lsgd_ctx* ctx, int64_t step, int32_t* d_idx) {
 lsgd_status lsgd_sync(lsgd_ctx* ctx) {
   LSGD_USABLE(ctx);
   LSGD_CK(ctx, hipStreamSynchronize(ctx->stream));
-  return LSGD_OK;
+  int flag = 0;
+  LSGD_CK(ctx, hipMemcpy(&flag, ctx->flag(), sizeof flag, hipMemcpyDeviceToHost));
+  return flag ? LSGD_E_NONFINITE : LSGD_OK;
 }
 
 lsgd_status lsgd_destroy(lsgd_ctx* ctx) {
@@ -1128,6 +1330,7 @@ const char* lsgd_status_string(lsgd_status s) {
     case LSGD_E_INVALID: return "invalid argument";
     case LSGD_E_WORKSPACE: return "workspace too small";
     case LSGD_E_HIP: return "HIP runtime error";
+    case LSGD_E_NONFINITE: return "non-finite loss";
     case LSGD_E_STATE: return "context unusable after an earlier HIP error";
     case LSGD_E_UNSUPPORTED: return "unsupported";
   }

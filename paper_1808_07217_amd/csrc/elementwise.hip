@@ -45,7 +45,7 @@ __global__ void k_sample_epoch(uint32_t key0, uint32_t key1, uint32_t e, long lo
 __global__ __launch_bounds__(256) void k_xent(const float* Z, const int32_t* y,
                                               const int32_t* idx, int B, int C,
                                               void* dZ, int dz_bf16,
-                                              float* loss) {
+                                              float* loss, int* nonfinite) {
   __shared__ float red[256];
   const int k = blockIdx.x;
   const float invB = 1.0f / (float)B;
@@ -80,7 +80,11 @@ __global__ __launch_bounds__(256) void k_xent(const float* Z, const int32_t* y,
     if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0 && loss) loss[k] = red[0] * invB;
+  if (threadIdx.x == 0) {
+    const float mean = red[0] * invB;
+    if (loss) loss[k] = mean;
+    if (nonfinite && !isfinite(mean)) *nonfinite = 1;
+  }
 }
 
 // ------------------------------------------------------------------ update
@@ -301,6 +305,20 @@ __global__ void k_to_bf16(const float* x, bf16_t* y, long long n) {
     y[i] = f32_to_bf16(x[i]);
 }
 
+// rows x n floats from src (row pitch spitch) to dst (row pitch dpitch):
+// the sections of the state blob against the padded replica rows
+__global__ void k_copy_rows(float* dst, long long dpitch, const float* src,
+                            long long spitch, long long n, int rows) {
+  const int r = blockIdx.y;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x)
+    dst[r * dpitch + i] = src[r * spitch + i];
+}
+
+__global__ void k_put_words(unsigned long long* dst, Words8 v) {
+  if (threadIdx.x < 8) dst[threadIdx.x] = v.w[threadIdx.x];
+}
+
 __global__ void k_fill(float* x, float v, long long n) {
   for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
        i += (long long)gridDim.x * blockDim.x)
@@ -347,9 +365,9 @@ hipError_t launch_sample_epoch(uint64_t seed, int64_t step, int K, int64_t N,
 
 hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,
                        int K, int B, int C, void* dZ, int dz_bf16, float* loss,
-                       hipStream_t s) {
+                       int* nonfinite, hipStream_t s) {
   hipLaunchKernelGGL(k_xent, dim3(K), dim3(256), 0, s, Z, y, idx, B, C, dZ,
-                     dz_bf16, loss);
+                     dz_bf16, loss, nonfinite);
   return hipGetLastError();
 }
 
@@ -454,6 +472,23 @@ hipError_t launch_to_bf16(const float* x, bf16_t* y, long long n,
                           hipStream_t s) {
   hipLaunchKernelGGL(k_to_bf16, dim3(grid_for(n, 256)), dim3(256), 0, s, x, y,
                      n);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(float* dst, long long dpitch, const float* src,
+                            long long spitch, long long n, int rows,
+                            hipStream_t s) {
+  if (rows <= 0 || n <= 0) return hipSuccess;
+  long long b = (n + 255) / 256;
+  if (b > 65535) b = 65535;
+  hipLaunchKernelGGL(k_copy_rows, dim3((unsigned)b, rows), dim3(256), 0, s, dst,
+                     dpitch, src, spitch, n, rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_put_words(void* dst, const Words8& v, hipStream_t s) {
+  hipLaunchKernelGGL(k_put_words, dim3(1), dim3(64), 0, s,
+                     (unsigned long long*)dst, v);
   return hipGetLastError();
 }
 

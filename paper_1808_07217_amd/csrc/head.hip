@@ -296,7 +296,13 @@ __global__ __launch_bounds__(256) void k_head_wgrad(HeadArgs h) {
     if ((int)threadIdx.x < w2) red[threadIdx.x] += red[threadIdx.x + w2];
     __syncthreads();
   }
-  if (threadIdx.x == 0 && h.loss) h.loss[k] = red[0] / (float)B;
+  if (threadIdx.x == 0) {
+    const float mean = red[0] / (float)B;
+    if (h.loss) h.loss[k] = mean;
+    // a non-finite loss raises the context's flag (a plain store: every
+    // writer stores the same value)
+    if (h.nonfinite && !isfinite(mean)) *h.nonfinite = 1;
+  }
 }
 
 // Weight gradient of the output layer in one memory round trip (fp32,
@@ -398,7 +404,13 @@ __global__ __launch_bounds__(256) void k_head_wgrad_vec(HeadArgs h) {
     if ((int)threadIdx.x < w2) red[threadIdx.x] += red[threadIdx.x + w2];
     __syncthreads();
   }
-  if (threadIdx.x == 0 && h.loss) h.loss[k] = red[0] / (float)B;
+  if (threadIdx.x == 0) {
+    const float mean = red[0] / (float)B;
+    if (h.loss) h.loss[k] = mean;
+    // a non-finite loss raises the context's flag (a plain store: every
+    // writer stores the same value)
+    if (h.nonfinite && !isfinite(mean)) *h.nonfinite = 1;
+  }
 }
 
 // Register-resident variant for fp32, a class count fixed at compile time,

@@ -114,6 +114,8 @@ struct HeadArgs {
   void* dZprev;              // [K][B][D] masked input gradient, or nullptr
   float* rowloss;            // [K][B]
   float* loss;               // [K] or nullptr
+  int* nonfinite;            // set to 1 when a replica's mean loss is not
+                             //   finite (never cleared here), or nullptr
   float lr, mom, wd;
   int nesterov;
   int nomask;                // dZprev without the ReLU mask (pooled inputs)
@@ -145,8 +147,12 @@ int conv_wgrad_splits(int Bt, int Ho, int Wo);
 // (per 256-row chunk, [G][R/256][Cout][2] doubles: sum, sum of squares) when
 // q.stats is set; the caller then finalises with launch_bn_finalize_chunks.
 bool conv_fwd_stats(const ConvGeom& q);
+// Both finalisers also update the running statistics when rm is set: the
+// running means rm[g * sRS + c] and variances rv[g * sRS + c] of replica g
+// (factor 0.1 on the batch mean and the unbiased batch variance).
 hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
-                                     float* mu, float* inv, hipStream_t st);
+                                     float* mu, float* inv, float* rm, float* rv,
+                                     long long sRS, hipStream_t st);
 int bn_chunks(int R);
 hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st);
 hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, float* W,
@@ -155,7 +161,8 @@ hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, floa
 hipError_t launch_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
                           float* Wt, hipStream_t st);
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
-                           float* mu, float* inv, hipStream_t st);
+                           float* mu, float* inv, float* rm, float* rv, long long sRS,
+                           hipStream_t st);
 hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
@@ -184,7 +191,7 @@ hipError_t launch_sample(uint64_t seed, int64_t step, int K, int64_t N,
                          int B, int32_t* idx, hipStream_t s);
 hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,
                        int K, int B, int C, void* dZ, int dz_bf16,
-                       float* loss, hipStream_t s);
+                       float* loss, int* nonfinite, hipStream_t s);
 hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
                              float lr, float mom, float wd, int nesterov,
                              hipStream_t s);
@@ -207,6 +214,7 @@ struct TinyArgs {
   float* W;            // [K][Ps] replicas (read, then the averaged model)
   float* U;            // [K][Ps] momentum buffers
   float* loss;         // [H][K] or nullptr
+  int* nonfinite;      // set to 1 on a non-finite mean loss, or nullptr
   long long N, Ps, step0;
   long long S;         // batches per epoch of the reshuffle sampler; 0: i.i.d.
   int K, B, D, C, H, m;
@@ -217,6 +225,8 @@ struct TinyArgs {
 };
 size_t tiny_round_lds_bytes(int K, int B, int D, int C);
 bool tiny_round_fits(int K, int B, int D, int C, int H);
+// true when the round takes the 256-thread-per-replica kernel
+bool tiny_round_wide(int K, int B, int D, int C, int H);
 hipError_t launch_tiny_round(const TinyArgs& a, hipStream_t s);
 // Sign-compressed synchronisation (compress.hip): W fp32 [K][Ps] replicas
 // (the first P elements of each row are the model), ws fp32 [Ps] the model
@@ -238,5 +248,12 @@ hipError_t launch_broadcast(const float* src, float* W, bf16_t* Wb, int K,
 hipError_t launch_to_bf16(const float* x, bf16_t* y, long long n,
                           hipStream_t s);
 hipError_t launch_fill(float* x, float v, long long n, hipStream_t s);
+// rows x n floats between row-pitched buffers (pitches in floats)
+hipError_t launch_copy_rows(float* dst, long long dpitch, const float* src,
+                            long long spitch, long long n, int rows,
+                            hipStream_t s);
+// eight 64-bit words, passed by value, stored at dst (8-byte aligned)
+struct Words8 { unsigned long long w[8]; };
+hipError_t launch_put_words(void* dst, const Words8& v, hipStream_t s);
 
 }  // namespace lsgd

@@ -1037,6 +1037,17 @@ __global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
   }
 }
 
+// Running statistics of a BN layer after a training batch of R values per
+// channel: exponential averages (factor kBnRunMomentum) of the batch mean and
+// of the unbiased variance var R / (R - 1), in fp64 and stored as fp32.
+constexpr double kBnRunMomentum = 0.1;
+__device__ __forceinline__ void bn_running(float* rm, float* rv, long long o, double m,
+                                           double var, int R) {
+  const double a = kBnRunMomentum;
+  rm[o] = (float)((1.0 - a) * (double)rm[o] + a * m);
+  rv[o] = (float)((1.0 - a) * (double)rv[o] + a * (var * ((double)R / (double)(R - 1))));
+}
+
 // Forward: mu, inv = 1/sqrt(var + eps) from the partials (chunks in order).
 // Backward: the input-gradient coefficients and the update of gamma, beta:
 //   dbeta = sum dz, dgamma = sum dz*xhat,
@@ -1046,7 +1057,8 @@ __global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
 __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int R,
                               float* mu, float* inv, float* coef, float* gamma,
                               float* beta, float* ug, float* ub, long long sP,
-                              float lr, float mom, int nesterov, float eps) {
+                              float lr, float mom, int nesterov, float eps, float* rm,
+                              float* rv, long long sRS) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= G * C) return;
   const int g = i / C, c = i % C;
@@ -1062,6 +1074,7 @@ __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int 
     if (var < 0.0) var = 0.0;
     mu[i] = (float)m;
     inv[i] = (float)(1.0 / sqrt(var + (double)eps));
+    if (rm) bn_running(rm, rv, (long long)g * sRS + c, m, var, R);
     return;
   }
   const long long o = (long long)g * sP + c;
@@ -1093,7 +1106,7 @@ __global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int 
 __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
     const double* part, int nchunk, int C, int R, float* mu, float* inv, float* coef,
     float* gamma, float* beta, float* ug, float* ub, long long sP, float lr, float mom,
-    int nesterov, float eps) {
+    int nesterov, float eps, float* rm, float* rv, long long sRS) {
   __shared__ double red[2][kT];
   const int g = blockIdx.x, t = threadIdx.x;
   const int L = kT / C, c = t % C, q = t / C;
@@ -1124,6 +1137,7 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
     if (var < 0.0) var = 0.0;
     mu[i] = (float)m;
     inv[i] = (float)(1.0 / sqrt(var + (double)eps));
+    if (rm) bn_running(rm, rv, (long long)g * sRS + c, m, var, R);
     return;
   }
   const long long o = (long long)g * sP + c;
@@ -1652,7 +1666,8 @@ bool al16p(const void* p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
 int bn_chunks(int R) { return (R + kChunkRows - 1) / kChunkRows; }
 
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
-                           float* mu, float* inv, hipStream_t st) {
+                           float* mu, float* inv, float* rm, float* rv, long long sRS,
+                           hipStream_t st) {
   const int nch = bn_chunks(R);
   if (bn_vec_shift(C) >= 0 && al16p(y) && (long long)R * C < (1LL << 31) && G <= 65535)
     hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
@@ -1663,24 +1678,25 @@ hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
   if (bn_vec_shift(C) >= 0 && C <= kT)
     hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R, mu,
                        inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
-                       1e-5f);
+                       1e-5f, rm, rv, sRS);
   else
     hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
                        nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
-                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
+                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f, rm, rv, sRS);
   return hipGetLastError();
 }
 
 hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
-                                     float* mu, float* inv, hipStream_t st) {
+                                     float* mu, float* inv, float* rm, float* rv,
+                                     long long sRS, hipStream_t st) {
   if (bn_vec_shift(C) >= 0 && C <= kT)
     hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nchunk, C, R, mu,
                        inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
-                       1e-5f);
+                       1e-5f, rm, rv, sRS);
   else
     hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
                        nchunk, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
-                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f);
+                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f, rm, rv, sRS);
   return hipGetLastError();
 }
 
@@ -1723,11 +1739,11 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
   if (bn_vec_shift(C) >= 0 && C <= kT)
     hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
                        (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
-                       nesterov, 1e-5f);
+                       nesterov, 1e-5f, nullptr, nullptr, 0LL);
   else
     hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
                        nch, G, C, R, (float*)mu, (float*)inv, coef, gamma, beta, ug, ub,
-                       sP, lr, mom, nesterov, 1e-5f);
+                       sP, lr, mom, nesterov, 1e-5f, nullptr, nullptr, 0LL);
   if (v4)
     hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
                        st, y, gup, maskv, R, C, mu, inv, coef, dy);

@@ -21,6 +21,8 @@
 //     in LDS.
 // Then the replicas are averaged in the replica-average tree order and
 // replicas and buffers are written back.
+#include <atomic>
+
 #include "kernels.h"
 #include "device_common.h"
 
@@ -176,7 +178,11 @@ __global__ __launch_bounds__(kTinyThreads) void k_tiny_round(TinyArgs a) {
           }
         }
         lsum = wave_sum_fixed(lsum);
-        if (lane == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
+        if (lane == 0) {
+          const float mean = lsum * invB;
+          if (a.loss) a.loss[h * K + k] = mean;
+          if (a.nonfinite && !isfinite(mean)) *a.nonfinite = 1;
+        }
       }
       __syncthreads();
       if (mine) {
@@ -544,7 +550,11 @@ __global__ __launch_bounds__(kWideThreads) void k_tiny_round_wide(TinyArgs a) {
           lsum += d <= 0.f ? log1pf(v) : d + logf(v);  // d = 0: the label is the max
         }
         lsum = wave_sum_fixed(lsum);
-        if (lane == 0 && a.loss) a.loss[h * K + k] = lsum * invB;
+        if (lane == 0) {
+          const float mean = lsum * invB;
+          if (a.loss) a.loss[h * K + k] = mean;
+          if (a.nonfinite && !isfinite(mean)) *a.nonfinite = 1;
+        }
       }
       // weight gradient and update: wave rank wr takes blocks wr, wr + 4, ...
       const int nib = (D + 16) >> 4;  // ceil((D + 1) / 16)
@@ -624,33 +634,38 @@ size_t tiny_wide_lds_bytes(int K, int B, int D, int C, int H) {
 }
 
 // The kernel's dynamic LDS above the default 64 KB: requested once per
-// device and instance (gfx950 compute units hold 160 KB).
+// device and instance (gfx950 compute units hold 160 KB). The per-device
+// flags are atomics: contexts on different host threads may launch at once
+// (the request itself is idempotent).
 template <int CM, bool Wide>
 hipError_t allow_lds(size_t bytes) {
-  static bool done[64] = {};
+  static std::atomic<bool> done[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess || dev < 0 || dev >= 64) return e != hipSuccess ? e : hipErrorInvalidDevice;
-  if (bytes <= 64 * 1024 || done[dev]) return hipSuccess;
+  if (bytes <= 64 * 1024 || done[dev].load(std::memory_order_acquire)) return hipSuccess;
   e = hipFuncSetAttribute(Wide ? (const void*)k_tiny_round_wide<CM> : (const void*)k_tiny_round<CM>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kTinyMaxLds);
-  if (e == hipSuccess) done[dev] = true;
+  if (e == hipSuccess) done[dev].store(true, std::memory_order_release);
   return e;
 }
 
-// LDS one workgroup may opt in to on the current device (cached per device).
+// LDS one workgroup may opt in to on the current device (cached per device
+// in an atomic; concurrent first queries store the same value).
 size_t tiny_lds_limit() {
-  static size_t limit[64] = {};
+  static std::atomic<size_t> limit[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (!limit[dev]) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeSharedMemPerBlockOptin, dev) != hipSuccess ||
-        v <= 0)
-      v = 64 * 1024;
-    limit[dev] = (size_t)v;
+  size_t v = limit[dev].load(std::memory_order_acquire);
+  if (!v) {
+    int q = 0;
+    if (hipDeviceGetAttribute(&q, hipDeviceAttributeSharedMemPerBlockOptin, dev) != hipSuccess ||
+        q <= 0)
+      q = 64 * 1024;
+    v = (size_t)q;
+    limit[dev].store(v, std::memory_order_release);
   }
-  return limit[dev];
+  return v;
 }
 
 bool tiny_round_fits(int K, int B, int D, int C, int H) {
@@ -660,11 +675,18 @@ bool tiny_round_fits(int K, int B, int D, int C, int H) {
   return lds <= kTinyMaxLds && lds <= tiny_lds_limit();
 }
 
+// Whether the 256-thread-per-replica kernel runs (up to four replicas, when
+// its larger LDS request fits); otherwise the wave-per-replica kernel does.
+bool tiny_round_wide(int K, int B, int D, int C, int H) {
+  const size_t wide = tiny_wide_lds_bytes(K, B, D, C, H);
+  return K * kRepThreads <= kWideThreads && wide <= kTinyMaxLds && wide <= tiny_lds_limit();
+}
+
 template <int CM>
 hipError_t launch_round(const TinyArgs& a, hipStream_t s) {
   hipError_t e;
-  const size_t wide = tiny_wide_lds_bytes(a.K, a.B, a.D, a.C, a.H);
-  if (a.K * kRepThreads <= kWideThreads && wide <= kTinyMaxLds && wide <= tiny_lds_limit()) {
+  if (tiny_round_wide(a.K, a.B, a.D, a.C, a.H)) {
+    const size_t wide = tiny_wide_lds_bytes(a.K, a.B, a.D, a.C, a.H);
     if ((e = allow_lds<CM, true>(wide)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_tiny_round_wide<CM>, dim3(1), dim3(kWideThreads), wide, s, a);
   } else {

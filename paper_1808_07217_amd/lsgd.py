@@ -79,6 +79,9 @@ _SIGS = {
     "lsgd_set_step": [_P, _c.c_int64],
     "lsgd_sample_indices": [_P, _c.c_int64, _P],
     "lsgd_sync": [_P],
+    "lsgd_state_bytes": [_c.POINTER(Config), _c.POINTER(_c.c_size_t)],
+    "lsgd_read_state": [_P, _P],
+    "lsgd_write_state": [_P, _P],
     "lsgd_destroy": [_P],
     "lsgd_status_string": [_c.c_int],
     "lsgd_last_error": [_P],
@@ -104,8 +107,20 @@ _lib.lsgd_last_error.restype = _c.c_char_p
 EXPORTED = tuple(_SIGS)
 
 
+E_NONFINITE = 6
+STATE_MAGIC = 0x3154535F4447534C
+STATE_SECTIONS = ("W", "U", "RS", "w_sync", "u_global", "E")
+
+
 class LsgdError(RuntimeError):
-    pass
+    def __init__(self, msg, status):
+        super().__init__(msg)
+        self.status = status
+
+
+class NonFiniteLoss(LsgdError):
+    """lsgd_sync reported LSGD_E_NONFINITE: a local step's loss was not
+    finite."""
 
 
 def _check(status: int, ctx=None) -> None:
@@ -115,7 +130,8 @@ def _check(status: int, ctx=None) -> None:
             detail = _lib.lsgd_last_error(ctx).decode()
             if detail:
                 msg += f" ({detail})"
-        raise LsgdError(f"liblsgd: {msg} [status {status}]")
+        cls = NonFiniteLoss if status == E_NONFINITE else LsgdError
+        raise cls(f"liblsgd: {msg} [status {status}]", status)
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -162,6 +178,39 @@ def workspace_bytes(cfg: Config) -> int:
     out = _c.c_size_t()
     _check(_lib.lsgd_workspace_bytes(_c.byref(cfg), _c.byref(out)))
     return out.value
+
+
+def state_bytes(cfg: Config) -> int:
+    out = _c.c_size_t()
+    _check(_lib.lsgd_state_bytes(_c.byref(cfg), _c.byref(out)))
+    return out.value
+
+
+def _aligned_bytes(n: int, device) -> torch.Tensor:
+    """A uint8 device tensor of n bytes starting on a 256-byte boundary."""
+    raw = torch.empty(n + 256, dtype=torch.uint8, device=device)
+    off = (-raw.data_ptr()) % 256
+    return raw[off:off + n]
+
+
+def parse_state(blob: torch.Tensor) -> dict:
+    """The header fields and section views (float32 [rows][n] on the blob's
+    device) of a state blob, by the layout lsgd.h documents."""
+    words = blob[:64].cpu().view(torch.int64).tolist()
+    if words[0] & (2**64 - 1) != STATE_MAGIC:
+        raise ValueError("not a state blob")
+    K, P, R, step, mask, total = words[2], words[3], words[4], words[5], words[6], words[7]
+    out = {"K": K, "P": P, "R": R, "step": step, "mask": mask, "bytes": total}
+    o = 256
+    shapes = {"W": (K, P), "U": (K, P), "RS": (K, R), "w_sync": (1, P),
+              "u_global": (1, P), "E": (K, P)}
+    for i, name in enumerate(STATE_SECTIONS):
+        if not mask >> i & 1:
+            continue
+        rows, n = shapes[name]
+        out[name] = blob[o:o + rows * n * 4].view(torch.float32).view(rows, n)
+        o = (o + rows * n * 4 + 255) // 256 * 256
+    return out
 
 
 class Replicas:
@@ -313,7 +362,24 @@ class Replicas:
         return out
 
     def sync(self):
+        """Wait for the stream; raises NonFiniteLoss after a non-finite
+        loss (see lsgd_sync)."""
         _check(_lib.lsgd_sync(self._ctx), self._ctx)
+
+    def read_state(self, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """The whole training state as one device blob (lsgd_read_state)."""
+        n = state_bytes(self.cfg)
+        out = out if out is not None else _aligned_bytes(n, self.device)
+        if out.dtype != torch.uint8 or out.numel() < n or out.data_ptr() % 256:
+            raise ValueError(f"out must be a 256-byte aligned uint8 tensor of {n} bytes")
+        _check(_lib.lsgd_read_state(self._ctx, _ptr(out)), self._ctx)
+        return out
+
+    def write_state(self, blob: torch.Tensor):
+        """Restore a blob written by read_state (lsgd_write_state)."""
+        if blob.dtype != torch.uint8 or blob.data_ptr() % 256:
+            raise ValueError("blob must be a 256-byte aligned uint8 tensor")
+        _check(_lib.lsgd_write_state(self._ctx, _ptr(blob)), self._ctx)
 
     def close(self):
         if getattr(self, "_ctx", None):

@@ -107,3 +107,63 @@ def test_null_context_calls_fail_cleanly():
     for s in range(7):
         assert lib.lsgd_status_string(s)
     assert lib.lsgd_last_error(None) == b""
+
+
+def test_header_compiles_as_c99(tmp_path):
+    """include/lsgd.h is a plain C99 header: a C translation unit that takes
+    the address of every declared function compiles warning-free with
+    -std=c99 -pedantic."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use_lsgd.c"
+    refs = "\n".join(f"  (void)&{n};" for n in _declared())
+    src.write_text('#include "lsgd.h"\n#include <stdio.h>\n'
+                   "int main(void) {\n"
+                   "  lsgd_config cfg = {0};\n"
+                   "  lsgd_status st = LSGD_E_NONFINITE;\n"
+                   f"{refs}\n"
+                   "  (void)cfg;\n"
+                   "  printf(\"%d\\n\", (int)st);\n"
+                   "  return 0;\n}\n")
+    r = subprocess.run([cc, "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror",
+                        "-I", os.path.join(ROOT, "include"), "-c", str(src), "-o",
+                        str(tmp_path / "use_lsgd.o")], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def _al(n):
+    return (n + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("name,scheme,gm,sections", [
+    ("resnet20", "local", 0.0, ("W", "U", "RS")),
+    ("mlp_512", "local", 0.0, ("W", "U")),
+    ("mlp_512", "ef_sign", 0.0, ("W", "U", "w_sync", "E")),
+    ("mlp_512", "sign", 0.0, ("W", "U", "w_sync")),
+    ("mlp_512", "local", 0.3, ("W", "U", "w_sync", "u_global")),
+])
+def test_state_blob_size_follows_the_documented_layout(name, scheme, gm, sections):
+    """lsgd_state_bytes: a 256-byte header, then each present section at a
+    256-byte aligned offset (replicas, momentum, BN running statistics of
+    R = 2 x (16 x 7 + 32 x 6 + 64 x 6) = 1376 values, w_s, u, memories)."""
+    from paper_1808_07217_amd import lsgd as L
+    w = wk.get(name)
+    cfg = L.make_config(w.widths, w.K, w.B_loc, w.N, dtype=w.dtype, model=w.model,
+                        scheme=scheme, global_momentum=gm)
+    K, P = w.K, L.param_count(cfg)
+    R = 2 * (16 * 7 + 32 * 6 + 64 * 6)
+    size = {"W": K * P, "U": K * P, "RS": K * R, "w_sync": P, "u_global": P, "E": K * P}
+    assert L.state_bytes(cfg) == 256 + sum(_al(4 * size[s]) for s in sections)
+
+
+def test_state_and_failure_calls_fail_cleanly():
+    from paper_1808_07217_amd import lsgd as L
+    lib = L._lib
+    assert lib.lsgd_read_state(None, None) == 1
+    assert lib.lsgd_write_state(None, None) == 1
+    assert lib.lsgd_sync(None) == 1
+    assert lib.lsgd_state_bytes(None, None) == 1
+    assert lib.lsgd_status_string(6) == b"non-finite loss"
