@@ -398,6 +398,26 @@ lsgd_status lsgd_replica_sign_sync(float* d_W, int32_t K, int64_t P,
                                    float* d_wsync, float* d_E, void* d_scratch,
                                    size_t scratch_bytes, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * lsgd_replica_sign_sync with its scratch taken from a static device array
+ * of LSGD_SIGN_SYNC_STATIC_BYTES that the library holds on each GPU it runs
+ * on until the process ends, so the call allocates nothing (the caller
+ * still passes d_W, d_wsync and d_E). Same arguments, kernels and results as
+ * lsgd_replica_sign_sync, bit for bit. Problems needing more scratch than
+ * the array holds (lsgd_sign_sync_scratch_bytes(K, P) > 16 MiB, i.e.
+ * about K * P > 6.7e7 elements) return LSGD_E_WORKSPACE and launch nothing.
+ * Every call on one GPU shares the array: calls that overlap on one GPU
+ * (different streams or host threads) race and must be ordered by the
+ * caller. The array keeps the last call's contents; nothing in it needs to
+ * start at zero.
+ */
+#define LSGD_SIGN_SYNC_STATIC_BYTES (16u << 20)
+lsgd_status lsgd_replica_sign_sync_static(float* d_W, int32_t K, int64_t P,
+                                          float* d_wsync, float* d_E,
+                                          void* stream);
+
 /* In-place block average of d_W fp32 [K][P]: each of the K/Kb groups of Kb
  * consecutive rows is replaced by its mean (the kernel behind
  * lsgd_average_blocks). Kb must divide K, else LSGD_E_INVALID. */

@@ -1471,6 +1471,18 @@ lsgd_status lsgd_replica_sign_sync(float* d_W, int32_t K, int64_t P,
                                                                 : LSGD_E_HIP);
 }
 
+lsgd_status lsgd_replica_sign_sync_static(float* d_W, int32_t K, int64_t P,
+                                          float* d_wsync, float* d_E, void* stream) {
+  static_assert(LSGD_SIGN_SYNC_STATIC_BYTES == lsgd::kSignSyncStaticBytes,
+                "the header states the static scratch size");
+  if (!d_W || !d_wsync || K < 1 || P < 0 || P % 4) return LSGD_E_INVALID;
+  if (lsgd::sign_sync_scratch_bytes(K, P) > lsgd::kSignSyncStaticBytes)
+    return LSGD_E_WORKSPACE;
+  hipError_t e = lsgd::launch_sign_sync_static(d_W, d_E, d_wsync, K, P, (hipStream_t)stream);
+  return e == hipSuccess ? LSGD_OK : (e == hipErrorInvalidValue ? LSGD_E_INVALID
+                                                                : LSGD_E_HIP);
+}
+
 lsgd_status lsgd_sgd_update(float* d_W, float* d_U, const float* d_G, int64_t n,
                             float lr, float momentum, float weight_decay,
                             int32_t nesterov, void* stream) {

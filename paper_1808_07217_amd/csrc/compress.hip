@@ -9,6 +9,8 @@
 // replica the scale p^k from its partials in a fixed order; then the new
 // model from the packed signs (or, with memories, from delta recomputed in
 // the same arithmetic, which also updates e^k = delta^k - s^k p^k).
+#include <mutex>
+
 #include "kernels.h"
 
 namespace lsgd {
@@ -156,6 +158,42 @@ SignPlan sign_plan(int K, long long Ps) {
 
 size_t sign_sync_scratch_bytes(int K, long long Ps) {
   return (K < 1 || Ps < 0) ? 0 : sign_plan(K, Ps).total;
+}
+
+// Scratch of the allocation-free sign synchronisation: one static array per
+// device, alive until the process ends. Every call on a device shares it
+// (calls that overlap on one device race); nothing in it needs clearing,
+// since each launch writes all of the scratch it later reads.
+__device__ __align__(256) unsigned char scratch[kSignSyncStaticBytes];
+
+namespace {
+// The array's device address, looked up once per device with that device
+// current (the host-side name is only a stand-in for the symbol).
+hipError_t static_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_sign_sync_static(float* W, float* E, float* ws, int K, long long P,
+                                   hipStream_t s) {
+  void* p = nullptr;
+  hipError_t e = static_scratch(&p);
+  if (e != hipSuccess) return e;
+  return launch_sign_sync(W, nullptr, E, ws, K, P, P, p, kSignSyncStaticBytes, s);
 }
 
 hipError_t launch_sign_sync(float* W, bf16_t* Wb, float* E, float* ws, int K,

@@ -237,6 +237,12 @@ size_t sign_sync_scratch_bytes(int K, long long Ps);
 hipError_t launch_sign_sync(float* W, bf16_t* Wb, float* E, float* ws, int K,
                             long long P, long long Ps, void* scratch,
                             size_t scratch_bytes, hipStream_t s);
+// The same on plain [K][P] arrays with the scratch in a static device array
+// of kSignSyncStaticBytes (no allocation; hipErrorInvalidValue when the
+// problem needs more).
+constexpr size_t kSignSyncStaticBytes = 16u << 20;
+hipError_t launch_sign_sync_static(float* W, float* E, float* ws, int K, long long P,
+                                   hipStream_t s);
 // The same average within each of `blocks` groups of Kb consecutive rows
 // (mean_out only with blocks == 1).
 hipError_t launch_average_blocks(float* W, bf16_t* Wb, int Kb, int blocks,

@@ -66,6 +66,7 @@ _SIGS = {
     "lsgd_sign_sync_scratch_bytes": [_c.c_int32, _c.c_int64, _P],
     "lsgd_replica_sign_sync": [_P, _c.c_int32, _c.c_int64, _P, _P, _P,
                                _c.c_size_t, _P],
+    "lsgd_replica_sign_sync_static": [_P, _c.c_int32, _c.c_int64, _P, _P, _P],
     "lsgd_read_global_momentum": [_P, _P],
     "lsgd_write_global_momentum": [_P, _P],
     "lsgd_replica_average_global_momentum": [_P, _c.c_int32, _c.c_int64, _P, _P,
@@ -491,6 +492,23 @@ def replica_sign_sync(W: torch.Tensor, w_sync: torch.Tensor,
     scratch = torch.empty(max(1, nb.value), dtype=torch.uint8, device=W.device)
     _check(_lib.lsgd_replica_sign_sync(
         _ptr(W), K, P, _ptr(w_sync), _ptr(E), _ptr(scratch), nb.value,
+        _stream_handle(torch.cuda.current_stream(W.device))))
+
+
+def replica_sign_sync_static(W: torch.Tensor, w_sync: torch.Tensor,
+                             E: Optional[torch.Tensor] = None) -> None:
+    """replica_sign_sync through the entry point that allocates nothing (its
+    scratch is the library's static device array)."""
+    ts = (W, w_sync) if E is None else (W, w_sync, E)
+    for t in ts:
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous float32")
+    if W.dim() != 2 or w_sync.numel() != W.shape[1] or (
+            E is not None and E.shape != W.shape):
+        raise ValueError("W, E must be [K][P] and w_sync [P]")
+    K, P = W.shape
+    _check(_lib.lsgd_replica_sign_sync_static(
+        _ptr(W), K, P, _ptr(w_sync), _ptr(E),
         _stream_handle(torch.cuda.current_stream(W.device))))
 
 
