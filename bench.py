@@ -182,7 +182,6 @@ def resnet_step_costs(w) -> dict:
         add("bn_apply", 0, 2 * y + sc)
         add("bn_bwd", 0, (7 if second else 5) * y)
         if i > 0:
-            add("conv_wt", 0, 2 * wt)
             add("conv_dgrad", fl, y + x + wt)
         add("conv_wgrad", fl, x + y + wt)
         add("conv_wupdate", 0, 5 * wt)

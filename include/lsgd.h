@@ -66,7 +66,7 @@ typedef enum lsgd_status {
 /* LSGD_MODEL_MLP: ReLU MLP with widths d_0 .. d_L (L = 1 is softmax
  * regression). LSGD_MODEL_RESNET20: the CIFAR ResNet-20 of the paper's Table 5
  * on 32x32x3 NHWC images (widths[0] = 3072, widths[1] = classes <= 32,
- * n_layers = 1, fp32): a 3x3 stem convolution to 16 channels, three stages of
+ * n_layers = 1, fp32, B_loc < 131072): a 3x3 stem convolution to 16 channels, three stages of
  * three basic blocks at 16/32/64 channels (stride 2 entering stages 2 and 3,
  * option-A shortcuts: subsample and zero-pad channels), batch normalisation
  * with per-replica batch statistics after every convolution (no weight decay

@@ -34,7 +34,7 @@ struct ResPlan {
   int64_t offFcW = 0, offFcB = 0;
   int classes = 0, feat = 64, side_out = 8;
   size_t featb = 0, dfeat = 0, dzh = 0, gbuf[4] = {}, mu = 0, inv = 0, coef = 0,
-         bnpart = 0, wpart = 0, wt = 0;
+         bnpart = 0, wpart = 0;
   // BN running statistics [K][Rs] fp32: per replica the running means of
   // every BN layer in convolution order (layer i from rsoff[i]), then the
   // running variances in the same order (from rs_half); R = 2 rs_half
@@ -71,8 +71,11 @@ int upd_mode(const lsgd_config& cf) {
 bool valid_config(const lsgd_config* c) {
   if (!c) return false;
   if (c->model == LSGD_MODEL_RESNET20) {
+    // B_loc below 2^17 keeps each replica's largest activation under 2^31
+    // values (the BN and shortcut kernels index it in 32 bits)
     if (c->n_layers != 1 || c->widths[0] != 3072 || c->widths[1] < 2 ||
-        c->widths[1] > lsgd::kHeadMaxClasses || c->gemm_dtype != LSGD_FP32)
+        c->widths[1] > lsgd::kHeadMaxClasses || c->gemm_dtype != LSGD_FP32 ||
+        c->B_loc >= (1 << 17))
       return false;
   } else if (c->model != LSGD_MODEL_MLP) {
     return false;
@@ -160,7 +163,7 @@ Layout make_resnet_layout(const lsgd_config* c) {
   }
   l.idx = take(K * B * 4);
   l.rowloss = take(K * B * 4);
-  size_t maxact = 0, maxpart = 0, maxbn = 0, maxwt = 0;
+  size_t maxact = 0, maxpart = 0, maxbn = 0;
   for (int i = 0; i < kResConvs; ++i) {
     const ConvSpec& q = r.cv[i];
     const size_t sz = K * B * q.Ho * q.Wo * q.Cout * 4;
@@ -172,7 +175,6 @@ Layout make_resnet_layout(const lsgd_config* c) {
     maxbn = std::max(maxbn, K * lsgd::bn_chunks(c->B_loc * q.Ho * q.Wo) * q.Cout * 2 * 8);
     // the forward convolutions' statistics: one partial per 256 output rows
     maxbn = std::max(maxbn, K * ((size_t)c->B_loc * q.Ho * q.Wo / 256 + 1) * q.Cout * 2 * 8);
-    maxwt = std::max(maxwt, K * 9 * q.Cin * q.Cout * 4);
   }
   r.featb = take(K * B * 64 * 4);
   r.dfeat = take(K * B * 64 * 4);
@@ -183,7 +185,6 @@ Layout make_resnet_layout(const lsgd_config* c) {
   r.coef = take(K * 64 * 5 * 4);
   r.bnpart = take(maxbn);
   r.wpart = take(maxpart);
-  r.wt = take(maxwt);
   l.total = t;
   return l;
 }
@@ -737,7 +738,6 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   float* gb[4] = {F(r.gbuf[0]), F(r.gbuf[1]), F(r.gbuf[2]), F(r.gbuf[3])};
   float* coef = F(r.coef);
   float* wpart = F(r.wpart);
-  float* wt = F(r.wt);
   LSGD_LAUNCH(c, "gap_bwd", lsgd::launch_gap(nullptr, K * B, S, 64, nullptr, true,
                                              F(r.dfeat), gb[0], s));
   int cur = 0;  // gb[cur] holds the gradient of the current block output
@@ -772,14 +772,10 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                           s));
     return LSGD_OK;
   };
-  // input gradient of conv i (old weight, channels swapped per tap)
+  // input gradient of conv i (reads the old weight, before its update)
   auto dgrad = [&](int i, const float* dy, float* dx) -> lsgd_status {
-    const ConvSpec& q = r.cv[i];
-    LSGD_LAUNCH(c, "conv_wt", lsgd::launch_conv_wt(W + q.offW, Ps, K, q.Cin, q.Cout, wt, s));
     lsgd::ConvGeom g = geom(i);
     g.dy = dy;
-    g.Wk = wt;
-    g.sW = 9LL * q.Cin * q.Cout;
     g.out = dx;
     LSGD_LAUNCH(c, "conv_dgrad", lsgd::launch_conv(lsgd::CONV_DGRAD_MODE, g, s));
     return LSGD_OK;

@@ -158,8 +158,6 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st);
 hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, float* W,
                                float* U, long long sP, float lr, float mom, float wd,
                                int nesterov, hipStream_t st);
-hipError_t launch_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
-                          float* Wt, hipStream_t st);
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
                            float* mu, float* inv, float* rm, float* rv, long long sRS,
                            hipStream_t st);

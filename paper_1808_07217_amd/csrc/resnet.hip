@@ -5,11 +5,12 @@
 //    fp32 matrix cores. The operand loader maps GEMM coordinates to tensor
 //    addresses on the fly -- no im2col buffer:
 //      forward      y[m][co]  = sum_k x(m, k) W[k][co],       k = (kh, kw, ci)
-//      input grad   dx[m][ci] = sum_k dy(m, k) Wt[k][ci],     k = (kh, kw, co)
+//      input grad   dx[m][ci] = sum_k dy(m, k) W[(kh, kw, ci)][co], k = (kh, kw, co)
 //      weight grad  dW[k][co] = sum_m x(m, k) dy[m][co]       (split over m)
-//    where x(m, k) is the padded input at output position m and tap (kh, kw),
-//    dy(m, k) the output gradient that reaches input position m through tap
-//    (kh, kw), and Wt the weight with (ci, co) swapped.
+//    where x(m, k) is the padded input at output position m and tap (kh, kw)
+//    and dy(m, k) the output gradient that reaches input position m through
+//    tap (kh, kw); the input gradient reads the weight in its forward layout
+//    with the channel roles swapped as it stages it.
 //  * batch normalisation with batch statistics per replica (the per-worker BN
 //    of the CIFAR setup): fp64 partial sums per row chunk, reduced in a fixed
 //    order, so the statistics are deterministic;
@@ -61,168 +62,6 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
   }
 }
 
-// Pointer to element (m, k) of the forward operand x(m, k), nullptr if the
-// tap falls into the padding.
-__device__ __forceinline__ const float* fwd_addr(const ConvArgs& c, int g, int m,
-                                                 int k) {
-  const int HWo = c.Ho * c.Wo;
-  const int b = m / HWo, p = m - b * HWo;
-  const int oh = p / c.Wo, ow = p - oh * c.Wo;
-  const int tap = k / c.Cin, ci = k - tap * c.Cin;
-  const int kh = tap / 3, kw = tap - kh * 3;
-  const int ih = oh * c.stride + kh - 1, iw = ow * c.stride + kw - 1;
-  if (ih < 0 || ih >= c.H || iw < 0 || iw >= c.W) return nullptr;
-  const long long img = c.rowmap ? (long long)c.rowmap[(long long)g * c.Bt + b] * c.H * c.W * c.Cin
-                                 : (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
-  return c.x + img + ((long long)ih * c.W + iw) * c.Cin + ci;
-}
-
-// Pointer to element (m, k) of the input-gradient operand dy(m, k): the
-// output position whose tap (kh, kw) reads input position m.
-__device__ __forceinline__ const float* dgrad_addr(const ConvArgs& c, int g, int m,
-                                                   int k) {
-  const int HW = c.H * c.W;
-  const int b = m / HW, p = m - b * HW;
-  const int h = p / c.W, w = p - h * c.W;
-  const int tap = k / c.Cout, co = k - tap * c.Cout;
-  const int kh = tap / 3, kw = tap - kh * 3;
-  const int th = h + 1 - kh, tw = w + 1 - kw;
-  if (th < 0 || tw < 0 || th % c.stride || tw % c.stride) return nullptr;
-  const int oh = th / c.stride, ow = tw / c.stride;
-  if (oh >= c.Ho || ow >= c.Wo) return nullptr;
-  return c.dy + ((long long)g * c.Bt + b) * c.Ho * c.Wo * c.Cout +
-         ((long long)oh * c.Wo + ow) * c.Cout + co;
-}
-
-// Four consecutive k of one row: one float4 when they share the tap (the
-// channel count is a multiple of 4), else element by element.
-template <int MODE>
-__device__ __forceinline__ float4 load_row4(const ConvArgs& c, int g, int m, int k,
-                                            int kmax, bool vec) {
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (vec && k + 3 < kmax) {
-    const float* p = MODE == CONV_DGRAD ? dgrad_addr(c, g, m, k) : fwd_addr(c, g, m, k);
-    if (p) v = *(const float4*)p;
-    return v;
-  }
-  float t[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    if (k + e >= kmax) break;
-    const float* p = MODE == CONV_DGRAD ? dgrad_addr(c, g, m, k + e)
-                                        : fwd_addr(c, g, m, k + e);
-    if (p) t[e] = *p;
-  }
-  return make_float4(t[0], t[1], t[2], t[3]);
-}
-
-// 64 x 64 output tile, 4 waves of 32 x 32 (v_mfma_f32_32x32x2f32), BK = 16,
-// double-buffered LDS. Forward / input gradient: rows = spatial positions,
-// columns = output channels (masked to the true count). Weight gradient:
-// rows = (kh, kw, ci), columns = output channels, reduction over a chunk of
-// spatial positions.
-template <int MODE>
-__global__ __launch_bounds__(kT) void k_conv_gemm(ConvArgs c, int vec) {
-  constexpr int BM = 64, BN = 64, BK = 16;
-  constexpr bool AT = MODE == CONV_WGRAD;
-  constexpr int PA = AT ? BM + 4 : BM + 2, PB = BN + 4;
-  __shared__ __attribute__((aligned(16))) float As[2][BK][PA];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BK][PB];
-
-  // GEMM shape of this mode
-  const int Mg = MODE == CONV_FWD ? c.Bt * c.Ho * c.Wo
-               : MODE == CONV_DGRAD ? c.Bt * c.H * c.W : 9 * c.Cin;
-  const int Ng = MODE == CONV_DGRAD ? c.Cin : c.Cout;
-  const int Kg = MODE == CONV_FWD ? 9 * c.Cin
-               : MODE == CONV_DGRAD ? 9 * c.Cout : c.Bt * c.Ho * c.Wo;
-  const int tm = (Mg + BM - 1) / BM, tn = (Ng + BN - 1) / BN;
-  int l = blockIdx.x;
-  const int n0 = (l % tn) * BN;
-  l /= tn;
-  const int m0 = (l % tm) * BM;
-  l /= tm;
-  const int s = AT ? l % c.splits : 0;
-  const int g = AT ? l / c.splits : l;
-  const int kbeg = AT ? s * c.mchunk : 0;
-  const int kend = AT ? min(Kg, kbeg + c.mchunk) : Kg;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
-  const int lk = lane >> 5, lr = lane & 31;
-  const float* Wg = c.Wk + (long long)g * c.sW;
-
-  float4 ra, rb;
-  auto gload = [&](int k0) {
-    // A: one float4 per thread
-    if constexpr (!AT) {  // rows m (BM of them), 4 float4 of k per row
-      const int r = tid >> 2, kq = k0 + (tid & 3) * 4, m = m0 + r;
-      ra = m < Mg ? load_row4<MODE>(c, g, m, kq, kend, vec) : make_float4(0.f, 0.f, 0.f, 0.f);
-    } else {              // rows k = spatial m, columns i = (kh, kw, ci)
-      const int r = tid >> 4, i0 = m0 + (tid & 15) * 4, kr = k0 + r;
-      ra = kr < kend ? load_row4<CONV_FWD>(c, g, kr, i0, Mg, vec) : make_float4(0.f, 0.f, 0.f, 0.f);
-      // load_row4's bound is on the column here (i < 9*Cin)
-    }
-    // B: [K][N] row-major, 16 rows x 64 columns, one float4 per thread
-    {
-      const int r = tid >> 4, cq = n0 + (tid & 15) * 4, kr = k0 + r;
-      rb = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (kr < kend) {
-        const float* row;
-        if constexpr (AT)
-          row = c.dy + ((long long)g * c.Bt * c.Ho * c.Wo + kr) * c.Cout;
-        else
-          row = Wg + (long long)kr * Ng;
-        float t[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) t[e] = cq + e < Ng ? row[cq + e] : 0.f;
-        rb = make_float4(t[0], t[1], t[2], t[3]);
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-    if constexpr (!AT) {
-      const int r = tid >> 2, kq = (tid & 3) * 4;
-      As[buf][kq + 0][r] = ra.x;
-      As[buf][kq + 1][r] = ra.y;
-      As[buf][kq + 2][r] = ra.z;
-      As[buf][kq + 3][r] = ra.w;
-    } else {
-      *(float4*)&As[buf][tid >> 4][(tid & 15) * 4] = ra;
-    }
-    *(float4*)&Bs[buf][tid >> 4][(tid & 15) * 4] = rb;
-  };
-
-  floatx16 acc;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-  const int nk = (kend - kbeg + BK - 1) / BK;
-  if (nk > 0) {
-    gload(kbeg);
-    lstore(0);
-  }
-  __syncthreads();
-  for (int it = 0; it < nk; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nk) gload(kbeg + (it + 1) * BK);
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 2)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[buf][kk + lk][wm0 + lr],
-                                                 Bs[buf][kk + lk][wn0 + lr], acc,
-                                                 0, 0, 0);
-    if (it + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
-  }
-
-  const int n = n0 + wn0 + lr;
-  float* out = AT ? c.out + ((long long)s * c.G + g) * Mg * Ng
-                  : c.out + (long long)g * Mg * Ng;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int m = m0 + wm0 + (v >> 2) * 8 + lk * 4 + (v & 3);
-    if (m < Mg && n < Ng) out[(long long)m * Ng + n] = acc[v];
-  }
-}
-
 // Forward / input-gradient convolution for reduction channel counts that
 // are multiples of 16 (every convolution after the first): the output tile
 // is 256 spatial rows x all BN (= 16, 32 or 64) channels, so no MFMA lane is
@@ -262,7 +101,7 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   const int g = blockIdx.x / tiles, m0 = (blockIdx.x - g * tiles) * BM;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kq = (tid & 3) * 4;  // this thread's 4 channels of the slab
-  const float* Bw = c.Wk + (long long)g * c.sW;  // [9 Cr][BN]
+  const float* Bw = c.Wk + (long long)g * c.sW;  // W [9 Cin][Cout] of replica g
   // P2: this tile's parity class and the slab count of its taps
   const int HWq = c.Ho * c.Wo, cls_rows = c.Bt * HWq;
   const int cls = P2 ? m0 / cls_rows : 0, ph = cls >> 1, pw = cls & 1;
@@ -335,13 +174,30 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       if (!ok) xa4[i] = v4f{0.f, 0.f, 0.f, 0.f};
     }
     const int bq = min(tid, BQ - 1);
-    const int wrow = tap * Cr + (s - ti * (Cr / BK)) * BK;  // slab's first weight row
-    xb = *(const v4f*)(Bw + (long long)(wrow + bq / (BN / 4)) * BN + (bq % (BN / 4)) * 4);
+    const int cbase = (s - ti * (Cr / BK)) * BK;  // slab's first reduction channel
+    if constexpr (MODE == CONV_FWD) {
+      // B[k = (tap, ci)][n = co] = W[(tap, ci)][co]: rows of 16 channels
+      xb = *(const v4f*)(Bw + (long long)(tap * Cr + cbase + bq / (BN / 4)) * BN +
+                         (bq % (BN / 4)) * 4);
+    } else {
+      // B[k = (tap, co)][n = ci] = W[(tap, ci)][co], read from the forward
+      // layout [9 Cin][Cout]: four consecutive co of one ci per thread
+      xb = *(const v4f*)(Bw + (long long)(tap * BN + bq / (BK / 4)) * Cr + cbase +
+                         (bq % (BK / 4)) * 4);
+    }
   };
   auto lstore = [&](int buf, const v4f(&xa4)[RPT], const v4f& xb) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < RPT; ++i) *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] = xa4[i];
-    if (tid < BQ) *(v4f*)&Bs[buf][tid / (BN / 4)][(tid % (BN / 4)) * 4] = xb;
+    if (tid < BQ) {
+      if constexpr (MODE == CONV_FWD) {
+        *(v4f*)&Bs[buf][tid / (BN / 4)][(tid % (BN / 4)) * 4] = xb;
+      } else {
+        const int ci = tid / (BK / 4), co4 = (tid % (BK / 4)) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Bs[buf][co4 + e][ci] = xb[e];
+      }
+    }
   };
   floatx4 acc[4][NBL];
 #pragma unroll
@@ -585,8 +441,8 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_stem(ConvArgs c) {
 // weights go to LDS once and all 9 taps read shifted views of the tile, so
 // each input value is fetched from memory about 1.25 times rather than once
 // per tap. Input gradient: the same convolution applied to dy with the
-// kernel flipped -- tap (kh, kw) uses weight row (2-kh, 2-kw) -- read from
-// the transposed copy Wt[(kh, kw, co)][ci]. Wave w owns output rows
+// kernel flipped -- tap (kh, kw) uses weight row (2-kh, 2-kw) -- and the
+// channels swapped, W[(2-kh, 2-kw, ci)][co] staged as [(kh, kw, co)][ci]. Wave w owns output rows
 // h0 + 2w, h0 + 2w + 1 as four 16 x 16 blocks of v_mfma_f32_16x16x4f32.
 template <int MODE>
 __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
@@ -622,6 +478,9 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   }
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
+    // forward: Ws row (tap, ci) is W row (tap, ci); input gradient: Ws row
+    // (tap, co) holds W[(8 - tap, ci)][co] over ci, so this thread reads W
+    // row (8 - tap, ci) and scatters its four co below
     const int q = min((int)threadIdx.x + kT * i, WQ - 1);
     const int row = q >> 2, c4 = (q & 3) * 4;
     const int tap = row / C, r = row - tap * C;
@@ -636,7 +495,15 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
     const int q = (int)threadIdx.x + kT * i;
-    if (q < WQ) *(v4f*)&Ws[(q >> 2) * CP + (q & 3) * 4] = wv[i];
+    if (q < WQ) {
+      if (MODE == CONV_FWD) {
+        *(v4f*)&Ws[(q >> 2) * CP + (q & 3) * 4] = wv[i];
+      } else {
+        const int row = q >> 2, tap = row / C, ci = row - tap * C, c4 = (q & 3) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Ws[(tap * C + c4 + e) * CP + ci] = wv[i][e];
+      }
+    }
   }
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -946,27 +813,17 @@ __global__ void k_conv_wupdate(const float* part, int G, int n, float* W, float*
   }
 }
 
-// Wt[g][(kh, kw, co)][ci] = W[g][(kh, kw, ci)][co]: the weight of the input
-// gradient (channels swapped per tap).
-__global__ void k_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
-                          float* Wt) {
-  const int n = 9 * Cin * Cout;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x;
-       i < (long long)G * n; i += (long long)gridDim.x * blockDim.x) {
-    const int g = (int)(i / n), r = (int)(i % n);
-    const int tap = r / (Cout * Cin), rem = r % (Cout * Cin);
-    const int co = rem / Cin, ci = rem % Cin;
-    Wt[i] = W[(long long)g * sP + ((long long)tap * Cin + ci) * Cout + co];
-  }
-}
-
 // ------------------------------------------------------------ batch norm
 // Partial sums of one row chunk per workgroup, fp64: for the forward pass
 // sum(y) and sum(y^2); for the backward pass sum(dz) and sum(dz * xhat),
 // where dz = upstream gradient masked by the ReLU derivative -- `maskv > 0`
 // when given, else bn_z(gamma, y, mu, inv, beta) > 0 -- and
-// xhat = (y - mu) * inv. Channel count C divides 256.
-constexpr int kChunkRows = 1024;
+// xhat = (y - mu) * inv. Channel count C divides 256. Rows per chunk: 1024
+// for the largest layers, fewer for smaller ones so that every layer's
+// launch has at least 32 chunks per replica to spread over the chip.
+__host__ __device__ __forceinline__ int bn_chunk_rows(int R) {
+  return R >= (1 << 17) ? 1024 : R >= (1 << 15) ? 512 : 256;
+}
 
 // The shifted, scaled BN output z = gamma * (y - mu) * inv + beta in one fixed
 // rounding order: the forward pass takes relu(z) (+ the shortcut) with it, and
@@ -979,64 +836,6 @@ __device__ __forceinline__ float bn_z(float gm, float y, float m, float iv, floa
 // coef[f * G * C + g * C + c]: gamma * inv, dbeta / R, dgamma / R, and gamma,
 // beta as they were before this step's update.
 
-__global__ __launch_bounds__(kT) void k_bn_partial(const float* y, int R, int C,
-                                                   const float* gup, const float* maskv,
-                                                   const float* mu, const float* inv,
-                                                   const float* gamma, const float* beta,
-                                                   long long sP, double* part, int nchunk) {
-  __shared__ double red[2][kT];
-  const int g = blockIdx.y, ch = blockIdx.x;
-  const int c = threadIdx.x % C, lane_r = threadIdx.x / C, rstep = kT / C;
-  const long long base = (long long)g * R * C;
-  const int r0 = ch * kChunkRows, r1 = min(R, r0 + kChunkRows);
-  const bool bwd = gup != nullptr;
-  const float m_c = bwd ? mu[g * C + c] : 0.f, i_c = bwd ? inv[g * C + c] : 0.f;
-  const bool zmask = bwd && maskv == nullptr;
-  const float g_c = zmask ? gamma[(long long)g * sP + c] : 0.f;
-  const float b_c = zmask ? beta[(long long)g * sP + c] : 0.f;
-  double s0 = 0.0, s1 = 0.0;
-  for (int rb = r0 + lane_r; rb < r1; rb += 4 * rstep) {
-    float yv[4], gv[4], mv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = rb + u * rstep;
-      const long long o = base + (long long)r * C + c;
-      yv[u] = r < r1 ? y[o] : 0.f;
-      gv[u] = (bwd && r < r1) ? gup[o] : 0.f;
-      mv[u] = (maskv && r < r1) ? maskv[o] : 1.f;
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (rb + u * rstep >= r1) continue;
-      if (!bwd) {
-        s0 += (double)yv[u];
-        s1 += (double)yv[u] * (double)yv[u];
-      } else {
-        const bool on = zmask ? bn_z(g_c, yv[u], m_c, i_c, b_c) > 0.f : mv[u] > 0.f;
-        const float dz = on ? gv[u] : 0.f;
-        const float xh = (yv[u] - m_c) * i_c;
-        s0 += (double)dz;
-        s1 += (double)dz * (double)xh;
-      }
-    }
-  }
-  red[0][threadIdx.x] = s0;
-  red[1][threadIdx.x] = s1;
-  __syncthreads();
-  for (int w = kT / 2; w >= C; w >>= 1) {
-    if ((int)threadIdx.x < w) {
-      red[0][threadIdx.x] += red[0][threadIdx.x + w];
-      red[1][threadIdx.x] += red[1][threadIdx.x + w];
-    }
-    __syncthreads();
-  }
-  if ((int)threadIdx.x < C) {
-    double* p = part + (((long long)g * nchunk + ch) * C + threadIdx.x) * 2;
-    p[0] = red[0][threadIdx.x];
-    p[1] = red[1][threadIdx.x];
-  }
-}
-
 // Running statistics of a BN layer after a training batch of R values per
 // channel: exponential averages (factor kBnRunMomentum) of the batch mean and
 // of the unbiased variance var R / (R - 1), in fp64 and stored as fp32.
@@ -1048,61 +847,16 @@ __device__ __forceinline__ void bn_running(float* rm, float* rv, long long o, do
   rv[o] = (float)((1.0 - a) * (double)rv[o] + a * (var * ((double)R / (double)(R - 1))));
 }
 
-// Forward: mu, inv = 1/sqrt(var + eps) from the partials (chunks in order).
+// Finalisation of one BN layer, one workgroup per replica: lane q of channel
+// c adds the chunk partials q, q + L, q + 2L, ... (L = 256 / C lanes,
+// ascending), then the lanes are added in a fixed tree, and thread c < C
+// finalises channel c.
+// Forward: mu, inv = 1/sqrt(var + eps) (and the running statistics).
 // Backward: the input-gradient coefficients and the update of gamma, beta:
 //   dbeta = sum dz, dgamma = sum dz*xhat,
 //   dy = gamma*inv*(dz - dbeta/R - xhat*dgamma/R)  -> coef = (gamma*inv,
 //   dbeta/R, dgamma/R, gamma, beta); then gamma, beta take a momentum-SGD step
 //   (no decay).
-__global__ void k_bn_finalize(const double* part, int nchunk, int G, int C, int R,
-                              float* mu, float* inv, float* coef, float* gamma,
-                              float* beta, float* ug, float* ub, long long sP,
-                              float lr, float mom, int nesterov, float eps, float* rm,
-                              float* rv, long long sRS) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= G * C) return;
-  const int g = i / C, c = i % C;
-  double s0 = 0.0, s1 = 0.0;
-  for (int ch = 0; ch < nchunk; ++ch) {
-    const double* p = part + (((long long)g * nchunk + ch) * C + c) * 2;
-    s0 += p[0];
-    s1 += p[1];
-  }
-  if (coef == nullptr) {  // forward statistics
-    const double m = s0 / R;
-    double var = s1 / R - m * m;
-    if (var < 0.0) var = 0.0;
-    mu[i] = (float)m;
-    inv[i] = (float)(1.0 / sqrt(var + (double)eps));
-    if (rm) bn_running(rm, rv, (long long)g * sRS + c, m, var, R);
-    return;
-  }
-  const long long o = (long long)g * sP + c;
-  float gm = gamma[o], bt = beta[o];
-  const int GC = G * C;
-  coef[i] = gm * inv[i];
-  coef[GC + i] = (float)(s0 / R);
-  coef[2 * GC + i] = (float)(s1 / R);
-  coef[3 * GC + i] = gm;
-  coef[4 * GC + i] = bt;
-  float u = ug[o];
-  const float dgm = (float)s1;
-  u = __builtin_fmaf(mom, u, dgm);
-  float d = step_dir(u, dgm, mom, nesterov);
-  gamma[o] = __builtin_fmaf(-lr, d, gm);
-  ug[o] = u;
-  u = ub[o];
-  const float dbt = (float)s0;
-  u = __builtin_fmaf(mom, u, dbt);
-  d = step_dir(u, dbt, mom, nesterov);
-  beta[o] = __builtin_fmaf(-lr, d, bt);
-  ub[o] = u;
-}
-
-// k_bn_finalize with the chunk sums spread over a workgroup per replica:
-// lane q of channel c adds chunks q, q + L, q + 2L, ... (L = 256 / C lanes,
-// ascending), then the lanes are added in a fixed tree; thread c < C then
-// finalises as k_bn_finalize does.
 __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
     const double* part, int nchunk, int C, int R, float* mu, float* inv, float* coef,
     float* gamma, float* beta, float* ug, float* ub, long long sP, float lr, float mom,
@@ -1162,70 +916,14 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
   ub[o] = u;
 }
 
-// z = gamma*(y - mu)*inv + beta; then one of
-//   mode 0: out = relu(z)
-//   mode 1: out = relu(z + x_in)               (identity shortcut)
-//   mode 2: out = relu(z + shortcutA(x_in))    (stride-2 option-A shortcut)
-__global__ void k_bn_apply(const float* y, int R, int C, const float* mu,
-                           const float* inv, const float* gamma, const float* beta,
-                           long long sP, int G, int mode, const float* xin,
-                           int Ho, int Wo, int Cin, float* out) {
-  const long long total = (long long)G * R * C;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(i % C);
-    const long long r = i / C;
-    const int g = (int)(r / R);
-    const float z = bn_z(gamma[(long long)g * sP + c], y[i], mu[g * C + c], inv[g * C + c],
-                         beta[(long long)g * sP + c]);
-    float v = z;
-    if (mode == 1) {
-      v += xin[i];
-    } else if (mode == 2) {
-      if (c < Cin) {
-        const long long rr = r - (long long)g * R;   // (b, oh, ow) in replica g
-        const int HWo = Ho * Wo;
-        const int b = (int)(rr / HWo), p = (int)(rr % HWo);
-        const int oh = p / Wo, ow = p % Wo;
-        const int H = 2 * Ho, W = 2 * Wo;
-        v += xin[(((long long)g * (R / HWo) + b) * H * W +
-                  (long long)(2 * oh) * W + 2 * ow) * Cin + c];
-      }
-    }
-    out[i] = v > 0.f ? v : 0.f;
-  }
-}
-
-// dy = coef0 * (dz - coef1 - xhat * coef2) with dz = gup masked by maskv > 0
-// (without maskv: by bn_z > 0 from the pre-update gamma, beta in coef) and
-// xhat = (y - mu) * inv.
-__global__ void k_bn_bwd_apply(const float* y, const float* gup, const float* maskv,
-                               int R, int C, int G, const float* mu, const float* inv,
-                               const float* coef, float* dy) {
-  const long long total = (long long)G * R * C;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(i % C);
-    const int g = (int)(i / ((long long)R * C));
-    const int gc = g * C + c;
-    const long long GC = (long long)G * C;
-    const float* cf = coef + gc;
-    const bool on = maskv ? maskv[i] > 0.f
-                          : bn_z(cf[3 * GC], y[i], mu[gc], inv[gc], cf[4 * GC]) > 0.f;
-    const float dz = on ? gup[i] : 0.f;
-    const float xh = (y[i] - mu[gc]) * inv[gc];
-    dy[i] = cf[0] * (dz - cf[GC] - xh * cf[2 * GC]);
-  }
-}
-
 // ---- float4 forms of the BN passes (channel count C a power of two >= 16):
 // the replica is the grid's y coordinate and a thread owns 4 consecutive
 // channels of one row, so the channel is a mask of the index and no 64-bit
 // division is left in the inner work.
 
-// Partial sums as k_bn_partial (same chunks, same fp64 sums per channel;
-// rows of a chunk interleaved over the 1024 / C row lanes of a workgroup,
-// then added in a fixed tree).
+// Partial sums of one row chunk per workgroup, 4 channels per thread: rows
+// of a chunk interleaved over the 1024 / C row lanes of a workgroup, fp64
+// sums per channel, then added in a fixed tree.
 __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C,
                                                     const float* gup, const float* maskv,
                                                     const float* mu, const float* inv,
@@ -1237,7 +935,8 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
   const int cq = C / 4;  // threads per row
   const int c0 = (threadIdx.x % cq) * 4, lane_r = threadIdx.x / cq, rstep = kT / cq;
   const long long base = (long long)g * R * C;
-  const int r0 = ch * kChunkRows, r1 = min(R, r0 + kChunkRows);
+  const int cr = bn_chunk_rows(R);
+  const int r0 = ch * cr, r1 = min(R, r0 + cr);
   const bool bwd = gup != nullptr;
   const bool zmask = bwd && maskv == nullptr;
   float m_c[4], i_c[4], g_c[4], b_c[4];
@@ -1306,9 +1005,12 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
   }
 }
 
-// k_bn_apply, 4 channels per thread; mu, inv (and gamma, beta when PV) read
-// as float4.
-template <bool PV>
+// BN output z = gamma*(y - mu)*inv + beta, 4 channels per thread (mu, inv,
+// gamma, beta read as float4); then one of
+//   mode 0: out = relu(z)
+//   mode 1: out = relu(z + x_in)               (identity shortcut)
+//   mode 2: out = relu(z + shortcutA(x_in))    (stride-2 option-A shortcut:
+//           every second pixel, the first Cin channels)
 __global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, int cshift,
                                                   const float* mu, const float* inv,
                                                   const float* gamma, const float* beta,
@@ -1331,17 +1033,8 @@ __global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, 
                               2 * ow) * Cin + c0);
   }
   const v4f m4 = *(const v4f*)(mu + g * C + c0), i4 = *(const v4f*)(inv + g * C + c0);
-  v4f g4, b4;
-  if constexpr (PV) {
-    g4 = *(const v4f*)(gamma + (long long)g * sP + c0);
-    b4 = *(const v4f*)(beta + (long long)g * sP + c0);
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      g4[e] = gamma[(long long)g * sP + c0 + e];
-      b4[e] = beta[(long long)g * sP + c0 + e];
-    }
-  }
+  const v4f g4 = *(const v4f*)(gamma + (long long)g * sP + c0);
+  const v4f b4 = *(const v4f*)(beta + (long long)g * sP + c0);
   v4f res;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -1415,31 +1108,6 @@ __global__ __launch_bounds__(kT) void k_shortcut_grad4(float* dx, const float* d
   *(v4f*)(dx + oi) = d;
 }
 
-// Gradient reaching a block's input: dx (from the first convolution of the
-// block) plus the shortcut's share of g = dh_out masked by h_out > 0:
-// identity (mode 1) or option A (mode 2: even pixels, first Cin channels).
-__global__ void k_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
-                                int G, int Bt, int H, int W, int Cin, int Cout,
-                                int mode) {
-  const long long total = (long long)G * Bt * H * W * Cin;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    if (mode == 1) {
-      dx[i] += h_out[i] > 0.f ? dh_out[i] : 0.f;
-      continue;
-    }
-    const int ci = (int)(i % Cin);
-    const long long pix = i / Cin;          // (g, b, h, w)
-    const int w = (int)(pix % W);
-    const int h = (int)((pix / W) % H);
-    if ((h & 1) || (w & 1)) continue;
-    const long long gb = pix / ((long long)H * W);
-    const int Ho = H / 2, Wo = W / 2;
-    const long long o = ((gb * Ho + h / 2) * Wo + w / 2) * Cout + ci;
-    dx[i] += h_out[o] > 0.f ? dh_out[o] : 0.f;
-  }
-}
-
 // Global average pool [G*Bt][S][C] -> [G*Bt][C] (sum in ascending position).
 __global__ void k_gap(const float* h, int rows, int S, int C, float* feat) {
   const long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x;
@@ -1503,10 +1171,13 @@ bool conv_fwd_stats(const ConvGeom& q) {
   return rows_shape(q, CONV_FWD) && ((long long)q.Bt * q.Ho * q.Wo) % 256 == 0;
 }
 
+// Splits of a weight gradient over the batch: a power of two that divides
+// the batch (the stem's kernel takes whole images per split), at most 64,
+// with at least 1024 positions per split.
 int conv_wgrad_splits(int Bt, int Ho, int Wo) {
   const int rows = Bt * Ho * Wo;
   int s = 1;
-  while (s < 64 && rows / (2 * s) >= 1024) s *= 2;
+  while (s < 64 && rows / (2 * s) >= 1024 && Bt % (2 * s) == 0) s *= 2;
   return s;
 }
 
@@ -1532,9 +1203,6 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   const int Mg = mode == CONV_FWD ? q.Bt * q.Ho * q.Wo
                : mode == CONV_DGRAD ? q.Bt * q.H * q.W : 9 * q.Cin;
   const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
-  const long long tiles = (long long)((Mg + 63) / 64) * ((Ng + 63) / 64);
-  const int vec = (mode == CONV_DGRAD ? q.Cout : q.Cin) % 4 == 0 &&
-                  ((uintptr_t)q.x & 15) == 0 && ((uintptr_t)q.dy & 15) == 0;
   if (mode == CONV_WGRAD) {
     c.splits = conv_wgrad_splits(q.Bt, q.Ho, q.Wo);
     const int rows = q.Bt * q.Ho * q.Wo;
@@ -1551,7 +1219,7 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
                          st, c);
       return hipGetLastError();
     }
-    if (stem_shape(q) && rows % (c.splits * kStemSide * kStemSide) == 0) {
+    if (stem_shape(q)) {
       c.mchunk = rows / c.splits;  // whole images per split
       hipLaunchKernelGGL(k_conv_wgrad_stem, dim3((unsigned)(q.G * c.splits)), dim3(kT), 0,
                          st, c);
@@ -1573,9 +1241,7 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
       LSGD_WG(64, 64)
 #undef LSGD_WG
     }
-    c.mchunk = ((rows + c.splits - 1) / c.splits + 15) / 16 * 16;
-    hipLaunchKernelGGL(k_conv_gemm<CONV_WGRAD>, dim3(tiles * c.splits * q.G), dim3(kT),
-                       0, st, c, vec);
+    return hipErrorInvalidValue;  // no weight-gradient kernel for this shape
   } else {
     const bool rows = rows_shape(q, mode), halo = halo_shape(q, mode);
     if (mode == CONV_FWD && stem_shape(q)) {
@@ -1615,10 +1281,8 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
         else LSGD_ROWS(CONV_DGRAD, 64);
       }
 #undef LSGD_ROWS
-    } else if (mode == CONV_FWD) {
-      hipLaunchKernelGGL(k_conv_gemm<CONV_FWD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
     } else {
-      hipLaunchKernelGGL(k_conv_gemm<CONV_DGRAD>, dim3(tiles * q.G), dim3(kT), 0, st, c, vec);
+      return hipErrorInvalidValue;  // no kernel for this shape
     }
   }
   return hipGetLastError();
@@ -1647,13 +1311,6 @@ hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, floa
   return hipGetLastError();
 }
 
-hipError_t launch_conv_wt(const float* W, long long sP, int G, int Cin, int Cout,
-                          float* Wt, hipStream_t st) {
-  hipLaunchKernelGGL(k_conv_wt, dim3(blocks_for((long long)G * 9 * Cin * Cout)), dim3(kT),
-                     0, st, W, sP, G, Cin, Cout, Wt);
-  return hipGetLastError();
-}
-
 // Channel counts the float4 BN forms take: powers of two from 16, aligned.
 int bn_vec_shift(int C) {
   if (C < 16 || (C & (C - 1))) return -1;
@@ -1663,40 +1320,36 @@ int bn_vec_shift(int C) {
 }
 bool al16p(const void* p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
 
-int bn_chunks(int R) { return (R + kChunkRows - 1) / kChunkRows; }
+int bn_chunks(int R) { return (R + bn_chunk_rows(R) - 1) / bn_chunk_rows(R); }
+
+// The BN kernels take 4 channels per thread: C a power of two >= 16 (and
+// <= 256), 16-byte aligned tensors, fewer than 2^31 values per replica and
+// at most 65535 replicas (the ResNet-20 plan meets all of these; anything
+// else is refused rather than run by a slower form).
+static bool bn_shape_ok(int G, int R, int C) {
+  return bn_vec_shift(C) >= 0 && C <= kT && (long long)R * C < (1LL << 31) && G <= 65535;
+}
 
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
                            float* mu, float* inv, float* rm, float* rv, long long sRS,
                            hipStream_t st) {
+  if (!bn_shape_ok(G, R, C) || !al16p(y)) return hipErrorInvalidValue;
   const int nch = bn_chunks(R);
-  if (bn_vec_shift(C) >= 0 && al16p(y) && (long long)R * C < (1LL << 31) && G <= 65535)
-    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
-                       nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, part, nch);
-  else
-    hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
-                       nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, part, nch);
-  if (bn_vec_shift(C) >= 0 && C <= kT)
-    hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R, mu,
-                       inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
-                       1e-5f, rm, rv, sRS);
-  else
-    hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
-                       nch, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
-                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f, rm, rv, sRS);
+  hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
+                     nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, part, nch);
+  hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R, mu,
+                     inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
+                     1e-5f, rm, rv, sRS);
   return hipGetLastError();
 }
 
 hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
                                      float* mu, float* inv, float* rm, float* rv,
                                      long long sRS, hipStream_t st) {
-  if (bn_vec_shift(C) >= 0 && C <= kT)
-    hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nchunk, C, R, mu,
-                       inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
-                       1e-5f, rm, rv, sRS);
-  else
-    hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
-                       nchunk, G, C, R, mu, inv, nullptr, nullptr, nullptr, nullptr,
-                       nullptr, 0LL, 0.f, 0.f, 0, 1e-5f, rm, rv, sRS);
+  if (!bn_shape_ok(G, R, C)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nchunk, C, R, mu,
+                     inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
+                     1e-5f, rm, rv, sRS);
   return hipGetLastError();
 }
 
@@ -1704,20 +1357,12 @@ hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
                            int Cin, float* out, hipStream_t st) {
-  const int cs = bn_vec_shift(C);
-  if (cs >= 0 && al16p(y) && al16p(out) && al16p(xin) && al16p(mu) && al16p(inv) &&
-      Cin % 4 == 0 && (long long)R * C < (1LL << 31) && G <= 65535) {
-    const dim3 grid((R * C / 4 + kT - 1) / kT, G);
-    if (sP % 4 == 0 && al16p(gamma) && al16p(beta))
-      hipLaunchKernelGGL(k_bn_apply4<true>, grid, dim3(kT), 0, st, y, R, C, cs, mu, inv,
-                         gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
-    else
-      hipLaunchKernelGGL(k_bn_apply4<false>, grid, dim3(kT), 0, st, y, R, C, cs, mu, inv,
-                         gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL(k_bn_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0, st,
-                     y, R, C, mu, inv, gamma, beta, sP, G, mode, xin, Ho, Wo, Cin, out);
+  if (!bn_shape_ok(G, R, C) || !al16p(y) || !al16p(out) || !al16p(xin) || !al16p(mu) ||
+      !al16p(inv) || !al16p(gamma) || !al16p(beta) || sP % 4 || Cin % 4)
+    return hipErrorInvalidValue;
+  const dim3 grid((R * C / 4 + kT - 1) / kT, G);
+  hipLaunchKernelGGL(k_bn_apply4, grid, dim3(kT), 0, st, y, R, C, bn_vec_shift(C), mu, inv,
+                     gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
   return hipGetLastError();
 }
 
@@ -1726,46 +1371,30 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
                               const float* inv, float* coef, float* gamma, float* beta,
                               float* ug, float* ub, long long sP, float lr, float mom,
                               int nesterov, float* dy, hipStream_t st) {
+  if (!bn_shape_ok(G, R, C) || !al16p(y) || !al16p(gup) || !al16p(maskv) || !al16p(dy) ||
+      !al16p(mu) || !al16p(inv) || !al16p(coef))
+    return hipErrorInvalidValue;
   const int nch = bn_chunks(R);
-  const bool v4 = bn_vec_shift(C) >= 0 && al16p(y) && al16p(gup) && al16p(maskv) &&
-                  al16p(dy) && al16p(mu) && al16p(inv) && al16p(coef) &&
-                  (long long)R * C < (1LL << 31) && G <= 65535;
-  if (v4)
-    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
-                       mu, inv, gamma, beta, sP, part, nch);
-  else
-    hipLaunchKernelGGL(k_bn_partial, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
-                       mu, inv, gamma, beta, sP, part, nch);
-  if (bn_vec_shift(C) >= 0 && C <= kT)
-    hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
-                       (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
-                       nesterov, 1e-5f, nullptr, nullptr, 0LL);
-  else
-    hipLaunchKernelGGL(k_bn_finalize, dim3((G * C + 255) / 256), dim3(256), 0, st, part,
-                       nch, G, C, R, (float*)mu, (float*)inv, coef, gamma, beta, ug, ub,
-                       sP, lr, mom, nesterov, 1e-5f, nullptr, nullptr, 0LL);
-  if (v4)
-    hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
-                       st, y, gup, maskv, R, C, mu, inv, coef, dy);
-  else
-    hipLaunchKernelGGL(k_bn_bwd_apply, dim3(blocks_for((long long)G * R * C)), dim3(kT), 0,
-                       st, y, gup, maskv, R, C, G, mu, inv, coef, dy);
+  hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
+                     mu, inv, gamma, beta, sP, part, nch);
+  hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
+                     (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
+                     nesterov, 1e-5f, nullptr, nullptr, 0LL);
+  hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
+                     st, y, gup, maskv, R, C, mu, inv, coef, dy);
   return hipGetLastError();
 }
 
 hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
                                 int G, int Bt, int H, int W, int Cin, int Cout,
                                 int mode, hipStream_t st) {
-  if (Cin % 4 == 0 && Cout % 4 == 0 && al16p(dx) && al16p(dh_out) && al16p(h_out) &&
-      (long long)Bt * H * W * Cin < (1LL << 31) && G <= 65535 && H % 2 == 0 && W % 2 == 0) {
-    const long long n4 = mode == 1 ? (long long)Bt * H * W * Cin / 4
-                                   : (long long)Bt * (H / 2) * (W / 2) * (Cin / 4);
-    hipLaunchKernelGGL(k_shortcut_grad4, dim3((unsigned)((n4 + kT - 1) / kT), G), dim3(kT),
-                       0, st, dx, dh_out, h_out, Bt, H, W, Cin, Cout, mode);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL(k_shortcut_grad, dim3(blocks_for((long long)G * Bt * H * W * Cin)),
-                     dim3(kT), 0, st, dx, dh_out, h_out, G, Bt, H, W, Cin, Cout, mode);
+  if (Cin % 4 || Cout % 4 || !al16p(dx) || !al16p(dh_out) || !al16p(h_out) ||
+      (long long)Bt * H * W * Cin >= (1LL << 31) || G > 65535 || H % 2 || W % 2)
+    return hipErrorInvalidValue;
+  const long long n4 = mode == 1 ? (long long)Bt * H * W * Cin / 4
+                                 : (long long)Bt * (H / 2) * (W / 2) * (Cin / 4);
+  hipLaunchKernelGGL(k_shortcut_grad4, dim3((unsigned)((n4 + kT - 1) / kT), G), dim3(kT),
+                     0, st, dx, dh_out, h_out, Bt, H, W, Cin, Cout, mode);
   return hipGetLastError();
 }
 

@@ -167,3 +167,14 @@ def test_state_and_failure_calls_fail_cleanly():
     assert lib.lsgd_sync(None) == 1
     assert lib.lsgd_state_bytes(None, None) == 1
     assert lib.lsgd_status_string(6) == b"non-finite loss"
+
+
+def test_resnet_batch_limit():
+    """ResNet-20 batches must stay below 2^17 images per replica (each
+    replica's largest activation then has fewer than 2^31 values)."""
+    from paper_1808_07217_amd import lsgd as L
+    ok = L.make_config((3072, 10), 2, (1 << 17) - 1, 4096, model="resnet20")
+    assert L.param_count(ok) == 269722
+    bad = L.make_config((3072, 10), 2, 1 << 17, 4096, model="resnet20")
+    with pytest.raises(L.LsgdError, match="invalid argument"):
+        L.param_count(bad)

@@ -48,6 +48,29 @@ def test_resnet20_every_step():
     assert e <= 1e-5
 
 
+def test_resnet20_batch_not_a_multiple_of_four():
+    """B_loc = 10 (K = 2, 4096-image subset, three steps, then the average):
+    the paths a batch of 128 never takes -- the stride-2 input gradients of
+    stage 3 through the nine-tap row kernel (10 x 8 x 8 rows are not whole
+    256-row parity-class tiles), BN statistics of stage 3 from a separate
+    pass (its outputs are not whole 256-row chunks), and weight-gradient
+    splits that divide 10. The sampler seed is one where perturbing the
+    oracle's initial weights by 1e-7 moves its replicas by 3.4e-7 over these
+    steps (small batches can put a channel's batch variance near zero)."""
+    base = wk.get("resnet20")
+    w = base.scaled(K=2, N=4096, B_loc=10, sample_seed=0x5EED0015)
+    X, y = wk.dataset(base)
+    X, y = np.ascontiguousarray(X[:4096]), np.ascontiguousarray(y[:4096])
+    w0 = wk.initial_weights(w)
+    print("resnet20 B=10", flush=True)
+    reps, st, worst = _compare(w, X, y, w0, 3, [0, 1], 1e-5, 1e-4)
+    reps.average()
+    st.W = O.average(st.W)
+    e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
+    print(f"resnet20 B=10: worst step error {worst:.3e}, averaged {e:.3e}", flush=True)
+    assert e <= 1e-5
+
+
 def test_resnet20_full_shape_first_steps():
     """Workload 5 at its real shape (K=16, B_loc=128): replicas 0 and 15 over
     the first two local steps."""
@@ -96,3 +119,4 @@ def test_resnet20_round_with_the_newer_schemes(variant):
         assert normwise(got, st.W[0]) <= 1e-5
         u = reps.read_global_momentum().cpu().numpy()
         assert np.max(np.abs(u - st.u_global)) * w.lr <= 1e-5 * scale
+
