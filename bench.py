@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3, help="untimed rounds")
     p.add_argument("--workload", default="resnet20")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--lazy-average", action="store_true",
+                   help="the lazy form of the plain average (the mean written "
+                        "once, read by the next local step; MLP workloads)")
     p.add_argument("--no-kernel-timing", action="store_true")
     p.add_argument("--sweep", action="store_true",
                    help="HBM sweep of the K-way average and the fused update "
@@ -87,6 +90,9 @@ def kernel_cost(tag: str, w) -> tuple:
         return None, None
     if tag == "xent":
         return 0, K * B * d[L] * (4 + e) + K * B * 8
+    if tag == "average" and getattr(w, "lazy_average", False):
+        # the mean written once (and its bf16 copy)
+        return K * P, K * P * 4 + P * 4 + (P * 2 if e == 2 else 0)
     if tag in ("average", "average_blocks"):   # same traffic per launch
         gm = 16 * P if w.global_momentum else 0  # w_sync and u read + written
         return K * P, K * P * 8 + (K * P * 2 if e == 2 else 0) + gm
@@ -467,6 +473,11 @@ def main():
     Xd = torch.from_numpy(np.array(X)).to(dev)
     yd = torch.from_numpy(np.array(y)).to(dev)
     reps = L.Replicas(cfg, Xd, yd, torch.from_numpy(w0).to(dev))
+    if args.lazy_average:
+        reps.set_lazy_average(True)
+        import dataclasses
+        w = dataclasses.replace(w)
+        object.__setattr__(w, "lazy_average", True)
     stream = reps.stream
     hier = w.Kb > 0
     H = w.H * w.Hb            # local steps per (outer) round
@@ -580,6 +591,7 @@ def main():
                    "K": w.K, "B_loc": w.B_loc, "H": H,
                    **({"K_block": w.Kb, "H_block": w.Hb} if hier else {}),
                    "samples_per_step": samples,
+                   **({"average_form": "lazy"} if args.lazy_average else {}),
                    "momentum": w.momentum, "nesterov": w.nesterov,
                    "weight_decay": w.weight_decay,
                    **({"scheme": w.scheme} if w.scheme != "local" else {}),
@@ -633,6 +645,16 @@ def main():
                 mf[t] = round(f * launches / (ms / 1e3) / (PEAK_TFLOPS[w.dtype] * 1e12), 4)
         if mf:
             out["kernel_mfma_frac"] = mf
+        if "average" in rep:   # the synchronisation kernel's own rate
+            n_avg, ms_avg = rep["average"]
+            _, by = kernel_cost("average", w)
+            t_avg = ms_avg / n_avg / 1e3
+            out["average_kernel"] = {
+                "form": "lazy" if getattr(w, "lazy_average", False) else "broadcast",
+                "avg_launch_us": round(t_avg * 1e6, 2),
+                "algorithmic_bytes_per_launch": by,
+                "GB/s": round(by / t_avg / 1e9, 1),
+                "frac_hbm": round(by / t_avg / 1e9 / PEAK_HBM_GBS, 4)}
     reps.close()
 
     if not args.no_cpu_baseline:

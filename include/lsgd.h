@@ -185,6 +185,23 @@ lsgd_status lsgd_local_step(lsgd_ctx* ctx, float lr, float* d_loss);
 lsgd_status lsgd_average(lsgd_ctx* ctx);
 
 /*
+ * The form of the plain average (lsgd_average, and the synchronisation of
+ * lsgd_run_round without global momentum or a sign scheme). enable = 0 (the
+ * default): the mean is written back into all K replicas (K P floats read
+ * and K P written). enable = 1, the lazy form that eq. 2 allows since every
+ * replica holds the same w after it: the mean is written once (P floats,
+ * plus its bf16 copy for LSGD_BF16); the next local step reads that copy as
+ * every replica's weights and writes each replica's stepped model. Results
+ * are bit for bit those of the default form: every call that reads the
+ * replicas (read_params, read_state, block averages, the single-launch
+ * softmax round, write_params of one replica) first writes the pending mean
+ * into them. MLP models under LSGD_SCHEME_LOCAL without global momentum
+ * only, else LSGD_E_UNSUPPORTED; enable outside {0, 1}: LSGD_E_INVALID.
+ * Switching it off writes a pending mean out.
+ */
+lsgd_status lsgd_set_lazy_average(lsgd_ctx* ctx, int32_t enable);
+
+/*
  * The end-of-round synchronisation. With a sign scheme it is the
  * sign-compressed synchronisation of Algorithm 3 or 4 (lr unused; see
  * LSGD_SCHEME_*). With global_momentum == 0 it is lsgd_average (lr unused). Otherwise it is local SGD with global momentum

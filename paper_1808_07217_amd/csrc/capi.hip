@@ -57,6 +57,7 @@ struct Layout {
   size_t Wsync = 0, Ug = 0;  // model at the last sync; global momentum buffer
   size_t E = 0, sign = 0, sign_bytes = 0;  // error memories; sign-sync scratch
   size_t flag = 0;    // int32: set by the loss kernels on a non-finite loss
+  size_t Wbar = 0, Wbarb = 0;  // lazy average: the mean [Ps] fp32 (+ bf16)
   bool head = false;  // top layer through the fused head kernels
   size_t act[LSGD_MAX_LAYERS] = {}, dZ[LSGD_MAX_LAYERS + 1] = {};
   size_t total = 0;
@@ -214,6 +215,9 @@ Layout make_layout(const lsgd_config* c) {
   l.W = take(K * l.Ps * 4);
   l.U = take(K * l.Ps * 4);
   l.flag = take(4);
+  // the synchronised model of a lazy average (and its bf16 copy)
+  l.Wbar = take(l.Ps * 4);
+  if (c->gemm_dtype == LSGD_BF16) l.Wbarb = take(l.Ps * 2);
   if (c->global_momentum != 0.f || c->scheme != LSGD_SCHEME_LOCAL)
     l.Wsync = take(l.Ps * 4);
   if (c->global_momentum != 0.f) l.Ug = take(l.Ps * 4);
@@ -305,6 +309,13 @@ struct lsgd_ctx {
   float* W() const { return (float*)(ws + lay.W); }
   float* U() const { return (float*)(ws + lay.U); }
   int* flag() const { return (int*)(ws + lay.flag); }
+  // Lazy average (MLP, plain scheme): the synchronisation writes the mean
+  // once to Wbar and sets `pending`; the next local step reads the weights
+  // from Wbar (replica stride 0) and writes every replica. Anything else that
+  // reads the replica array first materialises the mean into it.
+  bool lazy = false, pending = false;
+  float* Wbar() const { return (float*)(ws + lay.Wbar); }
+  bf16_t* Wbarb() const { return lay.Wbarb ? (bf16_t*)(ws + lay.Wbarb) : nullptr; }
   // BN running statistics (ResNet), else nullptr
   float* RS() const { return lay.resnet ? (float*)(ws + lay.rp.rs) : nullptr; }
   bool gm() const { return cfg.global_momentum != 0.f; }
@@ -432,6 +443,12 @@ GemmArgs wgrad_args(const lsgd_ctx* c, int l, float lr) {
   a.bias_w = c->W() + ly.offB[l - 1];
   a.bias_u = c->U() + ly.offB[l - 1];
   a.sBiasP = ly.Ps;
+  if (c->pending) {  // step the shared mean of a lazy average
+    a.Wsrc = c->Wbar() + ly.offW[l - 1];
+    a.sWsrc = 0;
+    a.bias_src = c->Wbar() + ly.offB[l - 1];
+    a.sBiasSrc = 0;
+  }
   a.splits = 1;
   return a;
 }
@@ -448,6 +465,11 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
   float* U = c->U();
   bf16_t* Wb = c->Wb();
   const void* X0 = dt ? (const void*)c->Xb() : (const void*)c->X;
+  // where this step reads the weights: the replicas, or the shared mean of
+  // a pending lazy average
+  const float* Wr = c->pending ? c->Wbar() : W;
+  const bf16_t* Wbr = c->pending ? c->Wbarb() : Wb;
+  const long long sWr = c->pending ? 0 : ly.Ps;
 
   // this step's rows: sampled by the step before on the side stream, or now
   if (c->presampled == c->step && c->lay.idx2 != 0)
@@ -477,11 +499,11 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       a.sA = (long long)B * din;
     }
     a.lda = din;
-    a.B = dt ? (const void*)(Wb + ly.offW[l - 1]) : (const void*)(W + ly.offW[l - 1]);
+    a.B = dt ? (const void*)(Wbr + ly.offW[l - 1]) : (const void*)(Wr + ly.offW[l - 1]);
     a.ldb = dout;
-    a.sB = ly.Ps;
-    a.bias = W + ly.offB[l - 1];
-    a.sBias = ly.Ps;
+    a.sB = sWr;
+    a.bias = Wr + ly.offB[l - 1];
+    a.sBias = sWr;
     a.ldc = dout;
     a.sC = (long long)B * dout;
     a.splits = lsgd::gemm_splits(dt, B, dout, din, K, lsgd::EPI_BIAS);
@@ -508,12 +530,16 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     h.sA = (long long)B * w[L - 1];
     h.rowmap = c->idx();
     h.y = c->y;
-    h.W = dt ? (const void*)(Wb + ly.offW[L - 1]) : (const void*)(W + ly.offW[L - 1]);
-    h.sW = ly.Ps;
+    h.W = dt ? (const void*)(Wbr + ly.offW[L - 1]) : (const void*)(Wr + ly.offW[L - 1]);
+    h.sW = sWr;
     h.Wm = W + ly.offW[L - 1];
     h.Um = U + ly.offW[L - 1];
     h.Wb = dt ? Wb + ly.offW[L - 1] : nullptr;
-    h.bias = W + ly.offB[L - 1];
+    h.bias = Wr + ly.offB[L - 1];
+    h.sBias = sWr;
+    h.Wsrc = Wr + ly.offW[L - 1];
+    h.bsrc = Wr + ly.offB[L - 1];
+    h.sSrc = sWr;
     h.bias_w = W + ly.offB[L - 1];
     h.bias_u = U + ly.offB[L - 1];
     h.sP = ly.Ps;
@@ -578,9 +604,9 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
       a.A = c->dZ(l);
       a.lda = dout;
       a.sA = (long long)B * dout;
-      a.B = dt ? (const void*)(Wb + ly.offW[l - 1]) : (const void*)(W + ly.offW[l - 1]);
+      a.B = dt ? (const void*)(Wbr + ly.offW[l - 1]) : (const void*)(Wr + ly.offW[l - 1]);
       a.ldb = dout;
-      a.sB = ly.Ps;
+      a.sB = sWr;
       a.C = c->dZ(l - 1);
       a.ldc = din;
       a.sC = (long long)B * din;
@@ -615,6 +641,7 @@ lsgd_status do_local_step(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_CK(c, hipStreamWaitEvent(s, c->join[1], 0));
   }
   c->step += 1;
+  c->pending = false;  // every replica now holds its own stepped model
   if (presample) c->presampled = c->step;
   return LSGD_OK;
 }
@@ -718,6 +745,10 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   h.Wm = W + r.offFcW;
   h.Um = U + r.offFcW;
   h.bias = W + r.offFcB;
+  h.sBias = Ps;
+  h.Wsrc = W + r.offFcW;
+  h.bsrc = W + r.offFcB;
+  h.sSrc = Ps;
   h.bias_w = W + r.offFcB;
   h.bias_u = U + r.offFcB;
   h.sP = Ps;
@@ -824,7 +855,28 @@ lsgd_status average_running_stats(lsgd_ctx* c, int Kb) {
   return LSGD_OK;
 }
 
+// A pending lazy average written out: every replica (and its bf16 copy)
+// := the mean. Bit for bit what the plain average would have left there.
+lsgd_status materialise(lsgd_ctx* c) {
+  if (!c->pending) return LSGD_OK;
+  LSGD_LAUNCH(c, "average_materialise",
+              lsgd::launch_broadcast(c->Wbar(), c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
+                                     c->lay.Ps, -1, c->stream));
+  c->pending = false;
+  return LSGD_OK;
+}
+
 lsgd_status do_average(lsgd_ctx* c) {
+  if (lsgd_status st = materialise(c)) return st;  // average the replicas as stored
+  if (c->lazy) {
+    // the mean once (and its bf16 copy); the next step reads it for every
+    // replica
+    LSGD_LAUNCH(c, "average",
+                lsgd::launch_average(c->W(), c->Wbarb(), c->cfg.K, c->lay.Ps, c->lay.Ps,
+                                     c->Wbar(), c->stream));
+    c->pending = true;
+    return LSGD_OK;
+  }
   LSGD_LAUNCH(c, "average",
               lsgd::launch_average(c->W(), c->Wb(), c->cfg.K, c->lay.Ps,
                                    c->lay.Ps, nullptr, c->stream));
@@ -853,6 +905,7 @@ lsgd_status do_synchronise(lsgd_ctx* c, float lr) {
 lsgd_status do_average_blocks(lsgd_ctx* c, int Kb) {
   if (Kb == c->cfg.K) return do_average(c);
   if (Kb == 1) return LSGD_OK;  // every block holds one replica
+  if (lsgd_status st = materialise(c)) return st;
   LSGD_LAUNCH(c, "average_blocks",
               lsgd::launch_average_blocks(c->W(), c->Wb(), Kb, c->cfg.K / Kb,
                                           c->lay.Ps, c->lay.Ps, nullptr,
@@ -870,6 +923,7 @@ bool tiny_round_ok(const lsgd_ctx* c, int H) {
 }
 
 lsgd_status do_tiny_round(lsgd_ctx* c, int H, const float* h_lr, float* d_loss) {
+  if (lsgd_status st = materialise(c)) return st;
   const lsgd_config& cf = c->cfg;
   lsgd::TinyArgs a{};
   a.X = c->X;
@@ -1118,6 +1172,11 @@ lsgd_status lsgd_run_hierarchical_round(lsgd_ctx* ctx, int32_t H, int32_t Hb,
 lsgd_status lsgd_read_params(lsgd_ctx* ctx, int32_t replica, float* d_dst) {
   LSGD_USABLE(ctx);
   if (!d_dst || replica < -1 || replica >= ctx->cfg.K) return LSGD_E_INVALID;
+  if (ctx->pending) {  // every replica is the pending mean
+    LSGD_CK(ctx, hipMemcpyAsync(d_dst, ctx->Wbar(), ctx->lay.P * sizeof(float),
+                                hipMemcpyDeviceToDevice, ctx->stream));
+    return LSGD_OK;
+  }
   if (replica >= 0) {
     LSGD_CK(ctx, hipMemcpyAsync(d_dst, ctx->W() + (size_t)replica * ctx->lay.Ps,
                                 ctx->lay.P * sizeof(float),
@@ -1142,6 +1201,10 @@ lsgd_status lsgd_write_params(lsgd_ctx* ctx, int32_t replica,
                               const float* d_src) {
   LSGD_USABLE(ctx);
   if (!d_src || replica < -1 || replica >= ctx->cfg.K) return LSGD_E_INVALID;
+  if (replica >= 0) {  // the other replicas keep the pending mean
+    if (lsgd_status st = materialise(ctx)) return st;
+  }
+  ctx->pending = false;
   LSGD_CK(ctx, lsgd::launch_broadcast(d_src, ctx->W(), ctx->Wb(), ctx->cfg.K,
                                       ctx->lay.P, ctx->lay.Ps, replica,
                                       ctx->stream));
@@ -1207,6 +1270,7 @@ lsgd_status lsgd_state_bytes(const lsgd_config* cfg, size_t* bytes) {
 lsgd_status lsgd_read_state(lsgd_ctx* ctx, void* d_dst) {
   LSGD_USABLE(ctx);
   if (!d_dst || ((uintptr_t)d_dst) % kAlign) return LSGD_E_INVALID;
+  if (lsgd_status st = materialise(ctx)) return st;
   const StatePlan sp = state_plan(ctx->cfg, ctx->lay);
   char* dst = (char*)d_dst;
   lsgd::Words8 h{};
@@ -1282,6 +1346,20 @@ lsgd_status lsgd_write_state(lsgd_ctx* ctx, const void* d_src) {
   LSGD_CK(ctx, lsgd::launch_fill((float*)ctx->flag(), 0.f, 1, s));
   ctx->step = (int64_t)h[5];
   ctx->presampled = -1;
+  ctx->pending = false;
+  return LSGD_OK;
+}
+
+lsgd_status lsgd_set_lazy_average(lsgd_ctx* ctx, int32_t enable) {
+  LSGD_USABLE(ctx);
+  if (enable != 0 && enable != 1) return LSGD_E_INVALID;
+  const lsgd_config& cf = ctx->cfg;
+  if (enable && (ctx->lay.resnet || cf.scheme != LSGD_SCHEME_LOCAL ||
+                 cf.global_momentum != 0.f))
+    return LSGD_E_UNSUPPORTED;
+  if (!enable)
+    if (lsgd_status st = materialise(ctx)) return st;
+  ctx->lazy = enable != 0;
   return LSGD_OK;
 }
 

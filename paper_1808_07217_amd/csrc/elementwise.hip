@@ -184,7 +184,8 @@ __device__ __forceinline__ void store_bf16x4(bf16_t* p, float4 v) {
 // Vectorised average: thread i owns elements 4i .. 4i+3 of every replica.
 // The grid's y index picks a block of K consecutive replicas (hierarchical
 // averaging; a single block is the global average).
-// mean_out != nullptr: write the mean there and leave W untouched.
+// mean_out != nullptr (one block): write the mean there (and its bf16 copy to
+// Wb [n] when given) and leave W untouched.
 template <int KT>
 __global__ void k_average4(float* W, bf16_t* Wb, int K, long long n,
                            long long ld, float* mean_out) {
@@ -203,6 +204,7 @@ __global__ void k_average4(float* W, bf16_t* Wb, int K, long long n,
     const float4 mean = div4(s, (float)K);
     if (mean_out) {
       ((float4*)mean_out)[i] = mean;
+      if (Wb) store_bf16x4(Wb + 4 * i, mean);
       continue;
     }
     for (int k = 0; k < K; ++k) {
@@ -277,6 +279,7 @@ __global__ void k_average1(float* W, bf16_t* Wb, int K, long long n,
     const float mean = tree_sum_rt<float>(W + i, ld, K) / (float)K;
     if (mean_out) {
       mean_out[i] = mean;
+      if (Wb) Wb[i] = f32_to_bf16(mean);
       continue;
     }
     for (int k = 0; k < K; ++k) {

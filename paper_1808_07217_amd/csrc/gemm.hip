@@ -85,7 +85,8 @@ __device__ __forceinline__ void finish(const GemmArgs& a, int g, int m, int n,
                                        float v) {
   const long long o = (long long)g * a.sC + (long long)m * a.ldc + n;
   if constexpr (EPI == EPI_SGD) {
-    float w = a.W[o], u = a.U[o];
+    float w = a.Wsrc ? a.Wsrc[(long long)g * a.sWsrc + (long long)m * a.ldc + n] : a.W[o];
+    float u = a.U[o];
     sgd_step(w, u, v, a);
     a.W[o] = w;
     a.U[o] = u;
@@ -120,7 +121,8 @@ __device__ __forceinline__ void emit(const GemmArgs& a, const Tile& t, int m,
 __device__ __forceinline__ void bias_update(const GemmArgs& a, const Tile& t,
                                             int n, float colsum) {
   const long long o = (long long)t.g * a.sBiasP + n;
-  float w = a.bias_w[o], u = a.bias_u[o];
+  float w = a.bias_src ? a.bias_src[(long long)t.g * a.sBiasSrc + n] : a.bias_w[o];
+  float u = a.bias_u[o];
   sgd_step(w, u, colsum, a);
   a.bias_w[o] = w;
   a.bias_u[o] = u;
@@ -167,11 +169,14 @@ __device__ __forceinline__ void epilogue_fragment(const GemmArgs& a, const Tile&
       if constexpr (EPI == EPI_SGD) {
         float* Wp = a.W + o1;
         float* Up = a.U + o1;
+        const float* Wr = a.Wsrc ? a.Wsrc + (long long)t.g * a.sWsrc +
+                                       (long long)m1 * a.ldc + n
+                                 : Wp;
         float wv[16], uv[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int dr = ((v >> 2) * 8 + (v & 3)) * ldc;
-          wv[v] = ok[v] ? Wp[dr] : 0.f;
+          wv[v] = ok[v] ? Wr[dr] : 0.f;
           uv[v] = ok[v] ? Up[dr] : 0.f;
         }
 #pragma unroll
@@ -240,7 +245,10 @@ struct SgdVec {
       bool ok;
       locate(a, t, half, p, r, c, off, ok);
       if (ok) {
-        wv[p] = *(const float4*)(a.W + off);
+        const float* wr = a.Wsrc ? a.Wsrc + (off - (long long)t.g * a.sC) +
+                                       (long long)t.g * a.sWsrc
+                                 : a.W + off;
+        wv[p] = *(const float4*)wr;
         uv[p] = *(const float4*)(a.U + off);
       }
     }
@@ -1008,9 +1016,10 @@ __global__ __launch_bounds__(kWsThreads) void gemm_f32_sgd_ws(WsArgs w) {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
           const int r = u / 32 + 8 * p, c = (u % 32) * 4;
-          const long long off = (long long)cur.g * a.sC +
-                                (long long)(cur.m0 + r) * a.ldc + cur.n0 + c;
-          wv[p] = *(const float4*)(a.W + off);
+          const long long in = (long long)(cur.m0 + r) * a.ldc + cur.n0 + c;
+          const long long off = (long long)cur.g * a.sC + in;
+          wv[p] = *(const float4*)(a.Wsrc ? a.Wsrc + (long long)cur.g * a.sWsrc + in
+                                          : a.W + off);
           uv[p] = *(const float4*)(a.U + off);
         }
       }
@@ -1033,7 +1042,8 @@ bool ws_eligible(int dtype, const GemmArgs& a) {
          a.lda % 2 == 0 && a.sA % 2 == 0 && al(a.A, pair) &&
          a.ldb % 2 == 0 && a.sB % 2 == 0 && al(a.B, pair) &&
          a.ldc % 4 == 0 && a.sC % 4 == 0 && al(a.W, 15) && al(a.U, 15) &&
-         (a.Wb == nullptr || al(a.Wb, 7));
+         (a.Wb == nullptr || al(a.Wb, 7)) &&
+         (a.Wsrc == nullptr || (al(a.Wsrc, 15) && a.sWsrc % 4 == 0));
 }
 
 // ------------------------------------------------------------------ bf16
@@ -1439,7 +1449,8 @@ hipError_t run(int dtype, GemmArgs a, hipStream_t s) {
   const int vecB = a.ldb % esz == 0 && a.sB % esz == 0 && aligned16(a.B);
   const int vecC = EPI == EPI_SGD && a.ldc % 4 == 0 && a.sC % 4 == 0 &&
                    aligned16(a.W) && aligned16(a.U) &&
-                   (a.Wb == nullptr || ((uintptr_t)a.Wb & 7u) == 0);
+                   (a.Wb == nullptr || ((uintptr_t)a.Wb & 7u) == 0) &&
+                   (a.Wsrc == nullptr || (aligned16(a.Wsrc) && a.sWsrc % 4 == 0));
   if constexpr (!AT && EPI != EPI_SGD) {
     if (dtype == 1 && vecA && vecB && a.M % 64 == 0 && a.N % 64 == 0 &&
         a.kchunk % 64 == 0 && (long long)a.kchunk * a.splits == a.Kd) {

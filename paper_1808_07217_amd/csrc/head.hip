@@ -128,7 +128,7 @@ __global__ __launch_bounds__(256) void k_head_fwd(HeadArgs h) {
       }
     }
   }
-  const float* bias = h.bias + (long long)k * h.sP;
+  const float* bias = h.bias + (long long)k * h.sBias;
   const float invB = 1.0f / (float)h.B;
   float dz[RPW][CMAX];
 #pragma unroll
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void k_head_wgrad(HeadArgs h) {
       const int c = grp + 4 * j;
       if (c >= C) continue;
       const long long o = (long long)k * h.sP + (long long)d * C + c;
-      float w = h.Wm[o], u = h.Um[o];
+      float w = h.Wsrc[(long long)k * h.sSrc + (long long)d * C + c], u = h.Um[o];
       sgd_step(w, u, acc[j], h);
       h.Wm[o] = w;
       h.Um[o] = u;
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256) void k_head_wgrad(HeadArgs h) {
   if (!first) return;  // uniform over the workgroup
   if ((int)threadIdx.x < C) {
     const long long o = (long long)k * h.sP + threadIdx.x;
-    float w = h.bias_w[o], u = h.bias_u[o];
+    float w = h.bsrc[(long long)k * h.sSrc + threadIdx.x], u = h.bias_u[o];
     sgd_step(w, u, bsum, h);
     h.bias_w[o] = w;
     h.bias_u[o] = u;
@@ -345,7 +345,7 @@ __global__ __launch_bounds__(256) void k_head_wgrad_vec(HeadArgs h) {
 #pragma unroll
   for (int q = 0; q < WPT; ++q) {
     const int e = min((int)threadIdx.x + 256 * q, 64 * C - 1);
-    wv[q] = h.Wm[wbase + e];
+    wv[q] = h.Wsrc[(long long)k * h.sSrc + (long long)dbase * C + e];
     uv[q] = h.Um[wbase + e];
   }
   const float rl = first ? h.rowloss[(long long)k * B + min((int)threadIdx.x, B - 1)] : 0.f;
@@ -393,7 +393,7 @@ __global__ __launch_bounds__(256) void k_head_wgrad_vec(HeadArgs h) {
     float bsum = 0.f;
     for (int b = 0; b < B; ++b) bsum += dzs[b * C + threadIdx.x];
     const long long o = (long long)k * h.sP + threadIdx.x;
-    float w = h.bias_w[o], u = h.bias_u[o];
+    float w = h.bsrc[(long long)k * h.sSrc + threadIdx.x], u = h.bias_u[o];
     sgd_step(w, u, bsum, h);
     h.bias_w[o] = w;
     h.bias_u[o] = u;
@@ -473,7 +473,7 @@ __global__ __launch_bounds__(256) void k_head_fwd_vec(HeadArgs h) {
       }
       z[q][c] = acc;
     }
-  const float* bias = h.bias + (long long)k * h.sP;
+  const float* bias = h.bias + (long long)k * h.sBias;
   const float invB = 1.0f / (float)h.B;
   float dz[RPW][C];
 #pragma unroll
@@ -616,7 +616,7 @@ __global__ __launch_bounds__(256) void k_head_fwd_bf16(HeadArgs h) {
       }
     __builtin_amdgcn_sched_barrier(0);  // one slice of W_L in registers at a time
   }
-  const float* bias = h.bias + (long long)k * h.sP;
+  const float* bias = h.bias + (long long)k * h.sBias;
   const float invB = 1.0f / (float)h.B;
   float dz[RPW][C];
 #pragma unroll

@@ -61,6 +61,13 @@ struct GemmArgs {
   float* W;
   float* U;
   bf16_t* Wb;
+  // when set, the update reads the weights (and the bias) it steps from here
+  // instead of W (bias_w): the synchronised model of a pending lazy average,
+  // same layout, replica stride sWsrc (sBiasSrc); it still writes W, U, Wb
+  const float* Wsrc;
+  long long sWsrc;
+  const float* bias_src;
+  long long sBiasSrc;
   float lr, mom, wd;
   int nesterov;
   // EPI_SGD: when bias_w != nullptr the kernel also forms the bias gradient
@@ -106,7 +113,7 @@ struct HeadArgs {
   float* Wm;                 // W_L master, momentum, bf16 copy (update)
   float* Um;
   bf16_t* Wb;
-  float* bias;               // b_L (read by the forward pass)
+  const float* bias;         // b_L (read by the forward pass)
   float* bias_w;             // b_L and its momentum (update)
   float* bias_u;
   long long sP;              // replica stride of the parameter buffers
@@ -114,6 +121,13 @@ struct HeadArgs {
   void* dZprev;              // [K][B][D] masked input gradient, or nullptr
   float* rowloss;            // [K][B]
   float* loss;               // [K] or nullptr
+  // the forward reads b_L at bias + k sBias; the update reads the W_L and b_L
+  // it steps at Wsrc / bsrc + k sSrc (the replica's own, or the shared model
+  // of a pending lazy average) and writes Wm / bias_w
+  long long sBias;
+  const float* Wsrc;
+  const float* bsrc;
+  long long sSrc;
   int* nonfinite;            // set to 1 when a replica's mean loss is not
                              //   finite (never cleared here), or nullptr
   float lr, mom, wd;
@@ -193,7 +207,9 @@ hipError_t launch_xent(const float* Z, const int32_t* y, const int32_t* idx,
 hipError_t launch_sgd_update(float* W, float* U, const float* G, long long n,
                              float lr, float mom, float wd, int nesterov,
                              hipStream_t s);
-// K-way average of the first n elements of K rows spaced ld apart.
+// K-way average of the first n elements of K rows spaced ld apart: every
+// row (and its bf16 copy in Wb) := the mean; with mean_out, only the mean is
+// written, to mean_out [n] (and its bf16 copy to Wb [n] when given).
 hipError_t launch_average(float* W, bf16_t* Wb, int K, long long n,
                           long long ld, float* mean_out, hipStream_t s);
 // The K-way average with global momentum: mean of the K rows, then

@@ -81,6 +81,7 @@ _SIGS = {
     "lsgd_sample_indices": [_P, _c.c_int64, _P],
     "lsgd_sync": [_P],
     "lsgd_state_bytes": [_c.POINTER(Config), _c.POINTER(_c.c_size_t)],
+    "lsgd_set_lazy_average": [_P, _c.c_int32],
     "lsgd_read_state": [_P, _P],
     "lsgd_write_state": [_P, _P],
     "lsgd_destroy": [_P],
@@ -252,6 +253,10 @@ class Replicas:
 
     def average(self):
         _check(_lib.lsgd_average(self._ctx), self._ctx)
+
+    def set_lazy_average(self, enable: bool = True):
+        """The lazy form of the plain average (lsgd_set_lazy_average)."""
+        _check(_lib.lsgd_set_lazy_average(self._ctx, int(bool(enable))), self._ctx)
 
     def run_round(self, lrs: Sequence[float], loss: Optional[torch.Tensor] = None):
         H = len(lrs)
