@@ -16,6 +16,8 @@
 //    order, so the statistics are deterministic;
 //  * ReLU, the option-A shortcut (every second pixel, channels zero-padded),
 //    global average pooling.
+#include <atomic>
+
 #include "kernels.h"
 
 namespace lsgd {
@@ -661,129 +663,145 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
 // CI x CO block on v_mfma_f32_16x16x4f32. The four waves' sums are added in
 // wave order at the end. Partials land in [S][G][9 CI][CO] as for the GEMM
 // form, reduced over s by k_conv_wupdate.
-template <int CI, int CO>
-__global__ __launch_bounds__(kT) void k_conv_wgrad_rows(ConvArgs c) {
-  constexpr int SP = 64;                       // positions per slab
-  constexpr int XQ = SP * CI / 4, DQ = SP * CO / 4;
+// Weight gradient of the stage-2 and stage-3 convolutions (output rows of
+// WO = 16 or 8 positions) from band tiles. A band is SP = 64 output positions,
+// 64 / WO whole output rows of one image; per band the output gradients
+// [64][CO] and the input rows its taps read, [(BH - 1) STRIDE + 3] x
+// [(WO - 1) STRIDE + 3] x CI with the zero padding, go to LDS once for all
+// nine taps (two buffers: the next band's loads are in flight while this band
+// computes). The (tap, 16-column block) pairs of dW are dealt to the waves --
+// pair p to wave p % 4 -- and each wave accumulates its pairs over all 64
+// positions of every band (v_mfma_f32_16x16x4f32: lane l takes input channel
+// 16 i + l % 16 and output channel 16 n + l % 16 at position 4 kk + l / 16),
+// so no cross-wave sum is needed. Workgroup (g, split s) walks bands
+// [s per, (s + 1) per) of replica g, per = ceil(bands / S), in ascending
+// order; its partial sum lands in [S][G][9 CI][CO] for k_conv_wupdate.
+template <int CI, int CO, int STRIDE, int WO>
+__global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
+  constexpr int SP = 64, BH = SP / WO;
+  constexpr int TH = (BH - 1) * STRIDE + 3, TW = (WO - 1) * STRIDE + 3;
+  constexpr int XP = CI + 4, DP = CO + 4;               // LDS pitches (16-byte rows)
+  constexpr int XQ = TH * TW * (CI / 4), DQ = SP * (CO / 4);  // float4 per tile
   constexpr int XPT = (XQ + kT - 1) / kT, DPT = (DQ + kT - 1) / kT;
-  constexpr int MB = CI / 16, NB = CO / 16;
-  constexpr int XP = CI + 4, DP = CO + 4;      // LDS pitches (16-byte rows)
-  constexpr int LDSF = 2 * SP * XP + 2 * SP * DP;
-  static_assert(4 * CI * CO <= LDSF, "wave reduction fits the slab buffers");
-  __shared__ __attribute__((aligned(16))) float lds[LDSF];
-  float* Xs = lds;                  // [2][SP][XP]
-  float* Ds = lds + 2 * SP * XP;    // [2][SP][DP]
+  constexpr int MB = CI / 16, NB = CO / 16, NP = 9 * NB, PPW = (NP + 3) / 4;
+  constexpr int XF = TH * TW * XP, DF = SP * DP;        // floats per buffer
+  static_assert(DQ % kT == 0, "whole float4 rounds of the gradient tile");
+  extern __shared__ __attribute__((aligned(16))) float lds[];  // [2][XF] then [2][DF]
+  float* Xs = lds;
+  float* Ds = lds + 2 * XF;
 
-  const int S = c.splits;
-  int l = blockIdx.x;
-  const int sp = l % S;
-  l /= S;
-  const int tap = l % 9, g = l / 9;
-  const int kh = tap / 3, kw = tap - kh * 3;
-  const int HWo = c.Ho * c.Wo, rows = c.Bt * HWo;
-  const int kbeg = sp * c.mchunk, kend = min(rows, kbeg + c.mchunk);
-  const int nsl = kend > kbeg ? (kend - kbeg) / SP : 0;
+  const int S = c.splits, sp = blockIdx.x % S, g = blockIdx.x / S;
+  const int bpi = c.Ho / BH;                            // bands per image
+  const int nbands = c.Bt * bpi, per = (nbands + S - 1) / S;
+  const int b0 = sp * per, nbd = max(0, min(nbands, b0 + per) - b0);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lq = lane >> 4, lm = lane & 15;
 
-  auto gload = [&](int j, v4f(&xr)[XPT], v4f(&dr)[DPT]) __attribute__((always_inline)) {
-    const int p0 = kbeg + j * SP;
-    const int b = p0 / HWo, pl0 = p0 - b * HWo;
-    const long long img = (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
+  // every load of band bd in flight at once (clamped addresses, padding
+  // zeroed at use)
+  auto gload = [&](int bd, v4f(&xr)[XPT], v4f(&dr)[DPT]) __attribute__((always_inline)) {
+    const int b = bd / bpi, oh0 = (bd - b * bpi) * BH;
+    const float* xs = c.x + (long long)g * c.sx + (long long)b * c.H * c.W * CI;
+    const int ih0 = oh0 * STRIDE - 1;
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
       const int q = min(tid + kT * i, XQ - 1);
-      const int pos = q / (CI / 4), c4 = (q - pos * (CI / 4)) * 4;
-      const int pl = pl0 + pos, oh = pl / c.Wo, ow = pl - oh * c.Wo;
-      const int ih = oh * c.stride + kh - 1, iw = ow * c.stride + kw - 1;
+      const int pix = q / (CI / 4), c4 = (q - pix * (CI / 4)) * 4;
+      const int tr = pix / TW, tc = pix - tr * TW;
+      const int ih = ih0 + tr, iw = tc - 1;
       const bool ok = ih >= 0 && ih < c.H && iw >= 0 && iw < c.W;
-      const long long o = img + ((long long)(ok ? ih : 0) * c.W + (ok ? iw : 0)) * c.Cin + c4;
-      xr[i] = *(const v4f*)(c.x + o);
+      xr[i] = *(const v4f*)(xs + ((long long)(ok ? ih : 0) * c.W + (ok ? iw : 0)) * CI + c4);
       if (!ok) xr[i] = v4f{0.f, 0.f, 0.f, 0.f};
     }
-    const long long drow = ((long long)g * c.Bt + b) * HWo + pl0;
+    const float* ds = c.dy + (((long long)g * c.Bt + b) * c.Ho + oh0) * WO * CO;
 #pragma unroll
-    for (int i = 0; i < DPT; ++i) {
-      const int q = min(tid + kT * i, DQ - 1);
-      const int pos = q / (CO / 4), c4 = (q - pos * (CO / 4)) * 4;
-      dr[i] = *(const v4f*)(c.dy + (drow + pos) * c.Cout + c4);
-    }
+    for (int i = 0; i < DPT; ++i) dr[i] = *(const v4f*)(ds + 4 * (tid + kT * i));
   };
   auto lstore = [&](int buf, const v4f(&xr)[XPT], const v4f(&dr)[DPT]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
       const int q = tid + kT * i;
       if (q < XQ) {
-        const int pos = q / (CI / 4), c4 = (q - pos * (CI / 4)) * 4;
-        *(v4f*)&Xs[(buf * SP + pos) * XP + c4] = xr[i];
+        const int pix = q / (CI / 4), c4 = (q - pix * (CI / 4)) * 4;
+        *(v4f*)&Xs[buf * XF + pix * XP + c4] = xr[i];
       }
     }
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int q = tid + kT * i;
-      if (q < DQ) {
-        const int pos = q / (CO / 4), c4 = (q - pos * (CO / 4)) * 4;
-        *(v4f*)&Ds[(buf * SP + pos) * DP + c4] = dr[i];
+      const int pos = q / (CO / 4), c4 = (q - pos * (CO / 4)) * 4;
+      *(v4f*)&Ds[buf * DF + pos * DP + c4] = dr[i];
+    }
+  };
+  floatx4 acc[PPW][MB];
+#pragma unroll
+  for (int pp = 0; pp < PPW; ++pp)
+#pragma unroll
+    for (int i = 0; i < MB; ++i) acc[pp][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const float* X = Xs + buf * XF;
+    const float* D = Ds + buf * DF;
+#pragma unroll 2
+    for (int kk = 0; kk < SP / 4; ++kk) {
+      const int pos = kk * 4 + lq, orow = pos / WO, ocol = pos - orow * WO;
+#pragma unroll
+      for (int pp = 0; pp < PPW; ++pp) {
+        const int p = wave + 4 * pp;  // uniform over the wave
+        if (p < NP) {
+          const int tap = p / NB, nbk = p - tap * NB, kh = tap / 3, kw = tap - kh * 3;
+          const float bv = D[pos * DP + nbk * 16 + lm];
+          const float* xa = X + ((orow * STRIDE + kh) * TW + ocol * STRIDE + kw) * XP + lm;
+#pragma unroll
+          for (int i = 0; i < MB; ++i)
+            acc[pp][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i * 16], bv, acc[pp][i], 0, 0, 0);
+        }
       }
     }
   };
-  floatx4 acc[MB][NB];
-#pragma unroll
-  for (int i = 0; i < MB; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int pos = wave * 16 + kk * 4 + lq;
-      float av[MB], bv[NB];
-#pragma unroll
-      for (int i = 0; i < MB; ++i) av[i] = Xs[(buf * SP + pos) * XP + i * 16 + lm];
-#pragma unroll
-      for (int j = 0; j < NB; ++j) bv[j] = Ds[(buf * SP + pos) * DP + j * 16 + lm];
-#pragma unroll
-      for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
-  };
-  if (nsl > 0) {
+  if (nbd > 0) {
     v4f xr0[XPT], xr1[XPT], dr0[DPT], dr1[DPT];
-    auto slab = [&](int t) __attribute__((always_inline)) { return min(t, nsl - 1); };
-    gload(slab(0), xr0, dr0);
-    gload(slab(1), xr1, dr1);
+    auto band = [&](int t) __attribute__((always_inline)) { return b0 + min(t, nbd - 1); };
+    gload(band(0), xr0, dr0);
+    gload(band(1), xr1, dr1);
     lstore(0, xr0, dr0);
     __syncthreads();
     int it = 0;
-    for (; it + 1 < nsl; it += 2) {
-      gload(slab(it + 2), xr0, dr0);
+    for (; it + 1 < nbd; it += 2) {
+      gload(band(it + 2), xr0, dr0);
       __builtin_amdgcn_sched_barrier(0);
       compute(0);
       lstore(1, xr1, dr1);
       __syncthreads();
-      gload(slab(it + 3), xr1, dr1);
+      gload(band(it + 3), xr1, dr1);
       __builtin_amdgcn_sched_barrier(0);
       compute(1);
       lstore(0, xr0, dr0);
       __syncthreads();
     }
-    if (it < nsl) compute(0);
+    if (it < nbd) compute(0);  // odd band count: the last band is in buffer 0
   }
-  // the four waves' sums, added in wave order: block (i, j) register v of
-  // lane l is dW[16 i + 4 (l/16) + v][16 j + l%16]
-  __syncthreads();
+  // block (pair, i) register v of lane l: dW[tap][16 i + 4 (l/16) + v][16 n + l%16]
+  float* out = c.out + ((long long)sp * c.G + g) * 9 * CI * CO;
 #pragma unroll
-  for (int i = 0; i < MB; ++i)
+  for (int pp = 0; pp < PPW; ++pp) {
+    const int p = wave + 4 * pp;
+    if (p < NP) {
+      const int tap = p / NB, nbk = p - tap * NB;
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+      for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        lds[wave * CI * CO + (i * 16 + lq * 4 + v) * CO + j * 16 + lm] = acc[i][j][v];
-  __syncthreads();
-  float* out = c.out + ((long long)sp * c.G + g) * 9 * CI * CO + (long long)tap * CI * CO;
-  for (int e = tid; e < CI * CO; e += kT)
-    out[e] = ((lds[e] + lds[CI * CO + e]) + lds[2 * CI * CO + e]) + lds[3 * CI * CO + e];
+        for (int v = 0; v < 4; ++v)
+          out[(long long)(tap * CI + i * 16 + 4 * lq + v) * CO + nbk * 16 + lm] = acc[pp][i][v];
+    }
+  }
+}
+
+// LDS bytes of a k_conv_wgrad_band instance (both buffers).
+template <int CI, int CO, int STRIDE, int WO>
+constexpr size_t wgrad_band_lds() {
+  constexpr int BH = 64 / WO;
+  constexpr int TH = (BH - 1) * STRIDE + 3, TW = (WO - 1) * STRIDE + 3;
+  return (size_t)2 * (TH * TW * (CI + 4) + 64 * (CO + 4)) * sizeof(float);
 }
 
 // Weight gradient: sum the S partials (ascending s) and apply the update to
@@ -1172,13 +1190,40 @@ bool conv_fwd_stats(const ConvGeom& q) {
 }
 
 // Splits of a weight gradient over the batch: a power of two that divides
-// the batch (the stem's kernel takes whole images per split), at most 64,
-// with at least 1024 positions per split.
+// the batch (the stem's kernel takes whole images per split). The band
+// kernel of the 16- and 8-wide stages takes 32 and 16 splits (about two and
+// one workgroups per compute unit at 16 replicas, each with whole bands);
+// the others at most 64 with at least 1024 positions per split.
 int conv_wgrad_splits(int Bt, int Ho, int Wo) {
   const int rows = Bt * Ho * Wo;
+  const int cap = Wo == 16 ? 32 : Wo == 8 ? 16 : 64;
   int s = 1;
-  while (s < 64 && rows / (2 * s) >= 1024 && Bt % (2 * s) == 0) s *= 2;
+  while (s < cap && rows / (2 * s) >= (Wo <= 16 ? 64 : 1024) && Bt % (2 * s) == 0) s *= 2;
   return s;
+}
+
+// One k_conv_wgrad_band launch; instances above 64 KB of LDS opt in to more
+// once per device (the per-device flags are atomics, the request idempotent).
+template <int CI, int CO, int STRIDE, int WO>
+hipError_t launch_wgrad_band(const ConvArgs& c, hipStream_t st) {
+  constexpr size_t lds = wgrad_band_lds<CI, CO, STRIDE, WO>();
+  static_assert(lds <= 160 * 1024, "fits one compute unit's LDS");
+  if (lds > 64 * 1024) {
+    static std::atomic<bool> done[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (!done[dev].load(std::memory_order_acquire)) {
+      e = hipFuncSetAttribute((const void*)k_conv_wgrad_band<CI, CO, STRIDE, WO>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      done[dev].store(true, std::memory_order_release);
+    }
+  }
+  hipLaunchKernelGGL((k_conv_wgrad_band<CI, CO, STRIDE, WO>), dim3((unsigned)(c.G * c.splits)),
+                     dim3(kT), lds, st, c);
+  return hipGetLastError();
 }
 
 hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
@@ -1206,10 +1251,6 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   if (mode == CONV_WGRAD) {
     c.splits = conv_wgrad_splits(q.Bt, q.Ho, q.Wo);
     const int rows = q.Bt * q.Ho * q.Wo;
-    auto chan = [](int v) { return v == 16 || v == 32 || v == 64; };
-    const bool rowsk = chan(q.Cin) && chan(q.Cout) && q.Cout >= q.Cin && !q.rowmap &&
-                       (q.Ho * q.Wo) % 64 == 0 && ((uintptr_t)q.x & 15) == 0 &&
-                       ((uintptr_t)q.dy & 15) == 0 && q.sx % 4 == 0;
     const bool halo = q.Cin == 16 && q.Cout == 16 && q.stride == 1 && q.W == 32 &&
                       q.Wo == 32 && q.H == q.Ho && q.H % 8 == 0 && !q.rowmap &&
                       ((uintptr_t)q.x & 15) == 0 && ((uintptr_t)q.dy & 15) == 0 &&
@@ -1225,21 +1266,21 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
                          st, c);
       return hipGetLastError();
     }
-    if (rowsk) {
-      // whole 64-position slabs per split
-      c.mchunk = ((rows + c.splits - 1) / c.splits + 63) / 64 * 64;
-      const dim3 grid((unsigned)(q.G * 9 * c.splits));
-#define LSGD_WG(CI, CO)                                                                \
-  if (q.Cin == CI && q.Cout == CO) {                                                   \
-    hipLaunchKernelGGL((k_conv_wgrad_rows<CI, CO>), grid, dim3(kT), 0, st, c);         \
-    return hipGetLastError();                                                          \
-  }
-      LSGD_WG(16, 16)
-      LSGD_WG(16, 32)
-      LSGD_WG(32, 32)
-      LSGD_WG(32, 64)
-      LSGD_WG(64, 64)
-#undef LSGD_WG
+    // band tiles: 64 output positions (whole 16- or 8-wide rows) per band
+    const bool bandk = !q.rowmap && (q.Wo == 16 || q.Wo == 8) && q.Ho % (64 / q.Wo) == 0 &&
+                       ((q.stride == 1 && q.H == q.Ho && q.W == q.Wo) ||
+                        (q.stride == 2 && q.H == 2 * q.Ho && q.W == 2 * q.Wo)) &&
+                       ((uintptr_t)q.x & 15) == 0 && ((uintptr_t)q.dy & 15) == 0 &&
+                       q.sx % 4 == 0;
+    if (bandk) {
+      if (q.Cin == 32 && q.Cout == 32 && q.stride == 1 && q.Wo == 16)
+        return launch_wgrad_band<32, 32, 1, 16>(c, st);
+      if (q.Cin == 16 && q.Cout == 32 && q.stride == 2 && q.Wo == 16)
+        return launch_wgrad_band<16, 32, 2, 16>(c, st);
+      if (q.Cin == 64 && q.Cout == 64 && q.stride == 1 && q.Wo == 8)
+        return launch_wgrad_band<64, 64, 1, 8>(c, st);
+      if (q.Cin == 32 && q.Cout == 64 && q.stride == 2 && q.Wo == 8)
+        return launch_wgrad_band<32, 64, 2, 8>(c, st);
     }
     return hipErrorInvalidValue;  // no weight-gradient kernel for this shape
   } else {
