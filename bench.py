@@ -185,7 +185,8 @@ def resnet_step_costs(w) -> dict:
         if second:
             cin_blk = convs[i - 1][0]
             sc = y if (convs[i - 1][2] == 1 and cin_blk == co) else K * B * so * so * cin_blk * 4
-        add("bn_apply", 0, 2 * y + sc)
+        if i % 2 == 0:   # a block's first BN-ReLU is formed by its consumers
+            add("bn_apply", 0, 2 * y + sc)
         add("bn_bwd", 0, (7 if second else 5) * y)
         if i > 0:
             add("conv_dgrad", fl, y + x + wt)

@@ -679,18 +679,30 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
 
   LSGD_LAUNCH(c, "sample", sample(c, c->step, c->idx(), s));
 
+  // the input of a block's second convolution is the first convolution's
+  // BN-ReLU output, which is never stored: the kernels form it from that
+  // convolution's pre-BN output (BN layer j) as they load it
+  auto bn_input = [&](lsgd::ConvGeom& g, int j) {
+    g.bn_mu = mu + (size_t)j * K * 64;
+    g.bn_inv = inv + (size_t)j * K * 64;
+    g.bn_g = W + r.cv[j].offG;
+    g.bn_b = W + r.cv[j].offB;
+    g.bn_sP = Ps;
+  };
+
   // forward: stem, then blocks (a: conv-BN-ReLU, b: conv-BN + shortcut, ReLU)
   for (int i = 0; i < kResConvs; ++i) {
     const ConvSpec& q = r.cv[i];
     lsgd::ConvGeom g = geom(i);
-    const float* xin = nullptr;  // input activation of conv i
     if (i == 0) {
       g.x = c->X;
       g.sx = 0;
       g.rowmap = c->idx();
-    } else {
-      xin = F(r.cv[i - 1].act);
-      g.x = xin;
+    } else if (i % 2 == 0) {  // second convolution of a block
+      g.x = F(r.cv[i - 1].y);
+      bn_input(g, i - 1);
+    } else {  // first convolution: the block input (stem or previous block output)
+      g.x = F(r.cv[i - 1].act);
     }
     g.out = F(q.y);
     // the convolution writes its BN statistics per 256-row chunk where its
@@ -710,10 +722,11 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     else
       LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
                                                        mi, ii, rm, rv, r.Rs, s));
+    if (i % 2 == 1) continue;  // a block's first BN-ReLU: formed by its consumers
     int mode = 0;
     const float* blk_in = nullptr;
     int cin_blk = 0;
-    if (i > 0 && i % 2 == 0) {  // second convolution of a block
+    if (i > 0) {  // second convolution of a block
       const ConvSpec& qa = r.cv[i - 1];
       blk_in = F(r.cv[i - 2].act);
       cin_blk = qa.Cin;
@@ -783,7 +796,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // weight gradient of conv i from its input x and output gradient dy into
   // per-split partials, then their fixed-order sum and the update (after
   // any input gradient that reads the old weight)
-  auto wgrad = [&](int i, const float* x, const float* dy) -> lsgd_status {
+  // (bn_layer >= 0: x is that BN layer's pre-BN output, see bn_input)
+  auto wgrad = [&](int i, const float* x, const float* dy, int bn_layer) -> lsgd_status {
     const ConvSpec& q = r.cv[i];
     lsgd::ConvGeom g = geom(i);
     if (i == 0) {
@@ -792,6 +806,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
       g.rowmap = c->idx();
     } else {
       g.x = x;
+      if (bn_layer >= 0) bn_input(g, bn_layer);
     }
     g.dy = dy;
     g.out = wpart;
@@ -820,11 +835,11 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     // second convolution: its output went through the shortcut add and ReLU
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1]));
     if (lsgd_status st = dgrad(ib, gb[1], gb[2])) return st;
-    if (lsgd_status st = wgrad(ib, F(r.cv[ia].act), gb[1])) return st;
+    if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), gb[1], ia)) return st;
     // first convolution: ReLU'd BN output, the mask recomputed from its input
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[1]));
     if (lsgd_status st = dgrad(ia, gb[1], gb[nxt])) return st;
-    if (lsgd_status st = wgrad(ia, h_in, gb[1])) return st;
+    if (lsgd_status st = wgrad(ia, h_in, gb[1], -1)) return st;
     // the shortcut's share of the block-output gradient
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
     LSGD_LAUNCH(c, "shortcut_bwd",
@@ -833,7 +848,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     cur = nxt;
   }
   LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1]));
-  if (lsgd_status st = wgrad(0, nullptr, gb[1])) return st;
+  if (lsgd_status st = wgrad(0, nullptr, gb[1], -1)) return st;
   c->step += 1;
   return LSGD_OK;
 }

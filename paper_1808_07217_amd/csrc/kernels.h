@@ -154,6 +154,15 @@ struct ConvGeom {
   long long sW;
   float* out;
   double* stats;  // forward: BN statistics per 256-row chunk (see conv_fwd_stats)
+  // forward / weight gradient of a block's second convolution: x is the
+  // first convolution's pre-BN output and the input is relu(BN(x)) with the
+  // replica's statistics (mu, inv at g * Cin + c) and parameters (gamma,
+  // beta at g * bn_sP + c), formed as the tiles are loaded; nullptr: x as is
+  const float* bn_mu;
+  const float* bn_inv;
+  const float* bn_g;
+  const float* bn_b;
+  long long bn_sP;
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
 int conv_wgrad_splits(int Bt, int Ho, int Wo);

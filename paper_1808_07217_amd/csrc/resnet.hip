@@ -44,13 +44,51 @@ struct ConvArgs {
   long long sx;          //   group stride (0 with a row map)
   const int32_t* rowmap; // sampled image indices [G][Bt] (first convolution)
   const float* dy;       // output gradient [G][Bt][Ho][Wo][Cout]
-  const float* Wk;       // weights: [9*Cin][Cout] (fwd, wgrad), [9*Cout][Cin] (dgrad)
+  const float* Wk;       // weights [9*Cin][Cout] (every mode)
   long long sW;          //   group stride
   float* out;            // fwd: y; dgrad: dx; wgrad: partials [S][G][9Cin][Cout]
   int splits, mchunk;    // wgrad split over the m = (b, oh, ow) rows
   double* stats;         // fwd: per 256-row chunk q of replica g, (sum y, sum y^2)
                          //   per channel at [g][q][Cout][2], or nullptr
+  const float* bn_mu;    // input BN-ReLU (see ConvGeom), or nullptr
+  const float* bn_inv;
+  const float* bn_g;
+  const float* bn_b;
+  long long bn_sP;
 };
+
+// The shifted, scaled BN output z = gamma * (y - mu) * inv + beta in one fixed
+// rounding order: the forward pass takes relu(z) (+ the shortcut) with it, and
+// the backward pass of a convolution followed by BN-ReLU alone recomputes the
+// ReLU mask z > 0 with it instead of reading the activation back.
+__device__ __forceinline__ float bn_z(float gm, float y, float m, float iv, float bt) {
+  return __builtin_fmaf(gm * (y - m), iv, bt);
+}
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// BN statistics and parameters of four consecutive input channels.
+struct BnIn4 {
+  v4f g, m, iv, b;
+};
+__device__ __forceinline__ BnIn4 bn_in_params(const ConvArgs& c, int g, int ch0) {
+  BnIn4 p;
+  p.m = *(const v4f*)(c.bn_mu + (long long)g * c.Cin + ch0);
+  p.iv = *(const v4f*)(c.bn_inv + (long long)g * c.Cin + ch0);
+  p.g = *(const v4f*)(c.bn_g + (long long)g * c.bn_sP + ch0);
+  p.b = *(const v4f*)(c.bn_b + (long long)g * c.bn_sP + ch0);
+  return p;
+}
+// relu(z) of four pre-BN values (the activation the BN pass would store)
+__device__ __forceinline__ v4f bn_in(const BnIn4& p, v4f v) {
+  v4f r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float z = bn_z(p.g[e], v[e], p.m[e], p.iv[e], p.b[e]);
+    r[e] = z > 0.f ? z : 0.f;
+  }
+  return r;
+}
 
 // BN statistics of a forward tile: lane partial sums (s0, s1) of one channel,
 // added over the lanes xor-ed by `mask_bits` (a fixed butterfly), written by
@@ -83,7 +121,6 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
 // 256-row tile lies in one class (Bt Ho Wo a multiple of 256) and its slabs
 // run over that class's taps only.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
 
 template <int MODE, int BN, bool P2 = false>
 __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
@@ -141,8 +178,26 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   }
   const float* src = MODE == CONV_FWD ? c.x : c.dy;
   const int nk = ntap * Cr / BK;
-  auto gload = [&](int s, v4f(&xa4)[RPT], v4f& xb) __attribute__((always_inline)) {
+  // forward of a block's second convolution: the input BN-ReLU, statistics
+  // and parameters of every input channel staged in LDS
+  const bool bnin = MODE == CONV_FWD && c.bn_mu != nullptr;
+  __shared__ __attribute__((aligned(16))) float bnp[4][64];
+  if (bnin) {
+    for (int t = tid; t < c.Cin; t += kT) {
+      bnp[0][t] = c.bn_mu[(long long)g * c.Cin + t];
+      bnp[1][t] = c.bn_inv[(long long)g * c.Cin + t];
+      bnp[2][t] = c.bn_g[(long long)g * c.bn_sP + t];
+      bnp[3][t] = c.bn_b[(long long)g * c.bn_sP + t];
+    }
+    __syncthreads();
+  }
+  // okm: which of this thread's rows read inside the image (bit i); chs: the
+  // slab's first channel of this thread
+  auto gload = [&](int s, v4f(&xa4)[RPT], v4f& xb, unsigned& okm, int& chs)
+      __attribute__((always_inline)) {
     const int ti = s / (Cr / BK), ch0 = (s - ti * (Cr / BK)) * BK + kq;
+    okm = 0;
+    chs = ch0;
     int kh, kw;
     if constexpr (P2) {  // the class's taps: kh = 1 or {0, 2}, kw likewise
       const int th = ti / nkw, tw = ti - th * nkw;
@@ -174,6 +229,7 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
         xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.Wo + xx) * c.Cout + ch0);
       }
       if (!ok) xa4[i] = v4f{0.f, 0.f, 0.f, 0.f};
+      okm |= (unsigned)ok << i;
     }
     const int bq = min(tid, BQ - 1);
     const int cbase = (s - ti * (Cr / BK)) * BK;  // slab's first reduction channel
@@ -188,9 +244,22 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
                          (bq % (BK / 4)) * 4);
     }
   };
-  auto lstore = [&](int buf, const v4f(&xa4)[RPT], const v4f& xb) __attribute__((always_inline)) {
+  auto lstore = [&](int buf, const v4f(&xa4)[RPT], const v4f& xb, unsigned okm, int chs)
+      __attribute__((always_inline)) {
+    if (bnin) {
+      BnIn4 p;
+      p.m = *(const v4f*)&bnp[0][chs];
+      p.iv = *(const v4f*)&bnp[1][chs];
+      p.g = *(const v4f*)&bnp[2][chs];
+      p.b = *(const v4f*)&bnp[3][chs];
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] = xa4[i];
+      for (int i = 0; i < RPT; ++i)  // padding stays 0
+        *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] =
+            (okm >> i & 1) ? bn_in(p, xa4[i]) : v4f{0.f, 0.f, 0.f, 0.f};
+    } else {
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] = xa4[i];
+    }
     if (tid < BQ) {
       if constexpr (MODE == CONV_FWD) {
         *(v4f*)&Bs[buf][tid / (BN / 4)][(tid % (BN / 4)) * 4] = xb;
@@ -223,22 +292,24 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
   };
   v4f ra0[RPT], ra1[RPT], rb0, rb1;
+  unsigned ok0, ok1;
+  int ch0s, ch1s;
   auto slab = [&](int t) __attribute__((always_inline)) { return min(t, nk - 1); };
-  gload(slab(0), ra0, rb0);
-  gload(slab(1), ra1, rb1);
-  lstore(0, ra0, rb0);
+  gload(slab(0), ra0, rb0, ok0, ch0s);
+  gload(slab(1), ra1, rb1, ok1, ch1s);
+  lstore(0, ra0, rb0, ok0, ch0s);
   __syncthreads();
   int it = 0;
   for (; it + 1 < nk; it += 2) {
-    gload(slab(it + 2), ra0, rb0);
+    gload(slab(it + 2), ra0, rb0, ok0, ch0s);
     __builtin_amdgcn_sched_barrier(0);
     compute(0);
-    lstore(1, ra1, rb1);
+    lstore(1, ra1, rb1, ok1, ch1s);
     __syncthreads();
-    gload(slab(it + 3), ra1, rb1);
+    gload(slab(it + 3), ra1, rb1, ok1, ch1s);
     __builtin_amdgcn_sched_barrier(0);
     compute(1);
-    lstore(0, ra0, rb0);
+    lstore(0, ra0, rb0, ok0, ch0s);
     __syncthreads();
   }
   if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
@@ -466,8 +537,14 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
                          ? c.x + (long long)g * c.sx + (long long)b * H * W * C
                          : c.dy + ((long long)g * c.Bt + b) * H * W * C;
   const float* Wg = c.Wk + (long long)g * c.sW;
+  // forward of a block's second convolution: the input BN-ReLU of this
+  // thread's four channels (c4 = 4 (tid % 4) for every float4 it stages)
+  const bool bnin = MODE == CONV_FWD && c.bn_mu != nullptr;
+  BnIn4 bp{};
+  if (bnin) bp = bn_in_params(c, g, (threadIdx.x & 3) * 4);
   // every load issued before the LDS stores (clamped addresses, zero-masked)
   v4f tv[TPT], wv[WPT];
+  unsigned okm = 0;
 #pragma unroll
   for (int i = 0; i < TPT; ++i) {
     const int q = min((int)threadIdx.x + kT * i, TQ - 1);
@@ -477,6 +554,7 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
     const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
     tv[i] = *(const v4f*)(src + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
     if (!ok) tv[i] = v4f{0.f, 0.f, 0.f, 0.f};
+    okm |= (unsigned)ok << i;
   }
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
@@ -492,7 +570,9 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
 #pragma unroll
   for (int i = 0; i < TPT; ++i) {
     const int q = (int)threadIdx.x + kT * i;
-    if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = tv[i];
+    v4f v = tv[i];
+    if (bnin) v = (okm >> i & 1) ? bn_in(bp, v) : v4f{0.f, 0.f, 0.f, 0.f};  // padding stays 0
+    if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = v;
   }
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
@@ -595,11 +675,17 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
   floatx4 acc[9];
 #pragma unroll
   for (int t = 0; t < 9; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // a block's second convolution: the input BN-ReLU of this thread's four
+  // channels (c4 = 4 (tid % 4) for every float4 it stages)
+  const bool bnin = c.bn_mu != nullptr;
+  BnIn4 bp{};
+  if (bnin) bp = bn_in_params(c, g, (threadIdx.x & 3) * 4);
   for (int bd = bb; bd < be; ++bd) {
     const int b = bd / bpi, h0 = (bd - b * bpi) * BH;
     const float* xs = c.x + (long long)g * c.sx + (long long)b * H * W * C;
     const float* ds = c.dy + (((long long)g * c.Bt + b) * H + h0) * W * C;
     v4f tv[TPT], dv[DPT];
+    unsigned okm = 0;
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       const int q = min((int)threadIdx.x + kT * i, TQ - 1);
@@ -609,6 +695,7 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
       const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
       tv[i] = *(const v4f*)(xs + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
       if (!ok) tv[i] = v4f{0.f, 0.f, 0.f, 0.f};
+      okm |= (unsigned)ok << i;
     }
 #pragma unroll
     for (int i = 0; i < DPT; ++i) dv[i] = *(const v4f*)(ds + 4 * ((int)threadIdx.x + kT * i));
@@ -616,7 +703,9 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       const int q = (int)threadIdx.x + kT * i;
-      if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = tv[i];
+      v4f v = tv[i];
+      if (bnin) v = (okm >> i & 1) ? bn_in(bp, v) : v4f{0.f, 0.f, 0.f, 0.f};
+      if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = v;
     }
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
@@ -686,9 +775,11 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
   constexpr int MB = CI / 16, NB = CO / 16, NP = 9 * NB, PPW = (NP + 3) / 4;
   constexpr int XF = TH * TW * XP, DF = SP * DP;        // floats per buffer
   static_assert(DQ % kT == 0, "whole float4 rounds of the gradient tile");
-  extern __shared__ __attribute__((aligned(16))) float lds[];  // [2][XF] then [2][DF]
+  // [2][XF], then [2][DF], then the input BN-ReLU's [4][CI]
+  extern __shared__ __attribute__((aligned(16))) float lds[];
   float* Xs = lds;
   float* Ds = lds + 2 * XF;
+  float* bnp = lds + 2 * (XF + DF);
 
   const int S = c.splits, sp = blockIdx.x % S, g = blockIdx.x / S;
   const int bpi = c.Ho / BH;                            // bands per image
@@ -696,10 +787,25 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
   const int b0 = sp * per, nbd = max(0, min(nbands, b0 + per) - b0);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lq = lane >> 4, lm = lane & 15;
+  // a block's second convolution: the input BN-ReLU (statistics and
+  // parameters per input channel in LDS; every float4 this thread stages
+  // has channels c4 .. c4 + 3, c4 = 4 (tid % (CI / 4)))
+  const bool bnin = c.bn_mu != nullptr;
+  if (bnin) {
+    for (int t = tid; t < CI; t += kT) {
+      bnp[t] = c.bn_mu[(long long)g * CI + t];
+      bnp[CI + t] = c.bn_inv[(long long)g * CI + t];
+      bnp[2 * CI + t] = c.bn_g[(long long)g * c.bn_sP + t];
+      bnp[3 * CI + t] = c.bn_b[(long long)g * c.bn_sP + t];
+    }
+    __syncthreads();
+  }
 
   // every load of band bd in flight at once (clamped addresses, padding
   // zeroed at use)
-  auto gload = [&](int bd, v4f(&xr)[XPT], v4f(&dr)[DPT]) __attribute__((always_inline)) {
+  auto gload = [&](int bd, v4f(&xr)[XPT], v4f(&dr)[DPT], unsigned& okm)
+      __attribute__((always_inline)) {
+    okm = 0;
     const int b = bd / bpi, oh0 = (bd - b * bpi) * BH;
     const float* xs = c.x + (long long)g * c.sx + (long long)b * c.H * c.W * CI;
     const int ih0 = oh0 * STRIDE - 1;
@@ -712,18 +818,30 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
       const bool ok = ih >= 0 && ih < c.H && iw >= 0 && iw < c.W;
       xr[i] = *(const v4f*)(xs + ((long long)(ok ? ih : 0) * c.W + (ok ? iw : 0)) * CI + c4);
       if (!ok) xr[i] = v4f{0.f, 0.f, 0.f, 0.f};
+      okm |= (unsigned)ok << i;
     }
     const float* ds = c.dy + (((long long)g * c.Bt + b) * c.Ho + oh0) * WO * CO;
 #pragma unroll
     for (int i = 0; i < DPT; ++i) dr[i] = *(const v4f*)(ds + 4 * (tid + kT * i));
   };
-  auto lstore = [&](int buf, const v4f(&xr)[XPT], const v4f(&dr)[DPT]) __attribute__((always_inline)) {
+  auto lstore = [&](int buf, const v4f(&xr)[XPT], const v4f(&dr)[DPT], unsigned okm)
+      __attribute__((always_inline)) {
+    BnIn4 p{};
+    if (bnin) {
+      const int c4 = (tid % (CI / 4)) * 4;
+      p.m = *(const v4f*)&bnp[c4];
+      p.iv = *(const v4f*)&bnp[CI + c4];
+      p.g = *(const v4f*)&bnp[2 * CI + c4];
+      p.b = *(const v4f*)&bnp[3 * CI + c4];
+    }
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
       const int q = tid + kT * i;
       if (q < XQ) {
         const int pix = q / (CI / 4), c4 = (q - pix * (CI / 4)) * 4;
-        *(v4f*)&Xs[buf * XF + pix * XP + c4] = xr[i];
+        v4f v = xr[i];
+        if (bnin) v = (okm >> i & 1) ? bn_in(p, v) : v4f{0.f, 0.f, 0.f, 0.f};  // padding stays 0
+        *(v4f*)&Xs[buf * XF + pix * XP + c4] = v;
       }
     }
 #pragma unroll
@@ -760,22 +878,23 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
   };
   if (nbd > 0) {
     v4f xr0[XPT], xr1[XPT], dr0[DPT], dr1[DPT];
+    unsigned ok0, ok1;
     auto band = [&](int t) __attribute__((always_inline)) { return b0 + min(t, nbd - 1); };
-    gload(band(0), xr0, dr0);
-    gload(band(1), xr1, dr1);
-    lstore(0, xr0, dr0);
+    gload(band(0), xr0, dr0, ok0);
+    gload(band(1), xr1, dr1, ok1);
+    lstore(0, xr0, dr0, ok0);
     __syncthreads();
     int it = 0;
     for (; it + 1 < nbd; it += 2) {
-      gload(band(it + 2), xr0, dr0);
+      gload(band(it + 2), xr0, dr0, ok0);
       __builtin_amdgcn_sched_barrier(0);
       compute(0);
-      lstore(1, xr1, dr1);
+      lstore(1, xr1, dr1, ok1);
       __syncthreads();
-      gload(band(it + 3), xr1, dr1);
+      gload(band(it + 3), xr1, dr1, ok1);
       __builtin_amdgcn_sched_barrier(0);
       compute(1);
-      lstore(0, xr0, dr0);
+      lstore(0, xr0, dr0, ok0);
       __syncthreads();
     }
     if (it < nbd) compute(0);  // odd band count: the last band is in buffer 0
@@ -801,7 +920,7 @@ template <int CI, int CO, int STRIDE, int WO>
 constexpr size_t wgrad_band_lds() {
   constexpr int BH = 64 / WO;
   constexpr int TH = (BH - 1) * STRIDE + 3, TW = (WO - 1) * STRIDE + 3;
-  return (size_t)2 * (TH * TW * (CI + 4) + 64 * (CO + 4)) * sizeof(float);
+  return ((size_t)2 * (TH * TW * (CI + 4) + 64 * (CO + 4)) + 4 * CI) * sizeof(float);
 }
 
 // Weight gradient: sum the S partials (ascending s) and apply the update to
@@ -843,13 +962,6 @@ __host__ __device__ __forceinline__ int bn_chunk_rows(int R) {
   return R >= (1 << 17) ? 1024 : R >= (1 << 15) ? 512 : 256;
 }
 
-// The shifted, scaled BN output z = gamma * (y - mu) * inv + beta in one fixed
-// rounding order: the forward pass takes relu(z) (+ the shortcut) with it, and
-// the backward pass of a convolution followed by BN-ReLU alone recomputes the
-// ReLU mask z > 0 with it instead of reading the activation back.
-__device__ __forceinline__ float bn_z(float gm, float y, float m, float iv, float bt) {
-  return __builtin_fmaf(gm * (y - m), iv, bt);
-}
 // Backward coefficients per (replica g, channel c), field f at
 // coef[f * G * C + g * C + c]: gamma * inv, dbeta / R, dgamma / R, and gamma,
 // beta as they were before this step's update.
@@ -1245,6 +1357,14 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   c.sW = q.sW;
   c.out = q.out;
   c.stats = mode == CONV_FWD ? q.stats : nullptr;
+  c.bn_mu = mode == CONV_DGRAD ? nullptr : q.bn_mu;
+  c.bn_inv = q.bn_inv;
+  c.bn_g = q.bn_g;
+  c.bn_b = q.bn_b;
+  c.bn_sP = q.bn_sP;
+  if (c.bn_mu && (q.Cin % 4 || q.bn_sP % 4 || ((uintptr_t)q.bn_mu | (uintptr_t)q.bn_inv |
+                                              (uintptr_t)q.bn_g | (uintptr_t)q.bn_b) & 15))
+    return hipErrorInvalidValue;
   const int Mg = mode == CONV_FWD ? q.Bt * q.Ho * q.Wo
                : mode == CONV_DGRAD ? q.Bt * q.H * q.W : 9 * q.Cin;
   const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
