@@ -47,7 +47,8 @@ struct ConvArgs {
   const float* Wk;       // weights [9*Cin][Cout] (every mode)
   long long sW;          //   group stride
   float* out;            // fwd: y; dgrad: dx; wgrad: partials [S][G][9Cin][Cout]
-  int splits, mchunk;    // wgrad split over the m = (b, oh, ow) rows
+  int splits, mchunk;    // wgrad split over the m = (b, oh, ow) rows; stride-2 input
+                         //   gradient: images per workgroup (mchunk)
   double* stats;         // fwd: per 256-row chunk q of replica g, (sum y, sum y^2)
                          //   per channel at [g][q][Cout][2], or nullptr
   const float* bn_mu;    // input BN-ReLU (see ConvGeom), or nullptr
@@ -112,20 +113,13 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
 // loads carry no branches. Two register sets: slab t+2 is in flight while
 // slab t computes. Each wave owns 64 rows as 16 x 16 blocks of
 // v_mfma_f32_16x16x4f32 (lane l: A[m = l%16][k = l/16], B[k = l/16][n = l%16],
-// accumulator v at C[4 (l/16) + v][l%16]).
-//
-// P2 (input gradient of a stride-2 convolution, H = 2 Ho, W = 2 Wo): an
-// input position (2i + ph, 2j + pw) only receives taps with kh = 1 (ph = 0)
-// or kh in {0, 2} (ph = 1), and likewise for kw -- 1, 2, 2 or 4 of the nine
-// by parity class. The rows are ordered (class, image, i, j) so that every
-// 256-row tile lies in one class (Bt Ho Wo a multiple of 256) and its slabs
-// run over that class's taps only.
+// accumulator v at C[4 (l/16) + v][l%16]). The input gradient here is that of
+// a stride-1 convolution.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-template <int MODE, int BN, bool P2 = false>
+template <int MODE, int BN>
 __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   static_assert(MODE == CONV_FWD || MODE == CONV_DGRAD, "row-tiled modes");
-  static_assert(!P2 || MODE == CONV_DGRAD, "parity classes are an input-gradient form");
   constexpr int BM = 256, BK = 16, PK = BK + 4;  // 80-byte A rows in LDS
   constexpr int NBL = BN / 16;                    // 16-wide column blocks
   constexpr int RPT = BM * BK / 4 / kT;           // A float4 per thread (4)
@@ -141,10 +135,7 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kq = (tid & 3) * 4;  // this thread's 4 channels of the slab
   const float* Bw = c.Wk + (long long)g * c.sW;  // W [9 Cin][Cout] of replica g
-  // P2: this tile's parity class and the slab count of its taps
-  const int HWq = c.Ho * c.Wo, cls_rows = c.Bt * HWq;
-  const int cls = P2 ? m0 / cls_rows : 0, ph = cls >> 1, pw = cls & 1;
-  const int nkw = P2 && pw ? 2 : 1, ntap = P2 ? (ph ? 2 : 1) * nkw : 9;
+  constexpr int ntap = 9;
 
   // rows of this thread: r = tid / 4 + 64 i
   long long base[RPT];  // image (or output-gradient image) base, elements
@@ -162,16 +153,9 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       xa[i] = ow * c.stride - 1;
       base[i] = c.rowmap ? (long long)c.rowmap[(long long)g * c.Bt + b] * c.H * c.W * c.Cin
                          : (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
-    } else if constexpr (P2) {
-      const int rem = mm - cls * cls_rows;
-      const int bb = rem / HWq, q = rem - bb * HWq;
-      const int ii = q / c.Wo, jj = q - ii * c.Wo;
-      ya[i] = 2 * ii + ph + 1;
-      xa[i] = 2 * jj + pw + 1;
-      base[i] = ((long long)g * c.Bt + bb) * c.Ho * c.Wo * c.Cout;
     } else {
       const int h = p / c.W, w = p - h * c.W;
-      ya[i] = h + 1;  // output-gradient row of tap kh: (ya - kh) / stride
+      ya[i] = h + 1;  // output-gradient row of tap kh: ya - kh
       xa[i] = w + 1;
       base[i] = ((long long)g * c.Bt + b) * c.Ho * c.Wo * c.Cout;
     }
@@ -198,16 +182,7 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     const int ti = s / (Cr / BK), ch0 = (s - ti * (Cr / BK)) * BK + kq;
     okm = 0;
     chs = ch0;
-    int kh, kw;
-    if constexpr (P2) {  // the class's taps: kh = 1 or {0, 2}, kw likewise
-      const int th = ti / nkw, tw = ti - th * nkw;
-      kh = ph ? 2 * th : 1;
-      kw = pw ? 2 * tw : 1;
-    } else {
-      kh = ti / 3;
-      kw = ti - kh * 3;
-    }
-    const int tap = kh * 3 + kw;
+    const int kh = ti / 3, kw = ti - kh * 3, tap = ti;
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
       int yy, xx;
@@ -220,10 +195,8 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
         xx = ok ? xx : 0;
         xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.W + xx) * c.Cin + ch0);
       } else {
-        const int th = ya[i] - kh, tw = xa[i] - kw;
-        const int oh = c.stride == 1 ? th : th >> 1, ow = c.stride == 1 ? tw : tw >> 1;
-        ok = rok[i] && th >= 0 && tw >= 0 && oh < c.Ho && ow < c.Wo &&
-             (c.stride == 1 || ((th | tw) & 1) == 0);
+        const int oh = ya[i] - kh, ow = xa[i] - kw;
+        ok = rok[i] && oh >= 0 && ow >= 0 && oh < c.Ho && ow < c.Wo;
         yy = ok ? oh : 0;
         xx = ok ? ow : 0;
         xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.Wo + xx) * c.Cout + ch0);
@@ -352,17 +325,207 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     for (int v = 0; v < 4; ++v) {
       const int m = m0 + wave * 64 + i * 16 + lq * 4 + v;
       if (m < Mg) {
-        long long row = m;
-        if constexpr (P2) {  // back to (image, h, w) order
-          const int rem = m - cls * cls_rows;
-          const int bb = rem / HWq, q = rem - bb * HWq;
-          const int ii = q / c.Wo, jj = q - ii * c.Wo;
-          row = ((long long)bb * c.H + 2 * ii + ph) * c.W + 2 * jj + pw;
-        }
 #pragma unroll
-        for (int j = 0; j < NBL; ++j) out[row * BN + j * 16 + lm] = acc[i][j][v];
+        for (int j = 0; j < NBL; ++j) out[(long long)m * BN + j * 16 + lm] = acc[i][j][v];
       }
     }
+}
+
+// Input gradient of a stride-2 convolution whose output has twice its
+// input's channels (the first convolution of the second and third stages):
+// dx (W x W x CI) from dy (Wo x Wo x CO), Wo = W / 2, square images.
+// Input position (2a + ph, 2j + pw) receives the taps kh = 1 when ph = 0 and
+// kh in {0, 2} when ph = 1 (likewise kw by pw), from dy row
+// a + (ph + 1 - kh) / 2 and column j + (pw + 1 - kw) / 2, so the four dy
+// neighbours (a + dr, j + dc), dr, dc in {0, 1}, feed all nine taps of the
+// four parity classes. A band of BH input rows (256 positions) splits into
+// the four classes of BH/2 x Wo = 64 positions, four 16-row MFMA blocks
+// each. The band's dy rows (one more below it, zero past the image) and
+// columns 0 .. Wo (the last one zero) go to LDS, double buffered: the next
+// band's loads are in flight while a band computes. Workgroup (g, i) takes
+// the c.mchunk images i c.mchunk, ... of replica g, band by band, and each
+// wave keeps the weights it needs in registers throughout:
+//   CI = 16: wave w owns block w of every class over the whole reduction;
+//   CI = 32: wave w owns every block of every class for input channels
+//     16 (w / 2) .. + 15 over half of the output channels (w % 2); the two
+//     halves are added through LDS, each wave storing two of the classes.
+// The reduction over k = (tap, co) takes co as 16 chunk + 4 (l / 16) + s at
+// MFMA step s of a chunk, so a lane reads its four k values of A and of B
+// as one float4 each.
+template <int CI, int CO, int W>
+__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(CI == 16 ? 3 : 2))) void k_conv_dgrad_s2(
+    ConvArgs c) {
+  constexpr int Wo = W / 2, BH = 256 / W, BANDS = W / BH;
+  constexpr int TR = BH / 2 + 1, TC = Wo + 1, PP = CO + 4;  // tile rows, cols, pitch
+  constexpr int TQ = TR * TC * (CO / 4);                     // float4 of a tile
+  constexpr int TPT = (TQ + kT - 1) / kT;
+  constexpr bool kSplit = CI == 32;
+  constexpr int NCH = CO / 16, NCW = kSplit ? NCH / 2 : NCH;  // chunks, per wave
+  constexpr int NBW = kSplit ? 4 : 1;                         // blocks of a class per wave
+  static_assert((CI == 16 || CI == 32) && CO == 2 * CI && (BH / 2) * Wo == 64 &&
+                    BH * W == 256, "stage shapes");
+  __shared__ __attribute__((aligned(16))) float T[2][TR * TC * PP];
+  // halves handed over: [wave][2 classes][4 blocks][4][64 lanes]
+  __shared__ __attribute__((aligned(16))) float X[kSplit ? 4 * 2 * 4 * 4 * 64 : 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lq = lane >> 4, lm = lane & 15;
+  const int ipw = c.mchunk, groups = c.Bt / ipw, units = ipw * BANDS;
+  const int g = blockIdx.x / groups, b0 = (blockIdx.x - g * groups) * ipw;
+  const float* dyg = c.dy + ((long long)g * c.Bt + b0) * Wo * Wo * CO;
+  const float* Wg = c.Wk + (long long)g * c.sW;  // W [9 CI][CO]
+  const int nb = kSplit ? wave >> 1 : 0, half = kSplit ? wave & 1 : 0;
+  const int blk0 = kSplit ? 0 : wave;            // first block of a class
+  // unit u: image b0 + u / BANDS, band u % BANDS. The loads go out with
+  // clamped addresses and are zeroed (bit i of ok clear) only as they are
+  // stored to LDS, so that nothing waits for them before then.
+  auto gload = [&](int u, v4f(&tv)[TPT], unsigned& ok) __attribute__((always_inline)) {
+    const int bi = u / BANDS, oh0 = (u - bi * BANDS) * (BH / 2);
+    const float* dy = dyg + (long long)bi * Wo * Wo * CO;
+    ok = 0;
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int q = min(tid + kT * i, TQ - 1);
+      const int pix = q / (CO / 4), c4 = (q - pix * (CO / 4)) * 4;
+      const int tr = pix / TC, tc = pix - tr * TC, oh = oh0 + tr;
+      const bool in = oh < Wo && tc < Wo;
+      tv[i] = *(const v4f*)(dy + ((long long)(in ? oh : 0) * Wo + (in ? tc : 0)) * CO + c4);
+      ok |= (unsigned)in << i;
+    }
+  };
+  auto lstore = [&](float* Tb, const v4f(&tv)[TPT], unsigned ok) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int q = tid + kT * i;
+      if (q < TQ) {
+        const int pix = q / (CO / 4);
+        *(v4f*)&Tb[pix * PP + (q - pix * (CO / 4)) * 4] =
+            (ok >> i & 1) ? tv[i] : v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  };
+  // kDeep: two register sets, so unit u + 2's loads are issued before unit u
+  // computes (the 32 -> 64 form has no registers to spare for them)
+  constexpr bool kDeep = !kSplit;
+  v4f tv[TPT], tw[kDeep ? TPT : 1];
+  unsigned okv, okw = 0;
+  gload(0, tv, okv);
+  if constexpr (kDeep) {
+    if (units > 1) gload(1, tw, okw);
+  }
+  // B[k][n] = W[(tap, ci)][co], n = ci - 16 nb = l % 16, co of this wave's chunks
+  v4f Bf[9][NCW];
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+    for (int cw = 0; cw < NCW; ++cw)
+      Bf[tap][cw] = *(const v4f*)(Wg + ((long long)tap * CI + nb * 16 + lm) * CO +
+                                  (half * NCW + cw) * 16 + lq * 4);
+  lstore(T[0], tv, okv);
+  // every weight fragment in its registers before the loop (vmcnt(0)), so
+  // that no wait for them is left inside it
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  // unit u with its tile in T[u & 1]; tn holds (or receives) unit u + 1's
+  // loads, tf is free (kDeep)
+  auto step = [&](int u, v4f(&tf)[TPT], unsigned& okf, v4f(&tn)[TPT], unsigned& okn)
+      __attribute__((always_inline)) {
+    const bool more = u + 1 < units;  // uniform over the workgroup
+    if constexpr (kDeep) {
+      if (u + 2 < units) gload(u + 2, tf, okf);
+    } else if (more) {
+      gload(u + 1, tn, okn);
+    }
+    const float* Tb = T[u & 1];
+    const int bi = u / BANDS, band = u - bi * BANDS;
+    floatx4 acc[4][NBW];
+#pragma unroll
+    for (int jb = 0; jb < NBW; ++jb) {
+      // one block's operands in registers at a time
+      if (jb > 0) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int cls = 0; cls < 4; ++cls) acc[cls][jb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      // block row m = l % 16 is class position 16 (blk0 + jb) + m: dy tile
+      // row (16 / Wo) (blk0 + jb) + m / Wo, column m % Wo
+      const float* ap = Tb + (((16 / Wo) * (blk0 + jb) + lm / Wo) * TC + lm % Wo) * PP +
+                        half * NCW * 16 + lq * 4;
+#pragma unroll
+      for (int cw = 0; cw < NCW; ++cw) {
+        v4f av[2][2];
+#pragma unroll
+        for (int dr = 0; dr < 2; ++dr)
+#pragma unroll
+          for (int dc = 0; dc < 2; ++dc)
+            av[dr][dc] = *(const v4f*)(ap + (dr * TC + dc) * PP + cw * 16);
+#pragma unroll
+        for (int cls = 0; cls < 4; ++cls) {
+          const int ph = cls >> 1, pw = cls & 1;
+#pragma unroll
+          for (int th = 0; th < 1 + ph; ++th) {
+            const int kh = ph ? 2 * th : 1, dr = (ph + 1 - kh) / 2;
+#pragma unroll
+            for (int tw = 0; tw < 1 + pw; ++tw) {
+              const int kw = pw ? 2 * tw : 1, dc = (pw + 1 - kw) / 2, tap = kh * 3 + kw;
+#pragma unroll
+              for (int s = 0; s < 4; ++s)
+                acc[cls][jb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                    av[dr][dc][s], Bf[tap][cw][s], acc[cls][jb], 0, 0, 0);
+            }
+          }
+        }
+      }
+    }
+    if (more) lstore(T[(u + 1) & 1], tn, okn);
+    // lane holds C[m = 4 (l/16) + v][n = l % 16] of each block: class
+    // position 16 (blk0 + jb) + 4 (l/16) + v, i.e. a = (16 / Wo) (blk0 + jb) +
+    // 4 (l/16) / Wo and j = 4 (l/16) % Wo + v, at input row band BH + 2 a + ph
+    // and column 2 j + pw
+    float* dx = c.out + ((long long)g * c.Bt + b0 + bi) * W * W * CI +
+                (((long long)band * BH + 2 * ((16 / Wo) * blk0 + (4 * lq) / Wo)) * W +
+                 2 * ((4 * lq) % Wo)) * CI + nb * 16 + lm;
+    auto store = [&](int cls, int jb, const floatx4& r) __attribute__((always_inline)) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        dx[((2 * (16 / Wo) * jb + (cls >> 1)) * W + 2 * v + (cls & 1)) * CI] = r[v];
+    };
+    if constexpr (kSplit) {
+      // half h stores classes 2h, 2h + 1 and hands the other two to its
+      // partner wave (w ^ 1); the two partial sums are added once
+      float* mine = X + wave * (2 * 4 * 4 * 64);
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            mine[((k * 4 + jb) * 4 + v) * 64 + lane] = half ? acc[k][jb][v] : acc[2 + k][jb][v];
+        }
+      __syncthreads();
+      const float* other = X + (wave ^ 1) * (2 * 4 * 4 * 64);
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) {
+          floatx4 r;
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            r[v] = (half ? acc[2 + k][jb][v] : acc[k][jb][v]) +
+                   other[((k * 4 + jb) * 4 + v) * 64 + lane];
+          store(2 * half + k, jb, r);
+        }
+    } else {
+#pragma unroll
+      for (int cls = 0; cls < 4; ++cls) store(cls, 0, acc[cls][0]);
+    }
+    __syncthreads();
+  };
+  if constexpr (kDeep) {
+    for (int u = 0; u < units; u += 2) {
+      step(u, tv, okv, tw, okw);
+      if (u + 1 < units) step(u + 1, tw, okw, tv, okv);
+    }
+  } else {
+    for (int u = 0; u < units; ++u) step(u, tv, okv, tv, okv);
+  }
 }
 
 // The stem: a 3 x 3 stride-1 convolution of a 3-channel 32 x 32 image (read
@@ -856,27 +1019,92 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
   for (int pp = 0; pp < PPW; ++pp)
 #pragma unroll
     for (int i = 0; i < MB; ++i) acc[pp][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // this wave's pairs: the offset of the pair's tap in the input tile and of
+  // its column block in the gradient tile
+  int xoff[PPW], doff[PPW];
+#pragma unroll
+  for (int pp = 0; pp < PPW; ++pp) {
+    const int p = min(wave + 4 * pp, NP - 1);
+    const int tap = p / NB, nbk = p - tap * NB, kh = tap / 3, kw = tap - kh * 3;
+    xoff[pp] = (kh * TW + kw) * XP + lm;
+    doff[pp] = nbk * 16 + lm;
+  }
+  // Large accumulator sets (64 output channels: one wave per SIMD) read the
+  // operands of step kk + 1 from LDS while step kk's MFMAs run; the smaller
+  // ones keep several waves per SIMD and read each step's operands as they
+  // go (measured: the read-ahead costs them occupancy and 50% more time).
+  constexpr bool kBig = PPW * MB > 16;
   auto compute = [&](int buf) __attribute__((always_inline)) {
     const float* X = Xs + buf * XF;
     const float* D = Ds + buf * DF;
+    if constexpr (!kBig) {
 #pragma unroll 2
-    for (int kk = 0; kk < SP / 4; ++kk) {
+      for (int kk = 0; kk < SP / 4; ++kk) {
+        const int pos = kk * 4 + lq, orow = pos / WO, ocol = pos - orow * WO;
+#pragma unroll
+        for (int pp = 0; pp < PPW; ++pp) {
+          const int p = wave + 4 * pp;  // uniform over the wave
+          if (p < NP) {
+            const int tap = p / NB, nbk = p - tap * NB, kh = tap / 3, kw = tap - kh * 3;
+            const float bv = D[pos * DP + nbk * 16 + lm];
+            const float* xa = X + ((orow * STRIDE + kh) * TW + ocol * STRIDE + kw) * XP + lm;
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+              acc[pp][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i * 16], bv, acc[pp][i], 0, 0, 0);
+          }
+        }
+      }
+      return;
+    }
+    float av[2][PPW][MB], bv[2][PPW];
+    auto fetch = [&](int kk, int st) __attribute__((always_inline)) {
       const int pos = kk * 4 + lq, orow = pos / WO, ocol = pos - orow * WO;
+      const int xb = (orow * STRIDE * TW + ocol * STRIDE) * XP, db = pos * DP;
 #pragma unroll
       for (int pp = 0; pp < PPW; ++pp) {
-        const int p = wave + 4 * pp;  // uniform over the wave
-        if (p < NP) {
-          const int tap = p / NB, nbk = p - tap * NB, kh = tap / 3, kw = tap - kh * 3;
-          const float bv = D[pos * DP + nbk * 16 + lm];
-          const float* xa = X + ((orow * STRIDE + kh) * TW + ocol * STRIDE + kw) * XP + lm;
+        if (wave + 4 * pp < NP) {  // uniform over the wave
+          bv[st][pp] = D[db + doff[pp]];
+#pragma unroll
+          for (int i = 0; i < MB; ++i) av[st][pp][i] = X[xb + xoff[pp] + i * 16];
+        }
+      }
+    };
+    fetch(0, 0);
+#pragma unroll 2
+    for (int kk = 0; kk < SP / 4; ++kk) {
+      const int st = kk & 1;
+      if (kk + 1 < SP / 4) fetch(kk + 1, st ^ 1);
+#pragma unroll
+      for (int pp = 0; pp < PPW; ++pp) {
+        if (wave + 4 * pp < NP) {
 #pragma unroll
           for (int i = 0; i < MB; ++i)
-            acc[pp][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i * 16], bv, acc[pp][i], 0, 0, 0);
+            acc[pp][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[st][pp][i], bv[st][pp],
+                                                              acc[pp][i], 0, 0, 0);
         }
       }
     }
   };
-  if (nbd > 0) {
+  // The large accumulator sets keep one register set of prefetched tiles:
+  // band t + 1's loads are in flight while band t computes, then go to the
+  // LDS buffer band t - 1 released at the last barrier.
+  if constexpr (kBig) {
+    if (nbd > 0) {
+      v4f xr[XPT], dr[DPT];
+      unsigned ok;
+      gload(b0, xr, dr, ok);
+      lstore(0, xr, dr, ok);
+      __syncthreads();
+      for (int t = 0; t < nbd; ++t) {
+        const bool more = t + 1 < nbd;  // uniform over the workgroup
+        if (more) gload(b0 + t + 1, xr, dr, ok);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(t & 1);
+        if (more) lstore((t + 1) & 1, xr, dr, ok);
+        __syncthreads();
+      }
+    }
+  } else if (nbd > 0) {
     v4f xr0[XPT], xr1[XPT], dr0[DPT], dr1[DPT];
     unsigned ok0, ok1;
     auto band = [&](int t) __attribute__((always_inline)) { return b0 + min(t, nbd - 1); };
@@ -1283,9 +1511,19 @@ static bool rows_shape(const ConvGeom& q, int mode) {
   const int Cr = mode == CONV_FWD ? q.Cin : q.Cout;
   const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
   return Cr % 16 == 0 && (Ng == 16 || Ng == 32 || Ng == 64) &&
-         (q.stride == 1 || q.stride == 2) && ((uintptr_t)q.Wk & 15) == 0 && (q.sW % 4 == 0) &&
+         (q.stride == 1 || (q.stride == 2 && mode == CONV_FWD)) && ((uintptr_t)q.Wk & 15) == 0 &&
+         (q.sW % 4 == 0) &&
          (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0 : ((uintptr_t)q.dy & 15) == 0) &&
          (mode == CONV_DGRAD || q.rowmap || q.sx % 4 == 0);
+}
+
+// Input gradients of the stride-2 convolutions: 16 -> 32 channels on 32-wide
+// images and 32 -> 64 on 16-wide ones.
+static bool dgrad_s2_shape(const ConvGeom& q) {
+  return q.stride == 2 && q.H == q.W && q.H == 2 * q.Ho && q.W == 2 * q.Wo &&
+         ((q.Cin == 16 && q.Cout == 32 && q.W == 32) ||
+          (q.Cin == 32 && q.Cout == 64 && q.W == 16)) &&
+         ((uintptr_t)q.Wk & 15) == 0 && q.sW % 4 == 0 && ((uintptr_t)q.dy & 15) == 0;
 }
 
 // Halo-tile kernel: the first stage's 16 -> 16 stride-1 convolutions.
@@ -1411,6 +1649,22 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
       hipLaunchKernelGGL(k_conv_stem_fwd, dim3((unsigned)nb), dim3(kT), 0, st, c);
       return hipGetLastError();
     }
+    if (mode == CONV_DGRAD && q.stride == 2) {
+      if (!dgrad_s2_shape(q)) return hipErrorInvalidValue;  // no kernel for this shape
+      // images per workgroup: up to 4 (the weights are loaded once for all
+      // of them) while at least 512 workgroups remain
+      c.mchunk = 1;
+      while (c.mchunk < 4 && q.Bt % (2 * c.mchunk) == 0 &&
+             (long long)q.G * (q.Bt / (2 * c.mchunk)) >= 512)
+        c.mchunk *= 2;
+      const long long nb = (long long)q.G * (q.Bt / c.mchunk);
+      if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
+      if (q.Cin == 16)
+        hipLaunchKernelGGL((k_conv_dgrad_s2<16, 32, 32>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+      else
+        hipLaunchKernelGGL((k_conv_dgrad_s2<32, 64, 16>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+      return hipGetLastError();
+    }
     if (halo) {
       const long long nb = (long long)q.G * q.Bt * (q.H / 8);
       if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -1427,15 +1681,6 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
         if (Ng == 16) LSGD_ROWS(CONV_FWD, 16);
         else if (Ng == 32) LSGD_ROWS(CONV_FWD, 32);
         else LSGD_ROWS(CONV_FWD, 64);
-      } else if (q.stride == 2 && q.H == 2 * q.Ho && q.W == 2 * q.Wo &&
-                 ((long long)q.Bt * q.Ho * q.Wo) % 256 == 0) {
-        // input gradient of a stride-2 convolution by parity class
-#define LSGD_ROWS2(NB)                                                                 \
-  hipLaunchKernelGGL((k_conv_rows<CONV_DGRAD, NB, true>), dim3((unsigned)rt), dim3(kT), 0, st, c)
-        if (Ng == 16) LSGD_ROWS2(16);
-        else if (Ng == 32) LSGD_ROWS2(32);
-        else LSGD_ROWS2(64);
-#undef LSGD_ROWS2
       } else {
         if (Ng == 16) LSGD_ROWS(CONV_DGRAD, 16);
         else if (Ng == 32) LSGD_ROWS(CONV_DGRAD, 32);
