@@ -960,7 +960,8 @@ def test_mlp_512_signsgd_first_round_full_size(img_data):
 
 def test_wide_bf16_first_round_two_replicas_full_size(img_data):
     """Workload 4 at its real shape (K=64, B_loc=64, H=8, bf16 operands):
-    replicas 0 and 63 through the first round's local steps."""
+    replicas 0 and 63 through the first round's local steps, then the
+    synchronised model of all 64 replicas."""
     w = wk.get("wide_mlp_2048_bf16")
     X, y = img_data
     w0 = wk.initial_weights(w)
@@ -978,3 +979,24 @@ def test_wide_bf16_first_round_two_replicas_full_size(img_data):
         e = normwise(reps.read_params(k).cpu().numpy(), st.W[k])
         print(f"wide bf16 replica {k} params normwise error {e:.3e}", flush=True)
         assert e <= 2e-3
+    # the synchronised model (eq. 2) against the oracle's, at the seeded
+    # sample positions tests/golden/make_round_models.py stored (oracle
+    # only), with a bar below the distance of the oracle's run without any
+    # bf16 rounding (same file): a path that skipped the roundings would fail
+    import json
+    import os
+    here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+    with open(os.path.join(here, "round1_wide_mlp_2048_bf16.json")) as f:
+        gold = json.load(f)
+    z = np.load(os.path.join(here, "round1_wide_mlp_2048_bf16.npz"))
+    reps.average()
+    wbar = reps.read_params(-1).cpu().numpy()
+    err = float(np.max(np.abs(wbar[z["positions"]] - z["values"])) / gold["max_abs_model"])
+    bar = NR_RATIO * gold["no_rounding_sampled_normwise"]
+    lerr = float(np.max(rel(got.mean(axis=1), np.asarray(gold["round1_step_mean_loss"]))))
+    lbar = NR_RATIO * gold["no_rounding_step_loss_rel"]
+    print(f"wide bf16 averaged model {err:.3e} (bar {bar:.3e}; oracle without rounding "
+          f"{gold['no_rounding_sampled_normwise']:.3e}), step losses {lerr:.3e} "
+          f"(bar {lbar:.3e})", flush=True)
+    assert err <= bar
+    assert lerr <= lbar
