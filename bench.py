@@ -252,8 +252,8 @@ TAG_KERNELS = {
     "wgrad_update": ("gemm_f32_sgd_ws<",),
     "average": ("k_average4<",),
     "conv_fwd": ("k_conv_stem_fwd", "k_conv_halo16<0>", "k_conv_rows<0,"),
-    "conv_dgrad": ("k_conv_halo16<1>", "k_conv_rows<1,"),
-    "conv_wgrad": ("k_conv_wgrad_stem", "k_conv_wgrad_halo16", "k_conv_wgrad_rows<"),
+    "conv_dgrad": ("k_conv_halo16<1>", "k_conv_rows<1,", "k_conv_dgrad_s2<"),
+    "conv_wgrad": ("k_conv_wgrad_stem", "k_conv_wgrad_halo16", "k_conv_wgrad_band<"),
     "bn_bwd": ("k_bn_partial4", "k_bn_finalize_wg", "k_bn_bwd_apply4"),
     "bn_apply": ("k_bn_apply4<",),
 }
@@ -280,8 +280,10 @@ def _counter_rows(path: str, counter: str) -> list:
 
 def _short(name: str) -> str:
     """A kernel's name without its namespaces and parameter list."""
-    name = name.split("(")[0] if not name.startswith("void ") else name[5:].split("(")[0]
-    return name.replace("lsgd::(anonymous namespace)::", "").replace("lsgd::", "")
+    name = name.replace("lsgd::(anonymous namespace)::", "").replace("lsgd::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    return name.split("(")[0]
 
 
 def _family_bytes(rows, prefixes) -> tuple:
@@ -495,8 +497,10 @@ def main():
 
     # Warmup. The rounds after the first bracket every launch with HIP events
     # (per-kernel breakdown, and the dominant kernel); the timed rounds then
-    # bracket two of the dominant kernel's launches per round (each bracket
-    # costs the stream some microseconds), on the stream it is launched on.
+    # bracket a sample of the dominant kernel's launches (two per round for a
+    # kernel launched once per step, every (n + 1)-th for a family of n
+    # launches per step; each bracket costs the stream some microseconds), on
+    # the stream it is launched on.
     timing = not args.no_kernel_timing and args.warmup >= 1
     prof_rounds = 0
     w0_ev, w1_ev = (torch.cuda.Event(enable_timing=True) for _ in range(2))
@@ -525,8 +529,17 @@ def main():
         per_round = {t: ms / prof_rounds for t, (n, ms) in rep.items()}
         dom = max(per_round, key=per_round.get)
         per_round_launches = rep[dom][0] // prof_rounds
-        reps.profile_select(dom, every=max(1, per_round_launches // 2) if sparse == 1
-                            else per_round_launches * sparse)
+        per_step = max(1, per_round_launches // H)
+        if sparse > 1:
+            every = per_round_launches * sparse
+        elif per_step > 1:
+            # a family of launches per local step (one per layer): every
+            # (n + 1)-th cycles through all of them, so the sampled average
+            # is the family's
+            every = per_step + 1
+        else:
+            every = max(1, per_round_launches // 2)
+        reps.profile_select(dom, every=every)
         reps.profile(True)
     torch.cuda.synchronize()
     # an event every `sparse` round boundaries: the total and the per-round
