@@ -904,17 +904,6 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
     out[e] = ((red[e] + red[9 * C * C + e]) + red[2 * 9 * C * C + e]) + red[3 * 9 * C * C + e];
 }
 
-// Weight gradient of a convolution with 16 / 32 / 64 channels in and out:
-// workgroup (replica g, tap t, split s) forms the partial
-//   dW[t][ci][co] = sum over output positions p of chunk s of
-//                   x(p shifted by tap t)[ci] * dy[p][co]
-// for all CI x CO channels of the tap. Slabs of 64 consecutive positions
-// (64 divides H_o W_o, so a slab lies in one image) go through LDS with
-// float4 loads of whole channel rows (padding taps masked to zero); each of
-// the 4 waves takes 16 positions of the slab and accumulates the full
-// CI x CO block on v_mfma_f32_16x16x4f32. The four waves' sums are added in
-// wave order at the end. Partials land in [S][G][9 CI][CO] as for the GEMM
-// form, reduced over s by k_conv_wupdate.
 // Weight gradient of the stage-2 and stage-3 convolutions (output rows of
 // WO = 16 or 8 positions) from band tiles. A band is SP = 64 output positions,
 // 64 / WO whole output rows of one image; per band the output gradients
