@@ -816,10 +816,13 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
 // band's output gradients go to LDS, and each wave takes 64 of the 256
 // positions and accumulates all nine taps' 16 x 16 blocks
 //   dW[tap][ci][co] += x(p shifted by tap)[ci] * dy[p][co].
-// The four waves' sums are added in wave order; the partial lands in
-// [S][G][144][16] for k_conv_wupdate.
+// The next band's tiles are loaded into registers while a band computes.
+// A lane reads channel l % 16 of position (l / 16), so unpadded 16-float
+// pixel rows are read without bank conflicts, and the LDS (38 KB) leaves
+// room for four workgroups per CU. The four waves' sums are added in wave
+// order; the partial lands in [S][G][144][16] for k_conv_wupdate.
 __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
-  constexpr int C = 16, CP = C + 4;
+  constexpr int C = 16, CP = C;
   constexpr int W = 32, BH = 8, TW = W + 2, TH = BH + 2;
   constexpr int TQ = TH * TW * (C / 4), DQ = BH * W * (C / 4);
   constexpr int TPT = (TQ + kT - 1) / kT, DPT = DQ / kT;
@@ -843,12 +846,15 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
   const bool bnin = c.bn_mu != nullptr;
   BnIn4 bp{};
   if (bnin) bp = bn_in_params(c, g, (threadIdx.x & 3) * 4);
-  for (int bd = bb; bd < be; ++bd) {
+  // band bd's tiles into registers: clamped addresses, padding marked in
+  // okm and zeroed at the LDS store
+  v4f tv[TPT], dv[DPT];
+  unsigned okm = 0;
+  auto gload = [&](int bd) __attribute__((always_inline)) {
     const int b = bd / bpi, h0 = (bd - b * bpi) * BH;
     const float* xs = c.x + (long long)g * c.sx + (long long)b * H * W * C;
     const float* ds = c.dy + (((long long)g * c.Bt + b) * H + h0) * W * C;
-    v4f tv[TPT], dv[DPT];
-    unsigned okm = 0;
+    okm = 0;
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       const int q = min((int)threadIdx.x + kT * i, TQ - 1);
@@ -857,17 +863,19 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
       const int ih = h0 - 1 + tr, iw = tc - 1;
       const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
       tv[i] = *(const v4f*)(xs + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
-      if (!ok) tv[i] = v4f{0.f, 0.f, 0.f, 0.f};
       okm |= (unsigned)ok << i;
     }
 #pragma unroll
     for (int i = 0; i < DPT; ++i) dv[i] = *(const v4f*)(ds + 4 * ((int)threadIdx.x + kT * i));
+  };
+  if (bb < be) gload(bb);
+  for (int bd = bb; bd < be; ++bd) {
     __syncthreads();  // the previous band's tiles are no longer read
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       const int q = (int)threadIdx.x + kT * i;
-      v4f v = tv[i];
-      if (bnin) v = (okm >> i & 1) ? bn_in(bp, v) : v4f{0.f, 0.f, 0.f, 0.f};
+      const bool in = okm >> i & 1;
+      const v4f v = !in ? v4f{0.f, 0.f, 0.f, 0.f} : bnin ? bn_in(bp, tv[i]) : tv[i];
       if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = v;
     }
 #pragma unroll
@@ -876,7 +884,8 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
       *(v4f*)&Dsh[(q >> 2) * CP + (q & 3) * 4] = dv[i];
     }
     __syncthreads();
-#pragma unroll 4
+    if (bd + 1 < be) gload(bd + 1);  // uniform over the workgroup
+#pragma unroll 2
     for (int ks = 0; ks < 16; ++ks) {
       // position of this lane's k: row 2w + ks/8, column 4 (ks%8) + lq
       const int pr = 2 * wave + (ks >> 3), pc = 4 * (ks & 7) + lq;
@@ -891,7 +900,7 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
   }
   // waves in order; block t register v of lane l: dW[t][4 (l/16) + v][l%16]
   __syncthreads();
-  float* red = lds;  // 4 x 144 x 16 floats fit the tile space (6800 + 5120)
+  float* red = lds;  // 4 x 144 x 16 floats fit the tile space (5440 + 4096)
   static_assert(4 * 9 * C * C <= TH * TW * CP + BH * W * CP, "reduction space");
 #pragma unroll
   for (int t = 0; t < 9; ++t)
