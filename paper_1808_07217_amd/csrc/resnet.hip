@@ -125,7 +125,9 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   constexpr int RPT = BM * BK / 4 / kT;           // A float4 per thread (4)
   constexpr int BQ = BK * BN / 4;                 // B float4 per slab
   __shared__ __attribute__((aligned(16))) float As[2][BM][PK];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + 4];
+  // B rows 16 floats apart modulo 64: the four k rows a B read spans fall
+  // in disjoint banks
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + 16];
 
   const int Cr = MODE == CONV_FWD ? c.Cin : c.Cout;  // reduction channels
   const int HWo = MODE == CONV_FWD ? c.Ho * c.Wo : c.H * c.W;
