@@ -674,15 +674,18 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_stem(ConvArgs c) {
 }
 
 // Stride-1 convolution with 16 channels in and out on 32-wide images (the
-// first stage): workgroup (g, b, band) computes 8 output rows x 32 columns x
-// 16 channels. The input rows h0-1 .. h0+8 (zero-padded) and the 144 x 16
-// weights go to LDS once and all 9 taps read shifted views of the tile, so
-// each input value is fetched from memory about 1.25 times rather than once
-// per tap. Input gradient: the same convolution applied to dy with the
-// kernel flipped -- tap (kh, kw) uses weight row (2-kh, 2-kw) -- and the
-// channels swapped, W[(2-kh, 2-kw, ci)][co] staged as [(kh, kw, co)][ci]. Wave w owns output rows
-// h0 + 2w, h0 + 2w + 1 as four 16 x 16 blocks of v_mfma_f32_16x16x4f32.
-template <int MODE>
+// first stage): workgroup (g, b, band group) computes NBW bands of 8 output
+// rows x 32 columns x 16 channels of image b, one after the other. The
+// 144 x 16 weights go to LDS once per workgroup; per band the input rows
+// h0-1 .. h0+8 (zero-padded) go to LDS and all 9 taps read shifted views of
+// the tile, so each input value is fetched from memory about 1.25 times
+// rather than once per tap, and the next band's rows are loaded into
+// registers while a band computes. Input gradient: the same convolution
+// applied to dy with the kernel flipped -- tap (kh, kw) uses weight row
+// (2-kh, 2-kw) -- and the channels swapped, W[(2-kh, 2-kw, ci)][co] staged
+// as [(kh, kw, co)][ci]. Wave w owns output rows h0 + 2w, h0 + 2w + 1 as
+// four 16 x 16 blocks of v_mfma_f32_16x16x4f32.
+template <int MODE, int NBW>
 __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   constexpr int C = 16, CP = C + 4;          // 80-byte pixel pitch in LDS
   constexpr int W = 32, BH = 8;
@@ -692,12 +695,11 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   constexpr int TPT = (TQ + kT - 1) / kT, WPT = (WQ + kT - 1) / kT;
   __shared__ __attribute__((aligned(16))) float T[TH * TW * CP];
   __shared__ __attribute__((aligned(16))) float Ws[9 * C * CP];
-  const int H = c.H, bands = H / BH;
+  const int H = c.H, bands = H / BH, groups = bands / NBW;
   int l = blockIdx.x;
-  const int band = l % bands;
-  l /= bands;
+  const int grp = l % groups;
+  l /= groups;
   const int b = l % c.Bt, g = l / c.Bt;
-  const int h0 = band * BH;
   const float* src = MODE == CONV_FWD
                          ? c.x + (long long)g * c.sx + (long long)b * H * W * C
                          : c.dy + ((long long)g * c.Bt + b) * H * W * C;
@@ -707,20 +709,34 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   const bool bnin = MODE == CONV_FWD && c.bn_mu != nullptr;
   BnIn4 bp{};
   if (bnin) bp = bn_in_params(c, g, (threadIdx.x & 3) * 4);
-  // every load issued before the LDS stores (clamped addresses, zero-masked)
-  v4f tv[TPT], wv[WPT];
+  // a band's input rows into registers: clamped addresses, the padding
+  // marked in okm and zeroed at the LDS store
+  v4f tv[TPT];
   unsigned okm = 0;
+  auto gload = [&](int h0) __attribute__((always_inline)) {
+    okm = 0;
 #pragma unroll
-  for (int i = 0; i < TPT; ++i) {
-    const int q = min((int)threadIdx.x + kT * i, TQ - 1);
-    const int pix = q >> 2, c4 = (q & 3) * 4;
-    const int tr = pix / TW, tc = pix - tr * TW;
-    const int ih = h0 - 1 + tr, iw = tc - 1;
-    const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
-    tv[i] = *(const v4f*)(src + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
-    if (!ok) tv[i] = v4f{0.f, 0.f, 0.f, 0.f};
-    okm |= (unsigned)ok << i;
-  }
+    for (int i = 0; i < TPT; ++i) {
+      const int q = min((int)threadIdx.x + kT * i, TQ - 1);
+      const int pix = q >> 2, c4 = (q & 3) * 4;
+      const int tr = pix / TW, tc = pix - tr * TW;
+      const int ih = h0 - 1 + tr, iw = tc - 1;
+      const bool ok = ih >= 0 && ih < H && iw >= 0 && iw < W;
+      tv[i] = *(const v4f*)(src + ((long long)(ok ? ih : 0) * W + (ok ? iw : 0)) * C + c4);
+      okm |= (unsigned)ok << i;
+    }
+  };
+  auto lstore = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      const int q = (int)threadIdx.x + kT * i;
+      const bool in = okm >> i & 1;
+      const v4f v = !in ? v4f{0.f, 0.f, 0.f, 0.f} : bnin ? bn_in(bp, tv[i]) : tv[i];
+      if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = v;
+    }
+  };
+  gload(grp * NBW * BH);
+  v4f wv[WPT];
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
     // forward: Ws row (tap, ci) is W row (tap, ci); input gradient: Ws row
@@ -732,13 +748,7 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
     const int srow = MODE == CONV_FWD ? row : (8 - tap) * C + r;
     wv[i] = *(const v4f*)(Wg + (long long)srow * C + c4);
   }
-#pragma unroll
-  for (int i = 0; i < TPT; ++i) {
-    const int q = (int)threadIdx.x + kT * i;
-    v4f v = tv[i];
-    if (bnin) v = (okm >> i & 1) ? bn_in(bp, v) : v4f{0.f, 0.f, 0.f, 0.f};  // padding stays 0
-    if (q < TQ) *(v4f*)&T[(q >> 2) * CP + (q & 3) * 4] = v;
-  }
+  lstore();
 #pragma unroll
   for (int i = 0; i < WPT; ++i) {
     const int q = (int)threadIdx.x + kT * i;
@@ -755,59 +765,68 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int lq = lane >> 4, lm = lane & 15;
-  floatx4 acc[4];
+  for (int u = 0; u < NBW; ++u) {
+    const int band = grp * NBW + u, h0 = band * BH;
+    if (u + 1 < NBW) gload(h0 + BH);  // the next band, in flight during this one
+    floatx4 acc[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 4; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int tap = 0; tap < 9; ++tap) {
-    const int kh = tap / 3, kw = tap - kh * 3;
+    for (int tap = 0; tap < 9; ++tap) {
+      const int kh = tap / 3, kw = tap - kh * 3;
 #pragma unroll
-    for (int cq = 0; cq < 4; ++cq) {
-      const int ci = cq * 4 + lq;
-      const float bv = Ws[(tap * C + ci) * CP + lm];
+      for (int cq = 0; cq < 4; ++cq) {
+        const int ci = cq * 4 + lq;
+        const float bv = Ws[(tap * C + ci) * CP + lm];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        // output (row 2w + i/2, col 16 (i%2) + lm) reads tile (row + kh, col + kw)
-        const int tr = 2 * wave + (i >> 1) + kh, tc = 16 * (i & 1) + lm + kw;
-        const float av = T[(tr * TW + tc) * CP + ci];
-        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i], 0, 0, 0);
+        for (int i = 0; i < 4; ++i) {
+          // output (row 2w + i/2, col 16 (i%2) + lm) reads tile (row + kh, col + kw)
+          const int tr = 2 * wave + (i >> 1) + kh, tc = 16 * (i & 1) + lm + kw;
+          const float av = T[(tr * TW + tc) * CP + ci];
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i], 0, 0, 0);
+        }
       }
     }
-  }
-  float* out = c.out + ((long long)g * c.Bt + b) * H * W * C;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
-      out[((long long)row * W + col) * C + lm] = acc[i][v];
-    }
-  if (MODE == CONV_FWD && c.stats) {
-    // BN statistics of the band (8 x 32 = 256 positions: one chunk): each
-    // wave's two rows by a lane butterfly, the four waves in order
-    __shared__ double red[4][C][2];
-    double s0 = 0.0, s1 = 0.0;
+    float* out = c.out + ((long long)g * c.Bt + b) * H * W * C;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const double y = (double)acc[i][v];
-        s0 += y;
-        s1 += y * y;
+        const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
+        out[((long long)row * W + col) * C + lm] = acc[i][v];
       }
-    stats_butterfly(s0, s1, 2, 4);
-    if (lq == 0) {
-      red[wave][lm][0] = s0;
-      red[wave][lm][1] = s1;
-    }
-    __syncthreads();
-    if (threadIdx.x < C) {
-      const int t = threadIdx.x;
-      const long long q = (long long)b * bands + band;
-      double* d = c.stats + (((long long)g * c.Bt * bands + q) * C + t) * 2;
+    if (MODE == CONV_FWD && c.stats) {
+      // BN statistics of the band (8 x 32 = 256 positions: one chunk): each
+      // wave's two rows by a lane butterfly, the four waves in order
+      __shared__ double red[4][C][2];
+      double s0 = 0.0, s1 = 0.0;
 #pragma unroll
-      for (int e = 0; e < 2; ++e)
-        d[e] = ((red[0][t][e] + red[1][t][e]) + red[2][t][e]) + red[3][t][e];
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const double y = (double)acc[i][v];
+          s0 += y;
+          s1 += y * y;
+        }
+      stats_butterfly(s0, s1, 2, 4);
+      if (lq == 0) {
+        red[wave][lm][0] = s0;
+        red[wave][lm][1] = s1;
+      }
+      __syncthreads();
+      if (threadIdx.x < C) {
+        const int t = threadIdx.x;
+        const long long q = (long long)b * bands + band;
+        double* d = c.stats + (((long long)g * c.Bt * bands + q) * C + t) * 2;
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+          d[e] = ((red[0][t][e] + red[1][t][e]) + red[2][t][e]) + red[3][t][e];
+      }
+    }
+    if (u + 1 < NBW) {
+      __syncthreads();  // every wave is done with this band's tile (and red)
+      lstore();
+      __syncthreads();
     }
   }
 }
@@ -1527,9 +1546,13 @@ static bool dgrad_s2_shape(const ConvGeom& q) {
 }
 
 // Halo-tile kernel: the first stage's 16 -> 16 stride-1 convolutions.
+// bands of 8 rows per workgroup of k_conv_halo16: the forward (with its
+// statistics epilogue) one, the input gradient several
+constexpr int kHaloBandsFwd = 1, kHaloBandsDgrad = 4;
 static bool halo_shape(const ConvGeom& q, int mode) {
   return q.Cin == 16 && q.Cout == 16 && q.stride == 1 && q.W == 32 && q.Wo == 32 &&
-         q.H == q.Ho && q.H % 8 == 0 && !q.rowmap && ((uintptr_t)q.Wk & 15) == 0 &&
+         q.H == q.Ho && q.H % (8 * (mode == CONV_FWD ? kHaloBandsFwd : kHaloBandsDgrad)) == 0 &&
+         !q.rowmap && ((uintptr_t)q.Wk & 15) == 0 &&
          q.sW % 4 == 0 && ((uintptr_t)(mode == CONV_FWD ? q.x : q.dy) & 15) == 0 &&
          (mode == CONV_DGRAD || q.sx % 4 == 0);
 }
@@ -1666,12 +1689,15 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
       return hipGetLastError();
     }
     if (halo) {
-      const long long nb = (long long)q.G * q.Bt * (q.H / 8);
+      const long long nb = (long long)q.G * q.Bt *
+                           (q.H / 8 / (mode == CONV_FWD ? kHaloBandsFwd : kHaloBandsDgrad));
       if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
       if (mode == CONV_FWD)
-        hipLaunchKernelGGL((k_conv_halo16<CONV_FWD>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+        hipLaunchKernelGGL((k_conv_halo16<CONV_FWD, kHaloBandsFwd>), dim3((unsigned)nb),
+                           dim3(kT), 0, st, c);
       else
-        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad>), dim3((unsigned)nb),
+                           dim3(kT), 0, st, c);
     } else if (rows) {
       const long long rt = (long long)((Mg + 255) / 256) * q.G;
       if (rt > 0x7fffffffLL) return hipErrorInvalidValue;
