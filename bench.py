@@ -334,7 +334,10 @@ def write_traffic(pmc_dir: str, w, tag: str) -> dict:
 def sweep():
     """Achieved bandwidth of the two HBM-bound building blocks against the
     working-set size. Sets up to ~256 MB can stay in the 256 MB Infinity
-    Cache between repetitions, so only the larger sizes measure HBM itself."""
+    Cache between repetitions, so only the larger sizes measure HBM itself.
+    For reference, the same working sets through kernels this library did
+    not write: torch's copy_ (read and write n floats) and add (two reads,
+    one write), timed the same way."""
     import torch
     from paper_1808_07217_amd import lsgd as L
     dev = torch.device("cuda", 0)
@@ -368,7 +371,26 @@ def sweep():
         torch.cuda.synchronize()
         t_upd = e0.elapsed_time(e1) / reps / 1e3
         upd_bytes = 20 * n                        # read W, U, G; write W, U
+
+        def ref(fn, nb):
+            fn()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / reps / 1e3
+            return {"us": round(t * 1e6, 2), "GB/s": round(nb / t / 1e9, 1),
+                    "frac_hbm": round(nb / t / 1e9 / PEAK_HBM_GBS, 4)}
+        torch_add = ref(lambda: torch.add(Wt, Gt, out=Ut), 12 * n)
         del Wt, Ut, Gt
+        torch.cuda.empty_cache()
+        nc = nbytes // (2 * 4) // 64 * 64          # source and copy of nc floats
+        src = torch.randn(nc, device=dev)
+        dst = torch.empty_like(src)
+        torch_copy = ref(lambda: dst.copy_(src), 8 * nc)
+        del src, dst
         torch.cuda.empty_cache()
         print(json.dumps({
             "working_set_MB": mb,
@@ -378,6 +400,7 @@ def sweep():
             "sgd_update": {"n": n, "us": round(t_upd * 1e6, 2),
                            "GB/s": round(upd_bytes / t_upd / 1e9, 1),
                            "frac_hbm": round(upd_bytes / t_upd / 1e9 / PEAK_HBM_GBS, 4)},
+            "torch_copy": torch_copy, "torch_add": torch_add,
         }), flush=True)
 
 
