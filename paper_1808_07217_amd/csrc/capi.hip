@@ -786,12 +786,16 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                              F(r.dfeat), gb[0], s));
   int cur = 0;  // gb[cur] holds the gradient of the current block output
   // BN backward (coefficients, gamma/beta update, input gradient into dy)
-  auto bn_bwd = [&](int i, const float* gup, const float* maskv, float* dy) {
+  // (fused_nchunk > 0: the sums are in bnpart already, from the input
+  // gradient that produced gup)
+  auto bn_bwd = [&](int i, const float* gup, const float* maskv, float* dy,
+                    int fused_nchunk) {
     const ConvSpec& q = r.cv[i];
     return lsgd::launch_bn_backward(F(q.y), gup, maskv, K, rows(i), q.Cout, bnpart,
                                     mu + (size_t)i * K * 64, inv + (size_t)i * K * 64,
                                     coef, W + q.offG, W + q.offB, U + q.offG,
-                                    U + q.offB, Ps, lr, cf.momentum, upd_mode(cf), dy, s);
+                                    U + q.offB, Ps, lr, cf.momentum, upd_mode(cf), dy,
+                                    fused_nchunk, s);
   };
   // weight gradient of conv i from its input x and output gradient dy into
   // per-split partials, then their fixed-order sum and the update (after
@@ -818,11 +822,25 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                           s));
     return LSGD_OK;
   };
-  // input gradient of conv i (reads the old weight, before its update)
-  auto dgrad = [&](int i, const float* dy, float* dx) -> lsgd_status {
+  // input gradient of conv i (reads the old weight, before its update).
+  // Where the kernel takes epilogues (*fused set): with sc_dh, sc_h the
+  // identity shortcut's share of the block-output gradient goes into dx; with
+  // bs_layer >= 0 the backward sums of BN layer bs_layer (whose activation
+  // gradient dx is) go to bnpart.
+  auto dgrad = [&](int i, const float* dy, float* dx, const float* sc_dh, const float* sc_h,
+                   int bs_layer, bool* fused) -> lsgd_status {
     lsgd::ConvGeom g = geom(i);
     g.dy = dy;
     g.out = dx;
+    *fused = (sc_dh || bs_layer >= 0) && lsgd::conv_dgrad_epilogues(g);
+    if (*fused && sc_dh) {
+      g.sc_dh = sc_dh;
+      g.sc_h = sc_h;
+    } else if (*fused) {
+      g.bs_y = F(r.cv[bs_layer].y);
+      g.bs_part = bnpart;
+      bn_input(g, bs_layer);
+    }
     LSGD_LAUNCH(c, "conv_dgrad", lsgd::launch_conv(lsgd::CONV_DGRAD_MODE, g, s));
     return LSGD_OK;
   };
@@ -833,21 +851,26 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     const float* h_in = F(r.cv[ia - 1].act);
     const int nxt = cur == 0 ? 3 : 0;
     // second convolution: its output went through the shortcut add and ReLU
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1]));
-    if (lsgd_status st = dgrad(ib, gb[1], gb[2])) return st;
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1], 0));
+    bool sums_fused = false, sc_fused = false;
+    if (lsgd_status st = dgrad(ib, gb[1], gb[2], nullptr, nullptr, ia, &sums_fused)) return st;
     if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), gb[1], ia)) return st;
     // first convolution: ReLU'd BN output, the mask recomputed from its input
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[1]));
-    if (lsgd_status st = dgrad(ia, gb[1], gb[nxt])) return st;
-    if (lsgd_status st = wgrad(ia, h_in, gb[1], -1)) return st;
-    // the shortcut's share of the block-output gradient
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[1], sums_fused ? rows(ia) / 256 : 0));
+    // the block-input gradient: the convolution path, and the shortcut's share
+    // of the block-output gradient (in the input gradient's epilogue where it can)
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
-    LSGD_LAUNCH(c, "shortcut_bwd",
-                lsgd::launch_shortcut_grad(gb[nxt], gb[cur], F(r.cv[ib].act), K, B,
-                                           qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
+    if (lsgd_status st = dgrad(ia, gb[1], gb[nxt], mode == 1 ? gb[cur] : nullptr,
+                               F(r.cv[ib].act), -1, &sc_fused))
+      return st;
+    if (lsgd_status st = wgrad(ia, h_in, gb[1], -1)) return st;
+    if (!sc_fused)
+      LSGD_LAUNCH(c, "shortcut_bwd",
+                  lsgd::launch_shortcut_grad(gb[nxt], gb[cur], F(r.cv[ib].act), K, B,
+                                             qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
     cur = nxt;
   }
-  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1]));
+  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1], 0));
   if (lsgd_status st = wgrad(0, nullptr, gb[1], -1)) return st;
   c->step += 1;
   return LSGD_OK;

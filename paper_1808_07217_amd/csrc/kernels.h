@@ -163,8 +163,24 @@ struct ConvGeom {
   const float* bn_g;
   const float* bn_b;
   long long bn_sP;
+  // input gradient, where conv_dgrad_epilogues(q) (nullptr: none; at most one
+  // of the two per launch):
+  //  * sc_dh, sc_h: the block output's gradient and activation (same shape as
+  //    dx, identity shortcut): dx gains sc_dh where sc_h > 0;
+  //  * bs_part: dx is the gradient of a BN-ReLU's output whose pre-BN values
+  //    are bs_y (same shape) and whose statistics and parameters come in
+  //    bn_* (as above): the BN backward sums (sum dz, sum dz x^ with dz = dx
+  //    where gamma (y - mu) inv + beta > 0 and x^ = (y - mu) inv) are written
+  //    per 256-row chunk, [G][R/256][Cin][2] doubles, for
+  //    launch_bn_backward's fused_nchunk
+  const float* sc_dh;
+  const float* sc_h;
+  const float* bs_y;
+  double* bs_part;
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
+// Whether the input-gradient launch of q takes the sc_* / bs_* epilogues.
+bool conv_dgrad_epilogues(const ConvGeom& q);
 int conv_wgrad_splits(int Bt, int Ho, int Wo);
 // Whether the forward convolution of q writes its output's BN statistics
 // (per 256-row chunk, [G][R/256][Cout][2] doubles: sum, sum of squares) when
@@ -192,11 +208,13 @@ hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
 // by maskv > 0 (the post-ReLU activation) or, with maskv null, by the sign of
 // the recomputed pre-ReLU BN output (a BN-ReLU with no shortcut add). coef
 // holds 5 floats per (replica, channel).
+// fused_nchunk > 0: the sums are already in part (fused_nchunk chunks per
+// replica, from an input-gradient epilogue) and are not formed again.
 hipError_t launch_bn_backward(const float* y, const float* gup, const float* maskv,
                               int G, int R, int C, double* part, const float* mu,
                               const float* inv, float* coef, float* gamma, float* beta,
                               float* ug, float* ub, long long sP, float lr, float mom,
-                              int nesterov, float* dy, hipStream_t st);
+                              int nesterov, float* dy, int fused_nchunk, hipStream_t st);
 hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
                                 int G, int Bt, int H, int W, int Cin, int Cout,
                                 int mode, hipStream_t st);

@@ -56,6 +56,12 @@ struct ConvArgs {
   const float* bn_g;
   const float* bn_b;
   long long bn_sP;
+  // stage-1 input gradient epilogues (see ConvGeom): the shortcut share and
+  // the backward BN sums of the layer whose activation gradient dx is
+  const float* sc_dh;
+  const float* sc_h;
+  const float* bs_y;
+  double* bs_part;
 };
 
 // The shifted, scaled BN output z = gamma * (y - mu) * inv + beta in one fixed
@@ -685,7 +691,16 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_stem(ConvArgs c) {
 // (2-kh, 2-kw) -- and the channels swapped, W[(2-kh, 2-kw, ci)][co] staged
 // as [(kh, kw, co)][ci]. Wave w owns output rows h0 + 2w, h0 + 2w + 1 as
 // four 16 x 16 blocks of v_mfma_f32_16x16x4f32.
-template <int MODE, int NBW>
+// Input-gradient epilogues (EPI bits, with their operands loaded at the start
+// of each band so that they arrive while the band computes):
+//   kEpiShortcut: dx += dh where h > 0 (c.sc_dh, c.sc_h: the block output's
+//     gradient and activation, same shape; the identity shortcut);
+//   kEpiBnSums: dx is the gradient of a BN-ReLU's output whose pre-BN values
+//     c.bs_y and BN parameters come in c.bn_*: per band, the backward sums
+//     sum dz and sum dz x^ (dz = dx where the ReLU passed, x^ = (y - mu) inv)
+//     go to c.bs_part as one 256-row chunk, in the forward statistics' layout.
+constexpr int kEpiShortcut = 1, kEpiBnSums = 2;
+template <int MODE, int NBW, int EPI = 0>
 __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   constexpr int C = 16, CP = C + 4;          // 80-byte pixel pitch in LDS
   constexpr int W = 32, BH = 8;
@@ -765,9 +780,37 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int lq = lane >> 4, lm = lane & 15;
+  // BN parameters of this lane's channel (kEpiBnSums)
+  float em = 0.f, ei = 0.f, eg = 0.f, eb = 0.f;
+  if constexpr ((EPI & kEpiBnSums) != 0) {
+    em = c.bn_mu[(long long)g * C + lm];
+    ei = c.bn_inv[(long long)g * C + lm];
+    eg = c.bn_g[(long long)g * c.bn_sP + lm];
+    eb = c.bn_b[(long long)g * c.bn_sP + lm];
+  }
+  const long long img = ((long long)g * c.Bt + b) * H * W * C;
   for (int u = 0; u < NBW; ++u) {
     const int band = grp * NBW + u, h0 = band * BH;
     if (u + 1 < NBW) gload(h0 + BH);  // the next band, in flight during this one
+    // this lane's 16 outputs: element img + eoff(i, v)
+    auto eoff = [&](int i, int v) __attribute__((always_inline)) {
+      const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
+      return ((long long)row * W + col) * C + lm;
+    };
+    float e0[4][4], e1[4][4];
+    if constexpr (EPI != 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if constexpr ((EPI & kEpiShortcut) != 0) {
+            e0[i][v] = c.sc_h[img + eoff(i, v)];
+            e1[i][v] = c.sc_dh[img + eoff(i, v)];
+          } else {
+            e0[i][v] = c.bs_y[img + eoff(i, v)];
+          }
+        }
+    }
     floatx4 acc[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -787,14 +830,41 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
         }
       }
     }
-    float* out = c.out + ((long long)g * c.Bt + b) * H * W * C;
+    double bs0 = 0.0, bs1 = 0.0;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
-        out[((long long)row * W + col) * C + lm] = acc[i][v];
+        float r = acc[i][v];
+        if constexpr ((EPI & kEpiShortcut) != 0) r += e0[i][v] > 0.f ? e1[i][v] : 0.f;
+        if constexpr ((EPI & kEpiBnSums) != 0) {
+          const float y = e0[i][v];
+          const float dz = bn_z(eg, y, em, ei, eb) > 0.f ? r : 0.f;
+          const float xh = (y - em) * ei;
+          bs0 += (double)dz;
+          bs1 += (double)dz * (double)xh;
+        }
+        c.out[img + eoff(i, v)] = r;
       }
+    if constexpr ((EPI & kEpiBnSums) != 0) {
+      // the band's 256 positions: each wave's two rows by a lane butterfly,
+      // the four waves in order
+      __shared__ double bred[4][C][2];
+      stats_butterfly(bs0, bs1, 2, 4);
+      if (lq == 0) {
+        bred[wave][lm][0] = bs0;
+        bred[wave][lm][1] = bs1;
+      }
+      __syncthreads();
+      if (threadIdx.x < C) {
+        const int t = threadIdx.x;
+        const long long q = (long long)b * bands + band;
+        double* d = c.bs_part + (((long long)g * c.Bt * bands + q) * C + t) * 2;
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+          d[e] = ((bred[0][t][e] + bred[1][t][e]) + bred[2][t][e]) + bred[3][t][e];
+      }
+    }
     if (MODE == CONV_FWD && c.stats) {
       // BN statistics of the band (8 x 32 = 256 positions: one chunk): each
       // wave's two rows by a lane butterfly, the four waves in order
@@ -1557,6 +1627,8 @@ static bool halo_shape(const ConvGeom& q, int mode) {
          (mode == CONV_DGRAD || q.sx % 4 == 0);
 }
 
+bool conv_dgrad_epilogues(const ConvGeom& q) { return halo_shape(q, CONV_DGRAD); }
+
 bool conv_fwd_stats(const ConvGeom& q) {
   if (stem_shape(q) || halo_shape(q, CONV_FWD)) return true;
   return rows_shape(q, CONV_FWD) && ((long long)q.Bt * q.Ho * q.Wo) % 256 == 0;
@@ -1618,11 +1690,19 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   c.sW = q.sW;
   c.out = q.out;
   c.stats = mode == CONV_FWD ? q.stats : nullptr;
-  c.bn_mu = mode == CONV_DGRAD ? nullptr : q.bn_mu;
+  c.bn_mu = mode == CONV_DGRAD && !q.bs_part ? nullptr : q.bn_mu;
   c.bn_inv = q.bn_inv;
   c.bn_g = q.bn_g;
   c.bn_b = q.bn_b;
   c.bn_sP = q.bn_sP;
+  c.sc_dh = mode == CONV_DGRAD ? q.sc_dh : nullptr;
+  c.sc_h = q.sc_h;
+  c.bs_y = q.bs_y;
+  c.bs_part = mode == CONV_DGRAD ? q.bs_part : nullptr;
+  const int epi = (c.sc_dh ? 1 : 0) | (c.bs_part ? 2 : 0);
+  if (epi && (epi == 3 || !conv_dgrad_epilogues(q) || (c.sc_dh && !c.sc_h) ||
+              (c.bs_part && (!c.bs_y || !c.bn_mu || !c.bn_inv || !c.bn_g || !c.bn_b))))
+    return hipErrorInvalidValue;
   if (c.bn_mu && (q.Cin % 4 || q.bn_sP % 4 || ((uintptr_t)q.bn_mu | (uintptr_t)q.bn_inv |
                                               (uintptr_t)q.bn_g | (uintptr_t)q.bn_b) & 15))
     return hipErrorInvalidValue;
@@ -1695,6 +1775,12 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
       if (mode == CONV_FWD)
         hipLaunchKernelGGL((k_conv_halo16<CONV_FWD, kHaloBandsFwd>), dim3((unsigned)nb),
                            dim3(kT), 0, st, c);
+      else if (epi == 1)
+        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiShortcut>),
+                           dim3((unsigned)nb), dim3(kT), 0, st, c);
+      else if (epi == 2)
+        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiBnSums>),
+                           dim3((unsigned)nb), dim3(kT), 0, st, c);
       else
         hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad>), dim3((unsigned)nb),
                            dim3(kT), 0, st, c);
@@ -1802,13 +1888,14 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
                               int G, int R, int C, double* part, const float* mu,
                               const float* inv, float* coef, float* gamma, float* beta,
                               float* ug, float* ub, long long sP, float lr, float mom,
-                              int nesterov, float* dy, hipStream_t st) {
+                              int nesterov, float* dy, int fused_nchunk, hipStream_t st) {
   if (!bn_shape_ok(G, R, C) || !al16p(y) || !al16p(gup) || !al16p(maskv) || !al16p(dy) ||
-      !al16p(mu) || !al16p(inv) || !al16p(coef))
+      !al16p(mu) || !al16p(inv) || !al16p(coef) || fused_nchunk < 0)
     return hipErrorInvalidValue;
-  const int nch = bn_chunks(R);
-  hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
-                     mu, inv, gamma, beta, sP, part, nch);
+  const int nch = fused_nchunk > 0 ? fused_nchunk : bn_chunks(R);
+  if (fused_nchunk == 0)
+    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
+                       mu, inv, gamma, beta, sP, part, nch);
   hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
                      (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
                      nesterov, 1e-5f, nullptr, nullptr, 0LL);
