@@ -832,7 +832,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     lsgd::ConvGeom g = geom(i);
     g.dy = dy;
     g.out = dx;
-    *fused = (sc_dh || bs_layer >= 0) && lsgd::conv_dgrad_epilogues(g);
+    *fused = (sc_dh && (lsgd::conv_dgrad_epilogues(g) & 1)) ||
+             (bs_layer >= 0 && (lsgd::conv_dgrad_epilogues(g) & 2));
     if (*fused && sc_dh) {
       g.sc_dh = sc_dh;
       g.sc_h = sc_h;

@@ -179,8 +179,9 @@ struct ConvGeom {
   double* bs_part;
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
-// Whether the input-gradient launch of q takes the sc_* / bs_* epilogues.
-bool conv_dgrad_epilogues(const ConvGeom& q);
+// Which epilogues the input-gradient launch of q takes: bit 0 the shortcut
+// share (sc_*), bit 1 the BN backward sums (bs_*).
+int conv_dgrad_epilogues(const ConvGeom& q);
 int conv_wgrad_splits(int Bt, int Ho, int Wo);
 // Whether the forward convolution of q writes its output's BN statistics
 // (per 256-row chunk, [G][R/256][Cout][2] doubles: sum, sum of squares) when

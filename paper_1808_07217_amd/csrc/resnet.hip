@@ -109,6 +109,17 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
   }
 }
 
+// Input-gradient epilogues (EPI bits; their operands are loaded while the
+// last k work of a tile or band runs):
+//   kEpiShortcut: dx += dh where h > 0 (c.sc_dh, c.sc_h: the block output's
+//     gradient and activation, same shape; the identity shortcut);
+//   kEpiBnSums: dx is the gradient of a BN-ReLU's output whose pre-BN values
+//     c.bs_y and BN parameters come in c.bn_*: per 256 output rows, the
+//     backward sums sum dz and sum dz x^ (dz = dx where the ReLU passed,
+//     x^ = (y - mu) inv) go to c.bs_part as one chunk, in the forward
+//     statistics' layout.
+constexpr int kEpiShortcut = 1, kEpiBnSums = 2;
+
 // Forward / input-gradient convolution for reduction channel counts that
 // are multiples of 16 (every convolution after the first): the output tile
 // is 256 spatial rows x all BN (= 16, 32 or 64) channels, so no MFMA lane is
@@ -123,9 +134,10 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
 // a stride-1 convolution.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-template <int MODE, int BN>
+template <int MODE, int BN, int EPI = 0>
 __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   static_assert(MODE == CONV_FWD || MODE == CONV_DGRAD, "row-tiled modes");
+  static_assert(EPI == 0 || MODE == CONV_DGRAD, "epilogues of the input gradient");
   constexpr int BM = 256, BK = 16, PK = BK + 4;  // 80-byte A rows in LDS
   constexpr int NBL = BN / 16;                    // 16-wide column blocks
   constexpr int RPT = BM * BK / 4 / kT;           // A float4 per thread (4)
@@ -174,7 +186,7 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   // and parameters of every input channel staged in LDS
   const bool bnin = MODE == CONV_FWD && c.bn_mu != nullptr;
   __shared__ __attribute__((aligned(16))) float bnp[4][64];
-  if (bnin) {
+  if (bnin || (EPI & kEpiBnSums) != 0) {  // (kEpiBnSums: the layer of dx, Cin channels)
     for (int t = tid; t < c.Cin; t += kT) {
       bnp[0][t] = c.bn_mu[(long long)g * c.Cin + t];
       bnp[1][t] = c.bn_inv[(long long)g * c.Cin + t];
@@ -280,20 +292,80 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   gload(slab(1), ra1, rb1, ok1, ch1s);
   lstore(0, ra0, rb0, ok0, ch0s);
   __syncthreads();
+  // epilogue operands of this thread's outputs (row block i, column block j,
+  // register v), issued while the last slabs compute
+  float e0[EPI ? 4 : 1][EPI ? NBL : 1][4], e1[(EPI & kEpiShortcut) ? 4 : 1][NBL][4];
+  auto eload = [&]() __attribute__((always_inline)) {
+    if constexpr (EPI != 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int m = min(m0 + wave * 64 + i * 16 + lq * 4 + v, Mg - 1);
+#pragma unroll
+          for (int j = 0; j < NBL; ++j) {
+            const long long o = ((long long)g * Mg + m) * BN + j * 16 + lm;
+            if constexpr ((EPI & kEpiShortcut) != 0) {
+              e0[i][j][v] = c.sc_h[o];
+              e1[i][j][v] = c.sc_dh[o];
+            } else {
+              e0[i][j][v] = c.bs_y[o];
+            }
+          }
+        }
+    }
+  };
   int it = 0;
-  for (; it + 1 < nk; it += 2) {
-    gload(slab(it + 2), ra0, rb0, ok0, ch0s);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(0);
-    lstore(1, ra1, rb1, ok1, ch1s);
-    __syncthreads();
-    gload(slab(it + 3), ra1, rb1, ok1, ch1s);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(1);
-    lstore(0, ra0, rb0, ok0, ch0s);
-    __syncthreads();
+  if constexpr (EPI == 0) {
+    for (; it + 1 < nk; it += 2) {
+      gload(slab(it + 2), ra0, rb0, ok0, ch0s);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, ra1, rb1, ok1, ch1s);
+      __syncthreads();
+      gload(slab(it + 3), ra1, rb1, ok1, ch1s);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      lstore(0, ra0, rb0, ok0, ch0s);
+      __syncthreads();
+    }
+    if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
+  } else {
+    // the same pipeline while both prefetches are real slabs (nk >= 2); the
+    // last two or three slabs then run with the epilogue loads in flight
+    for (; it + 3 < nk; it += 2) {
+      gload(slab(it + 2), ra0, rb0, ok0, ch0s);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, ra1, rb1, ok1, ch1s);
+      __syncthreads();
+      gload(slab(it + 3), ra1, rb1, ok1, ch1s);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      lstore(0, ra0, rb0, ok0, ch0s);
+      __syncthreads();
+    }
+    // slab it in buffer 0, slab it + 1 in ra1; nk - it is 2 or 3
+    if (it + 2 < nk) {
+      gload(slab(it + 2), ra0, rb0, ok0, ch0s);
+      eload();
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, ra1, rb1, ok1, ch1s);
+      __syncthreads();
+      compute(1);
+      lstore(0, ra0, rb0, ok0, ch0s);
+      __syncthreads();
+      compute(0);
+    } else {
+      eload();
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      lstore(1, ra1, rb1, ok1, ch1s);
+      __syncthreads();
+      compute(1);
+    }
   }
-  if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
 
   float* out = c.out + (long long)g * Mg * BN;
   if constexpr (MODE == CONV_FWD) {
@@ -324,6 +396,52 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
 #pragma unroll
         for (int e = 0; e < 2; ++e)
           d[e] = ((red[0][tid][e] + red[1][tid][e]) + red[2][tid][e]) + red[3][tid][e];
+      }
+    }
+  }
+  if constexpr (EPI != 0) {
+    // the shortcut share, or the BN backward sums of the tile's 256 rows
+    // (Mg is then a multiple of 256: one chunk; lanes by a butterfly, then
+    // the four waves in order)
+    double bs0[NBL], bs1[NBL];
+#pragma unroll
+    for (int j = 0; j < NBL; ++j) {
+      bs0[j] = 0.0;
+      bs1[j] = 0.0;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < NBL; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if constexpr ((EPI & kEpiShortcut) != 0) {
+            acc[i][j][v] += e0[i][j][v] > 0.f ? e1[i][j][v] : 0.f;
+          } else {
+            const int ch = j * 16 + lm;
+            const float y = e0[i][j][v], em = bnp[0][ch], ei = bnp[1][ch];
+            const float dz = bn_z(bnp[2][ch], y, em, ei, bnp[3][ch]) > 0.f ? acc[i][j][v] : 0.f;
+            const float xh = (y - em) * ei;
+            bs0[j] += (double)dz;
+            bs1[j] += (double)dz * (double)xh;
+          }
+        }
+    if constexpr ((EPI & kEpiBnSums) != 0) {
+      __shared__ double bred[4][BN][2];
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) {
+        stats_butterfly(bs0[j], bs1[j], 2, 4);
+        if (lq == 0) {
+          bred[wave][j * 16 + lm][0] = bs0[j];
+          bred[wave][j * 16 + lm][1] = bs1[j];
+        }
+      }
+      __syncthreads();
+      if (tid < BN) {
+        double* d = c.bs_part + (((long long)g * (Mg / 256) + m0 / 256) * BN + tid) * 2;
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+          d[e] = ((bred[0][tid][e] + bred[1][tid][e]) + bred[2][tid][e]) + bred[3][tid][e];
       }
     }
   }
@@ -691,15 +809,7 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_stem(ConvArgs c) {
 // (2-kh, 2-kw) -- and the channels swapped, W[(2-kh, 2-kw, ci)][co] staged
 // as [(kh, kw, co)][ci]. Wave w owns output rows h0 + 2w, h0 + 2w + 1 as
 // four 16 x 16 blocks of v_mfma_f32_16x16x4f32.
-// Input-gradient epilogues (EPI bits, with their operands loaded at the start
-// of each band so that they arrive while the band computes):
-//   kEpiShortcut: dx += dh where h > 0 (c.sc_dh, c.sc_h: the block output's
-//     gradient and activation, same shape; the identity shortcut);
-//   kEpiBnSums: dx is the gradient of a BN-ReLU's output whose pre-BN values
-//     c.bs_y and BN parameters come in c.bn_*: per band, the backward sums
-//     sum dz and sum dz x^ (dz = dx where the ReLU passed, x^ = (y - mu) inv)
-//     go to c.bs_part as one 256-row chunk, in the forward statistics' layout.
-constexpr int kEpiShortcut = 1, kEpiBnSums = 2;
+// (EPI: the input-gradient epilogues, loaded at the start of each band)
 template <int MODE, int NBW, int EPI = 0>
 __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   constexpr int C = 16, CP = C + 4;          // 80-byte pixel pitch in LDS
@@ -1627,7 +1737,14 @@ static bool halo_shape(const ConvGeom& q, int mode) {
          (mode == CONV_DGRAD || q.sx % 4 == 0);
 }
 
-bool conv_dgrad_epilogues(const ConvGeom& q) { return halo_shape(q, CONV_DGRAD); }
+int conv_dgrad_epilogues(const ConvGeom& q) {
+  if (halo_shape(q, CONV_DGRAD)) return kEpiShortcut | kEpiBnSums;
+  if (q.stride != 1 || !rows_shape(q, CONV_DGRAD) || q.Cin != q.Cout) return 0;
+  // the row kernel: 32 channels (at 64 the operands' registers cost more
+  // occupancy than the separate passes); the sums need whole 256-row chunks
+  const bool chunks = ((long long)q.Bt * q.H * q.W) % 256 == 0;
+  return q.Cin == 32 ? kEpiShortcut | (chunks ? kEpiBnSums : 0) : 0;
+}
 
 bool conv_fwd_stats(const ConvGeom& q) {
   if (stem_shape(q) || halo_shape(q, CONV_FWD)) return true;
@@ -1700,7 +1817,7 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   c.bs_y = q.bs_y;
   c.bs_part = mode == CONV_DGRAD ? q.bs_part : nullptr;
   const int epi = (c.sc_dh ? 1 : 0) | (c.bs_part ? 2 : 0);
-  if (epi && (epi == 3 || !conv_dgrad_epilogues(q) || (c.sc_dh && !c.sc_h) ||
+  if (epi && (epi == 3 || (conv_dgrad_epilogues(q) & epi) != epi || (c.sc_dh && !c.sc_h) ||
               (c.bs_part && (!c.bs_y || !c.bn_mu || !c.bn_inv || !c.bn_g || !c.bn_b))))
     return hipErrorInvalidValue;
   if (c.bn_mu && (q.Cin % 4 || q.bn_sP % 4 || ((uintptr_t)q.bn_mu | (uintptr_t)q.bn_inv |
@@ -1794,9 +1911,14 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
         else if (Ng == 32) LSGD_ROWS(CONV_FWD, 32);
         else LSGD_ROWS(CONV_FWD, 64);
       } else {
+#define LSGD_ROWS_E(NB, E)                                                                  \
+  hipLaunchKernelGGL((k_conv_rows<CONV_DGRAD, NB, E>), dim3((unsigned)rt), dim3(kT), 0, st, c)
         if (Ng == 16) LSGD_ROWS(CONV_DGRAD, 16);
+        else if (Ng == 32 && epi == kEpiShortcut) LSGD_ROWS_E(32, kEpiShortcut);
+        else if (Ng == 32 && epi == kEpiBnSums) LSGD_ROWS_E(32, kEpiBnSums);
         else if (Ng == 32) LSGD_ROWS(CONV_DGRAD, 32);
         else LSGD_ROWS(CONV_DGRAD, 64);
+#undef LSGD_ROWS_E
       }
 #undef LSGD_ROWS
     } else {
