@@ -1,18 +1,16 @@
 """Write the oracle's loss trajectories for the full workload runs.
 
 Usage (from the repository root; takes tens of minutes on 8 cores):
-    python tests/golden/make_trajectories.py [--perturbed] [workload ...]
+    python tests/golden/make_trajectories.py [workload ...]
 
 For each workload it runs the CPU oracle over the whole schedule from the
 seeded inputs and stores, per round, the mean mini-batch loss of every local
 step (averaged over the K replicas) in tests/golden/trajectory_<name>.json.
-
---perturbed: the same run from initial weights multiplied elementwise by
-(1 + 1e-7 z), z ~ N(0, 1) from a fixed seed -- a change of the size of fp32
-rounding -- written to trajectory_<name>_perturbed.json. The difference
-between the two oracle runs measures how strongly the trajectory itself
-amplifies rounding, which bounds what any fp32 implementation can match.
 Only the oracle and the seeded input module are used.
+
+ResNet-20's runs from perturbed initial weights (several independent draws,
+trajectory_resnet20_perturbed.json) are written by make_round_models.py,
+which also writes its unperturbed trajectory the same way.
 """
 import json
 import os
@@ -30,17 +28,10 @@ from oracle import lsgd_oracle as O  # noqa: E402
 FULL_RUNS = ["mlp_512", "postlocal_mlp_512", "wide_mlp_2048_bf16", "resnet20"]
 
 
-PERTURBATION = 1e-7
-PERTURBATION_SEED = 12345
-
-
-def trajectory(name, perturbed=False):
+def trajectory(name):
     w = wk.get(name)
     X, y = wk.dataset(w)
     w0 = np.asarray(wk.initial_weights(w), np.float64)
-    if perturbed:
-        z = np.random.default_rng(PERTURBATION_SEED).standard_normal(w0.size)
-        w0 = w0 * (1.0 + PERTURBATION * z)
     st = O.State(w0, w.K)
     rounds = []
     t0 = time.time()
@@ -53,21 +44,16 @@ def trajectory(name, perturbed=False):
     return {
         "workload": name,
         "source": "oracle.lsgd_oracle.run_round over the post-local schedule "
-                  "from workloads.initial_weights / workloads.dataset"
-                  + (f", initial weights x (1 + {PERTURBATION} z), z ~ N(0,1) "
-                     f"seed {PERTURBATION_SEED}" if perturbed else ""),
+                  "from workloads.initial_weights / workloads.dataset",
         "per_round_step_mean_loss": rounds,
     }
 
 
 def main():
-    args = sys.argv[1:]
-    perturbed = "--perturbed" in args
-    names = [a for a in args if a != "--perturbed"] or FULL_RUNS
+    names = sys.argv[1:] or FULL_RUNS
     for name in names:
-        out = trajectory(name, perturbed)
-        suffix = "_perturbed" if perturbed else ""
-        path = os.path.join(HERE, f"trajectory_{name}{suffix}.json")
+        out = trajectory(name)
+        path = os.path.join(HERE, f"trajectory_{name}.json")
         with open(path, "w") as f:
             json.dump(out, f)
         print(f"wrote {path}", flush=True)

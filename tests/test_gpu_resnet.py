@@ -120,3 +120,34 @@ def test_resnet20_round_with_the_newer_schemes(variant):
         u = reps.read_global_momentum().cpu().numpy()
         assert np.max(np.abs(u - st.u_global)) * w.lr <= 1e-5 * scale
 
+
+def test_resnet20_full_shape_first_round_model():
+    """Workload 5 at its real shape (K = 16, B_loc = 128, H = 16): the
+    synchronised model after round 1 (eq. 2 / Algorithm 1 with per-worker BN)
+    against the oracle's, which tests/golden/make_round_models.py wrote
+    (oracle only), and the round's per-step mean losses. Bar: normwise 1e-5,
+    or, where the oracle itself moves further when its initial weights are
+    perturbed by 1e-7 (eight independent draws, same file), the largest of
+    those distances (factor 1)."""
+    import json
+    import os
+    here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+    with open(os.path.join(here, "round1_resnet20.json")) as f:
+        gold = json.load(f)
+    model = np.load(os.path.join(here, "round1_resnet20_model.npy"))
+    assert len(gold["perturbed_round1_normwise"]) >= 3
+    bar = max(1e-5, max(gold["perturbed_round1_normwise"]))
+    w = wk.get("resnet20")
+    X, y = wk.dataset(w)
+    print("resnet20 full-shape round 1", flush=True)
+    reps = make_replicas(w, X, y)
+    loss = torch.empty(w.H, w.K, device=device())
+    reps.run_round([w.lr] * w.H, loss)
+    got = reps.read_params(0).cpu().numpy()
+    np.testing.assert_array_equal(got, reps.read_params(w.K - 1).cpu().numpy())
+    err = normwise(got, model)
+    lerr = rel(loss.cpu().numpy().mean(axis=1), np.asarray(gold["round1_step_mean_loss"]))
+    print(f"resnet20 round 1: model {err:.3e} (bar {bar:.3e}; oracle perturbed "
+          f"{gold['perturbed_round1_normwise']}), losses {lerr.max():.3e}", flush=True)
+    assert err <= bar
+    assert np.all(lerr <= 1e-3)

@@ -23,12 +23,26 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CASES = [("mlp_512", 1e-3), ("postlocal_mlp_512", 1e-3),
          ("wide_mlp_2048_bf16", 2e-2), ("resnet20", 1e-3)]
 # How far an fp32 run may legitimately drift from the fp64 oracle grows with
-# the trajectory's own sensitivity: where a golden run from initial weights
-# perturbed by 1e-7 (relative; trajectory_<name>_perturbed.json, also the
-# oracle's) has moved by rel_p, the bar is max(tol, ENVELOPE * running max of
-# rel_p). ResNet-20's batch-normalised descent amplifies a 1e-7 perturbation
-# to 3e-2 by the end of its five rounds.
-ENVELOPE = 4.0
+# the trajectory's own sensitivity. Where the oracle was also run from
+# initial weights perturbed by 1e-7 (relative; independent draws in
+# trajectory_<name>_perturbed.json, also the oracle's: eight for ResNet-20,
+# written by tests/golden/make_round_models.py), the bar at each step is
+# max(tol, the largest distance any draw has reached by that step) -- factor
+# 1, over at least three draws. ResNet-20's batch-normalised descent amplifies
+# a 1e-7 perturbation to about 2e-2 by the end of its five rounds.
+
+
+def _perturbed_envelope(name, want):
+    pert = os.path.join(HERE, "golden", f"trajectory_{name}_perturbed.json")
+    if not os.path.exists(pert):
+        return None
+    with open(pert) as f:
+        draws = json.load(f)["draws"]
+    env = np.zeros_like(want)
+    for d in draws:
+        moved = np.concatenate([np.asarray(r) for r in d["per_round_step_mean_loss"]])
+        env = np.maximum(env, np.maximum.accumulate(rel(moved, want)))
+    return env, len(draws)
 
 
 @pytest.mark.parametrize("name,tol", CASES)
@@ -49,12 +63,10 @@ def test_full_run_loss_trajectory(name, tol):
     want = np.concatenate([np.asarray(r) for r in gold])
     err = rel(got, want)
     bar = np.full_like(err, tol)
-    pert = os.path.join(HERE, "golden", f"trajectory_{name}_perturbed.json")
-    if os.path.exists(pert):
-        with open(pert) as f:
-            moved = np.concatenate([np.asarray(r) for r in
-                                    json.load(f)["per_round_step_mean_loss"]])
-        bar = np.maximum(bar, ENVELOPE * np.maximum.accumulate(rel(moved, want)))
+    env = _perturbed_envelope(name, want)
+    if env is not None:
+        assert env[1] >= 3
+        bar = np.maximum(bar, env[0])
     print(f"{name}: max relative loss error {err.max():.3e} at step "
           f"{int(err.argmax())} (bar there {bar[err.argmax()]:.3e}); final loss "
           f"{got[-1]:.5g} vs {want[-1]:.5g}", flush=True)
