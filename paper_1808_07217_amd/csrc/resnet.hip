@@ -123,29 +123,44 @@ constexpr int kEpiShortcut = 1, kEpiBnSums = 2;
 // Forward / input-gradient convolution for reduction channel counts that
 // are multiples of 16 (every convolution after the first): the output tile
 // is 256 spatial rows x all BN (= 16, 32 or 64) channels, so no MFMA lane is
-// spent on channels that do not exist. A k slab of 16 is one tap (kh, kw)
-// and 16 consecutive channels, so a thread decodes its rows (image, output
-// position) once and each slab only moves the tap; padding and the stride-2
-// parity become a validity mask (address clamped, value zeroed), and the
-// loads carry no branches. Two register sets: slab t+2 is in flight while
-// slab t computes. Each wave owns 64 rows as 16 x 16 blocks of
-// v_mfma_f32_16x16x4f32 (lane l: A[m = l%16][k = l/16], B[k = l/16][n = l%16],
-// accumulator v at C[4 (l/16) + v][l%16]). The input gradient here is that of
-// a stride-1 convolution.
+// spent on channels that do not exist. Each wave owns 64 rows as 16 x 16
+// blocks of v_mfma_f32_16x16x4f32 (lane l: A[m = l%16][k = l/16],
+// B[k = l/16][n = l%16], accumulator v at C[4 (l/16) + v][l%16]). A k slab
+// of 16 is one tap (kh, kw) and 16 consecutive channels, taken in the order
+// 4 (l/16) + s at MFMA step s: a lane's four A values of a row are then one
+// float4 of the activation, and the operands go from memory straight into
+// the registers the MFMAs read -- no LDS staging and no barriers, every wave
+// runs on its own. Operands are read through buffer resources: a lane
+// decodes its four rows (image, position, which of the nine taps fall inside
+// the image) once, a slab adds the tap's offset, and a tap outside the image
+// reads at an offset past the resource's end, which the hardware returns as
+// zero; the weights' slab offset is a scalar. Three register sets: slabs
+// t + 1 and t + 2 are in flight while slab t computes. The input gradient
+// here is that of a stride-1 convolution.
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// A raw buffer resource over `bytes` bytes at p (gfx9 word 3: 32-bit data
+// format); loads at offsets at or past `bytes` return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                           0x00020000);
+}
+constexpr unsigned kOutside = 0x80000000u;  // an offset past every resource here
+
+template <int BN>
+struct RowsSlab {
+  v4f a[4];          // A: rows 16 i + l%16, channels ch .. ch + 3
+  v4f b[BN / 16];    // B: k = ch .. ch + 3, column 16 j + l%16
+  unsigned okm;      // which of the four rows read inside the image (bit i)
+  int ch;            // the lane's first reduction channel
+};
 
 template <int MODE, int BN, int EPI = 0>
 __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   static_assert(MODE == CONV_FWD || MODE == CONV_DGRAD, "row-tiled modes");
   static_assert(EPI == 0 || MODE == CONV_DGRAD, "epilogues of the input gradient");
-  constexpr int BM = 256, BK = 16, PK = BK + 4;  // 80-byte A rows in LDS
-  constexpr int NBL = BN / 16;                    // 16-wide column blocks
-  constexpr int RPT = BM * BK / 4 / kT;           // A float4 per thread (4)
-  constexpr int BQ = BK * BN / 4;                 // B float4 per slab
-  __shared__ __attribute__((aligned(16))) float As[2][BM][PK];
-  // B rows 16 floats apart modulo 64: the four k rows a B read spans fall
-  // in disjoint banks
-  __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + 16];
+  constexpr int BM = 256;
+  constexpr int NBL = BN / 16;  // 16-wide column blocks
 
   const int Cr = MODE == CONV_FWD ? c.Cin : c.Cout;  // reduction channels
   const int HWo = MODE == CONV_FWD ? c.Ho * c.Wo : c.H * c.W;
@@ -153,35 +168,52 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   const int tiles = (Mg + BM - 1) / BM;
   const int g = blockIdx.x / tiles, m0 = (blockIdx.x - g * tiles) * BM;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kq = (tid & 3) * 4;  // this thread's 4 channels of the slab
-  const float* Bw = c.Wk + (long long)g * c.sW;  // W [9 Cin][Cout] of replica g
-  constexpr int ntap = 9;
+  const int lq = lane >> 4, lm = lane & 15;
 
-  // rows of this thread: r = tid / 4 + 64 i
-  long long base[RPT];  // image (or output-gradient image) base, elements
-  int ya[RPT], xa[RPT];
-  bool rok[RPT];
+  // the replica's operand tensor (the input, or the output gradient) and
+  // weights W [9 Cin][Cout]
+  const int Hs = MODE == CONV_FWD ? c.H : c.Ho, Ws = MODE == CONV_FWD ? c.W : c.Wo;
+  const float* src = MODE == CONV_FWD ? c.x + (long long)g * c.sx
+                                      : c.dy + (long long)g * c.Bt * c.Ho * c.Wo * c.Cout;
+  const auto rsA = buffer_rsrc(src, (unsigned)c.Bt * Hs * Ws * Cr * 4u);
+  const auto rsB = buffer_rsrc(c.Wk + (long long)g * c.sW, 9u * c.Cin * c.Cout * 4u);
+
+  // rows of this lane: m0 + 64 wave + 16 i + l%16; off: byte offset of the
+  // tap (1, 1) read plus the lane's channels; tapm: which taps are inside
+  int off[4];
+  unsigned tapm[4];
 #pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    const int m = m0 + (tid >> 2) + 64 * i;
-    rok[i] = m < Mg;
-    const int mm = rok[i] ? m : 0;
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + wave * 64 + i * 16 + lm;
+    const bool rok = m < Mg;
+    const int mm = rok ? m : 0;
     const int b = mm / HWo, p = mm - b * HWo;
+    int yc, xc;  // operand position of the centre tap
     if constexpr (MODE == CONV_FWD) {
       const int oh = p / c.Wo, ow = p - oh * c.Wo;
-      ya[i] = oh * c.stride - 1;  // input row of tap kh: ya + kh
-      xa[i] = ow * c.stride - 1;
-      base[i] = c.rowmap ? (long long)c.rowmap[(long long)g * c.Bt + b] * c.H * c.W * c.Cin
-                         : (long long)g * c.sx + (long long)b * c.H * c.W * c.Cin;
+      yc = oh * c.stride;
+      xc = ow * c.stride;
     } else {
-      const int h = p / c.W, w = p - h * c.W;
-      ya[i] = h + 1;  // output-gradient row of tap kh: ya - kh
-      xa[i] = w + 1;
-      base[i] = ((long long)g * c.Bt + b) * c.Ho * c.Wo * c.Cout;
+      yc = p / c.W;
+      xc = p - yc * c.W;
     }
+    unsigned t = 0;
+#pragma unroll
+    for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+      for (int kw = 0; kw < 3; ++kw) {
+        // forward: input (yc + kh - 1, xc + kw - 1); input gradient: output
+        // gradient (yc + 1 - kh, xc + 1 - kw)
+        const int yy = MODE == CONV_FWD ? yc + kh - 1 : yc + 1 - kh;
+        const int xx = MODE == CONV_FWD ? xc + kw - 1 : xc + 1 - kw;
+        const bool ok = rok && yy >= 0 && yy < Hs && xx >= 0 && xx < Ws;
+        t |= (unsigned)ok << (kh * 3 + kw);
+      }
+    tapm[i] = t;
+    off[i] = (((b * Hs + yc) * Ws + xc) * Cr + 4 * lq) * 4;
   }
-  const float* src = MODE == CONV_FWD ? c.x : c.dy;
-  const int nk = ntap * Cr / BK;
+  const int cpt = Cr / 16;     // slabs per tap
+  const int nk = 9 * cpt;      // a multiple of 3
   // forward of a block's second convolution: the input BN-ReLU, statistics
   // and parameters of every input channel staged in LDS
   const bool bnin = MODE == CONV_FWD && c.bn_mu != nullptr;
@@ -195,71 +227,42 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
     __syncthreads();
   }
-  // okm: which of this thread's rows read inside the image (bit i); chs: the
-  // slab's first channel of this thread
-  auto gload = [&](int s, v4f(&xa4)[RPT], v4f& xb, unsigned& okm, int& chs)
-      __attribute__((always_inline)) {
-    const int ti = s / (Cr / BK), ch0 = (s - ti * (Cr / BK)) * BK + kq;
-    okm = 0;
-    chs = ch0;
-    const int kh = ti / 3, kw = ti - kh * 3, tap = ti;
+  // the lane's B offsets: forward, rows ch + e of W at column 16 j + l%16;
+  // input gradient, row (tap, 16 j + l%16) of W at columns ch .. ch + 3
+  int boff[NBL];
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) {
-      int yy, xx;
-      bool ok;
-      if constexpr (MODE == CONV_FWD) {
-        yy = ya[i] + kh;
-        xx = xa[i] + kw;
-        ok = rok[i] && yy >= 0 && yy < c.H && xx >= 0 && xx < c.W;
-        yy = ok ? yy : 0;
-        xx = ok ? xx : 0;
-        xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.W + xx) * c.Cin + ch0);
-      } else {
-        const int oh = ya[i] - kh, ow = xa[i] - kw;
-        ok = rok[i] && oh >= 0 && ow >= 0 && oh < c.Ho && ow < c.Wo;
-        yy = ok ? oh : 0;
-        xx = ok ? ow : 0;
-        xa4[i] = *(const v4f*)(src + base[i] + ((long long)yy * c.Wo + xx) * c.Cout + ch0);
-      }
-      if (!ok) xa4[i] = v4f{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < NBL; ++j)
+    boff[j] = MODE == CONV_FWD ? ((4 * lq) * BN + j * 16 + lm) * 4
+                               : ((j * 16 + lm) * Cr + 4 * lq) * 4;
+  auto gload = [&](int s, RowsSlab<BN>& t) __attribute__((always_inline)) {
+    const int ti = s / cpt, cb = (s - ti * cpt) * 16;
+    const int kh = ti / 3, kw = ti - kh * 3;
+    // byte offset of tap (kh, kw), channel block cb, from the centre read
+    const int dt = MODE == CONV_FWD ? (((kh - 1) * Ws + (kw - 1)) * Cr + cb) * 4
+                                    : (((1 - kh) * Ws + (1 - kw)) * Cr + cb) * 4;
+    unsigned okm = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool ok = tapm[i] >> ti & 1;
+      const unsigned o = ok ? (unsigned)(off[i] + dt) : kOutside;
+      t.a[i] = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(rsA, o, 0, 0));
       okm |= (unsigned)ok << i;
     }
-    const int bq = min(tid, BQ - 1);
-    const int cbase = (s - ti * (Cr / BK)) * BK;  // slab's first reduction channel
-    if constexpr (MODE == CONV_FWD) {
-      // B[k = (tap, ci)][n = co] = W[(tap, ci)][co]: rows of 16 channels
-      xb = *(const v4f*)(Bw + (long long)(tap * Cr + cbase + bq / (BN / 4)) * BN +
-                         (bq % (BN / 4)) * 4);
-    } else {
-      // B[k = (tap, co)][n = ci] = W[(tap, ci)][co], read from the forward
-      // layout [9 Cin][Cout]: four consecutive co of one ci per thread
-      xb = *(const v4f*)(Bw + (long long)(tap * BN + bq / (BK / 4)) * Cr + cbase +
-                         (bq % (BK / 4)) * 4);
-    }
-  };
-  auto lstore = [&](int buf, const v4f(&xa4)[RPT], const v4f& xb, unsigned okm, int chs)
-      __attribute__((always_inline)) {
-    if (bnin) {
-      BnIn4 p;
-      p.m = *(const v4f*)&bnp[0][chs];
-      p.iv = *(const v4f*)&bnp[1][chs];
-      p.g = *(const v4f*)&bnp[2][chs];
-      p.b = *(const v4f*)&bnp[3][chs];
+    t.okm = okm;
+    t.ch = cb + 4 * lq;
+    // scalar part of the weights' offset
+    const int sb = MODE == CONV_FWD ? (ti * Cr + cb) * BN * 4 : (ti * BN * Cr + cb) * 4;
 #pragma unroll
-      for (int i = 0; i < RPT; ++i)  // padding stays 0
-        *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] =
-            (okm >> i & 1) ? bn_in(p, xa4[i]) : v4f{0.f, 0.f, 0.f, 0.f};
-    } else {
-#pragma unroll
-      for (int i = 0; i < RPT; ++i) *(v4f*)&As[buf][(tid >> 2) + 64 * i][kq] = xa4[i];
-    }
-    if (tid < BQ) {
+    for (int j = 0; j < NBL; ++j) {
       if constexpr (MODE == CONV_FWD) {
-        *(v4f*)&Bs[buf][tid / (BN / 4)][(tid % (BN / 4)) * 4] = xb;
-      } else {
-        const int ci = tid / (BK / 4), co4 = (tid % (BK / 4)) * 4;
+        // B[k = (tap, ci)][n = co] = W[(tap, ci)][co]: four rows of W
 #pragma unroll
-        for (int e = 0; e < 4; ++e) Bs[buf][co4 + e][ci] = xb[e];
+        for (int e = 0; e < 4; ++e)
+          t.b[j][e] = __builtin_bit_cast(
+              float, __builtin_amdgcn_raw_buffer_load_b32(rsB, boff[j] + e * BN * 4, sb, 0));
+      } else {
+        // B[k = (tap, co)][n = ci] = W[(tap, ci)][co]: four consecutive co
+        t.b[j] = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(rsB, boff[j], sb, 0));
       }
     }
   };
@@ -268,31 +271,34 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NBL; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int lq = lane >> 4, lm = lane & 15;
-  auto compute = [&](int buf) __attribute__((always_inline)) {
+  auto compute = [&](const RowsSlab<BN>& t) __attribute__((always_inline)) {
+    v4f a[4];
+    if (bnin) {
+      BnIn4 p;
+      p.m = *(const v4f*)&bnp[0][t.ch];
+      p.iv = *(const v4f*)&bnp[1][t.ch];
+      p.g = *(const v4f*)&bnp[2][t.ch];
+      p.b = *(const v4f*)&bnp[3][t.ch];
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 4) {
-      float av[4], bv[NBL];
+      for (int i = 0; i < 4; ++i) {  // padding stays 0
+        const v4f z = bn_in(p, t.a[i]);
+        const bool ok = t.okm >> i & 1;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = As[buf][wave * 64 + i * 16 + lm][kk + lq];
+        for (int e = 0; e < 4; ++e) a[i][e] = ok ? z[e] : 0.f;
+      }
+    } else {
 #pragma unroll
-      for (int j = 0; j < NBL; ++j) bv[j] = Bs[buf][kk + lq][j * 16 + lm];
+      for (int i = 0; i < 4; ++i) a[i] = t.a[i];  // zero outside the image
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < NBL; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][s], t.b[j][s], acc[i][j], 0, 0, 0);
   };
-  v4f ra0[RPT], ra1[RPT], rb0, rb1;
-  unsigned ok0, ok1;
-  int ch0s, ch1s;
-  auto slab = [&](int t) __attribute__((always_inline)) { return min(t, nk - 1); };
-  gload(slab(0), ra0, rb0, ok0, ch0s);
-  gload(slab(1), ra1, rb1, ok1, ch1s);
-  lstore(0, ra0, rb0, ok0, ch0s);
-  __syncthreads();
-  // epilogue operands of this thread's outputs (row block i, column block j,
+  // epilogue operands of this lane's outputs (row block i, column block j,
   // register v), issued while the last slabs compute
   float e0[EPI ? 4 : 1][EPI ? NBL : 1][4], e1[(EPI & kEpiShortcut) ? 4 : 1][NBL][4];
   auto eload = [&]() __attribute__((always_inline)) {
@@ -315,57 +321,25 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
         }
     }
   };
+  RowsSlab<BN> r0, r1, r2;
+  gload(0, r0);
+  gload(1, r1);
   int it = 0;
-  if constexpr (EPI == 0) {
-    for (; it + 1 < nk; it += 2) {
-      gload(slab(it + 2), ra0, rb0, ok0, ch0s);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(0);
-      lstore(1, ra1, rb1, ok1, ch1s);
-      __syncthreads();
-      gload(slab(it + 3), ra1, rb1, ok1, ch1s);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(1);
-      lstore(0, ra0, rb0, ok0, ch0s);
-      __syncthreads();
-    }
-    if (it < nk) compute(0);  // odd slab count: the last slab is in buffer 0
-  } else {
-    // the same pipeline while both prefetches are real slabs (nk >= 2); the
-    // last two or three slabs then run with the epilogue loads in flight
-    for (; it + 3 < nk; it += 2) {
-      gload(slab(it + 2), ra0, rb0, ok0, ch0s);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(0);
-      lstore(1, ra1, rb1, ok1, ch1s);
-      __syncthreads();
-      gload(slab(it + 3), ra1, rb1, ok1, ch1s);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(1);
-      lstore(0, ra0, rb0, ok0, ch0s);
-      __syncthreads();
-    }
-    // slab it in buffer 0, slab it + 1 in ra1; nk - it is 2 or 3
-    if (it + 2 < nk) {
-      gload(slab(it + 2), ra0, rb0, ok0, ch0s);
-      eload();
-      __builtin_amdgcn_sched_barrier(0);
-      compute(0);
-      lstore(1, ra1, rb1, ok1, ch1s);
-      __syncthreads();
-      compute(1);
-      lstore(0, ra0, rb0, ok0, ch0s);
-      __syncthreads();
-      compute(0);
-    } else {
-      eload();
-      __builtin_amdgcn_sched_barrier(0);
-      compute(0);
-      lstore(1, ra1, rb1, ok1, ch1s);
-      __syncthreads();
-      compute(1);
-    }
+  // every prefetch a real slab while it + 4 < nk; then the last three slabs
+  // with the epilogue loads in flight
+  for (; it + 5 <= nk; it += 3) {
+    gload(it + 2, r2);
+    compute(r0);
+    gload(it + 3, r0);
+    compute(r1);
+    gload(it + 4, r1);
+    compute(r2);
   }
+  gload(it + 2, r2);
+  eload();
+  compute(r0);
+  compute(r1);
+  compute(r2);
 
   float* out = c.out + (long long)g * Mg * BN;
   if constexpr (MODE == CONV_FWD) {
@@ -1709,11 +1683,16 @@ static bool stem_shape(const ConvGeom& q) {
 static bool rows_shape(const ConvGeom& q, int mode) {
   const int Cr = mode == CONV_FWD ? q.Cin : q.Cout;
   const int Ng = mode == CONV_DGRAD ? q.Cin : q.Cout;
+  // one replica's operand tensor is read through a buffer resource with
+  // 32-bit byte offsets
+  const long long opb = 4LL * q.Bt *
+                        (mode == CONV_FWD ? (long long)q.H * q.W * q.Cin
+                                          : (long long)q.Ho * q.Wo * q.Cout);
   return Cr % 16 == 0 && (Ng == 16 || Ng == 32 || Ng == 64) &&
          (q.stride == 1 || (q.stride == 2 && mode == CONV_FWD)) && ((uintptr_t)q.Wk & 15) == 0 &&
          (q.sW % 4 == 0) &&
          (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0 : ((uintptr_t)q.dy & 15) == 0) &&
-         (mode == CONV_DGRAD || q.rowmap || q.sx % 4 == 0);
+         (mode == CONV_DGRAD || (!q.rowmap && q.sx % 4 == 0)) && opb < (1LL << 31);
 }
 
 // Input gradients of the stride-2 convolutions: 16 -> 32 channels on 32-wide
