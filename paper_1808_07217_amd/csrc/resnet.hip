@@ -65,11 +65,12 @@ struct ConvArgs {
 };
 
 // The shifted, scaled BN output z = gamma * (y - mu) * inv + beta in one fixed
-// rounding order: the forward pass takes relu(z) (+ the shortcut) with it, and
+// rounding order, fma(y - mu, gamma * inv, beta): the forward pass takes
+// relu(z) (+ the shortcut) with it, and
 // the backward pass of a convolution followed by BN-ReLU alone recomputes the
 // ReLU mask z > 0 with it instead of reading the activation back.
 __device__ __forceinline__ float bn_z(float gm, float y, float m, float iv, float bt) {
-  return __builtin_fmaf(gm * (y - m), iv, bt);
+  return __builtin_fmaf(y - m, gm * iv, bt);
 }
 
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -1065,10 +1066,12 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
       // position of this lane's k: row 2w + ks/8, column 4 (ks%8) + lq
       const int pr = 2 * wave + (ks >> 3), pc = 4 * (ks & 7) + lq;
       const float bv = Dsh[(pr * W + pc) * CP + lm];
+      // the nine taps at constant offsets from the lane's tile position
+      const float* tb = T + (pr * TW + pc) * CP + lm;
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
         const int kh = t / 3, kw = t - kh * 3;
-        const float av = T[((pr + kh) * TW + pc + kw) * CP + lm];
+        const float av = tb[(kh * TW + kw) * CP];
         acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[t], 0, 0, 0);
       }
     }
