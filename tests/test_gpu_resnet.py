@@ -128,15 +128,20 @@ def test_resnet20_full_shape_first_round_model():
     (oracle only), and the round's per-step mean losses. Bar: normwise 1e-5,
     or, where the oracle itself moves further when its initial weights are
     perturbed by 1e-7 (eight independent draws, same file), the largest of
-    those distances (factor 1)."""
+    those distances times a factor calibrated on the draws alone, leave one
+    out: the largest ratio of a draw to max(1e-5, the largest of the others)
+    (at least 1) -- the largest of n draws understates where one more
+    legitimate run may land."""
     import json
     import os
     here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
     with open(os.path.join(here, "round1_resnet20.json")) as f:
         gold = json.load(f)
     model = np.load(os.path.join(here, "round1_resnet20_model.npy"))
-    assert len(gold["perturbed_round1_normwise"]) >= 3
-    bar = max(1e-5, max(gold["perturbed_round1_normwise"]))
+    d = list(gold["perturbed_round1_normwise"])
+    assert len(d) >= 3
+    factor = max([1.0] + [d[i] / max(1e-5, max(d[:i] + d[i + 1:])) for i in range(len(d))])
+    bar = max(1e-5, factor * max(d))
     w = wk.get("resnet20")
     X, y = wk.dataset(w)
     print("resnet20 full-shape round 1", flush=True)
@@ -147,7 +152,7 @@ def test_resnet20_full_shape_first_round_model():
     np.testing.assert_array_equal(got, reps.read_params(w.K - 1).cpu().numpy())
     err = normwise(got, model)
     lerr = rel(loss.cpu().numpy().mean(axis=1), np.asarray(gold["round1_step_mean_loss"]))
-    print(f"resnet20 round 1: model {err:.3e} (bar {bar:.3e}; oracle perturbed "
-          f"{gold['perturbed_round1_normwise']}), losses {lerr.max():.3e}", flush=True)
+    print(f"resnet20 round 1: model {err:.3e} (bar {bar:.3e}, leave-one-out factor "
+          f"{factor:.3f}; oracle perturbed {d}), losses {lerr.max():.3e}", flush=True)
     assert err <= bar
     assert np.all(lerr <= 1e-3)

@@ -26,23 +26,35 @@ CASES = [("mlp_512", 1e-3), ("postlocal_mlp_512", 1e-3),
 # the trajectory's own sensitivity. Where the oracle was also run from
 # initial weights perturbed by 1e-7 (relative; independent draws in
 # trajectory_<name>_perturbed.json, also the oracle's: eight for ResNet-20,
-# written by tests/golden/make_round_models.py), the bar at each step is
-# max(tol, the largest distance any draw has reached by that step) -- factor
-# 1, over at least three draws. ResNet-20's batch-normalised descent amplifies
-# a 1e-7 perturbation to about 2e-2 by the end of its five rounds.
+# written by tests/golden/make_round_models.py), the envelope at each step is
+# the largest distance any draw has reached by that step. ResNet-20's
+# batch-normalised descent amplifies a 1e-7 perturbation to about 2e-2 by the
+# end of its five rounds. The largest of n draws understates where one more
+# legitimate run may land, so the envelope is scaled by a factor calibrated
+# on the draws alone, leave one out: the largest ratio by which any draw
+# exceeds max(tol, the envelope of the others) (at least 1). The bar is
+# max(tol, factor x envelope), over at least three draws.
 
 
-def _perturbed_envelope(name, want):
+def _step_envelope(draws, want):
+    env = np.zeros_like(want)
+    for moved in draws:
+        env = np.maximum(env, np.maximum.accumulate(rel(moved, want)))
+    return env
+
+
+def _perturbed_envelope(name, want, tol):
     pert = os.path.join(HERE, "golden", f"trajectory_{name}_perturbed.json")
     if not os.path.exists(pert):
         return None
     with open(pert) as f:
-        draws = json.load(f)["draws"]
-    env = np.zeros_like(want)
-    for d in draws:
-        moved = np.concatenate([np.asarray(r) for r in d["per_round_step_mean_loss"]])
-        env = np.maximum(env, np.maximum.accumulate(rel(moved, want)))
-    return env, len(draws)
+        draws = [np.concatenate([np.asarray(r) for r in d["per_round_step_mean_loss"]])
+                 for d in json.load(f)["draws"]]
+    factor = 1.0
+    for i, d in enumerate(draws):
+        others = _step_envelope(draws[:i] + draws[i + 1:], want)
+        factor = max(factor, float(np.max(rel(d, want) / np.maximum(tol, others))))
+    return _step_envelope(draws, want), len(draws), factor
 
 
 @pytest.mark.parametrize("name,tol", CASES)
@@ -63,10 +75,12 @@ def test_full_run_loss_trajectory(name, tol):
     want = np.concatenate([np.asarray(r) for r in gold])
     err = rel(got, want)
     bar = np.full_like(err, tol)
-    env = _perturbed_envelope(name, want)
+    env = _perturbed_envelope(name, want, tol)
     if env is not None:
         assert env[1] >= 3
-        bar = np.maximum(bar, env[0])
+        bar = np.maximum(bar, env[2] * env[0])
+        print(f"{name}: {env[1]} perturbed oracle draws, leave-one-out factor {env[2]:.3f}",
+              flush=True)
     print(f"{name}: max relative loss error {err.max():.3e} at step "
           f"{int(err.argmax())} (bar there {bar[err.argmax()]:.3e}); final loss "
           f"{got[-1]:.5g} vs {want[-1]:.5g}", flush=True)
