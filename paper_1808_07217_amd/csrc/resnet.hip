@@ -1104,8 +1104,25 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_halo16(ConvArgs c) {
 // so no cross-wave sum is needed. Workgroup (g, split s) walks bands
 // [s per, (s + 1) per) of replica g, per = ceil(bands / S), in ascending
 // order; its partial sum lands in [S][G][9 CI][CO] for k_conv_wupdate.
+// LDS bytes of a k_conv_wgrad_band instance (both buffers).
 template <int CI, int CO, int STRIDE, int WO>
-__global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
+constexpr size_t wgrad_band_lds() {
+  constexpr int BH = 64 / WO;
+  constexpr int TH = (BH - 1) * STRIDE + 3, TW = (WO - 1) * STRIDE + 3;
+  return ((size_t)2 * (TH * TW * (CI + 4) + 64 * (CO + 4)) + 4 * CI) * sizeof(float);
+}
+// Workgroups per CU a k_conv_wgrad_band instance is built for: one for the
+// large accumulator sets (64 output channels), else as many as its LDS
+// allows, at most three (the register budget follows).
+template <int CI, int CO, int STRIDE, int WO>
+constexpr int wgrad_band_min_wgs() {
+  constexpr int lds_wgs = (int)(163840 / wgrad_band_lds<CI, CO, STRIDE, WO>());
+  return (9 * (CO / 16) + 3) / 4 * (CI / 16) > 16 ? 1 : (lds_wgs < 3 ? lds_wgs : 3);
+}
+
+template <int CI, int CO, int STRIDE, int WO>
+__global__ __launch_bounds__(kT, (wgrad_band_min_wgs<CI, CO, STRIDE, WO>())) void
+k_conv_wgrad_band(ConvArgs c) {
   constexpr int SP = 64, BH = SP / WO;
   constexpr int TH = (BH - 1) * STRIDE + 3, TW = (WO - 1) * STRIDE + 3;
   constexpr int XP = CI + 4, DP = CO + 4;               // LDS pitches (16-byte rows)
@@ -1124,7 +1141,15 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
   const int bpi = c.Ho / BH;                            // bands per image
   const int nbands = c.Bt * bpi, per = (nbands + S - 1) / S;
   const int b0 = sp * per, nbd = max(0, min(nbands, b0 + per) - b0);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // Large accumulator sets (64 output channels: one wave per SIMD) read the
+  // operands of step kk + 1 from LDS while step kk's MFMAs run; the smaller
+  // ones keep several waves per SIMD and read each step's operands as they
+  // go (measured: the read-ahead costs them occupancy and 50% more time).
+  constexpr bool kBig = PPW * MB > 16;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // (the small sets take the wave index as a scalar; measured: the large
+  // ones schedule worse with it)
+  const int wave = kBig ? tid >> 6 : __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lq = lane >> 4, lm = lane & 15;
   // a block's second convolution: the input BN-ReLU (statistics and
   // parameters per input channel in LDS; every float4 this thread stages
@@ -1205,30 +1230,29 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
     xoff[pp] = (kh * TW + kw) * XP + lm;
     doff[pp] = nbk * 16 + lm;
   }
-  // Large accumulator sets (64 output channels: one wave per SIMD) read the
-  // operands of step kk + 1 from LDS while step kk's MFMAs run; the smaller
-  // ones keep several waves per SIMD and read each step's operands as they
-  // go (measured: the read-ahead costs them occupancy and 50% more time).
-  constexpr bool kBig = PPW * MB > 16;
   auto compute = [&](int buf) __attribute__((always_inline)) {
     const float* X = Xs + buf * XF;
     const float* D = Ds + buf * DF;
     if constexpr (!kBig) {
+      // every pair slot computes (a slot past the last pair repeats the last
+      // pair's operands into accumulators that are never stored), so the
+      // reads of one step carry no branches and overlap the MFMAs
 #pragma unroll 2
       for (int kk = 0; kk < SP / 4; ++kk) {
         const int pos = kk * 4 + lq, orow = pos / WO, ocol = pos - orow * WO;
+        const int xb = (orow * STRIDE * TW + ocol * STRIDE) * XP, db = pos * DP;
+        float av[PPW][MB], bv[PPW];
 #pragma unroll
         for (int pp = 0; pp < PPW; ++pp) {
-          const int p = wave + 4 * pp;  // uniform over the wave
-          if (p < NP) {
-            const int tap = p / NB, nbk = p - tap * NB, kh = tap / 3, kw = tap - kh * 3;
-            const float bv = D[pos * DP + nbk * 16 + lm];
-            const float* xa = X + ((orow * STRIDE + kh) * TW + ocol * STRIDE + kw) * XP + lm;
+          bv[pp] = D[db + doff[pp]];
 #pragma unroll
-            for (int i = 0; i < MB; ++i)
-              acc[pp][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i * 16], bv, acc[pp][i], 0, 0, 0);
-          }
+          for (int i = 0; i < MB; ++i) av[pp][i] = X[xb + xoff[pp] + i * 16];
         }
+#pragma unroll
+        for (int pp = 0; pp < PPW; ++pp)
+#pragma unroll
+          for (int i = 0; i < MB; ++i)
+            acc[pp][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[pp][i], bv[pp], acc[pp][i], 0, 0, 0);
       }
       return;
     }
@@ -1317,14 +1341,6 @@ __global__ __launch_bounds__(kT) void k_conv_wgrad_band(ConvArgs c) {
           out[(long long)(tap * CI + i * 16 + 4 * lq + v) * CO + nbk * 16 + lm] = acc[pp][i][v];
     }
   }
-}
-
-// LDS bytes of a k_conv_wgrad_band instance (both buffers).
-template <int CI, int CO, int STRIDE, int WO>
-constexpr size_t wgrad_band_lds() {
-  constexpr int BH = 64 / WO;
-  constexpr int TH = (BH - 1) * STRIDE + 3, TW = (WO - 1) * STRIDE + 3;
-  return ((size_t)2 * (TH * TW * (CI + 4) + 64 * (CO + 4)) + 4 * CI) * sizeof(float);
 }
 
 // Weight gradient: sum the S partials (ascending s) and apply the update to
