@@ -35,6 +35,9 @@ struct ResPlan {
   int classes = 0, feat = 64, side_out = 8;
   size_t featb = 0, dfeat = 0, dzh = 0, gbuf[4] = {}, mu = 0, inv = 0, coef = 0,
          bnpart = 0, wpart = 0;
+  // per BN layer, the scale and shift its forward batch was normalised with
+  // ([kResConvs][K][64], layer i's [K][Cout] from i K 64)
+  size_t gsnap = 0, bsnap = 0;
   // BN running statistics [K][Rs] fp32: per replica the running means of
   // every BN layer in convolution order (layer i from rsoff[i]), then the
   // running variances in the same order (from rs_half); R = 2 rs_half
@@ -183,6 +186,8 @@ Layout make_resnet_layout(const lsgd_config* c) {
   for (int i = 0; i < 4; ++i) r.gbuf[i] = take(maxact);
   r.mu = take(kResConvs * K * 64 * 4);
   r.inv = take(kResConvs * K * 64 * 4);
+  r.gsnap = take(kResConvs * K * 64 * 4);
+  r.bsnap = take(kResConvs * K * 64 * 4);
   r.coef = take(K * 64 * 5 * 4);
   r.bnpart = take(maxbn);
   r.wpart = take(maxpart);
@@ -296,6 +301,9 @@ struct lsgd_ctx {
   // (default priority), with fork/join events; created at init
   hipStream_t side[2] = {nullptr, nullptr};
   hipEvent_t fork[2] = {nullptr, nullptr}, join[2] = {nullptr, nullptr};
+  // ResNet: completion of the side stream's weight gradients that read the
+  // gradient buffers 1 and 2
+  hipEvent_t done[2] = {nullptr, nullptr};
   bool use_side = false;
   Layout lay;
   const float* X = nullptr;
@@ -352,6 +360,7 @@ struct lsgd_ctx {
       }
       if (fork[i]) (void)hipEventDestroy(fork[i]);
       if (join[i]) (void)hipEventDestroy(join[i]);
+      if (done[i]) (void)hipEventDestroy(done[i]);
     }
   }
 
@@ -682,12 +691,16 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // the input of a block's second convolution is the first convolution's
   // BN-ReLU output, which is never stored: the kernels form it from that
   // convolution's pre-BN output (BN layer j) as they load it
+  // (the scale and shift as the forward batch used them: the backward pass
+  // steps gamma and beta while weight gradients that read them may still run)
+  float* gsnap = F(r.gsnap);
+  float* bsnap = F(r.bsnap);
   auto bn_input = [&](lsgd::ConvGeom& g, int j) {
     g.bn_mu = mu + (size_t)j * K * 64;
     g.bn_inv = inv + (size_t)j * K * 64;
-    g.bn_g = W + r.cv[j].offG;
-    g.bn_b = W + r.cv[j].offB;
-    g.bn_sP = Ps;
+    g.bn_g = gsnap + (size_t)j * K * 64;
+    g.bn_b = bsnap + (size_t)j * K * 64;
+    g.bn_sP = r.cv[j].Cout;
   };
 
   // forward: stem, then blocks (a: conv-BN-ReLU, b: conv-BN + shortcut, ReLU)
@@ -715,13 +728,17 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     // this replica's running statistics of BN layer i follow the batch
     float* rm = c->RS() + r.rsoff[i];
     float* rv = c->RS() + r.rs_half + r.rsoff[i];
+    float* gs = gsnap + (size_t)i * K * 64;
+    float* bs = bsnap + (size_t)i * K * 64;
     if (fused)
-      LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_finalize_chunks(bnpart, rows(i) / 256, K,
-                                                                 rows(i), q.Cout, mi, ii, rm,
-                                                                 rv, r.Rs, s));
+      LSGD_LAUNCH(c, "bn_stats",
+                  lsgd::launch_bn_finalize_chunks(bnpart, rows(i) / 256, K, rows(i), q.Cout,
+                                                  mi, ii, rm, rv, r.Rs, s, W + q.offG,
+                                                  W + q.offB, Ps, gs, bs));
     else
       LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
-                                                       mi, ii, rm, rv, r.Rs, s));
+                                                       mi, ii, rm, rv, r.Rs, s, W + q.offG,
+                                                       W + q.offB, Ps, gs, bs));
     if (i % 2 == 1) continue;  // a block's first BN-ReLU: formed by its consumers
     int mode = 0;
     const float* blk_in = nullptr;
@@ -801,7 +818,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // per-split partials, then their fixed-order sum and the update (after
   // any input gradient that reads the old weight)
   // (bn_layer >= 0: x is that BN layer's pre-BN output, see bn_input)
-  auto wgrad = [&](int i, const float* x, const float* dy, int bn_layer) -> lsgd_status {
+  auto wgrad = [&](int i, const float* x, const float* dy, int bn_layer,
+                   hipStream_t ws) -> lsgd_status {
     const ConvSpec& q = r.cv[i];
     lsgd::ConvGeom g = geom(i);
     if (i == 0) {
@@ -814,12 +832,41 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     }
     g.dy = dy;
     g.out = wpart;
-    LSGD_LAUNCH(c, "conv_wgrad", lsgd::launch_conv(lsgd::CONV_WGRAD_MODE, g, s));
-    LSGD_LAUNCH(c, "conv_wupdate",
-                lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo), K,
-                                          9 * q.Cin * q.Cout, W + q.offW, U + q.offW, Ps,
-                                          lr, cf.momentum, cf.weight_decay, upd_mode(cf),
-                                          s));
+    LSGD_LAUNCH_ON(c, ws, "conv_wgrad", lsgd::launch_conv(lsgd::CONV_WGRAD_MODE, g, ws));
+    LSGD_LAUNCH_ON(c, ws, "conv_wupdate",
+                   lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo),
+                                             K, 9 * q.Cin * q.Cout, W + q.offW, U + q.offW,
+                                             Ps, lr, cf.momentum, cf.weight_decay,
+                                             upd_mode(cf), ws));
+    return LSGD_OK;
+  };
+  // The weight gradients (and updates) of the blocks run on side stream 1:
+  // each forks after the input gradient that last reads its weights, and
+  // overlaps the BN backward passes and input gradients that follow on the
+  // main stream. Gradient buffer 1 (a block's second BN's dy) and 2 (its
+  // first BN's dy, formed in place over the gradient it came from) are
+  // rewritten only after the weight gradient reading them has completed
+  // (events done[0], done[1]); one wpart serves all, in the side stream's
+  // order. Without side streams everything runs in order on the main stream.
+  const bool sidew = c->use_side;
+  hipStream_t ws = sidew ? c->side[1] : s;
+  bool pend[2] = {false, false};
+  auto release = [&](int k) -> lsgd_status {  // before gradient buffer 1 + k is rewritten
+    if (pend[k]) LSGD_CK(c, hipStreamWaitEvent(s, c->done[k], 0));
+    pend[k] = false;
+    return LSGD_OK;
+  };
+  auto fork_wgrad = [&](int i, const float* x, const float* dy, int bn_layer,
+                        int k) -> lsgd_status {
+    if (sidew) {
+      LSGD_CK(c, hipEventRecord(c->fork[1], s));
+      LSGD_CK(c, hipStreamWaitEvent(ws, c->fork[1], 0));
+    }
+    if (lsgd_status st = wgrad(i, x, dy, bn_layer, ws)) return st;
+    if (sidew) {
+      LSGD_CK(c, hipEventRecord(c->done[k], ws));
+      pend[k] = true;
+    }
     return LSGD_OK;
   };
   // input gradient of conv i (reads the old weight, before its update).
@@ -852,27 +899,34 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     const float* h_in = F(r.cv[ia - 1].act);
     const int nxt = cur == 0 ? 3 : 0;
     // second convolution: its output went through the shortcut add and ReLU
+    if (lsgd_status st = release(0)) return st;
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1], 0));
     bool sums_fused = false, sc_fused = false;
+    if (lsgd_status st = release(1)) return st;
     if (lsgd_status st = dgrad(ib, gb[1], gb[2], nullptr, nullptr, ia, &sums_fused)) return st;
-    if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), gb[1], ia)) return st;
+    if (lsgd_status st = fork_wgrad(ib, F(r.cv[ia].y), gb[1], ia, 0)) return st;
     // first convolution: ReLU'd BN output, the mask recomputed from its input
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[1], sums_fused ? rows(ia) / 256 : 0));
+    // (dy in place over its gradient)
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[2], sums_fused ? rows(ia) / 256 : 0));
     // the block-input gradient: the convolution path, and the shortcut's share
     // of the block-output gradient (in the input gradient's epilogue where it can)
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
-    if (lsgd_status st = dgrad(ia, gb[1], gb[nxt], mode == 1 ? gb[cur] : nullptr,
+    if (lsgd_status st = dgrad(ia, gb[2], gb[nxt], mode == 1 ? gb[cur] : nullptr,
                                F(r.cv[ib].act), -1, &sc_fused))
       return st;
-    if (lsgd_status st = wgrad(ia, h_in, gb[1], -1)) return st;
+    if (lsgd_status st = fork_wgrad(ia, h_in, gb[2], -1, 1)) return st;
     if (!sc_fused)
       LSGD_LAUNCH(c, "shortcut_bwd",
                   lsgd::launch_shortcut_grad(gb[nxt], gb[cur], F(r.cv[ib].act), K, B,
                                              qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
     cur = nxt;
   }
+  if (lsgd_status st = release(0)) return st;
   LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1], 0));
-  if (lsgd_status st = wgrad(0, nullptr, gb[1], -1)) return st;
+  // join (the side stream's last work is done: all its updates, and wpart is
+  // free for the stem's weight gradient)
+  if (lsgd_status st = release(1)) return st;
+  if (lsgd_status st = wgrad(0, nullptr, gb[1], -1, s)) return st;
   c->step += 1;
   return LSGD_OK;
 }
@@ -1123,12 +1177,16 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
                                    c->stream), "running statistics to every replica");
   }
   // side streams pay off once there is a hidden layer (an update that can
-  // overlap the rest of the backward pass)
-  if (st == LSGD_OK && ly.head && ly.L >= 2) {
+  // overlap the rest of the backward pass), and for ResNet-20 (its weight
+  // gradients overlap the BN backward passes)
+  const bool resnet = c->cfg.model == LSGD_MODEL_RESNET20;
+  if (st == LSGD_OK && ((ly.head && ly.L >= 2) || resnet)) {
     for (int i = 0; i < 2; ++i) {
       check(hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking), "side stream");
       check(hipEventCreateWithFlags(&c->fork[i], hipEventDisableTiming), "fork event");
       check(hipEventCreateWithFlags(&c->join[i], hipEventDisableTiming), "join event");
+      if (resnet)
+        check(hipEventCreateWithFlags(&c->done[i], hipEventDisableTiming), "done event");
     }
     c->use_side = st == LSGD_OK;
   }

@@ -189,10 +189,16 @@ int conv_wgrad_splits(int Bt, int Ho, int Wo);
 bool conv_fwd_stats(const ConvGeom& q);
 // Both finalisers also update the running statistics when rm is set: the
 // running means rm[g * sRS + c] and variances rv[g * sRS + c] of replica g
-// (factor 0.1 on the batch mean and the unbiased batch variance).
+// (factor 0.1 on the batch mean and the unbiased batch variance); and, when
+// gsnap is set, copy the BN scale and shift the batch is normalised with
+// (gamma, beta at g * sP + c) to gsnap, bsnap [G][C], so that readers of the
+// forward's BN-ReLU see them after the backward pass has stepped gamma, beta.
 hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
                                      float* mu, float* inv, float* rm, float* rv,
-                                     long long sRS, hipStream_t st);
+                                     long long sRS, hipStream_t st,
+                                     const float* gamma = nullptr,
+                                     const float* beta = nullptr, long long sP = 0,
+                                     float* gsnap = nullptr, float* bsnap = nullptr);
 int bn_chunks(int R);
 hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st);
 hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, float* W,
@@ -200,7 +206,9 @@ hipError_t launch_conv_wupdate(const float* part, int splits, int G, int n, floa
                                int nesterov, hipStream_t st);
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
                            float* mu, float* inv, float* rm, float* rv, long long sRS,
-                           hipStream_t st);
+                           hipStream_t st, const float* gamma = nullptr,
+                           const float* beta = nullptr, long long sP = 0,
+                           float* gsnap = nullptr, float* bsnap = nullptr);
 hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,

@@ -1410,7 +1410,8 @@ __device__ __forceinline__ void bn_running(float* rm, float* rv, long long o, do
 __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
     const double* part, int nchunk, int C, int R, float* mu, float* inv, float* coef,
     float* gamma, float* beta, float* ug, float* ub, long long sP, float lr, float mom,
-    int nesterov, float eps, float* rm, float* rv, long long sRS) {
+    int nesterov, float eps, float* rm, float* rv, long long sRS, float* gsnap,
+    float* bsnap) {
   __shared__ double red[2][kT];
   const int g = blockIdx.x, t = threadIdx.x;
   const int L = kT / C, c = t % C, q = t / C;
@@ -1442,6 +1443,10 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
     mu[i] = (float)m;
     inv[i] = (float)(1.0 / sqrt(var + (double)eps));
     if (rm) bn_running(rm, rv, (long long)g * sRS + c, m, var, R);
+    if (gsnap) {  // the scale and shift this batch is normalised with
+      gsnap[i] = gamma[(long long)g * sP + c];
+      bsnap[i] = beta[(long long)g * sP + c];
+    }
     return;
   }
   const long long o = (long long)g * sP + c;
@@ -1970,24 +1975,29 @@ static bool bn_shape_ok(int G, int R, int C) {
 
 hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
                            float* mu, float* inv, float* rm, float* rv, long long sRS,
-                           hipStream_t st) {
-  if (!bn_shape_ok(G, R, C) || !al16p(y)) return hipErrorInvalidValue;
+                           hipStream_t st, const float* gamma, const float* beta,
+                           long long sP, float* gsnap, float* bsnap) {
+  if (!bn_shape_ok(G, R, C) || !al16p(y) || (gsnap && (!gamma || !beta || !bsnap)))
+    return hipErrorInvalidValue;
   const int nch = bn_chunks(R);
   hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, nullptr,
                      nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, part, nch);
   hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R, mu,
-                     inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
-                     1e-5f, rm, rv, sRS);
+                     inv, nullptr, (float*)gamma, (float*)beta, nullptr, nullptr, sP, 0.f,
+                     0.f, 0, 1e-5f, rm, rv, sRS, gsnap, bsnap);
   return hipGetLastError();
 }
 
 hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int R, int C,
                                      float* mu, float* inv, float* rm, float* rv,
-                                     long long sRS, hipStream_t st) {
-  if (!bn_shape_ok(G, R, C)) return hipErrorInvalidValue;
+                                     long long sRS, hipStream_t st, const float* gamma,
+                                     const float* beta, long long sP, float* gsnap,
+                                     float* bsnap) {
+  if (!bn_shape_ok(G, R, C) || (gsnap && (!gamma || !beta || !bsnap)))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nchunk, C, R, mu,
-                     inv, nullptr, nullptr, nullptr, nullptr, nullptr, 0LL, 0.f, 0.f, 0,
-                     1e-5f, rm, rv, sRS);
+                     inv, nullptr, (float*)gamma, (float*)beta, nullptr, nullptr, sP, 0.f,
+                     0.f, 0, 1e-5f, rm, rv, sRS, gsnap, bsnap);
   return hipGetLastError();
 }
 
@@ -2018,7 +2028,7 @@ hipError_t launch_bn_backward(const float* y, const float* gup, const float* mas
                        mu, inv, gamma, beta, sP, part, nch);
   hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
                      (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
-                     nesterov, 1e-5f, nullptr, nullptr, 0LL);
+                     nesterov, 1e-5f, nullptr, nullptr, 0LL, nullptr, nullptr);
   hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
                      st, y, gup, maskv, R, C, mu, inv, coef, dy);
   return hipGetLastError();
