@@ -33,7 +33,9 @@ struct ResPlan {
   ConvSpec cv[kResConvs];
   int64_t offFcW = 0, offFcB = 0;
   int classes = 0, feat = 64, side_out = 8;
-  size_t featb = 0, dfeat = 0, dzh = 0, gbuf[4] = {}, mu = 0, inv = 0, coef = 0,
+  // gradient buffers: 0 and 3 the block-output and block-input gradients,
+  // 1, 2 (4, 5) a block's two BN input gradients, by the block's parity
+  size_t featb = 0, dfeat = 0, dzh = 0, gbuf[6] = {}, mu = 0, inv = 0, coef = 0,
          bnpart = 0, wpart = 0;
   // per BN layer, the scale and shift its forward batch was normalised with
   // ([kResConvs][K][64], layer i's [K][Cout] from i K 64)
@@ -183,7 +185,7 @@ Layout make_resnet_layout(const lsgd_config* c) {
   r.featb = take(K * B * 64 * 4);
   r.dfeat = take(K * B * 64 * 4);
   r.dzh = take(K * B * r.classes * 4);
-  for (int i = 0; i < 4; ++i) r.gbuf[i] = take(maxact);
+  for (int i = 0; i < 6; ++i) r.gbuf[i] = take(maxact);
   r.mu = take(kResConvs * K * 64 * 4);
   r.inv = take(kResConvs * K * 64 * 4);
   r.gsnap = take(kResConvs * K * 64 * 4);
@@ -796,7 +798,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(0, h, s));
 
   // backward
-  float* gb[4] = {F(r.gbuf[0]), F(r.gbuf[1]), F(r.gbuf[2]), F(r.gbuf[3])};
+  float* gb[6];
+  for (int i = 0; i < 6; ++i) gb[i] = F(r.gbuf[i]);
   float* coef = F(r.coef);
   float* wpart = F(r.wpart);
   LSGD_LAUNCH(c, "gap_bwd", lsgd::launch_gap(nullptr, K * B, S, 64, nullptr, true,
@@ -840,33 +843,22 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                              upd_mode(cf), ws));
     return LSGD_OK;
   };
-  // The weight gradients (and updates) of the blocks run on side stream 1:
-  // each forks after the input gradient that last reads its weights, and
-  // overlaps the BN backward passes and input gradients that follow on the
-  // main stream. Gradient buffer 1 (a block's second BN's dy) and 2 (its
-  // first BN's dy, formed in place over the gradient it came from) are
-  // rewritten only after the weight gradient reading them has completed
-  // (events done[0], done[1]); one wpart serves all, in the side stream's
-  // order. Without side streams everything runs in order on the main stream.
+  // The weight gradients (and updates) of a block run on side stream 1: they
+  // fork after the block's last input gradient (the last reader of its
+  // weights) and overlap the next block's BN backward passes and input
+  // gradients on the main stream. A block's two BN input gradients (the
+  // second BN's, and the first BN's formed in place over the gradient it
+  // came from) live in buffers 1, 2 or 4, 5 by the block's parity, so the
+  // main stream rewrites them two blocks later, after event done[parity]
+  // says the side stream has read them; one wpart serves all, in the side
+  // stream's order. Without side streams everything runs in order on the
+  // main stream.
   const bool sidew = c->use_side;
   hipStream_t ws = sidew ? c->side[1] : s;
   bool pend[2] = {false, false};
-  auto release = [&](int k) -> lsgd_status {  // before gradient buffer 1 + k is rewritten
+  auto release = [&](int k) -> lsgd_status {  // before parity k's buffers are rewritten
     if (pend[k]) LSGD_CK(c, hipStreamWaitEvent(s, c->done[k], 0));
     pend[k] = false;
-    return LSGD_OK;
-  };
-  auto fork_wgrad = [&](int i, const float* x, const float* dy, int bn_layer,
-                        int k) -> lsgd_status {
-    if (sidew) {
-      LSGD_CK(c, hipEventRecord(c->fork[1], s));
-      LSGD_CK(c, hipStreamWaitEvent(ws, c->fork[1], 0));
-    }
-    if (lsgd_status st = wgrad(i, x, dy, bn_layer, ws)) return st;
-    if (sidew) {
-      LSGD_CK(c, hipEventRecord(c->done[k], ws));
-      pend[k] = true;
-    }
     return LSGD_OK;
   };
   // input gradient of conv i (reads the old weight, before its update).
@@ -894,38 +886,47 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   };
 
   for (int blk = 8; blk >= 0; --blk) {
-    const int ia = 2 * blk + 1, ib = 2 * blk + 2;
+    const int ia = 2 * blk + 1, ib = 2 * blk + 2, par = blk & 1;
     const ConvSpec& qa = r.cv[ia];
     const float* h_in = F(r.cv[ia - 1].act);
     const int nxt = cur == 0 ? 3 : 0;
+    float* g1 = gb[par ? 4 : 1];
+    float* g2 = gb[par ? 5 : 2];
+    if (lsgd_status st = release(par)) return st;
     // second convolution: its output went through the shortcut add and ReLU
-    if (lsgd_status st = release(0)) return st;
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), gb[1], 0));
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), g1, 0));
     bool sums_fused = false, sc_fused = false;
-    if (lsgd_status st = release(1)) return st;
-    if (lsgd_status st = dgrad(ib, gb[1], gb[2], nullptr, nullptr, ia, &sums_fused)) return st;
-    if (lsgd_status st = fork_wgrad(ib, F(r.cv[ia].y), gb[1], ia, 0)) return st;
+    if (lsgd_status st = dgrad(ib, g1, g2, nullptr, nullptr, ia, &sums_fused)) return st;
     // first convolution: ReLU'd BN output, the mask recomputed from its input
     // (dy in place over its gradient)
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, gb[2], nullptr, gb[2], sums_fused ? rows(ia) / 256 : 0));
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, g2, nullptr, g2, sums_fused ? rows(ia) / 256 : 0));
     // the block-input gradient: the convolution path, and the shortcut's share
     // of the block-output gradient (in the input gradient's epilogue where it can)
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
-    if (lsgd_status st = dgrad(ia, gb[2], gb[nxt], mode == 1 ? gb[cur] : nullptr,
+    if (lsgd_status st = dgrad(ia, g2, gb[nxt], mode == 1 ? gb[cur] : nullptr,
                                F(r.cv[ib].act), -1, &sc_fused))
       return st;
-    if (lsgd_status st = fork_wgrad(ia, h_in, gb[2], -1, 1)) return st;
+    if (sidew) {
+      LSGD_CK(c, hipEventRecord(c->fork[1], s));
+      LSGD_CK(c, hipStreamWaitEvent(ws, c->fork[1], 0));
+    }
+    if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), g1, ia, ws)) return st;
+    if (lsgd_status st = wgrad(ia, h_in, g2, -1, ws)) return st;
+    if (sidew) {
+      LSGD_CK(c, hipEventRecord(c->done[par], ws));
+      pend[par] = true;
+    }
     if (!sc_fused)
       LSGD_LAUNCH(c, "shortcut_bwd",
                   lsgd::launch_shortcut_grad(gb[nxt], gb[cur], F(r.cv[ib].act), K, B,
                                              qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
     cur = nxt;
   }
+  // join (the side stream's last work, block 0's, was recorded last: all its
+  // updates are done, and wpart is free for the stem's weight gradient)
+  if (lsgd_status st = release(1)) return st;
   if (lsgd_status st = release(0)) return st;
   LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1], 0));
-  // join (the side stream's last work is done: all its updates, and wpart is
-  // free for the stem's weight gradient)
-  if (lsgd_status st = release(1)) return st;
   if (lsgd_status st = wgrad(0, nullptr, gb[1], -1, s)) return st;
   c->step += 1;
   return LSGD_OK;
