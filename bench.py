@@ -478,7 +478,7 @@ def main():
         print(json.dumps(write_traffic(args.traffic_from, w, tag)))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU "
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU "
               "path (the K workers are replicas on one device)", file=sys.stderr)
         sys.exit(2)
 

@@ -58,7 +58,7 @@ typedef enum lsgd_status {
   LSGD_E_WORKSPACE = 2,   /* workspace smaller than lsgd_workspace_bytes */
   LSGD_E_HIP = 3,         /* a HIP runtime call or launch failed (latched) */
   LSGD_E_STATE = 4,       /* context unusable after an earlier HIP error */
-  LSGD_E_UNSUPPORTED = 5, /* valid request this build does not implement */
+  LSGD_E_UNSUPPORTED = 5, /* valid request the library does not implement */
   LSGD_E_NONFINITE = 6    /* a local step's loss was not finite (sticky; see
                              lsgd_sync) */
 } lsgd_status;
