@@ -226,8 +226,34 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       bnp[2][t] = c.bn_g[(long long)g * c.bn_sP + t];
       bnp[3][t] = c.bn_b[(long long)g * c.bn_sP + t];
     }
-    __syncthreads();
   }
+  // Input gradient with up to 32 channels (and at most 32 reduction
+  // channels): the replica's whole weight goes to LDS once, as B^T rows
+  // [tap][n][k] with k contiguous (pitch BP), so a slab's B values are one
+  // LDS float4 per column block; otherwise they are read from L1/L2 slab by
+  // slab (measured: the forward's transposing staging costs it more than
+  // the LDS reads save).
+  constexpr bool kLdsB = MODE == CONV_DGRAD && BN <= 32;
+  constexpr int BP = 32 + 4;
+  __shared__ __attribute__((aligned(16))) float Bsm[kLdsB ? 9 * BN * BP : 4];
+  if constexpr (kLdsB) {
+    // W [9 Cin][Cout]: forward, B^T[tap][co][ci] = W[(tap, ci)][co]; input
+    // gradient, B^T[tap][ci][co] = W[(tap, ci)][co]
+    const float* Wg = c.Wk + (long long)g * c.sW;
+    const int nq = 9 * c.Cin * c.Cout / 4;
+    for (int q = tid; q < nq; q += kT) {
+      const int e0 = 4 * q, row = e0 / c.Cout, co = e0 - row * c.Cout;
+      const int tap = row / c.Cin, ci = row - tap * c.Cin;
+      const v4f w = *(const v4f*)(Wg + e0);
+      if constexpr (MODE == CONV_FWD) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Bsm[(tap * BN + co + e) * BP + ci] = w[e];
+      } else {
+        *(v4f*)&Bsm[(tap * BN + ci) * BP + co] = w;
+      }
+    }
+  }
+  if (kLdsB || bnin || (EPI & kEpiBnSums) != 0) __syncthreads();
   // the lane's B offsets: forward, rows ch + e of W at column 16 j + l%16;
   // input gradient, row (tap, 16 j + l%16) of W at columns ch .. ch + 3
   int boff[NBL];
@@ -251,6 +277,13 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     }
     t.okm = okm;
     t.ch = cb + 4 * lq;
+    if constexpr (kLdsB) {
+      // B^T row (tap, 16 j + l%16), reduction channels ch .. ch + 3
+      const float* bb = Bsm + (ti * BN + lm) * BP + cb + 4 * lq;
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) t.b[j] = *(const v4f*)(bb + j * 16 * BP);
+      return;
+    }
     // scalar part of the weights' offset
     const int sb = MODE == CONV_FWD ? (ti * Cr + cb) * BN * 4 : (ti * BN * Cr + cb) * 4;
 #pragma unroll
@@ -1712,7 +1745,10 @@ static bool rows_shape(const ConvGeom& q, int mode) {
   const long long opb = 4LL * q.Bt *
                         (mode == CONV_FWD ? (long long)q.H * q.W * q.Cin
                                           : (long long)q.Ho * q.Wo * q.Cout);
+  // (an input gradient with up to 32 channels stages the whole weight in
+  // LDS: at most 32 reduction channels)
   return Cr % 16 == 0 && (Ng == 16 || Ng == 32 || Ng == 64) &&
+         (mode == CONV_FWD || Ng == 64 || Cr <= 32) &&
          (q.stride == 1 || (q.stride == 2 && mode == CONV_FWD)) && ((uintptr_t)q.Wk & 15) == 0 &&
          (q.sW % 4 == 0) &&
          (mode == CONV_FWD ? ((uintptr_t)q.x & 15) == 0 : ((uintptr_t)q.dy & 15) == 0) &&
