@@ -862,22 +862,29 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     return LSGD_OK;
   };
   // input gradient of conv i (reads the old weight, before its update).
-  // Where the kernel takes epilogues (*fused set): with sc_dh, sc_h the
-  // identity shortcut's share of the block-output gradient goes into dx; with
-  // bs_layer >= 0 the backward sums of BN layer bs_layer (whose activation
-  // gradient dx is) go to bnpart.
+  // Where the kernel takes the epilogues: with sc_dh, sc_h the identity
+  // shortcut's share of the block-output gradient goes into dx (*sc_fused);
+  // with bs_layer >= 0 the backward sums of BN layer bs_layer, whose
+  // activation's gradient dx is, go to bnpart (*sums_fused) -- its ReLU mask
+  // recomputed from the pre-BN output, or, with bs_act, read from that
+  // activation (a BN whose ReLU follows a shortcut add).
   auto dgrad = [&](int i, const float* dy, float* dx, const float* sc_dh, const float* sc_h,
-                   int bs_layer, bool* fused) -> lsgd_status {
+                   int bs_layer, const float* bs_act, bool* sc_fused,
+                   bool* sums_fused) -> lsgd_status {
     lsgd::ConvGeom g = geom(i);
     g.dy = dy;
     g.out = dx;
-    *fused = (sc_dh && (lsgd::conv_dgrad_epilogues(g) & 1)) ||
-             (bs_layer >= 0 && (lsgd::conv_dgrad_epilogues(g) & 2));
-    if (*fused && sc_dh) {
+    const int cap = lsgd::conv_dgrad_epilogues(g);
+    *sc_fused = sc_dh && (cap & 1);
+    *sums_fused = bs_layer >= 0 && (cap & (bs_act ? 4 : 2)) &&
+                  rows(bs_layer) == B * r.cv[i].H * r.cv[i].W && rows(bs_layer) % 256 == 0;
+    if (*sc_fused) {
       g.sc_dh = sc_dh;
       g.sc_h = sc_h;
-    } else if (*fused) {
+    }
+    if (*sums_fused) {
       g.bs_y = F(r.cv[bs_layer].y);
+      g.bs_h = bs_act;
       g.bs_part = bnpart;
       bn_input(g, bs_layer);
     }
@@ -885,6 +892,9 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     return LSGD_OK;
   };
 
+  // (out_sums: the backward sums of the BN whose output's gradient the last
+  // block-input gradient was are in bnpart already)
+  bool out_sums = false;
   for (int blk = 8; blk >= 0; --blk) {
     const int ia = 2 * blk + 1, ib = 2 * blk + 2, par = blk & 1;
     const ConvSpec& qa = r.cv[ia];
@@ -894,17 +904,25 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     float* g2 = gb[par ? 5 : 2];
     if (lsgd_status st = release(par)) return st;
     // second convolution: its output went through the shortcut add and ReLU
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), g1, 0));
-    bool sums_fused = false, sc_fused = false;
-    if (lsgd_status st = dgrad(ib, g1, g2, nullptr, nullptr, ia, &sums_fused)) return st;
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), g1,
+                                    out_sums ? rows(ib) / 256 : 0));
+    bool sums_fused = false, sc_fused = false, unused = false;
+    if (lsgd_status st = dgrad(ib, g1, g2, nullptr, nullptr, ia, nullptr, &unused, &sums_fused))
+      return st;
     // first convolution: ReLU'd BN output, the mask recomputed from its input
     // (dy in place over its gradient)
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ia, g2, nullptr, g2, sums_fused ? rows(ia) / 256 : 0));
     // the block-input gradient: the convolution path, and the shortcut's share
-    // of the block-output gradient (in the input gradient's epilogue where it can)
+    // of the block-output gradient, and (identity blocks) the backward sums of
+    // the BN before the block input -- the previous block's second BN, masked
+    // by its activation, or the stem's -- in the input gradient's epilogue
+    // where it can
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
+    const int prev_bn = ia - 1;
     if (lsgd_status st = dgrad(ia, g2, gb[nxt], mode == 1 ? gb[cur] : nullptr,
-                               F(r.cv[ib].act), -1, &sc_fused))
+                               F(r.cv[ib].act), mode == 1 ? prev_bn : -1,
+                               prev_bn > 0 ? F(r.cv[prev_bn].act) : nullptr, &sc_fused,
+                               &out_sums))
       return st;
     if (sidew) {
       LSGD_CK(c, hipEventRecord(c->fork[1], s));
@@ -926,7 +944,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // updates are done, and wpart is free for the stem's weight gradient)
   if (lsgd_status st = release(1)) return st;
   if (lsgd_status st = release(0)) return st;
-  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1], 0));
+  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1], out_sums ? rows(0) / 256 : 0));
   if (lsgd_status st = wgrad(0, nullptr, gb[1], -1, s)) return st;
   c->step += 1;
   return LSGD_OK;

@@ -163,24 +163,29 @@ struct ConvGeom {
   const float* bn_g;
   const float* bn_b;
   long long bn_sP;
-  // input gradient, where conv_dgrad_epilogues(q) (nullptr: none; at most one
-  // of the two per launch):
+  // input gradient, where conv_dgrad_epilogues(q) (nullptr: none):
   //  * sc_dh, sc_h: the block output's gradient and activation (same shape as
   //    dx, identity shortcut): dx gains sc_dh where sc_h > 0;
-  //  * bs_part: dx is the gradient of a BN-ReLU's output whose pre-BN values
-  //    are bs_y (same shape) and whose statistics and parameters come in
-  //    bn_* (as above): the BN backward sums (sum dz, sum dz x^ with dz = dx
-  //    where gamma (y - mu) inv + beta > 0 and x^ = (y - mu) inv) are written
-  //    per 256-row chunk, [G][R/256][Cin][2] doubles, for
-  //    launch_bn_backward's fused_nchunk
+  //  * bs_part: dx (with the shortcut's share, when both are set) is the
+  //    gradient of a BN-ReLU's output whose pre-BN values are bs_y (same
+  //    shape) and whose statistics and parameters come in bn_* (as above):
+  //    the BN backward sums (sum dz, sum dz x^ with x^ = (y - mu) inv) are
+  //    written per 256-row chunk, [G][R/256][Cin][2] doubles, for
+  //    launch_bn_backward's fused_nchunk; dz = dx where
+  //    gamma (y - mu) inv + beta > 0, or, with bs_h set (a BN whose ReLU
+  //    follows a shortcut add), where the activation bs_h > 0 (bn_g, bn_b
+  //    then unused)
   const float* sc_dh;
   const float* sc_h;
   const float* bs_y;
+  const float* bs_h;
   double* bs_part;
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
 // Which epilogues the input-gradient launch of q takes: bit 0 the shortcut
-// share (sc_*), bit 1 the BN backward sums (bs_*).
+// share (sc_*), bit 1 the BN backward sums with the recomputed mask (bs_*),
+// bit 2 the sums with the activation mask (bs_h). A launch takes one of them,
+// or the shortcut with one kind of sums.
 int conv_dgrad_epilogues(const ConvGeom& q);
 int conv_wgrad_splits(int Bt, int Ho, int Wo);
 // Whether the forward convolution of q writes its output's BN statistics

@@ -61,6 +61,7 @@ struct ConvArgs {
   const float* sc_dh;
   const float* sc_h;
   const float* bs_y;
+  const float* bs_h;
   double* bs_part;
 };
 
@@ -118,8 +119,13 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
 //     c.bs_y and BN parameters come in c.bn_*: per 256 output rows, the
 //     backward sums sum dz and sum dz x^ (dz = dx where the ReLU passed,
 //     x^ = (y - mu) inv) go to c.bs_part as one chunk, in the forward
-//     statistics' layout.
-constexpr int kEpiShortcut = 1, kEpiBnSums = 2;
+//     statistics' layout;
+//   kEpiBnSumsAct: the same sums where the ReLU follows a shortcut add (a
+//     block's second BN): dz = dx where the activation c.bs_h > 0.
+// The shortcut combines with either sums (dx then includes the shortcut
+// share); the sums' operands are then loaded after the k work, where the
+// shortcut's are free.
+constexpr int kEpiShortcut = 1, kEpiBnSums = 2, kEpiBnSumsAct = 4;
 
 // Forward / input-gradient convolution for reduction channel counts that
 // are multiples of 16 (every convolution after the first): the output tile
@@ -219,7 +225,10 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   // and parameters of every input channel staged in LDS
   const bool bnin = MODE == CONV_FWD && c.bn_mu != nullptr;
   __shared__ __attribute__((aligned(16))) float bnp[4][64];
-  if (bnin || (EPI & kEpiBnSums) != 0) {  // (kEpiBnSums: the layer of dx, Cin channels)
+  constexpr bool kSc = (EPI & kEpiShortcut) != 0;
+  constexpr bool kSums = (EPI & (kEpiBnSums | kEpiBnSumsAct)) != 0;
+  constexpr bool kMaskAct = (EPI & kEpiBnSumsAct) != 0;
+  if (bnin || kSums) {  // (the sums: the BN layer of dx, Cin channels)
     for (int t = tid; t < c.Cin; t += kT) {
       bnp[0][t] = c.bn_mu[(long long)g * c.Cin + t];
       bnp[1][t] = c.bn_inv[(long long)g * c.Cin + t];
@@ -253,7 +262,7 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       }
     }
   }
-  if (kLdsB || bnin || (EPI & kEpiBnSums) != 0) __syncthreads();
+  if (kLdsB || bnin || kSums) __syncthreads();
   // the lane's B offsets: forward, rows ch + e of W at column 16 j + l%16;
   // input gradient, row (tap, 16 j + l%16) of W at columns ch .. ch + 3
   int boff[NBL];
@@ -333,26 +342,39 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][s], t.b[j][s], acc[i][j], 0, 0, 0);
   };
   // epilogue operands of this lane's outputs (row block i, column block j,
-  // register v), issued while the last slabs compute
-  float e0[EPI ? 4 : 1][EPI ? NBL : 1][4], e1[(EPI & kEpiShortcut) ? 4 : 1][NBL][4];
-  auto eload = [&]() __attribute__((always_inline)) {
-    if constexpr (EPI != 0) {
+  // register v): the shortcut's (eh, edh), or the sums' alone (ey and, with
+  // the activation mask, ea), issued while the last slabs compute; the sums'
+  // next to the shortcut's after the k work
+  float eh[kSc ? 4 : 1][kSc ? NBL : 1][4], edh[kSc ? 4 : 1][kSc ? NBL : 1][4];
+  float ey[kSums ? 4 : 1][kSums ? NBL : 1][4], ea[kMaskAct ? 4 : 1][kMaskAct ? NBL : 1][4];
+  auto eoff = [&](int i, int j, int v) __attribute__((always_inline)) {
+    const int m = min(m0 + wave * 64 + i * 16 + lq * 4 + v, Mg - 1);
+    return ((long long)g * Mg + m) * BN + j * 16 + lm;
+  };
+  auto sc_load = [&]() __attribute__((always_inline)) {
+    if constexpr (kSc) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int m = min(m0 + wave * 64 + i * 16 + lq * 4 + v, Mg - 1);
+        for (int v = 0; v < 4; ++v)
 #pragma unroll
           for (int j = 0; j < NBL; ++j) {
-            const long long o = ((long long)g * Mg + m) * BN + j * 16 + lm;
-            if constexpr ((EPI & kEpiShortcut) != 0) {
-              e0[i][j][v] = c.sc_h[o];
-              e1[i][j][v] = c.sc_dh[o];
-            } else {
-              e0[i][j][v] = c.bs_y[o];
-            }
+            eh[i][j][v] = c.sc_h[eoff(i, j, v)];
+            edh[i][j][v] = c.sc_dh[eoff(i, j, v)];
           }
-        }
+    }
+  };
+  auto sums_load = [&]() __attribute__((always_inline)) {
+    if constexpr (kSums) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+          for (int j = 0; j < NBL; ++j) {
+            ey[i][j][v] = c.bs_y[eoff(i, j, v)];
+            if constexpr (kMaskAct) ea[i][j][v] = c.bs_h[eoff(i, j, v)];
+          }
     }
   };
   RowsSlab<BN> r0, r1, r2;
@@ -370,10 +392,14 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
     compute(r2);
   }
   gload(it + 2, r2);
-  eload();
+  if constexpr (kSc)
+    sc_load();
+  else
+    sums_load();
   compute(r0);
   compute(r1);
   compute(r2);
+  if constexpr (kSc) sums_load();
 
   float* out = c.out + (long long)g * Mg * BN;
   if constexpr (MODE == CONV_FWD) {
@@ -423,18 +449,22 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       for (int j = 0; j < NBL; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          if constexpr ((EPI & kEpiShortcut) != 0) {
-            acc[i][j][v] += e0[i][j][v] > 0.f ? e1[i][j][v] : 0.f;
-          } else {
+          if constexpr (kSc) acc[i][j][v] += eh[i][j][v] > 0.f ? edh[i][j][v] : 0.f;
+          if constexpr (kSums) {
             const int ch = j * 16 + lm;
-            const float y = e0[i][j][v], em = bnp[0][ch], ei = bnp[1][ch];
-            const float dz = bn_z(bnp[2][ch], y, em, ei, bnp[3][ch]) > 0.f ? acc[i][j][v] : 0.f;
+            const float y = ey[i][j][v], em = bnp[0][ch], ei = bnp[1][ch];
+            bool pass;
+            if constexpr (kMaskAct)
+              pass = ea[i][j][v] > 0.f;
+            else
+              pass = bn_z(bnp[2][ch], y, em, ei, bnp[3][ch]) > 0.f;
+            const float dz = pass ? acc[i][j][v] : 0.f;
             const float xh = (y - em) * ei;
             bs0[j] += (double)dz;
             bs1[j] += (double)dz * (double)xh;
           }
         }
-    if constexpr ((EPI & kEpiBnSums) != 0) {
+    if constexpr (kSums) {
       __shared__ double bred[4][BN][2];
 #pragma unroll
       for (int j = 0; j < NBL; ++j) {
@@ -898,13 +928,18 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int lq = lane >> 4, lm = lane & 15;
-  // BN parameters of this lane's channel (kEpiBnSums)
+  constexpr bool kSc = (EPI & kEpiShortcut) != 0;
+  constexpr bool kSums = (EPI & (kEpiBnSums | kEpiBnSumsAct)) != 0;
+  constexpr bool kMaskAct = (EPI & kEpiBnSumsAct) != 0;
+  // BN parameters of this lane's channel (the sums)
   float em = 0.f, ei = 0.f, eg = 0.f, eb = 0.f;
-  if constexpr ((EPI & kEpiBnSums) != 0) {
+  if constexpr (kSums) {
     em = c.bn_mu[(long long)g * C + lm];
     ei = c.bn_inv[(long long)g * C + lm];
-    eg = c.bn_g[(long long)g * c.bn_sP + lm];
-    eb = c.bn_b[(long long)g * c.bn_sP + lm];
+    if constexpr (!kMaskAct) {
+      eg = c.bn_g[(long long)g * c.bn_sP + lm];
+      eb = c.bn_b[(long long)g * c.bn_sP + lm];
+    }
   }
   const long long img = ((long long)g * c.Bt + b) * H * W * C;
   for (int u = 0; u < NBW; ++u) {
@@ -915,19 +950,32 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
       const int row = h0 + 2 * wave + (i >> 1), col = 16 * (i & 1) + 4 * lq + v;
       return ((long long)row * W + col) * C + lm;
     };
-    float e0[4][4], e1[4][4];
-    if constexpr (EPI != 0) {
+    // epilogue operands: the shortcut's (eh, edh), or the sums' alone (ey
+    // and, with the activation mask, ea), issued at the band's start; the
+    // sums' next to the shortcut's after the band's k work
+    float eh[kSc ? 4 : 1][4], edh[kSc ? 4 : 1][4], ey[kSums ? 4 : 1][4],
+        ea[kMaskAct ? 4 : 1][4];
+    auto sums_load = [&]() __attribute__((always_inline)) {
+      if constexpr (kSums) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            ey[i][v] = c.bs_y[img + eoff(i, v)];
+            if constexpr (kMaskAct) ea[i][v] = c.bs_h[img + eoff(i, v)];
+          }
+      }
+    };
+    if constexpr (kSc) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          if constexpr ((EPI & kEpiShortcut) != 0) {
-            e0[i][v] = c.sc_h[img + eoff(i, v)];
-            e1[i][v] = c.sc_dh[img + eoff(i, v)];
-          } else {
-            e0[i][v] = c.bs_y[img + eoff(i, v)];
-          }
+          eh[i][v] = c.sc_h[img + eoff(i, v)];
+          edh[i][v] = c.sc_dh[img + eoff(i, v)];
         }
+    } else {
+      sums_load();
     }
     floatx4 acc[4];
 #pragma unroll
@@ -948,23 +996,29 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
         }
       }
     }
+    if constexpr (kSc) sums_load();
     double bs0 = 0.0, bs1 = 0.0;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         float r = acc[i][v];
-        if constexpr ((EPI & kEpiShortcut) != 0) r += e0[i][v] > 0.f ? e1[i][v] : 0.f;
-        if constexpr ((EPI & kEpiBnSums) != 0) {
-          const float y = e0[i][v];
-          const float dz = bn_z(eg, y, em, ei, eb) > 0.f ? r : 0.f;
+        if constexpr (kSc) r += eh[i][v] > 0.f ? edh[i][v] : 0.f;
+        if constexpr (kSums) {
+          const float y = ey[i][v];
+          bool pass;
+          if constexpr (kMaskAct)
+            pass = ea[i][v] > 0.f;
+          else
+            pass = bn_z(eg, y, em, ei, eb) > 0.f;
+          const float dz = pass ? r : 0.f;
           const float xh = (y - em) * ei;
           bs0 += (double)dz;
           bs1 += (double)dz * (double)xh;
         }
         c.out[img + eoff(i, v)] = r;
       }
-    if constexpr ((EPI & kEpiBnSums) != 0) {
+    if constexpr (kSums) {
       // the band's 256 positions: each wave's two rows by a lane butterfly,
       // the four waves in order
       __shared__ double bred[4][C][2];
@@ -1777,13 +1831,22 @@ static bool halo_shape(const ConvGeom& q, int mode) {
 }
 
 int conv_dgrad_epilogues(const ConvGeom& q) {
-  if (halo_shape(q, CONV_DGRAD)) return kEpiShortcut | kEpiBnSums;
+  if (halo_shape(q, CONV_DGRAD)) return kEpiShortcut | kEpiBnSums | kEpiBnSumsAct;
   if (q.stride != 1 || !rows_shape(q, CONV_DGRAD) || q.Cin != q.Cout) return 0;
   // the row kernel: 32 channels (at 64 the operands' registers cost more
   // occupancy than the separate passes); the sums need whole 256-row chunks
   const bool chunks = ((long long)q.Bt * q.H * q.W) % 256 == 0;
-  return q.Cin == 32 ? kEpiShortcut | (chunks ? kEpiBnSums : 0) : 0;
+  return q.Cin == 32 ? kEpiShortcut | (chunks ? kEpiBnSums | kEpiBnSumsAct : 0) : 0;
 }
+
+namespace {
+// The kernel instances' epilogue sets: none, one of the three, or the
+// shortcut with either sums
+bool epi_instance(int e) {
+  return e == 0 || e == kEpiShortcut || e == kEpiBnSums || e == kEpiBnSumsAct ||
+         e == (kEpiShortcut | kEpiBnSums) || e == (kEpiShortcut | kEpiBnSumsAct);
+}
+}  // namespace
 
 bool conv_fwd_stats(const ConvGeom& q) {
   if (stem_shape(q) || halo_shape(q, CONV_FWD)) return true;
@@ -1854,10 +1917,14 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   c.sc_dh = mode == CONV_DGRAD ? q.sc_dh : nullptr;
   c.sc_h = q.sc_h;
   c.bs_y = q.bs_y;
+  c.bs_h = q.bs_h;
   c.bs_part = mode == CONV_DGRAD ? q.bs_part : nullptr;
-  const int epi = (c.sc_dh ? 1 : 0) | (c.bs_part ? 2 : 0);
-  if (epi && (epi == 3 || (conv_dgrad_epilogues(q) & epi) != epi || (c.sc_dh && !c.sc_h) ||
-              (c.bs_part && (!c.bs_y || !c.bn_mu || !c.bn_inv || !c.bn_g || !c.bn_b))))
+  const int epi = (c.sc_dh ? kEpiShortcut : 0) |
+                  (c.bs_part ? (c.bs_h ? kEpiBnSumsAct : kEpiBnSums) : 0);
+  if (epi && (!epi_instance(epi) || (conv_dgrad_epilogues(q) & epi) != epi ||
+              (c.sc_dh && !c.sc_h) ||
+              (c.bs_part && (!c.bs_y || !c.bn_mu || !c.bn_inv ||
+                             (!c.bs_h && (!c.bn_g || !c.bn_b))))))
     return hipErrorInvalidValue;
   if (c.bn_mu && (q.Cin % 4 || q.bn_sP % 4 || ((uintptr_t)q.bn_mu | (uintptr_t)q.bn_inv |
                                               (uintptr_t)q.bn_g | (uintptr_t)q.bn_b) & 15))
@@ -1931,11 +1998,21 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
       if (mode == CONV_FWD)
         hipLaunchKernelGGL((k_conv_halo16<CONV_FWD, kHaloBandsFwd>), dim3((unsigned)nb),
                            dim3(kT), 0, st, c);
-      else if (epi == 1)
+      else if (epi == kEpiShortcut)
         hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiShortcut>),
                            dim3((unsigned)nb), dim3(kT), 0, st, c);
-      else if (epi == 2)
+      else if (epi == kEpiBnSums)
         hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiBnSums>),
+                           dim3((unsigned)nb), dim3(kT), 0, st, c);
+      else if (epi == (kEpiShortcut | kEpiBnSums))
+        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiShortcut | kEpiBnSums>),
+                           dim3((unsigned)nb), dim3(kT), 0, st, c);
+      else if (epi == (kEpiShortcut | kEpiBnSumsAct))
+        hipLaunchKernelGGL(
+            (k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiShortcut | kEpiBnSumsAct>),
+            dim3((unsigned)nb), dim3(kT), 0, st, c);
+      else if (epi == kEpiBnSumsAct)
+        hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad, kEpiBnSumsAct>),
                            dim3((unsigned)nb), dim3(kT), 0, st, c);
       else
         hipLaunchKernelGGL((k_conv_halo16<CONV_DGRAD, kHaloBandsDgrad>), dim3((unsigned)nb),
@@ -1955,6 +2032,11 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
         if (Ng == 16) LSGD_ROWS(CONV_DGRAD, 16);
         else if (Ng == 32 && epi == kEpiShortcut) LSGD_ROWS_E(32, kEpiShortcut);
         else if (Ng == 32 && epi == kEpiBnSums) LSGD_ROWS_E(32, kEpiBnSums);
+        else if (Ng == 32 && epi == kEpiBnSumsAct) LSGD_ROWS_E(32, kEpiBnSumsAct);
+        else if (Ng == 32 && epi == (kEpiShortcut | kEpiBnSums))
+          LSGD_ROWS_E(32, kEpiShortcut | kEpiBnSums);
+        else if (Ng == 32 && epi == (kEpiShortcut | kEpiBnSumsAct))
+          LSGD_ROWS_E(32, kEpiShortcut | kEpiBnSumsAct);
         else if (Ng == 32) LSGD_ROWS(CONV_DGRAD, 32);
         else LSGD_ROWS(CONV_DGRAD, 64);
 #undef LSGD_ROWS_E
