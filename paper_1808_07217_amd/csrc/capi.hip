@@ -27,6 +27,7 @@ struct ConvSpec {
   int Cin, Cout, stride, H, W, Ho, Wo;
   int64_t offW, offG, offB;  // weight [9*Cin][Cout], BN scale, BN shift
   size_t y, act;             // pre-BN output, post-BN activation (ReLU'd)
+  size_t mbits;              // block outputs: the activation's ReLU mask as bits
 };
 constexpr int kResConvs = 19;
 struct ResPlan {
@@ -174,7 +175,10 @@ Layout make_resnet_layout(const lsgd_config* c) {
     const ConvSpec& q = r.cv[i];
     const size_t sz = K * B * q.Ho * q.Wo * q.Cout * 4;
     r.cv[i].y = take(sz);
-    r.cv[i].act = take(sz);
+    // a block's first BN-ReLU output is never stored (its consumers form it);
+    // a block output's mask bits serve the backward passes that need its sign
+    if (i % 2 == 0) r.cv[i].act = take(sz);
+    if (i % 2 == 0 && i > 0) r.cv[i].mbits = take(sz / 32);
     maxact = std::max(maxact, std::max(sz, K * B * q.H * q.W * q.Cin * 4));
     maxpart = std::max(maxpart, (size_t)lsgd::conv_wgrad_splits(c->B_loc, q.Ho, q.Wo) *
                                     K * 9 * q.Cin * q.Cout * 4);
@@ -666,6 +670,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   float* W = c->W();
   float* U = c->U();
   auto F = [&](size_t off) { return (float*)(c->ws + off); };
+  auto M = [&](size_t off) { return (unsigned*)(c->ws + off); };
   float* mu = F(r.mu);
   float* inv = F(r.inv);
   double* bnpart = (double*)(c->ws + r.bnpart);
@@ -754,7 +759,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     LSGD_LAUNCH(c, "bn_apply", lsgd::launch_bn_apply(F(q.y), K, rows(i), q.Cout, mi, ii,
                                                      W + q.offG, W + q.offB, Ps, mode,
                                                      blk_in, q.Ho, q.Wo, cin_blk,
-                                                     F(q.act), s));
+                                                     F(q.act), i > 0 ? M(q.mbits) : nullptr,
+                                                     s));
   }
 
   // head: global average pool, classifier, loss
@@ -808,10 +814,10 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // BN backward (coefficients, gamma/beta update, input gradient into dy)
   // (fused_nchunk > 0: the sums are in bnpart already, from the input
   // gradient that produced gup)
-  auto bn_bwd = [&](int i, const float* gup, const float* maskv, float* dy,
+  auto bn_bwd = [&](int i, const float* gup, const unsigned* mbits, float* dy,
                     int fused_nchunk) {
     const ConvSpec& q = r.cv[i];
-    return lsgd::launch_bn_backward(F(q.y), gup, maskv, K, rows(i), q.Cout, bnpart,
+    return lsgd::launch_bn_backward(F(q.y), gup, mbits, K, rows(i), q.Cout, bnpart,
                                     mu + (size_t)i * K * 64, inv + (size_t)i * K * 64,
                                     coef, W + q.offG, W + q.offB, U + q.offG,
                                     U + q.offB, Ps, lr, cf.momentum, upd_mode(cf), dy,
@@ -862,15 +868,15 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     return LSGD_OK;
   };
   // input gradient of conv i (reads the old weight, before its update).
-  // Where the kernel takes the epilogues: with sc_dh, sc_h the identity
+  // Where the kernel takes the epilogues: with sc_dh, sc_hb the identity
   // shortcut's share of the block-output gradient goes into dx (*sc_fused);
   // with bs_layer >= 0 the backward sums of BN layer bs_layer, whose
   // activation's gradient dx is, go to bnpart (*sums_fused) -- its ReLU mask
   // recomputed from the pre-BN output, or, with bs_act, read from that
-  // activation (a BN whose ReLU follows a shortcut add).
-  auto dgrad = [&](int i, const float* dy, float* dx, const float* sc_dh, const float* sc_h,
-                   int bs_layer, const float* bs_act, bool* sc_fused,
-                   bool* sums_fused) -> lsgd_status {
+  // activation's mask bits (a BN whose ReLU follows a shortcut add).
+  auto dgrad = [&](int i, const float* dy, float* dx, const float* sc_dh,
+                   const unsigned* sc_hb, int bs_layer, const unsigned* bs_act,
+                   bool* sc_fused, bool* sums_fused) -> lsgd_status {
     lsgd::ConvGeom g = geom(i);
     g.dy = dy;
     g.out = dx;
@@ -880,11 +886,11 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                   rows(bs_layer) == B * r.cv[i].H * r.cv[i].W && rows(bs_layer) % 256 == 0;
     if (*sc_fused) {
       g.sc_dh = sc_dh;
-      g.sc_h = sc_h;
+      g.sc_hb = sc_hb;
     }
     if (*sums_fused) {
       g.bs_y = F(r.cv[bs_layer].y);
-      g.bs_h = bs_act;
+      g.bs_hb = bs_act;
       g.bs_part = bnpart;
       bn_input(g, bs_layer);
     }
@@ -904,7 +910,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     float* g2 = gb[par ? 5 : 2];
     if (lsgd_status st = release(par)) return st;
     // second convolution: its output went through the shortcut add and ReLU
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], F(r.cv[ib].act), g1,
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], M(r.cv[ib].mbits), g1,
                                     out_sums ? rows(ib) / 256 : 0));
     bool sums_fused = false, sc_fused = false, unused = false;
     if (lsgd_status st = dgrad(ib, g1, g2, nullptr, nullptr, ia, nullptr, &unused, &sums_fused))
@@ -920,8 +926,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
     const int prev_bn = ia - 1;
     if (lsgd_status st = dgrad(ia, g2, gb[nxt], mode == 1 ? gb[cur] : nullptr,
-                               F(r.cv[ib].act), mode == 1 ? prev_bn : -1,
-                               prev_bn > 0 ? F(r.cv[prev_bn].act) : nullptr, &sc_fused,
+                               M(r.cv[ib].mbits), mode == 1 ? prev_bn : -1,
+                               prev_bn > 0 ? M(r.cv[prev_bn].mbits) : nullptr, &sc_fused,
                                &out_sums))
       return st;
     if (sidew) {
@@ -936,7 +942,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     }
     if (!sc_fused)
       LSGD_LAUNCH(c, "shortcut_bwd",
-                  lsgd::launch_shortcut_grad(gb[nxt], gb[cur], F(r.cv[ib].act), K, B,
+                  lsgd::launch_shortcut_grad(gb[nxt], gb[cur], M(r.cv[ib].mbits), K, B,
                                              qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
     cur = nxt;
   }

@@ -164,27 +164,29 @@ struct ConvGeom {
   const float* bn_b;
   long long bn_sP;
   // input gradient, where conv_dgrad_epilogues(q) (nullptr: none):
-  //  * sc_dh, sc_h: the block output's gradient and activation (same shape as
-  //    dx, identity shortcut): dx gains sc_dh where sc_h > 0;
+  //  * sc_dh, sc_hb: the block output's gradient (same shape as dx, identity
+  //    shortcut) and its activation's ReLU mask as bits (bit L % 32 of word
+  //    L / 32 for linear element L, as launch_bn_apply writes it): dx gains
+  //    sc_dh where the bit is set;
   //  * bs_part: dx (with the shortcut's share, when both are set) is the
   //    gradient of a BN-ReLU's output whose pre-BN values are bs_y (same
   //    shape) and whose statistics and parameters come in bn_* (as above):
   //    the BN backward sums (sum dz, sum dz x^ with x^ = (y - mu) inv) are
   //    written per 256-row chunk, [G][R/256][Cin][2] doubles, for
   //    launch_bn_backward's fused_nchunk; dz = dx where
-  //    gamma (y - mu) inv + beta > 0, or, with bs_h set (a BN whose ReLU
-  //    follows a shortcut add), where the activation bs_h > 0 (bn_g, bn_b
+  //    gamma (y - mu) inv + beta > 0, or, with bs_hb set (a BN whose ReLU
+  //    follows a shortcut add), where its activation's mask bit is set (bn_g, bn_b
   //    then unused)
   const float* sc_dh;
-  const float* sc_h;
+  const unsigned* sc_hb;
   const float* bs_y;
-  const float* bs_h;
+  const unsigned* bs_hb;
   double* bs_part;
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
 // Which epilogues the input-gradient launch of q takes: bit 0 the shortcut
 // share (sc_*), bit 1 the BN backward sums with the recomputed mask (bs_*),
-// bit 2 the sums with the activation mask (bs_h). A launch takes one of them,
+// bit 2 the sums with the activation mask (bs_hb). A launch takes one of them,
 // or the shortcut with one kind of sums.
 int conv_dgrad_epilogues(const ConvGeom& q);
 int conv_wgrad_splits(int Bt, int Ho, int Wo);
@@ -214,22 +216,28 @@ hipError_t launch_bn_stats(const float* y, int G, int R, int C, double* part,
                            hipStream_t st, const float* gamma = nullptr,
                            const float* beta = nullptr, long long sP = 0,
                            float* gsnap = nullptr, float* bsnap = nullptr);
+// BN output with the shortcut add (mode 1 identity, 2 option A from xin) and
+// ReLU into out; with mbits set, also the ReLU mask as bits (bit L % 32 of
+// word L / 32 set where out at linear element L is positive; R C a multiple
+// of 32), which the backward passes read instead of out.
 hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
-                           int Cin, float* out, hipStream_t st);
+                           int Cin, float* out, unsigned* mbits, hipStream_t st);
 // BN backward with the gamma/beta step: the upstream gradient gup is masked
-// by maskv > 0 (the post-ReLU activation) or, with maskv null, by the sign of
-// the recomputed pre-ReLU BN output (a BN-ReLU with no shortcut add). coef
-// holds 5 floats per (replica, channel).
+// by the activation's mask bits mbits (launch_bn_apply's) or, with mbits null,
+// by the sign of the recomputed pre-ReLU BN output (a BN-ReLU with no shortcut
+// add). coef holds 5 floats per (replica, channel).
 // fused_nchunk > 0: the sums are already in part (fused_nchunk chunks per
 // replica, from an input-gradient epilogue) and are not formed again.
-hipError_t launch_bn_backward(const float* y, const float* gup, const float* maskv,
+hipError_t launch_bn_backward(const float* y, const float* gup, const unsigned* mbits,
                               int G, int R, int C, double* part, const float* mu,
                               const float* inv, float* coef, float* gamma, float* beta,
                               float* ug, float* ub, long long sP, float lr, float mom,
                               int nesterov, float* dy, int fused_nchunk, hipStream_t st);
-hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
+// The shortcut's share dx += dh_out where the block output's mask bit
+// (hb_out, launch_bn_apply's) is set: identity (mode 1) or option A (mode 2).
+hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const unsigned* hb_out,
                                 int G, int Bt, int H, int W, int Cin, int Cout,
                                 int mode, hipStream_t st);
 hipError_t launch_gap(const float* h, int rows, int S, int C, float* feat, bool bwd,

@@ -59,9 +59,9 @@ struct ConvArgs {
   // stage-1 input gradient epilogues (see ConvGeom): the shortcut share and
   // the backward BN sums of the layer whose activation gradient dx is
   const float* sc_dh;
-  const float* sc_h;
+  const unsigned* sc_hb;
   const float* bs_y;
-  const float* bs_h;
+  const unsigned* bs_hb;
   double* bs_part;
 };
 
@@ -75,6 +75,15 @@ __device__ __forceinline__ float bn_z(float gm, float y, float m, float iv, floa
 }
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+
+// ReLU masks as bits: a tensor's mask holds bit L % 32 of word L / 32 for its
+// element at linear index L (whole tensor, [G][rows][C] order), set where the
+// activation is positive. A block output's mask is written with it
+// (k_bn_apply4); the backward passes that only need the activation's sign
+// read 1/32 of its bytes.
+__device__ __forceinline__ bool mask_bit(unsigned word, long long L) {
+  return (word >> (unsigned)(L & 31)) & 1u;
+}
 
 // BN statistics and parameters of four consecutive input channels.
 struct BnIn4 {
@@ -113,15 +122,17 @@ __device__ __forceinline__ void stats_butterfly(double& s0, double& s1, int widt
 
 // Input-gradient epilogues (EPI bits; their operands are loaded while the
 // last k work of a tile or band runs):
-//   kEpiShortcut: dx += dh where h > 0 (c.sc_dh, c.sc_h: the block output's
-//     gradient and activation, same shape; the identity shortcut);
+//   kEpiShortcut: dx += dh where h > 0 (c.sc_dh: the block output's
+//     gradient, same shape; c.sc_hb: its activation's mask bits; the
+//     identity shortcut);
 //   kEpiBnSums: dx is the gradient of a BN-ReLU's output whose pre-BN values
 //     c.bs_y and BN parameters come in c.bn_*: per 256 output rows, the
 //     backward sums sum dz and sum dz x^ (dz = dx where the ReLU passed,
 //     x^ = (y - mu) inv) go to c.bs_part as one chunk, in the forward
 //     statistics' layout;
 //   kEpiBnSumsAct: the same sums where the ReLU follows a shortcut add (a
-//     block's second BN): dz = dx where the activation c.bs_h > 0.
+//     block's second BN): dz = dx where the activation's mask bit (c.bs_hb)
+//     is set.
 // The shortcut combines with either sums (dx then includes the shortcut
 // share); the sums' operands are then loaded after the k work, where the
 // shortcut's are free.
@@ -345,23 +356,31 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
   // register v): the shortcut's (eh, edh), or the sums' alone (ey and, with
   // the activation mask, ea), issued while the last slabs compute; the sums'
   // next to the shortcut's after the k work
-  float eh[kSc ? 4 : 1][kSc ? NBL : 1][4], edh[kSc ? 4 : 1][kSc ? NBL : 1][4];
-  float ey[kSums ? 4 : 1][kSums ? NBL : 1][4], ea[kMaskAct ? 4 : 1][kMaskAct ? NBL : 1][4];
+  // (the masks as bit words: with BN a multiple of 32, a lane's column
+  // blocks 2 jw and 2 jw + 1 of a row share word jw of that row, at bits
+  // 16 (j % 2) + lm)
+  static_assert(!(kSc || kMaskAct) || BN % 32 == 0, "mask words span 32 channels");
+  constexpr int NW = (NBL + 1) / 2;
+  unsigned eh[kSc ? 4 : 1][kSc ? NW : 1][4], ea[kMaskAct ? 4 : 1][kMaskAct ? NW : 1][4];
+  float edh[kSc ? 4 : 1][kSc ? NBL : 1][4], ey[kSums ? 4 : 1][kSums ? NBL : 1][4];
   auto eoff = [&](int i, int j, int v) __attribute__((always_inline)) {
     const int m = min(m0 + wave * 64 + i * 16 + lq * 4 + v, Mg - 1);
     return ((long long)g * Mg + m) * BN + j * 16 + lm;
+  };
+  auto ebit = [&](unsigned w, int j) __attribute__((always_inline)) {
+    return ((w >> (unsigned)(((j & 1) << 4) + lm)) & 1u) != 0u;
   };
   auto sc_load = [&]() __attribute__((always_inline)) {
     if constexpr (kSc) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
+        for (int v = 0; v < 4; ++v) {
 #pragma unroll
-          for (int j = 0; j < NBL; ++j) {
-            eh[i][j][v] = c.sc_h[eoff(i, j, v)];
-            edh[i][j][v] = c.sc_dh[eoff(i, j, v)];
-          }
+          for (int jw = 0; jw < NW; ++jw) eh[i][jw][v] = c.sc_hb[eoff(i, 2 * jw, v) >> 5];
+#pragma unroll
+          for (int j = 0; j < NBL; ++j) edh[i][j][v] = c.sc_dh[eoff(i, j, v)];
+        }
     }
   };
   auto sums_load = [&]() __attribute__((always_inline)) {
@@ -369,12 +388,14 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
+        for (int v = 0; v < 4; ++v) {
 #pragma unroll
-          for (int j = 0; j < NBL; ++j) {
-            ey[i][j][v] = c.bs_y[eoff(i, j, v)];
-            if constexpr (kMaskAct) ea[i][j][v] = c.bs_h[eoff(i, j, v)];
+          for (int j = 0; j < NBL; ++j) ey[i][j][v] = c.bs_y[eoff(i, j, v)];
+          if constexpr (kMaskAct) {
+#pragma unroll
+            for (int jw = 0; jw < NW; ++jw) ea[i][jw][v] = c.bs_hb[eoff(i, 2 * jw, v) >> 5];
           }
+        }
     }
   };
   RowsSlab<BN> r0, r1, r2;
@@ -449,13 +470,13 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
       for (int j = 0; j < NBL; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          if constexpr (kSc) acc[i][j][v] += eh[i][j][v] > 0.f ? edh[i][j][v] : 0.f;
+          if constexpr (kSc) acc[i][j][v] += ebit(eh[i][j >> 1][v], j) ? edh[i][j][v] : 0.f;
           if constexpr (kSums) {
             const int ch = j * 16 + lm;
             const float y = ey[i][j][v], em = bnp[0][ch], ei = bnp[1][ch];
             bool pass;
             if constexpr (kMaskAct)
-              pass = ea[i][j][v] > 0.f;
+              pass = ebit(ea[i][j >> 1][v], j);
             else
               pass = bn_z(bnp[2][ch], y, em, ei, bnp[3][ch]) > 0.f;
             const float dz = pass ? acc[i][j][v] : 0.f;
@@ -953,27 +974,35 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
     // epilogue operands: the shortcut's (eh, edh), or the sums' alone (ey
     // and, with the activation mask, ea), issued at the band's start; the
     // sums' next to the shortcut's after the band's k work
-    float eh[kSc ? 4 : 1][4], edh[kSc ? 4 : 1][4], ey[kSums ? 4 : 1][4],
-        ea[kMaskAct ? 4 : 1][4];
+    // (the masks as bit words: 16 channels, so the even column 2 vp and the
+    // next one share a word, at bits 16 (v % 2) + lm; an image is a whole
+    // number of words)
+    unsigned eh[kSc ? 4 : 1][2], ea[kMaskAct ? 4 : 1][2];
+    float edh[kSc ? 4 : 1][4], ey[kSums ? 4 : 1][4];
+    auto ebit = [&](unsigned w, int v) __attribute__((always_inline)) {
+      return ((w >> (unsigned)(((v & 1) << 4) + lm)) & 1u) != 0u;
+    };
     auto sums_load = [&]() __attribute__((always_inline)) {
       if constexpr (kSums) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i) {
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            ey[i][v] = c.bs_y[img + eoff(i, v)];
-            if constexpr (kMaskAct) ea[i][v] = c.bs_h[img + eoff(i, v)];
+          for (int v = 0; v < 4; ++v) ey[i][v] = c.bs_y[img + eoff(i, v)];
+          if constexpr (kMaskAct) {
+#pragma unroll
+            for (int vp = 0; vp < 2; ++vp) ea[i][vp] = c.bs_hb[(img + eoff(i, 2 * vp)) >> 5];
           }
+        }
       }
     };
     if constexpr (kSc) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          eh[i][v] = c.sc_h[img + eoff(i, v)];
-          edh[i][v] = c.sc_dh[img + eoff(i, v)];
-        }
+        for (int vp = 0; vp < 2; ++vp) eh[i][vp] = c.sc_hb[(img + eoff(i, 2 * vp)) >> 5];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) edh[i][v] = c.sc_dh[img + eoff(i, v)];
+      }
     } else {
       sums_load();
     }
@@ -1003,12 +1032,12 @@ __global__ __launch_bounds__(kT) void k_conv_halo16(ConvArgs c) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         float r = acc[i][v];
-        if constexpr (kSc) r += eh[i][v] > 0.f ? edh[i][v] : 0.f;
+        if constexpr (kSc) r += ebit(eh[i][v >> 1], v) ? edh[i][v] : 0.f;
         if constexpr (kSums) {
           const float y = ey[i][v];
           bool pass;
           if constexpr (kMaskAct)
-            pass = ea[i][v] > 0.f;
+            pass = ebit(ea[i][v >> 1], v);
           else
             pass = bn_z(eg, y, em, ei, eb) > 0.f;
           const float dz = pass ? r : 0.f;
@@ -1460,8 +1489,8 @@ __global__ void k_conv_wupdate(const float* part, int G, int n, float* W, float*
 // ------------------------------------------------------------ batch norm
 // Partial sums of one row chunk per workgroup, fp64: for the forward pass
 // sum(y) and sum(y^2); for the backward pass sum(dz) and sum(dz * xhat),
-// where dz = upstream gradient masked by the ReLU derivative -- `maskv > 0`
-// when given, else bn_z(gamma, y, mu, inv, beta) > 0 -- and
+// where dz = upstream gradient masked by the ReLU derivative -- the
+// activation's mask bits when given, else bn_z(gamma, y, mu, inv, beta) > 0 -- and
 // xhat = (y - mu) * inv. Channel count C divides 256. Rows per chunk: 1024
 // for the largest layers, fewer for smaller ones so that every layer's
 // launch has at least 32 chunks per replica to spread over the chip.
@@ -1567,7 +1596,7 @@ __global__ __launch_bounds__(kT) void k_bn_finalize_wg(
 // of a chunk interleaved over the 1024 / C row lanes of a workgroup, fp64
 // sums per channel, then added in a fixed tree.
 __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C,
-                                                    const float* gup, const float* maskv,
+                                                    const float* gup, const unsigned* mbits,
                                                     const float* mu, const float* inv,
                                                     const float* gamma, const float* beta,
                                                     long long sP, double* part,
@@ -1580,7 +1609,7 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
   const int cr = bn_chunk_rows(R);
   const int r0 = ch * cr, r1 = min(R, r0 + cr);
   const bool bwd = gup != nullptr;
-  const bool zmask = bwd && maskv == nullptr;
+  const bool zmask = bwd && mbits == nullptr;
   float m_c[4], i_c[4], g_c[4], b_c[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -1591,17 +1620,19 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
   }
   double s0[4] = {0.0, 0.0, 0.0, 0.0}, s1[4] = {0.0, 0.0, 0.0, 0.0};
   for (int rb = r0 + lane_r; rb < r1; rb += 4 * rstep) {
-    v4f yv[4], gv[4], mv[4];
+    v4f yv[4], gv[4];
+    unsigned mw[4];  // the mask: bit e of (mw >> o % 32) is channel c0 + e's
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int r = min(rb + u * rstep, r1 - 1);
       const long long o = base + (long long)r * C + c0;
       yv[u] = *(const v4f*)(y + o);
       gv[u] = bwd ? *(const v4f*)(gup + o) : v4f{0.f, 0.f, 0.f, 0.f};
-      mv[u] = maskv ? *(const v4f*)(maskv + o) : v4f{1.f, 1.f, 1.f, 1.f};
+      mw[u] = mbits ? mbits[o >> 5] >> (unsigned)(o & 31) : 0u;
       if (zmask) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) mv[u][e] = bn_z(g_c[e], yv[u][e], m_c[e], i_c[e], b_c[e]);
+        for (int e = 0; e < 4; ++e)
+          mw[u] |= (bn_z(g_c[e], yv[u][e], m_c[e], i_c[e], b_c[e]) > 0.f ? 1u : 0u) << e;
       }
     }
 #pragma unroll
@@ -1613,7 +1644,7 @@ __global__ __launch_bounds__(kT) void k_bn_partial4(const float* y, int R, int C
           s0[e] += (double)yv[u][e];
           s1[e] += (double)yv[u][e] * (double)yv[u][e];
         } else {
-          const float dz = mv[u][e] > 0.f ? gv[u][e] : 0.f;
+          const float dz = (mw[u] >> e) & 1u ? gv[u][e] : 0.f;
           const float xh = (yv[u][e] - m_c[e]) * i_c[e];
           s0[e] += (double)dz;
           s1[e] += (double)dz * (double)xh;
@@ -1657,10 +1688,11 @@ __global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, 
                                                   const float* mu, const float* inv,
                                                   const float* gamma, const float* beta,
                                                   long long sP, int mode, const float* xin,
-                                                  int Ho, int Wo, int Cin, float* out) {
+                                                  int Ho, int Wo, int Cin, float* out,
+                                                  unsigned* mbits) {
   const int g = blockIdx.y;
   const int j = blockIdx.x * kT + threadIdx.x;
-  if (j >= R * C / 4) return;
+  if (j >= R * C / 4) return;  // R C / 4 is a multiple of 8 with mbits
   const int e4 = 4 * j, c0 = e4 & (C - 1), r = e4 >> cshift;
   const long long o = (long long)g * R * C + e4;
   const v4f yv = *(const v4f*)(y + o);
@@ -1678,17 +1710,31 @@ __global__ __launch_bounds__(kT) void k_bn_apply4(const float* y, int R, int C, 
   const v4f g4 = *(const v4f*)(gamma + (long long)g * sP + c0);
   const v4f b4 = *(const v4f*)(beta + (long long)g * sP + c0);
   v4f res;
+  unsigned nib = 0;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const float v = bn_z(g4[e], yv[e], m4[e], i4[e], b4[e]) + xv[e];
     res[e] = v > 0.f ? v : 0.f;
+    nib |= (v > 0.f ? 1u : 0u) << e;
   }
   *(v4f*)(out + o) = res;
+  if (mbits) {
+    // the mask word of 32 consecutive elements: the nibbles of the eight
+    // threads 8q .. 8q + 7 (all present: a group never straddles R C / 4)
+    unsigned w = nib << (4 * (threadIdx.x & 7));
+    w |= __shfl_xor(w, 1, 64);
+    w |= __shfl_xor(w, 2, 64);
+    w |= __shfl_xor(w, 4, 64);
+    if ((threadIdx.x & 7) == 0) mbits[o >> 5] = w;
+  }
 }
 
-// k_bn_bwd_apply, 4 channels per thread.
+// The BN input gradient, 4 channels per thread:
+//   dy = gamma inv (dz - dbeta / R - x^ dgamma / R) with the coefficients of
+// k_bn_finalize_wg, dz = gup where the ReLU passed (mask bits mbits, or, with
+// mbits null, the recomputed sign of gamma (y - mu) inv + beta), x^ = (y - mu) inv.
 __global__ __launch_bounds__(kT) void k_bn_bwd_apply4(const float* y, const float* gup,
-                                                      const float* maskv, int R, int C,
+                                                      const unsigned* mbits, int R, int C,
                                                       const float* mu, const float* inv,
                                                       const float* coef, float* dy) {
   const int g = blockIdx.y;
@@ -1701,29 +1747,32 @@ __global__ __launch_bounds__(kT) void k_bn_bwd_apply4(const float* y, const floa
   const v4f m4 = *(const v4f*)(mu + gc), i4 = *(const v4f*)(inv + gc);
   const v4f k0 = *(const v4f*)(coef + gc), k1 = *(const v4f*)(coef + GC + gc),
             k2 = *(const v4f*)(coef + 2 * GC + gc);
-  v4f mv;
-  if (maskv) {
-    mv = *(const v4f*)(maskv + o);
+  unsigned mw = 0;  // bit e: channel c0 + e passes the ReLU
+  if (mbits) {
+    mw = mbits[o >> 5] >> (unsigned)(o & 31);
   } else {
     const v4f k3 = *(const v4f*)(coef + 3 * GC + gc), k4 = *(const v4f*)(coef + 4 * GC + gc);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) mv[e] = bn_z(k3[e], yv[e], m4[e], i4[e], k4[e]);
+    for (int e = 0; e < 4; ++e)
+      mw |= (bn_z(k3[e], yv[e], m4[e], i4[e], k4[e]) > 0.f ? 1u : 0u) << e;
   }
   v4f res;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const float dz = mv[e] > 0.f ? gv[e] : 0.f;
+    const float dz = (mw >> e) & 1u ? gv[e] : 0.f;
     const float xh = (yv[e] - m4[e]) * i4[e];
     res[e] = k0[e] * (dz - k1[e] - xh * k2[e]);
   }
   *(v4f*)(dy + o) = res;
 }
 
-// k_shortcut_grad, 4 channels per thread. Identity: every element of dx.
-// Option A: one thread per (output position, 4 of the first Cin channels),
-// adding to the even input pixel it was taken from.
+// The shortcut's share of the block-input gradient, 4 channels per thread:
+// dx += dh_out where the block output passed its ReLU (mask bits hb_out).
+// Identity: every element of dx. Option A: one thread per (output position,
+// 4 of the first Cin channels), adding to the even input pixel it was taken
+// from.
 __global__ __launch_bounds__(kT) void k_shortcut_grad4(float* dx, const float* dh_out,
-                                                       const float* h_out, int Bt, int H,
+                                                       const unsigned* hb_out, int Bt, int H,
                                                        int W, int Cin, int Cout, int mode) {
   const int g = blockIdx.y;
   const int j = blockIdx.x * kT + threadIdx.x;
@@ -1731,9 +1780,10 @@ __global__ __launch_bounds__(kT) void k_shortcut_grad4(float* dx, const float* d
     if (j >= Bt * H * W * Cin / 4) return;
     const long long o = (long long)g * Bt * H * W * Cin + 4 * j;
     v4f d = *(const v4f*)(dx + o);
-    const v4f a = *(const v4f*)(h_out + o), gq = *(const v4f*)(dh_out + o);
+    const v4f gq = *(const v4f*)(dh_out + o);
+    const unsigned mw = hb_out[o >> 5] >> (unsigned)(o & 31);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) d[e] += a[e] > 0.f ? gq[e] : 0.f;
+    for (int e = 0; e < 4; ++e) d[e] += (mw >> e) & 1u ? gq[e] : 0.f;
     *(v4f*)(dx + o) = d;
     return;
   }
@@ -1744,9 +1794,10 @@ __global__ __launch_bounds__(kT) void k_shortcut_grad4(float* dx, const float* d
   const long long oo = ((long long)g * Bt * Ho * Wo + pos) * Cout + c0;
   const long long oi = (((long long)g * Bt + b) * H * W + (long long)(2 * oh) * W + 2 * ow) * Cin + c0;
   v4f d = *(const v4f*)(dx + oi);
-  const v4f a = *(const v4f*)(h_out + oo), gq = *(const v4f*)(dh_out + oo);
+  const v4f gq = *(const v4f*)(dh_out + oo);
+  const unsigned mw = hb_out[oo >> 5] >> (unsigned)(oo & 31);
 #pragma unroll
-  for (int e = 0; e < 4; ++e) d[e] += a[e] > 0.f ? gq[e] : 0.f;
+  for (int e = 0; e < 4; ++e) d[e] += (mw >> e) & 1u ? gq[e] : 0.f;
   *(v4f*)(dx + oi) = d;
 }
 
@@ -1915,16 +1966,17 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
   c.bn_b = q.bn_b;
   c.bn_sP = q.bn_sP;
   c.sc_dh = mode == CONV_DGRAD ? q.sc_dh : nullptr;
-  c.sc_h = q.sc_h;
+  c.sc_hb = q.sc_hb;
   c.bs_y = q.bs_y;
-  c.bs_h = q.bs_h;
+  c.bs_hb = q.bs_hb;
   c.bs_part = mode == CONV_DGRAD ? q.bs_part : nullptr;
   const int epi = (c.sc_dh ? kEpiShortcut : 0) |
-                  (c.bs_part ? (c.bs_h ? kEpiBnSumsAct : kEpiBnSums) : 0);
+                  (c.bs_part ? (c.bs_hb ? kEpiBnSumsAct : kEpiBnSums) : 0);
   if (epi && (!epi_instance(epi) || (conv_dgrad_epilogues(q) & epi) != epi ||
-              (c.sc_dh && !c.sc_h) ||
+              (c.sc_dh && (!c.sc_hb || ((uintptr_t)c.sc_hb & 3))) ||
+              (c.bs_hb && ((uintptr_t)c.bs_hb & 3)) ||
               (c.bs_part && (!c.bs_y || !c.bn_mu || !c.bn_inv ||
-                             (!c.bs_h && (!c.bn_g || !c.bn_b))))))
+                             (!c.bs_hb && (!c.bn_g || !c.bn_b))))))
     return hipErrorInvalidValue;
   if (c.bn_mu && (q.Cin % 4 || q.bn_sP % 4 || ((uintptr_t)q.bn_mu | (uintptr_t)q.bn_inv |
                                               (uintptr_t)q.bn_g | (uintptr_t)q.bn_b) & 15))
@@ -2122,46 +2174,50 @@ hipError_t launch_bn_finalize_chunks(const double* part, int nchunk, int G, int 
 hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
                            const float* inv, const float* gamma, const float* beta,
                            long long sP, int mode, const float* xin, int Ho, int Wo,
-                           int Cin, float* out, hipStream_t st) {
+                           int Cin, float* out, unsigned* mbits, hipStream_t st) {
   if (!bn_shape_ok(G, R, C) || !al16p(y) || !al16p(out) || !al16p(xin) || !al16p(mu) ||
-      !al16p(inv) || !al16p(gamma) || !al16p(beta) || sP % 4 || Cin % 4)
+      !al16p(inv) || !al16p(gamma) || !al16p(beta) || sP % 4 || Cin % 4 ||
+      (mbits && ((R * C) % 32 || !al16p(mbits))))
     return hipErrorInvalidValue;
   const dim3 grid((R * C / 4 + kT - 1) / kT, G);
   hipLaunchKernelGGL(k_bn_apply4, grid, dim3(kT), 0, st, y, R, C, bn_vec_shift(C), mu, inv,
-                     gamma, beta, sP, mode, xin, Ho, Wo, Cin, out);
+                     gamma, beta, sP, mode, xin, Ho, Wo, Cin, out, mbits);
   return hipGetLastError();
 }
 
-hipError_t launch_bn_backward(const float* y, const float* gup, const float* maskv,
+hipError_t launch_bn_backward(const float* y, const float* gup, const unsigned* mbits,
                               int G, int R, int C, double* part, const float* mu,
                               const float* inv, float* coef, float* gamma, float* beta,
                               float* ug, float* ub, long long sP, float lr, float mom,
                               int nesterov, float* dy, int fused_nchunk, hipStream_t st) {
-  if (!bn_shape_ok(G, R, C) || !al16p(y) || !al16p(gup) || !al16p(maskv) || !al16p(dy) ||
-      !al16p(mu) || !al16p(inv) || !al16p(coef) || fused_nchunk < 0)
+  if (!bn_shape_ok(G, R, C) || !al16p(y) || !al16p(gup) || !al16p(mbits) || !al16p(dy) ||
+      !al16p(mu) || !al16p(inv) || !al16p(coef) || fused_nchunk < 0 ||
+      (mbits && (R * C) % 32))
     return hipErrorInvalidValue;
   const int nch = fused_nchunk > 0 ? fused_nchunk : bn_chunks(R);
   if (fused_nchunk == 0)
-    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, maskv,
+    hipLaunchKernelGGL(k_bn_partial4, dim3(nch, G), dim3(kT), 0, st, y, R, C, gup, mbits,
                        mu, inv, gamma, beta, sP, part, nch);
   hipLaunchKernelGGL(k_bn_finalize_wg, dim3(G), dim3(kT), 0, st, part, nch, C, R,
                      (float*)mu, (float*)inv, coef, gamma, beta, ug, ub, sP, lr, mom,
                      nesterov, 1e-5f, nullptr, nullptr, 0LL, nullptr, nullptr);
   hipLaunchKernelGGL(k_bn_bwd_apply4, dim3((R * C / 4 + kT - 1) / kT, G), dim3(kT), 0,
-                     st, y, gup, maskv, R, C, mu, inv, coef, dy);
+                     st, y, gup, mbits, R, C, mu, inv, coef, dy);
   return hipGetLastError();
 }
 
-hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const float* h_out,
+hipError_t launch_shortcut_grad(float* dx, const float* dh_out, const unsigned* hb_out,
                                 int G, int Bt, int H, int W, int Cin, int Cout,
                                 int mode, hipStream_t st) {
-  if (Cin % 4 || Cout % 4 || !al16p(dx) || !al16p(dh_out) || !al16p(h_out) ||
-      (long long)Bt * H * W * Cin >= (1LL << 31) || G > 65535 || H % 2 || W % 2)
+  if (Cin % 4 || Cout % 4 || !al16p(dx) || !al16p(dh_out) || !hb_out || !al16p(hb_out) ||
+      (long long)Bt * H * W * Cin >= (1LL << 31) || G > 65535 || H % 2 || W % 2 ||
+      (mode == 1 ? (long long)Bt * H * W * Cin : (long long)Bt * (H / 2) * (W / 2) * Cout) %
+          32)
     return hipErrorInvalidValue;
   const long long n4 = mode == 1 ? (long long)Bt * H * W * Cin / 4
                                  : (long long)Bt * (H / 2) * (W / 2) * (Cin / 4);
   hipLaunchKernelGGL(k_shortcut_grad4, dim3((unsigned)((n4 + kT - 1) / kT), G), dim3(kT),
-                     0, st, dx, dh_out, h_out, Bt, H, W, Cin, Cout, mode);
+                     0, st, dx, dh_out, hb_out, Bt, H, W, Cin, Cout, mode);
   return hipGetLastError();
 }
 
