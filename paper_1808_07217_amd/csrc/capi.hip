@@ -37,7 +37,7 @@ struct ResPlan {
   // gradient buffers: 0 and 3 the block-output and block-input gradients,
   // 1, 2 (4, 5) a block's two BN input gradients, by the block's parity
   size_t featb = 0, dfeat = 0, dzh = 0, gbuf[6] = {}, mu = 0, inv = 0, coef = 0,
-         bnpart = 0, wpart = 0;
+         bnpart = 0, wpart = 0, wpart0 = 0;
   // per BN layer, the scale and shift its forward batch was normalised with
   // ([kResConvs][K][64], layer i's [K][Cout] from i K 64)
   size_t gsnap = 0, bsnap = 0;
@@ -197,6 +197,10 @@ Layout make_resnet_layout(const lsgd_config* c) {
   r.coef = take(K * 64 * 5 * 4);
   r.bnpart = take(maxbn);
   r.wpart = take(maxpart);
+  // the stem's weight-gradient partials apart: the main stream forms them
+  // while the side stream may still use wpart
+  r.wpart0 = take((size_t)lsgd::conv_wgrad_splits(c->B_loc, r.cv[0].Ho, r.cv[0].Wo) * K * 9 *
+                  r.cv[0].Cin * r.cv[0].Cout * 4);
   l.total = t;
   return l;
 }
@@ -827,8 +831,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // per-split partials, then their fixed-order sum and the update (after
   // any input gradient that reads the old weight)
   // (bn_layer >= 0: x is that BN layer's pre-BN output, see bn_input)
-  auto wgrad = [&](int i, const float* x, const float* dy, int bn_layer,
-                   hipStream_t ws) -> lsgd_status {
+  auto wgrad = [&](int i, const float* x, const float* dy, int bn_layer, hipStream_t ws,
+                   float* part) -> lsgd_status {
     const ConvSpec& q = r.cv[i];
     lsgd::ConvGeom g = geom(i);
     if (i == 0) {
@@ -840,10 +844,10 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
       if (bn_layer >= 0) bn_input(g, bn_layer);
     }
     g.dy = dy;
-    g.out = wpart;
+    g.out = part;
     LSGD_LAUNCH_ON(c, ws, "conv_wgrad", lsgd::launch_conv(lsgd::CONV_WGRAD_MODE, g, ws));
     LSGD_LAUNCH_ON(c, ws, "conv_wupdate",
-                   lsgd::launch_conv_wupdate(wpart, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo),
+                   lsgd::launch_conv_wupdate(part, lsgd::conv_wgrad_splits(B, q.Ho, q.Wo),
                                              K, 9 * q.Cin * q.Cout, W + q.offW, U + q.offW,
                                              Ps, lr, cf.momentum, cf.weight_decay,
                                              upd_mode(cf), ws));
@@ -852,19 +856,39 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // The weight gradients (and updates) of a block run on side stream 1: they
   // fork after the block's last input gradient (the last reader of its
   // weights) and overlap the next block's BN backward passes and input
-  // gradients on the main stream. A block's two BN input gradients (the
-  // second BN's, and the first BN's formed in place over the gradient it
-  // came from) live in buffers 1, 2 or 4, 5 by the block's parity, so the
-  // main stream rewrites them two blocks later, after event done[parity]
-  // says the side stream has read them; one wpart serves all, in the side
-  // stream's order. Without side streams everything runs in order on the
-  // main stream.
+  // gradients on the main stream (memory-bound passes beside the weight
+  // gradients' matrix work; a fork after the next BN's sums and coefficients,
+  // which then run alone, set the weight gradients against the input
+  // gradients' matrix work instead and was slower). A block's two BN input
+  // gradients (the second BN's, and the first BN's formed in place over the
+  // gradient it came from) live in buffers 1, 2 or 4, 5 by the block's
+  // parity, so the main stream rewrites them two blocks later, after event
+  // done[parity] says the side stream has read them; one wpart serves all
+  // blocks, in the side stream's order (the stem's weight gradient, on the
+  // main stream, has its own). Without side streams everything runs in
+  // order on the main stream.
   const bool sidew = c->use_side;
   hipStream_t ws = sidew ? c->side[1] : s;
   bool pend[2] = {false, false};
   auto release = [&](int k) -> lsgd_status {  // before parity k's buffers are rewritten
     if (pend[k]) LSGD_CK(c, hipStreamWaitEvent(s, c->done[k], 0));
     pend[k] = false;
+    return LSGD_OK;
+  };
+  // the weight gradients of block (ib, ia) with its BN input gradients g1, g2
+  // and input h_in, forked to the side stream
+  auto fork = [&](int ib, int ia, int par, const float* g1, const float* g2,
+                  const float* h_in) -> lsgd_status {
+    if (sidew) {
+      LSGD_CK(c, hipEventRecord(c->fork[1], s));
+      LSGD_CK(c, hipStreamWaitEvent(ws, c->fork[1], 0));
+    }
+    if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), g1, ia, ws, wpart)) return st;
+    if (lsgd_status st = wgrad(ia, h_in, g2, -1, ws, wpart)) return st;
+    if (sidew) {
+      LSGD_CK(c, hipEventRecord(c->done[par], ws));
+      pend[par] = true;
+    }
     return LSGD_OK;
   };
   // input gradient of conv i (reads the old weight, before its update).
@@ -904,14 +928,13 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   for (int blk = 8; blk >= 0; --blk) {
     const int ia = 2 * blk + 1, ib = 2 * blk + 2, par = blk & 1;
     const ConvSpec& qa = r.cv[ia];
-    const float* h_in = F(r.cv[ia - 1].act);
     const int nxt = cur == 0 ? 3 : 0;
     float* g1 = gb[par ? 4 : 1];
     float* g2 = gb[par ? 5 : 2];
     if (lsgd_status st = release(par)) return st;
     // second convolution: its output went through the shortcut add and ReLU
-    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], M(r.cv[ib].mbits), g1,
-                                    out_sums ? rows(ib) / 256 : 0));
+    const unsigned* mb = M(r.cv[ib].mbits);
+    LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], mb, g1, out_sums ? rows(ib) / 256 : 0));
     bool sums_fused = false, sc_fused = false, unused = false;
     if (lsgd_status st = dgrad(ib, g1, g2, nullptr, nullptr, ia, nullptr, &unused, &sums_fused))
       return st;
@@ -925,33 +948,25 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     // where it can
     const int mode = (qa.stride == 1 && qa.Cin == qa.Cout) ? 1 : 2;
     const int prev_bn = ia - 1;
-    if (lsgd_status st = dgrad(ia, g2, gb[nxt], mode == 1 ? gb[cur] : nullptr,
-                               M(r.cv[ib].mbits), mode == 1 ? prev_bn : -1,
+    if (lsgd_status st = dgrad(ia, g2, gb[nxt], gb[cur], mb, mode == 1 ? prev_bn : -1,
                                prev_bn > 0 ? M(r.cv[prev_bn].mbits) : nullptr, &sc_fused,
                                &out_sums))
       return st;
-    if (sidew) {
-      LSGD_CK(c, hipEventRecord(c->fork[1], s));
-      LSGD_CK(c, hipStreamWaitEvent(ws, c->fork[1], 0));
-    }
-    if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), g1, ia, ws)) return st;
-    if (lsgd_status st = wgrad(ia, h_in, g2, -1, ws)) return st;
-    if (sidew) {
-      LSGD_CK(c, hipEventRecord(c->done[par], ws));
-      pend[par] = true;
-    }
+    if (lsgd_status st = fork(ib, ia, par, g1, g2, F(r.cv[ia - 1].act))) return st;
     if (!sc_fused)
       LSGD_LAUNCH(c, "shortcut_bwd",
-                  lsgd::launch_shortcut_grad(gb[nxt], gb[cur], M(r.cv[ib].mbits), K, B,
-                                             qa.H, qa.W, qa.Cin, qa.Cout, mode, s));
+                  lsgd::launch_shortcut_grad(gb[nxt], gb[cur], mb, K, B, qa.H, qa.W, qa.Cin,
+                                             qa.Cout, mode, s));
     cur = nxt;
   }
-  // join (the side stream's last work, block 0's, was recorded last: all its
-  // updates are done, and wpart is free for the stem's weight gradient)
+  // the stem: its BN input gradient in place over the gradient it came from
+  // (the side stream reads none of buffers 0, 3), its weight gradient into
+  // its own partials; then the join (the side stream's last work, block 0's,
+  // was recorded last: all its updates are done)
+  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[cur], out_sums ? rows(0) / 256 : 0));
+  if (lsgd_status st = wgrad(0, nullptr, gb[cur], -1, s, F(r.wpart0))) return st;
   if (lsgd_status st = release(1)) return st;
   if (lsgd_status st = release(0)) return st;
-  LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[1], out_sums ? rows(0) / 256 : 0));
-  if (lsgd_status st = wgrad(0, nullptr, gb[1], -1, s)) return st;
   c->step += 1;
   return LSGD_OK;
 }

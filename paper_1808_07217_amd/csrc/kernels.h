@@ -164,10 +164,12 @@ struct ConvGeom {
   const float* bn_b;
   long long bn_sP;
   // input gradient, where conv_dgrad_epilogues(q) (nullptr: none):
-  //  * sc_dh, sc_hb: the block output's gradient (same shape as dx, identity
-  //    shortcut) and its activation's ReLU mask as bits (bit L % 32 of word
-  //    L / 32 for linear element L, as launch_bn_apply writes it): dx gains
-  //    sc_dh where the bit is set;
+  //  * sc_dh, sc_hb: the block output's gradient and its activation's ReLU
+  //    mask as bits (bit L % 32 of word L / 32 for linear element L, as
+  //    launch_bn_apply writes it): dx gains sc_dh where the bit is set --
+  //    element for element (identity shortcut, same shape as dx), or, for a
+  //    stride-2 input gradient (option A, output [G][Bt][Ho][Wo][Cout]), at
+  //    input position (2 oh, 2 ow) from output (oh, ow), first Cin channels;
   //  * bs_part: dx (with the shortcut's share, when both are set) is the
   //    gradient of a BN-ReLU's output whose pre-BN values are bs_y (same
   //    shape) and whose statistics and parameters come in bn_* (as above):
@@ -185,7 +187,8 @@ struct ConvGeom {
 };
 enum { CONV_FWD_MODE = 0, CONV_DGRAD_MODE = 1, CONV_WGRAD_MODE = 2 };
 // Which epilogues the input-gradient launch of q takes: bit 0 the shortcut
-// share (sc_*), bit 1 the BN backward sums with the recomputed mask (bs_*),
+// share (sc_*; option A for the stride-2 ones), bit 1 the BN backward sums
+// with the recomputed mask (bs_*),
 // bit 2 the sums with the activation mask (bs_hb). A launch takes one of them,
 // or the shortcut with one kind of sums.
 int conv_dgrad_epilogues(const ConvGeom& q);
@@ -230,6 +233,7 @@ hipError_t launch_bn_apply(const float* y, int G, int R, int C, const float* mu,
 // add). coef holds 5 floats per (replica, channel).
 // fused_nchunk > 0: the sums are already in part (fused_nchunk chunks per
 // replica, from an input-gradient epilogue) and are not formed again.
+// dy may be gup (the input gradient in place over it).
 hipError_t launch_bn_backward(const float* y, const float* gup, const unsigned* mbits,
                               int G, int R, int C, double* part, const float* mu,
                               const float* inv, float* coef, float* gamma, float* beta,

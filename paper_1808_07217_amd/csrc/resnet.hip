@@ -537,7 +537,11 @@ __global__ __launch_bounds__(kT) void k_conv_rows(ConvArgs c) {
 // The reduction over k = (tap, co) takes co as 16 chunk + 4 (l / 16) + s at
 // MFMA step s of a chunk, so a lane reads its four k values of A and of B
 // as one float4 each.
-template <int CI, int CO, int W>
+// SC: the option-A shortcut's share of the block-input gradient goes into dx
+// as it is stored: input position (2 oh, 2 ow) -- the parity class (0, 0) --
+// gains the block output's gradient c.sc_dh at (oh, ow) in its first CI
+// channels where the output's mask bit (c.sc_hb) is set.
+template <int CI, int CO, int W, bool SC>
 __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(CI == 16 ? 3 : 2))) void k_conv_dgrad_s2(
     ConvArgs c) {
   constexpr int Wo = W / 2, BH = 256 / W, BANDS = W / BH;
@@ -659,7 +663,36 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(CI == 16 ? 3
         }
       }
     }
+    // the shortcut's operands of this lane's class-0 outputs (output
+    // position (oh, ow) of block jb, register v), issued after the k work,
+    // where its operand registers are free: the 16 -> 32 form once the next
+    // tile is in LDS (its registers free too), and stores class 0 last
+    float sdh[SC ? NBW : 1][4];
+    unsigned swd[SC ? NBW : 1][4];
+    auto sc_fetch = [&]() __attribute__((always_inline)) {
+      if constexpr (SC) {
+        if (!kSplit || half == 0) {
+#pragma unroll
+          for (int jb = 0; jb < NBW; ++jb) {
+            // (v steps ow by one: CO floats, CO / 32 words)
+            const int oh = band * (BH / 2) + (16 / Wo) * (blk0 + jb) + (4 * lq) / Wo;
+            const long long e =
+                ((((long long)g * c.Bt + b0 + bi) * Wo + oh) * Wo + (4 * lq) % Wo) * CO +
+                nb * 16 + lm;
+            const float* pd = c.sc_dh + e;
+            const unsigned* pw = c.sc_hb + (e >> 5);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              sdh[jb][v] = pd[v * CO];
+              swd[jb][v] = pw[v * (CO / 32)];
+            }
+          }
+        }
+      }
+    };
+    if constexpr (kSplit) sc_fetch();
     if (more) lstore(T[(u + 1) & 1], tn, okn);
+    if constexpr (!kSplit) sc_fetch();
     // lane holds C[m = 4 (l/16) + v][n = l % 16] of each block: class
     // position 16 (blk0 + jb) + 4 (l/16) + v, i.e. a = (16 / Wo) (blk0 + jb) +
     // 4 (l/16) / Wo and j = 4 (l/16) % Wo + v, at input row band BH + 2 a + ph
@@ -667,7 +700,15 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(CI == 16 ? 3
     float* dx = c.out + ((long long)g * c.Bt + b0 + bi) * W * W * CI +
                 (((long long)band * BH + 2 * ((16 / Wo) * blk0 + (4 * lq) / Wo)) * W +
                  2 * ((4 * lq) % Wo)) * CI + nb * 16 + lm;
-    auto store = [&](int cls, int jb, const floatx4& r) __attribute__((always_inline)) {
+    auto store = [&](int cls, int jb, floatx4 r) __attribute__((always_inline)) {
+      if constexpr (SC) {
+        // (channel nb 16 + lm < 32: its bit in the position's first word)
+        if (cls == 0) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            r[v] += (swd[jb][v] >> (unsigned)(nb * 16 + lm)) & 1u ? sdh[jb][v] : 0.f;
+        }
+      }
 #pragma unroll
       for (int v = 0; v < 4; ++v)
         dx[((2 * (16 / Wo) * jb + (cls >> 1)) * W + 2 * v + (cls & 1)) * CI] = r[v];
@@ -699,7 +740,7 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(CI == 16 ? 3
         }
     } else {
 #pragma unroll
-      for (int cls = 0; cls < 4; ++cls) store(cls, 0, acc[cls][0]);
+      for (int cls = 3; cls >= 0; --cls) store(cls, 0, acc[cls][0]);
     }
     __syncthreads();
   };
@@ -1883,6 +1924,7 @@ static bool halo_shape(const ConvGeom& q, int mode) {
 
 int conv_dgrad_epilogues(const ConvGeom& q) {
   if (halo_shape(q, CONV_DGRAD)) return kEpiShortcut | kEpiBnSums | kEpiBnSumsAct;
+  if (dgrad_s2_shape(q)) return kEpiShortcut;  // option A
   if (q.stride != 1 || !rows_shape(q, CONV_DGRAD) || q.Cin != q.Cout) return 0;
   // the row kernel: 32 channels (at 64 the operands' registers cost more
   // occupancy than the separate passes); the sums need whole 256-row chunks
@@ -2037,10 +2079,18 @@ hipError_t launch_conv(int mode, const ConvGeom& q, hipStream_t st) {
         c.mchunk *= 2;
       const long long nb = (long long)q.G * (q.Bt / c.mchunk);
       if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
-      if (q.Cin == 16)
-        hipLaunchKernelGGL((k_conv_dgrad_s2<16, 32, 32>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+      if (q.Cin == 16 && c.sc_dh)
+        hipLaunchKernelGGL((k_conv_dgrad_s2<16, 32, 32, true>), dim3((unsigned)nb), dim3(kT), 0,
+                           st, c);
+      else if (q.Cin == 16)
+        hipLaunchKernelGGL((k_conv_dgrad_s2<16, 32, 32, false>), dim3((unsigned)nb), dim3(kT),
+                           0, st, c);
+      else if (c.sc_dh)
+        hipLaunchKernelGGL((k_conv_dgrad_s2<32, 64, 16, true>), dim3((unsigned)nb), dim3(kT), 0,
+                           st, c);
       else
-        hipLaunchKernelGGL((k_conv_dgrad_s2<32, 64, 16>), dim3((unsigned)nb), dim3(kT), 0, st, c);
+        hipLaunchKernelGGL((k_conv_dgrad_s2<32, 64, 16, false>), dim3((unsigned)nb), dim3(kT),
+                           0, st, c);
       return hipGetLastError();
     }
     if (halo) {
