@@ -37,7 +37,7 @@ struct ResPlan {
   // gradient buffers: 0 and 3 the block-output and block-input gradients,
   // 1, 2 (4, 5) a block's two BN input gradients, by the block's parity
   size_t featb = 0, dfeat = 0, dzh = 0, gbuf[6] = {}, mu = 0, inv = 0, coef = 0,
-         bnpart = 0, wpart = 0, wpart0 = 0;
+         bnpart = 0, bnpart2 = 0, wpart = 0, wpart0 = 0;
   // per BN layer, the scale and shift its forward batch was normalised with
   // ([kResConvs][K][64], layer i's [K][Cout] from i K 64)
   size_t gsnap = 0, bsnap = 0;
@@ -196,6 +196,7 @@ Layout make_resnet_layout(const lsgd_config* c) {
   r.bsnap = take(kResConvs * K * 64 * 4);
   r.coef = take(K * 64 * 5 * 4);
   r.bnpart = take(maxbn);
+  r.bnpart2 = take(maxbn);  // the second half's forward statistics
   r.wpart = take(maxpart);
   // the stem's weight-gradient partials apart: the main stream forms them
   // while the side stream may still use wpart
@@ -714,98 +715,150 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     g.bn_sP = r.cv[j].Cout;
   };
 
-  // forward: stem, then blocks (a: conv-BN-ReLU, b: conv-BN + shortcut, ReLU)
-  for (int i = 0; i < kResConvs; ++i) {
-    const ConvSpec& q = r.cv[i];
-    lsgd::ConvGeom g = geom(i);
-    if (i == 0) {
-      g.x = c->X;
-      g.sx = 0;
-      g.rowmap = c->idx();
-    } else if (i % 2 == 0) {  // second convolution of a block
-      g.x = F(r.cv[i - 1].y);
-      bn_input(g, i - 1);
-    } else {  // first convolution: the block input (stem or previous block output)
-      g.x = F(r.cv[i - 1].act);
-    }
-    g.out = F(q.y);
-    // the convolution writes its BN statistics per 256-row chunk where its
-    // kernel can; otherwise a separate pass reads the output
-    const bool fused = lsgd::conv_fwd_stats(g) && rows(i) % 256 == 0;
-    g.stats = fused ? bnpart : nullptr;
-    LSGD_LAUNCH(c, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, s));
-    float* mi = mu + (size_t)i * K * 64;
-    float* ii = inv + (size_t)i * K * 64;
-    // this replica's running statistics of BN layer i follow the batch
-    float* rm = c->RS() + r.rsoff[i];
-    float* rv = c->RS() + r.rs_half + r.rsoff[i];
-    float* gs = gsnap + (size_t)i * K * 64;
-    float* bs = bsnap + (size_t)i * K * 64;
-    if (fused)
-      LSGD_LAUNCH(c, "bn_stats",
-                  lsgd::launch_bn_finalize_chunks(bnpart, rows(i) / 256, K, rows(i), q.Cout,
-                                                  mi, ii, rm, rv, r.Rs, s, W + q.offG,
-                                                  W + q.offB, Ps, gs, bs));
-    else
-      LSGD_LAUNCH(c, "bn_stats", lsgd::launch_bn_stats(F(q.y), K, rows(i), q.Cout, bnpart,
-                                                       mi, ii, rm, rv, r.Rs, s, W + q.offG,
-                                                       W + q.offB, Ps, gs, bs));
-    if (i % 2 == 1) continue;  // a block's first BN-ReLU: formed by its consumers
-    int mode = 0;
-    const float* blk_in = nullptr;
-    int cin_blk = 0;
-    if (i > 0) {  // second convolution of a block
-      const ConvSpec& qa = r.cv[i - 1];
-      blk_in = F(r.cv[i - 2].act);
-      cin_blk = qa.Cin;
-      mode = (qa.stride == 1 && qa.Cin == q.Cout) ? 1 : 2;
-    }
-    LSGD_LAUNCH(c, "bn_apply", lsgd::launch_bn_apply(F(q.y), K, rows(i), q.Cout, mi, ii,
-                                                     W + q.offG, W + q.offB, Ps, mode,
-                                                     blk_in, q.Ho, q.Wo, cin_blk,
-                                                     F(q.act), i > 0 ? M(q.mbits) : nullptr,
-                                                     s));
-  }
-
-  // head: global average pool, classifier, loss
+  // The forward pass of replicas g0 .. g0 + Kh - 1 on stream fs, its BN
+  // statistics' partials in part: layer i of the stem and blocks (a:
+  // conv-BN-ReLU, b: conv-BN + shortcut, ReLU), then the head (pool,
+  // classifier, loss and the classifier's update). Every tensor is per
+  // replica, so a subset of them is a pointer offset and a smaller grid.
   const ConvSpec& last = r.cv[kResConvs - 1];
   const int S = last.Ho * last.Wo;
-  LSGD_LAUNCH(c, "gap", lsgd::launch_gap(F(last.act), K * B, S, 64, F(r.featb), false,
-                                         nullptr, nullptr, s));
-  lsgd::HeadArgs h{};
-  h.K = K;
-  h.B = B;
-  h.D = 64;
-  h.C = r.classes;
-  h.gather = 0;
-  h.A = F(r.featb);
-  h.sA = (long long)B * 64;
-  h.rowmap = c->idx();
-  h.y = c->y;
-  h.W = W + r.offFcW;
-  h.sW = Ps;
-  h.Wm = W + r.offFcW;
-  h.Um = U + r.offFcW;
-  h.bias = W + r.offFcB;
-  h.sBias = Ps;
-  h.Wsrc = W + r.offFcW;
-  h.bsrc = W + r.offFcB;
-  h.sSrc = Ps;
-  h.bias_w = W + r.offFcB;
-  h.bias_u = U + r.offFcB;
-  h.sP = Ps;
-  h.dZ = F(r.dzh);
-  h.dZprev = F(r.dfeat);
-  h.nomask = 1;
-  h.rowloss = c->rowloss();
-  h.loss = d_loss;
-  h.nonfinite = c->flag();
-  h.lr = lr;
-  h.mom = cf.momentum;
-  h.wd = cf.weight_decay;
-  h.nesterov = upd_mode(cf);
-  LSGD_LAUNCH(c, "head_fwd", lsgd::launch_head_fwd(0, h, s));
-  LSGD_LAUNCH(c, "head_wgrad", lsgd::launch_head_wgrad(0, h, s));
+  auto per = [&](int i) {  // values per replica of conv i's output
+    return (long long)B * r.cv[i].Ho * r.cv[i].Wo * r.cv[i].Cout;
+  };
+  auto fwd_layer = [&](int i, int g0, int Kh, hipStream_t fs, double* part) -> lsgd_status {
+    {
+      const ConvSpec& q = r.cv[i];
+      const int C = q.Cout;
+      lsgd::ConvGeom g = geom(i);
+      g.G = Kh;
+      g.Wk += (size_t)g0 * Ps;
+      if (i == 0) {
+        g.x = c->X;
+        g.sx = 0;
+        g.rowmap = c->idx() + (size_t)g0 * B;
+      } else if (i % 2 == 0) {  // second convolution of a block
+        g.x = F(r.cv[i - 1].y) + g0 * g.sx;
+        bn_input(g, i - 1);
+        const int Cj = r.cv[i - 1].Cout;
+        g.bn_mu += (size_t)g0 * Cj;
+        g.bn_inv += (size_t)g0 * Cj;
+        g.bn_g += (size_t)g0 * Cj;
+        g.bn_b += (size_t)g0 * Cj;
+      } else {  // first convolution: the block input (stem or previous block output)
+        g.x = F(r.cv[i - 1].act) + g0 * g.sx;
+      }
+      float* y = F(q.y) + g0 * per(i);
+      g.out = y;
+      // the convolution writes its BN statistics per 256-row chunk where its
+      // kernel can; otherwise a separate pass reads the output
+      const bool fused = lsgd::conv_fwd_stats(g) && rows(i) % 256 == 0;
+      g.stats = fused ? part : nullptr;
+      LSGD_LAUNCH_ON(c, fs, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, fs));
+      float* mi = mu + (size_t)i * K * 64 + (size_t)g0 * C;
+      float* ii = inv + (size_t)i * K * 64 + (size_t)g0 * C;
+      // this replica's running statistics of BN layer i follow the batch
+      float* rm = c->RS() + r.rsoff[i] + g0 * r.Rs;
+      float* rv = c->RS() + r.rs_half + r.rsoff[i] + g0 * r.Rs;
+      float* gs = gsnap + (size_t)i * K * 64 + (size_t)g0 * C;
+      float* bs = bsnap + (size_t)i * K * 64 + (size_t)g0 * C;
+      float* gm = W + q.offG + (size_t)g0 * Ps;
+      float* bt = W + q.offB + (size_t)g0 * Ps;
+      if (fused)
+        LSGD_LAUNCH_ON(c, fs, "bn_stats",
+                       lsgd::launch_bn_finalize_chunks(part, rows(i) / 256, Kh, rows(i), C, mi,
+                                                       ii, rm, rv, r.Rs, fs, gm, bt, Ps, gs,
+                                                       bs));
+      else
+        LSGD_LAUNCH_ON(c, fs, "bn_stats",
+                       lsgd::launch_bn_stats(y, Kh, rows(i), C, part, mi, ii, rm, rv, r.Rs, fs,
+                                             gm, bt, Ps, gs, bs));
+      if (i % 2 == 1) return LSGD_OK;  // a block's first BN-ReLU: formed by its consumers
+      int mode = 0;
+      const float* blk_in = nullptr;
+      int cin_blk = 0;
+      if (i > 0) {  // second convolution of a block
+        const ConvSpec& qa = r.cv[i - 1];
+        blk_in = F(r.cv[i - 2].act) + g0 * per(i - 2);
+        cin_blk = qa.Cin;
+        mode = (qa.stride == 1 && qa.Cin == q.Cout) ? 1 : 2;
+      }
+      LSGD_LAUNCH_ON(c, fs, "bn_apply",
+                     lsgd::launch_bn_apply(y, Kh, rows(i), C, mi, ii, gm, bt, Ps, mode, blk_in,
+                                           q.Ho, q.Wo, cin_blk, F(q.act) + g0 * per(i),
+                                           i > 0 ? M(q.mbits) + g0 * per(i) / 32 : nullptr,
+                                           fs));
+    }
+    return LSGD_OK;
+  };
+  auto fwd_head = [&](int g0, int Kh, hipStream_t fs) -> lsgd_status {
+    // head: global average pool, classifier, loss
+    LSGD_LAUNCH_ON(c, fs, "gap",
+                   lsgd::launch_gap(F(last.act) + g0 * per(kResConvs - 1), Kh * B, S, 64,
+                                    F(r.featb) + (size_t)g0 * B * 64, false, nullptr, nullptr,
+                                    fs));
+    const size_t pg = (size_t)g0 * Ps;
+    lsgd::HeadArgs h{};
+    h.K = Kh;
+    h.B = B;
+    h.D = 64;
+    h.C = r.classes;
+    h.gather = 0;
+    h.A = F(r.featb) + (size_t)g0 * B * 64;
+    h.sA = (long long)B * 64;
+    h.rowmap = c->idx() + (size_t)g0 * B;
+    h.y = c->y;
+    h.W = W + r.offFcW + pg;
+    h.sW = Ps;
+    h.Wm = W + r.offFcW + pg;
+    h.Um = U + r.offFcW + pg;
+    h.bias = W + r.offFcB + pg;
+    h.sBias = Ps;
+    h.Wsrc = W + r.offFcW + pg;
+    h.bsrc = W + r.offFcB + pg;
+    h.sSrc = Ps;
+    h.bias_w = W + r.offFcB + pg;
+    h.bias_u = U + r.offFcB + pg;
+    h.sP = Ps;
+    h.dZ = F(r.dzh) + (size_t)g0 * B * r.classes;
+    h.dZprev = F(r.dfeat) + (size_t)g0 * B * 64;
+    h.nomask = 1;
+    h.rowloss = c->rowloss() + (size_t)g0 * B;
+    h.loss = d_loss ? d_loss + g0 : nullptr;
+    h.nonfinite = c->flag();
+    h.lr = lr;
+    h.mom = cf.momentum;
+    h.wd = cf.weight_decay;
+    h.nesterov = upd_mode(cf);
+    LSGD_LAUNCH_ON(c, fs, "head_fwd", lsgd::launch_head_fwd(0, h, fs));
+    LSGD_LAUNCH_ON(c, fs, "head_wgrad", lsgd::launch_head_wgrad(0, h, fs));
+    return LSGD_OK;
+  };
+  // With side streams, the two halves of the replicas run their forward
+  // passes on the main and the side stream: nothing passes between replicas,
+  // and each half's memory-bound BN passes overlap the other's convolutions.
+  // The launches go out layer by layer, alternating, so that both streams
+  // have work from the start; the second half starts once the first has
+  // passed the stem, so that the two stay out of step (one's BN passes
+  // beside the other's convolutions).
+  if (c->use_side && K % 2 == 0) {
+    const int Kh = K / 2;
+    hipStream_t s2 = c->side[1];
+    double* part2 = (double*)(c->ws + r.bnpart2);
+    LSGD_CK(c, hipEventRecord(c->fork[1], s));
+    LSGD_CK(c, hipStreamWaitEvent(s2, c->fork[1], 0));
+    for (int i = 0; i < kResConvs; ++i) {
+      if (lsgd_status st = fwd_layer(i, 0, Kh, s, bnpart)) return st;
+      if (lsgd_status st = fwd_layer(i, Kh, Kh, s2, part2)) return st;
+    }
+    if (lsgd_status st = fwd_head(0, Kh, s)) return st;
+    if (lsgd_status st = fwd_head(Kh, Kh, s2)) return st;
+    LSGD_CK(c, hipEventRecord(c->join[1], s2));
+    LSGD_CK(c, hipStreamWaitEvent(s, c->join[1], 0));
+  } else {
+    for (int i = 0; i < kResConvs; ++i)
+      if (lsgd_status st = fwd_layer(i, 0, K, s, bnpart)) return st;
+    if (lsgd_status st = fwd_head(0, K, s)) return st;
+  }
 
   // backward
   float* gb[6];
