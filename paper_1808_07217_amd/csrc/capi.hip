@@ -837,9 +837,8 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // passes on the main and the side stream: nothing passes between replicas,
   // and each half's memory-bound BN passes overlap the other's convolutions.
   // The launches go out layer by layer, alternating, so that both streams
-  // have work from the start; the second half starts once the first has
-  // passed the stem, so that the two stay out of step (one's BN passes
-  // beside the other's convolutions).
+  // have work from the start (the second half started a layer behind the
+  // first measured no different).
   if (c->use_side && K % 2 == 0) {
     const int Kh = K / 2;
     hipStream_t s2 = c->side[1];
