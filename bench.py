@@ -607,6 +607,13 @@ def main():
         reps.profile_select(None)
         avg_s = ms / n / 1e3
         flops, nbytes = kernel_cost(dom, w)
+        if w.model == "resnet20" and flops is not None:
+            # the step's algorithmic totals over the launches the library
+            # makes per local step (it may split a layer's work, e.g. the
+            # forward pass over two halves of the replicas)
+            _, f_step, b_step = resnet_step_costs(w)[dom]
+            lps = per_round_launches / H
+            flops, nbytes = f_step / lps, b_step / lps
     ms_per_step = max(gpu_ms, wall * 1e3) / steps
     samples = w.K * H * w.B_loc
     value = samples / (ms_per_step / 1e3)
@@ -678,8 +685,12 @@ def main():
             except ValueError:
                 f = None
             if f and ms > 0:
-                launches = rep[t][0] / prof_rounds
-                mf[t] = round(f * launches / (ms / 1e3) / (PEAK_TFLOPS[w.dtype] * 1e12), 4)
+                if w.model == "resnet20" and t in resnet_step_costs(w):
+                    # the round's flops, however many launches carry them
+                    f_round = resnet_step_costs(w)[t][1] * H
+                else:
+                    f_round = f * rep[t][0] / prof_rounds
+                mf[t] = round(f_round / (ms / 1e3) / (PEAK_TFLOPS[w.dtype] * 1e12), 4)
         if mf:
             out["kernel_mfma_frac"] = mf
         if "average" in rep:   # the synchronisation kernel's own rate
