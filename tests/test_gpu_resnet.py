@@ -48,6 +48,24 @@ def test_resnet20_every_step():
     assert e <= 1e-5
 
 
+def test_resnet20_odd_replica_count():
+    """K = 3: the forward pass on one stream (an even replica count runs it
+    as two halves on two streams), every replica after every local step,
+    then the average."""
+    base = wk.get("resnet20")
+    w = base.scaled(K=3, N=4096)
+    X, y = wk.dataset(base)
+    X, y = np.ascontiguousarray(X[:4096]), np.ascontiguousarray(y[:4096])
+    w0 = wk.initial_weights(w)
+    print("resnet20 K=3", flush=True)
+    reps, st, worst = _compare(w, X, y, w0, 2, [0, 1, 2], 1e-5, 1e-4)
+    reps.average()
+    st.W = O.average(st.W)
+    e = normwise(reps.read_params(-1).cpu().numpy(), st.W[0])
+    print(f"resnet20 K=3: worst step error {worst:.3e}, averaged {e:.3e}", flush=True)
+    assert e <= 1e-5
+
+
 def test_resnet20_batch_not_a_multiple_of_four():
     """B_loc = 10 (K = 2, 4096-image subset, three steps, then the average):
     the paths a batch of 128 never takes -- the stride-2 input gradients of
