@@ -34,9 +34,10 @@ struct ResPlan {
   ConvSpec cv[kResConvs];
   int64_t offFcW = 0, offFcB = 0;
   int classes = 0, feat = 64, side_out = 8;
-  // gradient buffers: 0 and 3 the block-output and block-input gradients,
-  // 1, 2 (4, 5) a block's two BN input gradients, by the block's parity
-  size_t featb = 0, dfeat = 0, dzh = 0, gbuf[6] = {}, mu = 0, inv = 0, coef = 0,
+  // gradient buffers: gio the block-output and block-input gradients (the
+  // two swap roles block by block), bgrad[b] block b's two BN input gradients
+  size_t featb = 0, dfeat = 0, dzh = 0, gio[2] = {}, bgrad[9][2] = {}, mu = 0, inv = 0,
+         coef = 0,
          bnpart = 0, bnpart2 = 0, wpart = 0, wpart0 = 0;
   // per BN layer, the scale and shift its forward batch was normalised with
   // ([kResConvs][K][64], layer i's [K][Cout] from i K 64)
@@ -189,7 +190,13 @@ Layout make_resnet_layout(const lsgd_config* c) {
   r.featb = take(K * B * 64 * 4);
   r.dfeat = take(K * B * 64 * 4);
   r.dzh = take(K * B * r.classes * 4);
-  for (int i = 0; i < 6; ++i) r.gbuf[i] = take(maxact);
+  for (int i = 0; i < 2; ++i) r.gio[i] = take(maxact);
+  // each block's own BN input gradients (its second convolution's output size):
+  // the main stream never rewrites one that the side stream may still read
+  for (int b = 0; b < 9; ++b)
+    for (int j = 0; j < 2; ++j)
+      r.bgrad[b][j] = take(K * B * r.cv[2 * b + 2].Ho * r.cv[2 * b + 2].Wo *
+                           r.cv[2 * b + 2].Cout * 4);
   r.mu = take(kResConvs * K * 64 * 4);
   r.inv = take(kResConvs * K * 64 * 4);
   r.gsnap = take(kResConvs * K * 64 * 4);
@@ -860,8 +867,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   }
 
   // backward
-  float* gb[6];
-  for (int i = 0; i < 6; ++i) gb[i] = F(r.gbuf[i]);
+  float* gb[2] = {F(r.gio[0]), F(r.gio[1])};
   float* coef = F(r.coef);
   float* wpart = F(r.wpart);
   LSGD_LAUNCH(c, "gap_bwd", lsgd::launch_gap(nullptr, K * B, S, 64, nullptr, true,
@@ -913,16 +919,17 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // which then run alone, set the weight gradients against the input
   // gradients' matrix work instead and was slower). A block's two BN input
   // gradients (the second BN's, and the first BN's formed in place over the
-  // gradient it came from) live in buffers 1, 2 or 4, 5 by the block's
-  // parity, so the main stream rewrites them two blocks later, after event
-  // done[parity] says the side stream has read them; one wpart serves all
-  // blocks, in the side stream's order (the stem's weight gradient, on the
-  // main stream, has its own). Without side streams everything runs in
-  // order on the main stream.
+  // gradient it came from) have buffers of their own, so the main stream
+  // waits for the side stream only at the step's end (events done[parity],
+  // the last one recorded after all of the side stream's work; with buffers
+  // shared by parity, a wait before each block cost the main stream some µs
+  // each); one wpart serves all blocks, in the side stream's order (the
+  // stem's weight gradient, on the main stream, has its own). Without side
+  // streams everything runs in order on the main stream.
   const bool sidew = c->use_side;
   hipStream_t ws = sidew ? c->side[1] : s;
   bool pend[2] = {false, false};
-  auto release = [&](int k) -> lsgd_status {  // before parity k's buffers are rewritten
+  auto release = [&](int k) -> lsgd_status {  // the main stream waits for event done[k]
     if (pend[k]) LSGD_CK(c, hipStreamWaitEvent(s, c->done[k], 0));
     pend[k] = false;
     return LSGD_OK;
@@ -980,10 +987,9 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   for (int blk = 8; blk >= 0; --blk) {
     const int ia = 2 * blk + 1, ib = 2 * blk + 2, par = blk & 1;
     const ConvSpec& qa = r.cv[ia];
-    const int nxt = cur == 0 ? 3 : 0;
-    float* g1 = gb[par ? 4 : 1];
-    float* g2 = gb[par ? 5 : 2];
-    if (lsgd_status st = release(par)) return st;
+    const int nxt = 1 - cur;
+    float* g1 = F(r.bgrad[blk][0]);
+    float* g2 = F(r.bgrad[blk][1]);
     // second convolution: its output went through the shortcut add and ReLU
     const unsigned* mb = M(r.cv[ib].mbits);
     LSGD_LAUNCH(c, "bn_bwd", bn_bwd(ib, gb[cur], mb, g1, out_sums ? rows(ib) / 256 : 0));
@@ -1012,7 +1018,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     cur = nxt;
   }
   // the stem: its BN input gradient in place over the gradient it came from
-  // (the side stream reads none of buffers 0, 3), its weight gradient into
+  // (the side stream reads neither of gio), its weight gradient into
   // its own partials; then the join (the side stream's last work, block 0's,
   // was recorded last: all its updates are done)
   LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[cur], out_sums ? rows(0) / 256 : 0));
