@@ -319,9 +319,8 @@ struct lsgd_ctx {
   // (default priority), with fork/join events; created at init
   hipStream_t side[2] = {nullptr, nullptr};
   hipEvent_t fork[2] = {nullptr, nullptr}, join[2] = {nullptr, nullptr};
-  // ResNet: completion of the side stream's weight gradients that read the
-  // gradient buffers 1 and 2
-  hipEvent_t done[2] = {nullptr, nullptr};
+  // ResNet: completion of a step's side-stream work (its weight gradients)
+  hipEvent_t done = nullptr;
   bool use_side = false;
   Layout lay;
   const float* X = nullptr;
@@ -378,8 +377,8 @@ struct lsgd_ctx {
       }
       if (fork[i]) (void)hipEventDestroy(fork[i]);
       if (join[i]) (void)hipEventDestroy(join[i]);
-      if (done[i]) (void)hipEventDestroy(done[i]);
     }
+    if (done) (void)hipEventDestroy(done);
   }
 
   lsgd_status fail(hipError_t e, const char* what) {
@@ -920,23 +919,24 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // gradients' matrix work instead and was slower). A block's two BN input
   // gradients (the second BN's, and the first BN's formed in place over the
   // gradient it came from) have buffers of their own, so the main stream
-  // waits for the side stream only at the step's end (events done[parity],
-  // the last one recorded after all of the side stream's work; with buffers
-  // shared by parity, a wait before each block cost the main stream some µs
-  // each); one wpart serves all blocks, in the side stream's order (the
+  // waits for the side stream only at the step's end (with buffers shared
+  // by parity, a wait before each block cost the main stream some µs each);
+  // one wpart serves all blocks, in the side stream's order (the
   // stem's weight gradient, on the main stream, has its own). Without side
   // streams everything runs in order on the main stream.
   const bool sidew = c->use_side;
   hipStream_t ws = sidew ? c->side[1] : s;
-  bool pend[2] = {false, false};
-  auto release = [&](int k) -> lsgd_status {  // the main stream waits for event done[k]
-    if (pend[k]) LSGD_CK(c, hipStreamWaitEvent(s, c->done[k], 0));
-    pend[k] = false;
+  bool pend = false;
+  auto join_side = [&]() -> lsgd_status {  // the main stream waits for event done
+    if (pend) LSGD_CK(c, hipStreamWaitEvent(s, c->done, 0));
+    pend = false;
     return LSGD_OK;
   };
   // the weight gradients of block (ib, ia) with its BN input gradients g1, g2
   // and input h_in, forked to the side stream
-  auto fork = [&](int ib, int ia, int par, const float* g1, const float* g2,
+  // (the last block's, block 0's, records done after all of the side
+  // stream's work of the step)
+  auto fork = [&](int ib, int ia, bool last, const float* g1, const float* g2,
                   const float* h_in) -> lsgd_status {
     if (sidew) {
       LSGD_CK(c, hipEventRecord(c->fork[1], s));
@@ -944,9 +944,9 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     }
     if (lsgd_status st = wgrad(ib, F(r.cv[ia].y), g1, ia, ws, wpart)) return st;
     if (lsgd_status st = wgrad(ia, h_in, g2, -1, ws, wpart)) return st;
-    if (sidew) {
-      LSGD_CK(c, hipEventRecord(c->done[par], ws));
-      pend[par] = true;
+    if (sidew && last) {
+      LSGD_CK(c, hipEventRecord(c->done, ws));
+      pend = true;
     }
     return LSGD_OK;
   };
@@ -985,7 +985,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // block-input gradient was are in bnpart already)
   bool out_sums = false;
   for (int blk = 8; blk >= 0; --blk) {
-    const int ia = 2 * blk + 1, ib = 2 * blk + 2, par = blk & 1;
+    const int ia = 2 * blk + 1, ib = 2 * blk + 2;
     const ConvSpec& qa = r.cv[ia];
     const int nxt = 1 - cur;
     float* g1 = F(r.bgrad[blk][0]);
@@ -1010,7 +1010,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
                                prev_bn > 0 ? M(r.cv[prev_bn].mbits) : nullptr, &sc_fused,
                                &out_sums))
       return st;
-    if (lsgd_status st = fork(ib, ia, par, g1, g2, F(r.cv[ia - 1].act))) return st;
+    if (lsgd_status st = fork(ib, ia, blk == 0, g1, g2, F(r.cv[ia - 1].act))) return st;
     if (!sc_fused)
       LSGD_LAUNCH(c, "shortcut_bwd",
                   lsgd::launch_shortcut_grad(gb[nxt], gb[cur], mb, K, B, qa.H, qa.W, qa.Cin,
@@ -1023,8 +1023,7 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
   // was recorded last: all its updates are done)
   LSGD_LAUNCH(c, "bn_bwd", bn_bwd(0, gb[cur], nullptr, gb[cur], out_sums ? rows(0) / 256 : 0));
   if (lsgd_status st = wgrad(0, nullptr, gb[cur], -1, s, F(r.wpart0))) return st;
-  if (lsgd_status st = release(1)) return st;
-  if (lsgd_status st = release(0)) return st;
+  if (lsgd_status st = join_side()) return st;
   c->step += 1;
   return LSGD_OK;
 }
@@ -1283,9 +1282,8 @@ lsgd_status lsgd_init_replicas(const lsgd_config* cfg, const float* d_X,
       check(hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking), "side stream");
       check(hipEventCreateWithFlags(&c->fork[i], hipEventDisableTiming), "fork event");
       check(hipEventCreateWithFlags(&c->join[i], hipEventDisableTiming), "join event");
-      if (resnet)
-        check(hipEventCreateWithFlags(&c->done[i], hipEventDisableTiming), "done event");
     }
+    if (resnet) check(hipEventCreateWithFlags(&c->done, hipEventDisableTiming), "done event");
     c->use_side = st == LSGD_OK;
   }
   if (st != LSGD_OK) {
