@@ -732,68 +732,66 @@ lsgd_status do_local_step_resnet(lsgd_ctx* c, float lr, float* d_loss) {
     return (long long)B * r.cv[i].Ho * r.cv[i].Wo * r.cv[i].Cout;
   };
   auto fwd_layer = [&](int i, int g0, int Kh, hipStream_t fs, double* part) -> lsgd_status {
-    {
-      const ConvSpec& q = r.cv[i];
-      const int C = q.Cout;
-      lsgd::ConvGeom g = geom(i);
-      g.G = Kh;
-      g.Wk += (size_t)g0 * Ps;
-      if (i == 0) {
-        g.x = c->X;
-        g.sx = 0;
-        g.rowmap = c->idx() + (size_t)g0 * B;
-      } else if (i % 2 == 0) {  // second convolution of a block
-        g.x = F(r.cv[i - 1].y) + g0 * g.sx;
-        bn_input(g, i - 1);
-        const int Cj = r.cv[i - 1].Cout;
-        g.bn_mu += (size_t)g0 * Cj;
-        g.bn_inv += (size_t)g0 * Cj;
-        g.bn_g += (size_t)g0 * Cj;
-        g.bn_b += (size_t)g0 * Cj;
-      } else {  // first convolution: the block input (stem or previous block output)
-        g.x = F(r.cv[i - 1].act) + g0 * g.sx;
-      }
-      float* y = F(q.y) + g0 * per(i);
-      g.out = y;
-      // the convolution writes its BN statistics per 256-row chunk where its
-      // kernel can; otherwise a separate pass reads the output
-      const bool fused = lsgd::conv_fwd_stats(g) && rows(i) % 256 == 0;
-      g.stats = fused ? part : nullptr;
-      LSGD_LAUNCH_ON(c, fs, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, fs));
-      float* mi = mu + (size_t)i * K * 64 + (size_t)g0 * C;
-      float* ii = inv + (size_t)i * K * 64 + (size_t)g0 * C;
-      // this replica's running statistics of BN layer i follow the batch
-      float* rm = c->RS() + r.rsoff[i] + g0 * r.Rs;
-      float* rv = c->RS() + r.rs_half + r.rsoff[i] + g0 * r.Rs;
-      float* gs = gsnap + (size_t)i * K * 64 + (size_t)g0 * C;
-      float* bs = bsnap + (size_t)i * K * 64 + (size_t)g0 * C;
-      float* gm = W + q.offG + (size_t)g0 * Ps;
-      float* bt = W + q.offB + (size_t)g0 * Ps;
-      if (fused)
-        LSGD_LAUNCH_ON(c, fs, "bn_stats",
-                       lsgd::launch_bn_finalize_chunks(part, rows(i) / 256, Kh, rows(i), C, mi,
-                                                       ii, rm, rv, r.Rs, fs, gm, bt, Ps, gs,
-                                                       bs));
-      else
-        LSGD_LAUNCH_ON(c, fs, "bn_stats",
-                       lsgd::launch_bn_stats(y, Kh, rows(i), C, part, mi, ii, rm, rv, r.Rs, fs,
-                                             gm, bt, Ps, gs, bs));
-      if (i % 2 == 1) return LSGD_OK;  // a block's first BN-ReLU: formed by its consumers
-      int mode = 0;
-      const float* blk_in = nullptr;
-      int cin_blk = 0;
-      if (i > 0) {  // second convolution of a block
-        const ConvSpec& qa = r.cv[i - 1];
-        blk_in = F(r.cv[i - 2].act) + g0 * per(i - 2);
-        cin_blk = qa.Cin;
-        mode = (qa.stride == 1 && qa.Cin == q.Cout) ? 1 : 2;
-      }
-      LSGD_LAUNCH_ON(c, fs, "bn_apply",
-                     lsgd::launch_bn_apply(y, Kh, rows(i), C, mi, ii, gm, bt, Ps, mode, blk_in,
-                                           q.Ho, q.Wo, cin_blk, F(q.act) + g0 * per(i),
-                                           i > 0 ? M(q.mbits) + g0 * per(i) / 32 : nullptr,
-                                           fs));
+    const ConvSpec& q = r.cv[i];
+    const int C = q.Cout;
+    lsgd::ConvGeom g = geom(i);
+    g.G = Kh;
+    g.Wk += (size_t)g0 * Ps;
+    if (i == 0) {
+      g.x = c->X;
+      g.sx = 0;
+      g.rowmap = c->idx() + (size_t)g0 * B;
+    } else if (i % 2 == 0) {  // second convolution of a block
+      g.x = F(r.cv[i - 1].y) + g0 * g.sx;
+      bn_input(g, i - 1);
+      const int Cj = r.cv[i - 1].Cout;
+      g.bn_mu += (size_t)g0 * Cj;
+      g.bn_inv += (size_t)g0 * Cj;
+      g.bn_g += (size_t)g0 * Cj;
+      g.bn_b += (size_t)g0 * Cj;
+    } else {  // first convolution: the block input (stem or previous block output)
+      g.x = F(r.cv[i - 1].act) + g0 * g.sx;
     }
+    float* y = F(q.y) + g0 * per(i);
+    g.out = y;
+    // the convolution writes its BN statistics per 256-row chunk where its
+    // kernel can; otherwise a separate pass reads the output
+    const bool fused = lsgd::conv_fwd_stats(g) && rows(i) % 256 == 0;
+    g.stats = fused ? part : nullptr;
+    LSGD_LAUNCH_ON(c, fs, "conv_fwd", lsgd::launch_conv(lsgd::CONV_FWD_MODE, g, fs));
+    float* mi = mu + (size_t)i * K * 64 + (size_t)g0 * C;
+    float* ii = inv + (size_t)i * K * 64 + (size_t)g0 * C;
+    // this replica's running statistics of BN layer i follow the batch
+    float* rm = c->RS() + r.rsoff[i] + g0 * r.Rs;
+    float* rv = c->RS() + r.rs_half + r.rsoff[i] + g0 * r.Rs;
+    float* gs = gsnap + (size_t)i * K * 64 + (size_t)g0 * C;
+    float* bs = bsnap + (size_t)i * K * 64 + (size_t)g0 * C;
+    float* gm = W + q.offG + (size_t)g0 * Ps;
+    float* bt = W + q.offB + (size_t)g0 * Ps;
+    if (fused)
+      LSGD_LAUNCH_ON(c, fs, "bn_stats",
+                     lsgd::launch_bn_finalize_chunks(part, rows(i) / 256, Kh, rows(i), C, mi,
+                                                     ii, rm, rv, r.Rs, fs, gm, bt, Ps, gs,
+                                                     bs));
+    else
+      LSGD_LAUNCH_ON(c, fs, "bn_stats",
+                     lsgd::launch_bn_stats(y, Kh, rows(i), C, part, mi, ii, rm, rv, r.Rs, fs,
+                                           gm, bt, Ps, gs, bs));
+    if (i % 2 == 1) return LSGD_OK;  // a block's first BN-ReLU: formed by its consumers
+    int mode = 0;
+    const float* blk_in = nullptr;
+    int cin_blk = 0;
+    if (i > 0) {  // second convolution of a block
+      const ConvSpec& qa = r.cv[i - 1];
+      blk_in = F(r.cv[i - 2].act) + g0 * per(i - 2);
+      cin_blk = qa.Cin;
+      mode = (qa.stride == 1 && qa.Cin == q.Cout) ? 1 : 2;
+    }
+    LSGD_LAUNCH_ON(c, fs, "bn_apply",
+                   lsgd::launch_bn_apply(y, Kh, rows(i), C, mi, ii, gm, bt, Ps, mode, blk_in,
+                                         q.Ho, q.Wo, cin_blk, F(q.act) + g0 * per(i),
+                                         i > 0 ? M(q.mbits) + g0 * per(i) / 32 : nullptr,
+                                         fs));
     return LSGD_OK;
   };
   auto fwd_head = [&](int g0, int Kh, hipStream_t fs) -> lsgd_status {
